@@ -1,0 +1,133 @@
+"""CPU oracle for Y = X.W^T + R (TEST INFRASTRUCTURE ONLY).
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
+``bench.py`` may import this package.  The GPU library never imports, links
+or falls back to it, and the two share no code: the only thing they have in
+common is the byte content of the seeded inputs.
+
+The arithmetic lives in ``kernelarc_oracle.c`` (plain C, fp64, ascending k);
+this module builds it with gcc and marshals numpy arrays through ctypes.
+Inputs are bf16 bit patterns held in ``numpy.uint16`` arrays.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+SOURCE = os.path.join(HERE, "kernelarc_oracle.c")
+LIBRARY = os.path.join(HERE, "libkernelarc_oracle.so")
+
+# -O2 without -ffast-math and with contraction off keeps the k-order and the
+# separate multiply/add of the definition; OpenMP only splits output rows.
+CFLAGS = ["-std=c11", "-O2", "-ffp-contract=off", "-fno-fast-math", "-fopenmp",
+          "-shared", "-fPIC"]
+
+
+def build(source: str = SOURCE, output: str = LIBRARY) -> str:
+    """Compile the oracle with gcc into a shared library; returns its path."""
+    tmp = output + ".tmp"
+    cmd = ["gcc", *CFLAGS, "-o", tmp, source, "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, output)
+    return output
+
+
+_I64 = ctypes.c_int64
+_P = ctypes.c_void_p
+
+
+class Oracle:
+    """ctypes view of one compiled oracle library."""
+
+    def __init__(self, path: str = LIBRARY):
+        if not os.path.exists(path):
+            raise FileNotFoundError(
+                f"oracle library {path} is not built; run __graft_entry__.build()")
+        lib = ctypes.CDLL(path)
+        lib.ka_oracle_linear.argtypes = [_I64, _I64, _I64, _P, _P, _P, _P]
+        lib.ka_oracle_linear.restype = ctypes.c_int
+        lib.ka_oracle_linear_at.argtypes = [_I64, _I64, _I64, _P, _P, _P, _I64, _P, _P, _P]
+        lib.ka_oracle_linear_at.restype = ctypes.c_int
+        lib.ka_oracle_round_bf16.argtypes = [_I64, _P, _P]
+        lib.ka_oracle_round_bf16.restype = None
+        self.lib = lib
+        self.path = path
+
+    @staticmethod
+    def _bits(a, shape):
+        a = np.ascontiguousarray(a)
+        if a.dtype != np.uint16:
+            raise TypeError("oracle inputs are bf16 bit patterns (numpy.uint16)")
+        if a.shape != shape:
+            raise ValueError(f"expected shape {shape}, got {a.shape}")
+        return a
+
+    def linear(self, X, W, R=None) -> np.ndarray:
+        """Y[i,j] = sum_k X[i,k] W[j,k] (+ R[i,j]) in float64."""
+        M, K = X.shape
+        N = W.shape[0]
+        X = self._bits(X, (M, K))
+        W = self._bits(W, (N, K))
+        Rp = None
+        if R is not None:
+            R = self._bits(R, (M, N))
+            Rp = R.ctypes.data
+        Y = np.empty((M, N), dtype=np.float64)
+        rc = self.lib.ka_oracle_linear(M, N, K, X.ctypes.data, W.ctypes.data, Rp,
+                                       Y.ctypes.data)
+        if rc != 0:
+            raise ValueError("oracle rejected its arguments")
+        return Y
+
+    def linear_at(self, X, W, R, rows, cols) -> np.ndarray:
+        """The same definition evaluated at the positions (rows[t], cols[t])."""
+        M, K = X.shape
+        N = W.shape[0]
+        X = self._bits(X, (M, K))
+        W = self._bits(W, (N, K))
+        Rp = None
+        if R is not None:
+            R = self._bits(R, (M, N))
+            Rp = R.ctypes.data
+        rows = np.ascontiguousarray(rows, dtype=np.int64)
+        cols = np.ascontiguousarray(cols, dtype=np.int64)
+        if rows.shape != cols.shape or rows.ndim != 1:
+            raise ValueError("rows and cols must be 1-D and of equal length")
+        out = np.empty(rows.shape[0], dtype=np.float64)
+        rc = self.lib.ka_oracle_linear_at(M, N, K, X.ctypes.data, W.ctypes.data, Rp,
+                                          rows.shape[0], rows.ctypes.data,
+                                          cols.ctypes.data, out.ctypes.data)
+        if rc != 0:
+            raise ValueError("oracle rejected its arguments")
+        return out
+
+    def round_bf16(self, values) -> np.ndarray:
+        """Round float64 values to bf16 bit patterns (nearest, ties to even)."""
+        v = np.ascontiguousarray(values, dtype=np.float64)
+        out = np.empty(v.shape, dtype=np.uint16)
+        self.lib.ka_oracle_round_bf16(v.size, v.ctypes.data, out.ctypes.data)
+        return out
+
+
+_default: Oracle | None = None
+
+
+def default() -> Oracle:
+    """The oracle built in-tree (built on first use if it is missing)."""
+    global _default
+    if _default is None:
+        if not os.path.exists(LIBRARY):
+            build()
+        _default = Oracle(LIBRARY)
+    return _default
+
+
+def bf16_bits_to_f64(bits) -> np.ndarray:
+    """Exact widening of bf16 bit patterns to float64 (for the test checks)."""
+    b = np.asarray(bits, dtype=np.uint16).astype(np.uint32) << 16
+    with np.errstate(invalid="ignore"):          # signalling-NaN patterns
+        return b.view(np.float32).astype(np.float64)

@@ -1,0 +1,124 @@
+/*
+ * Plain CPU oracle for the fused linear-plus-residual operator
+ *
+ *     Y[i,j] = sum_k X[i,k] * W[j,k]  +  R[i,j]          (R optional)
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is the slow, obviously correct
+ * reference that the GPU library is checked against.  Only the test suite,
+ * the smoke check and the CPU-baseline leg of the benchmark load it; the
+ * product library never links, calls or falls back to it, and it shares no
+ * code, header, table or helper with the HIP sources.
+ *
+ * What it follows (KernelArc paper):
+ *   - Sec. "L1-030: attention output projection with residual" and Alg. 3:
+ *     the destination aliases the residual and the library computes
+ *     O <- W^T A + O with alpha = beta = 1 (cuBLASLt column-major notation).
+ *     Read in row-major, nn.Linear orientation (W stored [out, in] = [N, K]),
+ *     that is Y = X W^T + R.
+ *   - Sec. "Guided Sequential GEMM Boundary Study": BF16 operands.
+ *   - The inputs are bf16 bit patterns; every value is widened exactly to
+ *     double, every product of two bf16 values is exact in double, and the
+ *     k-sum runs in ascending k in double (no reassociation: build with
+ *     -O2 -ffp-contract=off and without -ffast-math).  The result is returned
+ *     in double and is NOT rounded to bf16.
+ *
+ * Pins: tests/test_oracle_pins.py (exact rational brute force, a hand-worked
+ * fixture, numpy's float64 matmul, W = 0, W = I, rank-1 integer closed form,
+ * row/K permutation and transpose invariants, and planted-mistake runs).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+/* bf16 is the top half of an IEEE binary32: widen by a 16-bit left shift. */
+static double bf16_bits_to_double(uint16_t bits)
+{
+    uint32_t u = (uint32_t)bits << 16;
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return (double)f;
+}
+
+/* One output element, straight from the definition. */
+static double element(int64_t i, int64_t j, int64_t N, int64_t K,
+                      const uint16_t *X, const uint16_t *W, const uint16_t *R)
+{
+    double acc = 0.0;
+    for (int64_t k = 0; k < K; ++k)
+        acc += bf16_bits_to_double(X[i * K + k]) * bf16_bits_to_double(W[j * K + k]);
+    if (R)
+        acc += bf16_bits_to_double(R[i * N + j]);
+    return acc;
+}
+
+/*
+ * Full output.  X is [M,K], W is [N,K], R is [M,N] or NULL, all row-major
+ * bf16 bit patterns; Y is [M,N] doubles.  Returns 0, or -1 on a negative
+ * dimension or a NULL buffer that is needed.
+ */
+int ka_oracle_linear(int64_t M, int64_t N, int64_t K,
+                     const uint16_t *X, const uint16_t *W, const uint16_t *R,
+                     double *Y)
+{
+    if (M < 0 || N < 0 || K < 0) return -1;
+    if (M * N > 0 && !Y) return -1;
+    if (M * K > 0 && !X) return -1;
+    if (N * K > 0 && !W) return -1;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t i = 0; i < M; ++i)
+        for (int64_t j = 0; j < N; ++j)
+            Y[i * N + j] = element(i, j, N, K, X, W, R);
+    return 0;
+}
+
+/*
+ * The same definition evaluated only at the n listed positions
+ * (rows[t], cols[t]); used for sampled checks at sizes where the full
+ * product is too slow on the CPU.  Indices must lie in [0,M) x [0,N).
+ */
+int ka_oracle_linear_at(int64_t M, int64_t N, int64_t K,
+                        const uint16_t *X, const uint16_t *W, const uint16_t *R,
+                        int64_t n, const int64_t *rows, const int64_t *cols,
+                        double *out)
+{
+    if (M < 0 || N < 0 || K < 0 || n < 0) return -1;
+    for (int64_t t = 0; t < n; ++t)
+        if (rows[t] < 0 || rows[t] >= M || cols[t] < 0 || cols[t] >= N) return -1;
+#pragma omp parallel for schedule(dynamic, 16)
+    for (int64_t t = 0; t < n; ++t)
+        out[t] = element(rows[t], cols[t], N, K, X, W, R);
+    return 0;
+}
+
+/*
+ * Round doubles to bf16 bit patterns, round-to-nearest, ties to even
+ * (IEEE 754 roundTiesToEven applied to the bf16 format: 8 significant bits,
+ * exponent range of binary32).  Written from the definition: the spacing of
+ * bf16 values around |x| is a power of two, so x is scaled by that spacing,
+ * rounded to the nearest integer (ties to even, the default rounding mode of
+ * rint) and scaled back.  Results above the largest finite bf16 after
+ * rounding become infinity; NaN becomes the quiet NaN 0x7FC0 with x's sign.
+ */
+void ka_oracle_round_bf16(int64_t n, const double *in, uint16_t *out)
+{
+    for (int64_t t = 0; t < n; ++t) {
+        double x = in[t];
+        uint16_t sign = signbit(x) ? 0x8000u : 0u;
+        if (isnan(x)) { out[t] = (uint16_t)(sign | 0x7FC0u); continue; }
+        double a = fabs(x);
+        if (isinf(a)) { out[t] = (uint16_t)(sign | 0x7F80u); continue; }
+        if (a == 0.0) { out[t] = sign; continue; }
+        int e;
+        frexp(a, &e);               /* a = f * 2^e, f in [0.5, 1) */
+        int exp2 = e - 1;           /* a in [2^exp2, 2^(exp2+1)) */
+        if (exp2 < -126) exp2 = -126; /* subnormal bf16: fixed spacing */
+        double spacing = ldexp(1.0, exp2 - 7);
+        double r = rint(a / spacing) * spacing;
+        const double max_finite = ldexp(255.0, 120); /* (2 - 2^-7) * 2^127 */
+        if (r > max_finite) { out[t] = (uint16_t)(sign | 0x7F80u); continue; }
+        float rf = (float)r;        /* exact: r is a bf16 value */
+        uint32_t u;
+        memcpy(&u, &rf, sizeof u);
+        out[t] = (uint16_t)(sign | (uint16_t)(u >> 16));
+    }
+}

@@ -1,0 +1,156 @@
+"""Seeded synthetic inputs for Y = X.W^T + R.
+
+This module only draws and lays out input bytes; it holds none of the
+operator's arithmetic.  Both the GPU library (through the tests and the
+benchmark) and the CPU oracle consume exactly the bytes produced here.
+
+Recipe (all tensors bf16, dense, row-major; X is [M,K], W is [N,K] in
+nn.Linear [out, in] layout, R is [M,N]):
+
+* ``g = torch.Generator().manual_seed(seed)``; X is drawn first, then W,
+  then R, each as float32 and rounded to bf16 (nearest-even) by torch.
+* ``normal``:  X, W ~ N(0,1)/sqrt(K) and R ~ N(0,1).
+* ``uniform``: X, W ~ U(-1,1)/sqrt(K) (``rand*2-1``), no residual.
+
+The named workloads are the attention-output-projection shapes the paper
+motivates (Sec. "From Sequential Plateaus to Design Requirements": one
+operator scored over 16 shapes with per-M configuration choices; Sec.
+"Guided Sequential GEMM Boundary Study": a large square BF16 GEMM).  The
+benchmark suite's own 16 shapes are not public in the paper; the sweep
+below (M in {1, 64, 512, 4096} x hidden in {2048, 4096, 5120, 8192}, N = K =
+hidden) stands in for them.
+"""
+from __future__ import annotations
+
+import hashlib
+import math
+from dataclasses import dataclass
+
+import numpy as np
+import torch
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    M: int
+    N: int
+    K: int
+    residual: bool
+    dist: str          # "normal" or "uniform"
+    seed: int
+
+    @property
+    def flops(self) -> int:
+        return 2 * self.M * self.N * self.K
+
+    @property
+    def algorithmic_bytes(self) -> int:
+        """Each operand read once and Y written once, 2 bytes per element."""
+        b = 2 * (self.M * self.K + self.N * self.K + self.M * self.N)
+        if self.residual:
+            b += 2 * self.M * self.N
+        return b
+
+
+SWEEP_M = (1, 64, 512, 4096)
+SWEEP_HIDDEN = (2048, 4096, 5120, 8192)
+
+
+def _sweep():
+    out = []
+    for mi, m in enumerate(SWEEP_M):
+        for hi, h in enumerate(SWEEP_HIDDEN):
+            s = mi * len(SWEEP_HIDDEN) + hi
+            out.append(Workload(f"sweep_s{s:02d}_m{m}_h{h}", m, h, h, True, "normal", s))
+    return tuple(out)
+
+
+TINY = Workload("tiny_m128_n256_k256", 128, 256, 256, True, "normal", 0)
+DECODE = Workload("decode_m16_h4096", 16, 4096, 4096, True, "normal", 0)
+PREFILL = Workload("prefill_m4096_h4096", 4096, 4096, 4096, True, "normal", 0)
+SQUARE = Workload("square_plain_8192", 8192, 8192, 8192, False, "uniform", 0)
+SWEEP = _sweep()
+ALL = (TINY, DECODE, PREFILL, SQUARE) + SWEEP
+BY_NAME = {w.name: w for w in ALL}
+
+
+def custom(M: int, N: int, K: int, residual: bool = True, dist: str = "normal",
+           seed: int = 0, name: str | None = None) -> Workload:
+    return Workload(name or f"custom_m{M}_n{N}_k{K}", M, N, K, residual, dist, seed)
+
+
+def make_inputs(w: Workload) -> dict:
+    """Draw X, W (and R) on the host as bf16 CPU tensors."""
+    g = torch.Generator().manual_seed(w.seed)
+    scale = 1.0 / math.sqrt(w.K) if w.K > 0 else 1.0
+
+    def draw(shape):
+        if w.dist == "normal":
+            return torch.randn(shape, generator=g, dtype=torch.float32)
+        if w.dist == "uniform":
+            return torch.rand(shape, generator=g, dtype=torch.float32) * 2.0 - 1.0
+        raise ValueError(f"unknown distribution {w.dist!r}")
+
+    X = (draw((w.M, w.K)) * scale).to(torch.bfloat16)
+    W = (draw((w.N, w.K)) * scale).to(torch.bfloat16)
+    out = {"X": X, "W": W, "R": None}
+    if w.residual:
+        out["R"] = torch.randn((w.M, w.N), generator=g, dtype=torch.float32).to(torch.bfloat16)
+    return out
+
+
+def bits(t: torch.Tensor) -> np.ndarray:
+    """The bf16 bit patterns of a CPU tensor as a numpy uint16 array (a view)."""
+    if t.dtype != torch.bfloat16:
+        raise TypeError("expected a bf16 tensor")
+    return t.contiguous().view(torch.int16).numpy().view(np.uint16)
+
+
+def from_bits(a: np.ndarray) -> torch.Tensor:
+    """bf16 CPU tensor holding the given uint16 bit patterns."""
+    a = np.ascontiguousarray(a, dtype=np.uint16)
+    return torch.from_numpy(a.view(np.int16).copy()).view(torch.bfloat16)
+
+
+def sha256(*tensors) -> str:
+    h = hashlib.sha256()
+    for t in tensors:
+        if t is not None:
+            h.update(bits(t).tobytes())
+    return h.hexdigest()
+
+
+# ---- structured inputs for closed-form checks (bit patterns only) ----------
+
+def rank1_integer(M: int, N: int, K: int, seed: int = 0, residual: bool = True):
+    """X[i,k] = a_i u_k and W[j,k] = b_j v_k with small integers.
+
+    a, b are drawn from [-8, 8]; u, v from {-1, 0, 1} and forced
+    non-constant.  With R drawn from the integers in [-64, 64] every value is
+    exactly representable in bf16, and every partial sum of the product is an
+    integer of magnitude below 2^24.  Returns (X, W, R, a, b, u, v) with the
+    tensors as bf16 and the factors as int64 numpy arrays.
+    """
+    rng = np.random.default_rng(seed)
+    a = rng.integers(-8, 9, size=M)
+    b = rng.integers(-8, 9, size=N)
+    u = rng.integers(-1, 2, size=K)
+    v = rng.integers(-1, 2, size=K)
+    if K >= 2:
+        u[0], u[-1] = 1, -1
+        v[0], v[1 % K] = 1, 1
+    X = torch.from_numpy(np.outer(a, u).astype(np.float32)).to(torch.bfloat16)
+    W = torch.from_numpy(np.outer(b, v).astype(np.float32)).to(torch.bfloat16)
+    R = None
+    if residual:
+        R = torch.from_numpy(rng.integers(-64, 65, size=(M, N)).astype(np.float32)).to(torch.bfloat16)
+    return X, W, R, a.astype(np.int64), b.astype(np.int64), u.astype(np.int64), v.astype(np.int64)
+
+
+def identity_weight(K: int) -> torch.Tensor:
+    return torch.eye(K, dtype=torch.float32).to(torch.bfloat16)
+
+
+def zero_weight(N: int, K: int) -> torch.Tensor:
+    return torch.zeros((N, K), dtype=torch.bfloat16)

@@ -1,0 +1,63 @@
+"""Planted mistakes in a copy of the oracle must each fail some pin.
+
+The real oracle source is patched in a temporary directory (never in the
+tree), rebuilt with the same flags, and the whole pin battery is run against
+it; a mutant that passes every pin would mean the pins cannot see that kind
+of mistake.
+"""
+import os
+
+import pytest
+
+import oracle
+from tests import pin_battery
+
+MUTANTS = {
+    "drop_last_k": ("for (int64_t k = 0; k < K; ++k)", "for (int64_t k = 0; k < K - 1; ++k)"),
+    "w_transposed": ("bf16_bits_to_double(W[j * K + k])",
+                     "bf16_bits_to_double(W[(k % N) * K + (j % K)])"),
+    "x_wrong_row": ("bf16_bits_to_double(X[i * K + k])",
+                    "bf16_bits_to_double(X[((i + 1) % M) * K + k])"),
+    "residual_sign": ("acc += bf16_bits_to_double(R[i * N + j]);",
+                      "acc -= bf16_bits_to_double(R[i * N + j]);"),
+    "residual_transposed": ("acc += bf16_bits_to_double(R[i * N + j]);",
+                            "acc += bf16_bits_to_double(R[(j % M) * N + (i % N)]);"),
+    "float_accumulator": ("double acc = 0.0;", "float acc = 0.0f;"),
+    "round_ties_away": ("rint(a / spacing)", "floor(a / spacing + 0.5)"),
+    "round_truncate": ("rint(a / spacing)", "trunc(a / spacing)"),
+    "round_no_subnormal_clamp": ("if (exp2 < -126) exp2 = -126;", "if (exp2 < -1022) exp2 = -1022;"),
+}
+
+
+def _patched_source(src, old, new, tmp_path):
+    assert src.count(old) >= 1, f"mutation target {old!r} no longer in the oracle"
+    text = src.replace(old, new)
+    if "(i + 1) % M" in new or "(j % M)" in new:
+        # these mutants need M in scope inside element(); pass it through
+        text = text.replace("static double element(int64_t i, int64_t j, int64_t N, int64_t K,",
+                            "static int64_t M_;\nstatic double element(int64_t i, int64_t j, int64_t N, int64_t K,")
+        text = text.replace("% M)", "% M_)")
+        text = text.replace("    if (M < 0 || N < 0 || K < 0) return -1;\n",
+                            "    if (M < 0 || N < 0 || K < 0) return -1;\n    M_ = M;\n")
+        text = text.replace("    if (M < 0 || N < 0 || K < 0 || n < 0) return -1;\n",
+                            "    if (M < 0 || N < 0 || K < 0 || n < 0) return -1;\n    M_ = M;\n")
+    path = tmp_path / "mutant.c"
+    path.write_text(text)
+    return str(path)
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutant_is_caught(name, tmp_path):
+    with open(oracle.SOURCE) as f:
+        src = f.read()
+    old, new = MUTANTS[name]
+    path = _patched_source(src, old, new, tmp_path)
+    lib = oracle.build(path, str(tmp_path / "libmutant.so"))
+    orc = oracle.Oracle(lib)
+    failed = []
+    for pin in pin_battery.ALL_PINS:
+        try:
+            pin(orc)
+        except AssertionError:
+            failed.append(pin.__name__)
+    assert failed, f"planted mistake {name} passed every pin"
