@@ -1,0 +1,133 @@
+/*
+ * kernelarc.h -- C ABI of the MI355X (gfx950) BF16 linear-plus-residual library.
+ *
+ * The operation is the attention output projection with residual addition of
+ * the KernelArc paper (Sec. "L1-030: attention output projection with
+ * residual" and Alg. 3): the destination aliases the residual and the
+ * library computes O <- W^T A + O with alpha = beta = 1, written there in
+ * column-major cuBLASLt notation.  In the row-major, nn.Linear reading used
+ * here (W stored [out, in] = [N, K]):
+ *
+ *     Y[i,j] = bf16( sum_k X[i,k] * W[j,k]  +  R[i,j] )
+ *
+ * with every product and partial sum in fp32 and a single round-to-nearest-
+ * even conversion of the fp32 result (accumulator plus residual) to bf16.
+ * The order in which the k-terms are summed is not part of the contract;
+ * it is fixed per plan, so one plan gives bitwise-identical results for
+ * identical inputs (no floating-point atomics anywhere).
+ *
+ * Types and layout (all entry points):
+ *   - X, W, R, Y are device pointers on the calling thread's current HIP
+ *     device, holding bf16 values as raw 16-bit patterns;
+ *   - X is [M,K], W is [N,K], R and Y are [M,N]; all dense row-major with no
+ *     padding (leading dimensions K, K, N, N);
+ *   - the caller owns every buffer; the library never allocates, frees or
+ *     retains them.  Internal state is limited to a per-device property cache
+ *     and per-device split-K workspaces that the library allocates once and
+ *     keeps until the process ends.
+ *
+ * Execution: calls enqueue work on `stream` and return without synchronising;
+ * a fault in a kernel surfaces at the caller's next synchronisation.  Calls
+ * on one stream are ordered; the split-K workspace of a device is shared, so
+ * calls that may run concurrently on different streams of the same device
+ * must not both pick a split-K plan (kernelarc_plan_uses_workspace).
+ *
+ * Errors: every entry point returns a status (KERNELARC_OK on success) and
+ * never throws, aborts or prints.  kernelarc_last_error() gives a detail
+ * string for the calling thread's most recent failure.
+ */
+#ifndef KERNELARC_H
+#define KERNELARC_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum kernelarc_status {
+    KERNELARC_OK = 0,
+    KERNELARC_ERR_INVALID_ARG = 1, /* negative size, NULL operand, bad overlap, size limit  */
+    KERNELARC_ERR_UNSUPPORTED = 2, /* no gfx950 device, or a forced plan that cannot run it */
+    KERNELARC_ERR_LAUNCH = 3,      /* the HIP runtime refused a launch or an allocation     */
+};
+
+/*
+ * Y = X W^T + R  (Alg. 3: O <- W^T A + O, alpha = beta = 1; the destination
+ * may alias the residual).
+ *
+ * M: rows of X, R, Y (the flattened token count); N: rows of W, columns of R
+ * and Y; K: columns of X and W.  M, N, K >= 0 and each below 2^31.
+ * Y == R (the same address) computes in place.  Any other overlap of Y's
+ * byte range with X, W or R is rejected with KERNELARC_ERR_INVALID_ARG.
+ * M == 0 or N == 0: nothing to do, returns KERNELARC_OK without a launch.
+ * K == 0: Y = R.
+ * Pointers that are 16-byte aligned with K a multiple of 8 take the MFMA
+ * kernels; anything else takes a slower generic kernel with the same result
+ * contract.
+ */
+int kernelarc_gemm_bf16_residual(int64_t M, int64_t N, int64_t K,
+                                 const void *X, const void *W, const void *R,
+                                 void *Y, hipStream_t stream);
+
+/*
+ * Y = X W^T  (the same operation without a residual; the plain BF16 GEMM of
+ * the paper's Sec. "Guided Sequential GEMM Boundary Study").  Arguments and
+ * errors as above; K == 0 gives Y = +0.
+ */
+int kernelarc_gemm_bf16(int64_t M, int64_t N, int64_t K,
+                        const void *X, const void *W, void *Y, hipStream_t stream);
+
+/*
+ * Plan introspection and forced-plan execution (for tests, the benchmark
+ * and offline tuning; Alg. 3's per-M plan cache, static validated table and
+ * heuristic fallback correspond to kernelarc_select_plan).
+ *
+ * A plan is one kernel variant (tile shape, staging depth, split-K rule).
+ * Plan ids run from 0 to kernelarc_plan_count() - 1.  None of these touch
+ * the GPU.
+ */
+int kernelarc_plan_count(void);
+
+/* Static, NUL-terminated name of a plan, or NULL for an unknown id. */
+const char *kernelarc_plan_name(int plan);
+
+/*
+ * 1 if `plan` can compute this shape (size limits and the K % 8 rule of the
+ * MFMA plans; pointer alignment is checked at call time), 0 if not, and -1
+ * for an unknown plan or negative sizes.
+ */
+int kernelarc_plan_supports(int plan, int64_t M, int64_t N, int64_t K, int residual);
+
+/*
+ * The plan the library runs for this shape when the pointers are 16-byte
+ * aligned, or -1 for negative sizes.  Depends on the shape only, never on
+ * data.
+ */
+int kernelarc_select_plan(int64_t M, int64_t N, int64_t K, int residual);
+
+/* 1 if `plan` on this shape uses the per-device split-K workspace, else 0. */
+int kernelarc_plan_uses_workspace(int plan, int64_t M, int64_t N, int64_t K);
+
+/*
+ * Y = X W^T (+ R if R != NULL) computed with the given plan.  Returns
+ * KERNELARC_ERR_UNSUPPORTED if the plan cannot compute this shape or these
+ * pointers' alignment, otherwise as kernelarc_gemm_bf16_residual.
+ */
+int kernelarc_gemm_bf16_with_plan(int plan, int64_t M, int64_t N, int64_t K,
+                                  const void *X, const void *W, const void *R,
+                                  void *Y, hipStream_t stream);
+
+/* Static description of a status code. */
+const char *kernelarc_status_string(int status);
+
+/* Detail of the calling thread's most recent failed call ("" if none). */
+const char *kernelarc_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KERNELARC_H */

@@ -1,0 +1,62 @@
+// Private declarations shared by the library's translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace kernelarc {
+
+// ---------------------------------------------------------------- plans ----
+// One plan = one kernel variant.  The table and the selection rules live in
+// plan.hip; the launchers live beside their kernels.
+enum PlanId : int {
+    PLAN_GENERIC = 0,        // scalar LDS-tiled kernel: any K, any alignment
+    PLAN_SKINNY = 1,         // M <= 64: stream W once, MFMA 16x16x32, in-WG split-K
+    PLAN_SKINNY_SPLITK = 2,  // as PLAN_SKINNY plus a cross-workgroup split-K
+    PLAN_TILE_256x256 = 3,   // MFMA macro-tile 256x256x64, 4 waves of 128x128
+    PLAN_TILE_256x128 = 4,   // MFMA macro-tile 256x128x64, 4 waves of 128x64
+    PLAN_TILE_128x128 = 5,   // MFMA macro-tile 128x128x64, 4 waves of 64x64
+    PLAN_COUNT = 6,
+};
+
+struct Problem {
+    int64_t M, N, K;
+    const uint16_t *X, *W, *R;   // R may be null (plain variant)
+    uint16_t *Y;
+};
+
+// Per-device split-K workspace: fp32 partials followed by tile counters.
+struct Workspace {
+    float *partials;
+    int64_t partial_floats;
+    unsigned *counters;
+    int64_t counter_count;
+};
+
+// Launchers: validate nothing (plan.hip has done it), enqueue, return the
+// hipError_t of the launch.
+hipError_t launch_generic(const Problem &p, hipStream_t s);
+hipError_t launch_skinny(const Problem &p, int split_k, const Workspace *ws, hipStream_t s);
+hipError_t launch_tile(int plan, const Problem &p, int num_cus, hipStream_t s);
+
+// Shape rules of the kernels, used by the plan table (host only).
+int skinny_split_for(int64_t M, int64_t N, int64_t K);
+int64_t skinny_workspace_floats(int64_t M, int64_t N, int split_k);
+int64_t skinny_counter_count(int64_t N);
+
+// ------------------------------------------------------- device helpers ----
+// bf16 <-> fp32.  Widening is exact (bf16 is the top half of a binary32).
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) {
+    return __uint_as_float(static_cast<uint32_t>(b) << 16);
+}
+
+// fp32 -> bf16, round to nearest, ties to even; NaN stays NaN (quiet),
+// finite values beyond the bf16 range round to infinity.
+__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<uint16_t>((u >> 16) | 0x0040u);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return static_cast<uint16_t>(u >> 16);
+}
+
+}  // namespace kernelarc

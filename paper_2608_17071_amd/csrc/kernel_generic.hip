@@ -1,0 +1,88 @@
+// Generic kernel: Y = X W^T (+ R) for any shape and any pointer alignment.
+//
+// This is the correctness fallback (K not a multiple of 8, pointers not
+// 16-byte aligned).  Each 256-thread workgroup computes a 64x64 output tile;
+// each thread owns a 4x4 sub-block strided by 16 in both directions.  Both
+// operands are staged through LDS as fp32 in 16-deep K slices with bounds-
+// checked scalar loads; products of bf16 values are exact in fp32 and the
+// k-terms are accumulated in ascending order.
+#include "internal.h"
+
+namespace kernelarc {
+namespace {
+
+constexpr int GT = 64;   // output tile edge
+constexpr int GK = 16;   // K slice
+
+__global__ __launch_bounds__(256) void generic_kernel(Problem p, int64_t tiles_n) {
+    __shared__ float xs[GK][GT + 1];
+    __shared__ float ws[GK][GT + 1];
+
+    const int tx = threadIdx.x & 15;
+    const int ty = threadIdx.x >> 4;
+    const int64_t tile = blockIdx.x;
+    const int64_t m0 = (tile / tiles_n) * GT;
+    const int64_t n0 = (tile % tiles_n) * GT;
+
+    float acc[4][4];
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int b = 0; b < 4; ++b) acc[a][b] = 0.0f;
+
+    for (int64_t k0 = 0; k0 < p.K; k0 += GK) {
+        // 64 rows x 16 k of each operand = 1024 values = 4 per thread.
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            const int idx = threadIdx.x + 256 * t;
+            const int r = idx / GK;
+            const int kk = idx % GK;
+            const int64_t k = k0 + kk;
+            const int64_t xm = m0 + r;
+            const int64_t wn = n0 + r;
+            xs[kk][r] = (xm < p.M && k < p.K) ? bf16_to_f32(p.X[xm * p.K + k]) : 0.0f;
+            ws[kk][r] = (wn < p.N && k < p.K) ? bf16_to_f32(p.W[wn * p.K + k]) : 0.0f;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int kk = 0; kk < GK; ++kk) {
+            float xv[4], wv[4];
+#pragma unroll
+            for (int a = 0; a < 4; ++a) xv[a] = xs[kk][ty + 16 * a];
+#pragma unroll
+            for (int b = 0; b < 4; ++b) wv[b] = ws[kk][tx + 16 * b];
+#pragma unroll
+            for (int a = 0; a < 4; ++a)
+#pragma unroll
+                for (int b = 0; b < 4; ++b) acc[a][b] = fmaf(xv[a], wv[b], acc[a][b]);
+        }
+        __syncthreads();
+    }
+
+#pragma unroll
+    for (int a = 0; a < 4; ++a) {
+        const int64_t i = m0 + ty + 16 * a;
+        if (i >= p.M) continue;
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+            const int64_t j = n0 + tx + 16 * b;
+            if (j >= p.N) continue;
+            float y = acc[a][b];
+            if (p.R) y += bf16_to_f32(p.R[i * p.N + j]);
+            p.Y[i * p.N + j] = f32_to_bf16_rne(y);
+        }
+    }
+}
+
+}  // namespace
+
+hipError_t launch_generic(const Problem &p, hipStream_t s) {
+    const int64_t tiles_m = (p.M + GT - 1) / GT;
+    const int64_t tiles_n = (p.N + GT - 1) / GT;
+    const int64_t tiles = tiles_m * tiles_n;
+    hipLaunchKernelGGL(generic_kernel, dim3(static_cast<unsigned>(tiles)), dim3(256), 0, s, p,
+                       tiles_n);
+    return hipGetLastError();
+}
+
+}  // namespace kernelarc

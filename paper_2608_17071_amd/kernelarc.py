@@ -1,0 +1,153 @@
+"""Python binding of the HIP library ``libkernelarc.so`` (ctypes).
+
+Only argument marshalling happens here: shapes and dtypes are checked,
+leading dimensions of X are flattened into M (the token count, Alg. 3), and
+the raw device pointers plus torch's current HIP stream are handed to the
+C ABI declared in ``include/kernelarc.h``.  Every arithmetic step runs in the
+library's kernels; there is no other backend, and importing this module
+raises if the library has not been built.
+
+The C entry points are also exposed under their own names
+(``kernelarc_gemm_bf16_residual`` and so on) for callers that manage raw
+pointers themselves.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+LIBRARY = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libkernelarc.so")
+
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_LAUNCH = 0, 1, 2, 3
+
+if not os.path.exists(LIBRARY):
+    raise ImportError(
+        f"{LIBRARY} is missing: build it with `python -m paper_2608_17071_amd.build` "
+        "(there is no fallback implementation)")
+
+_lib = ctypes.CDLL(LIBRARY)
+_I64 = ctypes.c_int64
+_P = ctypes.c_void_p
+
+_SIGS = {
+    "kernelarc_gemm_bf16_residual": (ctypes.c_int, [_I64, _I64, _I64, _P, _P, _P, _P, _P]),
+    "kernelarc_gemm_bf16": (ctypes.c_int, [_I64, _I64, _I64, _P, _P, _P, _P]),
+    "kernelarc_gemm_bf16_with_plan": (ctypes.c_int, [ctypes.c_int, _I64, _I64, _I64, _P, _P, _P, _P, _P]),
+    "kernelarc_plan_count": (ctypes.c_int, []),
+    "kernelarc_plan_name": (ctypes.c_char_p, [ctypes.c_int]),
+    "kernelarc_plan_supports": (ctypes.c_int, [ctypes.c_int, _I64, _I64, _I64, ctypes.c_int]),
+    "kernelarc_select_plan": (ctypes.c_int, [_I64, _I64, _I64, ctypes.c_int]),
+    "kernelarc_plan_uses_workspace": (ctypes.c_int, [ctypes.c_int, _I64, _I64, _I64]),
+    "kernelarc_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    "kernelarc_last_error": (ctypes.c_char_p, []),
+}
+
+for _name, (_res, _args) in _SIGS.items():
+    _fn = getattr(_lib, _name)
+    _fn.restype = _res
+    _fn.argtypes = _args
+    globals()[_name] = _fn
+
+EXPORTED = tuple(_SIGS)
+
+
+class KernelArcError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        detail = _lib.kernelarc_last_error().decode(errors="replace")
+        msg = _lib.kernelarc_status_string(status).decode()
+        super().__init__(f"{where}: {msg} ({detail})" if detail else f"{where}: {msg}")
+        self.status = status
+
+
+def _check(status: int, where: str) -> None:
+    if status != OK:
+        raise KernelArcError(status, where)
+
+
+def plan_count() -> int:
+    return _lib.kernelarc_plan_count()
+
+
+def plan_name(plan: int) -> str | None:
+    n = _lib.kernelarc_plan_name(plan)
+    return n.decode() if n is not None else None
+
+
+def plan_names() -> list[str]:
+    return [plan_name(i) for i in range(plan_count())]
+
+
+def select_plan(M: int, N: int, K: int, residual: bool = True) -> int:
+    return _lib.kernelarc_select_plan(M, N, K, int(residual))
+
+
+def plan_supports(plan: int, M: int, N: int, K: int, residual: bool = True) -> bool:
+    return _lib.kernelarc_plan_supports(plan, M, N, K, int(residual)) == 1
+
+
+def _stream_handle(stream=None) -> int:
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+def _operands(x: torch.Tensor, w: torch.Tensor, r: torch.Tensor | None, out: torch.Tensor | None):
+    if w.dim() != 2:
+        raise ValueError("w must be [N, K]")
+    N, K = w.shape
+    if x.shape[-1] != K:
+        raise ValueError(f"x's last dimension {x.shape[-1]} does not match K={K}")
+    lead = tuple(x.shape[:-1])
+    M = 1
+    for d in lead:
+        M *= d
+    for name, t in (("x", x), ("w", w), ("r", r), ("out", out)):
+        if t is None:
+            continue
+        if t.dtype != torch.bfloat16:
+            raise TypeError(f"{name} must be bfloat16")
+        if not t.is_cuda:
+            raise ValueError(f"{name} must be a GPU tensor")
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+        if t.device != x.device:
+            raise ValueError(f"{name} is on {t.device}, x on {x.device}")
+    if r is not None and tuple(r.shape) != lead + (N,):
+        raise ValueError(f"r must have shape {lead + (N,)}")
+    if out is None:
+        out = torch.empty(lead + (N,), dtype=torch.bfloat16, device=x.device)
+    elif tuple(out.shape) != lead + (N,):
+        raise ValueError(f"out must have shape {lead + (N,)}")
+    return M, N, K, out
+
+
+def gemm_bf16_residual(x, w, r, out=None, stream=None):
+    """Y = X W^T + R (out may be r itself for the in-place form)."""
+    M, N, K, out = _operands(x, w, r, out)
+    with torch.cuda.device(x.device):
+        st = _lib.kernelarc_gemm_bf16_residual(M, N, K, x.data_ptr(), w.data_ptr(), r.data_ptr(),
+                                               out.data_ptr(), _stream_handle(stream))
+    _check(st, "kernelarc_gemm_bf16_residual")
+    return out
+
+
+def gemm_bf16(x, w, out=None, stream=None):
+    """Y = X W^T."""
+    M, N, K, out = _operands(x, w, None, out)
+    with torch.cuda.device(x.device):
+        st = _lib.kernelarc_gemm_bf16(M, N, K, x.data_ptr(), w.data_ptr(), out.data_ptr(),
+                                      _stream_handle(stream))
+    _check(st, "kernelarc_gemm_bf16")
+    return out
+
+
+def gemm_bf16_with_plan(plan, x, w, r=None, out=None, stream=None):
+    """Y = X W^T (+ R) with an explicit plan id."""
+    M, N, K, out = _operands(x, w, r, out)
+    with torch.cuda.device(x.device):
+        st = _lib.kernelarc_gemm_bf16_with_plan(plan, M, N, K, x.data_ptr(), w.data_ptr(),
+                                                r.data_ptr() if r is not None else None,
+                                                out.data_ptr(), _stream_handle(stream))
+    _check(st, f"kernelarc_gemm_bf16_with_plan({plan_name(plan)})")
+    return out

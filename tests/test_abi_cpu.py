@@ -1,0 +1,124 @@
+"""The C-ABI library without a GPU: symbols, plan table, argument checks.
+
+Nothing here launches a kernel; every call either is host-only (plan
+queries) or returns before any device work (argument validation), or, on a
+host without a gfx950 device, must report KERNELARC_ERR_UNSUPPORTED.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "kernelarc.h")
+
+
+@pytest.fixture(scope="module")
+def ka():
+    from paper_2608_17071_amd import kernelarc
+    return kernelarc
+
+
+def header_functions():
+    with open(HEADER) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(kernelarc_\w+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported(ka):
+    names = header_functions()
+    assert len(names) >= 10
+    lib = ctypes.CDLL(ka.LIBRARY)
+    for n in names:
+        assert hasattr(lib, n), f"{n} declared in kernelarc.h but not exported"
+    assert set(names) == set(ka.EXPORTED), "binding and header disagree"
+
+
+def test_status_strings(ka):
+    for st in (ka.OK, ka.ERR_INVALID_ARG, ka.ERR_UNSUPPORTED, ka.ERR_LAUNCH):
+        assert ka.kernelarc_status_string(st)
+    assert ka.kernelarc_status_string(99) == b"unknown status"
+
+
+def test_plan_table(ka):
+    names = ka.plan_names()
+    assert len(names) == ka.plan_count() >= 6
+    assert len(set(names)) == len(names)
+    assert ka.plan_name(-1) is None and ka.plan_name(ka.plan_count()) is None
+    gen = names.index("generic_64x64_scalar")
+    # K not a multiple of 8 -> generic; skinny M -> a skinny plan; big -> a tile plan
+    assert ka.select_plan(128, 256, 250) == gen
+    for M in (1, 16, 64):
+        assert names[ka.select_plan(M, 4096, 4096)].startswith("skinny")
+    for M in (65, 512, 4096, 8192):
+        assert names[ka.select_plan(M, 4096, 4096)].startswith("tile")
+    assert ka.select_plan(-1, 4, 4) == -1
+    # every selected plan supports its shape; the generic plan supports everything
+    for (M, N, K) in [(1, 2048, 2048), (64, 8192, 8192), (512, 5120, 5120), (4096, 8192, 8192),
+                      (7, 9, 24), (300, 77, 1000), (0, 5, 8)]:
+        p = ka.select_plan(M, N, K)
+        assert ka.plan_supports(p, M, N, K), (M, N, K, names[p])
+        assert ka.plan_supports(gen, M, N, K)
+
+
+def test_plan_limits(ka):
+    names = ka.plan_names()
+    tile = names.index("tile_256x256x64_mfma32_w4")
+    skinny = names.index("skinny_mfma16_w8")
+    assert not ka.plan_supports(tile, 512, 512, 12)            # K % 8
+    assert not ka.plan_supports(skinny, 65, 512, 512)          # M > 64
+    assert not ka.plan_supports(skinny, 0, 512, 512)
+    assert ka.kernelarc_plan_supports(99, 1, 1, 1, 1) == -1
+    assert ka.kernelarc_plan_supports(tile, -1, 1, 1, 1) == -1
+    split = names.index("skinny_mfma16_w8_splitk")
+    assert ka.kernelarc_plan_uses_workspace(split, 16, 1024, 4096) == 1
+    assert ka.kernelarc_plan_uses_workspace(skinny, 16, 1024, 4096) == 0
+
+
+def test_validation_before_any_device_work(ka):
+    f = ka.kernelarc_gemm_bf16_residual
+    buf = (ctypes.c_uint16 * 4096)()
+    base = ctypes.addressof(buf)
+    # negative sizes
+    assert f(-1, 4, 4, base, base, base, base, None) == ka.ERR_INVALID_ARG
+    assert ka.kernelarc_last_error().startswith(b"negative size")
+    # empty output: nothing to do
+    assert f(0, 4, 4, None, None, None, None, None) == ka.OK
+    assert f(4, 0, 4, None, None, None, None, None) == ka.OK
+    # NULL operands
+    assert f(4, 4, 4, base, base, base, None, None) == ka.ERR_INVALID_ARG
+    assert f(4, 4, 4, None, base, base, base + 4096, None) == ka.ERR_INVALID_ARG
+    assert f(4, 4, 4, base, base, None, base + 4096, None) == ka.ERR_INVALID_ARG
+    # Y overlapping X, or partially overlapping R
+    X, W, R, Y = base, base + 64, base + 128, base + 256
+    assert f(4, 4, 4, X, W, R, X + 16, None) == ka.ERR_INVALID_ARG
+    assert f(4, 4, 4, X, W, R, R + 2, None) == ka.ERR_INVALID_ARG
+    assert ka.kernelarc_gemm_bf16(4, 4, 4, X, W, W + 8, None) == ka.ERR_INVALID_ARG
+    # a forced plan id out of range
+    assert ka.kernelarc_gemm_bf16_with_plan(-3, 4, 4, 4, X, W, R, Y, None) == ka.ERR_UNSUPPORTED
+    assert ka.kernelarc_gemm_bf16_with_plan(99, 4, 4, 4, X, W, R, Y, None) == ka.ERR_UNSUPPORTED
+
+
+def test_no_device_is_unsupported(ka):
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is present")
+    buf = (ctypes.c_uint16 * 4096)()
+    base = ctypes.addressof(buf)
+    st = ka.kernelarc_gemm_bf16_residual(4, 4, 4, base, base + 64, base + 128, base + 256, None)
+    assert st == ka.ERR_UNSUPPORTED
+    assert ka.kernelarc_last_error()
+
+
+def test_python_side_checks(ka):
+    import torch
+    x = torch.zeros(4, 8, dtype=torch.bfloat16)
+    w = torch.zeros(4, 8, dtype=torch.bfloat16)
+    with pytest.raises(ValueError):
+        ka.gemm_bf16(x, w)                       # CPU tensors are rejected before the ABI
+    with pytest.raises(TypeError):
+        ka.gemm_bf16(x.float(), w)
+    with pytest.raises(ValueError):
+        ka.gemm_bf16(torch.zeros(4, 7, dtype=torch.bfloat16), w)
