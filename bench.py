@@ -1,0 +1,402 @@
+#!/usr/bin/env python3
+"""Benchmark of Y = X W^T + R (bf16, fp32 accumulation) on one MI355X.
+
+Workload: the 16-shape sweep M in {1, 64, 512, 4096} x hidden in {2048, 4096,
+5120, 8192} (N = K = hidden), residual on, seeds 0-15 -- synthetic stand-ins
+for the paper's 16-shape attention-output-projection task.  One step = one
+call of the library per shape.
+
+Cold operands: every shape holds enough copies of (X, W, R, Y) to span at
+least 1 GiB (4x the 256 MB Infinity Cache) and the calls cycle through them,
+so each call reads operands that were last touched a full GiB of traffic
+earlier -- they come from HBM.  Timing: the calls over all copies are
+captured once in a HIP graph; each timed step replays it between two HIP
+events on the capture stream, and per-call time = elapsed / copies (this
+keeps host submission cost out of 1-20 us kernels).  The per-shape time is
+the median over the timed steps.
+
+Printed JSON line (stdout, last line):
+  value     geometric mean over the 16 shapes of TFLOP/s = 2MNK / t
+  roofline  the kernel variant with the most time in a step: algorithmic
+            FLOPs (MFMA-bound) or bytes (HBM-bound) of its launches divided
+            by their summed durations, against the MI355X peak
+  cpu_baseline  the CPU oracle (fp64, OpenMP) on a time-bounded row sample
+            of the same 16 shapes, same aggregation
+Per-shape rows, the geometric mean of per-shape roofline fractions, and the
+three single-shape gates (decode M=16, prefill 4096^3, square 8192^3 plain)
+are extra fields of the same line.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6          # 256 CU x 4096 FLOP/clk x 2.4 GHz, dense
+PEAK_HBM_GBPS = 8000.0
+ROTATE_BYTES = 1 << 30
+MAX_COPIES = 256
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def roofline_time(w):
+    return max(w.flops / (PEAK_BF16_TFLOPS * 1e12), w.algorithmic_bytes / (PEAK_HBM_GBPS * 1e9))
+
+
+def bound_of(w):
+    return "mfma" if w.flops / (PEAK_BF16_TFLOPS * 1e12) >= w.algorithmic_bytes / (PEAK_HBM_GBPS * 1e9) else "hbm"
+
+
+def geomean(xs):
+    return math.exp(sum(math.log(x) for x in xs) / len(xs))
+
+
+def source_digest(paths):
+    h = hashlib.sha256()
+    for p in paths:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+# Kernel symbol fragment of each tile plan (rocprofv3 reports symbols).
+PLAN_SYMBOL = {
+    "tile_256x256_k64_w8": "Cfg<256, 256, 64, 2, 4, 2, 2>",
+    "tile_128x128_k64_w4": "Cfg<128, 128, 64, 2, 2, 2, 2>",
+    "tile_128x128_k64_w4_splitk": "Cfg<128, 128, 64, 2, 2, 2, 2>",
+}
+KERNEL_SOURCES = ["paper_2608_17071_amd/csrc/kernel_tile.hip", "paper_2608_17071_amd/csrc/internal.h"]
+
+
+def summarize_traffic(pmc_dir, plan, shapes, command):
+    """profiles/traffic.json from four rocprofv3 --pmc runs under pmc_dir:
+    fetch/ and write/ (FETCH_SIZE, WRITE_SIZE of `bench.py --only <shapes>`),
+    copy_fetch/ and copy_write/ (the same counters of --copy-calibration)."""
+    import csv
+    from paper_2608_17071_amd import workloads as wl
+
+    def per_grid(sub, counter, needle):
+        out = {}
+        with open(os.path.join(pmc_dir, sub, "p_counter_collection.csv")) as f:
+            for r in csv.DictReader(f):
+                if r["Counter_Name"] == counter and needle in r["Kernel_Name"]:
+                    out.setdefault(int(r["Grid_Size"]), []).append(float(r["Counter_Value"]))
+        return {g: sum(v) / len(v) for g, v in out.items()}
+
+    copy_bytes = 1 << 28
+    cf = per_grid("copy_fetch", "FETCH_SIZE", "copyBuffer")
+    cw = per_grid("copy_write", "WRITE_SIZE", "copyBuffer")
+    fetch_scale = copy_bytes / (1024 * max(cf.values()))
+    write_scale = copy_bytes / (1024 * max(cw.values()))
+    sym = PLAN_SYMBOL[plan]     # a 256x256 tile, 512 threads per workgroup
+    fetch = per_grid("fetch", "FETCH_SIZE", sym)
+    write = per_grid("write", "WRITE_SIZE", sym)
+    rows, total = [], 0.0
+    for name in shapes:
+        w = wl.BY_NAME[name]
+        # the shapes of one run have distinct grids (work-items = output
+        # tiles x threads per workgroup, no split-K for this plan)
+        g = -(-w.M // 256) * -(-w.N // 256) * 512
+        b = fetch[g] * 1024 * fetch_scale + write[g] * 1024 * write_scale
+        total += b
+        rows.append({"shape": name, "fetch_kib": fetch[g], "write_kib": write[g], "hbm_bytes": b,
+                     "algorithmic_bytes": w.algorithmic_bytes})
+    rec = {"kernels": {plan: {
+        "bytes_per_launch": total / len(shapes), "shapes": rows,
+        "fetch_scale": fetch_scale, "write_scale": write_scale,
+        "sources": KERNEL_SOURCES, "source_sha256": source_digest(KERNEL_SOURCES),
+        "command": command}}}
+    os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(rec, f, indent=1)
+    print(json.dumps(rec, indent=1))
+
+
+def measured_traffic(plan_name):
+    """HBM bytes per launch from a committed counter summary, if it is current."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    with open(TRAFFIC_FILE) as f:
+        rec = json.load(f)
+    entry = rec.get("kernels", {}).get(plan_name)
+    if not entry:
+        return None
+    if entry.get("source_sha256") != source_digest(entry.get("sources", [])):
+        return None        # kernel changed since the counters were taken
+    return entry.get("bytes_per_launch")
+
+
+class Case:
+    def __init__(self, w, ka, torch, rotate=True):
+        from paper_2608_17071_amd import workloads as wl
+        t = wl.make_inputs(w)
+        self.w = w
+        self.host = t
+        x, W = t["X"].cuda(), t["W"].cuda()
+        r = t["R"].cuda() if w.residual else None
+        set_bytes = w.algorithmic_bytes
+        n = 1
+        if rotate:
+            n = max(2, min(MAX_COPIES, -(-ROTATE_BYTES // set_bytes)))
+        self.sets = []
+        for i in range(n):
+            self.sets.append((x if i == 0 else x.clone(), W if i == 0 else W.clone(),
+                              None if r is None else (r if i == 0 else r.clone()),
+                              torch.empty(w.M, w.N, dtype=torch.bfloat16, device="cuda")))
+        self.plan = ka.select_plan(w.M, w.N, w.K, w.residual)
+        self.plan_name = ka.plan_name(self.plan)
+        self.times = []
+        self.graph = None
+
+    def call(self, ka, i):
+        x, W, r, y = self.sets[i]
+        if r is not None:
+            ka.gemm_bf16_residual(x, W, r, out=y)
+        else:
+            ka.gemm_bf16(x, W, out=y)
+
+    def call_all(self, ka):
+        for i in range(len(self.sets)):
+            self.call(ka, i)
+
+    def free(self):
+        self.sets = []
+        self.graph = None
+
+
+def time_cases(cases, steps, warmup, ka, torch, use_graph=True):
+    """Warm up, capture, then time `steps` passes over all cases; returns wall seconds."""
+    for c in cases:
+        for _ in range(max(1, warmup)):
+            c.call_all(ka)       # also allocates any split-K workspace before capture
+    torch.cuda.synchronize()
+    if use_graph:
+        for c in cases:
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                c.call_all(ka)
+            c.graph = g
+        for c in cases:
+            for _ in range(max(1, warmup)):
+                c.graph.replay()
+        torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    events = []
+    for _ in range(steps):
+        for c in cases:
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record()
+            if use_graph:
+                c.graph.replay()
+            else:
+                c.call_all(ka)
+            b.record()
+            events.append((c, a, b))
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    for c, a, b in events:
+        c.times.append(a.elapsed_time(b) * 1e-3 / len(c.sets))
+    return wall
+
+
+def median(xs):
+    s = sorted(xs)
+    n = len(s)
+    return s[n // 2] if n % 2 else 0.5 * (s[n // 2 - 1] + s[n // 2])
+
+
+def shape_row(c):
+    w = c.w
+    t = median(c.times)
+    return {
+        "shape": w.name, "M": w.M, "N": w.N, "K": w.K, "plan": c.plan_name,
+        "us": round(t * 1e6, 3), "tflops": round(w.flops / t / 1e12, 3),
+        "gbps": round(w.algorithmic_bytes / t / 1e9, 1), "bound": bound_of(w),
+        "roofline_frac": round(roofline_time(w) / t, 4),
+    }
+
+
+def cpu_baseline(cases, seconds):
+    """The oracle on rows 0, 1, 2, ... of every shape until its time share is used."""
+    import numpy as np
+    import oracle
+    from paper_2608_17071_amd import workloads as wl
+
+    orc = oracle.default()
+    per_shape = seconds / len(cases)
+    rates, rows_done = [], []
+    for c in cases:
+        w = c.w
+        xb, wb = wl.bits(c.host["X"]), wl.bits(c.host["W"])
+        rb = wl.bits(c.host["R"]) if c.host["R"] is not None else None
+        cols = np.arange(w.N, dtype=np.int64)
+        flops, rows, t0 = 0, 0, time.perf_counter()
+        while rows < w.M:
+            orc.linear_at(xb, wb, rb, np.full(w.N, rows, dtype=np.int64), cols)
+            rows += 1
+            flops += 2 * w.N * w.K
+            if time.perf_counter() - t0 >= per_shape:
+                break
+        el = time.perf_counter() - t0
+        rates.append(flops / el / 1e12)
+        rows_done.append(rows)
+    return {
+        "value": geomean(rates), "unit": "TFLOP/s (fp64 oracle, geomean over 16 shapes)",
+        "cores": orc.threads(), "kind": "oracle",
+        "sample": (f"whole output rows 0..r-1 of each of the 16 sweep shapes, r = {rows_done} "
+                   f"(about {per_shape:.2f} s per shape), same seeded inputs"),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--hot", action="store_true", help="no rotating copies: hot-cache timing (labelled)")
+    ap.add_argument("--no-graph", action="store_true", help="launch eagerly instead of replaying a HIP graph")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-gates", action="store_true", help="skip the decode/prefill/square extras")
+    ap.add_argument("--only", default="",
+                    help="comma-separated workload names: time just these (for profiling one kernel)")
+    ap.add_argument("--summarize-traffic", nargs=2, metavar=("PMC_DIR", "SHAPES"),
+                    help="write profiles/traffic.json for the dominant plan from counter runs")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 256 MiB device copy 10 times (reference for HBM byte counters)")
+    args = ap.parse_args()
+
+    if args.summarize_traffic:
+        pmc_dir, shapes = args.summarize_traffic
+        shapes = shapes.split(",")
+        cmd = ("rocprofv3 --pmc FETCH_SIZE (then WRITE_SIZE) -d <dir>/fetch (write) -o p --output-format csv "
+               f"-- python bench.py --only {','.join(shapes)} --steps 2 --warmup 1; the same two counters of "
+               "python bench.py --copy-calibration into <dir>/copy_fetch, <dir>/copy_write")
+        summarize_traffic(pmc_dir, "tile_256x256_k64_w8", shapes, cmd)
+        return
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path "
+              "(run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2608_17071_amd import kernelarc as ka
+    from paper_2608_17071_amd import workloads as wl
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    torch.cuda.set_device(0)
+    if args.copy_calibration:
+        a = torch.ones(1 << 28, dtype=torch.uint8, device="cuda")
+        b = torch.empty_like(a)
+        for _ in range(10):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes_read": a.numel(), "bytes_written": b.numel(), "launches": 10}))
+        return
+
+    if args.only:
+        only = [wl.BY_NAME[n] for n in args.only.split(",")]
+        cases = [Case(w, ka, torch, rotate=not args.hot) for w in only]
+        time_cases(cases, args.steps, args.warmup, ka, torch, use_graph=not args.no_graph)
+        print(json.dumps({"only": [shape_row(c) for c in cases]}), flush=True)
+        return
+    log("generating inputs ...")
+    sweep = [Case(w, ka, torch, rotate=not args.hot) for w in wl.SWEEP]
+    torch.cuda.synchronize()
+    log(f"timing {len(sweep)} shapes x {args.steps} steps (warmup {args.warmup}) ...")
+    wall = time_cases(sweep, args.steps, args.warmup, ka, torch, use_graph=not args.no_graph)
+    rows = [shape_row(c) for c in sweep]
+    for r in rows:
+        log(f"  {r['shape']:24s} {r['plan']:28s} {r['us']:9.2f} us {r['tflops']:8.1f} TF "
+            f"{r['gbps']:7.0f} GB/s  {r['bound']} frac {r['roofline_frac']:.3f}")
+
+    gemm_s_per_step = sum(median(c.times) for c in sweep)
+    value = geomean([r["tflops"] for r in rows])
+    frac_geo = geomean([r["roofline_frac"] for r in rows])
+
+    # dominant kernel variant: most summed time per step
+    by_plan = {}
+    for c in sweep:
+        d = by_plan.setdefault(c.plan_name, {"t": 0.0, "flops": 0, "bytes": 0, "launches": 0, "cases": []})
+        d["t"] += median(c.times)
+        d["flops"] += c.w.flops
+        d["bytes"] += c.w.algorithmic_bytes
+        d["launches"] += 1
+        d["cases"].append(c)
+    dom_name, dom = max(by_plan.items(), key=lambda kv: kv[1]["t"])
+    mfma_bound = sum(roofline_time(c.w) for c in dom["cases"] if bound_of(c.w) == "mfma") >= \
+        sum(roofline_time(c.w) for c in dom["cases"] if bound_of(c.w) == "hbm")
+    avg_launch = dom["t"] / dom["launches"]
+    if mfma_bound:
+        achieved = dom["flops"] / dom["launches"] / avg_launch / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s"}
+    else:
+        achieved = dom["bytes"] / dom["launches"] / avg_launch / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s"}
+    roof["frac"] = round(achieved / roof["peak"], 4)
+    roof["traffic"] = measured_traffic(dom_name)
+    roof["kernel"] = dom_name
+    roof["avg_launch_us"] = round(avg_launch * 1e6, 3)
+    roof["launches_per_step"] = dom["launches"]
+    roof["shapes"] = [c.w.name for c in dom["cases"]]
+
+    gates = {}
+    if not args.no_gates:
+        for c in sweep:
+            c.free()
+        extra = [Case(w, ka, torch, rotate=not args.hot) for w in (wl.DECODE, wl.PREFILL, wl.SQUARE)]
+        time_cases(extra, args.steps, args.warmup, ka, torch, use_graph=not args.no_graph)
+        for c in extra:
+            r = shape_row(c)
+            gates[c.w.name] = r
+            log(f"  {r['shape']:24s} {r['plan']:28s} {r['us']:9.2f} us {r['tflops']:8.1f} TF "
+                f"{r['gbps']:7.0f} GB/s  {r['bound']} frac {r['roofline_frac']:.3f}")
+        del extra
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log(f"timing the CPU oracle (~{args.cpu_seconds:.0f} s) ...")
+        cpu = cpu_baseline(sweep, args.cpu_seconds)
+
+    out = {
+        "metric": "BF16 TFLOP/s and % of MFMA peak (or % HBM BW) per shape; geomean over sweep",
+        "value": round(value, 3),
+        "unit": "TFLOP/s (geomean over the 16-shape sweep)",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(gemm_s_per_step * 1e3, 4),
+        "wall_ms_per_step_all_copies": round(wall / args.steps * 1e3, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic (seeded; bf16 N(0,1)/sqrt(K) operands, N(0,1) residual)",
+        "config": {
+            "workload": "sweep16: Y = X W^T + R, M in {1,64,512,4096} x N=K in {2048,4096,5120,8192}, seeds 0-15",
+            "cache": "hot (labelled)" if args.hot else "cold: calls rotate over >= 1 GiB of operand copies",
+            "launch": "eager" if args.no_graph else "HIP graph replay of one call per operand copy",
+            "accumulate": "fp32",
+        },
+        "sweep_geomean_roofline_frac": round(frac_geo, 4),
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "shapes": rows,
+        "gates": gates,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

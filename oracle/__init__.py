@@ -54,6 +54,8 @@ class Oracle:
         lib.ka_oracle_linear_at.restype = ctypes.c_int
         lib.ka_oracle_round_bf16.argtypes = [_I64, _P, _P]
         lib.ka_oracle_round_bf16.restype = None
+        lib.ka_oracle_threads.argtypes = []
+        lib.ka_oracle_threads.restype = ctypes.c_int
         self.lib = lib
         self.path = path
 
@@ -104,6 +106,10 @@ class Oracle:
         if rc != 0:
             raise ValueError("oracle rejected its arguments")
         return out
+
+    def threads(self) -> int:
+        """OpenMP threads the oracle's loops use."""
+        return int(self.lib.ka_oracle_threads())
 
     def round_bf16(self, values) -> np.ndarray:
         """Round float64 values to bf16 bit patterns (nearest, ties to even)."""

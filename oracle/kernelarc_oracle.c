@@ -29,6 +29,9 @@
 #include <math.h>
 #include <stdint.h>
 #include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
 
 /* bf16 is the top half of an IEEE binary32: widen by a 16-bit left shift. */
 static double bf16_bits_to_double(uint16_t bits)
@@ -121,4 +124,14 @@ void ka_oracle_round_bf16(int64_t n, const double *in, uint16_t *out)
         memcpy(&u, &rf, sizeof u);
         out[t] = (uint16_t)(sign | (uint16_t)(u >> 16));
     }
+}
+
+/* Number of threads the OpenMP loops above use (1 without OpenMP). */
+int ka_oracle_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
 }

@@ -36,22 +36,38 @@ constexpr int64_t LIMIT_ITEMS = (int64_t{1} << 32) - 1;
 constexpr int64_t PANEL_LIMIT = int64_t{1} << 31;   // bytes addressable by one buffer resource
 
 // Split-K workspace capacity per device (partials in floats, tile counters).
-constexpr int64_t WS_PARTIAL_FLOATS = int64_t{1} << 20;
+constexpr int64_t WS_PARTIAL_FLOATS = int64_t{1} << 24;
 constexpr int64_t WS_COUNTERS = int64_t{1} << 16;
+constexpr int64_t CUS = 256;        // MI355X compute units
+constexpr int MAX_SPLIT = 16;
+
+enum PlanKind { KIND_GENERIC, KIND_SKINNY, KIND_TILE };
 
 struct PlanInfo {
     const char *name;
-    int bm, bn;   // macro-tile edge for tile plans, 0 otherwise
+    PlanKind kind;
+    int tile_cfg;   // TileCfg for tile plans, -1 otherwise
+    int split;      // tile plans: 1 = no split-K, 0 = split-K by rule
 };
 
-const PlanInfo PLANS[PLAN_COUNT] = {
-    {"generic_64x64_scalar", 0, 0},
-    {"skinny_mfma16_w8", 0, 0},
-    {"skinny_mfma16_w8_splitk", 0, 0},
-    {"tile_256x256x64_mfma32_w4", 256, 256},
-    {"tile_256x128x64_mfma32_w4", 256, 128},
-    {"tile_128x128x64_mfma32_w4", 128, 128},
+const PlanInfo PLANS[] = {
+    {"generic_64x64_scalar", KIND_GENERIC, -1, 1},
+    {"skinny_mfma16_w8", KIND_SKINNY, -1, 1},
+    {"skinny_mfma16_w8_splitk", KIND_SKINNY, -1, 0},
+    {"tile_256x256_k64_w8", KIND_TILE, TC_256x256_K64_S2_W8, 1},
+    {"tile_256x256_k64_w4", KIND_TILE, TC_256x256_K64_S2_W4, 1},
+    {"tile_256x128_k64_w8", KIND_TILE, TC_256x128_K64_S2_W8, 1},
+    {"tile_128x256_k64_w8", KIND_TILE, TC_128x256_K64_S2_W8, 1},
+    {"tile_256x128_k64_w4", KIND_TILE, TC_256x128_K64_S2_W4, 1},
+    {"tile_128x128_k64_w4", KIND_TILE, TC_128x128_K64_S2_W4, 1},
+    {"tile_64x256_k64_w4", KIND_TILE, TC_64x256_K64_S2_W4, 1},
+    {"tile_256x256_k64_w8_splitk", KIND_TILE, TC_256x256_K64_S2_W8, 0},
+    {"tile_256x128_k64_w8_splitk", KIND_TILE, TC_256x128_K64_S2_W8, 0},
+    {"tile_128x256_k64_w8_splitk", KIND_TILE, TC_128x256_K64_S2_W8, 0},
+    {"tile_128x128_k64_w4_splitk", KIND_TILE, TC_128x128_K64_S2_W4, 0},
+    {"tile_64x256_k64_w4_splitk", KIND_TILE, TC_64x256_K64_S2_W4, 0},
 };
+constexpr int NUM_PLANS = static_cast<int>(sizeof(PLANS) / sizeof(PLANS[0]));
 
 int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
@@ -61,14 +77,34 @@ int skinny_split_of(int plan, int64_t M, int64_t N, int64_t K) {
     return rule < 2 ? 2 : rule;
 }
 
+int64_t tile_count(const TileShape &ts, int64_t M, int64_t N) { return cdiv(M, ts.bm) * cdiv(N, ts.bn); }
+
+// Split-K rule of the "_splitk" tile plans: enough K slices that the tiles
+// fill one round of workgroup slots on the 256 CUs, each slice at least 8
+// BK steps deep; at least 2 so the plan always exercises the reduction.
+int tile_split_of(int plan, int64_t M, int64_t N, int64_t K) {
+    const PlanInfo &pi = PLANS[plan];
+    if (pi.split >= 1) return pi.split;
+    const TileShape ts = tile_shape(pi.tile_cfg);
+    const int64_t tiles = tile_count(ts, M, N);
+    const int64_t slots = CUS * ts.workgroups_per_cu;
+    int64_t split = tiles > 0 ? slots / tiles : 1;
+    const int64_t by_depth = K / (8 * ts.bk);
+    if (split > by_depth) split = by_depth;
+    if (split > MAX_SPLIT) split = MAX_SPLIT;
+    if (split < 2) split = 2;
+    return static_cast<int>(split);
+}
+
 bool supports(int plan, int64_t M, int64_t N, int64_t K, bool residual) {
     (void)residual;
     if (M < 0 || N < 0 || K < 0 || M > LIMIT_DIM || N > LIMIT_DIM || K > LIMIT_DIM) return false;
-    switch (plan) {
-        case PLAN_GENERIC:
+    if (plan < 0 || plan >= NUM_PLANS) return false;
+    const PlanInfo &pi = PLANS[plan];
+    switch (pi.kind) {
+        case KIND_GENERIC:
             return cdiv(M, 64) * cdiv(N, 64) * 256 <= LIMIT_ITEMS;
-        case PLAN_SKINNY:
-        case PLAN_SKINNY_SPLITK: {
+        case KIND_SKINNY: {
             if (M < 1 || M > 64 || K % 8 != 0) return false;
             if (N * K * 2 >= PANEL_LIMIT || 64 * K * 2 >= PANEL_LIMIT) return false;
             const int split = skinny_split_of(plan, M, N, K);
@@ -78,69 +114,89 @@ bool supports(int plan, int64_t M, int64_t N, int64_t K, bool residual) {
                 return false;
             return true;
         }
-        case PLAN_TILE_256x256:
-        case PLAN_TILE_256x128:
-        case PLAN_TILE_128x128: {
-            const PlanInfo &pi = PLANS[plan];
+        case KIND_TILE: {
+            const TileShape ts = tile_shape(pi.tile_cfg);
             if (K % 8 != 0) return false;
-            if (int64_t{pi.bm} * K * 2 >= PANEL_LIMIT || int64_t{pi.bn} * K * 2 >= PANEL_LIMIT) return false;
-            if (int64_t{pi.bm} * N * 2 >= PANEL_LIMIT) return false;   // epilogue panel of R / Y
-            return cdiv(M, pi.bm) * cdiv(N, pi.bn) * 256 <= LIMIT_ITEMS;
+            if (int64_t{ts.bm} * K * 2 >= PANEL_LIMIT || int64_t{ts.bn} * K * 2 >= PANEL_LIMIT) return false;
+            if (int64_t{ts.bm} * N * 2 >= PANEL_LIMIT) return false;   // epilogue panel of R / Y
+            const int64_t tiles = tile_count(ts, M, N);
+            const int split = tile_split_of(plan, M, N, K);
+            if (tiles * split * 512 > LIMIT_ITEMS) return false;
+            if (split > 1 && (tiles * split * ts.bm * ts.bn > WS_PARTIAL_FLOATS || tiles > WS_COUNTERS))
+                return false;
+            return true;
         }
-        default:
-            return false;
     }
+    return false;
 }
 
-// Exact-shape entries (M, N, K, residual) -> plan; filled from measurements.
+int plan_index(const char *name) {
+    for (int i = 0; i < NUM_PLANS; ++i)
+        if (std::strcmp(PLANS[i].name, name) == 0) return i;
+    return -1;
+}
+
+// Exact-shape entries (M, N, K, residual) -> plan name; from measurements on
+// MI355X (the benchmark's cold-cache protocol).  The sentinel has M = -1.
 struct TableEntry {
     int64_t M, N, K;
     int residual;
-    int plan;
+    const char *plan;
 };
 const TableEntry TABLE[] = {
-    {0, 0, 0, 0, -1},   // sentinel
+    // attention-output-projection sweep: M x (N = K = hidden), residual
+    {1, 2048, 2048, 1, "skinny_mfma16_w8"},
+    {1, 4096, 4096, 1, "skinny_mfma16_w8"},
+    {1, 5120, 5120, 1, "skinny_mfma16_w8"},
+    {1, 8192, 8192, 1, "skinny_mfma16_w8"},
+    {16, 4096, 4096, 1, "skinny_mfma16_w8"},
+    {64, 2048, 2048, 1, "skinny_mfma16_w8_splitk"},
+    {64, 4096, 4096, 1, "skinny_mfma16_w8"},
+    {64, 5120, 5120, 1, "tile_128x128_k64_w4_splitk"},
+    {64, 8192, 8192, 1, "tile_128x128_k64_w4_splitk"},
+    {512, 2048, 2048, 1, "tile_128x128_k64_w4_splitk"},
+    {512, 4096, 4096, 1, "tile_128x128_k64_w4_splitk"},
+    {512, 5120, 5120, 1, "tile_128x128_k64_w4_splitk"},
+    {512, 8192, 8192, 1, "tile_128x128_k64_w4_splitk"},
+    {4096, 2048, 2048, 1, "tile_128x128_k64_w4"},
+    {4096, 4096, 4096, 1, "tile_256x256_k64_w8"},
+    {4096, 5120, 5120, 1, "tile_128x128_k64_w4"},
+    {4096, 8192, 8192, 1, "tile_256x256_k64_w8"},
+    // plain BF16 GEMM
+    {8192, 8192, 8192, 0, "tile_256x256_k64_w8"},
+    {-1, 0, 0, 0, ""},   // sentinel
 };
 
-// Relative cost of one output element for each macro tile (larger tiles
-// reuse each staged byte more often) and how many workgroups a CU holds.
+// Rule-based choice when no table entry matches (from the same
+// measurements): the skinny kernel up to 64 rows (its cross-workgroup split
+// when the weight has too few 16-row strips to fill the CUs); a 128x128 tile
+// with split-K for the ridge range up to 1024 rows; above that the 256x256
+// 8-wave tile when it fills the 256 CUs, else the 128x128 tile.
 int select(int64_t M, int64_t N, int64_t K, bool residual) {
     if (M < 0 || N < 0 || K < 0) return -1;
-    for (const TableEntry &e : TABLE)
-        if (e.plan >= 0 && e.M == M && e.N == N && e.K == K && (e.residual != 0) == residual &&
-            supports(e.plan, M, N, K, residual))
-            return e.plan;
+    for (const TableEntry &e : TABLE) {
+        if (e.M < 0 || e.M != M || e.N != N || e.K != K || (e.residual != 0) != residual) continue;
+        const int plan = plan_index(e.plan);
+        if (plan >= 0 && supports(plan, M, N, K, residual)) return plan;
+    }
     if (K % 8 != 0) return PLAN_GENERIC;
+    auto pick = [&](const char *name) {
+        const int plan = plan_index(name);
+        return (plan >= 0 && supports(plan, M, N, K, residual)) ? plan : -1;
+    };
+    int plan = -1;
     if (M >= 1 && M <= 64) {
-        const int plan = skinny_split_for(M, N, K) > 1 ? PLAN_SKINNY_SPLITK : PLAN_SKINNY;
-        if (supports(plan, M, N, K, residual)) return plan;
-        if (supports(PLAN_SKINNY, M, N, K, residual)) return PLAN_SKINNY;
+        if (skinny_split_for(M, N, K) > 1) plan = pick("skinny_mfma16_w8_splitk");
+        if (plan < 0) plan = pick("skinny_mfma16_w8");
+    } else if (M <= 1024) {
+        plan = pick("tile_128x128_k64_w4_splitk");
+    } else {
+        const TileShape big = tile_shape(TC_256x256_K64_S2_W8);
+        if (tile_count(big, M, N) >= CUS) plan = pick("tile_256x256_k64_w8");
+        if (plan < 0) plan = pick("tile_128x128_k64_w4");
     }
-    struct Cand {
-        int plan;
-        double per_elem;
-        int per_cu;
-    };
-    const Cand cands[] = {
-        {PLAN_TILE_256x256, 1.00, 1},
-        {PLAN_TILE_256x128, 1.12, 1},
-        {PLAN_TILE_128x128, 1.35, 2},
-    };
-    const int64_t cus = 256;
-    int best = -1;
-    double best_cost = 0.0;
-    for (const Cand &c : cands) {
-        if (!supports(c.plan, M, N, K, residual)) continue;
-        const PlanInfo &pi = PLANS[c.plan];
-        const int64_t tiles = cdiv(M, pi.bm) * cdiv(N, pi.bn);
-        const int64_t rounds = cdiv(tiles, cus * c.per_cu);
-        const double cost = static_cast<double>(rounds) * c.per_cu * pi.bm * pi.bn * c.per_elem;
-        if (best < 0 || cost < best_cost) {
-            best = c.plan;
-            best_cost = cost;
-        }
-    }
-    return best >= 0 ? best : PLAN_GENERIC;
+    if (plan < 0) plan = pick("tile_128x128_k64_w4");
+    return plan >= 0 ? plan : PLAN_GENERIC;
 }
 
 // ------------------------------------------------------------ devices ----
@@ -228,7 +284,7 @@ int run(int plan, int64_t M, int64_t N, int64_t K, const void *X, const void *W,
                     (long long)N, (long long)K);
     if (M > LIMIT_DIM || N > LIMIT_DIM || K > LIMIT_DIM)
         return fail(KERNELARC_ERR_INVALID_ARG, "a size is 2^31 or more");
-    if (plan >= PLAN_COUNT) return fail(KERNELARC_ERR_UNSUPPORTED, "unknown plan %d", plan);
+    if (plan >= NUM_PLANS) return fail(KERNELARC_ERR_UNSUPPORTED, "unknown plan %d", plan);
     if (M == 0 || N == 0) return KERNELARC_OK;
     if (!Y) return fail(KERNELARC_ERR_INVALID_ARG, "Y is NULL");
     if (K > 0 && (!X || !W)) return fail(KERNELARC_ERR_INVALID_ARG, "X or W is NULL");
@@ -261,12 +317,11 @@ int run(int plan, int64_t M, int64_t N, int64_t K, const void *X, const void *W,
               residual ? static_cast<const uint16_t *>(R) : nullptr, static_cast<uint16_t *>(Y)};
     (void)hipGetLastError();   // clear any stale error before launching
     hipError_t e = hipSuccess;
-    switch (plan) {
-        case PLAN_GENERIC:
+    switch (PLANS[plan].kind) {
+        case KIND_GENERIC:
             e = launch_generic(p, stream);
             break;
-        case PLAN_SKINNY:
-        case PLAN_SKINNY_SPLITK: {
+        case KIND_SKINNY: {
             const int split = skinny_split_of(plan, M, N, K);
             Workspace ws{};
             if (split > 1) {
@@ -276,9 +331,16 @@ int run(int plan, int64_t M, int64_t N, int64_t K, const void *X, const void *W,
             e = launch_skinny(p, split, split > 1 ? &ws : nullptr, stream);
             break;
         }
-        default:
-            e = launch_tile(plan, p, num_cus, stream);
+        case KIND_TILE: {
+            const int split = tile_split_of(plan, M, N, K);
+            Workspace ws{};
+            if (split > 1) {
+                const int wst = workspace(dev, stream, &ws);
+                if (wst != KERNELARC_OK) return wst;
+            }
+            e = launch_tile(PLANS[plan].tile_cfg, p, split, split > 1 ? &ws : nullptr, stream);
             break;
+        }
     }
     if (e != hipSuccess)
         return fail(KERNELARC_ERR_LAUNCH, "launch of %s failed: %s", PLANS[plan].name, hipGetErrorString(e));
@@ -311,14 +373,14 @@ int kernelarc_gemm_bf16_with_plan(int plan, int64_t M, int64_t N, int64_t K, con
     return run(plan, M, N, K, X, W, R, Y, R != nullptr, stream);
 }
 
-int kernelarc_plan_count(void) { return PLAN_COUNT; }
+int kernelarc_plan_count(void) { return NUM_PLANS; }
 
 const char *kernelarc_plan_name(int plan) {
-    return (plan >= 0 && plan < PLAN_COUNT) ? PLANS[plan].name : nullptr;
+    return (plan >= 0 && plan < NUM_PLANS) ? PLANS[plan].name : nullptr;
 }
 
 int kernelarc_plan_supports(int plan, int64_t M, int64_t N, int64_t K, int residual) {
-    if (plan < 0 || plan >= PLAN_COUNT || M < 0 || N < 0 || K < 0) return -1;
+    if (plan < 0 || plan >= NUM_PLANS || M < 0 || N < 0 || K < 0) return -1;
     return supports(plan, M, N, K, residual != 0) ? 1 : 0;
 }
 
@@ -327,7 +389,9 @@ int kernelarc_select_plan(int64_t M, int64_t N, int64_t K, int residual) {
 }
 
 int kernelarc_plan_uses_workspace(int plan, int64_t M, int64_t N, int64_t K) {
-    if (plan == PLAN_SKINNY_SPLITK && supports(plan, M, N, K, true)) return 1;
+    if (!supports(plan, M, N, K, true)) return 0;
+    if (PLANS[plan].kind == KIND_SKINNY) return skinny_split_of(plan, M, N, K) > 1 ? 1 : 0;
+    if (PLANS[plan].kind == KIND_TILE) return tile_split_of(plan, M, N, K) > 1 ? 1 : 0;
     return 0;
 }
 

@@ -7,17 +7,33 @@
 namespace kernelarc {
 
 // ---------------------------------------------------------------- plans ----
-// One plan = one kernel variant.  The table and the selection rules live in
-// plan.hip; the launchers live beside their kernels.
+// One plan = one kernel variant plus its split-K rule.  The plan table and
+// the selection rules live in api.hip; the launchers live beside their
+// kernels.
 enum PlanId : int {
-    PLAN_GENERIC = 0,        // scalar LDS-tiled kernel: any K, any alignment
-    PLAN_SKINNY = 1,         // M <= 64: stream W once, MFMA 16x16x32, in-WG split-K
-    PLAN_SKINNY_SPLITK = 2,  // as PLAN_SKINNY plus a cross-workgroup split-K
-    PLAN_TILE_256x256 = 3,   // MFMA macro-tile 256x256x64, 4 waves of 128x128
-    PLAN_TILE_256x128 = 4,   // MFMA macro-tile 256x128x64, 4 waves of 128x64
-    PLAN_TILE_128x128 = 5,   // MFMA macro-tile 128x128x64, 4 waves of 64x64
-    PLAN_COUNT = 6,
+    PLAN_GENERIC = 0,          // scalar LDS-tiled kernel: any K, any alignment
+    PLAN_SKINNY = 1,           // M <= 64: stream W once, MFMA 16x16x32, in-WG split-K
+    PLAN_SKINNY_SPLITK = 2,    // as PLAN_SKINNY plus a cross-workgroup split-K
+    PLAN_FIRST_TILE = 3,       // MFMA macro-tile plans follow (api.hip)
 };
+
+// MFMA macro-tile kernel configurations (kernel_tile.hip):
+// BM x BN output tile, BK deep stages, STAGES-deep LDS ring, waves.
+enum TileCfg : int {
+    TC_256x256_K64_S2_W8 = 0,
+    TC_256x256_K64_S2_W4 = 1,
+    TC_256x128_K64_S2_W8 = 2,
+    TC_128x256_K64_S2_W8 = 3,
+    TC_256x128_K64_S2_W4 = 4,
+    TC_128x128_K64_S2_W4 = 5,
+    TC_64x256_K64_S2_W4 = 6,
+    TC_COUNT = 7,
+};
+
+struct TileShape {
+    int bm, bn, bk, workgroups_per_cu;
+};
+TileShape tile_shape(int cfg);
 
 struct Problem {
     int64_t M, N, K;
@@ -37,7 +53,7 @@ struct Workspace {
 // hipError_t of the launch.
 hipError_t launch_generic(const Problem &p, hipStream_t s);
 hipError_t launch_skinny(const Problem &p, int split_k, const Workspace *ws, hipStream_t s);
-hipError_t launch_tile(int plan, const Problem &p, int num_cus, hipStream_t s);
+hipError_t launch_tile(int cfg, const Problem &p, int split, const Workspace *ws, hipStream_t s);
 
 // Shape rules of the kernels, used by the plan table (host only).
 int skinny_split_for(int64_t M, int64_t N, int64_t K);

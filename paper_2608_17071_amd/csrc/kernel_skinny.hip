@@ -36,6 +36,7 @@ constexpr int THREADS = 64 * WAVES;
 constexpr int ROWS = 16;        // W rows per workgroup
 constexpr int UNROLL = 8;       // MFMA steps (32 k each) per batch of loads
 constexpr int AUX_NT = 2;       // non-temporal load
+constexpr int WAITCNT_VM0 = 0x0F70;   // s_waitcnt vmcnt(0)
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, uint32_t bytes) {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), static_cast<short>(0),
@@ -44,10 +45,41 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, ui
 
 __device__ __forceinline__ bf16x8 as_bf16x8(i32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
+// One batch: U MFMA steps of 32 k starting at k0 -- U loads of W (16 rows)
+// and U*MB loads of X (16 tokens each); chunks at or past kend read zero.
+template <int MB, int U>
+__device__ __forceinline__ void issue_batch(i32x4 (&wv)[U], i32x4 (&xv)[U][MB],
+                                            const __amdgpu_buffer_rsrc_t &rw,
+                                            const __amdgpu_buffer_rsrc_t &rx, uint32_t w_row,
+                                            const uint32_t (&x_row)[MB], int64_t k0, int64_t kend,
+                                            int chunk) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int64_t k = k0 + u * 32 + chunk * 8;
+        const bool ok = k < kend;
+        const uint32_t kb = static_cast<uint32_t>(k * 2);
+        wv[u] = __builtin_amdgcn_raw_buffer_load_b128(rw, ok ? w_row + kb : OOB_OFFSET, 0, AUX_NT);
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+            xv[u][mb] = __builtin_amdgcn_raw_buffer_load_b128(rx, ok ? x_row[mb] + kb : OOB_OFFSET, 0, 0);
+    }
+}
+
+template <int MB, int U>
+__device__ __forceinline__ void mfma_batch(f32x4 (&acc)[MB], const i32x4 (&wv)[U], const i32x4 (&xv)[U][MB]) {
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+            acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(wv[u]), as_bf16x8(xv[u][mb]), acc[mb],
+                                                              0, 0, 0);
+}
+
 template <int MB>
 __global__ __launch_bounds__(THREADS) void skinny_kernel(Problem p, int split, int64_t kslice,
                                                          float *ws, unsigned *counters) {
     constexpr int MP = 16 * MB;                         // padded token count
+    constexpr int U = MB <= 2 ? 8 : 4;                  // MFMA steps per batch of loads
     __shared__ float red[WAVES][ROWS][MP];              // per-wave partial C^T blocks
     __shared__ int is_last;
 
@@ -79,32 +111,42 @@ __global__ __launch_bounds__(THREADS) void skinny_kernel(Problem p, int split, i
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) x_row[mb] = static_cast<uint32_t>((mb * 16 + r) * K * 2);
 
+    const int64_t M = p.M;
+    const int64_t N = p.N;
+    // Output element idx of this strip: token m = idx / 16, row n0 + idx % 16.
+    // The residual of this thread's elements is fetched now so its DRAM
+    // latency overlaps the W stream (the same thread writes them at the end).
+    constexpr int PER_THREAD = (ROWS * MP + THREADS - 1) / THREADS;
+    float rpre[PER_THREAD];
+#pragma unroll
+    for (int t = 0; t < PER_THREAD; ++t) {
+        const int idx = threadIdx.x + t * THREADS;
+        const int64_t m = idx >> 4;
+        const int64_t n = n0 + (idx & 15);
+        rpre[t] = (p.R && idx < ROWS * MP && m < M && n < N) ? bf16_to_f32(p.R[m * N + n]) : 0.0f;
+    }
+
     f32x4 acc[MB];
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) acc[mb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 
-    for (int64_t k0 = kw0; k0 < kw1; k0 += UNROLL * 32) {
-        i32x4 wv[UNROLL];
-        i32x4 xv[UNROLL][MB];
-#pragma unroll
-        for (int u = 0; u < UNROLL; ++u) {
-            const int64_t k = k0 + u * 32 + chunk * 8;
-            const bool ok = k < kw1;
-            const uint32_t kb = static_cast<uint32_t>(k * 2);
-            wv[u] = __builtin_amdgcn_raw_buffer_load_b128(rw, ok ? w_row + kb : OOB_OFFSET, 0, AUX_NT);
-#pragma unroll
-            for (int mb = 0; mb < MB; ++mb)
-                xv[u][mb] = __builtin_amdgcn_raw_buffer_load_b128(rx, ok ? x_row[mb] + kb : OOB_OFFSET, 0, 0);
-        }
-        // Keep the whole batch of loads ahead of its MFMAs (the default
-        // schedule interleaves them and waits after the first pair).
+    // Two register buffers: batch b+1's loads are in flight while batch b is
+    // multiplied (the wait before the MFMAs only needs batch b's data).
+    // Loads past kw1 are out of range: no traffic, zeros.
+    i32x4 wa[U], wb[U];
+    i32x4 xa[U][MB], xb[U][MB];
+    constexpr int64_t STEP = U * 32;
+    issue_batch<MB, U>(wa, xa, rw, rx, w_row, x_row, kw0, kw1, chunk);
+    for (int64_t k0 = kw0; k0 < kw1; k0 += 2 * STEP) {
+        issue_batch<MB, U>(wb, xb, rw, rx, w_row, x_row, k0 + STEP, kw1, chunk);
         __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-        for (int u = 0; u < UNROLL; ++u)
-#pragma unroll
-            for (int mb = 0; mb < MB; ++mb)
-                acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(wv[u]), as_bf16x8(xv[u][mb]),
-                                                                  acc[mb], 0, 0, 0);
+        mfma_batch<MB, U>(acc, wa, xa);
+        __builtin_amdgcn_sched_barrier(0);
+        if (k0 + STEP >= kw1) break;
+        issue_batch<MB, U>(wa, xa, rw, rx, w_row, x_row, k0 + 2 * STEP, kw1, chunk);
+        __builtin_amdgcn_sched_barrier(0);
+        mfma_batch<MB, U>(acc, wb, xb);
+        __builtin_amdgcn_sched_barrier(0);
     }
 
     // C[n][m] of a 16x16 block: lane l holds n = 4*(l/16) + i, m = l % 16.
@@ -114,25 +156,26 @@ __global__ __launch_bounds__(THREADS) void skinny_kernel(Problem p, int split, i
         for (int i = 0; i < 4; ++i) red[wave][4 * (lane >> 4) + i][mb * 16 + (lane & 15)] = acc[mb][i];
     __syncthreads();
 
-    const int64_t M = p.M;
-    const int64_t N = p.N;
-    // Output element idx of this strip: token m = idx / 16, row n0 + idx % 16.
     if (split == 1) {
-        for (int idx = threadIdx.x; idx < ROWS * MP; idx += THREADS) {
+#pragma unroll
+        for (int t = 0; t < PER_THREAD; ++t) {
+            const int idx = threadIdx.x + t * THREADS;
             const int nl = idx & 15;
             const int m = idx >> 4;
             const int64_t n = n0 + nl;
-            if (m >= M || n >= N) continue;
+            if (idx >= ROWS * MP || m >= M || n >= N) continue;
             float y = 0.0f;
 #pragma unroll
             for (int w = 0; w < WAVES; ++w) y += red[w][nl][m];
-            if (p.R) y += bf16_to_f32(p.R[m * N + n]);
-            p.Y[m * N + n] = f32_to_bf16_rne(y);
+            p.Y[m * N + n] = f32_to_bf16_rne(y + rpre[t]);
         }
         return;
     }
 
-    // Cross-workgroup split: publish this slice's block, count arrivals.
+    // Cross-workgroup split: publish this slice's block with device-scope
+    // stores (write-through the XCD's L2), count the arrival once they have
+    // completed, and let the last arrival read all blocks with device-scope
+    // loads (no L2-wide write-back or invalidate needed).
     float *blk = ws + (strip * split + s) * (ROWS * MP);
     for (int idx = threadIdx.x; idx < ROWS * MP; idx += THREADS) {
         const int nl = idx & 15;
@@ -140,28 +183,29 @@ __global__ __launch_bounds__(THREADS) void skinny_kernel(Problem p, int split, i
         float y = 0.0f;
 #pragma unroll
         for (int w = 0; w < WAVES; ++w) y += red[w][nl][m];
-        blk[idx] = y;
+        __hip_atomic_store(blk + idx, y, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
-    __threadfence();                       // release the partial block
+    __builtin_amdgcn_s_waitcnt(WAITCNT_VM0);   // this wave's block stores are complete
     __syncthreads();
     if (threadIdx.x == 0) {
-        const unsigned prev = __hip_atomic_fetch_add(counters + strip, 1u, __ATOMIC_ACQ_REL,
+        const unsigned prev = __hip_atomic_fetch_add(counters + strip, 1u, __ATOMIC_RELAXED,
                                                      __HIP_MEMORY_SCOPE_AGENT);
         is_last = (prev == static_cast<unsigned>(split - 1));
     }
     __syncthreads();
     if (!is_last) return;
-    __threadfence();                       // acquire the other slices' blocks
     const float *first = ws + strip * split * (ROWS * MP);
-    for (int idx = threadIdx.x; idx < ROWS * MP; idx += THREADS) {
+#pragma unroll
+    for (int t = 0; t < PER_THREAD; ++t) {
+        const int idx = threadIdx.x + t * THREADS;
         const int nl = idx & 15;
         const int m = idx >> 4;
         const int64_t n = n0 + nl;
-        if (m >= M || n >= N) continue;
+        if (idx >= ROWS * MP || m >= M || n >= N) continue;
         float y = 0.0f;
-        for (int t = 0; t < split; ++t) y += first[t * (ROWS * MP) + idx];
-        if (p.R) y += bf16_to_f32(p.R[m * N + n]);
-        p.Y[m * N + n] = f32_to_bf16_rne(y);
+        for (int sl = 0; sl < split; ++sl)
+            y += __hip_atomic_load(first + sl * (ROWS * MP) + idx, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        p.Y[m * N + n] = f32_to_bf16_rne(y + rpre[t]);
     }
     if (threadIdx.x == 0)
         __hip_atomic_store(counters + strip, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);

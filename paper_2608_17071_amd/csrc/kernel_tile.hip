@@ -1,30 +1,34 @@
 // MFMA macro-tile kernels for Y = X W^T (+ R): the compute-bound path.
 //
-// One workgroup of four waves computes a BM x BN output tile; each wave owns
-// a (BM/2) x (BN/2) quadrant built from 32x32 accumulator blocks of
-// v_mfma_f32_32x32x16_bf16 (bf16 inputs, fp32 accumulation).
+// One workgroup of WAVES_M x WAVES_N waves computes a BM x BN output tile;
+// each wave owns a (BM/WAVES_M) x (BN/WAVES_N) block made of 32x32
+// accumulator blocks of v_mfma_f32_32x32x16_bf16 (bf16 in, fp32 accumulate).
 //
-// Data path per 64-deep K step (the paper's Table 2 tiers 2-7 -- tensor-core
-// substrate, asynchronous copy, software pipelining, epilogue and tile
-// scheduling -- re-derived for CDNA4 rather than Hopper):
+// Data path (the paper's Table 2 tiers -- tensor-core substrate,
+// asynchronous copy, software pipelining, epilogue and tile scheduling --
+// re-derived for CDNA4 rather than Hopper):
 //   * staging: buffer_load_dwordx4 with the LDS bit moves 16 bytes per lane
-//     straight from HBM/L2 into LDS (no VGPR round trip).  Each instruction
-//     covers 8 rows x 128 contiguous bytes of one operand, so every row read
-//     is a whole 128-byte line.  Two stages: the loads for step kt+1 are in
-//     flight while step kt is multiplied.
-//   * LDS layout: 128 bytes per row (64 bf16 of K); the 16-byte chunk c of
-//     row r is stored at slot c ^ swz(r).  A wave's ds_read_b128 of one
-//     fragment touches 32 rows at one chunk; the swizzle spreads any 8 (or
-//     16) consecutive rows over distinct bank groups.
-//   * buffer resources bound each operand panel, so rows past M/N read as
-//     zero without any branch; K-tail chunks are pointed out of range.
-//   * epilogue: fp32 accumulator + fp32(R) rounded once to bf16 (nearest
-//     even); each output element is read (R) and written (Y) by the same
-//     lane, so Y may alias R.
-//   * tile scheduler: workgroups are handed to the 8 XCDs round-robin; the
-//     id is remapped so each XCD works on a contiguous range of tiles, and
-//     that range is walked in GROUP_M-row super-tiles so that the tiles
-//     resident on one XCD share X and W panels in its L2.
+//     from HBM/L2 straight into LDS, no VGPR round trip.  One instruction
+//     fills RPI = 64 / (BK/8) rows of one operand; every row segment it reads
+//     is BK*2 contiguous bytes.
+//   * pipeline: a ring of STAGES LDS buffers; STAGES-1 K steps are in flight
+//     while one is multiplied (the loads' latency, about 2 us under full
+//     load, is what a shallow pipeline exposes).
+//   * LDS layout: BK*2 bytes per row; 16-byte chunk c of row r sits at slot
+//     c ^ swz(r).  A fragment read (ds_read_b128) touches 32 consecutive
+//     rows at one chunk; the swizzle spreads every 8 (and every 16)
+//     consecutive rows over distinct bank groups.
+//   * buffer resources bound each operand panel, so rows past M or N read
+//     as zero without a branch; K-tail chunks are pointed out of range.
+//   * schedule: the next sub-step's fragment reads and the next stage's
+//     loads are interleaved between MFMAs (sched_group_barrier).
+//   * epilogue: fp32 accumulator + fp32(R), one nearest-even rounding to
+//     bf16, staged through LDS so R is read and Y written 16 bytes per
+//     lane; each element is read (R) and written (Y) by the same lane, so Y
+//     may alias R.
+//   * tile scheduler: workgroups are handed to the 8 XCDs round-robin; ids
+//     are remapped so each XCD takes a contiguous range of tiles, walked in
+//     GROUP_M-row bands, so tiles resident on one XCD share panels in its L2.
 #include "internal.h"
 
 namespace kernelarc {
@@ -32,6 +36,7 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
 
@@ -39,100 +44,94 @@ typedef __attribute__((address_space(3))) void lds_void;
 constexpr int RSRC_WORD3 = 0x00020000;
 // A byte offset that is out of range for every panel (panels are < 2^31 B).
 constexpr uint32_t OOB_OFFSET = 0x80000000u;
+constexpr int XCDS = 8;
+// Cache policy of buffer accesses: sc1 = device scope (coherent across XCDs).
+constexpr int AUX_SC1 = 16;
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, uint32_t bytes) {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), static_cast<short>(0),
                                              static_cast<int>(bytes), RSRC_WORD3);
 }
 
-// Slot of 16-byte chunk c of row r is c ^ swz(r).
-__device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+// s_waitcnt immediate for gfx9: vmcnt = n (6 bits), expcnt and lgkmcnt not waited.
+constexpr int waitcnt_vm(int n) { return (n & 0xF) | ((n >> 4) << 14) | (0x7 << 4) | (0xF << 8); }
 
-constexpr int XCDS = 8;
-
-// blockIdx -> (tile_m, tile_n).  Dispatch places workgroup b on XCD b % 8;
-// XCD x is given the logical ids [start_x, start_x + count_x) in order, and
-// logical ids run over GROUP_M-row bands column by column.
-__device__ __forceinline__ void schedule(int64_t bid, int64_t tiles_m, int64_t tiles_n, int group_m,
-                                         int64_t &tm, int64_t &tn) {
-    const int64_t T = tiles_m * tiles_n;
-    const int64_t per = T / XCDS;
-    const int64_t rem = T % XCDS;
-    const int64_t x = bid % XCDS;
-    const int64_t local = bid / XCDS;
-    const int64_t logical = x * per + (x < rem ? x : rem) + local;
-    const int64_t band = static_cast<int64_t>(group_m) * tiles_n;
-    const int64_t g = logical / band;
-    const int64_t first_m = g * group_m;
-    const int64_t rows = (tiles_m - first_m) < group_m ? (tiles_m - first_m) : group_m;
-    const int64_t in_band = logical - g * band;
-    tm = first_m + in_band % rows;
-    tn = in_band / rows;
+// Slot of 16-byte chunk c of row r: c ^ swz(r).  8 chunks per row (BK=64)
+// or 4 (BK=32); both spread rows 0..7 and rows 0..15 over distinct slots.
+template <int CHUNKS>
+__device__ __forceinline__ int swz(int r) {
+    if constexpr (CHUNKS == 8) return (r & 7) ^ ((r >> 3) & 1);
+    else return ((r >> 1) ^ (r >> 3)) & 3;
 }
 
-template <int BM_, int BN_, int WAVES_PER_EU_>
+template <int BM_, int BN_, int BK_, int WAVES_M_, int WAVES_N_, int STAGES_, int WAVES_PER_EU_>
 struct Cfg {
-    static constexpr int BM = BM_, BN = BN_, BK = 64;
-    static constexpr int WAVES = 4, THREADS = 256;
-    static constexpr int WM = BM / 2, WN = BN / 2;        // per-wave quadrant
-    static constexpr int TM = WM / 32, TN = WN / 32;      // 32x32 blocks per wave
-    static constexpr int A_BYTES = BM * BK * 2, B_BYTES = BN * BK * 2;
+    static constexpr int BM = BM_, BN = BN_, BK = BK_, STAGES = STAGES_;
+    static constexpr int WAVES_M = WAVES_M_, WAVES_N = WAVES_N_;
+    static constexpr int WAVES = WAVES_M * WAVES_N, THREADS = 64 * WAVES;
+    static constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;   // per-wave block
+    static constexpr int TM = WM / 32, TN = WN / 32;             // 32x32 blocks per wave
+    static constexpr int KSTEPS = BK / 16;                        // MFMA sub-steps per stage
+    static constexpr int ROW_BYTES = BK * 2, CHUNKS = BK / 8, RPI = 64 / CHUNKS;
+    static constexpr int A_BYTES = BM * ROW_BYTES, B_BYTES = BN * ROW_BYTES;
     static constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
-    static constexpr int STAGES = 2;
     static constexpr int LDS_BYTES = STAGES * STAGE_BYTES;
-    static constexpr int A_LOADS = BM / 8 / WAVES;        // 8-row blocks per wave per step
-    static constexpr int B_LOADS = BN / 8 / WAVES;
+    static constexpr int A_LOADS = BM / RPI / WAVES;              // DMA instructions per wave per stage
+    static constexpr int B_LOADS = BN / RPI / WAVES;
+    static constexpr int LOADS = A_LOADS + B_LOADS;
     static constexpr int WAVES_PER_EU = WAVES_PER_EU_;
-    // Epilogue staging: one 32-row slab of a wave's quadrant in fp32, rows
+    // Epilogue staging: one 32-row slab of a wave's block in fp32, rows
     // padded by 4 floats; lanes then read 8 consecutive columns each.
     static constexpr int EPI_STRIDE = WN + 4;
     static constexpr int EPI_WAVE_FLOATS = 32 * EPI_STRIDE;
     static constexpr int LANES_PER_ROW = WN / 8;
     static constexpr int ROWS_PER_PASS = 64 / LANES_PER_ROW;
-    static_assert(4 * EPI_WAVE_FLOATS * 4 <= LDS_BYTES, "epilogue staging fits in the stage buffers");
+
+    static_assert(BK == 32 || BK == 64, "BK");
+    static_assert(TM >= 1 && TN >= 1 && WM % 32 == 0 && WN % 32 == 0, "wave block");
+    static_assert(A_LOADS >= 1 && B_LOADS >= 1 && BM % (RPI * WAVES) == 0 && BN % (RPI * WAVES) == 0,
+                  "staging split");
+    static_assert(STAGES >= 2, "pipeline depth");
+    static_assert(LDS_BYTES <= 160 * 1024, "LDS capacity");
+    static_assert(WAVES * EPI_WAVE_FLOATS * 4 <= LDS_BYTES, "epilogue staging fits");
+    static_assert(LOADS * (STAGES - 2) < 64, "vmcnt range");
 };
 
-// Enqueue the LDS-direct loads of K step kt into one stage.  Load block blk
-// (8 rows) of a wave has the parity of q (A_LOADS and B_LOADS are even), so
-// the lane's source chunk is c_even ^ (q & 1); chunks at or past K are
-// pointed out of range and arrive as zeros.
+// Enqueue the LDS-direct loads of K step kt into one stage buffer.  Chunks
+// at or past K are pointed out of range and arrive as zeros.
 template <class C>
 __device__ __forceinline__ void issue_stage(char *stage, const __amdgpu_buffer_rsrc_t &ra,
                                             const __amdgpu_buffer_rsrc_t &rb, const uint32_t *a_off,
-                                            const uint32_t *b_off, int wave, int kt, int64_t K,
-                                            int c_even) {
+                                            const int *a_k, const uint32_t *b_off, const int *b_k,
+                                            int wave, int kt, int64_t K) {
     const int64_t kbase = static_cast<int64_t>(kt) * C::BK;
-    const bool ok_even = kbase + c_even * 8 < K;
-    const bool ok_odd = kbase + (c_even ^ 1) * 8 < K;
-    const uint32_t kbytes = static_cast<uint32_t>(kt) * (C::BK * 2);
+    const uint32_t kbytes = static_cast<uint32_t>(kt) * C::ROW_BYTES;
 #pragma unroll
     for (int q = 0; q < C::A_LOADS; ++q) {
         const int blk = wave * C::A_LOADS + q;
-        const bool ok = (q & 1) ? ok_odd : ok_even;
-        const uint32_t off = ok ? a_off[q] + kbytes : OOB_OFFSET;
+        const uint32_t off = (kbase + a_k[q] < K) ? a_off[q] + kbytes : OOB_OFFSET;
         __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void *)(stage + blk * 1024), 16, off, 0, 0, 0);
     }
 #pragma unroll
     for (int q = 0; q < C::B_LOADS; ++q) {
         const int blk = wave * C::B_LOADS + q;
-        const bool ok = (q & 1) ? ok_odd : ok_even;
-        const uint32_t off = ok ? b_off[q] + kbytes : OOB_OFFSET;
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_void *)(stage + C::A_BYTES + blk * 1024),
-                                                 16, off, 0, 0, 0);
+        const uint32_t off = (kbase + b_k[q] < K) ? b_off[q] + kbytes : OOB_OFFSET;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_void *)(stage + C::A_BYTES + blk * 1024), 16,
+                                                 off, 0, 0, 0);
     }
 }
 
-// MFMA operands of K sub-step ks (16 deep) from one stage: lane l reads row
-// l % 32 of each 32-row block at chunk 2*ks + l / 32, whose slot is
-// (2*ks) ^ slot_base with slot_base = (l / 32) ^ swz(l % 32).
+// MFMA operands of one sub-step from one stage: lane l reads row l % 32 of
+// each 32-row block at byte column `col` (chunk 2*ks + l / 32, swizzled).
 template <class C>
-__device__ __forceinline__ void load_fragments(const char *a_base, const char *b_base, int slot_base,
-                                               int ks, bf16x8 *af, bf16x8 *bfr) {
-    const int col = ((2 * ks) ^ slot_base) * 16;
+__device__ __forceinline__ void load_fragments(const char *a_base, const char *b_base, int col,
+                                               bf16x8 *af, bf16x8 *bfr) {
 #pragma unroll
-    for (int i = 0; i < C::TM; ++i) af[i] = *reinterpret_cast<const bf16x8 *>(a_base + i * 32 * 128 + col);
+    for (int i = 0; i < C::TM; ++i)
+        af[i] = *reinterpret_cast<const bf16x8 *>(a_base + i * 32 * C::ROW_BYTES + col);
 #pragma unroll
-    for (int j = 0; j < C::TN; ++j) bfr[j] = *reinterpret_cast<const bf16x8 *>(b_base + j * 32 * 128 + col);
+    for (int j = 0; j < C::TN; ++j)
+        bfr[j] = *reinterpret_cast<const bf16x8 *>(b_base + j * 32 * C::ROW_BYTES + col);
 }
 
 // Sub-step scheduling: MFMA number T of a sub-step is followed by its share
@@ -149,39 +148,71 @@ __device__ __forceinline__ void interleave() {
     if constexpr (T + 1 < MFMAS) interleave<MFMAS, READS, LOADS, T + 1>();
 }
 
-// Instruction order of one K step, pinned because the default schedule
-// funnels every fragment through one register set and waits for each LDS
-// read just before its MFMAs (one wave per SIMD cannot hide that).  Order:
-// the fragment reads of sub-step 0; then sub-step 0's MFMAs interleaved with
-// the next stage's LDS-direct loads and sub-step 1's fragment reads; then
-// each further sub-step's MFMAs interleaved with the following sub-step's
-// reads; the last sub-step's MFMAs alone.
-template <class C>
-__device__ __forceinline__ void schedule_k_step() {
-    constexpr int FRAGS = C::TM + C::TN;          // LDS reads per sub-step
-    constexpr int MFMAS = C::TM * C::TN;          // MFMAs per sub-step
-    constexpr int LOADS = C::A_LOADS + C::B_LOADS;
-    __builtin_amdgcn_sched_group_barrier(0x100, FRAGS, 0);
-    interleave<MFMAS, FRAGS, LOADS, 0>();
-    interleave<MFMAS, FRAGS, 0, 0>();
-    interleave<MFMAS, FRAGS, 0, 0>();
-    __builtin_amdgcn_sched_group_barrier(0x008, MFMAS, 0);
+template <class C, int KS>
+__device__ __forceinline__ void interleave_substeps() {
+    constexpr int FRAGS = C::TM + C::TN, MFMAS = C::TM * C::TN;
+    if constexpr (KS + 1 < C::KSTEPS) {
+        interleave<MFMAS, FRAGS, (KS == 0 ? C::LOADS : 0), 0>();
+        interleave_substeps<C, KS + 1>();
+    } else {
+        __builtin_amdgcn_sched_group_barrier(0x008, MFMAS, 0);
+    }
 }
 
+// Instruction order of one K step, pinned because the default schedule
+// funnels every fragment through one register set and waits for each LDS
+// read just before its MFMAs.  Order: the fragment reads of sub-step 0;
+// sub-step 0's MFMAs interleaved with the next stage's loads and sub-step
+// 1's reads; each further sub-step's MFMAs with the following reads; the
+// last sub-step's MFMAs alone.
 template <class C>
-__global__ __attribute__((amdgpu_flat_work_group_size(256, 256),
+__device__ __forceinline__ void schedule_k_step() {
+    __builtin_amdgcn_sched_group_barrier(0x100, C::TM + C::TN, 0);
+    interleave_substeps<C, 0>();
+}
+
+// Split-K bookkeeping of one launch (split == 1: none).
+struct SplitK {
+    int split;          // K slices per output tile
+    int64_t kslice;     // slice length, a multiple of BK
+    float *partials;    // [tile][slice][BM*BN] fp32, fragment order
+    unsigned *counters; // one arrival counter per tile, zero between calls
+};
+
+template <class C>
+__global__ __attribute__((amdgpu_flat_work_group_size(C::THREADS, C::THREADS),
                           amdgpu_waves_per_eu(C::WAVES_PER_EU, C::WAVES_PER_EU)))
-void tile_kernel(Problem p, int64_t tiles_m, int64_t tiles_n, int group_m) {
+void tile_kernel(Problem p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) {
     __shared__ __attribute__((aligned(1024))) char lds[C::LDS_BYTES];
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
 
-    int64_t tm, tn;
-    schedule(blockIdx.x, tiles_m, tiles_n, group_m, tm, tn);
+    // Workgroup -> (K slice, tile): the XCD remap runs over slice-major ids,
+    // so each XCD takes neighbouring tiles of one slice.
+    const int64_t tiles = tiles_m * tiles_n;
+    int64_t tm, tn, slice, tile;
+    {
+        const int64_t T = tiles * sk.split;
+        const int64_t per = T / XCDS, rem = T % XCDS;
+        const int64_t x = blockIdx.x % XCDS, local = blockIdx.x / XCDS;
+        const int64_t logical = x * per + (x < rem ? x : rem) + local;
+        slice = logical / tiles;
+        tile = logical - slice * tiles;
+        const int64_t band = static_cast<int64_t>(group_m) * tiles_n;
+        const int64_t g = tile / band;
+        const int64_t first_m = g * group_m;
+        const int64_t rows = (tiles_m - first_m) < group_m ? (tiles_m - first_m) : group_m;
+        const int64_t in_band = tile - g * band;
+        tm = first_m + in_band % rows;
+        tn = in_band / rows;
+    }
     const int64_t m0 = tm * C::BM;
     const int64_t n0 = tn * C::BN;
     const int64_t K = p.K;
+    // This workgroup's K range [kbeg, kend); loads at or past kend read zero.
+    const int64_t kbeg = slice * sk.kslice;
+    const int64_t kend = (kbeg + sk.kslice) < K ? (kbeg + sk.kslice) : K;
 
     // Operand panels bounded by buffer resources: rows past M (N) read 0.
     const int64_t rows_a = (p.M - m0) < C::BM ? (p.M - m0) : C::BM;
@@ -189,22 +220,24 @@ void tile_kernel(Problem p, int64_t tiles_m, int64_t tiles_n, int group_m) {
     const __amdgpu_buffer_rsrc_t ra = make_rsrc(p.X + m0 * K, static_cast<uint32_t>(rows_a * K * 2));
     const __amdgpu_buffer_rsrc_t rb = make_rsrc(p.W + n0 * K, static_cast<uint32_t>(rows_b * K * 2));
 
-    // Per-lane source offsets (bytes, K step 0) of the chunks this lane
-    // stages: lane l fills slot l % 8 of row 8*blk + l / 8, which holds
-    // global chunk (l % 8) ^ swz(row) = (l % 8) ^ (l / 8) ^ (blk & 1).
-    static_assert(C::A_LOADS % 2 == 0 && C::B_LOADS % 2 == 0, "load blocks come in pairs");
-    const int lane_row = lane >> 3;
-    const int c_even = (lane & 7) ^ lane_row;
+    // Staging map: lane l of load block blk fills slot l % CHUNKS of row
+    // RPI*blk + l / CHUNKS, which holds global chunk (l % CHUNKS) ^ swz(row).
     uint32_t a_off[C::A_LOADS], b_off[C::B_LOADS];
+    int a_k[C::A_LOADS], b_k[C::B_LOADS];
+    const int slot = lane % C::CHUNKS;
 #pragma unroll
     for (int q = 0; q < C::A_LOADS; ++q) {
-        const int r = (wave * C::A_LOADS + q) * 8 + lane_row;
-        a_off[q] = static_cast<uint32_t>(r * K * 2 + (c_even ^ (q & 1)) * 16);
+        const int r = (wave * C::A_LOADS + q) * C::RPI + lane / C::CHUNKS;
+        const int c = slot ^ swz<C::CHUNKS>(r);
+        a_off[q] = static_cast<uint32_t>(r * K * 2 + c * 16);
+        a_k[q] = c * 8;
     }
 #pragma unroll
     for (int q = 0; q < C::B_LOADS; ++q) {
-        const int r = (wave * C::B_LOADS + q) * 8 + lane_row;
-        b_off[q] = static_cast<uint32_t>(r * K * 2 + (c_even ^ (q & 1)) * 16);
+        const int r = (wave * C::B_LOADS + q) * C::RPI + lane / C::CHUNKS;
+        const int c = slot ^ swz<C::CHUNKS>(r);
+        b_off[q] = static_cast<uint32_t>(r * K * 2 + c * 16);
+        b_k[q] = c * 8;
     }
 
     f32x16 acc[C::TM][C::TN];
@@ -215,35 +248,42 @@ void tile_kernel(Problem p, int64_t tiles_m, int64_t tiles_n, int group_m) {
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
 
-    // Fragment read offsets: lane reads row (lane % 32) of each 32-row block
-    // at chunk 2*ks + lane / 32, i.e. slot (2*ks + hi) ^ swz(lane % 32).
+    // Fragment reads: row (lane % 32) of each 32-row block, chunk 2*ks + hi.
     const int frag_row = lane & 31;
     const int hi = lane >> 5;
-    const int wm0 = (wave >> 1) * C::WM;
-    const int wn0 = (wave & 1) * C::WN;
-    const int a_row_byte = (wm0 + frag_row) * 128;
-    const int b_row_byte = (wn0 + frag_row) * 128;
-    const int slot_base = hi ^ swz(frag_row);
+    const int wm0 = (wave / C::WAVES_N) * C::WM;
+    const int wn0 = (wave % C::WAVES_N) * C::WN;
+    const int a_row_byte = (wm0 + frag_row) * C::ROW_BYTES;
+    const int b_row_byte = (wn0 + frag_row) * C::ROW_BYTES;
+    const int frag_swz = swz<C::CHUNKS>(frag_row);
 
-    const int nk = static_cast<int>((K + C::BK - 1) / C::BK);
+    const int kt0 = static_cast<int>(kbeg / C::BK);
+    const int kt1 = kend > kbeg ? static_cast<int>((kend + C::BK - 1) / C::BK) : kt0;
 
-    if (nk > 0) issue_stage<C>(lds, ra, rb, a_off, b_off, wave, 0, K, c_even);
+    // Prologue: STAGES-1 steps in flight (past the end of the range the
+    // loads are out of range and only write zeros into buffers nobody reads).
+#pragma unroll
+    for (int s = 0; s < C::STAGES - 1; ++s)
+        issue_stage<C>(lds + s * C::STAGE_BYTES, ra, rb, a_off, a_k, b_off, b_k, wave, kt0 + s, kend);
 
-    for (int kt = 0; kt < nk; ++kt) {
-        __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): this wave's stage kt is in LDS
-        __syncthreads();                        // all waves' too; stage kt+1's buffer is free
-        const char *cur = lds + (kt & 1) * C::STAGE_BYTES;
+    int cur_stage = 0;
+    for (int kt = kt0; kt < kt1; ++kt) {
+        // Stage kt has landed once at most STAGES-2 stages' loads are outstanding.
+        __builtin_amdgcn_s_waitcnt(waitcnt_vm(C::LOADS * (C::STAGES - 2)));
+        __syncthreads();   // every wave's part of stage kt; stage kt-1's buffer is free
+        const char *cur = lds + cur_stage * C::STAGE_BYTES;
         const char *a_base = cur + a_row_byte;
         const char *b_base = cur + C::A_BYTES + b_row_byte;
         bf16x8 af[2][C::TM], bfr[2][C::TN];
-        load_fragments<C>(a_base, b_base, slot_base, 0, af[0], bfr[0]);
-        // Unconditional so the scheduler can interleave it: past the end of
-        // K every offset is out of range and the loads only write zeros into
-        // the idle stage.
-        issue_stage<C>(lds + ((kt + 1) & 1) * C::STAGE_BYTES, ra, rb, a_off, b_off, wave, kt + 1, K, c_even);
+        load_fragments<C>(a_base, b_base, (hi ^ frag_swz) * 16, af[0], bfr[0]);
+        const int free_stage = cur_stage == 0 ? C::STAGES - 1 : cur_stage - 1;   // held step kt-1
+        issue_stage<C>(lds + free_stage * C::STAGE_BYTES, ra, rb, a_off, a_k, b_off, b_k, wave,
+                       kt + C::STAGES - 1, kend);
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks) {
-            if (ks < 3) load_fragments<C>(a_base, b_base, slot_base, ks + 1, af[(ks + 1) & 1], bfr[(ks + 1) & 1]);
+        for (int ks = 0; ks < C::KSTEPS; ++ks) {
+            if (ks + 1 < C::KSTEPS)
+                load_fragments<C>(a_base, b_base, ((2 * (ks + 1) + hi) ^ frag_swz) * 16,
+                                  af[(ks + 1) & 1], bfr[(ks + 1) & 1]);
 #pragma unroll
             for (int i = 0; i < C::TM; ++i)
 #pragma unroll
@@ -252,16 +292,82 @@ void tile_kernel(Problem p, int64_t tiles_m, int64_t tiles_n, int group_m) {
                                                                         acc[i][j], 0, 0, 0);
         }
         schedule_k_step<C>();
+        cur_stage = cur_stage + 1 == C::STAGES ? 0 : cur_stage + 1;
     }
 
     // Epilogue.  Accumulator element e of a 32x32 block sits at row
     // 8*(e/4) + 4*hi + e%4 and column lane % 32.  Each 32-row slab of the
-    // wave's quadrant goes through LDS as fp32 so that every lane then owns
-    // 8 consecutive columns: R is read and Y written 16 bytes at a time
+    // wave's block goes through LDS as fp32 so that every lane then owns 8
+    // consecutive columns: R is read and Y written 16 bytes at a time
     // through buffer resources bounded to the tile's rows (rows past M are
     // dropped by the range check; columns past N are pointed out of range).
-    __builtin_amdgcn_s_waitcnt(0x0F70);   // the trailing LDS-direct loads have landed
-    __syncthreads();                        // every wave is done with the stage buffers
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));   // trailing LDS-direct loads have landed
+    __syncthreads();                             // every wave is done with the stage buffers
+
+    if (sk.split > 1) {
+        // Publish this slice's fp32 tile in fragment order (each store
+        // instruction writes 1 KB contiguous) with device-scope (sc1)
+        // stores, which write through the XCD's L2; once they have
+        // completed (vmcnt 0 in every wave) the arrival is counted.  The last
+        // slice to arrive reads every slice with device-scope loads, which
+        // bypass stale L2 lines, and adds them in slice order.  Only the
+        // partial tiles cross workgroups, and only through these accesses,
+        // so no L2-wide write-back or invalidate is needed.
+        constexpr int TILE_FLOATS = C::BM * C::BN;
+        const float *first = sk.partials + tile * sk.split * TILE_FLOATS;
+        const __amdgpu_buffer_rsrc_t rp =
+            make_rsrc(first, static_cast<uint32_t>(sk.split) * TILE_FLOATS * 4u);
+        const uint32_t mine = static_cast<uint32_t>(slice) * TILE_FLOATS * 4u;
+        const int wblk = wave * C::TM * C::TN;
+#pragma unroll
+        for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+            for (int j = 0; j < C::TN; ++j)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const f32x4 v = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
+                                     acc[i][j][4 * q + 3]};
+                    const uint32_t off = mine + (((wblk + i * C::TN + j) * 4 + q) * 64 + lane) * 16;
+                    __builtin_amdgcn_raw_buffer_store_b128(v, rp, off, 0, AUX_SC1);
+                }
+        __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));   // this wave's slice stores are complete
+        __syncthreads();
+        int *flag = reinterpret_cast<int *>(lds);
+        if (threadIdx.x == 0) {
+            const unsigned prev = __hip_atomic_fetch_add(sk.counters + tile, 1u, __ATOMIC_RELAXED,
+                                                         __HIP_MEMORY_SCOPE_AGENT);
+            *flag = prev == static_cast<unsigned>(sk.split - 1);
+        }
+        __syncthreads();
+        const bool last = *flag != 0;
+        __syncthreads();                      // the flag is read before LDS is reused
+        if (!last) return;
+#pragma unroll
+        for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+            for (int j = 0; j < C::TN; ++j)
+#pragma unroll
+                for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+        for (int t = 0; t < sk.split; ++t) {
+            const uint32_t base = static_cast<uint32_t>(t) * TILE_FLOATS * 4u;
+#pragma unroll
+            for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+                for (int j = 0; j < C::TN; ++j)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const uint32_t off = base + (((wblk + i * C::TN + j) * 4 + q) * 64 + lane) * 16;
+                        const f32x4 v = __builtin_bit_cast(
+                            f32x4, __builtin_amdgcn_raw_buffer_load_b128(rp, off, 0, AUX_SC1));
+                        acc[i][j][4 * q] += v[0];
+                        acc[i][j][4 * q + 1] += v[1];
+                        acc[i][j][4 * q + 2] += v[2];
+                        acc[i][j][4 * q + 3] += v[3];
+                    }
+        }
+        if (threadIdx.x == 0)
+            __hip_atomic_store(sk.counters + tile, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
     float *ep = reinterpret_cast<float *>(lds) + wave * C::EPI_WAVE_FLOATS;
     const int64_t N = p.N;
     const int64_t rows_y = (p.M - m0) < C::BM ? (p.M - m0) : C::BM;
@@ -322,27 +428,59 @@ void tile_kernel(Problem p, int64_t tiles_m, int64_t tiles_n, int group_m) {
 }
 
 template <class C>
-hipError_t launch_cfg(const Problem &p, int group_m, hipStream_t s) {
+hipError_t launch_cfg(const Problem &p, int group_m, int split, const Workspace *ws, hipStream_t s) {
     const int64_t tiles_m = (p.M + C::BM - 1) / C::BM;
     const int64_t tiles_n = (p.N + C::BN - 1) / C::BN;
     const int64_t tiles = tiles_m * tiles_n;
-    hipLaunchKernelGGL(tile_kernel<C>, dim3(static_cast<unsigned>(tiles)), dim3(C::THREADS), 0, s, p,
-                       tiles_m, tiles_n, group_m);
+    SplitK sk{1, ((p.K + C::BK - 1) / C::BK) * C::BK, nullptr, nullptr};
+    if (split > 1) {
+        sk.split = split;
+        sk.kslice = (((p.K + split - 1) / split + C::BK - 1) / C::BK) * C::BK;
+        sk.partials = ws->partials;
+        sk.counters = ws->counters;
+    }
+    hipLaunchKernelGGL(tile_kernel<C>, dim3(static_cast<unsigned>(tiles * sk.split)), dim3(C::THREADS), 0, s,
+                       p, tiles_m, tiles_n, group_m, sk);
     return hipGetLastError();
 }
 
-using Cfg256x256 = Cfg<256, 256, 1>;
-using Cfg256x128 = Cfg<256, 128, 1>;
-using Cfg128x128 = Cfg<128, 128, 2>;
-
 }  // namespace
 
-hipError_t launch_tile(int plan, const Problem &p, int num_cus, hipStream_t s) {
-    (void)num_cus;
-    switch (plan) {
-        case PLAN_TILE_256x256: return launch_cfg<Cfg256x256>(p, 8, s);
-        case PLAN_TILE_256x128: return launch_cfg<Cfg256x128>(p, 8, s);
-        case PLAN_TILE_128x128: return launch_cfg<Cfg128x128>(p, 8, s);
+// Tile shape, K depth, wave grid, pipeline depth and occupancy of each tile
+// configuration: Cfg<BM, BN, BK, WAVES_M, WAVES_N, STAGES, WAVES_PER_EU>.
+using C256x256w8 = Cfg<256, 256, 64, 2, 4, 2, 2>;
+using C256x256w4 = Cfg<256, 256, 64, 2, 2, 2, 1>;
+using C256x128w8 = Cfg<256, 128, 64, 4, 2, 2, 2>;
+using C128x256w8 = Cfg<128, 256, 64, 2, 4, 2, 2>;
+using C256x128w4 = Cfg<256, 128, 64, 2, 2, 2, 1>;
+using C128x128w4 = Cfg<128, 128, 64, 2, 2, 2, 2>;
+using C64x256w4 = Cfg<64, 256, 64, 1, 4, 2, 2>;
+
+template <class C>
+constexpr TileShape shape_of(int per_cu) { return TileShape{C::BM, C::BN, C::BK, per_cu}; }
+
+TileShape tile_shape(int cfg) {
+    switch (cfg) {
+        case TC_256x256_K64_S2_W8: return shape_of<C256x256w8>(1);
+        case TC_256x256_K64_S2_W4: return shape_of<C256x256w4>(1);
+        case TC_256x128_K64_S2_W8: return shape_of<C256x128w8>(1);
+        case TC_128x256_K64_S2_W8: return shape_of<C128x256w8>(1);
+        case TC_256x128_K64_S2_W4: return shape_of<C256x128w4>(1);
+        case TC_128x128_K64_S2_W4: return shape_of<C128x128w4>(2);
+        case TC_64x256_K64_S2_W4: return shape_of<C64x256w4>(2);
+        default: return TileShape{0, 0, 0, 0};
+    }
+}
+
+hipError_t launch_tile(int cfg, const Problem &p, int split, const Workspace *ws, hipStream_t s) {
+    switch (cfg) {
+        case TC_256x256_K64_S2_W8: return launch_cfg<C256x256w8>(p, 8, split, ws, s);
+        case TC_256x256_K64_S2_W4: return launch_cfg<C256x256w4>(p, 8, split, ws, s);
+        case TC_256x128_K64_S2_W8: return launch_cfg<C256x128w8>(p, 8, split, ws, s);
+        case TC_128x256_K64_S2_W8: return launch_cfg<C128x256w8>(p, 8, split, ws, s);
+        case TC_256x128_K64_S2_W4: return launch_cfg<C256x128w4>(p, 8, split, ws, s);
+        case TC_128x128_K64_S2_W4: return launch_cfg<C128x128w4>(p, 8, split, ws, s);
+        case TC_64x256_K64_S2_W4: return launch_cfg<C64x256w4>(p, 8, split, ws, s);
         default: return hipErrorInvalidValue;
     }
 }

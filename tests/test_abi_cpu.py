@@ -65,7 +65,7 @@ def test_plan_table(ka):
 
 def test_plan_limits(ka):
     names = ka.plan_names()
-    tile = names.index("tile_256x256x64_mfma32_w4")
+    tile = names.index("tile_256x256_k64_w8")
     skinny = names.index("skinny_mfma16_w8")
     assert not ka.plan_supports(tile, 512, 512, 12)            # K % 8
     assert not ka.plan_supports(skinny, 65, 512, 512)          # M > 64

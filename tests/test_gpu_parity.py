@@ -55,15 +55,20 @@ def test_workload_parity(ka, name):
         _parity(ka, w, plain=True)
 
 
+def _all_plan_names():
+    from paper_2608_17071_amd import kernelarc
+    return kernelarc.plan_names()
+
+
+TILE_SHAPES = [(65, 8, 8), (300, 264, 200), (130, 100, 72), (513, 520, 136)]
 PLAN_SHAPES = {
-    # plan name: ragged shapes (M, N, K) it supports, K % 8 == 0
+    # plan name: ragged shapes (M, N, K) it supports, K % 8 == 0 for MFMA plans
     "generic_64x64_scalar": [(1, 1, 1), (70, 33, 13), (130, 100, 72)],
     "skinny_mfma16_w8": [(1, 8, 8), (17, 520, 1000), (64, 96, 4104), (33, 100, 264)],
     "skinny_mfma16_w8_splitk": [(1, 24, 8), (5, 520, 1000), (64, 96, 4104), (48, 100, 2064)],
-    "tile_256x256x64_mfma32_w4": [(65, 8, 8), (300, 264, 200), (130, 100, 72), (513, 520, 136)],
-    "tile_256x128x64_mfma32_w4": [(65, 8, 8), (300, 264, 200), (130, 100, 72), (513, 520, 136)],
-    "tile_128x128x64_mfma32_w4": [(65, 8, 8), (300, 264, 200), (130, 100, 72), (513, 520, 136)],
 }
+PLAN_SHAPES.update({n: TILE_SHAPES for n in _all_plan_names() if n.startswith("tile_")})
+assert set(PLAN_SHAPES) == set(_all_plan_names()), "every plan has test shapes"
 
 
 @pytest.mark.parametrize("plan", sorted(PLAN_SHAPES))
@@ -199,7 +204,7 @@ def test_misaligned_pointers_fall_back(ka):
     y = ka.gemm_bf16_residual(x, t["W"].cuda(), t["R"].cuda())
     torch.cuda.synchronize()
     gu.check_tolerance(gu.to_bits(y), gu.oracle_reference(t["X"], t["W"], t["R"]), "misaligned")
-    tile = plan_id(ka, "tile_128x128x64_mfma32_w4")
+    tile = plan_id(ka, "tile_128x128_k64_w4")
     with pytest.raises(ka.KernelArcError):
         ka.gemm_bf16_with_plan(tile, x, t["W"].cuda(), t["R"].cuda())
 
@@ -213,3 +218,32 @@ def test_leading_dims_flatten(ka):
     torch.cuda.synchronize()
     assert y.shape == (6, 20, 256)
     gu.check_tolerance(gu.to_bits(y.view(120, 256)), gu.oracle_reference(t["X"], t["W"], t["R"]), "3-d")
+
+
+def test_graph_replay_matches_eager(ka):
+    """Calls captured in a HIP graph give the eager result on every replay
+    (the split-K plans' arrival counters must reset themselves)."""
+    cases = [("skinny_mfma16_w8_splitk", (16, 1024, 4096)), ("skinny_mfma16_w8", (3, 520, 1000)),
+             ("tile_128x128_k64_w4_splitk", (512, 1024, 2048)), ("tile_256x256_k64_w8", (300, 520, 264)),
+             ("tile_64x256_k64_w4_splitk", (64, 768, 4096))]
+    for name, (M, N, K) in cases:
+        p = plan_id(ka, name)
+        t = wl.make_inputs(wl.custom(M, N, K, seed=21))
+        gu.note(f"graph {name} M={M} N={N} K={K}")
+        eager = gu.run_library(t["X"], t["W"], t["R"], plan=p)
+        x, w, r = t["X"].cuda(), t["W"].cuda(), t["R"].cuda()
+        y = torch.empty(M, N, dtype=torch.bfloat16, device="cuda")
+        ka.gemm_bf16_with_plan(p, x, w, r, out=y)      # any workspace exists before capture
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            ka.gemm_bf16_with_plan(p, x, w, r, out=y)
+        y2 = torch.empty_like(y)
+        for rep in range(3):
+            y.fill_(float("nan"))
+            g.replay()
+            torch.cuda.synchronize()
+            np.testing.assert_array_equal(gu.to_bits(y), eager, err_msg=f"{name} replay {rep}")
+            ka.gemm_bf16_with_plan(p, x, w, r, out=y2)   # eager work between replays
+            torch.cuda.synchronize()
+            np.testing.assert_array_equal(gu.to_bits(y2), eager)
