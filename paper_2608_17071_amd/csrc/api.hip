@@ -41,7 +41,7 @@ constexpr int64_t WS_COUNTERS = int64_t{1} << 16;
 constexpr int64_t CUS = 256;        // MI355X compute units
 constexpr int MAX_SPLIT = 16;
 
-enum PlanKind { KIND_GENERIC, KIND_SKINNY, KIND_TILE };
+enum PlanKind { KIND_GENERIC, KIND_SKINNY, KIND_GEMV, KIND_TILE };
 
 struct PlanInfo {
     const char *name;
@@ -54,6 +54,7 @@ const PlanInfo PLANS[] = {
     {"generic_64x64_scalar", KIND_GENERIC, -1, 1},
     {"skinny_mfma16_w8", KIND_SKINNY, -1, 1},
     {"skinny_mfma16_w8_splitk", KIND_SKINNY, -1, 0},
+    {"gemv_valu_w4", KIND_GEMV, -1, 1},
     {"tile_256x256_k64_w8", KIND_TILE, TC_256x256_K64_S2_W8, 1},
     {"tile_256x256_k64_w4", KIND_TILE, TC_256x256_K64_S2_W4, 1},
     {"tile_256x128_k64_w8", KIND_TILE, TC_256x128_K64_S2_W8, 1},
@@ -66,6 +67,13 @@ const PlanInfo PLANS[] = {
     {"tile_128x256_k64_w8_splitk", KIND_TILE, TC_128x256_K64_S2_W8, 0},
     {"tile_128x128_k64_w4_splitk", KIND_TILE, TC_128x128_K64_S2_W4, 0},
     {"tile_64x256_k64_w4_splitk", KIND_TILE, TC_64x256_K64_S2_W4, 0},
+    {"tile_128x128_k64s4_w4", KIND_TILE, TC_128x128_K64_S4_W4, 1},
+    {"tile_128x128_k64s4_w4_splitk", KIND_TILE, TC_128x128_K64_S4_W4, 0},
+    {"tile_128x128_k64s3_w4", KIND_TILE, TC_128x128_K64_S3_W4, 1},
+    {"tile_128x128_k64s3_w4_splitk", KIND_TILE, TC_128x128_K64_S3_W4, 0},
+    {"tile_64x256_k64s3_w4_splitk", KIND_TILE, TC_64x256_K64_S3_W4, 0},
+    {"tile_256x128_k64s3_w8", KIND_TILE, TC_256x128_K64_S3_W8, 1},
+    {"tile_256x128_k64s3_w8_splitk", KIND_TILE, TC_256x128_K64_S3_W8, 0},
 };
 constexpr int NUM_PLANS = static_cast<int>(sizeof(PLANS) / sizeof(PLANS[0]));
 
@@ -114,6 +122,8 @@ bool supports(int plan, int64_t M, int64_t N, int64_t K, bool residual) {
                 return false;
             return true;
         }
+        case KIND_GEMV:
+            return gemv_fits(M, N, K) && cdiv(N, 4) * 256 <= LIMIT_ITEMS;
         case KIND_TILE: {
             const TileShape ts = tile_shape(pi.tile_cfg);
             if (K % 8 != 0) return false;
@@ -145,14 +155,14 @@ struct TableEntry {
 };
 const TableEntry TABLE[] = {
     // attention-output-projection sweep: M x (N = K = hidden), residual
-    {1, 2048, 2048, 1, "skinny_mfma16_w8"},
-    {1, 4096, 4096, 1, "skinny_mfma16_w8"},
-    {1, 5120, 5120, 1, "skinny_mfma16_w8"},
-    {1, 8192, 8192, 1, "skinny_mfma16_w8"},
+    {1, 2048, 2048, 1, "gemv_valu_w4"},
+    {1, 4096, 4096, 1, "gemv_valu_w4"},
+    {1, 5120, 5120, 1, "gemv_valu_w4"},
+    {1, 8192, 8192, 1, "gemv_valu_w4"},
     {16, 4096, 4096, 1, "skinny_mfma16_w8"},
     {64, 2048, 2048, 1, "skinny_mfma16_w8_splitk"},
     {64, 4096, 4096, 1, "skinny_mfma16_w8"},
-    {64, 5120, 5120, 1, "tile_128x128_k64_w4_splitk"},
+    {64, 5120, 5120, 1, "tile_128x128_k64s3_w4_splitk"},
     {64, 8192, 8192, 1, "tile_128x128_k64_w4_splitk"},
     {512, 2048, 2048, 1, "tile_128x128_k64_w4_splitk"},
     {512, 4096, 4096, 1, "tile_128x128_k64_w4_splitk"},
@@ -168,8 +178,9 @@ const TableEntry TABLE[] = {
 };
 
 // Rule-based choice when no table entry matches (from the same
-// measurements): the skinny kernel up to 64 rows (its cross-workgroup split
-// when the weight has too few 16-row strips to fill the CUs); a 128x128 tile
+// measurements): the VALU GEMV up to 4 rows; the skinny kernel up to 64 rows
+// (its cross-workgroup split when the weight has too few 16-row strips to
+// fill the CUs); a 128x128 tile
 // with split-K for the ridge range up to 1024 rows; above that the 256x256
 // 8-wave tile when it fills the 256 CUs, else the 128x128 tile.
 int select(int64_t M, int64_t N, int64_t K, bool residual) {
@@ -185,6 +196,8 @@ int select(int64_t M, int64_t N, int64_t K, bool residual) {
         return (plan >= 0 && supports(plan, M, N, K, residual)) ? plan : -1;
     };
     int plan = -1;
+    if (M >= 1 && M <= 4) plan = pick("gemv_valu_w4");
+    if (plan >= 0) return plan;
     if (M >= 1 && M <= 64) {
         if (skinny_split_for(M, N, K) > 1) plan = pick("skinny_mfma16_w8_splitk");
         if (plan < 0) plan = pick("skinny_mfma16_w8");
@@ -331,6 +344,9 @@ int run(int plan, int64_t M, int64_t N, int64_t K, const void *X, const void *W,
             e = launch_skinny(p, split, split > 1 ? &ws : nullptr, stream);
             break;
         }
+        case KIND_GEMV:
+            e = launch_gemv(p, stream);
+            break;
         case KIND_TILE: {
             const int split = tile_split_of(plan, M, N, K);
             Workspace ws{};

@@ -14,7 +14,8 @@ enum PlanId : int {
     PLAN_GENERIC = 0,          // scalar LDS-tiled kernel: any K, any alignment
     PLAN_SKINNY = 1,           // M <= 64: stream W once, MFMA 16x16x32, in-WG split-K
     PLAN_SKINNY_SPLITK = 2,    // as PLAN_SKINNY plus a cross-workgroup split-K
-    PLAN_FIRST_TILE = 3,       // MFMA macro-tile plans follow (api.hip)
+    PLAN_GEMV = 3,             // M <= 4: contiguous W stream, VALU dot products
+    PLAN_FIRST_TILE = 4,       // MFMA macro-tile plans follow (api.hip)
 };
 
 // MFMA macro-tile kernel configurations (kernel_tile.hip):
@@ -27,7 +28,11 @@ enum TileCfg : int {
     TC_256x128_K64_S2_W4 = 4,
     TC_128x128_K64_S2_W4 = 5,
     TC_64x256_K64_S2_W4 = 6,
-    TC_COUNT = 7,
+    TC_128x128_K64_S4_W4 = 7,
+    TC_128x128_K64_S3_W4 = 8,
+    TC_64x256_K64_S3_W4 = 9,
+    TC_256x128_K64_S3_W8 = 10,
+    TC_COUNT = 11,
 };
 
 struct TileShape {
@@ -52,6 +57,7 @@ struct Workspace {
 // Launchers: validate nothing (plan.hip has done it), enqueue, return the
 // hipError_t of the launch.
 hipError_t launch_generic(const Problem &p, hipStream_t s);
+hipError_t launch_gemv(const Problem &p, hipStream_t s);
 hipError_t launch_skinny(const Problem &p, int split_k, const Workspace *ws, hipStream_t s);
 hipError_t launch_tile(int cfg, const Problem &p, int split, const Workspace *ws, hipStream_t s);
 
@@ -59,6 +65,7 @@ hipError_t launch_tile(int cfg, const Problem &p, int split, const Workspace *ws
 int skinny_split_for(int64_t M, int64_t N, int64_t K);
 int64_t skinny_workspace_floats(int64_t M, int64_t N, int split_k);
 int64_t skinny_counter_count(int64_t N);
+bool gemv_fits(int64_t M, int64_t N, int64_t K);
 
 // ------------------------------------------------------- device helpers ----
 // bf16 <-> fp32.  Widening is exact (bf16 is the top half of a binary32).

@@ -455,6 +455,10 @@ using C128x256w8 = Cfg<128, 256, 64, 2, 4, 2, 2>;
 using C256x128w4 = Cfg<256, 128, 64, 2, 2, 2, 1>;
 using C128x128w4 = Cfg<128, 128, 64, 2, 2, 2, 2>;
 using C64x256w4 = Cfg<64, 256, 64, 1, 4, 2, 2>;
+using C128x128s4 = Cfg<128, 128, 64, 2, 2, 4, 1>;
+using C128x128s3 = Cfg<128, 128, 64, 2, 2, 3, 1>;
+using C64x256s3 = Cfg<64, 256, 64, 1, 4, 3, 1>;
+using C256x128s3w8 = Cfg<256, 128, 64, 4, 2, 3, 2>;
 
 template <class C>
 constexpr TileShape shape_of(int per_cu) { return TileShape{C::BM, C::BN, C::BK, per_cu}; }
@@ -468,6 +472,10 @@ TileShape tile_shape(int cfg) {
         case TC_256x128_K64_S2_W4: return shape_of<C256x128w4>(1);
         case TC_128x128_K64_S2_W4: return shape_of<C128x128w4>(2);
         case TC_64x256_K64_S2_W4: return shape_of<C64x256w4>(2);
+        case TC_128x128_K64_S4_W4: return shape_of<C128x128s4>(1);
+        case TC_128x128_K64_S3_W4: return shape_of<C128x128s3>(1);
+        case TC_64x256_K64_S3_W4: return shape_of<C64x256s3>(1);
+        case TC_256x128_K64_S3_W8: return shape_of<C256x128s3w8>(1);
         default: return TileShape{0, 0, 0, 0};
     }
 }
@@ -481,6 +489,10 @@ hipError_t launch_tile(int cfg, const Problem &p, int split, const Workspace *ws
         case TC_256x128_K64_S2_W4: return launch_cfg<C256x128w4>(p, 8, split, ws, s);
         case TC_128x128_K64_S2_W4: return launch_cfg<C128x128w4>(p, 8, split, ws, s);
         case TC_64x256_K64_S2_W4: return launch_cfg<C64x256w4>(p, 8, split, ws, s);
+        case TC_128x128_K64_S4_W4: return launch_cfg<C128x128s4>(p, 8, split, ws, s);
+        case TC_128x128_K64_S3_W4: return launch_cfg<C128x128s3>(p, 8, split, ws, s);
+        case TC_64x256_K64_S3_W4: return launch_cfg<C64x256s3>(p, 8, split, ws, s);
+        case TC_256x128_K64_S3_W8: return launch_cfg<C256x128s3w8>(p, 8, split, ws, s);
         default: return hipErrorInvalidValue;
     }
 }

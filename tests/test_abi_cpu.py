@@ -50,7 +50,9 @@ def test_plan_table(ka):
     gen = names.index("generic_64x64_scalar")
     # K not a multiple of 8 -> generic; skinny M -> a skinny plan; big -> a tile plan
     assert ka.select_plan(128, 256, 250) == gen
-    for M in (1, 16, 64):
+    for M in (1, 4):
+        assert names[ka.select_plan(M, 4096, 4096)].startswith("gemv")
+    for M in (16, 64):
         assert names[ka.select_plan(M, 4096, 4096)].startswith("skinny")
     for M in (65, 512, 4096, 8192):
         assert names[ka.select_plan(M, 4096, 4096)].startswith("tile")

@@ -66,6 +66,7 @@ PLAN_SHAPES = {
     "generic_64x64_scalar": [(1, 1, 1), (70, 33, 13), (130, 100, 72)],
     "skinny_mfma16_w8": [(1, 8, 8), (17, 520, 1000), (64, 96, 4104), (33, 100, 264)],
     "skinny_mfma16_w8_splitk": [(1, 24, 8), (5, 520, 1000), (64, 96, 4104), (48, 100, 2064)],
+    "gemv_valu_w4": [(1, 8, 8), (1, 520, 1000), (3, 100, 4104), (4, 2048, 2048), (2, 77, 136), (1, 9000, 520)],
 }
 PLAN_SHAPES.update({n: TILE_SHAPES for n in _all_plan_names() if n.startswith("tile_")})
 assert set(PLAN_SHAPES) == set(_all_plan_names()), "every plan has test shapes"
@@ -91,6 +92,8 @@ def _unsigned_zero(bits):
 
 
 def _closed_form_shapes(plan):
+    if plan.startswith("gemv"):
+        return (4, 200, 200), (3, 136, 1000)
     if plan.startswith("skinny"):
         return (23, 200, 200), (40, 136, 1000)
     return (300, 264, 264), (130, 100, 520)
@@ -224,6 +227,7 @@ def test_graph_replay_matches_eager(ka):
     """Calls captured in a HIP graph give the eager result on every replay
     (the split-K plans' arrival counters must reset themselves)."""
     cases = [("skinny_mfma16_w8_splitk", (16, 1024, 4096)), ("skinny_mfma16_w8", (3, 520, 1000)),
+             ("gemv_valu_w4", (1, 4096, 4096)),
              ("tile_128x128_k64_w4_splitk", (512, 1024, 2048)), ("tile_256x256_k64_w8", (300, 520, 264)),
              ("tile_64x256_k64_w4_splitk", (64, 768, 4096))]
     for name, (M, N, K) in cases:
