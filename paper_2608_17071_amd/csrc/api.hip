@@ -74,6 +74,18 @@ const PlanInfo PLANS[] = {
     {"tile_64x256_k64s3_w4_splitk", KIND_TILE, TC_64x256_K64_S3_W4, 0},
     {"tile_256x128_k64s3_w8", KIND_TILE, TC_256x128_K64_S3_W8, 1},
     {"tile_256x128_k64s3_w8_splitk", KIND_TILE, TC_256x128_K64_S3_W8, 0},
+    {"tile_64x64_k64_w4", KIND_TILE, TC_64x64_K64_S2_W4, 1},
+    {"tile_64x64_k64_w4_splitk", KIND_TILE, TC_64x64_K64_S2_W4, 0},
+    {"tile_64x128_k64_w4", KIND_TILE, TC_64x128_K64_S2_W4, 1},
+    {"tile_64x128_k64_w4_splitk", KIND_TILE, TC_64x128_K64_S2_W4, 0},
+    {"tile_64x64_k128_w4", KIND_TILE, TC_64x64_K128_S2_W4, 1},
+    {"tile_64x64_k128_w4_splitk", KIND_TILE, TC_64x64_K128_S2_W4, 0},
+    {"tile_128x128_k128_w4", KIND_TILE, TC_128x128_K128_S2_W4, 1},
+    {"tile_128x128_k128_w4_splitk", KIND_TILE, TC_128x128_K128_S2_W4, 0},
+    {"tile_64x128_k128_w4", KIND_TILE, TC_64x128_K128_S2_W4, 1},
+    {"tile_64x128_k128_w4_splitk", KIND_TILE, TC_64x128_K128_S2_W4, 0},
+    {"tile_64x64_k128s3_w4", KIND_TILE, TC_64x64_K128_S3_W4, 1},
+    {"tile_64x64_k128s3_w4_splitk", KIND_TILE, TC_64x64_K128_S3_W4, 0},
 };
 constexpr int NUM_PLANS = static_cast<int>(sizeof(PLANS) / sizeof(PLANS[0]));
 
@@ -161,11 +173,11 @@ const TableEntry TABLE[] = {
     {1, 8192, 8192, 1, "gemv_valu_w4"},
     {16, 4096, 4096, 1, "skinny_mfma16_w8"},
     {64, 2048, 2048, 1, "skinny_mfma16_w8_splitk"},
-    {64, 4096, 4096, 1, "skinny_mfma16_w8"},
-    {64, 5120, 5120, 1, "tile_128x128_k64s3_w4_splitk"},
-    {64, 8192, 8192, 1, "tile_128x128_k64_w4_splitk"},
-    {512, 2048, 2048, 1, "tile_128x128_k64_w4_splitk"},
-    {512, 4096, 4096, 1, "tile_128x128_k64_w4_splitk"},
+    {64, 4096, 4096, 1, "tile_64x64_k128_w4_splitk"},
+    {64, 5120, 5120, 1, "tile_64x64_k128_w4_splitk"},
+    {64, 8192, 8192, 1, "tile_64x64_k128_w4_splitk"},
+    {512, 2048, 2048, 1, "tile_64x64_k128_w4_splitk"},
+    {512, 4096, 4096, 1, "tile_64x64_k128_w4"},
     {512, 5120, 5120, 1, "tile_128x128_k64_w4_splitk"},
     {512, 8192, 8192, 1, "tile_128x128_k64_w4_splitk"},
     {4096, 2048, 2048, 1, "tile_128x128_k64_w4"},
@@ -178,10 +190,11 @@ const TableEntry TABLE[] = {
 };
 
 // Rule-based choice when no table entry matches (from the same
-// measurements): the VALU GEMV up to 4 rows; the skinny kernel up to 64 rows
+// measurements): the VALU GEMV up to 4 rows; the skinny kernel up to 32 rows
 // (its cross-workgroup split when the weight has too few 16-row strips to
-// fill the CUs); a 128x128 tile
-// with split-K for the ridge range up to 1024 rows; above that the 256x256
+// fill the CUs); up to 1024 rows a 64x64 tile with K depth 128 while it
+// makes at most two tiles per 128 KB LDS pair of slots (split-K when that
+// leaves CUs idle), else a 128x128 tile with split-K; above that the 256x256
 // 8-wave tile when it fills the 256 CUs, else the 128x128 tile.
 int select(int64_t M, int64_t N, int64_t K, bool residual) {
     if (M < 0 || N < 0 || K < 0) return -1;
@@ -198,11 +211,15 @@ int select(int64_t M, int64_t N, int64_t K, bool residual) {
     int plan = -1;
     if (M >= 1 && M <= 4) plan = pick("gemv_valu_w4");
     if (plan >= 0) return plan;
-    if (M >= 1 && M <= 64) {
+    if (M >= 1 && M <= 32) {
         if (skinny_split_for(M, N, K) > 1) plan = pick("skinny_mfma16_w8_splitk");
         if (plan < 0) plan = pick("skinny_mfma16_w8");
     } else if (M <= 1024) {
-        plan = pick("tile_128x128_k64_w4_splitk");
+        const TileShape small = tile_shape(TC_64x64_K128_S2_W4);
+        const int64_t tiles = tile_count(small, M, N), slots = CUS * small.workgroups_per_cu;
+        if (2 * tiles <= slots) plan = pick("tile_64x64_k128_w4_splitk");
+        else if (tiles <= slots) plan = pick("tile_64x64_k128_w4");
+        if (plan < 0) plan = pick("tile_128x128_k64_w4_splitk");
     } else {
         const TileShape big = tile_shape(TC_256x256_K64_S2_W8);
         if (tile_count(big, M, N) >= CUS) plan = pick("tile_256x256_k64_w8");

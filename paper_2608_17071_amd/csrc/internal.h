@@ -32,7 +32,13 @@ enum TileCfg : int {
     TC_128x128_K64_S3_W4 = 8,
     TC_64x256_K64_S3_W4 = 9,
     TC_256x128_K64_S3_W8 = 10,
-    TC_COUNT = 11,
+    TC_64x64_K64_S2_W4 = 11,
+    TC_64x128_K64_S2_W4 = 12,
+    TC_64x64_K128_S2_W4 = 13,
+    TC_128x128_K128_S2_W4 = 14,
+    TC_64x128_K128_S2_W4 = 15,
+    TC_64x64_K128_S3_W4 = 16,
+    TC_COUNT = 17,
 };
 
 struct TileShape {

@@ -56,11 +56,13 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, ui
 // s_waitcnt immediate for gfx9: vmcnt = n (6 bits), expcnt and lgkmcnt not waited.
 constexpr int waitcnt_vm(int n) { return (n & 0xF) | ((n >> 4) << 14) | (0x7 << 4) | (0xF << 8); }
 
-// Slot of 16-byte chunk c of row r: c ^ swz(r).  8 chunks per row (BK=64)
-// or 4 (BK=32); both spread rows 0..7 and rows 0..15 over distinct slots.
+// Slot of 16-byte chunk c of row r: c ^ swz(r).  16 chunks per row
+// (BK=128), 8 (BK=64) or 4 (BK=32); each spreads rows 0..7 and rows 0..15
+// over distinct bank groups.
 template <int CHUNKS>
 __device__ __forceinline__ int swz(int r) {
-    if constexpr (CHUNKS == 8) return (r & 7) ^ ((r >> 3) & 1);
+    if constexpr (CHUNKS == 16) return r & 15;
+    else if constexpr (CHUNKS == 8) return (r & 7) ^ ((r >> 3) & 1);
     else return ((r >> 1) ^ (r >> 3)) & 3;
 }
 
@@ -87,7 +89,7 @@ struct Cfg {
     static constexpr int LANES_PER_ROW = WN / 8;
     static constexpr int ROWS_PER_PASS = 64 / LANES_PER_ROW;
 
-    static_assert(BK == 32 || BK == 64, "BK");
+    static_assert(BK == 32 || BK == 64 || BK == 128, "BK");
     static_assert(TM >= 1 && TN >= 1 && WM % 32 == 0 && WN % 32 == 0, "wave block");
     static_assert(A_LOADS >= 1 && B_LOADS >= 1 && BM % (RPI * WAVES) == 0 && BN % (RPI * WAVES) == 0,
                   "staging split");
@@ -459,6 +461,12 @@ using C128x128s4 = Cfg<128, 128, 64, 2, 2, 4, 1>;
 using C128x128s3 = Cfg<128, 128, 64, 2, 2, 3, 1>;
 using C64x256s3 = Cfg<64, 256, 64, 1, 4, 3, 1>;
 using C256x128s3w8 = Cfg<256, 128, 64, 4, 2, 3, 2>;
+using C64x64w4 = Cfg<64, 64, 64, 2, 2, 2, 4>;
+using C64x128w4 = Cfg<64, 128, 64, 2, 2, 2, 3>;
+using C64x64k128 = Cfg<64, 64, 128, 2, 2, 2, 2>;
+using C128x128k128 = Cfg<128, 128, 128, 2, 2, 2, 1>;
+using C64x128k128 = Cfg<64, 128, 128, 2, 2, 2, 1>;
+using C64x64k128s3 = Cfg<64, 64, 128, 2, 2, 3, 1>;
 
 template <class C>
 constexpr TileShape shape_of(int per_cu) { return TileShape{C::BM, C::BN, C::BK, per_cu}; }
@@ -476,6 +484,12 @@ TileShape tile_shape(int cfg) {
         case TC_128x128_K64_S3_W4: return shape_of<C128x128s3>(1);
         case TC_64x256_K64_S3_W4: return shape_of<C64x256s3>(1);
         case TC_256x128_K64_S3_W8: return shape_of<C256x128s3w8>(1);
+        case TC_64x64_K64_S2_W4: return shape_of<C64x64w4>(4);
+        case TC_64x128_K64_S2_W4: return shape_of<C64x128w4>(3);
+        case TC_64x64_K128_S2_W4: return shape_of<C64x64k128>(2);
+        case TC_128x128_K128_S2_W4: return shape_of<C128x128k128>(1);
+        case TC_64x128_K128_S2_W4: return shape_of<C64x128k128>(1);
+        case TC_64x64_K128_S3_W4: return shape_of<C64x64k128s3>(1);
         default: return TileShape{0, 0, 0, 0};
     }
 }
@@ -493,6 +507,12 @@ hipError_t launch_tile(int cfg, const Problem &p, int split, const Workspace *ws
         case TC_128x128_K64_S3_W4: return launch_cfg<C128x128s3>(p, 8, split, ws, s);
         case TC_64x256_K64_S3_W4: return launch_cfg<C64x256s3>(p, 8, split, ws, s);
         case TC_256x128_K64_S3_W8: return launch_cfg<C256x128s3w8>(p, 8, split, ws, s);
+        case TC_64x64_K64_S2_W4: return launch_cfg<C64x64w4>(p, 8, split, ws, s);
+        case TC_64x128_K64_S2_W4: return launch_cfg<C64x128w4>(p, 8, split, ws, s);
+        case TC_64x64_K128_S2_W4: return launch_cfg<C64x64k128>(p, 8, split, ws, s);
+        case TC_128x128_K128_S2_W4: return launch_cfg<C128x128k128>(p, 8, split, ws, s);
+        case TC_64x128_K128_S2_W4: return launch_cfg<C64x128k128>(p, 8, split, ws, s);
+        case TC_64x64_K128_S3_W4: return launch_cfg<C64x64k128s3>(p, 8, split, ws, s);
         default: return hipErrorInvalidValue;
     }
 }

@@ -52,9 +52,9 @@ def test_plan_table(ka):
     assert ka.select_plan(128, 256, 250) == gen
     for M in (1, 4):
         assert names[ka.select_plan(M, 4096, 4096)].startswith("gemv")
-    for M in (16, 64):
+    for M in (16, 32):
         assert names[ka.select_plan(M, 4096, 4096)].startswith("skinny")
-    for M in (65, 512, 4096, 8192):
+    for M in (33, 64, 65, 512, 4096, 8192):
         assert names[ka.select_plan(M, 4096, 4096)].startswith("tile")
     assert ka.select_plan(-1, 4, 4) == -1
     # every selected plan supports its shape; the generic plan supports everything
