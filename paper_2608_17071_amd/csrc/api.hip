@@ -41,13 +41,13 @@ constexpr int64_t WS_COUNTERS = int64_t{1} << 16;
 constexpr int64_t CUS = 256;        // MI355X compute units
 constexpr int MAX_SPLIT = 16;
 
-enum PlanKind { KIND_GENERIC, KIND_SKINNY, KIND_GEMV, KIND_TILE };
+enum PlanKind { KIND_GENERIC, KIND_SKINNY, KIND_GEMV, KIND_TILE, KIND_STREAM };
 
 struct PlanInfo {
     const char *name;
     PlanKind kind;
-    int tile_cfg;   // TileCfg for tile plans, -1 otherwise
-    int split;      // tile plans: 1 = no split-K, 0 = split-K by rule
+    int tile_cfg;   // TileCfg for tile plans, K depth (BK) for stream plans, -1 otherwise
+    int split;      // tile and stream plans: 1 = no split-K, 0 = split-K by rule
 };
 
 const PlanInfo PLANS[] = {
@@ -86,6 +86,9 @@ const PlanInfo PLANS[] = {
     {"tile_64x128_k128_w4_splitk", KIND_TILE, TC_64x128_K128_S2_W4, 0},
     {"tile_64x64_k128s3_w4", KIND_TILE, TC_64x64_K128_S3_W4, 1},
     {"tile_64x64_k128s3_w4_splitk", KIND_TILE, TC_64x64_K128_S3_W4, 0},
+    {"stream_mfma16_k128", KIND_STREAM, 128, 1},
+    {"stream_mfma16_k128_splitk", KIND_STREAM, 128, 0},
+    {"stream_mfma16_k64_splitk", KIND_STREAM, 64, 0},
 };
 constexpr int NUM_PLANS = static_cast<int>(sizeof(PLANS) / sizeof(PLANS[0]));
 
@@ -116,6 +119,15 @@ int tile_split_of(int plan, int64_t M, int64_t N, int64_t K) {
     return static_cast<int>(split);
 }
 
+// Split-K of the stream plans: the kernel's rule, at least 2 for the
+// "_splitk" plans so they always exercise the reduction.
+int stream_split_of(int plan, int64_t M, int64_t N, int64_t K) {
+    const PlanInfo &pi = PLANS[plan];
+    if (pi.split >= 1) return pi.split;
+    const int rule = stream_split_for(M, N, K, pi.tile_cfg);
+    return rule < 2 ? 2 : rule;
+}
+
 bool supports(int plan, int64_t M, int64_t N, int64_t K, bool residual) {
     (void)residual;
     if (M < 0 || N < 0 || K < 0 || M > LIMIT_DIM || N > LIMIT_DIM || K > LIMIT_DIM) return false;
@@ -136,6 +148,16 @@ bool supports(int plan, int64_t M, int64_t N, int64_t K, bool residual) {
         }
         case KIND_GEMV:
             return gemv_fits(M, N, K) && cdiv(N, 4) * 256 <= LIMIT_ITEMS;
+        case KIND_STREAM: {
+            if (M < 1 || M > 64 || K % 8 != 0) return false;
+            if (64 * K * 2 >= PANEL_LIMIT || M * N * 2 >= PANEL_LIMIT) return false;
+            const int split = stream_split_of(plan, M, N, K);
+            if (cdiv(N, 64) * split * 256 > LIMIT_ITEMS) return false;
+            if (split > 1 && (stream_workspace_floats(M, N, split) > WS_PARTIAL_FLOATS ||
+                              stream_counter_count(N) > WS_COUNTERS))
+                return false;
+            return true;
+        }
         case KIND_TILE: {
             const TileShape ts = tile_shape(pi.tile_cfg);
             if (K % 8 != 0) return false;
@@ -171,8 +193,8 @@ const TableEntry TABLE[] = {
     {1, 4096, 4096, 1, "gemv_valu_w4"},
     {1, 5120, 5120, 1, "gemv_valu_w4"},
     {1, 8192, 8192, 1, "gemv_valu_w4"},
-    {16, 4096, 4096, 1, "skinny_mfma16_w8"},
-    {64, 2048, 2048, 1, "skinny_mfma16_w8_splitk"},
+    {16, 4096, 4096, 1, "stream_mfma16_k64_splitk"},
+    {64, 2048, 2048, 1, "stream_mfma16_k128_splitk"},
     {64, 4096, 4096, 1, "tile_64x64_k128_w4_splitk"},
     {64, 5120, 5120, 1, "tile_64x64_k128_w4_splitk"},
     {64, 8192, 8192, 1, "tile_64x64_k128_w4_splitk"},
@@ -190,9 +212,8 @@ const TableEntry TABLE[] = {
 };
 
 // Rule-based choice when no table entry matches (from the same
-// measurements): the VALU GEMV up to 4 rows; the skinny kernel up to 32 rows
-// (its cross-workgroup split when the weight has too few 16-row strips to
-// fill the CUs); up to 1024 rows a 64x64 tile with K depth 128 while it
+// measurements): the VALU GEMV up to 4 rows; the streaming kernel with
+// split-K up to 32 rows; up to 1024 rows a 64x64 tile with K depth 128 while it
 // makes at most two tiles per 128 KB LDS pair of slots (split-K when that
 // leaves CUs idle), else a 128x128 tile with split-K; above that the 256x256
 // 8-wave tile when it fills the 256 CUs, else the 128x128 tile.
@@ -212,7 +233,7 @@ int select(int64_t M, int64_t N, int64_t K, bool residual) {
     if (M >= 1 && M <= 4) plan = pick("gemv_valu_w4");
     if (plan >= 0) return plan;
     if (M >= 1 && M <= 32) {
-        if (skinny_split_for(M, N, K) > 1) plan = pick("skinny_mfma16_w8_splitk");
+        plan = pick("stream_mfma16_k64_splitk");
         if (plan < 0) plan = pick("skinny_mfma16_w8");
     } else if (M <= 1024) {
         const TileShape small = tile_shape(TC_64x64_K128_S2_W4);
@@ -374,6 +395,16 @@ int run(int plan, int64_t M, int64_t N, int64_t K, const void *X, const void *W,
             e = launch_tile(PLANS[plan].tile_cfg, p, split, split > 1 ? &ws : nullptr, stream);
             break;
         }
+        case KIND_STREAM: {
+            const int split = stream_split_of(plan, M, N, K);
+            Workspace ws{};
+            if (split > 1) {
+                const int wst = workspace(dev, stream, &ws);
+                if (wst != KERNELARC_OK) return wst;
+            }
+            e = launch_stream(p, PLANS[plan].tile_cfg, split, split > 1 ? &ws : nullptr, stream);
+            break;
+        }
     }
     if (e != hipSuccess)
         return fail(KERNELARC_ERR_LAUNCH, "launch of %s failed: %s", PLANS[plan].name, hipGetErrorString(e));
@@ -425,6 +456,7 @@ int kernelarc_plan_uses_workspace(int plan, int64_t M, int64_t N, int64_t K) {
     if (!supports(plan, M, N, K, true)) return 0;
     if (PLANS[plan].kind == KIND_SKINNY) return skinny_split_of(plan, M, N, K) > 1 ? 1 : 0;
     if (PLANS[plan].kind == KIND_TILE) return tile_split_of(plan, M, N, K) > 1 ? 1 : 0;
+    if (PLANS[plan].kind == KIND_STREAM) return stream_split_of(plan, M, N, K) > 1 ? 1 : 0;
     return 0;
 }
 

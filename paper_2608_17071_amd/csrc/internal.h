@@ -66,12 +66,16 @@ hipError_t launch_generic(const Problem &p, hipStream_t s);
 hipError_t launch_gemv(const Problem &p, hipStream_t s);
 hipError_t launch_skinny(const Problem &p, int split_k, const Workspace *ws, hipStream_t s);
 hipError_t launch_tile(int cfg, const Problem &p, int split, const Workspace *ws, hipStream_t s);
+hipError_t launch_stream(const Problem &p, int bk, int split, const Workspace *ws, hipStream_t s);
 
 // Shape rules of the kernels, used by the plan table (host only).
 int skinny_split_for(int64_t M, int64_t N, int64_t K);
 int64_t skinny_workspace_floats(int64_t M, int64_t N, int split_k);
 int64_t skinny_counter_count(int64_t N);
 bool gemv_fits(int64_t M, int64_t N, int64_t K);
+int stream_split_for(int64_t M, int64_t N, int64_t K, int bk);
+int64_t stream_workspace_floats(int64_t M, int64_t N, int split);
+int64_t stream_counter_count(int64_t N);
 
 // ------------------------------------------------------- device helpers ----
 // bf16 <-> fp32.  Widening is exact (bf16 is the top half of a binary32).

@@ -1,0 +1,355 @@
+// Streaming MFMA kernel for few rows (M <= 64): Y = X W^T (+ R) as one pass
+// over the weight.
+//
+// With at most 64 rows of X the work is bound by reading W (N*K*2 bytes)
+// from HBM, and the time a load takes to come back (microseconds under load)
+// decides the rate unless each CU keeps several tens of kilobytes in flight.
+// The tile kernels synchronise their waves at every K step; here no wave
+// ever waits for another inside the K loop:
+//   * a workgroup of 4 waves owns one 64-row block of W and one K slice;
+//     each wave takes a contiguous quarter of the slice's BK steps and runs
+//     its own pipeline;
+//   * W goes through LDS-direct loads into the wave's private two-buffer
+//     ring (64 rows x BK, 16-byte chunk c of row r at slot c ^ swz(r)); one
+//     load instruction reads 64/(BK/8) whole row segments of BK*2
+//     contiguous bytes, and the wave's own vmcnt says when a buffer has
+//     landed;
+//   * X (at most 64 rows, L2-resident after first use) is read straight
+//     into MFMA A fragments, one step ahead;
+//   * v_mfma_f32_16x16x32_bf16 with A = 16 rows of X x 32 k and B = 16 rows
+//     of W x 32 k: MB = ceil(M/16) x 4 blocks per 32-k step, fp32
+//     accumulation in K order.
+// After the loop the four wave partials are added in LDS in wave order; a
+// split of K across workgroups goes through the fp32 workspace, where the
+// last workgroup of a row block adds the slices in slice order.  The
+// epilogue adds fp32(R) and rounds once to bf16; each output element is
+// read (R) and written (Y) by one lane, so Y may alias R.
+#include "internal.h"
+
+namespace kernelarc {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void;
+
+constexpr int RSRC_WORD3 = 0x00020000;
+constexpr uint32_t OOB_OFFSET = 0x80000000u;
+constexpr int AUX_SC1 = 16;   // device-scope (cross-XCD coherent) access
+constexpr int WAVES = 4;
+constexpr int THREADS = 64 * WAVES;
+constexpr int ROWS = 64;      // W rows per workgroup
+constexpr int STAGES = 2;     // per-wave W buffers
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), static_cast<short>(0),
+                                             static_cast<int>(bytes), RSRC_WORD3);
+}
+
+constexpr int waitcnt_vm(int n) { return (n & 0xF) | ((n >> 4) << 14) | (0x7 << 4) | (0xF << 8); }
+
+// Slot of 16-byte chunk c of row r is c ^ swz(r); a fragment read (16
+// consecutive rows at one chunk) then touches 16 distinct bank groups.
+template <int CHUNKS>
+__device__ __forceinline__ int swz(int r) {
+    if constexpr (CHUNKS == 16) return r & 15;
+    else return (r & 7) ^ ((r >> 3) & 1);
+}
+
+struct StreamSplit {
+    int split;          // K slices per row block (1: none)
+    int64_t kslice;     // slice length, a multiple of BK
+    float *partials;    // [row block][slice][wave][token block][lane] f32x4
+    unsigned *counters; // one arrival counter per row block, zero between calls
+};
+
+template <int MB, int BK>
+struct StreamCfg {
+    static constexpr int CHUNKS = BK / 8, ROW_BYTES = BK * 2, RPI = 64 / CHUNKS;
+    static constexpr int STAGE_BYTES = ROWS * ROW_BYTES;
+    static constexpr int W_LOADS = STAGE_BYTES / 1024;   // load instructions per stage
+    static constexpr int KS = BK / 32;                    // MFMA k steps per stage
+    static constexpr int X_LOADS = MB * KS;
+    static constexpr int WAVE_BYTES = STAGES * STAGE_BYTES;
+    static constexpr int LDS_BYTES = WAVES * WAVE_BYTES;
+    static constexpr int RED_BYTES = WAVES * MB * 4 * 64 * 16;   // wave partials, f32x4 per lane
+    static_assert(BK == 64 || BK == 128, "BK");
+    static_assert(MB >= 1 && MB <= 4, "token blocks");
+    static_assert(RED_BYTES <= LDS_BYTES, "reduction fits in the stage buffers");
+    static_assert(W_LOADS + X_LOADS < 64, "vmcnt range");
+};
+
+template <int MB, int BK>
+__global__ __launch_bounds__(THREADS) void stream_kernel(Problem p, int64_t nblocks, StreamSplit sk) {
+    using C = StreamCfg<MB, BK>;
+    __shared__ __attribute__((aligned(1024))) char lds[C::LDS_BYTES];
+
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t nb = blockIdx.x % nblocks;
+    const int64_t slice = blockIdx.x / nblocks;
+    const int64_t n0 = nb * ROWS;
+    const int64_t K = p.K;
+
+    // K range of the workgroup, then of this wave (a quarter of its steps).
+    const int64_t kbeg = slice * sk.kslice;
+    const int64_t kend = (kbeg + sk.kslice) < K ? (kbeg + sk.kslice) : K;
+    const int64_t steps = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
+    const int64_t step0 = kbeg / BK + steps * wave / WAVES;
+    const int nsteps = static_cast<int>(steps * (wave + 1) / WAVES - steps * wave / WAVES);
+
+    // Residual of the outputs this lane writes in the epilogue (wave w owns
+    // row block w after the reduction): fetched now, so its latency hides
+    // under the K loop.  Every element is read here before any lane writes
+    // Y, so Y may alias R.
+    const int64_t N = p.N;
+    const uint32_t ybytes = static_cast<uint32_t>(p.M * N * 2);
+    const __amdgpu_buffer_rsrc_t ry = make_rsrc(p.Y, ybytes);
+    // Without a residual the R resource is empty: its loads read zero.
+    const __amdgpu_buffer_rsrc_t rr = make_rsrc(p.R ? p.R : p.Y, p.R ? ybytes : 0u);
+    const int64_t n_out = n0 + 16 * wave + (lane & 15);
+    // Offset of output (16i + 4*(l/16) + e, n_out): rows past M fall outside
+    // the resource; a column past N is pointed out of range.  Computed
+    // without branches so the loads below issue back to back.
+    const uint32_t y_base = static_cast<uint32_t>((4 * (lane >> 4) * N + n_out) * 2);
+    const uint32_t row_bytes = static_cast<uint32_t>(N * 2);
+    const bool col_ok = n_out < N;
+    auto y_off = [&](int i, int e) {
+        const uint32_t off = y_base + static_cast<uint32_t>(16 * i + e) * row_bytes;
+        return col_ok ? off : OOB_OFFSET;
+    };
+    uint16_t rres[MB][4];
+#pragma unroll
+    for (int i = 0; i < MB; ++i)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) rres[i][e] = __builtin_amdgcn_raw_buffer_load_b16(rr, y_off(i, e), 0, 0);
+
+    const int64_t rows_w = (p.N - n0) < ROWS ? (p.N - n0) : ROWS;
+    const __amdgpu_buffer_rsrc_t rw = make_rsrc(p.W + n0 * K, static_cast<uint32_t>(rows_w * K * 2));
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc(p.X, static_cast<uint32_t>(p.M * K * 2));
+
+    // W staging map: lane l of load q fills slot l % CHUNKS of row
+    // RPI*q + l / CHUNKS with global chunk slot ^ swz(row).
+    uint32_t w_off[C::W_LOADS];
+    int w_k[C::W_LOADS];
+#pragma unroll
+    for (int q = 0; q < C::W_LOADS; ++q) {
+        const int r = q * C::RPI + lane / C::CHUNKS;
+        const int c = (lane % C::CHUNKS) ^ swz<C::CHUNKS>(r);
+        w_off[q] = static_cast<uint32_t>(r * K * 2 + c * 16);
+        w_k[q] = c * 8;
+    }
+    // A fragment of token block i at k step s: token 16i + l % 16, k chunk
+    // 4s + l / 16 of the stage.
+    const uint32_t x_row = static_cast<uint32_t>((lane & 15) * K * 2);
+    const int x_k = 8 * (lane >> 4);
+    char *ring = lds + wave * C::WAVE_BYTES;
+
+    // Loads of one step: chunks at or past the end of the wave's range
+    // (rem = k values left in the step, 0 for a step past the range) are
+    // pointed out of range; they move no data and only complete in order.
+    auto rem_of = [&](int64_t step, bool valid) {
+        const int64_t left = kend - step * BK;
+        return valid ? static_cast<int>(left < BK ? left : BK) : 0;
+    };
+    auto issue_w = [&](int buf, int64_t step, int rem) {
+        const uint32_t kb2 = static_cast<uint32_t>(step * BK * 2);
+#pragma unroll
+        for (int q = 0; q < C::W_LOADS; ++q) {
+            const uint32_t off = w_k[q] < rem ? w_off[q] + kb2 : OOB_OFFSET;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_void *)(ring + buf * C::STAGE_BYTES + q * 1024), 16,
+                                                     off, 0, 0, 0);
+        }
+    };
+    // X fragments of sub-step s of a step, token blocks 0..MB-1.
+    auto issue_x = [&](bf16x8 (&xs)[MB], int64_t step, int s, int rem) {
+        const int kr = 32 * s + x_k;
+        const uint32_t base = x_row + static_cast<uint32_t>((step * BK + kr) * 2);
+#pragma unroll
+        for (int i = 0; i < MB; ++i) {
+            const uint32_t off = kr < rem ? base + static_cast<uint32_t>(16 * i * K * 2) : OOB_OFFSET;
+            xs[i] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rx, off, 0, 0));
+        }
+    };
+
+    f32x4 acc[MB][4];
+#pragma unroll
+    for (int i = 0; i < MB; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+
+    // B fragment of row block j at k step s: row 16j + l % 16, chunk
+    // 4s + l / 16.
+    const int frag_row = lane & 15;
+    const int frag_hi = lane >> 4;
+
+    // Pipeline: step t's W is in buffer t % 2, issued one step ahead; X
+    // sub-step s of step t+1 is loaded into the registers of sub-step s of
+    // step t as soon as those have been multiplied (one step of lookahead).
+    bf16x8 xf[C::KS][MB];
+    if (nsteps > 0) {
+        const int rem0 = rem_of(step0, true);
+        issue_w(0, step0, rem0);
+#pragma unroll
+        for (int s = 0; s < C::KS; ++s) issue_x(xf[s], step0, s, rem0);
+    }
+    for (int t = 0; t < nsteps; ++t) {
+        const int64_t step = step0 + t;
+        const int buf = t & 1;
+        const int rem1 = rem_of(step + 1, t + 1 < nsteps);
+        issue_w(buf ^ 1, step + 1, rem1);
+        // Step t's W has landed once only step t+1's W and step t's X (in
+        // issue order after it) may be outstanding.
+        __builtin_amdgcn_s_waitcnt(waitcnt_vm(C::W_LOADS + C::X_LOADS));
+        const char *base = ring + buf * C::STAGE_BYTES + frag_row * C::ROW_BYTES;
+#pragma unroll
+        for (int s = 0; s < C::KS; ++s) {
+            bf16x8 wf[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int slot = (4 * s + frag_hi) ^ swz<C::CHUNKS>(16 * j + frag_row);
+                wf[j] = *reinterpret_cast<const bf16x8 *>(base + 16 * j * C::ROW_BYTES + slot * 16);
+            }
+#pragma unroll
+            for (int i = 0; i < MB; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xf[s][i], wf[j], acc[i][j], 0, 0, 0);
+            issue_x(xf[s], step + 1, s, rem1);
+        }
+    }
+
+    // Add the four wave partials in LDS (wave order).  Wave w then owns row
+    // block j = w of every token block.
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+    __syncthreads();
+    f32x4 *red = reinterpret_cast<f32x4 *>(lds);
+#pragma unroll
+    for (int i = 0; i < MB; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) red[((wave * MB + i) * 4 + j) * 64 + lane] = acc[i][j];
+    __syncthreads();
+    f32x4 sum[MB];
+#pragma unroll
+    for (int i = 0; i < MB; ++i) {
+        sum[i] = red[((0 * MB + i) * 4 + wave) * 64 + lane];
+#pragma unroll
+        for (int w = 1; w < WAVES; ++w) sum[i] += red[((w * MB + i) * 4 + wave) * 64 + lane];
+    }
+
+    if (sk.split > 1) {
+        // Publish this slice with device-scope stores; once every wave's
+        // stores have completed the arrival is counted, and the last slice
+        // to arrive adds all slices (device-scope loads) in slice order.
+        constexpr int BLOCK_FLOATS = WAVES * MB * 64 * 4;
+        const float *first = sk.partials + nb * sk.split * BLOCK_FLOATS;
+        const __amdgpu_buffer_rsrc_t rp = make_rsrc(first, static_cast<uint32_t>(sk.split) * BLOCK_FLOATS * 4u);
+        const uint32_t mine = static_cast<uint32_t>(slice) * BLOCK_FLOATS * 4u;
+#pragma unroll
+        for (int i = 0; i < MB; ++i)
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(i32x4, sum[i]), rp,
+                                                   mine + ((wave * MB + i) * 64 + lane) * 16, 0, AUX_SC1);
+        __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+        __syncthreads();
+        int *flag = reinterpret_cast<int *>(lds);   // every wave has read its sums (barrier above)
+        if (threadIdx.x == 0) {
+            const unsigned prev =
+                __hip_atomic_fetch_add(sk.counters + nb, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            *flag = prev == static_cast<unsigned>(sk.split - 1);
+        }
+        __syncthreads();
+        const bool last = *flag != 0;
+        if (!last) return;
+#pragma unroll
+        for (int i = 0; i < MB; ++i) sum[i] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+        // Eight slices per round trip; a slice past the last reads out of
+        // range and is not added, so the sum runs over the slices in order.
+        constexpr int D = 8;
+        for (int t0 = 0; t0 < sk.split; t0 += D) {
+            f32x4 v[D][MB];
+#pragma unroll
+            for (int d = 0; d < D; ++d)
+#pragma unroll
+                for (int i = 0; i < MB; ++i)
+                    v[d][i] = __builtin_bit_cast(
+                        f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                   rp, static_cast<uint32_t>(t0 + d) * BLOCK_FLOATS * 4u + ((wave * MB + i) * 64 + lane) * 16,
+                                   0, AUX_SC1));
+#pragma unroll
+            for (int d = 0; d < D; ++d) {
+                if (t0 + d >= sk.split) break;
+#pragma unroll
+                for (int i = 0; i < MB; ++i) sum[i] += v[d][i];
+            }
+        }
+        if (threadIdx.x == 0)
+            __hip_atomic_store(sk.counters + nb, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+
+    // Epilogue: sum[i][e] is Y[16i + 4*(l/16) + e][n0 + 16*wave + l%16].
+#pragma unroll
+    for (int i = 0; i < MB; ++i)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            float y = sum[i][e];
+            if (p.R) y += bf16_to_f32(rres[i][e]);
+            __builtin_amdgcn_raw_buffer_store_b16(f32_to_bf16_rne(y), ry, y_off(i, e), 0, 0);
+        }
+}
+
+template <int MB, int BK>
+hipError_t launch_mb(const Problem &p, int split, const Workspace *ws, hipStream_t s) {
+    const int64_t nblocks = (p.N + ROWS - 1) / ROWS;
+    StreamSplit sk{1, ((p.K + BK - 1) / BK) * BK, nullptr, nullptr};
+    if (split > 1) {
+        sk.split = split;
+        sk.kslice = (((p.K + split - 1) / split + BK - 1) / BK) * BK;
+        sk.partials = ws->partials;
+        sk.counters = ws->counters;
+    }
+    hipLaunchKernelGGL((stream_kernel<MB, BK>), dim3(static_cast<unsigned>(nblocks * sk.split)), dim3(THREADS), 0,
+                       s, p, nblocks, sk);
+    return hipGetLastError();
+}
+
+template <int BK>
+hipError_t launch_bk(const Problem &p, int split, const Workspace *ws, hipStream_t s) {
+    switch ((p.M + 15) / 16) {
+        case 1: return launch_mb<1, BK>(p, split, ws, s);
+        case 2: return launch_mb<2, BK>(p, split, ws, s);
+        case 3: return launch_mb<3, BK>(p, split, ws, s);
+        case 4: return launch_mb<4, BK>(p, split, ws, s);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace
+
+// K slices per 64-row block: enough workgroups for one per CU, each wave
+// at least one BK step of its slice.
+int stream_split_for(int64_t M, int64_t N, int64_t K, int bk) {
+    (void)M;
+    const int64_t nblocks = (N + ROWS - 1) / ROWS;
+    int64_t split = nblocks > 0 ? 256 / nblocks : 1;
+    const int64_t by_depth = K / (WAVES * bk);
+    if (split > by_depth) split = by_depth;
+    if (split > 16) split = 16;
+    return split < 1 ? 1 : static_cast<int>(split);
+}
+
+int64_t stream_workspace_floats(int64_t M, int64_t N, int split) {
+    const int64_t nblocks = (N + ROWS - 1) / ROWS;
+    return nblocks * split * WAVES * ((M + 15) / 16) * 64 * 4;
+}
+
+int64_t stream_counter_count(int64_t N) { return (N + ROWS - 1) / ROWS; }
+
+hipError_t launch_stream(const Problem &p, int bk, int split, const Workspace *ws, hipStream_t s) {
+    if (p.M < 1 || p.M > 64) return hipErrorInvalidValue;
+    if (bk == 128) return launch_bk<128>(p, split, ws, s);
+    if (bk == 64) return launch_bk<64>(p, split, ws, s);
+    return hipErrorInvalidValue;
+}
+
+}  // namespace kernelarc

@@ -306,6 +306,33 @@ void tile_kernel(Problem p, int64_t tiles_m, int64_t tiles_n, int group_m, Split
     __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));   // trailing LDS-direct loads have landed
     __syncthreads();                             // every wave is done with the stage buffers
 
+    // Epilogue constants.
+    float *ep = reinterpret_cast<float *>(lds) + wave * C::EPI_WAVE_FLOATS;
+    const int64_t N = p.N;
+    const int64_t rows_y = (p.M - m0) < C::BM ? (p.M - m0) : C::BM;
+    const uint32_t ybytes = static_cast<uint32_t>(rows_y * N * 2);
+    const __amdgpu_buffer_rsrc_t ry = make_rsrc(p.Y + m0 * N, ybytes);
+    const __amdgpu_buffer_rsrc_t rr = make_rsrc(p.R ? p.R + m0 * N : p.Y + m0 * N, ybytes);
+    const bool has_r = p.R != nullptr;
+    const bool vec = (N & 7) == 0;
+    const int pr = lane / C::LANES_PER_ROW;             // row within a pass
+    const int pc = (lane % C::LANES_PER_ROW) * 8;       // first of 8 columns
+    const int64_t col0 = n0 + wn0 + pc;
+    constexpr int PASSES = 32 / C::ROWS_PER_PASS;
+    auto base_of = [&](int i, int v) {
+        const int64_t row_local = wm0 + i * 32 + v * C::ROWS_PER_PASS + pr;
+        return static_cast<uint32_t>(row_local * N * 2 + col0 * 2);
+    };
+    // All of a slab's R is read before any of its Y is written (each element
+    // by the same lane), so the loads do not wait behind the stores and Y
+    // may alias R.
+    auto load_r = [&](int i, i32x4 (&rv)[PASSES]) {
+#pragma unroll
+        for (int v = 0; v < PASSES; ++v)
+            rv[v] = __builtin_amdgcn_raw_buffer_load_b128(rr, col0 < N ? base_of(i, v) : OOB_OFFSET, 0, 0);
+    };
+    i32x4 rv[PASSES];
+
     if (sk.split > 1) {
         // Publish this slice's fp32 tile in fragment order (each store
         // instruction writes 1 KB contiguous) with device-scope (sc1)
@@ -350,39 +377,66 @@ void tile_kernel(Problem p, int64_t tiles_m, int64_t tiles_n, int group_m, Split
             for (int j = 0; j < C::TN; ++j)
 #pragma unroll
                 for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
-        for (int t = 0; t < sk.split; ++t) {
-            const uint32_t base = static_cast<uint32_t>(t) * TILE_FLOATS * 4u;
+        // Small tiles: D slices per round trip (as many as 128 registers
+        // hold); a slice past the last reads out of range and is not added,
+        // so the sum still runs over the slices in order.  Large tiles
+        // (a slice fills 128 registers) go one slice at a time.
+        constexpr int NB = C::TM * C::TN * 4;
+        constexpr int D = NB * 4 >= 128 ? 1 : (128 / (NB * 4) > 8 ? 8 : 128 / (NB * 4));
+        if constexpr (D == 1) {
+            for (int t = 0; t < sk.split; ++t) {
+                const uint32_t base = static_cast<uint32_t>(t) * TILE_FLOATS * 4u;
 #pragma unroll
-            for (int i = 0; i < C::TM; ++i)
+                for (int i = 0; i < C::TM; ++i)
 #pragma unroll
-                for (int j = 0; j < C::TN; ++j)
+                    for (int j = 0; j < C::TN; ++j)
 #pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        const uint32_t off = base + (((wblk + i * C::TN + j) * 4 + q) * 64 + lane) * 16;
-                        const f32x4 v = __builtin_bit_cast(
-                            f32x4, __builtin_amdgcn_raw_buffer_load_b128(rp, off, 0, AUX_SC1));
-                        acc[i][j][4 * q] += v[0];
-                        acc[i][j][4 * q + 1] += v[1];
-                        acc[i][j][4 * q + 2] += v[2];
-                        acc[i][j][4 * q + 3] += v[3];
-                    }
+                        for (int q = 0; q < 4; ++q) {
+                            const uint32_t off = base + (((wblk + i * C::TN + j) * 4 + q) * 64 + lane) * 16;
+                            const f32x4 v = __builtin_bit_cast(
+                                f32x4, __builtin_amdgcn_raw_buffer_load_b128(rp, off, 0, AUX_SC1));
+                            acc[i][j][4 * q] += v[0];
+                            acc[i][j][4 * q + 1] += v[1];
+                            acc[i][j][4 * q + 2] += v[2];
+                            acc[i][j][4 * q + 3] += v[3];
+                        }
+            }
+        } else {
+            for (int t0 = 0; t0 < sk.split; t0 += D) {
+                f32x4 v[D][NB];
+#pragma unroll
+                for (int d = 0; d < D; ++d) {
+                    const uint32_t base = static_cast<uint32_t>(t0 + d) * TILE_FLOATS * 4u;
+#pragma unroll
+                    for (int b = 0; b < NB; ++b)
+                        v[d][b] = __builtin_bit_cast(
+                            f32x4, __builtin_amdgcn_raw_buffer_load_b128(rp, base + ((wblk * 4 + b) * 64 + lane) * 16,
+                                                                         0, AUX_SC1));
+                }
+#pragma unroll
+                for (int d = 0; d < D; ++d) {
+                    if (t0 + d >= sk.split) break;
+#pragma unroll
+                    for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+                        for (int j = 0; j < C::TN; ++j)
+#pragma unroll
+                            for (int q = 0; q < 4; ++q) {
+                                const f32x4 &w = v[d][(i * C::TN + j) * 4 + q];
+                                acc[i][j][4 * q] += w[0];
+                                acc[i][j][4 * q + 1] += w[1];
+                                acc[i][j][4 * q + 2] += w[2];
+                                acc[i][j][4 * q + 3] += w[3];
+                            }
+                }
+            }
         }
         if (threadIdx.x == 0)
             __hip_atomic_store(sk.counters + tile, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
-    float *ep = reinterpret_cast<float *>(lds) + wave * C::EPI_WAVE_FLOATS;
-    const int64_t N = p.N;
-    const int64_t rows_y = (p.M - m0) < C::BM ? (p.M - m0) : C::BM;
-    const uint32_t ybytes = static_cast<uint32_t>(rows_y * N * 2);
-    const __amdgpu_buffer_rsrc_t ry = make_rsrc(p.Y + m0 * N, ybytes);
-    const __amdgpu_buffer_rsrc_t rr = make_rsrc(p.R ? p.R + m0 * N : p.Y + m0 * N, ybytes);
-    const bool has_r = p.R != nullptr;
-    const bool vec = (N & 7) == 0;
-    const int pr = lane / C::LANES_PER_ROW;             // row within a pass
-    const int pc = (lane % C::LANES_PER_ROW) * 8;       // first of 8 columns
-    const int64_t col0 = n0 + wn0 + pc;
 #pragma unroll
     for (int i = 0; i < C::TM; ++i) {
+        if (vec && has_r) load_r(i, rv);
 #pragma unroll
         for (int j = 0; j < C::TN; ++j)
 #pragma unroll
@@ -390,21 +444,17 @@ void tile_kernel(Problem p, int64_t tiles_m, int64_t tiles_n, int group_m, Split
                 ep[(8 * (e >> 2) + 4 * hi + (e & 3)) * C::EPI_STRIDE + j * 32 + frag_row] = acc[i][j][e];
         __syncthreads();
 #pragma unroll
-        for (int v = 0; v < 32 / C::ROWS_PER_PASS; ++v) {
-            const int r = v * C::ROWS_PER_PASS + pr;
-            const float *src = ep + r * C::EPI_STRIDE + pc;
+        for (int v = 0; v < PASSES; ++v) {
+            const float *src = ep + (v * C::ROWS_PER_PASS + pr) * C::EPI_STRIDE + pc;
             float y[8];
 #pragma unroll
             for (int t = 0; t < 8; ++t) y[t] = src[t];
-            const int64_t row_local = wm0 + i * 32 + r;
-            const uint32_t base = static_cast<uint32_t>(row_local * N * 2 + col0 * 2);
+            const uint32_t base = base_of(i, v);
             if (vec) {
-                const uint32_t off = col0 < N ? base : OOB_OFFSET;
                 if (has_r) {
-                    const i32x4 rv = __builtin_amdgcn_raw_buffer_load_b128(rr, off, 0, 0);
 #pragma unroll
                     for (int t = 0; t < 4; ++t) {
-                        const uint32_t w = static_cast<uint32_t>(rv[t]);
+                        const uint32_t w = static_cast<uint32_t>(rv[v][t]);
                         y[2 * t] += bf16_to_f32(static_cast<uint16_t>(w & 0xffffu));
                         y[2 * t + 1] += bf16_to_f32(static_cast<uint16_t>(w >> 16));
                     }
@@ -414,14 +464,18 @@ void tile_kernel(Problem p, int64_t tiles_m, int64_t tiles_n, int group_m, Split
                 for (int t = 0; t < 4; ++t)
                     out[t] = static_cast<int>(static_cast<uint32_t>(f32_to_bf16_rne(y[2 * t])) |
                                               (static_cast<uint32_t>(f32_to_bf16_rne(y[2 * t + 1])) << 16));
-                __builtin_amdgcn_raw_buffer_store_b128(out, ry, off, 0, 0);
+                __builtin_amdgcn_raw_buffer_store_b128(out, ry, col0 < N ? base : OOB_OFFSET, 0, 0);
             } else {
+                uint16_t rs[8];
 #pragma unroll
                 for (int t = 0; t < 8; ++t) {
                     const uint32_t off = (col0 + t) < N ? base + 2 * t : OOB_OFFSET;
-                    float yt = y[t];
-                    if (has_r) yt += bf16_to_f32(__builtin_amdgcn_raw_buffer_load_b16(rr, off, 0, 0));
-                    __builtin_amdgcn_raw_buffer_store_b16(f32_to_bf16_rne(yt), ry, off, 0, 0);
+                    rs[t] = has_r ? __builtin_amdgcn_raw_buffer_load_b16(rr, off, 0, 0) : 0;
+                }
+#pragma unroll
+                for (int t = 0; t < 8; ++t) {
+                    const uint32_t off = (col0 + t) < N ? base + 2 * t : OOB_OFFSET;
+                    __builtin_amdgcn_raw_buffer_store_b16(f32_to_bf16_rne(y[t] + bf16_to_f32(rs[t])), ry, off, 0, 0);
                 }
             }
         }

@@ -53,7 +53,7 @@ def test_plan_table(ka):
     for M in (1, 4):
         assert names[ka.select_plan(M, 4096, 4096)].startswith("gemv")
     for M in (16, 32):
-        assert names[ka.select_plan(M, 4096, 4096)].startswith("skinny")
+        assert names[ka.select_plan(M, 4096, 4096)].startswith("stream")
     for M in (33, 64, 65, 512, 4096, 8192):
         assert names[ka.select_plan(M, 4096, 4096)].startswith("tile")
     assert ka.select_plan(-1, 4, 4) == -1
@@ -77,6 +77,13 @@ def test_plan_limits(ka):
     split = names.index("skinny_mfma16_w8_splitk")
     assert ka.kernelarc_plan_uses_workspace(split, 16, 1024, 4096) == 1
     assert ka.kernelarc_plan_uses_workspace(skinny, 16, 1024, 4096) == 0
+    stream = names.index("stream_mfma16_k128")
+    stream_split = names.index("stream_mfma16_k64_splitk")
+    assert ka.plan_supports(stream, 64, 8192, 8192) and ka.plan_supports(stream, 1, 8, 8)
+    assert not ka.plan_supports(stream, 65, 512, 512)          # M > 64
+    assert not ka.plan_supports(stream_split, 16, 512, 516)     # K % 8
+    assert ka.kernelarc_plan_uses_workspace(stream_split, 16, 4096, 4096) == 1
+    assert ka.kernelarc_plan_uses_workspace(stream, 16, 4096, 4096) == 0
 
 
 def test_validation_before_any_device_work(ka):

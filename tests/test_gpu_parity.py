@@ -67,6 +67,9 @@ PLAN_SHAPES = {
     "skinny_mfma16_w8": [(1, 8, 8), (17, 520, 1000), (64, 96, 4104), (33, 100, 264)],
     "skinny_mfma16_w8_splitk": [(1, 24, 8), (5, 520, 1000), (64, 96, 4104), (48, 100, 2064)],
     "gemv_valu_w4": [(1, 8, 8), (1, 520, 1000), (3, 100, 4104), (4, 2048, 2048), (2, 77, 136), (1, 9000, 520)],
+    "stream_mfma16_k128": [(1, 8, 8), (17, 520, 1000), (64, 96, 4104), (33, 100, 264), (49, 130, 136)],
+    "stream_mfma16_k128_splitk": [(1, 24, 8), (5, 520, 1000), (64, 96, 4104), (48, 100, 2064), (16, 70, 1032)],
+    "stream_mfma16_k64_splitk": [(2, 24, 8), (31, 520, 1000), (64, 96, 4104), (60, 200, 2056)],
 }
 PLAN_SHAPES.update({n: TILE_SHAPES for n in _all_plan_names() if n.startswith("tile_")})
 assert set(PLAN_SHAPES) == set(_all_plan_names()), "every plan has test shapes"
@@ -94,7 +97,7 @@ def _unsigned_zero(bits):
 def _closed_form_shapes(plan):
     if plan.startswith("gemv"):
         return (4, 200, 200), (3, 136, 1000)
-    if plan.startswith("skinny"):
+    if plan.startswith("skinny") or plan.startswith("stream"):
         return (23, 200, 200), (40, 136, 1000)
     return (300, 264, 264), (130, 100, 520)
 
@@ -229,7 +232,8 @@ def test_graph_replay_matches_eager(ka):
     cases = [("skinny_mfma16_w8_splitk", (16, 1024, 4096)), ("skinny_mfma16_w8", (3, 520, 1000)),
              ("gemv_valu_w4", (1, 4096, 4096)),
              ("tile_128x128_k64_w4_splitk", (512, 1024, 2048)), ("tile_256x256_k64_w8", (300, 520, 264)),
-             ("tile_64x256_k64_w4_splitk", (64, 768, 4096))]
+             ("tile_64x256_k64_w4_splitk", (64, 768, 4096)), ("stream_mfma16_k128_splitk", (64, 1024, 4096)),
+             ("stream_mfma16_k64_splitk", (16, 2048, 2048))]
     for name, (M, N, K) in cases:
         p = plan_id(ka, name)
         t = wl.make_inputs(wl.custom(M, N, K, seed=21))
