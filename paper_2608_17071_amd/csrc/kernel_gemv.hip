@@ -8,14 +8,17 @@
 // rows.  The dot products run on the VALU with v_dot2_f32_bf16 (bf16 pairs,
 // fp32 accumulation) -- at M <= 4 that is a few percent of the VALU's rate.
 //
-//   * X (M x K, at most 64 KB) is copied to LDS once per workgroup; lane l
-//     reads the 8 values of X that face its 16 bytes of W.
+//   * X (M x K, at most 64 KB) is copied to LDS once per workgroup with
+//     LDS-direct loads (1 KB each, all in flight together); lane l reads the
+//     8 values of X that face its 16 bytes of W.
 //   * a wave owns RPW consecutive rows and walks them k-segment by
 //     k-segment (all rows of a segment share one read of X from LDS), two
 //     batches of BATCH loads in flight;
 //   * per row and token the 64 lane partials are added by a fixed xor
 //     butterfly, then one lane adds fp32(R) and rounds once to bf16.  The
-//     residual is fetched at kernel start.  Y may alias R.
+//     residual is fetched at kernel start (from an empty resource when there
+//     is none, so the load needs no branch and nothing waits for it until
+//     the end).  Y may alias R.
 #include "internal.h"
 
 namespace kernelarc {
@@ -23,10 +26,12 @@ namespace {
 
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) void lds_void;
 
 constexpr int RSRC_WORD3 = 0x00020000;
 constexpr uint32_t OOB_OFFSET = 0x80000000u;
 constexpr int AUX_NT = 2;
+constexpr int WAITCNT_VM0 = 0x0F70;      // s_waitcnt vmcnt(0); expcnt and lgkmcnt not waited
 constexpr int WAVES = 4;
 constexpr int THREADS = 64 * WAVES;
 constexpr int BATCH = 4;                 // loads per batch (one kilobyte each)
@@ -66,7 +71,7 @@ __global__ __launch_bounds__(THREADS) void gemv_kernel(Problem p) {
     extern __shared__ __attribute__((aligned(16))) char xs[];   // X, M * K * 2 bytes
 
     const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int64_t K = p.K;
     const int64_t N = p.N;
     const int64_t row0 = (static_cast<int64_t>(blockIdx.x) * WAVES + wave) * RPW;
@@ -77,15 +82,21 @@ __global__ __launch_bounds__(THREADS) void gemv_kernel(Problem p) {
     const int my_t = lane / RPW;
     const int my_r = lane % RPW;
     const bool writer = my_t < MT && my_t < p.M && row0 + my_r < N;
-    float rres = 0.0f;
-    if (writer && p.R) rres = bf16_to_f32(p.R[my_t * N + row0 + my_r]);
+    const uint32_t y_off = writer ? static_cast<uint32_t>((my_t * N + row0 + my_r) * 2) : OOB_OFFSET;
+    const __amdgpu_buffer_rsrc_t rr = make_rsrc(p.R ? p.R : p.Y, p.R ? static_cast<uint32_t>(p.M * N * 2) : 0u);
+    const uint16_t rbits = __builtin_amdgcn_raw_buffer_load_b16(rr, y_off, 0, 0);
 
-    // X -> LDS, 16 bytes per thread per round (rows of X are K-contiguous).
+    // X -> LDS: every wave issues its share of the 1 KB LDS-direct loads
+    // (X is M*K*2 contiguous bytes; the tail past it reads zero), then one
+    // wait and one barrier.
     {
-        const int64_t chunks = p.M * K / 8;
-        const i32x4 *xg = reinterpret_cast<const i32x4 *>(p.X);
-        i32x4 *xl = reinterpret_cast<i32x4 *>(xs);
-        for (int64_t c = threadIdx.x; c < chunks; c += THREADS) xl[c] = xg[c];
+        const uint32_t xbytes = static_cast<uint32_t>(p.M * K * 2);
+        const __amdgpu_buffer_rsrc_t rxs = make_rsrc(p.X, xbytes);
+        const int xloads = static_cast<int>((xbytes + 1023) / 1024);
+        for (int q = wave; q < xloads; q += WAVES)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rxs, (lds_void *)(xs + q * 1024), 16,
+                                                     static_cast<uint32_t>(q * 1024 + lane * 16), 0, 0, 0);
+        __builtin_amdgcn_s_waitcnt(WAITCNT_VM0);
     }
     __syncthreads();
 
@@ -147,14 +158,18 @@ __global__ __launch_bounds__(THREADS) void gemv_kernel(Problem p) {
             const float v = wave_sum(acc[r][t]);
             if (lane == t * RPW + r) mine = v;
         }
-    if (writer) p.Y[my_t * N + row0 + my_r] = f32_to_bf16_rne(mine + rres);
+    if (writer) {
+        float y = mine;
+        if (p.R) y += bf16_to_f32(rbits);
+        p.Y[my_t * N + row0 + my_r] = f32_to_bf16_rne(y);
+    }
 }
 
 template <int MT>
 hipError_t launch_mt(const Problem &p, int rpw, hipStream_t s) {
     const int64_t rows_per_wg = static_cast<int64_t>(rpw) * WAVES;
     const dim3 grid(static_cast<unsigned>((p.N + rows_per_wg - 1) / rows_per_wg));
-    const size_t lds = static_cast<size_t>(p.M * p.K * 2);
+    const size_t lds = static_cast<size_t>((p.M * p.K * 2 + 1023) / 1024 * 1024);   // whole 1 KB loads
     switch (rpw) {
         case 1: hipLaunchKernelGGL((gemv_kernel<MT, 1>), grid, dim3(THREADS), lds, s, p); break;
         case 2: hipLaunchKernelGGL((gemv_kernel<MT, 2>), grid, dim3(THREADS), lds, s, p); break;
