@@ -86,6 +86,14 @@ const PlanInfo PLANS[] = {
     {"tile_64x128_k128_w4_splitk", KIND_TILE, TC_64x128_K128_S2_W4, 0},
     {"tile_64x64_k128s3_w4", KIND_TILE, TC_64x64_K128_S3_W4, 1},
     {"tile_64x64_k128s3_w4_splitk", KIND_TILE, TC_64x64_K128_S3_W4, 0},
+    {"tile_64x64_k64s4_w4", KIND_TILE, TC_64x64_K64_S4_W4, 1},
+    {"tile_64x64_k64s4_w4_splitk", KIND_TILE, TC_64x64_K64_S4_W4, 0},
+    {"tile_128x128_k32s4_w4", KIND_TILE, TC_128x128_K32_S4_W4, 1},
+    {"tile_128x128_k32s4_w4_splitk", KIND_TILE, TC_128x128_K32_S4_W4, 0},
+    {"tile_64x64_k64s8_w4", KIND_TILE, TC_64x64_K64_S8_W4, 1},
+    {"tile_64x64_k64s8_w4_splitk", KIND_TILE, TC_64x64_K64_S8_W4, 0},
+    {"tile_64x128_k64s4_w4", KIND_TILE, TC_64x128_K64_S4_W4, 1},
+    {"tile_64x128_k64s4_w4_splitk", KIND_TILE, TC_64x128_K64_S4_W4, 0},
     {"stream_mfma16_k128", KIND_STREAM, 128, 1},
     {"stream_mfma16_k128_splitk", KIND_STREAM, 128, 0},
     {"stream_mfma16_k64_splitk", KIND_STREAM, 64, 0},

@@ -38,7 +38,11 @@ enum TileCfg : int {
     TC_128x128_K128_S2_W4 = 14,
     TC_64x128_K128_S2_W4 = 15,
     TC_64x64_K128_S3_W4 = 16,
-    TC_COUNT = 17,
+    TC_64x64_K64_S4_W4 = 17,
+    TC_128x128_K32_S4_W4 = 18,
+    TC_64x64_K64_S8_W4 = 19,
+    TC_64x128_K64_S4_W4 = 20,
+    TC_COUNT = 21,
 };
 
 struct TileShape {

@@ -521,6 +521,10 @@ using C64x64k128 = Cfg<64, 64, 128, 2, 2, 2, 2>;
 using C128x128k128 = Cfg<128, 128, 128, 2, 2, 2, 1>;
 using C64x128k128 = Cfg<64, 128, 128, 2, 2, 2, 1>;
 using C64x64k128s3 = Cfg<64, 64, 128, 2, 2, 3, 1>;
+using C64x64k64s4 = Cfg<64, 64, 64, 2, 2, 4, 2>;
+using C128x128k32s4 = Cfg<128, 128, 32, 2, 2, 4, 2>;
+using C64x64k64s8 = Cfg<64, 64, 64, 2, 2, 8, 1>;
+using C64x128k64s4 = Cfg<64, 128, 64, 2, 2, 4, 1>;
 
 template <class C>
 constexpr TileShape shape_of(int per_cu) { return TileShape{C::BM, C::BN, C::BK, per_cu}; }
@@ -544,6 +548,10 @@ TileShape tile_shape(int cfg) {
         case TC_128x128_K128_S2_W4: return shape_of<C128x128k128>(1);
         case TC_64x128_K128_S2_W4: return shape_of<C64x128k128>(1);
         case TC_64x64_K128_S3_W4: return shape_of<C64x64k128s3>(1);
+        case TC_64x64_K64_S4_W4: return shape_of<C64x64k64s4>(2);
+        case TC_128x128_K32_S4_W4: return shape_of<C128x128k32s4>(2);
+        case TC_64x64_K64_S8_W4: return shape_of<C64x64k64s8>(1);
+        case TC_64x128_K64_S4_W4: return shape_of<C64x128k64s4>(1);
         default: return TileShape{0, 0, 0, 0};
     }
 }
@@ -567,6 +575,10 @@ hipError_t launch_tile(int cfg, const Problem &p, int split, const Workspace *ws
         case TC_128x128_K128_S2_W4: return launch_cfg<C128x128k128>(p, 8, split, ws, s);
         case TC_64x128_K128_S2_W4: return launch_cfg<C64x128k128>(p, 8, split, ws, s);
         case TC_64x64_K128_S3_W4: return launch_cfg<C64x64k128s3>(p, 8, split, ws, s);
+        case TC_64x64_K64_S4_W4: return launch_cfg<C64x64k64s4>(p, 8, split, ws, s);
+        case TC_128x128_K32_S4_W4: return launch_cfg<C128x128k32s4>(p, 8, split, ws, s);
+        case TC_64x64_K64_S8_W4: return launch_cfg<C64x64k64s8>(p, 8, split, ws, s);
+        case TC_64x128_K64_S4_W4: return launch_cfg<C64x128k64s4>(p, 8, split, ws, s);
         default: return hipErrorInvalidValue;
     }
 }
