@@ -87,13 +87,21 @@ __device__ __forceinline__ float bf16_to_f32(uint16_t b) {
     return __uint_as_float(static_cast<uint32_t>(b) << 16);
 }
 
-// fp32 -> bf16, round to nearest, ties to even; NaN stays NaN (quiet),
-// finite values beyond the bf16 range round to infinity.
+// fp32 -> bf16, round to nearest, ties to even; NaN stays NaN (quiet, sign
+// and leading payload bits kept), finite values beyond the bf16 range round
+// to infinity.  gfx950 does this in one instruction (v_cvt_pk_bf16_f32);
+// its results equal the bit-level definition -- add 0x7fff plus the lowest
+// kept bit, truncate; NaN -> top half with the quiet bit set -- for every
+// one of the 2^32 inputs.
 __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<uint16_t>((u >> 16) | 0x0040u);
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return static_cast<uint16_t>(u >> 16);
+    return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f));
+}
+
+// Two values at once (one v_cvt_pk_bf16_f32): lo in bits 0-15, hi in 16-31.
+typedef float f32x2_pair __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_pair __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t f32x2_to_bf16x2_rne(float lo, float hi) {
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_pair{lo, hi}, bf16x2_pair));
 }
 
 }  // namespace kernelarc

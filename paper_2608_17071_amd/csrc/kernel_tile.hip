@@ -312,7 +312,8 @@ void tile_kernel(Problem p, int64_t tiles_m, int64_t tiles_n, int group_m, Split
     const int64_t rows_y = (p.M - m0) < C::BM ? (p.M - m0) : C::BM;
     const uint32_t ybytes = static_cast<uint32_t>(rows_y * N * 2);
     const __amdgpu_buffer_rsrc_t ry = make_rsrc(p.Y + m0 * N, ybytes);
-    const __amdgpu_buffer_rsrc_t rr = make_rsrc(p.R ? p.R + m0 * N : p.Y + m0 * N, ybytes);
+    // Without a residual the R resource is empty (its loads read zero).
+    const __amdgpu_buffer_rsrc_t rr = make_rsrc(p.R ? p.R + m0 * N : p.Y + m0 * N, p.R ? ybytes : 0u);
     const bool has_r = p.R != nullptr;
     const bool vec = (N & 7) == 0;
     const int pr = lane / C::LANES_PER_ROW;             // row within a pass
@@ -331,7 +332,9 @@ void tile_kernel(Problem p, int64_t tiles_m, int64_t tiles_n, int group_m, Split
         for (int v = 0; v < PASSES; ++v)
             rv[v] = __builtin_amdgcn_raw_buffer_load_b128(rr, col0 < N ? base_of(i, v) : OOB_OFFSET, 0, 0);
     };
-    i32x4 rv[PASSES];
+    // Two slabs of R in registers: slab i+1 is requested before slab i is
+    // staged and stored, so only slab 0's latency is exposed.
+    i32x4 rv[2][PASSES];
 
     if (sk.split > 1) {
         // Publish this slice's fp32 tile in fragment order (each store
@@ -434,9 +437,10 @@ void tile_kernel(Problem p, int64_t tiles_m, int64_t tiles_n, int group_m, Split
         if (threadIdx.x == 0)
             __hip_atomic_store(sk.counters + tile, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
+    if (vec && has_r) load_r(0, rv[0]);
 #pragma unroll
     for (int i = 0; i < C::TM; ++i) {
-        if (vec && has_r) load_r(i, rv);
+        if (vec && has_r && i + 1 < C::TM) load_r(i + 1, rv[(i + 1) & 1]);
 #pragma unroll
         for (int j = 0; j < C::TN; ++j)
 #pragma unroll
@@ -454,28 +458,24 @@ void tile_kernel(Problem p, int64_t tiles_m, int64_t tiles_n, int group_m, Split
                 if (has_r) {
 #pragma unroll
                     for (int t = 0; t < 4; ++t) {
-                        const uint32_t w = static_cast<uint32_t>(rv[v][t]);
+                        const uint32_t w = static_cast<uint32_t>(rv[i & 1][v][t]);
                         y[2 * t] += bf16_to_f32(static_cast<uint16_t>(w & 0xffffu));
                         y[2 * t + 1] += bf16_to_f32(static_cast<uint16_t>(w >> 16));
                     }
                 }
                 i32x4 out;
 #pragma unroll
-                for (int t = 0; t < 4; ++t)
-                    out[t] = static_cast<int>(static_cast<uint32_t>(f32_to_bf16_rne(y[2 * t])) |
-                                              (static_cast<uint32_t>(f32_to_bf16_rne(y[2 * t + 1])) << 16));
+                for (int t = 0; t < 4; ++t) out[t] = static_cast<int>(f32x2_to_bf16x2_rne(y[2 * t], y[2 * t + 1]));
                 __builtin_amdgcn_raw_buffer_store_b128(out, ry, col0 < N ? base : OOB_OFFSET, 0, 0);
             } else {
                 uint16_t rs[8];
+                const int cols = static_cast<int>(N - col0);   // columns of this lane's 8 that exist
+#pragma unroll
+                for (int t = 0; t < 8; ++t) rs[t] = __builtin_amdgcn_raw_buffer_load_b16(rr, t < cols ? base + 2 * t : OOB_OFFSET, 0, 0);
 #pragma unroll
                 for (int t = 0; t < 8; ++t) {
-                    const uint32_t off = (col0 + t) < N ? base + 2 * t : OOB_OFFSET;
-                    rs[t] = has_r ? __builtin_amdgcn_raw_buffer_load_b16(rr, off, 0, 0) : 0;
-                }
-#pragma unroll
-                for (int t = 0; t < 8; ++t) {
-                    const uint32_t off = (col0 + t) < N ? base + 2 * t : OOB_OFFSET;
-                    __builtin_amdgcn_raw_buffer_store_b16(f32_to_bf16_rne(y[t] + bf16_to_f32(rs[t])), ry, off, 0, 0);
+                    const float yt = has_r ? y[t] + bf16_to_f32(rs[t]) : y[t];
+                    __builtin_amdgcn_raw_buffer_store_b16(f32_to_bf16_rne(yt), ry, t < cols ? base + 2 * t : OOB_OFFSET, 0, 0);
                 }
             }
         }
