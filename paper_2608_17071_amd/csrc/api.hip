@@ -94,6 +94,12 @@ const PlanInfo PLANS[] = {
     {"tile_64x64_k64s8_w4_splitk", KIND_TILE, TC_64x64_K64_S8_W4, 0},
     {"tile_64x128_k64s4_w4", KIND_TILE, TC_64x128_K64_S4_W4, 1},
     {"tile_64x128_k64s4_w4_splitk", KIND_TILE, TC_64x128_K64_S4_W4, 0},
+    {"tile_64x64_k128_g2", KIND_TILE, TC_64x64_K128_S2_G2, 1},
+    {"tile_64x64_k128_g2_splitk", KIND_TILE, TC_64x64_K128_S2_G2, 0},
+    {"tile_128x128_k64_g2", KIND_TILE, TC_128x128_K64_S2_G2, 1},
+    {"tile_128x128_k64_g2_splitk", KIND_TILE, TC_128x128_K64_S2_G2, 0},
+    {"tile_64x64_k64_g4", KIND_TILE, TC_64x64_K64_S2_G4, 1},
+    {"tile_64x64_k64_g4_splitk", KIND_TILE, TC_64x64_K64_S2_G4, 0},
     {"stream_mfma16_k128", KIND_STREAM, 128, 1},
     {"stream_mfma16_k128_splitk", KIND_STREAM, 128, 0},
     {"stream_mfma16_k64_splitk", KIND_STREAM, 64, 0},
@@ -203,11 +209,11 @@ const TableEntry TABLE[] = {
     {1, 8192, 8192, 1, "gemv_valu_w4"},
     {16, 4096, 4096, 1, "stream_mfma16_k64_splitk"},
     {64, 2048, 2048, 1, "stream_mfma16_k128_splitk"},
-    {64, 4096, 4096, 1, "tile_64x64_k128_w4_splitk"},
+    {64, 4096, 4096, 1, "tile_64x64_k128_g2_splitk"},
     {64, 5120, 5120, 1, "tile_64x64_k128_w4_splitk"},
-    {64, 8192, 8192, 1, "tile_64x64_k128_w4_splitk"},
-    {512, 2048, 2048, 1, "tile_64x64_k128_w4_splitk"},
-    {512, 4096, 4096, 1, "tile_64x64_k128_w4"},
+    {64, 8192, 8192, 1, "tile_64x64_k64_g4_splitk"},
+    {512, 2048, 2048, 1, "tile_64x64_k128_g2"},
+    {512, 4096, 4096, 1, "tile_128x128_k64_g2_splitk"},
     {512, 5120, 5120, 1, "tile_128x128_k64_w4_splitk"},
     {512, 8192, 8192, 1, "tile_128x128_k64_w4_splitk"},
     {4096, 2048, 2048, 1, "tile_128x128_k64_w4"},

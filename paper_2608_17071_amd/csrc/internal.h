@@ -42,7 +42,10 @@ enum TileCfg : int {
     TC_128x128_K32_S4_W4 = 18,
     TC_64x64_K64_S8_W4 = 19,
     TC_64x128_K64_S4_W4 = 20,
-    TC_COUNT = 21,
+    TC_64x64_K128_S2_G2 = 21,     // two K groups of 4 waves (8 waves)
+    TC_128x128_K64_S2_G2 = 22,
+    TC_64x64_K64_S2_G4 = 23,      // four K groups (16 waves)
+    TC_COUNT = 24,
 };
 
 struct TileShape {

@@ -66,20 +66,25 @@ __device__ __forceinline__ int swz(int r) {
     else return ((r >> 1) ^ (r >> 3)) & 3;
 }
 
-template <int BM_, int BN_, int BK_, int WAVES_M_, int WAVES_N_, int STAGES_, int WAVES_PER_EU_>
+template <int BM_, int BN_, int BK_, int WAVES_M_, int WAVES_N_, int STAGES_, int WAVES_PER_EU_, int KGROUPS_ = 1>
 struct Cfg {
     static constexpr int BM = BM_, BN = BN_, BK = BK_, STAGES = STAGES_;
     static constexpr int WAVES_M = WAVES_M_, WAVES_N = WAVES_N_;
-    static constexpr int WAVES = WAVES_M * WAVES_N, THREADS = 64 * WAVES;
+    // KGROUPS groups of WAVES_M x WAVES_N waves each run the whole tile over
+    // their own part of the workgroup's K range, in their own LDS ring.
+    static constexpr int KGROUPS = KGROUPS_;
+    static constexpr int TILE_WAVES = WAVES_M * WAVES_N;
+    static constexpr int WAVES = TILE_WAVES * KGROUPS, THREADS = 64 * WAVES;
     static constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;   // per-wave block
     static constexpr int TM = WM / 32, TN = WN / 32;             // 32x32 blocks per wave
     static constexpr int KSTEPS = BK / 16;                        // MFMA sub-steps per stage
     static constexpr int ROW_BYTES = BK * 2, CHUNKS = BK / 8, RPI = 64 / CHUNKS;
     static constexpr int A_BYTES = BM * ROW_BYTES, B_BYTES = BN * ROW_BYTES;
     static constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
-    static constexpr int LDS_BYTES = STAGES * STAGE_BYTES;
-    static constexpr int A_LOADS = BM / RPI / WAVES;              // DMA instructions per wave per stage
-    static constexpr int B_LOADS = BN / RPI / WAVES;
+    static constexpr int GROUP_BYTES = STAGES * STAGE_BYTES;
+    static constexpr int LDS_BYTES = KGROUPS * GROUP_BYTES;
+    static constexpr int A_LOADS = BM / RPI / TILE_WAVES;         // DMA instructions per wave per stage
+    static constexpr int B_LOADS = BN / RPI / TILE_WAVES;
     static constexpr int LOADS = A_LOADS + B_LOADS;
     static constexpr int WAVES_PER_EU = WAVES_PER_EU_;
     // Epilogue staging: one 32-row slab of a wave's block in fp32, rows
@@ -88,14 +93,18 @@ struct Cfg {
     static constexpr int EPI_WAVE_FLOATS = 32 * EPI_STRIDE;
     static constexpr int LANES_PER_ROW = WN / 8;
     static constexpr int ROWS_PER_PASS = 64 / LANES_PER_ROW;
+    // K-group partials handed to group 0 through LDS (fp32, fragment order).
+    static constexpr int RED_BYTES = (KGROUPS - 1) * TILE_WAVES * TM * TN * 16 * 64 * 4;
 
     static_assert(BK == 32 || BK == 64 || BK == 128, "BK");
     static_assert(TM >= 1 && TN >= 1 && WM % 32 == 0 && WN % 32 == 0, "wave block");
-    static_assert(A_LOADS >= 1 && B_LOADS >= 1 && BM % (RPI * WAVES) == 0 && BN % (RPI * WAVES) == 0,
+    static_assert(A_LOADS >= 1 && B_LOADS >= 1 && BM % (RPI * TILE_WAVES) == 0 && BN % (RPI * TILE_WAVES) == 0,
                   "staging split");
     static_assert(STAGES >= 2, "pipeline depth");
+    static_assert(KGROUPS >= 1 && WAVES <= 16, "workgroup size");
     static_assert(LDS_BYTES <= 160 * 1024, "LDS capacity");
-    static_assert(WAVES * EPI_WAVE_FLOATS * 4 <= LDS_BYTES, "epilogue staging fits");
+    static_assert(TILE_WAVES * EPI_WAVE_FLOATS * 4 <= LDS_BYTES, "epilogue staging fits");
+    static_assert(RED_BYTES <= LDS_BYTES, "K-group reduction fits");
     static_assert(LOADS * (STAGES - 2) < 64, "vmcnt range");
 };
 
@@ -188,7 +197,10 @@ void tile_kernel(Problem p, int64_t tiles_m, int64_t tiles_n, int group_m, Split
     __shared__ __attribute__((aligned(1024))) char lds[C::LDS_BYTES];
 
     const int lane = threadIdx.x & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wave_id = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int group = wave_id / C::TILE_WAVES;              // K group
+    const int wave = wave_id - group * C::TILE_WAVES;       // wave within the tile
+    char *const glds = lds + group * C::GROUP_BYTES;        // this group's LDS ring
 
     // Workgroup -> (K slice, tile): the XCD remap runs over slice-major ids,
     // so each XCD takes neighbouring tiles of one slice.
@@ -259,28 +271,37 @@ void tile_kernel(Problem p, int64_t tiles_m, int64_t tiles_n, int group_m, Split
     const int b_row_byte = (wn0 + frag_row) * C::ROW_BYTES;
     const int frag_swz = swz<C::CHUNKS>(frag_row);
 
+    // The workgroup's BK steps [kt0, kt1); K group g takes the contiguous
+    // part [g0, g1).  Every group runs the same number of iterations (the
+    // barrier is shared); steps past its part load out-of-range zeros.
     const int kt0 = static_cast<int>(kbeg / C::BK);
     const int kt1 = kend > kbeg ? static_cast<int>((kend + C::BK - 1) / C::BK) : kt0;
+    const int nsteps = kt1 - kt0;
+    const int g0 = kt0 + nsteps * group / C::KGROUPS;
+    const int g1 = kt0 + nsteps * (group + 1) / C::KGROUPS;
+    const int iters = (nsteps + C::KGROUPS - 1) / C::KGROUPS;
+    const int64_t gend = (static_cast<int64_t>(g1) * C::BK) < kend ? static_cast<int64_t>(g1) * C::BK : kend;
 
     // Prologue: STAGES-1 steps in flight (past the end of the range the
     // loads are out of range and only write zeros into buffers nobody reads).
 #pragma unroll
     for (int s = 0; s < C::STAGES - 1; ++s)
-        issue_stage<C>(lds + s * C::STAGE_BYTES, ra, rb, a_off, a_k, b_off, b_k, wave, kt0 + s, kend);
+        issue_stage<C>(glds + s * C::STAGE_BYTES, ra, rb, a_off, a_k, b_off, b_k, wave, g0 + s, gend);
 
     int cur_stage = 0;
-    for (int kt = kt0; kt < kt1; ++kt) {
+    for (int it = 0; it < iters; ++it) {
+        const int kt = g0 + it;
         // Stage kt has landed once at most STAGES-2 stages' loads are outstanding.
         __builtin_amdgcn_s_waitcnt(waitcnt_vm(C::LOADS * (C::STAGES - 2)));
         __syncthreads();   // every wave's part of stage kt; stage kt-1's buffer is free
-        const char *cur = lds + cur_stage * C::STAGE_BYTES;
+        const char *cur = glds + cur_stage * C::STAGE_BYTES;
         const char *a_base = cur + a_row_byte;
         const char *b_base = cur + C::A_BYTES + b_row_byte;
         bf16x8 af[2][C::TM], bfr[2][C::TN];
         load_fragments<C>(a_base, b_base, (hi ^ frag_swz) * 16, af[0], bfr[0]);
         const int free_stage = cur_stage == 0 ? C::STAGES - 1 : cur_stage - 1;   // held step kt-1
-        issue_stage<C>(lds + free_stage * C::STAGE_BYTES, ra, rb, a_off, a_k, b_off, b_k, wave,
-                       kt + C::STAGES - 1, kend);
+        issue_stage<C>(glds + free_stage * C::STAGE_BYTES, ra, rb, a_off, a_k, b_off, b_k, wave,
+                       kt + C::STAGES - 1, gend);
 #pragma unroll
         for (int ks = 0; ks < C::KSTEPS; ++ks) {
             if (ks + 1 < C::KSTEPS)
@@ -305,6 +326,42 @@ void tile_kernel(Problem p, int64_t tiles_m, int64_t tiles_n, int group_m, Split
     // dropped by the range check; columns past N are pointed out of range).
     __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));   // trailing LDS-direct loads have landed
     __syncthreads();                             // every wave is done with the stage buffers
+
+    // K groups 1.. hand their partial tiles to group 0 through LDS; group 0
+    // adds them in group order and does the rest.  The other waves stay to
+    // the end, so every barrier below is reached by the whole workgroup.
+    if constexpr (C::KGROUPS > 1) {
+        f32x4 *red = reinterpret_cast<f32x4 *>(lds);
+        constexpr int NB = C::TM * C::TN * 4;        // f32x4 per lane per wave
+        if (group > 0) {
+#pragma unroll
+            for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+                for (int j = 0; j < C::TN; ++j)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q)
+                        red[(((group - 1) * C::TILE_WAVES + wave) * NB + (i * C::TN + j) * 4 + q) * 64 + lane] =
+                            f32x4{acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+        }
+        __syncthreads();
+        if (group == 0) {
+            for (int g = 1; g < C::KGROUPS; ++g)
+#pragma unroll
+                for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < C::TN; ++j)
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) {
+                            const f32x4 v = red[(((g - 1) * C::TILE_WAVES + wave) * NB + (i * C::TN + j) * 4 + q) * 64 + lane];
+                            acc[i][j][4 * q] += v[0];
+                            acc[i][j][4 * q + 1] += v[1];
+                            acc[i][j][4 * q + 2] += v[2];
+                            acc[i][j][4 * q + 3] += v[3];
+                        }
+        }
+        __syncthreads();   // the partials are read before LDS is reused
+    }
+    const bool owner = group == 0;   // the waves that hold the tile's result
 
     // Epilogue constants.
     float *ep = reinterpret_cast<float *>(lds) + wave * C::EPI_WAVE_FLOATS;
@@ -351,17 +408,19 @@ void tile_kernel(Problem p, int64_t tiles_m, int64_t tiles_n, int group_m, Split
             make_rsrc(first, static_cast<uint32_t>(sk.split) * TILE_FLOATS * 4u);
         const uint32_t mine = static_cast<uint32_t>(slice) * TILE_FLOATS * 4u;
         const int wblk = wave * C::TM * C::TN;
+        if (owner) {
 #pragma unroll
-        for (int i = 0; i < C::TM; ++i)
+            for (int i = 0; i < C::TM; ++i)
 #pragma unroll
-            for (int j = 0; j < C::TN; ++j)
+                for (int j = 0; j < C::TN; ++j)
 #pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const f32x4 v = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
-                                     acc[i][j][4 * q + 3]};
-                    const uint32_t off = mine + (((wblk + i * C::TN + j) * 4 + q) * 64 + lane) * 16;
-                    __builtin_amdgcn_raw_buffer_store_b128(v, rp, off, 0, AUX_SC1);
-                }
+                    for (int q = 0; q < 4; ++q) {
+                        const f32x4 v = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
+                                         acc[i][j][4 * q + 3]};
+                        const uint32_t off = mine + (((wblk + i * C::TN + j) * 4 + q) * 64 + lane) * 16;
+                        __builtin_amdgcn_raw_buffer_store_b128(v, rp, off, 0, AUX_SC1);
+                    }
+        }
         __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));   // this wave's slice stores are complete
         __syncthreads();
         int *flag = reinterpret_cast<int *>(lds);
@@ -374,108 +433,114 @@ void tile_kernel(Problem p, int64_t tiles_m, int64_t tiles_n, int group_m, Split
         const bool last = *flag != 0;
         __syncthreads();                      // the flag is read before LDS is reused
         if (!last) return;
+        if (owner) {
 #pragma unroll
-        for (int i = 0; i < C::TM; ++i)
+            for (int i = 0; i < C::TM; ++i)
 #pragma unroll
-            for (int j = 0; j < C::TN; ++j)
+                for (int j = 0; j < C::TN; ++j)
 #pragma unroll
-                for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
-        // Small tiles: D slices per round trip (as many as 128 registers
-        // hold); a slice past the last reads out of range and is not added,
-        // so the sum still runs over the slices in order.  Large tiles
-        // (a slice fills 128 registers) go one slice at a time.
-        constexpr int NB = C::TM * C::TN * 4;
-        constexpr int D = NB * 4 >= 128 ? 1 : (128 / (NB * 4) > 8 ? 8 : 128 / (NB * 4));
-        if constexpr (D == 1) {
-            for (int t = 0; t < sk.split; ++t) {
-                const uint32_t base = static_cast<uint32_t>(t) * TILE_FLOATS * 4u;
-#pragma unroll
-                for (int i = 0; i < C::TM; ++i)
-#pragma unroll
-                    for (int j = 0; j < C::TN; ++j)
-#pragma unroll
-                        for (int q = 0; q < 4; ++q) {
-                            const uint32_t off = base + (((wblk + i * C::TN + j) * 4 + q) * 64 + lane) * 16;
-                            const f32x4 v = __builtin_bit_cast(
-                                f32x4, __builtin_amdgcn_raw_buffer_load_b128(rp, off, 0, AUX_SC1));
-                            acc[i][j][4 * q] += v[0];
-                            acc[i][j][4 * q + 1] += v[1];
-                            acc[i][j][4 * q + 2] += v[2];
-                            acc[i][j][4 * q + 3] += v[3];
-                        }
-            }
-        } else {
-            for (int t0 = 0; t0 < sk.split; t0 += D) {
-                f32x4 v[D][NB];
-#pragma unroll
-                for (int d = 0; d < D; ++d) {
-                    const uint32_t base = static_cast<uint32_t>(t0 + d) * TILE_FLOATS * 4u;
-#pragma unroll
-                    for (int b = 0; b < NB; ++b)
-                        v[d][b] = __builtin_bit_cast(
-                            f32x4, __builtin_amdgcn_raw_buffer_load_b128(rp, base + ((wblk * 4 + b) * 64 + lane) * 16,
-                                                                         0, AUX_SC1));
-                }
-#pragma unroll
-                for (int d = 0; d < D; ++d) {
-                    if (t0 + d >= sk.split) break;
+                    for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+            // Small tiles: D slices per round trip (as many as 128 registers
+            // hold); a slice past the last reads out of range and is not added,
+            // so the sum still runs over the slices in order.  Large tiles
+            // (a slice fills 128 registers) go one slice at a time.
+            constexpr int NB = C::TM * C::TN * 4;
+            constexpr int D = NB * 4 >= 128 ? 1 : (128 / (NB * 4) > 8 ? 8 : 128 / (NB * 4));
+            if constexpr (D == 1) {
+                for (int t = 0; t < sk.split; ++t) {
+                    const uint32_t base = static_cast<uint32_t>(t) * TILE_FLOATS * 4u;
 #pragma unroll
                     for (int i = 0; i < C::TM; ++i)
 #pragma unroll
                         for (int j = 0; j < C::TN; ++j)
 #pragma unroll
                             for (int q = 0; q < 4; ++q) {
-                                const f32x4 &w = v[d][(i * C::TN + j) * 4 + q];
-                                acc[i][j][4 * q] += w[0];
-                                acc[i][j][4 * q + 1] += w[1];
-                                acc[i][j][4 * q + 2] += w[2];
-                                acc[i][j][4 * q + 3] += w[3];
+                                const uint32_t off = base + (((wblk + i * C::TN + j) * 4 + q) * 64 + lane) * 16;
+                                const f32x4 v = __builtin_bit_cast(
+                                    f32x4, __builtin_amdgcn_raw_buffer_load_b128(rp, off, 0, AUX_SC1));
+                                acc[i][j][4 * q] += v[0];
+                                acc[i][j][4 * q + 1] += v[1];
+                                acc[i][j][4 * q + 2] += v[2];
+                                acc[i][j][4 * q + 3] += v[3];
                             }
+                }
+            } else {
+                for (int t0 = 0; t0 < sk.split; t0 += D) {
+                    f32x4 v[D][NB];
+#pragma unroll
+                    for (int d = 0; d < D; ++d) {
+                        const uint32_t base = static_cast<uint32_t>(t0 + d) * TILE_FLOATS * 4u;
+#pragma unroll
+                        for (int b = 0; b < NB; ++b)
+                            v[d][b] = __builtin_bit_cast(
+                                f32x4, __builtin_amdgcn_raw_buffer_load_b128(rp, base + ((wblk * 4 + b) * 64 + lane) * 16,
+                                                                             0, AUX_SC1));
+                    }
+#pragma unroll
+                    for (int d = 0; d < D; ++d) {
+                        if (t0 + d >= sk.split) break;
+#pragma unroll
+                        for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+                            for (int j = 0; j < C::TN; ++j)
+#pragma unroll
+                                for (int q = 0; q < 4; ++q) {
+                                    const f32x4 &w = v[d][(i * C::TN + j) * 4 + q];
+                                    acc[i][j][4 * q] += w[0];
+                                    acc[i][j][4 * q + 1] += w[1];
+                                    acc[i][j][4 * q + 2] += w[2];
+                                    acc[i][j][4 * q + 3] += w[3];
+                                }
+                    }
                 }
             }
         }
         if (threadIdx.x == 0)
             __hip_atomic_store(sk.counters + tile, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
-    if (vec && has_r) load_r(0, rv[0]);
+    if (owner && vec && has_r) load_r(0, rv[0]);
 #pragma unroll
     for (int i = 0; i < C::TM; ++i) {
-        if (vec && has_r && i + 1 < C::TM) load_r(i + 1, rv[(i + 1) & 1]);
+        if (owner && vec && has_r && i + 1 < C::TM) load_r(i + 1, rv[(i + 1) & 1]);
+        if (owner) {
 #pragma unroll
-        for (int j = 0; j < C::TN; ++j)
+            for (int j = 0; j < C::TN; ++j)
 #pragma unroll
-            for (int e = 0; e < 16; ++e)
-                ep[(8 * (e >> 2) + 4 * hi + (e & 3)) * C::EPI_STRIDE + j * 32 + frag_row] = acc[i][j][e];
+                for (int e = 0; e < 16; ++e)
+                    ep[(8 * (e >> 2) + 4 * hi + (e & 3)) * C::EPI_STRIDE + j * 32 + frag_row] = acc[i][j][e];
+        }
         __syncthreads();
+        if (owner) {
 #pragma unroll
-        for (int v = 0; v < PASSES; ++v) {
-            const float *src = ep + (v * C::ROWS_PER_PASS + pr) * C::EPI_STRIDE + pc;
-            float y[8];
+            for (int v = 0; v < PASSES; ++v) {
+                const float *src = ep + (v * C::ROWS_PER_PASS + pr) * C::EPI_STRIDE + pc;
+                float y[8];
 #pragma unroll
-            for (int t = 0; t < 8; ++t) y[t] = src[t];
-            const uint32_t base = base_of(i, v);
-            if (vec) {
-                if (has_r) {
+                for (int t = 0; t < 8; ++t) y[t] = src[t];
+                const uint32_t base = base_of(i, v);
+                if (vec) {
+                    if (has_r) {
 #pragma unroll
-                    for (int t = 0; t < 4; ++t) {
-                        const uint32_t w = static_cast<uint32_t>(rv[i & 1][v][t]);
-                        y[2 * t] += bf16_to_f32(static_cast<uint16_t>(w & 0xffffu));
-                        y[2 * t + 1] += bf16_to_f32(static_cast<uint16_t>(w >> 16));
+                        for (int t = 0; t < 4; ++t) {
+                            const uint32_t w = static_cast<uint32_t>(rv[i & 1][v][t]);
+                            y[2 * t] += bf16_to_f32(static_cast<uint16_t>(w & 0xffffu));
+                            y[2 * t + 1] += bf16_to_f32(static_cast<uint16_t>(w >> 16));
+                        }
                     }
-                }
-                i32x4 out;
+                    i32x4 out;
 #pragma unroll
-                for (int t = 0; t < 4; ++t) out[t] = static_cast<int>(f32x2_to_bf16x2_rne(y[2 * t], y[2 * t + 1]));
-                __builtin_amdgcn_raw_buffer_store_b128(out, ry, col0 < N ? base : OOB_OFFSET, 0, 0);
-            } else {
-                uint16_t rs[8];
-                const int cols = static_cast<int>(N - col0);   // columns of this lane's 8 that exist
+                    for (int t = 0; t < 4; ++t) out[t] = static_cast<int>(f32x2_to_bf16x2_rne(y[2 * t], y[2 * t + 1]));
+                    __builtin_amdgcn_raw_buffer_store_b128(out, ry, col0 < N ? base : OOB_OFFSET, 0, 0);
+                } else {
+                    uint16_t rs[8];
+                    const int cols = static_cast<int>(N - col0);   // columns of this lane's 8 that exist
 #pragma unroll
-                for (int t = 0; t < 8; ++t) rs[t] = __builtin_amdgcn_raw_buffer_load_b16(rr, t < cols ? base + 2 * t : OOB_OFFSET, 0, 0);
+                    for (int t = 0; t < 8; ++t) rs[t] = __builtin_amdgcn_raw_buffer_load_b16(rr, t < cols ? base + 2 * t : OOB_OFFSET, 0, 0);
 #pragma unroll
-                for (int t = 0; t < 8; ++t) {
-                    const float yt = has_r ? y[t] + bf16_to_f32(rs[t]) : y[t];
-                    __builtin_amdgcn_raw_buffer_store_b16(f32_to_bf16_rne(yt), ry, t < cols ? base + 2 * t : OOB_OFFSET, 0, 0);
+                    for (int t = 0; t < 8; ++t) {
+                        const float yt = has_r ? y[t] + bf16_to_f32(rs[t]) : y[t];
+                        __builtin_amdgcn_raw_buffer_store_b16(f32_to_bf16_rne(yt), ry, t < cols ? base + 2 * t : OOB_OFFSET, 0, 0);
+                    }
                 }
             }
         }
@@ -525,6 +590,9 @@ using C64x64k64s4 = Cfg<64, 64, 64, 2, 2, 4, 2>;
 using C128x128k32s4 = Cfg<128, 128, 32, 2, 2, 4, 2>;
 using C64x64k64s8 = Cfg<64, 64, 64, 2, 2, 8, 1>;
 using C64x128k64s4 = Cfg<64, 128, 64, 2, 2, 4, 1>;
+using C64x64k128g2 = Cfg<64, 64, 128, 2, 2, 2, 2, 2>;
+using C128x128k64g2 = Cfg<128, 128, 64, 2, 2, 2, 2, 2>;
+using C64x64k64g4 = Cfg<64, 64, 64, 2, 2, 2, 4, 4>;
 
 template <class C>
 constexpr TileShape shape_of(int per_cu) { return TileShape{C::BM, C::BN, C::BK, per_cu}; }
@@ -552,6 +620,9 @@ TileShape tile_shape(int cfg) {
         case TC_128x128_K32_S4_W4: return shape_of<C128x128k32s4>(2);
         case TC_64x64_K64_S8_W4: return shape_of<C64x64k64s8>(1);
         case TC_64x128_K64_S4_W4: return shape_of<C64x128k64s4>(1);
+        case TC_64x64_K128_S2_G2: return shape_of<C64x64k128g2>(1);
+        case TC_128x128_K64_S2_G2: return shape_of<C128x128k64g2>(1);
+        case TC_64x64_K64_S2_G4: return shape_of<C64x64k64g4>(1);
         default: return TileShape{0, 0, 0, 0};
     }
 }
@@ -579,6 +650,9 @@ hipError_t launch_tile(int cfg, const Problem &p, int split, const Workspace *ws
         case TC_128x128_K32_S4_W4: return launch_cfg<C128x128k32s4>(p, 8, split, ws, s);
         case TC_64x64_K64_S8_W4: return launch_cfg<C64x64k64s8>(p, 8, split, ws, s);
         case TC_64x128_K64_S4_W4: return launch_cfg<C64x128k64s4>(p, 8, split, ws, s);
+        case TC_64x64_K128_S2_G2: return launch_cfg<C64x64k128g2>(p, 8, split, ws, s);
+        case TC_128x128_K64_S2_G2: return launch_cfg<C128x128k64g2>(p, 8, split, ws, s);
+        case TC_64x64_K64_S2_G4: return launch_cfg<C64x64k64g4>(p, 8, split, ws, s);
         default: return hipErrorInvalidValue;
     }
 }
