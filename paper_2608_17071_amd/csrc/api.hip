@@ -47,7 +47,8 @@ struct PlanInfo {
     const char *name;
     PlanKind kind;
     int tile_cfg;   // TileCfg for tile plans, K depth (BK) for stream plans, -1 otherwise
-    int split;      // tile and stream plans: 1 = no split-K, 0 = split-K by rule
+    int split;      // tile and stream plans: 1 = no split-K, 0 = split-K by rule,
+                    // -1 (tile) = split only the tiles of a partial last round
 };
 
 const PlanInfo PLANS[] = {
@@ -100,6 +101,9 @@ const PlanInfo PLANS[] = {
     {"tile_128x128_k64_g2_splitk", KIND_TILE, TC_128x128_K64_S2_G2, 0},
     {"tile_64x64_k64_g4", KIND_TILE, TC_64x64_K64_S2_G4, 1},
     {"tile_64x64_k64_g4_splitk", KIND_TILE, TC_64x64_K64_S2_G4, 0},
+    {"tile_128x128_k64_w4_tailsplit", KIND_TILE, TC_128x128_K64_S2_W4, -1},
+    {"tile_256x256_k64_w8_tailsplit", KIND_TILE, TC_256x256_K64_S2_W8, -1},
+    {"tile_256x128_k64_w8_tailsplit", KIND_TILE, TC_256x128_K64_S2_W8, -1},
     {"stream_mfma16_k128", KIND_STREAM, 128, 1},
     {"stream_mfma16_k128_splitk", KIND_STREAM, 128, 0},
     {"stream_mfma16_k64_splitk", KIND_STREAM, 64, 0},
@@ -119,19 +123,39 @@ int64_t tile_count(const TileShape &ts, int64_t M, int64_t N) { return cdiv(M, t
 // Split-K rule of the "_splitk" tile plans: enough K slices that the tiles
 // fill one round of workgroup slots on the 256 CUs, each slice at least 8
 // BK steps deep; at least 2 so the plan always exercises the reduction.
-int tile_split_of(int plan, int64_t M, int64_t N, int64_t K) {
+// "_tailsplit" plans: the tiles that fill whole rounds run whole and the
+// rest are split so that they fill the last round (each XCD must get equal
+// shares of both kinds of work, else no split).
+struct TileSplit {
+    int split;
+    int64_t full_tiles;   // > 0: tail split
+};
+
+TileSplit tile_split_plan(int plan, int64_t M, int64_t N, int64_t K) {
     const PlanInfo &pi = PLANS[plan];
-    if (pi.split >= 1) return pi.split;
+    if (pi.split >= 1) return {pi.split, 0};
     const TileShape ts = tile_shape(pi.tile_cfg);
     const int64_t tiles = tile_count(ts, M, N);
     const int64_t slots = CUS * ts.workgroups_per_cu;
+    if (pi.split < 0) {
+        const int64_t full = (tiles / slots) * slots, rest = tiles - full;
+        if (full == 0 || rest == 0) return {1, 0};
+        int64_t split = slots / rest;
+        const int64_t by_depth = K / (4 * ts.bk);
+        if (split > by_depth) split = by_depth;
+        if (split > MAX_SPLIT) split = MAX_SPLIT;
+        if (split < 2 || full % 8 != 0 || (rest * split) % 8 != 0) return {1, 0};
+        return {static_cast<int>(split), full};
+    }
     int64_t split = tiles > 0 ? slots / tiles : 1;
     const int64_t by_depth = K / (8 * ts.bk);
     if (split > by_depth) split = by_depth;
     if (split > MAX_SPLIT) split = MAX_SPLIT;
     if (split < 2) split = 2;
-    return static_cast<int>(split);
+    return {static_cast<int>(split), 0};
 }
+
+int tile_split_of(int plan, int64_t M, int64_t N, int64_t K) { return tile_split_plan(plan, M, N, K).split; }
 
 // Split-K of the stream plans: the kernel's rule, at least 2 for the
 // "_splitk" plans so they always exercise the reduction.
@@ -178,9 +202,11 @@ bool supports(int plan, int64_t M, int64_t N, int64_t K, bool residual) {
             if (int64_t{ts.bm} * K * 2 >= PANEL_LIMIT || int64_t{ts.bn} * K * 2 >= PANEL_LIMIT) return false;
             if (int64_t{ts.bm} * N * 2 >= PANEL_LIMIT) return false;   // epilogue panel of R / Y
             const int64_t tiles = tile_count(ts, M, N);
-            const int split = tile_split_of(plan, M, N, K);
-            if (tiles * split * 512 > LIMIT_ITEMS) return false;
-            if (split > 1 && (tiles * split * ts.bm * ts.bn > WS_PARTIAL_FLOATS || tiles > WS_COUNTERS))
+            const TileSplit sp = tile_split_plan(plan, M, N, K);
+            const int64_t split_tiles = tiles - sp.full_tiles;
+            if ((sp.full_tiles + split_tiles * sp.split) * 1024 > LIMIT_ITEMS) return false;
+            if (sp.split > 1 &&
+                (split_tiles * sp.split * ts.bm * ts.bn > WS_PARTIAL_FLOATS || split_tiles > WS_COUNTERS))
                 return false;
             return true;
         }
@@ -218,7 +244,7 @@ const TableEntry TABLE[] = {
     {512, 8192, 8192, 1, "tile_128x128_k64_w4_splitk"},
     {4096, 2048, 2048, 1, "tile_128x128_k64_w4"},
     {4096, 4096, 4096, 1, "tile_256x256_k64_w8"},
-    {4096, 5120, 5120, 1, "tile_128x128_k64_w4"},
+    {4096, 5120, 5120, 1, "tile_256x256_k64_w8_tailsplit"},
     {4096, 8192, 8192, 1, "tile_256x256_k64_w8"},
     // plain BF16 GEMM
     {8192, 8192, 8192, 0, "tile_256x256_k64_w8"},
@@ -257,7 +283,7 @@ int select(int64_t M, int64_t N, int64_t K, bool residual) {
         if (plan < 0) plan = pick("tile_128x128_k64_w4_splitk");
     } else {
         const TileShape big = tile_shape(TC_256x256_K64_S2_W8);
-        if (tile_count(big, M, N) >= CUS) plan = pick("tile_256x256_k64_w8");
+        if (tile_count(big, M, N) >= CUS) plan = pick("tile_256x256_k64_w8_tailsplit");
         if (plan < 0) plan = pick("tile_128x128_k64_w4");
     }
     if (plan < 0) plan = pick("tile_128x128_k64_w4");
@@ -400,13 +426,13 @@ int run(int plan, int64_t M, int64_t N, int64_t K, const void *X, const void *W,
             e = launch_gemv(p, stream);
             break;
         case KIND_TILE: {
-            const int split = tile_split_of(plan, M, N, K);
+            const TileSplit sp = tile_split_plan(plan, M, N, K);
             Workspace ws{};
-            if (split > 1) {
+            if (sp.split > 1) {
                 const int wst = workspace(dev, stream, &ws);
                 if (wst != KERNELARC_OK) return wst;
             }
-            e = launch_tile(PLANS[plan].tile_cfg, p, split, split > 1 ? &ws : nullptr, stream);
+            e = launch_tile(PLANS[plan].tile_cfg, p, sp.split, sp.full_tiles, sp.split > 1 ? &ws : nullptr, stream);
             break;
         }
         case KIND_STREAM: {

@@ -72,7 +72,9 @@ struct Workspace {
 hipError_t launch_generic(const Problem &p, hipStream_t s);
 hipError_t launch_gemv(const Problem &p, hipStream_t s);
 hipError_t launch_skinny(const Problem &p, int split_k, const Workspace *ws, hipStream_t s);
-hipError_t launch_tile(int cfg, const Problem &p, int split, const Workspace *ws, hipStream_t s);
+// full_tiles > 0 with split > 1: tiles past the first full_tiles (band
+// order) are split in K, the others run whole (see kernel_tile.hip).
+hipError_t launch_tile(int cfg, const Problem &p, int split, int64_t full_tiles, const Workspace *ws, hipStream_t s);
 hipError_t launch_stream(const Problem &p, int bk, int split, const Workspace *ws, hipStream_t s);
 
 // Shape rules of the kernels, used by the plan table (host only).

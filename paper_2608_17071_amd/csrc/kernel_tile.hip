@@ -184,10 +184,14 @@ __device__ __forceinline__ void schedule_k_step() {
 
 // Split-K bookkeeping of one launch (split == 1: none).
 struct SplitK {
-    int split;          // K slices per output tile
+    int split;          // K slices per split tile (1: none)
     int64_t kslice;     // slice length, a multiple of BK
-    float *partials;    // [tile][slice][BM*BN] fp32, fragment order
-    unsigned *counters; // one arrival counter per tile, zero between calls
+    float *partials;    // [split tile][slice][BM*BN] fp32, fragment order
+    unsigned *counters; // one arrival counter per split tile, zero between calls
+    // Tail split: tiles [0, full_tiles) of the band order run whole and only
+    // the rest are split (0: every tile is split when split > 1).  Used when
+    // whole rounds of workgroups leave a partial last round.
+    int64_t full_tiles;
 };
 
 template <class C>
@@ -202,17 +206,36 @@ void tile_kernel(Problem p, int64_t tiles_m, int64_t tiles_n, int group_m, Split
     const int wave = wave_id - group * C::TILE_WAVES;       // wave within the tile
     char *const glds = lds + group * C::GROUP_BYTES;        // this group's LDS ring
 
-    // Workgroup -> (K slice, tile): the XCD remap runs over slice-major ids,
-    // so each XCD takes neighbouring tiles of one slice.
+    // Workgroup -> (K slice, tile).  Workgroups go to the 8 XCDs round-robin;
+    // each XCD takes a contiguous range of work (slice-major ids), walked in
+    // GROUP_M-row bands.  With a tail split each XCD takes an equal share of
+    // the whole tiles first and then an equal share of the tail pieces.
     const int64_t tiles = tiles_m * tiles_n;
     int64_t tm, tn, slice, tile;
+    bool piece;   // a K slice of a split tile
     {
-        const int64_t T = tiles * sk.split;
-        const int64_t per = T / XCDS, rem = T % XCDS;
         const int64_t x = blockIdx.x % XCDS, local = blockIdx.x / XCDS;
-        const int64_t logical = x * per + (x < rem ? x : rem) + local;
-        slice = logical / tiles;
-        tile = logical - slice * tiles;
+        if (sk.split > 1 && sk.full_tiles > 0) {
+            const int64_t rest = tiles - sk.full_tiles;
+            const int64_t f8 = sk.full_tiles / XCDS, p8 = rest * sk.split / XCDS;
+            if (local < f8) {
+                tile = x * f8 + local;
+                slice = 0;
+                piece = false;
+            } else {
+                const int64_t q = x * p8 + (local - f8);
+                slice = q / rest;
+                tile = sk.full_tiles + (q - slice * rest);
+                piece = true;
+            }
+        } else {
+            const int64_t T = tiles * sk.split;
+            const int64_t per = T / XCDS, rem = T % XCDS;
+            const int64_t logical = x * per + (x < rem ? x : rem) + local;
+            slice = logical / tiles;
+            tile = logical - slice * tiles;
+            piece = sk.split > 1;
+        }
         const int64_t band = static_cast<int64_t>(group_m) * tiles_n;
         const int64_t g = tile / band;
         const int64_t first_m = g * group_m;
@@ -225,8 +248,8 @@ void tile_kernel(Problem p, int64_t tiles_m, int64_t tiles_n, int group_m, Split
     const int64_t n0 = tn * C::BN;
     const int64_t K = p.K;
     // This workgroup's K range [kbeg, kend); loads at or past kend read zero.
-    const int64_t kbeg = slice * sk.kslice;
-    const int64_t kend = (kbeg + sk.kslice) < K ? (kbeg + sk.kslice) : K;
+    const int64_t kbeg = piece ? slice * sk.kslice : 0;
+    const int64_t kend = piece ? ((kbeg + sk.kslice) < K ? (kbeg + sk.kslice) : K) : K;
 
     // Operand panels bounded by buffer resources: rows past M (N) read 0.
     const int64_t rows_a = (p.M - m0) < C::BM ? (p.M - m0) : C::BM;
@@ -393,7 +416,7 @@ void tile_kernel(Problem p, int64_t tiles_m, int64_t tiles_n, int group_m, Split
     // staged and stored, so only slab 0's latency is exposed.
     i32x4 rv[2][PASSES];
 
-    if (sk.split > 1) {
+    if (piece) {
         // Publish this slice's fp32 tile in fragment order (each store
         // instruction writes 1 KB contiguous) with device-scope (sc1)
         // stores, which write through the XCD's L2; once they have
@@ -403,7 +426,8 @@ void tile_kernel(Problem p, int64_t tiles_m, int64_t tiles_n, int group_m, Split
         // partial tiles cross workgroups, and only through these accesses,
         // so no L2-wide write-back or invalidate is needed.
         constexpr int TILE_FLOATS = C::BM * C::BN;
-        const float *first = sk.partials + tile * sk.split * TILE_FLOATS;
+        const int64_t stile = tile - sk.full_tiles;   // index among the split tiles
+        const float *first = sk.partials + stile * sk.split * TILE_FLOATS;
         const __amdgpu_buffer_rsrc_t rp =
             make_rsrc(first, static_cast<uint32_t>(sk.split) * TILE_FLOATS * 4u);
         const uint32_t mine = static_cast<uint32_t>(slice) * TILE_FLOATS * 4u;
@@ -425,7 +449,7 @@ void tile_kernel(Problem p, int64_t tiles_m, int64_t tiles_n, int group_m, Split
         __syncthreads();
         int *flag = reinterpret_cast<int *>(lds);
         if (threadIdx.x == 0) {
-            const unsigned prev = __hip_atomic_fetch_add(sk.counters + tile, 1u, __ATOMIC_RELAXED,
+            const unsigned prev = __hip_atomic_fetch_add(sk.counters + stile, 1u, __ATOMIC_RELAXED,
                                                          __HIP_MEMORY_SCOPE_AGENT);
             *flag = prev == static_cast<unsigned>(sk.split - 1);
         }
@@ -496,7 +520,7 @@ void tile_kernel(Problem p, int64_t tiles_m, int64_t tiles_n, int group_m, Split
             }
         }
         if (threadIdx.x == 0)
-            __hip_atomic_store(sk.counters + tile, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(sk.counters + stile, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
     if (owner && vec && has_r) load_r(0, rv[0]);
 #pragma unroll
@@ -549,19 +573,26 @@ void tile_kernel(Problem p, int64_t tiles_m, int64_t tiles_n, int group_m, Split
 }
 
 template <class C>
-hipError_t launch_cfg(const Problem &p, int group_m, int split, const Workspace *ws, hipStream_t s) {
+hipError_t launch_cfg(const Problem &p, int group_m, int split, int64_t full_tiles, const Workspace *ws,
+                      hipStream_t s) {
     const int64_t tiles_m = (p.M + C::BM - 1) / C::BM;
     const int64_t tiles_n = (p.N + C::BN - 1) / C::BN;
     const int64_t tiles = tiles_m * tiles_n;
-    SplitK sk{1, ((p.K + C::BK - 1) / C::BK) * C::BK, nullptr, nullptr};
+    SplitK sk{1, ((p.K + C::BK - 1) / C::BK) * C::BK, nullptr, nullptr, 0};
     if (split > 1) {
         sk.split = split;
         sk.kslice = (((p.K + split - 1) / split + C::BK - 1) / C::BK) * C::BK;
         sk.partials = ws->partials;
         sk.counters = ws->counters;
+        sk.full_tiles = full_tiles;
+        // the tail mapping hands the XCDs equal shares of both kinds of work
+        if (full_tiles > 0 && (full_tiles >= tiles || full_tiles % XCDS != 0 ||
+                               ((tiles - full_tiles) * split) % XCDS != 0))
+            return hipErrorInvalidValue;
     }
-    hipLaunchKernelGGL(tile_kernel<C>, dim3(static_cast<unsigned>(tiles * sk.split)), dim3(C::THREADS), 0, s,
-                       p, tiles_m, tiles_n, group_m, sk);
+    const int64_t wgs = sk.full_tiles + (tiles - sk.full_tiles) * sk.split;
+    hipLaunchKernelGGL(tile_kernel<C>, dim3(static_cast<unsigned>(wgs)), dim3(C::THREADS), 0, s, p, tiles_m,
+                       tiles_n, group_m, sk);
     return hipGetLastError();
 }
 
@@ -627,32 +658,33 @@ TileShape tile_shape(int cfg) {
     }
 }
 
-hipError_t launch_tile(int cfg, const Problem &p, int split, const Workspace *ws, hipStream_t s) {
+hipError_t launch_tile(int cfg, const Problem &p, int split, int64_t full_tiles, const Workspace *ws,
+                       hipStream_t s) {
     switch (cfg) {
-        case TC_256x256_K64_S2_W8: return launch_cfg<C256x256w8>(p, 8, split, ws, s);
-        case TC_256x256_K64_S2_W4: return launch_cfg<C256x256w4>(p, 8, split, ws, s);
-        case TC_256x128_K64_S2_W8: return launch_cfg<C256x128w8>(p, 8, split, ws, s);
-        case TC_128x256_K64_S2_W8: return launch_cfg<C128x256w8>(p, 8, split, ws, s);
-        case TC_256x128_K64_S2_W4: return launch_cfg<C256x128w4>(p, 8, split, ws, s);
-        case TC_128x128_K64_S2_W4: return launch_cfg<C128x128w4>(p, 8, split, ws, s);
-        case TC_64x256_K64_S2_W4: return launch_cfg<C64x256w4>(p, 8, split, ws, s);
-        case TC_128x128_K64_S4_W4: return launch_cfg<C128x128s4>(p, 8, split, ws, s);
-        case TC_128x128_K64_S3_W4: return launch_cfg<C128x128s3>(p, 8, split, ws, s);
-        case TC_64x256_K64_S3_W4: return launch_cfg<C64x256s3>(p, 8, split, ws, s);
-        case TC_256x128_K64_S3_W8: return launch_cfg<C256x128s3w8>(p, 8, split, ws, s);
-        case TC_64x64_K64_S2_W4: return launch_cfg<C64x64w4>(p, 8, split, ws, s);
-        case TC_64x128_K64_S2_W4: return launch_cfg<C64x128w4>(p, 8, split, ws, s);
-        case TC_64x64_K128_S2_W4: return launch_cfg<C64x64k128>(p, 8, split, ws, s);
-        case TC_128x128_K128_S2_W4: return launch_cfg<C128x128k128>(p, 8, split, ws, s);
-        case TC_64x128_K128_S2_W4: return launch_cfg<C64x128k128>(p, 8, split, ws, s);
-        case TC_64x64_K128_S3_W4: return launch_cfg<C64x64k128s3>(p, 8, split, ws, s);
-        case TC_64x64_K64_S4_W4: return launch_cfg<C64x64k64s4>(p, 8, split, ws, s);
-        case TC_128x128_K32_S4_W4: return launch_cfg<C128x128k32s4>(p, 8, split, ws, s);
-        case TC_64x64_K64_S8_W4: return launch_cfg<C64x64k64s8>(p, 8, split, ws, s);
-        case TC_64x128_K64_S4_W4: return launch_cfg<C64x128k64s4>(p, 8, split, ws, s);
-        case TC_64x64_K128_S2_G2: return launch_cfg<C64x64k128g2>(p, 8, split, ws, s);
-        case TC_128x128_K64_S2_G2: return launch_cfg<C128x128k64g2>(p, 8, split, ws, s);
-        case TC_64x64_K64_S2_G4: return launch_cfg<C64x64k64g4>(p, 8, split, ws, s);
+        case TC_256x256_K64_S2_W8: return launch_cfg<C256x256w8>(p, 8, split, full_tiles, ws, s);
+        case TC_256x256_K64_S2_W4: return launch_cfg<C256x256w4>(p, 8, split, full_tiles, ws, s);
+        case TC_256x128_K64_S2_W8: return launch_cfg<C256x128w8>(p, 8, split, full_tiles, ws, s);
+        case TC_128x256_K64_S2_W8: return launch_cfg<C128x256w8>(p, 8, split, full_tiles, ws, s);
+        case TC_256x128_K64_S2_W4: return launch_cfg<C256x128w4>(p, 8, split, full_tiles, ws, s);
+        case TC_128x128_K64_S2_W4: return launch_cfg<C128x128w4>(p, 8, split, full_tiles, ws, s);
+        case TC_64x256_K64_S2_W4: return launch_cfg<C64x256w4>(p, 8, split, full_tiles, ws, s);
+        case TC_128x128_K64_S4_W4: return launch_cfg<C128x128s4>(p, 8, split, full_tiles, ws, s);
+        case TC_128x128_K64_S3_W4: return launch_cfg<C128x128s3>(p, 8, split, full_tiles, ws, s);
+        case TC_64x256_K64_S3_W4: return launch_cfg<C64x256s3>(p, 8, split, full_tiles, ws, s);
+        case TC_256x128_K64_S3_W8: return launch_cfg<C256x128s3w8>(p, 8, split, full_tiles, ws, s);
+        case TC_64x64_K64_S2_W4: return launch_cfg<C64x64w4>(p, 8, split, full_tiles, ws, s);
+        case TC_64x128_K64_S2_W4: return launch_cfg<C64x128w4>(p, 8, split, full_tiles, ws, s);
+        case TC_64x64_K128_S2_W4: return launch_cfg<C64x64k128>(p, 8, split, full_tiles, ws, s);
+        case TC_128x128_K128_S2_W4: return launch_cfg<C128x128k128>(p, 8, split, full_tiles, ws, s);
+        case TC_64x128_K128_S2_W4: return launch_cfg<C64x128k128>(p, 8, split, full_tiles, ws, s);
+        case TC_64x64_K128_S3_W4: return launch_cfg<C64x64k128s3>(p, 8, split, full_tiles, ws, s);
+        case TC_64x64_K64_S4_W4: return launch_cfg<C64x64k64s4>(p, 8, split, full_tiles, ws, s);
+        case TC_128x128_K32_S4_W4: return launch_cfg<C128x128k32s4>(p, 8, split, full_tiles, ws, s);
+        case TC_64x64_K64_S8_W4: return launch_cfg<C64x64k64s8>(p, 8, split, full_tiles, ws, s);
+        case TC_64x128_K64_S4_W4: return launch_cfg<C64x128k64s4>(p, 8, split, full_tiles, ws, s);
+        case TC_64x64_K128_S2_G2: return launch_cfg<C64x64k128g2>(p, 8, split, full_tiles, ws, s);
+        case TC_128x128_K64_S2_G2: return launch_cfg<C128x128k64g2>(p, 8, split, full_tiles, ws, s);
+        case TC_64x64_K64_S2_G4: return launch_cfg<C64x64k64g4>(p, 8, split, full_tiles, ws, s);
         default: return hipErrorInvalidValue;
     }
 }

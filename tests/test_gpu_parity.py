@@ -140,6 +140,35 @@ def test_closed_forms_bitwise_every_plan(ka, plan):
                                   orc.round_bf16(exact1 + bf16_bits_to_f64(wl.bits(R1)) + 0.0))
 
 
+# Shapes where the tail-split plans split only the tiles of a partial last
+# round: (plan, M, N, K).  Each is checked to really take that path.
+TAIL_SPLIT_CASES = [("tile_128x128_k64_w4_tailsplit", 2048, 4224, 1024),    # 528 tiles, 512 slots
+                    ("tile_256x256_k64_w8_tailsplit", 2048, 8448, 1024),    # 264 tiles, 256 slots
+                    ("tile_256x128_k64_w8_tailsplit", 2048, 8448, 1040)]    # 528 tiles, K tail
+
+
+@pytest.mark.parametrize("case", TAIL_SPLIT_CASES, ids=[c[0] for c in TAIL_SPLIT_CASES])
+def test_tail_split_whole_output(ka, case):
+    plan, M, N, K = case
+    p = plan_id(ka, plan)
+    assert ka.kernelarc_plan_uses_workspace(p, M, N, K) == 1, "the tail tiles must be split"
+    orc = oracle.default()
+    # every element bitwise, through rank-1 integer inputs
+    gu.note(f"{plan} tail split rank-1 M={M} N={N} K={K}")
+    X1, W1, R1, a, b, u, v = wl.rank1_integer(M, N, K, seed=7)
+    exact1 = (np.outer(a, b) * int(np.dot(u, v))).astype(np.float64) + 0.0
+    y = gu.run_library(X1, W1, R1, plan=p)
+    np.testing.assert_array_equal(_unsigned_zero(y), orc.round_bf16(exact1 + bf16_bits_to_f64(wl.bits(R1)) + 0.0))
+    # random inputs: whole sampled rows and columns against the oracle, and
+    # the same bits on a second call
+    gu.note(f"{plan} tail split random M={M} N={N} K={K}")
+    t = wl.make_inputs(wl.custom(M, N, K, seed=12))
+    y1 = gu.run_library(t["X"], t["W"], t["R"], plan=p)
+    pos = gu.sample_positions(M, N, seed=12)
+    gu.check_tolerance(y1[pos[0], pos[1]], gu.oracle_reference(t["X"], t["W"], t["R"], pos), plan)
+    np.testing.assert_array_equal(gu.run_library(t["X"], t["W"], t["R"], plan=p), y1)
+
+
 @pytest.mark.parametrize("plan", sorted(PLAN_SHAPES))
 def test_deterministic_and_row_permutation(ka, plan):
     p = plan_id(ka, plan)
@@ -233,7 +262,8 @@ def test_graph_replay_matches_eager(ka):
              ("gemv_valu_w4", (1, 4096, 4096)),
              ("tile_128x128_k64_w4_splitk", (512, 1024, 2048)), ("tile_256x256_k64_w8", (300, 520, 264)),
              ("tile_64x256_k64_w4_splitk", (64, 768, 4096)), ("stream_mfma16_k128_splitk", (64, 1024, 4096)),
-             ("stream_mfma16_k64_splitk", (16, 2048, 2048))]
+             ("stream_mfma16_k64_splitk", (16, 2048, 2048)),
+             ("tile_128x128_k64_w4_tailsplit", (2048, 4224, 1024))]
     for name, (M, N, K) in cases:
         p = plan_id(ka, name)
         t = wl.make_inputs(wl.custom(M, N, K, seed=21))
