@@ -253,10 +253,11 @@ const TableEntry TABLE[] = {
 
 // Rule-based choice when no table entry matches (from the same
 // measurements): the VALU GEMV up to 4 rows; the streaming kernel with
-// split-K up to 32 rows; up to 1024 rows a 64x64 tile with K depth 128 while it
-// makes at most two tiles per 128 KB LDS pair of slots (split-K when that
-// leaves CUs idle), else a 128x128 tile with split-K; above that the 256x256
-// 8-wave tile when it fills the 256 CUs, else the 128x128 tile.
+// split-K up to 32 rows; up to 1024 rows a 64x64 tile with K depth 128 while
+// its tiles fit two per CU (split-K when they leave CUs idle), else a
+// 128x128 tile with split-K; above that the 256x256 8-wave tile when it fills
+// the 256 CUs (tail split: the tiles of a partial last round are split in K),
+// else the 128x128 tile.
 int select(int64_t M, int64_t N, int64_t K, bool residual) {
     if (M < 0 || N < 0 || K < 0) return -1;
     for (const TableEntry &e : TABLE) {
