@@ -104,6 +104,10 @@ const PlanInfo PLANS[] = {
     {"tile_128x128_k64_w4_tailsplit", KIND_TILE, TC_128x128_K64_S2_W4, -1},
     {"tile_256x256_k64_w8_tailsplit", KIND_TILE, TC_256x256_K64_S2_W8, -1},
     {"tile_256x128_k64_w8_tailsplit", KIND_TILE, TC_256x128_K64_S2_W8, -1},
+    {"tile_256x128_k64s3_w8_lag", KIND_TILE, TC_256x128_K64_S3_W8_L, 1},
+    {"tile_256x128_k64s3_w8_lag_splitk", KIND_TILE, TC_256x128_K64_S3_W8_L, 0},
+    {"tile_128x128_k64s4_w4_lag", KIND_TILE, TC_128x128_K64_S4_W4_L, 1},
+    {"tile_128x128_k64s4_w4_lag_splitk", KIND_TILE, TC_128x128_K64_S4_W4_L, 0},
     {"stream_mfma16_k128", KIND_STREAM, 128, 1},
     {"stream_mfma16_k128_splitk", KIND_STREAM, 128, 0},
     {"stream_mfma16_k64_splitk", KIND_STREAM, 64, 0},
@@ -234,15 +238,15 @@ const TableEntry TABLE[] = {
     {1, 5120, 5120, 1, "gemv_valu_w4"},
     {1, 8192, 8192, 1, "gemv_valu_w4"},
     {16, 4096, 4096, 1, "stream_mfma16_k64_splitk"},
-    {64, 2048, 2048, 1, "stream_mfma16_k128_splitk"},
-    {64, 4096, 4096, 1, "tile_64x64_k128_g2_splitk"},
-    {64, 5120, 5120, 1, "tile_64x64_k128_w4_splitk"},
-    {64, 8192, 8192, 1, "tile_64x64_k64_g4_splitk"},
-    {512, 2048, 2048, 1, "tile_64x64_k128_g2"},
-    {512, 4096, 4096, 1, "tile_128x128_k64_g2_splitk"},
-    {512, 5120, 5120, 1, "tile_128x128_k64_w4_splitk"},
-    {512, 8192, 8192, 1, "tile_128x128_k64_w4_splitk"},
-    {4096, 2048, 2048, 1, "tile_128x128_k64_w4"},
+    {64, 2048, 2048, 1, "tile_64x64_k64s4_w4_splitk"},
+    {64, 4096, 4096, 1, "tile_64x64_k128s3_w4_splitk"},
+    {64, 5120, 5120, 1, "tile_64x64_k128s3_w4_splitk"},
+    {64, 8192, 8192, 1, "tile_64x64_k128s3_w4_splitk"},
+    {512, 2048, 2048, 1, "tile_64x64_k64s4_w4"},
+    {512, 4096, 4096, 1, "tile_128x128_k64s3_w4_splitk"},
+    {512, 5120, 5120, 1, "tile_256x128_k64s3_w8_splitk"},
+    {512, 8192, 8192, 1, "tile_128x128_k64s4_w4_lag"},
+    {4096, 2048, 2048, 1, "tile_256x128_k64s3_w8_lag"},
     {4096, 4096, 4096, 1, "tile_256x256_k64_w8"},
     {4096, 5120, 5120, 1, "tile_256x256_k64_w8_tailsplit"},
     {4096, 8192, 8192, 1, "tile_256x256_k64_w8"},
@@ -253,11 +257,14 @@ const TableEntry TABLE[] = {
 
 // Rule-based choice when no table entry matches (from the same
 // measurements): the VALU GEMV up to 4 rows; the streaming kernel with
-// split-K up to 32 rows; up to 1024 rows a 64x64 tile with K depth 128 while
-// its tiles fit two per CU (split-K when they leave CUs idle), else a
-// 128x128 tile with split-K; above that the 256x256 8-wave tile when it fills
-// the 256 CUs (tail split: the tiles of a partial last round are split in K),
-// else the 128x128 tile.
+// split-K up to 32 rows; up to 1024 rows: 64x64 tiles (3 stages of K depth
+// 128, split-K) while they fill at most half the CUs, 64x64 tiles (4 stages
+// of depth 64, two per CU) while they fit one round, else 128x128 tiles
+// (3 stages with split-K when at most half the CUs would be busy, else 4
+// stages with the lagged refill); above that the 256x256 8-wave tile when it
+// fills the 256 CUs (tail split: the tiles of a partial last round are split
+// in K), the 256x128 8-wave tile (3 stages, lagged refill) when that fills
+// them, else the 128x128 tile.
 int select(int64_t M, int64_t N, int64_t K, bool residual) {
     if (M < 0 || N < 0 || K < 0) return -1;
     for (const TableEntry &e : TABLE) {
@@ -277,14 +284,16 @@ int select(int64_t M, int64_t N, int64_t K, bool residual) {
         plan = pick("stream_mfma16_k64_splitk");
         if (plan < 0) plan = pick("skinny_mfma16_w8");
     } else if (M <= 1024) {
-        const TileShape small = tile_shape(TC_64x64_K128_S2_W4);
-        const int64_t tiles = tile_count(small, M, N), slots = CUS * small.workgroups_per_cu;
-        if (2 * tiles <= slots) plan = pick("tile_64x64_k128_w4_splitk");
-        else if (tiles <= slots) plan = pick("tile_64x64_k128_w4");
+        const int64_t tiles64 = tile_count(tile_shape(TC_64x64_K64_S4_W4), M, N);
+        const int64_t tiles128 = tile_count(tile_shape(TC_128x128_K64_S4_W4_L), M, N);
+        if (2 * tiles64 <= CUS) plan = pick("tile_64x64_k128s3_w4_splitk");
+        else if (tiles64 <= 2 * CUS) plan = pick("tile_64x64_k64s4_w4");
+        else if (2 * tiles128 <= CUS) plan = pick("tile_128x128_k64s3_w4_splitk");
+        else plan = pick("tile_128x128_k64s4_w4_lag");
         if (plan < 0) plan = pick("tile_128x128_k64_w4_splitk");
     } else {
-        const TileShape big = tile_shape(TC_256x256_K64_S2_W8);
-        if (tile_count(big, M, N) >= CUS) plan = pick("tile_256x256_k64_w8_tailsplit");
+        if (tile_count(tile_shape(TC_256x256_K64_S2_W8), M, N) >= CUS) plan = pick("tile_256x256_k64_w8_tailsplit");
+        else if (tile_count(tile_shape(TC_256x128_K64_S3_W8_L), M, N) >= CUS) plan = pick("tile_256x128_k64s3_w8_lag");
         if (plan < 0) plan = pick("tile_128x128_k64_w4");
     }
     if (plan < 0) plan = pick("tile_128x128_k64_w4");

@@ -45,7 +45,9 @@ enum TileCfg : int {
     TC_64x64_K128_S2_G2 = 21,     // two K groups of 4 waves (8 waves)
     TC_128x128_K64_S2_G2 = 22,
     TC_64x64_K64_S2_G4 = 23,      // four K groups (16 waves)
-    TC_COUNT = 24,
+    TC_256x128_K64_S3_W8_L = 24,   // lagged refill
+    TC_128x128_K64_S4_W4_L = 25,
+    TC_COUNT = 26,
 };
 
 struct TileShape {

@@ -20,8 +20,9 @@
 //     consecutive rows over distinct bank groups.
 //   * buffer resources bound each operand panel, so rows past M or N read
 //     as zero without a branch; K-tail chunks are pointed out of range.
-//   * schedule: the next sub-step's fragment reads and the next stage's
-//     loads are interleaved between MFMAs (sched_group_barrier).
+//   * schedule: fragment reads run PD sub-steps ahead of the MFMAs and the
+//     refill loads go among the last sub-steps' MFMAs, after the step's
+//     barrier; the order is pinned slot by slot (sched_barrier).
 //   * epilogue: fp32 accumulator + fp32(R), one nearest-even rounding to
 //     bf16, staged through LDS so R is read and Y written 16 bytes per
 //     lane; each element is read (R) and written (Y) by the same lane, so Y
@@ -30,6 +31,8 @@
 //     are remapped so each XCD takes a contiguous range of tiles, walked in
 //     GROUP_M-row bands, so tiles resident on one XCD share panels in its L2.
 #include "internal.h"
+
+#include <utility>
 
 namespace kernelarc {
 namespace {
@@ -66,7 +69,8 @@ __device__ __forceinline__ int swz(int r) {
     else return ((r >> 1) ^ (r >> 3)) & 3;
 }
 
-template <int BM_, int BN_, int BK_, int WAVES_M_, int WAVES_N_, int STAGES_, int WAVES_PER_EU_, int KGROUPS_ = 1>
+template <int BM_, int BN_, int BK_, int WAVES_M_, int WAVES_N_, int STAGES_, int WAVES_PER_EU_, int KGROUPS_ = 1,
+          int PD_ = 1, bool LAG_ = false>
 struct Cfg {
     static constexpr int BM = BM_, BN = BN_, BK = BK_, STAGES = STAGES_;
     static constexpr int WAVES_M = WAVES_M_, WAVES_N = WAVES_N_;
@@ -78,6 +82,15 @@ struct Cfg {
     static constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;   // per-wave block
     static constexpr int TM = WM / 32, TN = WN / 32;             // 32x32 blocks per wave
     static constexpr int KSTEPS = BK / 16;                        // MFMA sub-steps per stage
+    // Fragment prefetch distance: the LDS reads of sub-step s + PD are
+    // issued among the MFMAs of sub-step s (PD + 1 register sets).
+    static constexpr int PD = PD_;
+    // Refill timing (STAGES >= 3 only when set): the buffer freed at step
+    // kt-1's barrier is refilled with step kt+STAGES-1 by loads spread over
+    // all of step kt's MFMAs (STAGES-2 steps of latency slack, no burst);
+    // when clear, the buffer freed at step kt's own barrier is refilled
+    // with step kt+STAGES among the MFMAs after that barrier.
+    static constexpr bool LAG = LAG_;
     static constexpr int ROW_BYTES = BK * 2, CHUNKS = BK / 8, RPI = 64 / CHUNKS;
     static constexpr int A_BYTES = BM * ROW_BYTES, B_BYTES = BN * ROW_BYTES;
     static constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
@@ -106,10 +119,41 @@ struct Cfg {
     static_assert(TILE_WAVES * EPI_WAVE_FLOATS * 4 <= LDS_BYTES, "epilogue staging fits");
     static_assert(RED_BYTES <= LDS_BYTES, "K-group reduction fits");
     static_assert(LOADS * (STAGES - 2) < 64, "vmcnt range");
+    static_assert(PD >= 1 && PD < KSTEPS && KSTEPS % (PD + 1) == 0, "fragment prefetch distance");
+    static_assert(!LAG || STAGES >= 3, "lagged refill needs three stages");
 };
 
-// Enqueue the LDS-direct loads of K step kt into one stage buffer.  Chunks
+// Enqueue LDS-direct load q (A loads first, then B) of the K step at
+// element kbase (byte kbytes within a row) into one stage buffer.  Chunks
 // at or past K are pointed out of range and arrive as zeros.
+template <class C, int q>
+__device__ __forceinline__ void issue_load(char *stage, const __amdgpu_buffer_rsrc_t &ra,
+                                           const __amdgpu_buffer_rsrc_t &rb, const uint32_t *a_off,
+                                           const int *a_k, const uint32_t *b_off, const int *b_k, int wave,
+                                           int64_t kbase, uint32_t kbytes, int64_t K) {
+    if constexpr (q < C::A_LOADS) {
+        const int blk = wave * C::A_LOADS + q;
+        const uint32_t off = (kbase + a_k[q] < K) ? a_off[q] + kbytes : OOB_OFFSET;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void *)(stage + blk * 1024), 16, off, 0, 0, 0);
+    } else {
+        constexpr int qb = q - C::A_LOADS;
+        const int blk = wave * C::B_LOADS + qb;
+        const uint32_t off = (kbase + b_k[qb] < K) ? b_off[qb] + kbytes : OOB_OFFSET;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_void *)(stage + C::A_BYTES + blk * 1024), 16,
+                                                 off, 0, 0, 0);
+    }
+}
+
+// Compile-time loop: f(std::integral_constant<int, I>) for I = B .. E-1.
+template <int B, class F, int... I>
+__device__ __forceinline__ void static_for_impl(F &&f, std::integer_sequence<int, I...>) {
+    (f(std::integral_constant<int, B + I>{}), ...);
+}
+template <int B, int E, class F>
+__device__ __forceinline__ void static_for(F &&f) {
+    if constexpr (E > B) static_for_impl<B>(f, std::make_integer_sequence<int, E - B>{});
+}
+
 template <class C>
 __device__ __forceinline__ void issue_stage(char *stage, const __amdgpu_buffer_rsrc_t &ra,
                                             const __amdgpu_buffer_rsrc_t &rb, const uint32_t *a_off,
@@ -117,69 +161,34 @@ __device__ __forceinline__ void issue_stage(char *stage, const __amdgpu_buffer_r
                                             int wave, int kt, int64_t K) {
     const int64_t kbase = static_cast<int64_t>(kt) * C::BK;
     const uint32_t kbytes = static_cast<uint32_t>(kt) * C::ROW_BYTES;
-#pragma unroll
-    for (int q = 0; q < C::A_LOADS; ++q) {
-        const int blk = wave * C::A_LOADS + q;
-        const uint32_t off = (kbase + a_k[q] < K) ? a_off[q] + kbytes : OOB_OFFSET;
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void *)(stage + blk * 1024), 16, off, 0, 0, 0);
-    }
-#pragma unroll
-    for (int q = 0; q < C::B_LOADS; ++q) {
-        const int blk = wave * C::B_LOADS + q;
-        const uint32_t off = (kbase + b_k[q] < K) ? b_off[q] + kbytes : OOB_OFFSET;
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_void *)(stage + C::A_BYTES + blk * 1024), 16,
-                                                 off, 0, 0, 0);
-    }
+    static_for<0, C::LOADS>([&](auto q) {
+        issue_load<C, decltype(q)::value>(stage, ra, rb, a_off, a_k, b_off, b_k, wave, kbase, kbytes, K);
+    });
 }
 
-// MFMA operands of one sub-step from one stage: lane l reads row l % 32 of
-// each 32-row block at byte column `col` (chunk 2*ks + l / 32, swizzled).
-template <class C>
-__device__ __forceinline__ void load_fragments(const char *a_base, const char *b_base, int col,
-                                               bf16x8 *af, bf16x8 *bfr) {
-#pragma unroll
-    for (int i = 0; i < C::TM; ++i)
-        af[i] = *reinterpret_cast<const bf16x8 *>(a_base + i * 32 * C::ROW_BYTES + col);
-#pragma unroll
-    for (int j = 0; j < C::TN; ++j)
-        bfr[j] = *reinterpret_cast<const bf16x8 *>(b_base + j * 32 * C::ROW_BYTES + col);
+// Fragment read r of one sub-step, in the order the sub-step's MFMAs first
+// use them (a0, b0 .. b[TN-1], a1 .. a[TM-1]): lane l reads row l % 32 of a
+// 32-row block at byte column col.
+template <class C, int r>
+__device__ __forceinline__ void read_frag(const char *a_base, const char *b_base, int col, bf16x8 *fa,
+                                          bf16x8 *fb) {
+    if constexpr (r == 0)
+        fa[0] = *reinterpret_cast<const bf16x8 *>(a_base + col);
+    else if constexpr (r <= C::TN)
+        fb[r - 1] = *reinterpret_cast<const bf16x8 *>(b_base + (r - 1) * 32 * C::ROW_BYTES + col);
+    else
+        fa[r - C::TN] = *reinterpret_cast<const bf16x8 *>(a_base + (r - C::TN) * 32 * C::ROW_BYTES + col);
 }
 
-// Sub-step scheduling: MFMA number T of a sub-step is followed by its share
-// of the LDS reads (next sub-step's fragments) and of the VMEM loads (next
-// stage), spread evenly over the MFMAS MFMAs.
-template <int MFMAS, int READS, int LOADS, int T>
-__device__ __forceinline__ void interleave() {
-    constexpr int MFMA = 0x008, VMEM_READ = 0x020, DS_READ = 0x100;
-    constexpr int r = ((T + 1) * READS) / MFMAS - (T * READS) / MFMAS;
-    constexpr int l = ((T + 1) * LOADS) / MFMAS - (T * LOADS) / MFMAS;
-    __builtin_amdgcn_sched_group_barrier(MFMA, 1, 0);
-    if constexpr (l > 0) __builtin_amdgcn_sched_group_barrier(VMEM_READ, l, 0);
-    if constexpr (r > 0) __builtin_amdgcn_sched_group_barrier(DS_READ, r, 0);
-    if constexpr (T + 1 < MFMAS) interleave<MFMAS, READS, LOADS, T + 1>();
-}
-
-template <class C, int KS>
-__device__ __forceinline__ void interleave_substeps() {
-    constexpr int FRAGS = C::TM + C::TN, MFMAS = C::TM * C::TN;
-    if constexpr (KS + 1 < C::KSTEPS) {
-        interleave<MFMAS, FRAGS, (KS == 0 ? C::LOADS : 0), 0>();
-        interleave_substeps<C, KS + 1>();
-    } else {
-        __builtin_amdgcn_sched_group_barrier(0x008, MFMAS, 0);
-    }
-}
-
-// Instruction order of one K step, pinned because the default schedule
-// funnels every fragment through one register set and waits for each LDS
-// read just before its MFMAs.  Order: the fragment reads of sub-step 0;
-// sub-step 0's MFMAs interleaved with the next stage's loads and sub-step
-// 1's reads; each further sub-step's MFMAs with the following reads; the
-// last sub-step's MFMAs alone.
-template <class C>
-__device__ __forceinline__ void schedule_k_step() {
-    __builtin_amdgcn_sched_group_barrier(0x100, C::TM + C::TN, 0);
-    interleave_substeps<C, 0>();
+// Workgroup barrier that keeps the newest N LDS-direct loads of each wave
+// in flight.  A __syncthreads() here would drain every outstanding load
+// (its fence waits for vmcnt(0)) and so empty the staging ring at every K
+// step.  The wave's LDS reads are complete before it arrives (lgkmcnt(0)),
+// so the buffer they read may be refilled once all waves have passed; the
+// memory clobber keeps the compiler from moving LDS accesses across it.
+template <int N>
+__device__ __forceinline__ void stage_barrier() {
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
 }
 
 // Split-K bookkeeping of one launch (split == 1: none).
@@ -305,40 +314,90 @@ void tile_kernel(Problem p, int64_t tiles_m, int64_t tiles_n, int group_m, Split
     const int iters = (nsteps + C::KGROUPS - 1) / C::KGROUPS;
     const int64_t gend = (static_cast<int64_t>(g1) * C::BK) < kend ? static_cast<int64_t>(g1) * C::BK : kend;
 
-    // Prologue: STAGES-1 steps in flight (past the end of the range the
-    // loads are out of range and only write zeros into buffers nobody reads).
+    // Software pipeline.  Per K step: the MFMAs of its KSTEPS sub-steps;
+    // among the MFMAs of sub-step s, the LDS reads of sub-step s + PD's
+    // fragments.  The barrier sits before the last PD sub-steps: there every
+    // wave has read the whole step (its buffer may be refilled) and the next
+    // step has landed, so the reads that run ahead into the next step and
+    // the refill (step kt + STAGES into this buffer) go among those last
+    // MFMAs, whose operands are already in registers.  The instruction order
+    // is pinned slot by slot (one MFMA and its share of reads and loads).
+    constexpr int KS = C::KSTEPS, PD = C::PD, NSETS = PD + 1;
+    constexpr int MF = C::TM * C::TN, FR = C::TM + C::TN, POST = PD * MF, SLOTS = KS * MF;
+    // Loads a wave may leave in flight at a step's barrier (step kt+1 must
+    // have landed): the steps requested after it, and with the lagged
+    // refill also the loads of this step's refill issued before the barrier.
+    constexpr int LPRE = C::LAG ? ((KS - PD) * MF * C::LOADS) / SLOTS : 0;
+    constexpr int VM_KEEP = C::LAG ? C::LOADS * (C::STAGES - 3) + LPRE : C::LOADS * (C::STAGES - 2);
+    constexpr int VM_KEEP0 = C::LOADS * (C::STAGES - 2);   // prologue: step g0 landed
+    int colk[KS];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) colk[ks] = ((2 * ks + hi) ^ frag_swz) * 16;
+    bf16x8 fa[NSETS][C::TM], fb[NSETS][C::TN];
+
+    // Prologue: steps g0 .. g0+STAGES-2 requested, step g0 landed in every
+    // wave, the fragments of its first PD sub-steps requested, then step
+    // g0+STAGES-1 into the last buffer.  Past the end of the range the loads
+    // only write zeros into buffers whose contents are never used.
 #pragma unroll
     for (int s = 0; s < C::STAGES - 1; ++s)
         issue_stage<C>(glds + s * C::STAGE_BYTES, ra, rb, a_off, a_k, b_off, b_k, wave, g0 + s, gend);
+    stage_barrier<VM_KEEP0>();
+    static_for<0, PD>([&](auto ksc) {
+        constexpr int ks = decltype(ksc)::value;
+        static_for<0, FR>([&](auto rc) {
+            read_frag<C, decltype(rc)::value>(glds + a_row_byte, glds + C::A_BYTES + b_row_byte, colk[ks],
+                                              fa[ks], fb[ks]);
+        });
+    });
+    if constexpr (!C::LAG)
+        issue_stage<C>(glds + (C::STAGES - 1) * C::STAGE_BYTES, ra, rb, a_off, a_k, b_off, b_k, wave,
+                       g0 + C::STAGES - 1, gend);
 
     int cur_stage = 0;
     for (int it = 0; it < iters; ++it) {
-        const int kt = g0 + it;
-        // Stage kt has landed once at most STAGES-2 stages' loads are outstanding.
-        __builtin_amdgcn_s_waitcnt(waitcnt_vm(C::LOADS * (C::STAGES - 2)));
-        __syncthreads();   // every wave's part of stage kt; stage kt-1's buffer is free
-        const char *cur = glds + cur_stage * C::STAGE_BYTES;
-        const char *a_base = cur + a_row_byte;
-        const char *b_base = cur + C::A_BYTES + b_row_byte;
-        bf16x8 af[2][C::TM], bfr[2][C::TN];
-        load_fragments<C>(a_base, b_base, (hi ^ frag_swz) * 16, af[0], bfr[0]);
-        const int free_stage = cur_stage == 0 ? C::STAGES - 1 : cur_stage - 1;   // held step kt-1
-        issue_stage<C>(glds + free_stage * C::STAGE_BYTES, ra, rb, a_off, a_k, b_off, b_k, wave,
-                       kt + C::STAGES - 1, gend);
-#pragma unroll
-        for (int ks = 0; ks < C::KSTEPS; ++ks) {
-            if (ks + 1 < C::KSTEPS)
-                load_fragments<C>(a_base, b_base, ((2 * (ks + 1) + hi) ^ frag_swz) * 16,
-                                  af[(ks + 1) & 1], bfr[(ks + 1) & 1]);
-#pragma unroll
-            for (int i = 0; i < C::TM; ++i)
-#pragma unroll
-                for (int j = 0; j < C::TN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[ks & 1][i], bfr[ks & 1][j],
-                                                                        acc[i][j], 0, 0, 0);
-        }
-        schedule_k_step<C>();
-        cur_stage = cur_stage + 1 == C::STAGES ? 0 : cur_stage + 1;
+        const int next_stage = cur_stage + 1 == C::STAGES ? 0 : cur_stage + 1;
+        char *const cur = glds + cur_stage * C::STAGE_BYTES;
+        const char *const nxt = glds + next_stage * C::STAGE_BYTES;
+        // The buffer refilled during this step and the step it receives.
+        const int prev_stage = cur_stage == 0 ? C::STAGES - 1 : cur_stage - 1;
+        char *const dst = C::LAG ? glds + prev_stage * C::STAGE_BYTES : cur;
+        const int refill = g0 + it + (C::LAG ? C::STAGES - 1 : C::STAGES);
+        const int64_t kbase = static_cast<int64_t>(refill) * C::BK;
+        const uint32_t kbytes = static_cast<uint32_t>(refill) * C::ROW_BYTES;
+        static_for<0, KS>([&](auto ksc) {
+            constexpr int ks = decltype(ksc)::value;
+            if constexpr (ks == KS - PD) stage_barrier<VM_KEEP>();
+            constexpr int set = ks % NSETS;
+            constexpr int tgt = ks + PD;              // sub-step whose fragments are read
+            constexpr int tset = tgt % NSETS;
+            const char *const src = tgt < KS ? cur : nxt;
+            const int tcol = colk[tgt % KS];
+            static_for<0, MF>([&](auto tc) {
+                constexpr int t = decltype(tc)::value;
+                constexpr int i = t / C::TN, j = t % C::TN;
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[set][i], fb[set][j], acc[i][j], 0, 0, 0);
+                static_for<t * FR / MF, (t + 1) * FR / MF>([&](auto rc) {
+                    read_frag<C, decltype(rc)::value>(src + a_row_byte, src + C::A_BYTES + b_row_byte, tcol,
+                                                      fa[tset], fb[tset]);
+                });
+                if constexpr (C::LAG) {
+                    constexpr int u = ks * MF + t;
+                    static_for<u * C::LOADS / SLOTS, (u + 1) * C::LOADS / SLOTS>([&](auto q) {
+                        issue_load<C, decltype(q)::value>(dst, ra, rb, a_off, a_k, b_off, b_k, wave, kbase,
+                                                          kbytes, gend);
+                    });
+                } else if constexpr (ks >= KS - PD) {
+                    constexpr int u = (ks - (KS - PD)) * MF + t;
+                    static_for<u * C::LOADS / POST, (u + 1) * C::LOADS / POST>([&](auto q) {
+                        issue_load<C, decltype(q)::value>(dst, ra, rb, a_off, a_k, b_off, b_k, wave, kbase,
+                                                          kbytes, gend);
+                    });
+                }
+                __builtin_amdgcn_sched_barrier(0);
+            });
+        });
+        cur_stage = next_stage;
     }
 
     // Epilogue.  Accumulator element e of a 32x32 block sits at row
@@ -624,6 +683,8 @@ using C64x128k64s4 = Cfg<64, 128, 64, 2, 2, 4, 1>;
 using C64x64k128g2 = Cfg<64, 64, 128, 2, 2, 2, 2, 2>;
 using C128x128k64g2 = Cfg<128, 128, 64, 2, 2, 2, 2, 2>;
 using C64x64k64g4 = Cfg<64, 64, 64, 2, 2, 2, 4, 4>;
+using C256x128s3w8L = Cfg<256, 128, 64, 4, 2, 3, 2, 1, 1, true>;
+using C128x128s4L = Cfg<128, 128, 64, 2, 2, 4, 1, 1, 1, true>;
 
 template <class C>
 constexpr TileShape shape_of(int per_cu) { return TileShape{C::BM, C::BN, C::BK, per_cu}; }
@@ -654,6 +715,8 @@ TileShape tile_shape(int cfg) {
         case TC_64x64_K128_S2_G2: return shape_of<C64x64k128g2>(1);
         case TC_128x128_K64_S2_G2: return shape_of<C128x128k64g2>(1);
         case TC_64x64_K64_S2_G4: return shape_of<C64x64k64g4>(1);
+        case TC_256x128_K64_S3_W8_L: return shape_of<C256x128s3w8L>(1);
+        case TC_128x128_K64_S4_W4_L: return shape_of<C128x128s4L>(1);
         default: return TileShape{0, 0, 0, 0};
     }
 }
@@ -685,6 +748,8 @@ hipError_t launch_tile(int cfg, const Problem &p, int split, int64_t full_tiles,
         case TC_64x64_K128_S2_G2: return launch_cfg<C64x64k128g2>(p, 8, split, full_tiles, ws, s);
         case TC_128x128_K64_S2_G2: return launch_cfg<C128x128k64g2>(p, 8, split, full_tiles, ws, s);
         case TC_64x64_K64_S2_G4: return launch_cfg<C64x64k64g4>(p, 8, split, full_tiles, ws, s);
+        case TC_256x128_K64_S3_W8_L: return launch_cfg<C256x128s3w8L>(p, 8, split, full_tiles, ws, s);
+        case TC_128x128_K64_S4_W4_L: return launch_cfg<C128x128s4L>(p, 8, split, full_tiles, ws, s);
         default: return hipErrorInvalidValue;
     }
 }
