@@ -71,10 +71,9 @@ def source_digest(paths):
 
 
 # Kernel symbol fragment of each tile plan (rocprofv3 reports symbols).
+# Cfg<BM, BN, BK, WAVES_M, WAVES_N, STAGES, WAVES_PER_EU, KGROUPS, PD, LAG>.
 PLAN_SYMBOL = {
-    "tile_256x256_k64_w8": "Cfg<256, 256, 64, 2, 4, 2, 2>",
-    "tile_128x128_k64_w4": "Cfg<128, 128, 64, 2, 2, 2, 2>",
-    "tile_128x128_k64_w4_splitk": "Cfg<128, 128, 64, 2, 2, 2, 2>",
+    "tile_256x256_k64_w8": "Cfg<256, 256, 64, 2, 4, 2, 2, 1, 1, false>",
 }
 KERNEL_SOURCES = ["paper_2608_17071_amd/csrc/kernel_tile.hip", "paper_2608_17071_amd/csrc/internal.h"]
 
