@@ -314,6 +314,43 @@ void tile_kernel(Problem p, int64_t tiles_m, int64_t tiles_n, int group_m, Split
     const int iters = (nsteps + C::KGROUPS - 1) / C::KGROUPS;
     const int64_t gend = (static_cast<int64_t>(g1) * C::BK) < kend ? static_cast<int64_t>(g1) * C::BK : kend;
 
+    const bool owner = group == 0;   // the waves that hold the tile's result
+
+    // Epilogue constants (the residual may be requested before the K loop).
+    const int64_t N = p.N;
+    const int64_t rows_y = (p.M - m0) < C::BM ? (p.M - m0) : C::BM;
+    const uint32_t ybytes = static_cast<uint32_t>(rows_y * N * 2);
+    const __amdgpu_buffer_rsrc_t ry = make_rsrc(p.Y + m0 * N, ybytes);
+    // Without a residual the R resource is empty (its loads read zero).
+    const __amdgpu_buffer_rsrc_t rr = make_rsrc(p.R ? p.R + m0 * N : p.Y + m0 * N, p.R ? ybytes : 0u);
+    const bool has_r = p.R != nullptr;
+    const bool vec = (N & 7) == 0;
+    const int pr = lane / C::LANES_PER_ROW;             // row within a pass
+    const int pc = (lane % C::LANES_PER_ROW) * 8;       // first of 8 columns
+    const int64_t col0 = n0 + wn0 + pc;
+    constexpr int PASSES = 32 / C::ROWS_PER_PASS;
+    auto base_of = [&](int i, int v) {
+        const int64_t row_local = wm0 + i * 32 + v * C::ROWS_PER_PASS + pr;
+        return static_cast<uint32_t>(row_local * N * 2 + col0 * 2);
+    };
+    // All of a slab's R is read before any of its Y is written (each element
+    // by the same lane), so the loads do not wait behind the stores and Y
+    // may alias R.
+    auto load_r = [&](int i, i32x4 (&rv)[PASSES]) {
+#pragma unroll
+        for (int v = 0; v < PASSES; ++v)
+            rv[v] = __builtin_amdgcn_raw_buffer_load_b128(rr, col0 < N ? base_of(i, v) : OOB_OFFSET, 0, 0);
+    };
+    // Two slabs of R in registers: slab i+1 is requested before slab i is
+    // staged and stored, so only slab 0's latency is exposed.
+    i32x4 rv[2][PASSES];
+    // Small tiles request the first slab of R before the K loop (a few
+    // registers); it is then in flight with the first loads instead of after
+    // the loop, or after the split-K hand-off.
+    constexpr bool EARLY_R = C::TM * C::TN <= 4 && C::WAVES_PER_EU <= 2 && C::WAVES <= 4;
+    if constexpr (EARLY_R)
+        if (owner && vec && has_r) load_r(0, rv[0]);
+
     // Software pipeline.  Per K step: the MFMAs of its KSTEPS sub-steps;
     // among the MFMAs of sub-step s, the LDS reads of sub-step s + PD's
     // fragments.  The barrier sits before the last PD sub-steps: there every
@@ -443,37 +480,6 @@ void tile_kernel(Problem p, int64_t tiles_m, int64_t tiles_n, int group_m, Split
         }
         __syncthreads();   // the partials are read before LDS is reused
     }
-    const bool owner = group == 0;   // the waves that hold the tile's result
-
-    // Epilogue constants.
-    float *ep = reinterpret_cast<float *>(lds) + wave * C::EPI_WAVE_FLOATS;
-    const int64_t N = p.N;
-    const int64_t rows_y = (p.M - m0) < C::BM ? (p.M - m0) : C::BM;
-    const uint32_t ybytes = static_cast<uint32_t>(rows_y * N * 2);
-    const __amdgpu_buffer_rsrc_t ry = make_rsrc(p.Y + m0 * N, ybytes);
-    // Without a residual the R resource is empty (its loads read zero).
-    const __amdgpu_buffer_rsrc_t rr = make_rsrc(p.R ? p.R + m0 * N : p.Y + m0 * N, p.R ? ybytes : 0u);
-    const bool has_r = p.R != nullptr;
-    const bool vec = (N & 7) == 0;
-    const int pr = lane / C::LANES_PER_ROW;             // row within a pass
-    const int pc = (lane % C::LANES_PER_ROW) * 8;       // first of 8 columns
-    const int64_t col0 = n0 + wn0 + pc;
-    constexpr int PASSES = 32 / C::ROWS_PER_PASS;
-    auto base_of = [&](int i, int v) {
-        const int64_t row_local = wm0 + i * 32 + v * C::ROWS_PER_PASS + pr;
-        return static_cast<uint32_t>(row_local * N * 2 + col0 * 2);
-    };
-    // All of a slab's R is read before any of its Y is written (each element
-    // by the same lane), so the loads do not wait behind the stores and Y
-    // may alias R.
-    auto load_r = [&](int i, i32x4 (&rv)[PASSES]) {
-#pragma unroll
-        for (int v = 0; v < PASSES; ++v)
-            rv[v] = __builtin_amdgcn_raw_buffer_load_b128(rr, col0 < N ? base_of(i, v) : OOB_OFFSET, 0, 0);
-    };
-    // Two slabs of R in registers: slab i+1 is requested before slab i is
-    // staged and stored, so only slab 0's latency is exposed.
-    i32x4 rv[2][PASSES];
 
     if (piece) {
         // Publish this slice's fp32 tile in fragment order (each store
@@ -581,7 +587,9 @@ void tile_kernel(Problem p, int64_t tiles_m, int64_t tiles_n, int group_m, Split
         if (threadIdx.x == 0)
             __hip_atomic_store(sk.counters + stile, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
-    if (owner && vec && has_r) load_r(0, rv[0]);
+    if constexpr (!EARLY_R)
+        if (owner && vec && has_r) load_r(0, rv[0]);
+    float *ep = reinterpret_cast<float *>(lds) + wave * C::EPI_WAVE_FLOATS;
 #pragma unroll
     for (int i = 0; i < C::TM; ++i) {
         if (owner && vec && has_r && i + 1 < C::TM) load_r(i + 1, rv[(i + 1) & 1]);
