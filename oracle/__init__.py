@@ -1,4 +1,5 @@
-"""CPU oracle for Y = X.W^T + R (TEST INFRASTRUCTURE ONLY).
+"""CPU oracle for Y = X.W^T + R and its general form
+D = alpha.X.W^T + beta.C + bias (TEST INFRASTRUCTURE ONLY).
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
 ``bench.py`` may import this package.  The GPU library never imports, links
@@ -52,6 +53,12 @@ class Oracle:
         lib.ka_oracle_linear.restype = ctypes.c_int
         lib.ka_oracle_linear_at.argtypes = [_I64, _I64, _I64, _P, _P, _P, _I64, _P, _P, _P]
         lib.ka_oracle_linear_at.restype = ctypes.c_int
+        lib.ka_oracle_linear_ex.argtypes = [_I64, _I64, _I64, ctypes.c_float, _P, _I64, _P, _I64,
+                                            ctypes.c_float, _P, _I64, _P, _P]
+        lib.ka_oracle_linear_ex.restype = ctypes.c_int
+        lib.ka_oracle_linear_ex_at.argtypes = [_I64, _I64, _I64, ctypes.c_float, _P, _I64, _P, _I64,
+                                               ctypes.c_float, _P, _I64, _P, _I64, _P, _P, _P]
+        lib.ka_oracle_linear_ex_at.restype = ctypes.c_int
         lib.ka_oracle_round_bf16.argtypes = [_I64, _P, _P]
         lib.ka_oracle_round_bf16.restype = None
         lib.ka_oracle_threads.argtypes = []
@@ -105,6 +112,65 @@ class Oracle:
                                           cols.ctypes.data, out.ctypes.data)
         if rc != 0:
             raise ValueError("oracle rejected its arguments")
+        return out
+
+    @staticmethod
+    def _strided(a, rows, cols, what):
+        """A 2-D bf16 view with unit stride along its last axis: (array, ld)."""
+        if not isinstance(a, np.ndarray) or a.dtype != np.uint16:
+            raise TypeError(f"{what}: oracle inputs are bf16 bit patterns (numpy.uint16)")
+        if a.ndim != 2 or a.shape != (rows, cols):
+            raise ValueError(f"{what}: expected shape {(rows, cols)}, got {a.shape}")
+        if rows > 0 and cols > 0 and a.strides[1] != 2:
+            raise ValueError(f"{what}: the last axis must be contiguous")
+        ld = a.strides[0] // 2 if rows > 1 else max(cols, 1)
+        if rows > 1 and (a.strides[0] % 2 or ld < cols):
+            raise ValueError(f"{what}: bad row stride")
+        return a, ld
+
+    def _ex_args(self, X, W, C, bias, alpha, beta):
+        M, K = X.shape
+        N = W.shape[0]
+        X, ldx = self._strided(X, M, K, "X")
+        W, ldw = self._strided(W, N, K, "W")
+        Cp, ldc = None, max(N, 1)
+        if C is not None:
+            C, ldc = self._strided(C, M, N, "C")
+            Cp = C.ctypes.data
+        bp = None
+        if bias is not None:
+            bias = np.ascontiguousarray(bias)
+            if bias.dtype != np.uint16 or bias.shape != (N,):
+                raise ValueError("bias: expected bf16 bit patterns of shape (N,)")
+            bp = bias.ctypes.data
+        keep = (X, W, C, bias)
+        return (M, N, K, float(alpha), X.ctypes.data, ldx, W.ctypes.data, ldw,
+                float(beta), Cp, ldc, bp), keep
+
+    def linear_ex(self, X, W, C=None, bias=None, alpha=1.0, beta=1.0) -> np.ndarray:
+        """D = alpha * X W^T + beta * C + bias in float64 (X, W, C may be
+        row-strided views; beta = 0 leaves C unread)."""
+        args, keep = self._ex_args(X, W, C, bias, alpha, beta)
+        D = np.empty((args[0], args[1]), dtype=np.float64)
+        rc = self.lib.ka_oracle_linear_ex(*args, D.ctypes.data)
+        if rc != 0:
+            raise ValueError("oracle rejected its arguments")
+        del keep
+        return D
+
+    def linear_ex_at(self, X, W, C, bias, alpha, beta, rows, cols) -> np.ndarray:
+        """The general form at the positions (rows[t], cols[t])."""
+        args, keep = self._ex_args(X, W, C, bias, alpha, beta)
+        rows = np.ascontiguousarray(rows, dtype=np.int64)
+        cols = np.ascontiguousarray(cols, dtype=np.int64)
+        if rows.shape != cols.shape or rows.ndim != 1:
+            raise ValueError("rows and cols must be 1-D and of equal length")
+        out = np.empty(rows.shape[0], dtype=np.float64)
+        rc = self.lib.ka_oracle_linear_ex_at(*args, rows.shape[0], rows.ctypes.data,
+                                             cols.ctypes.data, out.ctypes.data)
+        if rc != 0:
+            raise ValueError("oracle rejected its arguments")
+        del keep
         return out
 
     def threads(self) -> int:

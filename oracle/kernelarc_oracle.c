@@ -126,6 +126,76 @@ void ka_oracle_round_bf16(int64_t n, const double *in, uint16_t *out)
     }
 }
 
+/*
+ * General form: the library epilogue the paper's GEMM sites invoke
+ * (D = alpha * W^T A + beta * C in cuBLASLt's column-major notation, Alg. 3
+ * and the decoder-layer case study, whose two residual GEMMs are this
+ * operator with K = hidden size or K = intermediate size), read row-major
+ * as for the plain operator, with a bias row and leading dimensions:
+ *
+ *     D[i,j] = alpha * sum_k X[i*ldx + k] W[j*ldw + k]
+ *              + beta * C[i*ldc + j] + bias[j]
+ *
+ * alpha and beta are binary32 values (widened exactly); C and bias are bf16
+ * bit patterns or NULL.  When beta == 0, C is not read (so it may be NULL or
+ * hold non-finite values), as in BLAS; alpha always multiplies the product.
+ * Evaluated in double: the k-sum ascending, then the alpha product, then
+ * the C term, then the bias.  D is dense [M,N] doubles, not rounded.
+ */
+static double element_ex(int64_t i, int64_t j, int64_t K, double alpha,
+                         const uint16_t *X, int64_t ldx, const uint16_t *W, int64_t ldw,
+                         double beta, const uint16_t *C, int64_t ldc, const uint16_t *bias)
+{
+    double s = 0.0;
+    for (int64_t k = 0; k < K; ++k)
+        s += bf16_bits_to_double(X[i * ldx + k]) * bf16_bits_to_double(W[j * ldw + k]);
+    double d = alpha * s;
+    if (C && beta != 0.0)
+        d += beta * bf16_bits_to_double(C[i * ldc + j]);
+    if (bias)
+        d += bf16_bits_to_double(bias[j]);
+    return d;
+}
+
+static int check_ex(int64_t M, int64_t N, int64_t K, const uint16_t *X, int64_t ldx,
+                    const uint16_t *W, int64_t ldw, float beta, const uint16_t *C, int64_t ldc)
+{
+    if (M < 0 || N < 0 || K < 0) return -1;
+    if (M > 0 && K > 0 && (!X || ldx < K)) return -1;
+    if (N > 0 && K > 0 && (!W || ldw < K)) return -1;
+    if (M > 0 && N > 0 && beta != 0.0f && C && ldc < N) return -1;
+    return 0;
+}
+
+int ka_oracle_linear_ex(int64_t M, int64_t N, int64_t K, float alpha,
+                        const uint16_t *X, int64_t ldx, const uint16_t *W, int64_t ldw,
+                        float beta, const uint16_t *C, int64_t ldc, const uint16_t *bias,
+                        double *D)
+{
+    if (check_ex(M, N, K, X, ldx, W, ldw, beta, C, ldc) != 0) return -1;
+    if (M * N > 0 && !D) return -1;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t i = 0; i < M; ++i)
+        for (int64_t j = 0; j < N; ++j)
+            D[i * N + j] = element_ex(i, j, K, (double)alpha, X, ldx, W, ldw, (double)beta, C, ldc, bias);
+    return 0;
+}
+
+/* The general form at the n positions (rows[t], cols[t]). */
+int ka_oracle_linear_ex_at(int64_t M, int64_t N, int64_t K, float alpha,
+                           const uint16_t *X, int64_t ldx, const uint16_t *W, int64_t ldw,
+                           float beta, const uint16_t *C, int64_t ldc, const uint16_t *bias,
+                           int64_t n, const int64_t *rows, const int64_t *cols, double *out)
+{
+    if (check_ex(M, N, K, X, ldx, W, ldw, beta, C, ldc) != 0 || n < 0) return -1;
+    for (int64_t t = 0; t < n; ++t)
+        if (rows[t] < 0 || rows[t] >= M || cols[t] < 0 || cols[t] >= N) return -1;
+#pragma omp parallel for schedule(dynamic, 16)
+    for (int64_t t = 0; t < n; ++t)
+        out[t] = element_ex(rows[t], cols[t], K, (double)alpha, X, ldx, W, ldw, (double)beta, C, ldc, bias);
+    return 0;
+}
+
 /* Number of threads the OpenMP loops above use (1 without OpenMP). */
 int ka_oracle_threads(void)
 {

@@ -16,6 +16,12 @@ fix independently:
   neighbour, overflow goes to infinity, and float32 inputs round as torch
   rounds them.
 
+The general form D = alpha X W^T + beta C + bias (leading dimensions, bias
+row; ``EX_PINS``) is pinned by exact rational arithmetic with strided
+operands over NaN padding, by reduction to the plain operator at
+alpha = beta = 1, by the W = 0 closed form, by beta = 0 leaving C unread,
+by exact scaling with power-of-two alpha, and by strided = dense.
+
 ``ALL_PINS`` is run against the real oracle (all must pass) and against
 copies of the oracle with a planted mistake (at least one must fail).
 """
@@ -203,6 +209,142 @@ def pin_round_like_torch(orc, seed=8):
     np.testing.assert_array_equal(orc.round_bf16(f.astype(np.float64)), t)
 
 
+# ---- general form D = alpha X W^T + beta C + bias (strided operands) ----
+
+_ALPHAS = (1.0, -2.0, 0.5, 0.0, 3.0517578125e-05, 1.7310791015625, -0.3333333432674408)
+
+
+def _padded(rng, arr, extra):
+    """arr as the leading columns of a wider buffer whose padding is NaN."""
+    rows, cols = arr.shape
+    buf = np.full((rows, cols + extra), 0x7FC0, np.uint16)
+    buf[:, :cols] = arr
+    return buf[:, :cols]
+
+
+def pin_ex_exact_bruteforce(orc, trials=40, seed=4321):
+    """General form within 2^-49 (|alpha| sum|x w| + |beta c| + |b|) of the
+    exact rational result, with strided operands over NaN padding."""
+    rng = np.random.default_rng(seed)
+    for t in range(trials):
+        M, N, K = (int(v) for v in rng.integers(1, 13, size=3))
+        X = _padded(rng, _rand_bits(rng, (M, K), 1.0 / np.sqrt(K)), int(rng.integers(0, 5)))
+        W = _padded(rng, _rand_bits(rng, (N, K), 1.0 / np.sqrt(K)), int(rng.integers(0, 5)))
+        C = _padded(rng, _rand_bits(rng, (M, N)), int(rng.integers(0, 5))) if rng.random() < 0.7 else None
+        b = _rand_bits(rng, (N,)) if rng.random() < 0.6 else None
+        alpha = float(np.float32(_ALPHAS[t % len(_ALPHAS)]))
+        beta = float(np.float32(_ALPHAS[(3 * t + 1) % len(_ALPHAS)]))
+        D = orc.linear_ex(X, W, C, b, alpha, beta)
+        assert np.isfinite(D).all(), (M, N, K, "non-finite output from finite operands")
+        xf, wf = bf16_bits_to_f64(X), bf16_bits_to_f64(W)
+        cf = bf16_bits_to_f64(C) if C is not None else None
+        bf = bf16_bits_to_f64(b) if b is not None else None
+        for i in range(M):
+            for j in range(N):
+                s = Fraction(0)
+                mag = Fraction(0)
+                for k in range(K):
+                    p = Fraction(xf[i, k]) * Fraction(wf[j, k])
+                    s += p
+                    mag += abs(p)
+                exact = Fraction(alpha) * s
+                mag = abs(Fraction(alpha)) * mag
+                if cf is not None and beta != 0.0:
+                    exact += Fraction(beta) * Fraction(cf[i, j])
+                    mag += abs(Fraction(beta) * Fraction(cf[i, j]))
+                if bf is not None:
+                    exact += Fraction(bf[j])
+                    mag += abs(Fraction(bf[j]))
+                err = abs(Fraction(D[i, j]) - exact)
+                assert err <= mag / 2**49, (M, N, K, alpha, beta, i, j, float(err))
+
+
+def pin_ex_reduces_to_base(orc, seed=11):
+    """alpha = beta = 1 without bias is the plain operator, bit for bit."""
+    rng = np.random.default_rng(seed)
+    for M, N, K in ((5, 7, 9), (16, 3, 40), (1, 33, 17)):
+        X = _rand_bits(rng, (M, K))
+        W = _rand_bits(rng, (N, K))
+        R = _rand_bits(rng, (M, N))
+        np.testing.assert_array_equal(orc.linear_ex(X, W, R, None, 1.0, 1.0), orc.linear(X, W, R))
+        np.testing.assert_array_equal(orc.linear_ex(X, W, None, None, 1.0, 1.0), orc.linear(X, W))
+
+
+def pin_ex_zero_weight(orc, seed=12):
+    """W = 0: D = beta C + bias (the product term vanishes for finite X)."""
+    rng = np.random.default_rng(seed)
+    M, N, K = 9, 11, 13
+    X = _rand_bits(rng, (M, K))
+    W = np.zeros((N, K), np.uint16)
+    C = _rand_bits(rng, (M, N))
+    b = _rand_bits(rng, (N,))
+    D = orc.linear_ex(X, W, C, b, -2.0, 0.5)
+    cf, bf = bf16_bits_to_f64(C), bf16_bits_to_f64(b)
+    for i in range(M):
+        for j in range(N):
+            exact = Fraction(0.5) * Fraction(cf[i, j]) + Fraction(bf[j])
+            assert abs(Fraction(D[i, j]) - exact) <= abs(exact) / 2**52, (i, j)
+
+
+def pin_ex_beta_zero_skips_c(orc, seed=13):
+    """beta = 0: C is not read (NaN in C does not reach D)."""
+    rng = np.random.default_rng(seed)
+    M, N, K = 6, 5, 8
+    X = _rand_bits(rng, (M, K))
+    W = _rand_bits(rng, (N, K))
+    b = _rand_bits(rng, (N,))
+    C = np.full((M, N), 0x7FC0, np.uint16)
+    D = orc.linear_ex(X, W, C, b, 1.0, 0.0)
+    assert np.isfinite(D).all()
+    np.testing.assert_array_equal(D, orc.linear_ex(X, W, None, b, 1.0, 1.0))
+
+
+def pin_ex_alpha_power_of_two(orc, seed=14):
+    """A power-of-two alpha scales the product exactly."""
+    rng = np.random.default_rng(seed)
+    X = _rand_bits(rng, (7, 19))
+    W = _rand_bits(rng, (9, 19))
+    base = orc.linear(X, W)
+    for a in (4.0, 0.125, -1.0):
+        np.testing.assert_array_equal(orc.linear_ex(X, W, None, None, a, 0.0), a * base)
+
+
+def pin_ex_strided_equals_dense(orc, seed=15):
+    """Row-strided views (NaN padding) give the dense result, bit for bit."""
+    rng = np.random.default_rng(seed)
+    M, N, K = 10, 12, 21
+    X = _rand_bits(rng, (M, K))
+    W = _rand_bits(rng, (N, K))
+    C = _rand_bits(rng, (M, N))
+    b = _rand_bits(rng, (N,))
+    dense = orc.linear_ex(X, W, C, b, 0.75, -1.5)
+    strided = orc.linear_ex(_padded(rng, X, 5), _padded(rng, W, 3), _padded(rng, C, 7), b, 0.75, -1.5)
+    np.testing.assert_array_equal(strided, dense)
+
+
+def pin_ex_at_matches_full(orc, seed=16):
+    rng = np.random.default_rng(seed)
+    M, N, K = 8, 9, 10
+    X = _padded(rng, _rand_bits(rng, (M, K)), 2)
+    W = _rand_bits(rng, (N, K))
+    C = _rand_bits(rng, (M, N))
+    b = _rand_bits(rng, (N,))
+    full = orc.linear_ex(X, W, C, b, 1.25, 2.0)
+    rows = rng.integers(0, M, 40)
+    cols = rng.integers(0, N, 40)
+    np.testing.assert_array_equal(orc.linear_ex_at(X, W, C, b, 1.25, 2.0, rows, cols), full[rows, cols])
+
+
+EX_PINS = [
+    pin_ex_exact_bruteforce,
+    pin_ex_reduces_to_base,
+    pin_ex_zero_weight,
+    pin_ex_beta_zero_skips_c,
+    pin_ex_alpha_power_of_two,
+    pin_ex_strided_equals_dense,
+    pin_ex_at_matches_full,
+]
+
 ALL_PINS = [
     pin_exact_bruteforce,
     pin_golden_hand_worked,
@@ -216,4 +358,4 @@ ALL_PINS = [
     pin_round_midpoints,
     pin_round_specials,
     pin_round_like_torch,
-]
+] + EX_PINS

@@ -26,6 +26,13 @@ MUTANTS = {
     "round_ties_away": ("rint(a / spacing)", "floor(a / spacing + 0.5)"),
     "round_truncate": ("rint(a / spacing)", "trunc(a / spacing)"),
     "round_no_subnormal_clamp": ("if (exp2 < -126) exp2 = -126;", "if (exp2 < -1022) exp2 = -1022;"),
+    "ex_bias_dropped": ("        d += bf16_bits_to_double(bias[j]);", "        d += 0.0;"),
+    "ex_ldx_ignored": ("bf16_bits_to_double(X[i * ldx + k])", "bf16_bits_to_double(X[i * K + k])"),
+    "ex_ldw_ignored": ("bf16_bits_to_double(W[j * ldw + k])", "bf16_bits_to_double(W[j * K + k])"),
+    "ex_alpha_on_c": ("d += beta * bf16_bits_to_double(C[i * ldc + j]);",
+                      "d += alpha * beta * bf16_bits_to_double(C[i * ldc + j]);"),
+    "ex_beta_zero_reads_c": ("if (C && beta != 0.0)", "if (C)"),
+    "ex_alpha_dropped": ("double d = alpha * s;", "double d = s;"),
 }
 
 
