@@ -120,6 +120,49 @@ int kernelarc_gemm_bf16_with_plan(int plan, int64_t M, int64_t N, int64_t K,
                                   const void *X, const void *W, const void *R,
                                   void *Y, hipStream_t stream);
 
+/*
+ * General form: the library epilogue of the paper's GEMM sites (cuBLASLt's
+ * D = alpha W^T A + beta C, Alg. 3 and the decoder-layer case study, whose
+ * two residual GEMMs are this operator with K = hidden or K = intermediate
+ * size), in the same row-major reading, with a bias row and leading
+ * dimensions:
+ *
+ *     Y[i,j] = bf16( alpha * sum_k X[i*ldx+k] W[j*ldw+k]
+ *                    + beta * C[i*ldc+j] + bias[j] )
+ *
+ * fp32 accumulation; alpha * acc, then + beta * C as one fused multiply-add,
+ * then + bias, in fp32; one round-to-nearest-even to bf16.  With
+ * alpha = beta = 1, bias == NULL and dense leading dimensions the result is
+ * bit-identical to kernelarc_gemm_bf16_residual (C != NULL) or
+ * kernelarc_gemm_bf16 (C == NULL).
+ *
+ * ldx, ldw, ldc, ldy: row strides in elements (ldx, ldw >= K; ldc, ldy >= N;
+ * each below 2^31).  C may be NULL (no C term); when beta == 0, C is not
+ * read at all.  bias is N bf16 values or NULL.  Y may equal C when
+ * ldy == ldc (in place); any other overlap of Y's rows with X, W, C or the
+ * bias is rejected with KERNELARC_ERR_INVALID_ARG.  Pointers 16-byte aligned
+ * with K, ldx and ldw multiples of 8 take the MFMA and GEMV kernels (16-byte
+ * R/Y accesses also need ldc and ldy multiples of 8, otherwise 2-byte ones);
+ * anything else takes the generic kernel.  The streaming kernels of the
+ * dense form (4 < M <= 32) are not used for the general form.
+ */
+int kernelarc_gemm_bf16_ex(int64_t M, int64_t N, int64_t K, float alpha,
+                           const void *X, int64_t ldx, const void *W, int64_t ldw,
+                           float beta, const void *C, int64_t ldc, const void *bias,
+                           void *Y, int64_t ldy, hipStream_t stream);
+
+/* The general form with a forced plan (KERNELARC_ERR_UNSUPPORTED if the plan
+ * cannot compute it). */
+int kernelarc_gemm_bf16_ex_with_plan(int plan, int64_t M, int64_t N, int64_t K, float alpha,
+                                     const void *X, int64_t ldx, const void *W, int64_t ldw,
+                                     float beta, const void *C, int64_t ldc, const void *bias,
+                                     void *Y, int64_t ldy, hipStream_t stream);
+
+/* The plan kernelarc_gemm_bf16_ex runs for these sizes, strides and scalars
+ * when the pointers are suitably aligned; -1 for negative sizes. */
+int kernelarc_select_plan_ex(int64_t M, int64_t N, int64_t K, int has_c, int64_t ldx, int64_t ldw,
+                             int64_t ldc, int64_t ldy, float alpha, float beta, int has_bias);
+
 /* Static description of a status code. */
 const char *kernelarc_status_string(int status);
 

@@ -170,7 +170,17 @@ int stream_split_of(int plan, int64_t M, int64_t N, int64_t K) {
     return rule < 2 ? 2 : rule;
 }
 
-bool supports(int plan, int64_t M, int64_t N, int64_t K, bool residual) {
+// Row strides of a call and whether it is the general form (strides other
+// than dense, alpha or beta other than 1, or a bias).  The streaming and
+// skinny kernels compute only the dense plain form; the GEMV, tile and
+// generic kernels compute every form.
+struct Layout {
+    int64_t ldx, ldw, ldr, ldy;
+    bool general;
+};
+Layout dense_layout(int64_t N, int64_t K) { return Layout{K, K, N, N, false}; }
+
+bool supports(int plan, int64_t M, int64_t N, int64_t K, bool residual, const Layout &lay) {
     (void)residual;
     if (M < 0 || N < 0 || K < 0 || M > LIMIT_DIM || N > LIMIT_DIM || K > LIMIT_DIM) return false;
     if (plan < 0 || plan >= NUM_PLANS) return false;
@@ -179,7 +189,7 @@ bool supports(int plan, int64_t M, int64_t N, int64_t K, bool residual) {
         case KIND_GENERIC:
             return cdiv(M, 64) * cdiv(N, 64) * 256 <= LIMIT_ITEMS;
         case KIND_SKINNY: {
-            if (M < 1 || M > 64 || K % 8 != 0) return false;
+            if (lay.general || M < 1 || M > 64 || K % 8 != 0) return false;
             if (N * K * 2 >= PANEL_LIMIT || 64 * K * 2 >= PANEL_LIMIT) return false;
             const int split = skinny_split_of(plan, M, N, K);
             if (cdiv(N, 16) * split * 512 > LIMIT_ITEMS) return false;
@@ -189,9 +199,10 @@ bool supports(int plan, int64_t M, int64_t N, int64_t K, bool residual) {
             return true;
         }
         case KIND_GEMV:
-            return gemv_fits(M, N, K) && cdiv(N, 4) * 256 <= LIMIT_ITEMS;
+            return gemv_fits(M, N, K, lay.ldw) && cdiv(N, 4) * 256 <= LIMIT_ITEMS &&
+                   strided_bytes(M, N, lay.ldy) < PANEL_LIMIT && strided_bytes(M, N, lay.ldr) < PANEL_LIMIT;
         case KIND_STREAM: {
-            if (M < 1 || M > 64 || K % 8 != 0) return false;
+            if (lay.general || M < 1 || M > 64 || K % 8 != 0) return false;
             if (64 * K * 2 >= PANEL_LIMIT || M * N * 2 >= PANEL_LIMIT) return false;
             const int split = stream_split_of(plan, M, N, K);
             if (cdiv(N, 64) * split * 256 > LIMIT_ITEMS) return false;
@@ -203,8 +214,11 @@ bool supports(int plan, int64_t M, int64_t N, int64_t K, bool residual) {
         case KIND_TILE: {
             const TileShape ts = tile_shape(pi.tile_cfg);
             if (K % 8 != 0) return false;
-            if (int64_t{ts.bm} * K * 2 >= PANEL_LIMIT || int64_t{ts.bn} * K * 2 >= PANEL_LIMIT) return false;
-            if (int64_t{ts.bm} * N * 2 >= PANEL_LIMIT) return false;   // epilogue panel of R / Y
+            if (strided_bytes(ts.bm, K, lay.ldx) >= PANEL_LIMIT || strided_bytes(ts.bn, K, lay.ldw) >= PANEL_LIMIT)
+                return false;
+            // epilogue panels of R and Y
+            if (strided_bytes(ts.bm, N, lay.ldy) >= PANEL_LIMIT || strided_bytes(ts.bm, N, lay.ldr) >= PANEL_LIMIT)
+                return false;
             const int64_t tiles = tile_count(ts, M, N);
             const TileSplit sp = tile_split_plan(plan, M, N, K);
             const int64_t split_tiles = tiles - sp.full_tiles;
@@ -265,17 +279,17 @@ const TableEntry TABLE[] = {
 // fills the 256 CUs (tail split: the tiles of a partial last round are split
 // in K), the 256x128 8-wave tile (3 stages, lagged refill) when that fills
 // them, else the 128x128 tile.
-int select(int64_t M, int64_t N, int64_t K, bool residual) {
+int select(int64_t M, int64_t N, int64_t K, bool residual, const Layout &lay) {
     if (M < 0 || N < 0 || K < 0) return -1;
     for (const TableEntry &e : TABLE) {
         if (e.M < 0 || e.M != M || e.N != N || e.K != K || (e.residual != 0) != residual) continue;
         const int plan = plan_index(e.plan);
-        if (plan >= 0 && supports(plan, M, N, K, residual)) return plan;
+        if (plan >= 0 && supports(plan, M, N, K, residual, lay)) return plan;
     }
     if (K % 8 != 0) return PLAN_GENERIC;
     auto pick = [&](const char *name) {
         const int plan = plan_index(name);
-        return (plan >= 0 && supports(plan, M, N, K, residual)) ? plan : -1;
+        return (plan >= 0 && supports(plan, M, N, K, residual, lay)) ? plan : -1;
     };
     int plan = -1;
     if (M >= 1 && M <= 4) plan = pick("gemv_valu_w4");
@@ -283,6 +297,7 @@ int select(int64_t M, int64_t N, int64_t K, bool residual) {
     if (M >= 1 && M <= 32) {
         plan = pick("stream_mfma16_k64_splitk");
         if (plan < 0) plan = pick("skinny_mfma16_w8");
+        if (plan < 0) plan = pick("tile_64x64_k128s3_w4_splitk");   // general form
     } else if (M <= 1024) {
         const int64_t tiles64 = tile_count(tile_shape(TC_64x64_K64_S4_W4), M, N);
         const int64_t tiles128 = tile_count(tile_shape(TC_128x128_K64_S4_W4_L), M, N);
@@ -376,46 +391,76 @@ bool overlaps(const void *a, int64_t abytes, const void *b, int64_t bbytes) {
 
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+// One call as the entry points pass it (leading dimensions in elements).
+struct Request {
+    int64_t M, N, K;
+    float alpha;
+    const void *X;
+    int64_t ldx;
+    const void *W;
+    int64_t ldw;
+    float beta;
+    const void *R;    // residual / C; null: none
+    int64_t ldr;
+    const void *bias; // [N] or null
+    void *Y;
+    int64_t ldy;
+};
+
 // plan < 0: choose; otherwise run exactly that plan.
-int run(int plan, int64_t M, int64_t N, int64_t K, const void *X, const void *W, const void *R,
-        void *Y, bool residual, hipStream_t stream) {
+int run(int plan, Request q, hipStream_t stream) {
     g_last_error[0] = '\0';
+    const int64_t M = q.M, N = q.N, K = q.K;
     if (M < 0 || N < 0 || K < 0)
         return fail(KERNELARC_ERR_INVALID_ARG, "negative size M=%lld N=%lld K=%lld", (long long)M,
                     (long long)N, (long long)K);
     if (M > LIMIT_DIM || N > LIMIT_DIM || K > LIMIT_DIM)
         return fail(KERNELARC_ERR_INVALID_ARG, "a size is 2^31 or more");
     if (plan >= NUM_PLANS) return fail(KERNELARC_ERR_UNSUPPORTED, "unknown plan %d", plan);
+    if (q.beta == 0.0f) q.R = nullptr;   // beta = 0: the residual term is not read
+    const bool residual = q.R != nullptr;
+    if (q.ldx < 0 || q.ldw < 0 || q.ldy < 0 || q.ldr < 0 || q.ldx > LIMIT_DIM || q.ldw > LIMIT_DIM ||
+        q.ldy > LIMIT_DIM || q.ldr > LIMIT_DIM)
+        return fail(KERNELARC_ERR_INVALID_ARG, "a leading dimension is negative or 2^31 or more");
     if (M == 0 || N == 0) return KERNELARC_OK;
-    if (!Y) return fail(KERNELARC_ERR_INVALID_ARG, "Y is NULL");
-    if (K > 0 && (!X || !W)) return fail(KERNELARC_ERR_INVALID_ARG, "X or W is NULL");
-    if (residual && !R) return fail(KERNELARC_ERR_INVALID_ARG, "R is NULL");
-    const int64_t ybytes = M * N * 2;
-    if (overlaps(Y, ybytes, X, M * K * 2) || overlaps(Y, ybytes, W, N * K * 2))
+    if (!q.Y) return fail(KERNELARC_ERR_INVALID_ARG, "Y is NULL");
+    if (K > 0 && (!q.X || !q.W)) return fail(KERNELARC_ERR_INVALID_ARG, "X or W is NULL");
+    if (q.ldy < N || (residual && q.ldr < N) || (K > 0 && (q.ldx < K || q.ldw < K)))
+        return fail(KERNELARC_ERR_INVALID_ARG, "a leading dimension is smaller than its row length");
+    const int64_t ybytes = strided_bytes(M, N, q.ldy);
+    if (overlaps(q.Y, ybytes, q.X, strided_bytes(M, K, q.ldx)) || overlaps(q.Y, ybytes, q.W, strided_bytes(N, K, q.ldw)))
         return fail(KERNELARC_ERR_INVALID_ARG, "Y overlaps X or W");
-    if (residual && R != Y && overlaps(Y, ybytes, R, ybytes))
-        return fail(KERNELARC_ERR_INVALID_ARG, "Y partially overlaps R (only Y == R is allowed)");
+    if (overlaps(q.Y, ybytes, q.bias, N * 2)) return fail(KERNELARC_ERR_INVALID_ARG, "Y overlaps the bias");
+    if (residual && !(q.R == q.Y && q.ldr == q.ldy) && overlaps(q.Y, ybytes, q.R, strided_bytes(M, N, q.ldr)))
+        return fail(KERNELARC_ERR_INVALID_ARG,
+                    "Y partially overlaps R (only Y == R with the same leading dimension is allowed)");
 
     int dev = 0, num_cus = 0;
     const int st = current_device(&dev, &num_cus);
     if (st != KERNELARC_OK) return st;
 
-    const bool vec_ok = aligned16(X) && aligned16(W) && aligned16(Y) && (!residual || aligned16(R)) &&
-                        K % 8 == 0;
+    const Layout lay{q.ldx, q.ldw, residual ? q.ldr : N, q.ldy,
+                     q.ldx != K || q.ldw != K || (residual && q.ldr != N) || q.ldy != N || q.alpha != 1.0f ||
+                         q.beta != 1.0f || q.bias != nullptr};
+    // 16-byte operand loads need every row of X and W 16-byte aligned.
+    const bool vec_ok = aligned16(q.X) && aligned16(q.W) && aligned16(q.Y) && (!residual || aligned16(q.R)) &&
+                        K % 8 == 0 && q.ldx % 8 == 0 && q.ldw % 8 == 0;
     if (plan < 0) {
-        plan = select(M, N, K, residual);
+        plan = select(M, N, K, residual, lay);
         if (plan != PLAN_GENERIC && !vec_ok) plan = PLAN_GENERIC;
     } else {
-        if (!supports(plan, M, N, K, residual))
-            return fail(KERNELARC_ERR_UNSUPPORTED, "plan %s cannot compute M=%lld N=%lld K=%lld",
-                        PLANS[plan].name, (long long)M, (long long)N, (long long)K);
+        if (!supports(plan, M, N, K, residual, lay))
+            return fail(KERNELARC_ERR_UNSUPPORTED, "plan %s cannot compute M=%lld N=%lld K=%lld%s",
+                        PLANS[plan].name, (long long)M, (long long)N, (long long)K,
+                        lay.general ? " in the general form" : "");
         if (plan != PLAN_GENERIC && !vec_ok)
-            return fail(KERNELARC_ERR_UNSUPPORTED, "plan %s needs 16-byte aligned pointers and K %% 8 == 0",
-                        PLANS[plan].name);
+            return fail(KERNELARC_ERR_UNSUPPORTED,
+                        "plan %s needs 16-byte aligned pointers and K, ldx, ldw multiples of 8", PLANS[plan].name);
     }
 
-    Problem p{M, N, K, static_cast<const uint16_t *>(X), static_cast<const uint16_t *>(W),
-              residual ? static_cast<const uint16_t *>(R) : nullptr, static_cast<uint16_t *>(Y)};
+    Problem p{M, N, K, static_cast<const uint16_t *>(q.X), static_cast<const uint16_t *>(q.W),
+              static_cast<const uint16_t *>(q.R), static_cast<uint16_t *>(q.Y), q.ldx, q.ldw, lay.ldr, q.ldy,
+              q.alpha, residual ? q.beta : 1.0f, static_cast<const uint16_t *>(q.bias)};
     (void)hipGetLastError();   // clear any stale error before launching
     hipError_t e = hipSuccess;
     switch (PLANS[plan].kind) {
@@ -468,14 +513,22 @@ using namespace kernelarc;
 
 extern "C" {
 
+Request dense_request(int64_t M, int64_t N, int64_t K, const void *X, const void *W, const void *R, void *Y) {
+    return Request{M, N, K, 1.0f, X, K, W, K, 1.0f, R, N, nullptr, Y, N};
+}
+
 int kernelarc_gemm_bf16_residual(int64_t M, int64_t N, int64_t K, const void *X, const void *W,
                                  const void *R, void *Y, hipStream_t stream) {
-    return run(-1, M, N, K, X, W, R, Y, true, stream);
+    if (!R && M > 0 && N > 0) {
+        g_last_error[0] = '\0';
+        return fail(KERNELARC_ERR_INVALID_ARG, "R is NULL");
+    }
+    return run(-1, dense_request(M, N, K, X, W, R, Y), stream);
 }
 
 int kernelarc_gemm_bf16(int64_t M, int64_t N, int64_t K, const void *X, const void *W, void *Y,
                         hipStream_t stream) {
-    return run(-1, M, N, K, X, W, nullptr, Y, false, stream);
+    return run(-1, dense_request(M, N, K, X, W, nullptr, Y), stream);
 }
 
 int kernelarc_gemm_bf16_with_plan(int plan, int64_t M, int64_t N, int64_t K, const void *X,
@@ -484,7 +537,33 @@ int kernelarc_gemm_bf16_with_plan(int plan, int64_t M, int64_t N, int64_t K, con
         g_last_error[0] = '\0';
         return fail(KERNELARC_ERR_UNSUPPORTED, "unknown plan %d", plan);
     }
-    return run(plan, M, N, K, X, W, R, Y, R != nullptr, stream);
+    return run(plan, dense_request(M, N, K, X, W, R, Y), stream);
+}
+
+int kernelarc_gemm_bf16_ex(int64_t M, int64_t N, int64_t K, float alpha, const void *X, int64_t ldx,
+                           const void *W, int64_t ldw, float beta, const void *C, int64_t ldc, const void *bias,
+                           void *Y, int64_t ldy, hipStream_t stream) {
+    return run(-1, Request{M, N, K, alpha, X, ldx, W, ldw, beta, C, ldc, bias, Y, ldy}, stream);
+}
+
+int kernelarc_gemm_bf16_ex_with_plan(int plan, int64_t M, int64_t N, int64_t K, float alpha, const void *X,
+                                     int64_t ldx, const void *W, int64_t ldw, float beta, const void *C,
+                                     int64_t ldc, const void *bias, void *Y, int64_t ldy, hipStream_t stream) {
+    if (plan < 0) {
+        g_last_error[0] = '\0';
+        return fail(KERNELARC_ERR_UNSUPPORTED, "unknown plan %d", plan);
+    }
+    return run(plan, Request{M, N, K, alpha, X, ldx, W, ldw, beta, C, ldc, bias, Y, ldy}, stream);
+}
+
+int kernelarc_select_plan_ex(int64_t M, int64_t N, int64_t K, int has_c, int64_t ldx, int64_t ldw, int64_t ldc,
+                             int64_t ldy, float alpha, float beta, int has_bias) {
+    if (M < 0 || N < 0 || K < 0) return -1;
+    const bool residual = has_c != 0 && beta != 0.0f;
+    const Layout lay{ldx, ldw, residual ? ldc : N, ldy,
+                     ldx != K || ldw != K || (residual && ldc != N) || ldy != N || alpha != 1.0f || beta != 1.0f ||
+                         has_bias != 0};
+    return select(M, N, K, residual, lay);
 }
 
 int kernelarc_plan_count(void) { return NUM_PLANS; }
@@ -495,15 +574,15 @@ const char *kernelarc_plan_name(int plan) {
 
 int kernelarc_plan_supports(int plan, int64_t M, int64_t N, int64_t K, int residual) {
     if (plan < 0 || plan >= NUM_PLANS || M < 0 || N < 0 || K < 0) return -1;
-    return supports(plan, M, N, K, residual != 0) ? 1 : 0;
+    return supports(plan, M, N, K, residual != 0, dense_layout(N, K)) ? 1 : 0;
 }
 
 int kernelarc_select_plan(int64_t M, int64_t N, int64_t K, int residual) {
-    return select(M, N, K, residual != 0);
+    return select(M, N, K, residual != 0, dense_layout(N, K));
 }
 
 int kernelarc_plan_uses_workspace(int plan, int64_t M, int64_t N, int64_t K) {
-    if (!supports(plan, M, N, K, true)) return 0;
+    if (!supports(plan, M, N, K, true, dense_layout(N, K))) return 0;
     if (PLANS[plan].kind == KIND_SKINNY) return skinny_split_of(plan, M, N, K) > 1 ? 1 : 0;
     if (PLANS[plan].kind == KIND_TILE) return tile_split_of(plan, M, N, K) > 1 ? 1 : 0;
     if (PLANS[plan].kind == KIND_STREAM) return stream_split_of(plan, M, N, K) > 1 ? 1 : 0;

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 namespace kernelarc {
 
 // ---------------------------------------------------------------- plans ----
@@ -55,11 +57,55 @@ struct TileShape {
 };
 TileShape tile_shape(int cfg);
 
+// One call: Y = bf16(alpha * X W^T + beta * R + bias) with row strides
+// (in elements).  The plain entry points pass dense strides (K, K, N, N),
+// alpha = beta = 1 and no bias; R and bias may be null.
 struct Problem {
     int64_t M, N, K;
-    const uint16_t *X, *W, *R;   // R may be null (plain variant)
+    const uint16_t *X, *W, *R;   // R may be null (no residual term)
+    uint16_t *Y;
+    int64_t ldx, ldw, ldr, ldy;
+    float alpha, beta;
+    const uint16_t *bias;        // [N] or null
+};
+
+// The plain operator's arguments alone (dense strides, alpha = beta = 1, no
+// bias): what the kernels of the plain entry points receive, so their
+// argument block and its loads stay as small as the operation needs.
+struct DenseProblem {
+    int64_t M, N, K;
+    const uint16_t *X, *W, *R;
     uint16_t *Y;
 };
+
+// Uniform access to either form inside the kernels.
+__host__ __device__ inline int64_t ldx_of(const Problem &p) { return p.ldx; }
+__host__ __device__ inline int64_t ldw_of(const Problem &p) { return p.ldw; }
+__host__ __device__ inline int64_t ldr_of(const Problem &p) { return p.ldr; }
+__host__ __device__ inline int64_t ldy_of(const Problem &p) { return p.ldy; }
+__host__ __device__ inline float alpha_of(const Problem &p) { return p.alpha; }
+__host__ __device__ inline float beta_of(const Problem &p) { return p.beta; }
+__host__ __device__ inline const uint16_t *bias_of(const Problem &p) { return p.bias; }
+__host__ __device__ inline int64_t ldx_of(const DenseProblem &p) { return p.K; }
+__host__ __device__ inline int64_t ldw_of(const DenseProblem &p) { return p.K; }
+__host__ __device__ inline int64_t ldr_of(const DenseProblem &p) { return p.N; }
+__host__ __device__ inline int64_t ldy_of(const DenseProblem &p) { return p.N; }
+__host__ __device__ inline float alpha_of(const DenseProblem &) { return 1.0f; }
+__host__ __device__ inline float beta_of(const DenseProblem &) { return 1.0f; }
+__host__ __device__ inline const uint16_t *bias_of(const DenseProblem &) { return nullptr; }
+
+// True unless the call is the plain operator (then the dense kernels run).
+inline bool is_general(const Problem &p) {
+    return p.ldx != p.K || p.ldw != p.K || (p.R && p.ldr != p.N) || p.ldy != p.N || p.alpha != 1.0f ||
+           (p.R && p.beta != 1.0f) || p.bias != nullptr;
+}
+inline DenseProblem dense_of(const Problem &p) { return DenseProblem{p.M, p.N, p.K, p.X, p.W, p.R, p.Y}; }
+
+// Bytes a buffer resource must cover for `rows` rows of `cols` elements at
+// row stride `ld` (the last row ends at its last element).
+__host__ __device__ inline int64_t strided_bytes(int64_t rows, int64_t cols, int64_t ld) {
+    return rows > 0 && cols > 0 ? ((rows - 1) * ld + cols) * 2 : 0;
+}
 
 // Per-device split-K workspace: fp32 partials followed by tile counters.
 struct Workspace {
@@ -83,7 +129,7 @@ hipError_t launch_stream(const Problem &p, int bk, int split, const Workspace *w
 int skinny_split_for(int64_t M, int64_t N, int64_t K);
 int64_t skinny_workspace_floats(int64_t M, int64_t N, int split_k);
 int64_t skinny_counter_count(int64_t N);
-bool gemv_fits(int64_t M, int64_t N, int64_t K);
+bool gemv_fits(int64_t M, int64_t N, int64_t K, int64_t ldw);
 int stream_split_for(int64_t M, int64_t N, int64_t K, int bk);
 int64_t stream_workspace_floats(int64_t M, int64_t N, int split);
 int64_t stream_counter_count(int64_t N);
@@ -102,6 +148,14 @@ __device__ __forceinline__ float bf16_to_f32(uint16_t b) {
 // one of the 2^32 inputs.
 __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
     return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f));
+}
+
+// The epilogue's value before rounding: alpha * acc, then + beta * r as one
+// fused multiply-add when there is a residual.  With alpha = beta = 1 this is
+// exactly acc + r (one rounding), the plain operator's value.
+__device__ __forceinline__ float combine(float acc, float r, bool has_r, float alpha, float beta) {
+    const float a = alpha * acc;
+    return has_r ? __builtin_fmaf(beta, r, a) : a;
 }
 
 // Two values at once (one v_cvt_pk_bf16_f32): lo in bits 0-15, hi in 16-31.

@@ -1,4 +1,5 @@
-// GEMV kernel for M <= 4 tokens: Y = X W^T (+ R) as a pure stream over W.
+// GEMV kernel for M <= 4 tokens: Y = alpha X W^T (+ beta R) (+ bias) as a
+// pure stream over W.
 //
 // With one to four tokens the multiply is negligible and the time is the
 // single pass over W (N*K*2 bytes).  The measured best way to stream HBM on
@@ -8,9 +9,10 @@
 // rows.  The dot products run on the VALU with v_dot2_f32_bf16 (bf16 pairs,
 // fp32 accumulation) -- at M <= 4 that is a few percent of the VALU's rate.
 //
-//   * X (M x K, at most 64 KB) is copied to LDS once per workgroup with
-//     LDS-direct loads (1 KB each, all in flight together); lane l reads the
-//     8 values of X that face its 16 bytes of W.
+//   * X (M rows of K, each row padded to whole kilobytes in LDS, at most
+//     64 KB) is copied to LDS once per workgroup with LDS-direct loads (1 KB
+//     each, all in flight together); lane l reads the 8 values of X that
+//     face its 16 bytes of W.
 //   * a wave owns RPW consecutive rows and walks them k-segment by
 //     k-segment (all rows of a segment share one read of X from LDS), two
 //     batches of BATCH loads in flight;
@@ -36,7 +38,10 @@ constexpr int WAVES = 4;
 constexpr int THREADS = 64 * WAVES;
 constexpr int BATCH = 4;                 // loads per batch (one kilobyte each)
 constexpr int MAX_ROWS_PER_WAVE = 4;     // a batch must hold whole segments
-constexpr int X_LDS_BYTES = 64 * 1024;   // X lives in LDS: M * K * 2 <= 64 KB
+constexpr int X_LDS_BYTES = 64 * 1024;   // X lives in LDS: M rows of x_pitch(K) bytes
+
+// LDS bytes of one row of X: K * 2 rounded up to whole 1 KB loads.
+__host__ __device__ inline int64_t x_pitch(int64_t K) { return (K * 2 + 1023) / 1024 * 1024; }
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, uint32_t bytes) {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), static_cast<short>(0),
@@ -66,8 +71,12 @@ __device__ __forceinline__ float wave_sum(float v) {
     return v;
 }
 
-template <int MT, int RPW>
-__global__ __launch_bounds__(THREADS) void gemv_kernel(Problem p) {
+// P = Problem: the general form (row strides, alpha, beta, bias);
+// P = DenseProblem: dense operands, the residual added as is (the plain
+// operator).
+template <int MT, int RPW, class P>
+__global__ __launch_bounds__(THREADS) void gemv_kernel(P p) {
+    constexpr bool GEN = std::is_same<P, Problem>::value;
     extern __shared__ __attribute__((aligned(16))) char xs[];   // X, M * K * 2 bytes
 
     const int lane = threadIdx.x & 63;
@@ -82,25 +91,43 @@ __global__ __launch_bounds__(THREADS) void gemv_kernel(Problem p) {
     const int my_t = lane / RPW;
     const int my_r = lane % RPW;
     const bool writer = my_t < MT && my_t < p.M && row0 + my_r < N;
-    const uint32_t y_off = writer ? static_cast<uint32_t>((my_t * N + row0 + my_r) * 2) : OOB_OFFSET;
-    const __amdgpu_buffer_rsrc_t rr = make_rsrc(p.R ? p.R : p.Y, p.R ? static_cast<uint32_t>(p.M * N * 2) : 0u);
-    const uint16_t rbits = __builtin_amdgcn_raw_buffer_load_b16(rr, y_off, 0, 0);
+    const int64_t ldx = ldx_of(p), ldw = ldw_of(p), ldr = ldr_of(p), ldy = ldy_of(p);
+    const uint32_t r_off = writer ? static_cast<uint32_t>((my_t * ldr + row0 + my_r) * 2) : OOB_OFFSET;
+    const __amdgpu_buffer_rsrc_t rr = make_rsrc(
+        p.R ? p.R : p.Y, p.R ? static_cast<uint32_t>(GEN ? strided_bytes(p.M, N, ldr) : p.M * N * 2) : 0u);
+    const uint16_t rbits = __builtin_amdgcn_raw_buffer_load_b16(rr, r_off, 0, 0);
+    uint16_t bbits = 0;
+    if constexpr (GEN) {
+        const __amdgpu_buffer_rsrc_t rbias =
+            make_rsrc(bias_of(p) ? bias_of(p) : p.Y, bias_of(p) ? static_cast<uint32_t>(N * 2) : 0u);
+        bbits = __builtin_amdgcn_raw_buffer_load_b16(rbias, writer ? static_cast<uint32_t>((row0 + my_r) * 2) : OOB_OFFSET, 0, 0);
+    }
 
     // X -> LDS: every wave issues its share of the 1 KB LDS-direct loads
-    // (X is M*K*2 contiguous bytes; the tail past it reads zero), then one
-    // wait and one barrier.
-    {
+    // (row t of X goes to xs + t * x_pitch(K); a row's tail past K reads
+    // zero), then one wait and one barrier.
+    const int64_t xp = GEN ? x_pitch(K) : K * 2;
+    if constexpr (GEN) {
+        const int per_row = static_cast<int>(xp / 1024);
+        for (int t = 0; t < p.M; ++t) {
+            const __amdgpu_buffer_rsrc_t rxs = make_rsrc(p.X + t * ldx, static_cast<uint32_t>(K * 2));
+            for (int c = wave; c < per_row; c += WAVES)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rxs, (lds_void *)(xs + t * xp + c * 1024), 16,
+                                                         static_cast<uint32_t>(c * 1024 + lane * 16), 0, 0, 0);
+        }
+    } else {
+        // dense X: M*K*2 contiguous bytes, the tail past it reads zero
         const uint32_t xbytes = static_cast<uint32_t>(p.M * K * 2);
         const __amdgpu_buffer_rsrc_t rxs = make_rsrc(p.X, xbytes);
         const int xloads = static_cast<int>((xbytes + 1023) / 1024);
         for (int q = wave; q < xloads; q += WAVES)
             __builtin_amdgcn_raw_ptr_buffer_load_lds(rxs, (lds_void *)(xs + q * 1024), 16,
                                                      static_cast<uint32_t>(q * 1024 + lane * 16), 0, 0, 0);
-        __builtin_amdgcn_s_waitcnt(WAITCNT_VM0);
     }
+    __builtin_amdgcn_s_waitcnt(WAITCNT_VM0);
     __syncthreads();
 
-    const __amdgpu_buffer_rsrc_t rw = make_rsrc(p.W, static_cast<uint32_t>(N * K * 2));
+    const __amdgpu_buffer_rsrc_t rw = make_rsrc(p.W, static_cast<uint32_t>(GEN ? strided_bytes(N, K, ldw) : N * K * 2));
     float acc[RPW][MT];
 #pragma unroll
     for (int r = 0; r < RPW; ++r)
@@ -116,7 +143,7 @@ __global__ __launch_bounds__(THREADS) void gemv_kernel(Problem p) {
         for (int b = 0; b < BATCH; ++b) {
             const int64_t k = static_cast<int64_t>(seg0 + b / RPW) * 512 + lane * 8;
             const int64_t row = row0 + b % RPW;
-            const uint32_t off = (row < N && k < K) ? static_cast<uint32_t>(row * K * 2 + k * 2) : OOB_OFFSET;
+            const uint32_t off = (row < N && k < K) ? static_cast<uint32_t>(row * ldw * 2 + k * 2) : OOB_OFFSET;
             wv[b] = __builtin_amdgcn_raw_buffer_load_b128(rw, off, 0, AUX_NT);
         }
     };
@@ -128,7 +155,7 @@ __global__ __launch_bounds__(THREADS) void gemv_kernel(Problem p) {
 #pragma unroll
             for (int t = 0; t < MT; ++t) {
                 if (t >= p.M) break;
-                const i32x4 xv = *reinterpret_cast<const i32x4 *>(xs + (t * K + k) * 2);
+                const i32x4 xv = *reinterpret_cast<const i32x4 *>(xs + t * xp + k * 2);
 #pragma unroll
                 for (int r = 0; r < RPW; ++r) acc[r][t] = dot8(wv[sb * RPW + r], xv, acc[r][t]);
             }
@@ -159,24 +186,37 @@ __global__ __launch_bounds__(THREADS) void gemv_kernel(Problem p) {
             if (lane == t * RPW + r) mine = v;
         }
     if (writer) {
-        float y = mine;
-        if (p.R) y += bf16_to_f32(rbits);
-        p.Y[my_t * N + row0 + my_r] = f32_to_bf16_rne(y);
+        float y;
+        if constexpr (GEN) {
+            y = combine(mine, bf16_to_f32(rbits), p.R != nullptr, alpha_of(p), beta_of(p));
+            if (bias_of(p)) y += bf16_to_f32(bbits);
+        } else {
+            y = mine;
+            if (p.R) y += bf16_to_f32(rbits);
+        }
+        p.Y[my_t * ldy + row0 + my_r] = f32_to_bf16_rne(y);
     }
+}
+
+template <int MT, class P>
+hipError_t launch_mt(const P &p, int rpw, hipStream_t s) {
+    constexpr bool GEN = std::is_same<P, Problem>::value;
+    const int64_t rows_per_wg = static_cast<int64_t>(rpw) * WAVES;
+    const dim3 grid(static_cast<unsigned>((p.N + rows_per_wg - 1) / rows_per_wg));
+    // whole 1 KB loads per row (general form) or over the dense X
+    const size_t lds = static_cast<size_t>(GEN ? p.M * x_pitch(p.K) : (p.M * p.K * 2 + 1023) / 1024 * 1024);
+    switch (rpw) {
+        case 1: hipLaunchKernelGGL((gemv_kernel<MT, 1, P>), grid, dim3(THREADS), lds, s, p); break;
+        case 2: hipLaunchKernelGGL((gemv_kernel<MT, 2, P>), grid, dim3(THREADS), lds, s, p); break;
+        case 4: hipLaunchKernelGGL((gemv_kernel<MT, 4, P>), grid, dim3(THREADS), lds, s, p); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
 }
 
 template <int MT>
 hipError_t launch_mt(const Problem &p, int rpw, hipStream_t s) {
-    const int64_t rows_per_wg = static_cast<int64_t>(rpw) * WAVES;
-    const dim3 grid(static_cast<unsigned>((p.N + rows_per_wg - 1) / rows_per_wg));
-    const size_t lds = static_cast<size_t>((p.M * p.K * 2 + 1023) / 1024 * 1024);   // whole 1 KB loads
-    switch (rpw) {
-        case 1: hipLaunchKernelGGL((gemv_kernel<MT, 1>), grid, dim3(THREADS), lds, s, p); break;
-        case 2: hipLaunchKernelGGL((gemv_kernel<MT, 2>), grid, dim3(THREADS), lds, s, p); break;
-        case 4: hipLaunchKernelGGL((gemv_kernel<MT, 4>), grid, dim3(THREADS), lds, s, p); break;
-        default: return hipErrorInvalidValue;
-    }
-    return hipGetLastError();
+    return is_general(p) ? launch_mt<MT, Problem>(p, rpw, s) : launch_mt<MT, DenseProblem>(dense_of(p), rpw, s);
 }
 
 }  // namespace
@@ -191,8 +231,9 @@ int gemv_rows_per_wave(int64_t M, int64_t N, int64_t K) {
     return rpw;
 }
 
-bool gemv_fits(int64_t M, int64_t N, int64_t K) {
-    return M >= 1 && M <= 4 && K % 8 == 0 && M * K * 2 <= X_LDS_BYTES && N * K * 2 < (int64_t{1} << 31);
+bool gemv_fits(int64_t M, int64_t N, int64_t K, int64_t ldw) {
+    return M >= 1 && M <= 4 && K % 8 == 0 && M * x_pitch(K) <= X_LDS_BYTES &&
+           strided_bytes(N, K, ldw) < (int64_t{1} << 31);
 }
 
 hipError_t launch_gemv(const Problem &p, hipStream_t s) {

@@ -1,4 +1,5 @@
-// Generic kernel: Y = X W^T (+ R) for any shape and any pointer alignment.
+// Generic kernel: Y = alpha X W^T (+ beta R) (+ bias) for any shape, any
+// row strides and any pointer alignment.
 //
 // This is the correctness fallback (K not a multiple of 8, pointers not
 // 16-byte aligned).  Each 256-thread workgroup computes a 64x64 output tile;
@@ -40,8 +41,8 @@ __global__ __launch_bounds__(256) void generic_kernel(Problem p, int64_t tiles_n
             const int64_t k = k0 + kk;
             const int64_t xm = m0 + r;
             const int64_t wn = n0 + r;
-            xs[kk][r] = (xm < p.M && k < p.K) ? bf16_to_f32(p.X[xm * p.K + k]) : 0.0f;
-            ws[kk][r] = (wn < p.N && k < p.K) ? bf16_to_f32(p.W[wn * p.K + k]) : 0.0f;
+            xs[kk][r] = (xm < p.M && k < p.K) ? bf16_to_f32(p.X[xm * p.ldx + k]) : 0.0f;
+            ws[kk][r] = (wn < p.N && k < p.K) ? bf16_to_f32(p.W[wn * p.ldw + k]) : 0.0f;
         }
         __syncthreads();
 #pragma unroll
@@ -67,9 +68,10 @@ __global__ __launch_bounds__(256) void generic_kernel(Problem p, int64_t tiles_n
         for (int b = 0; b < 4; ++b) {
             const int64_t j = n0 + tx + 16 * b;
             if (j >= p.N) continue;
-            float y = acc[a][b];
-            if (p.R) y += bf16_to_f32(p.R[i * p.N + j]);
-            p.Y[i * p.N + j] = f32_to_bf16_rne(y);
+            const float r = p.R ? bf16_to_f32(p.R[i * p.ldr + j]) : 0.0f;
+            float y = combine(acc[a][b], r, p.R != nullptr, p.alpha, p.beta);
+            if (p.bias) y += bf16_to_f32(p.bias[j]);
+            p.Y[i * p.ldy + j] = f32_to_bf16_rne(y);
         }
     }
 }

@@ -76,7 +76,7 @@ __device__ __forceinline__ void mfma_batch(f32x4 (&acc)[MB], const i32x4 (&wv)[U
 }
 
 template <int MB>
-__global__ __launch_bounds__(THREADS) void skinny_kernel(Problem p, int split, int64_t kslice,
+__global__ __launch_bounds__(THREADS) void skinny_kernel(DenseProblem p, int split, int64_t kslice,
                                                          float *ws, unsigned *counters) {
     constexpr int MP = 16 * MB;                         // padded token count
     constexpr int U = MB <= 2 ? 8 : 4;                  // MFMA steps per batch of loads
@@ -218,7 +218,7 @@ hipError_t launch_mb(const Problem &p, int split, const Workspace *ws, hipStream
     float *partials = split > 1 ? ws->partials : nullptr;
     unsigned *counters = split > 1 ? ws->counters : nullptr;
     hipLaunchKernelGGL(skinny_kernel<MB>, dim3(static_cast<unsigned>(strips * split)), dim3(THREADS), 0,
-                       s, p, split, kslice, partials, counters);
+                       s, dense_of(p), split, kslice, partials, counters);
     return hipGetLastError();
 }
 

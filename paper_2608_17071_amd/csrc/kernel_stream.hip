@@ -81,7 +81,7 @@ struct StreamCfg {
 };
 
 template <int MB, int BK>
-__global__ __launch_bounds__(THREADS) void stream_kernel(Problem p, int64_t nblocks, StreamSplit sk) {
+__global__ __launch_bounds__(THREADS) void stream_kernel(DenseProblem p, int64_t nblocks, StreamSplit sk) {
     using C = StreamCfg<MB, BK>;
     __shared__ __attribute__((aligned(1024))) char lds[C::LDS_BYTES];
 
@@ -309,7 +309,7 @@ hipError_t launch_mb(const Problem &p, int split, const Workspace *ws, hipStream
         sk.counters = ws->counters;
     }
     hipLaunchKernelGGL((stream_kernel<MB, BK>), dim3(static_cast<unsigned>(nblocks * sk.split)), dim3(THREADS), 0,
-                       s, p, nblocks, sk);
+                       s, dense_of(p), nblocks, sk);
     return hipGetLastError();
 }
 

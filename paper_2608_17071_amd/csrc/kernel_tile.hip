@@ -1,4 +1,5 @@
-// MFMA macro-tile kernels for Y = X W^T (+ R): the compute-bound path.
+// MFMA macro-tile kernels for Y = alpha X W^T (+ beta R) (+ bias): the
+// compute-bound path.  Operands may be row-strided (leading dimensions).
 //
 // One workgroup of WAVES_M x WAVES_N waves computes a BM x BN output tile;
 // each wave owns a (BM/WAVES_M) x (BN/WAVES_N) block made of 32x32
@@ -203,10 +204,15 @@ struct SplitK {
     int64_t full_tiles;
 };
 
-template <class C>
+// P = Problem: the general form (row strides, alpha, beta, bias);
+// P = DenseProblem: dense operands, and the epilogue adds R as is (the plain
+// operator).
+template <class C, class P>
 __global__ __attribute__((amdgpu_flat_work_group_size(C::THREADS, C::THREADS),
                           amdgpu_waves_per_eu(C::WAVES_PER_EU, C::WAVES_PER_EU)))
-void tile_kernel(Problem p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) {
+void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) {
+    constexpr bool GEN = std::is_same<P, Problem>::value;
+    const int64_t ldx = ldx_of(p), ldw = ldw_of(p), ldr = ldr_of(p), ldy = ldy_of(p);
     __shared__ __attribute__((aligned(1024))) char lds[C::LDS_BYTES];
 
     const int lane = threadIdx.x & 63;
@@ -263,8 +269,10 @@ void tile_kernel(Problem p, int64_t tiles_m, int64_t tiles_n, int group_m, Split
     // Operand panels bounded by buffer resources: rows past M (N) read 0.
     const int64_t rows_a = (p.M - m0) < C::BM ? (p.M - m0) : C::BM;
     const int64_t rows_b = (p.N - n0) < C::BN ? (p.N - n0) : C::BN;
-    const __amdgpu_buffer_rsrc_t ra = make_rsrc(p.X + m0 * K, static_cast<uint32_t>(rows_a * K * 2));
-    const __amdgpu_buffer_rsrc_t rb = make_rsrc(p.W + n0 * K, static_cast<uint32_t>(rows_b * K * 2));
+    const __amdgpu_buffer_rsrc_t ra =
+        make_rsrc(p.X + m0 * ldx, static_cast<uint32_t>(GEN ? strided_bytes(rows_a, K, ldx) : rows_a * K * 2));
+    const __amdgpu_buffer_rsrc_t rb =
+        make_rsrc(p.W + n0 * ldw, static_cast<uint32_t>(GEN ? strided_bytes(rows_b, K, ldw) : rows_b * K * 2));
 
     // Staging map: lane l of load block blk fills slot l % CHUNKS of row
     // RPI*blk + l / CHUNKS, which holds global chunk (l % CHUNKS) ^ swz(row).
@@ -275,14 +283,14 @@ void tile_kernel(Problem p, int64_t tiles_m, int64_t tiles_n, int group_m, Split
     for (int q = 0; q < C::A_LOADS; ++q) {
         const int r = (wave * C::A_LOADS + q) * C::RPI + lane / C::CHUNKS;
         const int c = slot ^ swz<C::CHUNKS>(r);
-        a_off[q] = static_cast<uint32_t>(r * K * 2 + c * 16);
+        a_off[q] = static_cast<uint32_t>(r * ldx * 2 + c * 16);
         a_k[q] = c * 8;
     }
 #pragma unroll
     for (int q = 0; q < C::B_LOADS; ++q) {
         const int r = (wave * C::B_LOADS + q) * C::RPI + lane / C::CHUNKS;
         const int c = slot ^ swz<C::CHUNKS>(r);
-        b_off[q] = static_cast<uint32_t>(r * K * 2 + c * 16);
+        b_off[q] = static_cast<uint32_t>(r * ldw * 2 + c * 16);
         b_k[q] = c * 8;
     }
 
@@ -319,19 +327,22 @@ void tile_kernel(Problem p, int64_t tiles_m, int64_t tiles_n, int group_m, Split
     // Epilogue constants (the residual may be requested before the K loop).
     const int64_t N = p.N;
     const int64_t rows_y = (p.M - m0) < C::BM ? (p.M - m0) : C::BM;
-    const uint32_t ybytes = static_cast<uint32_t>(rows_y * N * 2);
-    const __amdgpu_buffer_rsrc_t ry = make_rsrc(p.Y + m0 * N, ybytes);
+    const uint32_t ybytes = static_cast<uint32_t>(GEN ? strided_bytes(rows_y, N, ldy) : rows_y * N * 2);
+    const uint32_t rbytes = static_cast<uint32_t>(GEN ? strided_bytes(rows_y, N, ldr) : rows_y * N * 2);
+    const __amdgpu_buffer_rsrc_t ry = make_rsrc(p.Y + m0 * ldy, ybytes);
     // Without a residual the R resource is empty (its loads read zero).
-    const __amdgpu_buffer_rsrc_t rr = make_rsrc(p.R ? p.R + m0 * N : p.Y + m0 * N, p.R ? ybytes : 0u);
+    const __amdgpu_buffer_rsrc_t rr = make_rsrc(p.R ? p.R + m0 * ldr : p.Y, p.R ? rbytes : 0u);
     const bool has_r = p.R != nullptr;
-    const bool vec = (N & 7) == 0;
+    // 16-byte R/Y accesses need every row to start 16-byte aligned.
+    const bool vec = (N & 7) == 0 && (ldy & 7) == 0 && (!has_r || (ldr & 7) == 0);
     const int pr = lane / C::LANES_PER_ROW;             // row within a pass
     const int pc = (lane % C::LANES_PER_ROW) * 8;       // first of 8 columns
     const int64_t col0 = n0 + wn0 + pc;
     constexpr int PASSES = 32 / C::ROWS_PER_PASS;
-    auto base_of = [&](int i, int v) {
-        const int64_t row_local = wm0 + i * 32 + v * C::ROWS_PER_PASS + pr;
-        return static_cast<uint32_t>(row_local * N * 2 + col0 * 2);
+    auto row_of = [&](int i, int v) { return static_cast<int64_t>(wm0 + i * 32 + v * C::ROWS_PER_PASS + pr); };
+    auto base_of = [&](int i, int v) { return static_cast<uint32_t>(row_of(i, v) * ldy * 2 + col0 * 2); };
+    auto rbase_of = [&](int i, int v) {
+        return GEN ? static_cast<uint32_t>(row_of(i, v) * ldr * 2 + col0 * 2) : base_of(i, v);
     };
     // All of a slab's R is read before any of its Y is written (each element
     // by the same lane), so the loads do not wait behind the stores and Y
@@ -339,11 +350,19 @@ void tile_kernel(Problem p, int64_t tiles_m, int64_t tiles_n, int group_m, Split
     auto load_r = [&](int i, i32x4 (&rv)[PASSES]) {
 #pragma unroll
         for (int v = 0; v < PASSES; ++v)
-            rv[v] = __builtin_amdgcn_raw_buffer_load_b128(rr, col0 < N ? base_of(i, v) : OOB_OFFSET, 0, 0);
+            rv[v] = __builtin_amdgcn_raw_buffer_load_b128(rr, col0 < N ? rbase_of(i, v) : OOB_OFFSET, 0, 0);
     };
     // Two slabs of R in registers: slab i+1 is requested before slab i is
     // staged and stored, so only slab 0's latency is exposed.
     i32x4 rv[2][PASSES];
+    const bool has_bias = GEN && bias_of(p) != nullptr;
+    const float alpha = alpha_of(p), beta = beta_of(p);
+    // The value before rounding: the plain operator's acc + r, or the
+    // general form's alpha * acc + beta * r (the two agree at alpha = beta = 1).
+    auto value = [&](float acc, float r) {
+        if constexpr (GEN) return combine(acc, r, has_r, alpha, beta);
+        else return has_r ? acc + r : acc;
+    };
     // Small tiles request the first slab of R before the K loop (a few
     // registers); it is then in flight with the first loads instead of after
     // the loop, or after the split-K hand-off.
@@ -589,6 +608,15 @@ void tile_kernel(Problem p, int64_t tiles_m, int64_t tiles_n, int group_m, Split
     }
     if constexpr (!EARLY_R)
         if (owner && vec && has_r) load_r(0, rv[0]);
+    // The bias of the lane's 8 columns (fixed for the whole tile).
+    float bv[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    if (has_bias && owner) {
+        const __amdgpu_buffer_rsrc_t rbias = make_rsrc(bias_of(p), static_cast<uint32_t>(N * 2));
+#pragma unroll
+        for (int t = 0; t < 8; ++t)
+            bv[t] = bf16_to_f32(__builtin_amdgcn_raw_buffer_load_b16(
+                rbias, col0 + t < N ? static_cast<uint32_t>((col0 + t) * 2) : OOB_OFFSET, 0, 0));
+    }
     float *ep = reinterpret_cast<float *>(lds) + wave * C::EPI_WAVE_FLOATS;
 #pragma unroll
     for (int i = 0; i < C::TM; ++i) {
@@ -610,7 +638,18 @@ void tile_kernel(Problem p, int64_t tiles_m, int64_t tiles_n, int group_m, Split
                 for (int t = 0; t < 8; ++t) y[t] = src[t];
                 const uint32_t base = base_of(i, v);
                 if (vec) {
-                    if (has_r) {
+                    if constexpr (GEN) {
+#pragma unroll
+                        for (int t = 0; t < 4; ++t) {
+                            const uint32_t w = static_cast<uint32_t>(rv[i & 1][v][t]);
+                            y[2 * t] = value(y[2 * t], bf16_to_f32(static_cast<uint16_t>(w & 0xffffu)));
+                            y[2 * t + 1] = value(y[2 * t + 1], bf16_to_f32(static_cast<uint16_t>(w >> 16)));
+                        }
+                        if (has_bias) {
+#pragma unroll
+                            for (int t = 0; t < 8; ++t) y[t] += bv[t];
+                        }
+                    } else if (has_r) {
 #pragma unroll
                         for (int t = 0; t < 4; ++t) {
                             const uint32_t w = static_cast<uint32_t>(rv[i & 1][v][t]);
@@ -625,11 +664,13 @@ void tile_kernel(Problem p, int64_t tiles_m, int64_t tiles_n, int group_m, Split
                 } else {
                     uint16_t rs[8];
                     const int cols = static_cast<int>(N - col0);   // columns of this lane's 8 that exist
+                    const uint32_t rbase = rbase_of(i, v);
 #pragma unroll
-                    for (int t = 0; t < 8; ++t) rs[t] = __builtin_amdgcn_raw_buffer_load_b16(rr, t < cols ? base + 2 * t : OOB_OFFSET, 0, 0);
+                    for (int t = 0; t < 8; ++t) rs[t] = __builtin_amdgcn_raw_buffer_load_b16(rr, t < cols ? rbase + 2 * t : OOB_OFFSET, 0, 0);
 #pragma unroll
                     for (int t = 0; t < 8; ++t) {
-                        const float yt = has_r ? y[t] + bf16_to_f32(rs[t]) : y[t];
+                        float yt = value(y[t], bf16_to_f32(rs[t]));
+                        if (has_bias) yt += bv[t];
                         __builtin_amdgcn_raw_buffer_store_b16(f32_to_bf16_rne(yt), ry, t < cols ? base + 2 * t : OOB_OFFSET, 0, 0);
                     }
                 }
@@ -658,8 +699,12 @@ hipError_t launch_cfg(const Problem &p, int group_m, int split, int64_t full_til
             return hipErrorInvalidValue;
     }
     const int64_t wgs = sk.full_tiles + (tiles - sk.full_tiles) * sk.split;
-    hipLaunchKernelGGL(tile_kernel<C>, dim3(static_cast<unsigned>(wgs)), dim3(C::THREADS), 0, s, p, tiles_m,
-                       tiles_n, group_m, sk);
+    if (is_general(p))
+        hipLaunchKernelGGL((tile_kernel<C, Problem>), dim3(static_cast<unsigned>(wgs)), dim3(C::THREADS), 0, s, p,
+                           tiles_m, tiles_n, group_m, sk);
+    else
+        hipLaunchKernelGGL((tile_kernel<C, DenseProblem>), dim3(static_cast<unsigned>(wgs)), dim3(C::THREADS), 0, s,
+                           dense_of(p), tiles_m, tiles_n, group_m, sk);
     return hipGetLastError();
 }
 

@@ -40,6 +40,12 @@ _SIGS = {
     "kernelarc_plan_supports": (ctypes.c_int, [ctypes.c_int, _I64, _I64, _I64, ctypes.c_int]),
     "kernelarc_select_plan": (ctypes.c_int, [_I64, _I64, _I64, ctypes.c_int]),
     "kernelarc_plan_uses_workspace": (ctypes.c_int, [ctypes.c_int, _I64, _I64, _I64]),
+    "kernelarc_gemm_bf16_ex": (ctypes.c_int, [_I64, _I64, _I64, ctypes.c_float, _P, _I64, _P, _I64,
+                                              ctypes.c_float, _P, _I64, _P, _P, _I64, _P]),
+    "kernelarc_gemm_bf16_ex_with_plan": (ctypes.c_int, [ctypes.c_int, _I64, _I64, _I64, ctypes.c_float, _P, _I64,
+                                                        _P, _I64, ctypes.c_float, _P, _I64, _P, _P, _I64, _P]),
+    "kernelarc_select_plan_ex": (ctypes.c_int, [_I64, _I64, _I64, ctypes.c_int, _I64, _I64, _I64, _I64,
+                                                ctypes.c_float, ctypes.c_float, ctypes.c_int]),
     "kernelarc_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "kernelarc_last_error": (ctypes.c_char_p, []),
 }
@@ -151,3 +157,57 @@ def gemm_bf16_with_plan(plan, x, w, r=None, out=None, stream=None):
                                                 out.data_ptr(), _stream_handle(stream))
     _check(st, f"kernelarc_gemm_bf16_with_plan({plan_name(plan)})")
     return out
+
+
+def _rows(t: torch.Tensor, name: str, rows: int, cols: int) -> int:
+    """Leading dimension (elements) of a 2-D bf16 GPU view with unit column stride."""
+    if t.dtype != torch.bfloat16:
+        raise TypeError(f"{name} must be bfloat16")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if t.dim() != 2 or tuple(t.shape) != (rows, cols):
+        raise ValueError(f"{name} must have shape {(rows, cols)}, got {tuple(t.shape)}")
+    if rows > 0 and cols > 1 and t.stride(1) != 1:
+        raise ValueError(f"{name} must have unit stride along its last dimension")
+    return t.stride(0) if rows > 1 else max(cols, 1)
+
+
+def gemm_bf16_ex(x, w, c=None, bias=None, alpha=1.0, beta=1.0, out=None, stream=None, plan=None):
+    """Y = alpha X W^T + beta C + bias with row-strided 2-D operands.
+
+    x [M, K], w [N, K], c and out [M, N] may be row-strided views (unit
+    stride along the last dimension); bias is [N] or None; c is not read
+    when beta == 0.  ``out`` may be ``c`` itself (same view).
+    """
+    if x.dim() != 2 or w.dim() != 2:
+        raise ValueError("x must be [M, K] and w [N, K]")
+    M, K = x.shape
+    N = w.shape[0]
+    ldx = _rows(x, "x", M, K)
+    ldw = _rows(w, "w", N, K)
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.bfloat16, device=x.device)
+    ldy = _rows(out, "out", M, N)
+    ldc = _rows(c, "c", M, N) if c is not None else max(N, 1)
+    if bias is not None:
+        if bias.dtype != torch.bfloat16 or not bias.is_cuda or tuple(bias.shape) != (N,) or not bias.is_contiguous():
+            raise ValueError(f"bias must be a contiguous bfloat16 GPU tensor of shape {(N,)}")
+    for t in (w, c, bias, out):
+        if t is not None and t.device != x.device:
+            raise ValueError(f"operands on different devices ({t.device} vs {x.device})")
+    args = (M, N, K, float(alpha), x.data_ptr(), ldx, w.data_ptr(), ldw, float(beta),
+            c.data_ptr() if c is not None else None, ldc,
+            bias.data_ptr() if bias is not None else None, out.data_ptr(), ldy)
+    with torch.cuda.device(x.device):
+        if plan is None:
+            st = _lib.kernelarc_gemm_bf16_ex(*args, _stream_handle(stream))
+        else:
+            st = _lib.kernelarc_gemm_bf16_ex_with_plan(plan, *args, _stream_handle(stream))
+    _check(st, "kernelarc_gemm_bf16_ex" if plan is None else f"kernelarc_gemm_bf16_ex_with_plan({plan_name(plan)})")
+    return out
+
+
+def select_plan_ex(M, N, K, has_c, ldx, ldw, ldc, ldy, alpha, beta, has_bias) -> int:
+    """The plan the general form would run for these strides and scalars."""
+    return _lib.kernelarc_select_plan_ex(M, N, K, int(has_c), ldx, ldw, ldc, ldy, float(alpha), float(beta),
+                                         int(has_bias))

@@ -131,3 +131,34 @@ def test_python_side_checks(ka):
         ka.gemm_bf16(x.float(), w)
     with pytest.raises(ValueError):
         ka.gemm_bf16(torch.zeros(4, 7, dtype=torch.bfloat16), w)
+
+
+def test_general_form_validation(ka):
+    f = ka.kernelarc_gemm_bf16_ex
+    buf = (ctypes.c_uint16 * 8192)()
+    base = ctypes.addressof(buf)
+    X, W, C, B, Y = base, base + 2048, base + 4096, base + 6144, base + 8192
+    # (M, N, K, alpha, X, ldx, W, ldw, beta, C, ldc, bias, Y, ldy, stream)
+    assert f(4, 4, 8, 1.0, X, 7, W, 8, 1.0, C, 4, None, Y, 4, None) == ka.ERR_INVALID_ARG   # ldx < K
+    assert ka.kernelarc_last_error().startswith(b"a leading dimension is smaller")
+    assert f(4, 4, 8, 1.0, X, 8, W, 8, 1.0, C, 3, None, Y, 4, None) == ka.ERR_INVALID_ARG   # ldc < N
+    assert f(4, 4, 8, 1.0, X, 8, W, 8, 1.0, C, 4, None, Y, -1, None) == ka.ERR_INVALID_ARG  # negative ld
+    assert f(4, 4, 8, 1.0, X, 8, W, 8, 0.0, C, 3, None, Y, 4, None) != ka.ERR_INVALID_ARG   # beta 0: C unused
+    # Y overlapping the bias, or C in part (only Y == C with ldy == ldc is allowed)
+    assert f(4, 4, 8, 1.0, X, 8, W, 8, 1.0, C, 4, Y + 4, Y, 4, None) == ka.ERR_INVALID_ARG
+    assert f(4, 4, 8, 1.0, X, 8, W, 8, 1.0, Y + 2, 4, None, Y, 4, None) == ka.ERR_INVALID_ARG
+    assert f(4, 4, 8, 1.0, X, 8, W, 8, 1.0, Y, 6, None, Y, 4, None) == ka.ERR_INVALID_ARG
+    # strided extents count: row 3 of a ldy = 512 Y reaches W
+    assert f(4, 4, 8, 1.0, X, 8, W, 8, 1.0, None, 4, None, X - 3 * 1024 + 2048 + 16, 512, None) == ka.ERR_INVALID_ARG
+    assert f(0, 4, 8, 1.0, None, 8, None, 8, 1.0, None, 4, None, None, 4, None) == ka.OK
+
+
+def test_general_form_plan_selection(ka):
+    names = ka.plan_names()
+    # the dense form of a decode shape streams; the general form of it cannot
+    dense = names[ka.select_plan_ex(16, 4096, 4096, 1, 4096, 4096, 4096, 4096, 1.0, 1.0, 0)]
+    general = names[ka.select_plan_ex(16, 4096, 4096, 1, 4096, 4096, 4096, 4096, 2.0, 1.0, 0)]
+    assert dense == names[ka.select_plan(16, 4096, 4096, True)]
+    assert dense.startswith("stream") and general.startswith("tile")
+    assert names[ka.select_plan_ex(2, 4096, 4096, 1, 4104, 4096, 4096, 4096, 1.0, 1.0, 1)] == "gemv_valu_w4"
+    assert names[ka.select_plan_ex(4096, 4096, 14336, 1, 14336, 14336, 4096, 4096, 1.0, 1.0, 1)].startswith("tile")
