@@ -174,6 +174,69 @@ class Case:
         self.graph = None
 
 
+class GeneralCase(Case):
+    """A general-form workload: X read through its row stride, C, bias, alpha, beta."""
+
+    def __init__(self, w, ka, torch, rotate=True):
+        from paper_2608_17071_amd import workloads as wl
+        t = wl.make_general_inputs(w)
+        self.w = w
+        self.host = t
+        xbuf = torch.zeros((w.M, w.ldx), dtype=torch.bfloat16, device="cuda")
+        xbuf[:, :w.K] = t["X"].cuda()
+        W = t["W"].cuda()
+        c = t["C"].cuda() if t["C"] is not None else None
+        b = t["bias"].cuda() if t["bias"] is not None else None
+        n = 1
+        if rotate:
+            n = max(2, min(MAX_COPIES, -(-ROTATE_BYTES // w.algorithmic_bytes)))
+        self.sets = []
+        for i in range(n):
+            xb = xbuf if i == 0 else xbuf.clone()
+            self.sets.append((xb[:, :w.K], W if i == 0 else W.clone(),
+                              None if c is None else (c if i == 0 else c.clone()),
+                              torch.empty(w.M, w.N, dtype=torch.bfloat16, device="cuda"), b))
+        self.plan = ka.select_plan_ex(w.M, w.N, w.K, w.has_c, w.ldx, w.K, w.N, w.N, w.alpha, w.beta, w.has_bias)
+        self.plan_name = ka.plan_name(self.plan)
+        self.times = []
+        self.graph = None
+
+    def call(self, ka, i):
+        x, W, c, y, b = self.sets[i]
+        ka.gemm_bf16_ex(x, W, c, b, self.w.alpha, self.w.beta, out=y)
+
+
+def cpu_baseline_general(cases, seconds):
+    """The oracle's general form on rows 0, 1, ... of each case until its time share is used."""
+    import numpy as np
+    import oracle
+    from paper_2608_17071_amd import workloads as wl
+
+    orc = oracle.default()
+    per_shape = seconds / len(cases)
+    rates, rows_done = [], []
+    for c in cases:
+        w, h = c.w, c.host
+        xb, wb = wl.bits(h["X"]), wl.bits(h["W"])
+        cb = wl.bits(h["C"]) if h["C"] is not None else None
+        bb = wl.bits(h["bias"]) if h["bias"] is not None else None
+        cols = np.arange(w.N, dtype=np.int64)
+        flops, rows, t0 = 0, 0, time.perf_counter()
+        while rows < w.M:
+            orc.linear_ex_at(xb, wb, cb, bb, w.alpha, w.beta, np.full(w.N, rows, dtype=np.int64), cols)
+            rows += 1
+            flops += 2 * w.N * w.K
+            if time.perf_counter() - t0 >= per_shape:
+                break
+        rates.append(flops / (time.perf_counter() - t0) / 1e12)
+        rows_done.append(rows)
+    return {
+        "value": geomean(rates), "unit": "TFLOP/s (fp64 oracle, general form, geomean over its shapes)",
+        "cores": orc.threads(), "kind": "oracle",
+        "sample": f"whole output rows 0..r-1 of each general-form shape, r = {rows_done} (about {per_shape:.2f} s each)",
+    }
+
+
 def time_cases(cases, steps, warmup, ka, torch, use_graph=True):
     """Warm up, capture, then time `steps` passes over all cases; returns wall seconds."""
     for c in cases:
@@ -219,8 +282,11 @@ def median(xs):
 def shape_row(c):
     w = c.w
     t = median(c.times)
+    extra = {}
+    if hasattr(w, "alpha"):
+        extra = {"alpha": w.alpha, "beta": w.beta, "C": w.has_c, "bias": w.has_bias, "ldx": w.ldx}
     return {
-        "shape": w.name, "M": w.M, "N": w.N, "K": w.K, "plan": c.plan_name,
+        "shape": w.name, "M": w.M, "N": w.N, "K": w.K, **extra, "plan": c.plan_name,
         "us": round(t * 1e6, 3), "tflops": round(w.flops / t / 1e12, 3),
         "gbps": round(w.algorithmic_bytes / t / 1e9, 1), "bound": bound_of(w),
         "roofline_frac": round(roofline_time(w) / t, 4),
@@ -269,6 +335,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-gates", action="store_true", help="skip the decode/prefill/square extras")
+    ap.add_argument("--no-general", action="store_true",
+                    help="skip the general-form shapes (alpha, beta, bias, row strides)")
     ap.add_argument("--only", default="",
                     help="comma-separated workload names: time just these (for profiling one kernel)")
     ap.add_argument("--summarize-traffic", nargs=2, metavar=("PMC_DIR", "SHAPES"),
@@ -368,6 +436,30 @@ def main():
                 f"{r['gbps']:7.0f} GB/s  {r['bound']} frac {r['roofline_frac']:.3f}")
         del extra
 
+    # The general form (NEXT row: alpha, beta, bias, row strides) on the
+    # decoder layer's residual GEMM sites; reported beside the metric.
+    general = None
+    if not args.no_general:
+        for c in sweep:
+            c.free()
+        gcases = [GeneralCase(w, ka, torch, rotate=not args.hot) for w in wl.GENERAL]
+        time_cases(gcases, args.steps, args.warmup, ka, torch, use_graph=not args.no_graph)
+        grows = []
+        for c in gcases:
+            r = shape_row(c)
+            grows.append(r)
+            log(f"  {r['shape']:40s} {r['plan']:28s} {r['us']:9.2f} us {r['tflops']:8.1f} TF "
+                f"{r['gbps']:7.0f} GB/s  {r['bound']} frac {r['roofline_frac']:.3f}")
+        general = {"shapes": grows,
+                   "geomean_tflops": round(geomean([r["tflops"] for r in grows]), 3),
+                   "geomean_roofline_frac": round(geomean([r["roofline_frac"] for r in grows]), 4)}
+        if not args.no_cpu_baseline:
+            log("timing the CPU oracle on the general form (~4 s) ...")
+            general["cpu_baseline"] = cpu_baseline_general(gcases, 4.0)
+        for c in gcases:
+            c.free()
+        del gcases
+
     cpu = None
     if not args.no_cpu_baseline:
         log(f"timing the CPU oracle (~{args.cpu_seconds:.0f} s) ...")
@@ -393,6 +485,7 @@ def main():
         "cpu_baseline": cpu,
         "shapes": rows,
         "gates": gates,
+        "general": general,
     }
     print(json.dumps(out), flush=True)
 

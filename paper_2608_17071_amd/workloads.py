@@ -75,6 +75,69 @@ ALL = (TINY, DECODE, PREFILL, SQUARE) + SWEEP
 BY_NAME = {w.name: w for w in ALL}
 
 
+# ---- the general form Y = alpha X W^T + beta C + bias ----------------------
+
+@dataclass(frozen=True)
+class GeneralWorkload:
+    """A general-form call: X is the leading K columns of an [M, K + x_pad]
+    buffer (row stride ldx = K + x_pad); C ([M,N], when has_c) and bias ([N],
+    when has_bias) are drawn like R; alpha and beta are binary32 values."""
+    name: str
+    M: int
+    N: int
+    K: int
+    alpha: float
+    beta: float
+    has_c: bool
+    has_bias: bool
+    x_pad: int
+    seed: int
+
+    @property
+    def ldx(self) -> int:
+        return self.K + self.x_pad
+
+    @property
+    def flops(self) -> int:
+        return 2 * self.M * self.N * self.K
+
+    @property
+    def algorithmic_bytes(self) -> int:
+        """X, W, C and bias read once, Y written once, 2 bytes per element."""
+        b = 2 * (self.M * self.K + self.N * self.K + self.M * self.N)
+        if self.has_c and self.beta != 0.0:
+            b += 2 * self.M * self.N
+        if self.has_bias:
+            b += 2 * self.N
+        return b
+
+
+# The decoder layer's two residual GEMM sites at Llama-class sizes (hidden
+# 4096, intermediate 14336; hidden 5120, intermediate 13824): the
+# output projection with a bias, the down projection reading its input
+# through a row stride (a slice of a wider activation buffer), a decode
+# step with a scaled residual, and a prefill step with beta != 1 and a bias.
+GENERAL = (
+    GeneralWorkload("general_oproj_bias_m4096_h4096", 4096, 4096, 4096, 1.0, 1.0, True, True, 0, 101),
+    GeneralWorkload("general_down_strided_m4096_n4096_k14336", 4096, 4096, 14336, 1.0, 1.0, True, False, 128, 102),
+    GeneralWorkload("general_down_scaled_m16_n4096_k14336", 16, 4096, 14336, 1.0, 0.5, True, False, 0, 103),
+    GeneralWorkload("general_down_bias_m512_n5120_k13824", 512, 5120, 13824, 0.5, 0.25, True, True, 0, 104),
+)
+GENERAL_BY_NAME = {w.name: w for w in GENERAL}
+
+
+def make_general_inputs(w: GeneralWorkload) -> dict:
+    """Draw X (dense [M,K]), W, C and bias as bf16 CPU tensors: X ~ N(0,1)/sqrt(K),
+    W ~ N(0,1)/sqrt(K), C ~ N(0,1), bias ~ N(0,1), in that order from one seed."""
+    g = torch.Generator().manual_seed(w.seed)
+    scale = 1.0 / math.sqrt(w.K) if w.K > 0 else 1.0
+    X = (torch.randn((w.M, w.K), generator=g) * scale).to(torch.bfloat16)
+    W = (torch.randn((w.N, w.K), generator=g) * scale).to(torch.bfloat16)
+    C = torch.randn((w.M, w.N), generator=g).to(torch.bfloat16)
+    b = torch.randn((w.N,), generator=g).to(torch.bfloat16)
+    return {"X": X, "W": W, "C": C if w.has_c else None, "bias": b if w.has_bias else None}
+
+
 def custom(M: int, N: int, K: int, residual: bool = True, dist: str = "normal",
            seed: int = 0, name: str | None = None) -> Workload:
     return Workload(name or f"custom_m{M}_n{N}_k{K}", M, N, K, residual, dist, seed)

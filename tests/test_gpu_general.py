@@ -205,3 +205,25 @@ def test_general_graph_replay(ka):
         graph.replay()
         torch.cuda.synchronize()
         assert torch.equal(out.view(torch.int16), eager.view(torch.int16))
+
+
+@pytest.mark.parametrize("name", [w.name for w in wl.GENERAL])
+def test_general_bench_workloads(ka, name):
+    """The benchmark's general-form shapes, launched as the benchmark launches
+    them (X through its row stride, the selected plan), on sampled outputs."""
+    w = wl.GENERAL_BY_NAME[name]
+    t = wl.make_general_inputs(w)
+    xbuf = torch.zeros((w.M, w.ldx), dtype=torch.bfloat16)
+    xbuf[:, :w.K] = t["X"]
+    xbuf = xbuf.cuda()
+    c = t["C"].cuda() if t["C"] is not None else None
+    b = t["bias"].cuda() if t["bias"] is not None else None
+    plan = ka.select_plan_ex(w.M, w.N, w.K, w.has_c, w.ldx, w.K, w.N, w.N, w.alpha, w.beta, w.has_bias)
+    gu.note(f"general bench {name} plan={ka.plan_name(plan)}")
+    y = ka.gemm_bf16_ex(xbuf[:, :w.K], t["W"].cuda(), c, b, w.alpha, w.beta)
+    torch.cuda.synchronize()
+    pos = gu.sample_positions(w.M, w.N, rows=4, cols=3, seed=w.seed)
+    ref = oracle.default().linear_ex_at(wl.bits(t["X"]), wl.bits(t["W"]), wl.bits(t["C"]) if t["C"] is not None else None,
+                                        wl.bits(t["bias"]) if t["bias"] is not None else None, w.alpha, w.beta,
+                                        pos[0], pos[1])
+    gu.check_tolerance(gu.to_bits(y)[pos[0], pos[1]], ref, name)
