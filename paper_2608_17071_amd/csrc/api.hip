@@ -274,8 +274,10 @@ const TableEntry TABLE[] = {
 // split-K up to 32 rows; up to 1024 rows: 64x64 tiles (3 stages of K depth
 // 128, split-K) while they fill at most half the CUs, 64x64 tiles (4 stages
 // of depth 64, two per CU) while they fit one round, else 128x128 tiles
-// (3 stages with split-K when at most half the CUs would be busy, else 4
-// stages with the lagged refill); above that the 256x256 8-wave tile when it
+// with 3 stages and split-K when they would keep at most half the CUs busy,
+// 256x128 8-wave tiles (3 stages, lagged refill) with split-K when 128x128
+// tiles would leave some CUs idle, else 128x128 tiles with 4 stages and the
+// lagged refill; above that the 256x256 8-wave tile when it
 // fills the 256 CUs (tail split: the tiles of a partial last round are split
 // in K), the 256x128 8-wave tile (3 stages, lagged refill) when that fills
 // them, else the 128x128 tile.
@@ -304,6 +306,7 @@ int select(int64_t M, int64_t N, int64_t K, bool residual, const Layout &lay) {
         if (2 * tiles64 <= CUS) plan = pick("tile_64x64_k128s3_w4_splitk");
         else if (tiles64 <= 2 * CUS) plan = pick("tile_64x64_k64s4_w4");
         else if (2 * tiles128 <= CUS) plan = pick("tile_128x128_k64s3_w4_splitk");
+        else if (tiles128 < CUS) plan = pick("tile_256x128_k64s3_w8_lag_splitk");
         else plan = pick("tile_128x128_k64s4_w4_lag");
         if (plan < 0) plan = pick("tile_128x128_k64_w4_splitk");
     } else {
