@@ -1,5 +1,6 @@
-"""CPU oracle for Y = X.W^T + R and its general form
-D = alpha.X.W^T + beta.C + bias (TEST INFRASTRUCTURE ONLY).
+"""CPU oracle for Y = X.W^T + R, its general form
+D = alpha.X.W^T + beta.C + bias, and the gated MLP input projection
+H = silu(X.Wg^T) * (X.Wu^T) (TEST INFRASTRUCTURE ONLY).
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
 ``bench.py`` may import this package.  The GPU library never imports, links
@@ -59,6 +60,10 @@ class Oracle:
         lib.ka_oracle_linear_ex_at.argtypes = [_I64, _I64, _I64, ctypes.c_float, _P, _I64, _P, _I64,
                                                ctypes.c_float, _P, _I64, _P, _I64, _P, _P, _P]
         lib.ka_oracle_linear_ex_at.restype = ctypes.c_int
+        lib.ka_oracle_swiglu.argtypes = [_I64, _I64, _I64, _P, _P, _P, _P]
+        lib.ka_oracle_swiglu.restype = ctypes.c_int
+        lib.ka_oracle_swiglu_at.argtypes = [_I64, _I64, _I64, _P, _P, _P, _I64, _P, _P, _P]
+        lib.ka_oracle_swiglu_at.restype = ctypes.c_int
         lib.ka_oracle_round_bf16.argtypes = [_I64, _P, _P]
         lib.ka_oracle_round_bf16.restype = None
         lib.ka_oracle_threads.argtypes = []
@@ -171,6 +176,40 @@ class Oracle:
         if rc != 0:
             raise ValueError("oracle rejected its arguments")
         del keep
+        return out
+
+    def swiglu(self, X, Wg, Wu) -> np.ndarray:
+        """H[i,j] = silu(G[i,j]) * U[i,j] in float64, with G = X Wg^T,
+        U = X Wu^T and silu(z) = z / (1 + exp(-z))."""
+        M, K = X.shape
+        N = Wg.shape[0]
+        X = self._bits(X, (M, K))
+        Wg = self._bits(Wg, (N, K))
+        Wu = self._bits(Wu, (N, K))
+        H = np.empty((M, N), dtype=np.float64)
+        rc = self.lib.ka_oracle_swiglu(M, N, K, X.ctypes.data, Wg.ctypes.data, Wu.ctypes.data,
+                                       H.ctypes.data)
+        if rc != 0:
+            raise ValueError("oracle rejected its arguments")
+        return H
+
+    def swiglu_at(self, X, Wg, Wu, rows, cols) -> np.ndarray:
+        """SwiGLU at the positions (rows[t], cols[t])."""
+        M, K = X.shape
+        N = Wg.shape[0]
+        X = self._bits(X, (M, K))
+        Wg = self._bits(Wg, (N, K))
+        Wu = self._bits(Wu, (N, K))
+        rows = np.ascontiguousarray(rows, dtype=np.int64)
+        cols = np.ascontiguousarray(cols, dtype=np.int64)
+        if rows.shape != cols.shape or rows.ndim != 1:
+            raise ValueError("rows and cols must be 1-D and of equal length")
+        out = np.empty(rows.shape[0], dtype=np.float64)
+        rc = self.lib.ka_oracle_swiglu_at(M, N, K, X.ctypes.data, Wg.ctypes.data, Wu.ctypes.data,
+                                          rows.shape[0], rows.ctypes.data, cols.ctypes.data,
+                                          out.ctypes.data)
+        if rc != 0:
+            raise ValueError("oracle rejected its arguments")
         return out
 
     def threads(self) -> int:

@@ -3,6 +3,9 @@
  *
  *     Y[i,j] = sum_k X[i,k] * W[j,k]  +  R[i,j]          (R optional)
  *
+ * its general form (alpha, beta, bias, leading dimensions) and the gated
+ * MLP input projection H = silu(X Wg^T) * (X Wu^T) (SwiGLU).
+ *
  * TEST INFRASTRUCTURE ONLY.  This file is the slow, obviously correct
  * reference that the GPU library is checked against.  Only the test suite,
  * the smoke check and the CPU-baseline leg of the benchmark load it; the
@@ -24,7 +27,10 @@
  *
  * Pins: tests/test_oracle_pins.py (exact rational brute force, a hand-worked
  * fixture, numpy's float64 matmul, W = 0, W = I, rank-1 integer closed form,
- * row/K permutation and transpose invariants, and planted-mistake runs).
+ * row/K permutation and transpose invariants, and planted-mistake runs; for
+ * SwiGLU, brute force with a high-precision decimal exponential, scipy's
+ * logistic function, closed forms at e, the odd and even parts of SiLU,
+ * saturated tails and zero operands).
  */
 #include <math.h>
 #include <stdint.h>
@@ -193,6 +199,75 @@ int ka_oracle_linear_ex_at(int64_t M, int64_t N, int64_t K, float alpha,
 #pragma omp parallel for schedule(dynamic, 16)
     for (int64_t t = 0; t < n; ++t)
         out[t] = element_ex(rows[t], cols[t], K, (double)alpha, X, ldx, W, ldw, (double)beta, C, ldc, bias);
+    return 0;
+}
+
+/*
+ * Gated MLP input projection with the SiLU-multiply (SwiGLU): the decoder
+ * layer's gate and up projections and the activation that joins them
+ * (decoder-layer case study, Alg. 7: its BF16 gate/up projections followed
+ * by a SiLU-multiply, and its fused gate/up GEMM with a SwiGLU epilogue):
+ *
+ *     G[i,j] = sum_k X[i,k] Wg[j,k]        U[i,j] = sum_k X[i,k] Wu[j,k]
+ *     H[i,j] = silu(G[i,j]) * U[i,j]       silu(z) = z / (1 + e^(-z))
+ *
+ * The paper names the operation without writing it out; SiLU is the
+ * sigmoid-weighted linear unit z * sigmoid(z), and SwiGLU gates the up
+ * projection with SiLU of the gate projection.  X is [M,K], Wg and Wu are
+ * [N,K] (nn.Linear orientation, N = intermediate size), H is [M,N] doubles.
+ * G and U are the k-sums in double (ascending k), never rounded to bf16:
+ * the fused epilogue has no intermediate tensor.  H is not rounded.
+ */
+static double silu(double z)
+{
+    return z / (1.0 + exp(-z));
+}
+
+static double element_swiglu(int64_t i, int64_t j, int64_t K, const uint16_t *X,
+                             const uint16_t *Wg, const uint16_t *Wu)
+{
+    double g = 0.0;
+    double u = 0.0;
+    for (int64_t k = 0; k < K; ++k) {
+        double x = bf16_bits_to_double(X[i * K + k]);
+        g += x * bf16_bits_to_double(Wg[j * K + k]);
+        u += x * bf16_bits_to_double(Wu[j * K + k]);
+    }
+    return silu(g) * u;
+}
+
+static int check_swiglu(int64_t M, int64_t N, int64_t K, const uint16_t *X,
+                        const uint16_t *Wg, const uint16_t *Wu)
+{
+    if (M < 0 || N < 0 || K < 0) return -1;
+    if (M * K > 0 && !X) return -1;
+    if (N * K > 0 && (!Wg || !Wu)) return -1;
+    return 0;
+}
+
+int ka_oracle_swiglu(int64_t M, int64_t N, int64_t K, const uint16_t *X,
+                     const uint16_t *Wg, const uint16_t *Wu, double *H)
+{
+    if (check_swiglu(M, N, K, X, Wg, Wu) != 0) return -1;
+    if (M * N > 0 && !H) return -1;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t i = 0; i < M; ++i)
+        for (int64_t j = 0; j < N; ++j)
+            H[i * N + j] = element_swiglu(i, j, K, X, Wg, Wu);
+    return 0;
+}
+
+/* SwiGLU at the n positions (rows[t], cols[t]). */
+int ka_oracle_swiglu_at(int64_t M, int64_t N, int64_t K, const uint16_t *X,
+                        const uint16_t *Wg, const uint16_t *Wu, int64_t n,
+                        const int64_t *rows, const int64_t *cols, double *out)
+{
+    if (check_swiglu(M, N, K, X, Wg, Wu) != 0 || n < 0) return -1;
+    for (int64_t t = 0; t < n; ++t)
+        if (rows[t] < 0 || rows[t] >= M || cols[t] < 0 || cols[t] >= N) return -1;
+#pragma omp parallel for schedule(dynamic, 16)
+    for (int64_t t = 0; t < n; ++t)
+        out[t] = element_swiglu(rows[t], cols[t], K, X, Wg, Wu);
     return 0;
 }
 

@@ -22,13 +22,24 @@ operands over NaN padding, by reduction to the plain operator at
 alpha = beta = 1, by the W = 0 closed form, by beta = 0 leaving C unread,
 by exact scaling with power-of-two alpha, and by strided = dense.
 
+The gated MLP input projection H = silu(X Wg^T) * (X Wu^T) (SwiGLU,
+``GLU_PINS``) is pinned by exact rational k-sums with SiLU evaluated by
+Python's decimal module at 60 digits (correctly rounded exp, not libm), by
+closed forms at e (silu(1) = e/(1+e), silu(-1) = -1/(1+e), silu(2), silu(-2),
+silu(1/2)), by numpy's matmul with scipy's logistic function, by the odd
+part silu(z) - silu(-z) = z and the even part silu(z) + silu(-z) =
+z tanh(z/2), by the saturated tails (z >= 40: silu(z) = z in double;
+z <= -800: 0), by zero operands, and by row and column permutations.
+
 ``ALL_PINS`` is run against the real oracle (all must pass) and against
 copies of the oracle with a planted mistake (at least one must fail).
 """
 from __future__ import annotations
 
 import json
+import math
 import os
+from decimal import Decimal, localcontext
 from fractions import Fraction
 
 import numpy as np
@@ -345,6 +356,179 @@ EX_PINS = [
     pin_ex_at_matches_full,
 ]
 
+# ----------------------------------------------------------------- SwiGLU ----
+def _neg_bits(bits):
+    """Exact negation of bf16 bit patterns (sign bit flipped)."""
+    return (np.asarray(bits, dtype=np.uint16) ^ np.uint16(0x8000)).astype(np.uint16)
+
+
+def _glu_f64(X, Wg, Wu):
+    """G = X Wg^T and U = X Wu^T by numpy's float64 matmul, and the
+    magnitudes |X| |Wg|^T and |X| |Wu|^T that bound their rounding."""
+    xf, gf, uf = bf16_bits_to_f64(X), bf16_bits_to_f64(Wg), bf16_bits_to_f64(Wu)
+    return xf @ gf.T, xf @ uf.T, np.abs(xf) @ np.abs(gf).T, np.abs(xf) @ np.abs(uf).T
+
+
+def _glu_bound(G, U, magG, magU, ref, rel):
+    """Error allowed for H near silu(G) U when G and U carry k-sum rounding
+    up to rel * their magnitudes (|silu'| <= 1.1), plus the final rounding."""
+    s = np.abs(G) / (1.0 + np.exp(-np.clip(G, -700, 700)))
+    return rel * (1.1 * magG * np.abs(U) + s * magU) + 1e-15 * np.abs(ref) + 1e-300
+
+
+def pin_glu_exact_bruteforce(orc, trials=30, seed=2468):
+    """Oracle within 2^-46 of silu(G) U computed from the exact rational G and
+    U with a 60-digit decimal exponential (over the tails too: |G| up to ~100)."""
+    rng = np.random.default_rng(seed)
+    for t in range(trials):
+        M, N, K = (int(v) for v in rng.integers(1, 9, size=3))
+        spread = (1.0, 4.0, 30.0)[t % 3]
+        X = _rand_bits(rng, (M, K), spread)
+        Wg = _rand_bits(rng, (N, K), 1.0 / np.sqrt(K))
+        Wu = _rand_bits(rng, (N, K), 1.0 / np.sqrt(K))
+        H = orc.swiglu(X, Wg, Wu)
+        assert np.isfinite(H).all()
+        xf, gf, uf = bf16_bits_to_f64(X), bf16_bits_to_f64(Wg), bf16_bits_to_f64(Wu)
+        with localcontext() as ctx:
+            ctx.prec = 60
+            for i in range(M):
+                for j in range(N):
+                    g = sum((Fraction(xf[i, k]) * Fraction(gf[j, k]) for k in range(K)), Fraction(0))
+                    u = sum((Fraction(xf[i, k]) * Fraction(uf[j, k]) for k in range(K)), Fraction(0))
+                    mg = sum(abs(Fraction(xf[i, k]) * Fraction(gf[j, k])) for k in range(K))
+                    mu = sum(abs(Fraction(xf[i, k]) * Fraction(uf[j, k])) for k in range(K))
+                    gd = Decimal(g.numerator) / Decimal(g.denominator)
+                    ud = Decimal(u.numerator) / Decimal(u.denominator)
+                    sd = gd / (1 + (-gd).exp())
+                    ref = sd * ud
+                    bound = (Decimal(1.1) * Decimal(float(mg)) * abs(ud) + abs(sd) * Decimal(float(mu))) \
+                        * Decimal(2) ** -46 + abs(ref) * Decimal(2) ** -50
+                    err = abs(Decimal(float(H[i, j])) - ref)
+                    assert err <= bound, (M, N, K, i, j, float(err), float(bound))
+
+
+def pin_glu_closed_forms(orc):
+    """K = 1 cases whose SiLU has a closed form in e."""
+    e = math.e
+    # X is one column of scalars, the weights are scalars: G = x*wg, U = x*wu.
+    xs = [1.0, -1.0, 2.0, 0.5]
+    wg = [1.0, 2.0, -1.0]
+    wu = [1.0, -0.5, 3.0]
+    X = wl.bits(torch.tensor(xs, dtype=torch.float32).reshape(4, 1).to(torch.bfloat16))
+    Wg = wl.bits(torch.tensor(wg, dtype=torch.float32).reshape(3, 1).to(torch.bfloat16))
+    Wu = wl.bits(torch.tensor(wu, dtype=torch.float32).reshape(3, 1).to(torch.bfloat16))
+    silu_closed = {1.0: e / (1 + e), -1.0: -1 / (1 + e), 2.0: 2 * e * e / (1 + e * e),
+                   -2.0: -2 / (1 + e * e), 0.5: 0.5 * math.sqrt(e) / (1 + math.sqrt(e)),
+                   -0.5: -0.5 / (1 + math.sqrt(e)), 4.0: 4 * e ** 4 / (1 + e ** 4), -4.0: -4 / (1 + e ** 4)}
+    H = orc.swiglu(X, Wg, Wu)
+    for i, x in enumerate(xs):
+        for j in range(3):
+            ref = silu_closed[x * wg[j]] * (x * wu[j])
+            assert abs(H[i, j] - ref) <= 4e-16 * abs(ref), (i, j, H[i, j], ref)
+
+
+def pin_glu_scipy_expit(orc, seed=21):
+    """numpy's float64 matmul with scipy's logistic function."""
+    from scipy.special import expit
+    rng = np.random.default_rng(seed)
+    M, N, K = 23, 31, 257
+    X = _rand_bits(rng, (M, K), 3.0)
+    Wg = _rand_bits(rng, (N, K), 1.0 / np.sqrt(K))
+    Wu = _rand_bits(rng, (N, K), 1.0 / np.sqrt(K))
+    G, U, mg, mu = _glu_f64(X, Wg, Wu)
+    ref = G * expit(G) * U
+    H = orc.swiglu(X, Wg, Wu)
+    assert (np.abs(H - ref) <= _glu_bound(G, U, mg, mu, ref, 1e-13)).all()
+
+
+def pin_glu_odd_even_parts(orc, seed=22):
+    """silu(z) - silu(-z) = z and silu(z) + silu(-z) = z tanh(z/2): with the
+    gate weights negated, H - H' = G U and H + H' = G U tanh(G/2)."""
+    rng = np.random.default_rng(seed)
+    M, N, K = 17, 13, 64
+    X = _rand_bits(rng, (M, K), 2.0)
+    Wg = _rand_bits(rng, (N, K), 1.0 / np.sqrt(K))
+    Wu = _rand_bits(rng, (N, K), 1.0 / np.sqrt(K))
+    G, U, mg, mu = _glu_f64(X, Wg, Wu)
+    H = orc.swiglu(X, Wg, Wu)
+    Hn = orc.swiglu(X, _neg_bits(Wg), Wu)
+    odd = G * U
+    even = G * U * np.tanh(G / 2)
+    assert (np.abs((H - Hn) - odd) <= _glu_bound(G, U, mg, mu, odd, 1e-13) * 4).all()
+    assert (np.abs((H + Hn) - even) <= _glu_bound(G, U, mg, mu, even, 1e-13) * 4).all()
+
+
+def pin_glu_tails(orc):
+    """Integer operands: gate sums >= 40 give H = G U exactly (the sigmoid is 1
+    in double), gate sums <= -800 give H = 0 (the exponential overflows)."""
+    X = wl.bits(torch.tensor([[8.0, 8.0], [-16.0, 4.0]]).to(torch.bfloat16))
+    Wg = wl.bits(torch.tensor([[4.0, 2.0], [-64.0, -64.0], [-4.0, 8.0]]).to(torch.bfloat16))
+    Wu = wl.bits(torch.tensor([[3.0, -1.0], [1.0, 1.0], [0.5, 2.0]]).to(torch.bfloat16))
+    H = orc.swiglu(X, Wg, Wu)
+    xf, gf, uf = bf16_bits_to_f64(X), bf16_bits_to_f64(Wg), bf16_bits_to_f64(Wu)
+    G, U = xf @ gf.T, xf @ uf.T
+    for i in range(2):
+        for j in range(3):
+            if G[i, j] >= 40:
+                assert H[i, j] == G[i, j] * U[i, j], (i, j)
+            elif G[i, j] <= -800:
+                assert H[i, j] == 0.0, (i, j)
+    assert (G >= 40).sum() >= 2 and (G <= -800).sum() >= 1
+
+
+def pin_glu_zero_operands(orc, seed=23):
+    """A zero gate, a zero up projection, zero activations or K = 0 give H = 0."""
+    rng = np.random.default_rng(seed)
+    M, N, K = 6, 7, 33
+    X = _rand_bits(rng, (M, K))
+    Wg = _rand_bits(rng, (N, K))
+    Wu = _rand_bits(rng, (N, K))
+    z = np.zeros
+    for args in ((X, z((N, K), np.uint16), Wu), (X, Wg, z((N, K), np.uint16)), (z((M, K), np.uint16), Wg, Wu)):
+        assert (orc.swiglu(*args) == 0).all()
+    e = np.zeros((M, 0), np.uint16)
+    assert (orc.swiglu(e, np.zeros((N, 0), np.uint16), np.zeros((N, 0), np.uint16)) == 0).all()
+
+
+def pin_glu_permutations(orc, seed=24):
+    """Permuting X's rows permutes H's rows; permuting Wg's and Wu's rows
+    together permutes H's columns (bit for bit: each element is computed on
+    its own); a gate/up swap changes the result."""
+    rng = np.random.default_rng(seed)
+    M, N, K = 9, 11, 40
+    X = _rand_bits(rng, (M, K), 2.0)
+    Wg = _rand_bits(rng, (N, K), 1.0 / np.sqrt(K))
+    Wu = _rand_bits(rng, (N, K), 1.0 / np.sqrt(K))
+    H = orc.swiglu(X, Wg, Wu)
+    pr, pc = rng.permutation(M), rng.permutation(N)
+    np.testing.assert_array_equal(orc.swiglu(X[pr], Wg, Wu), H[pr])
+    np.testing.assert_array_equal(orc.swiglu(X, Wg[pc], Wu[pc]), H[:, pc])
+    assert not np.allclose(orc.swiglu(X, Wu, Wg), H)
+
+
+def pin_glu_at_matches_full(orc, seed=25):
+    rng = np.random.default_rng(seed)
+    M, N, K = 8, 9, 10
+    X = _rand_bits(rng, (M, K), 2.0)
+    Wg = _rand_bits(rng, (N, K))
+    Wu = _rand_bits(rng, (N, K))
+    full = orc.swiglu(X, Wg, Wu)
+    rows = rng.integers(0, M, 40)
+    cols = rng.integers(0, N, 40)
+    np.testing.assert_array_equal(orc.swiglu_at(X, Wg, Wu, rows, cols), full[rows, cols])
+
+
+GLU_PINS = [
+    pin_glu_exact_bruteforce,
+    pin_glu_closed_forms,
+    pin_glu_scipy_expit,
+    pin_glu_odd_even_parts,
+    pin_glu_tails,
+    pin_glu_zero_operands,
+    pin_glu_permutations,
+    pin_glu_at_matches_full,
+]
+
 ALL_PINS = [
     pin_exact_bruteforce,
     pin_golden_hand_worked,
@@ -358,4 +542,4 @@ ALL_PINS = [
     pin_round_midpoints,
     pin_round_specials,
     pin_round_like_torch,
-] + EX_PINS
+] + EX_PINS + GLU_PINS

@@ -33,6 +33,16 @@ MUTANTS = {
                       "d += alpha * beta * bf16_bits_to_double(C[i * ldc + j]);"),
     "ex_beta_zero_reads_c": ("if (C && beta != 0.0)", "if (C)"),
     "ex_alpha_dropped": ("double d = alpha * s;", "double d = s;"),
+    "glu_silu_dropped": ("return silu(g) * u;", "return g * u;"),
+    "glu_sigmoid_sign": ("return z / (1.0 + exp(-z));", "return z / (1.0 + exp(z));"),
+    "glu_sigmoid_only": ("return z / (1.0 + exp(-z));", "return 1.0 / (1.0 + exp(-z));"),
+    "glu_gate_up_swapped": ("return silu(g) * u;", "return silu(u) * g;"),
+    "glu_gate_reads_up": ("g += x * bf16_bits_to_double(Wg[j * K + k]);",
+                          "g += x * bf16_bits_to_double(Wu[j * K + k]);"),
+    "glu_up_k_shifted": ("u += x * bf16_bits_to_double(Wu[j * K + k]);",
+                         "u += x * bf16_bits_to_double(Wu[j * K + (k + 1) % K]);"),
+    "glu_float_gate": ("    double g = 0.0;\n", "    float g = 0.0f;\n"),
+    "glu_exp_base_2": ("return z / (1.0 + exp(-z));", "return z / (1.0 + exp2(-z));"),
 }
 
 
