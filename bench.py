@@ -22,9 +22,11 @@ Printed JSON line (stdout, last line):
             by their summed durations, against the MI355X peak
   cpu_baseline  the CPU oracle (fp64, OpenMP) on a time-bounded row sample
             of the same 16 shapes, same aggregation
-Per-shape rows, the geometric mean of per-shape roofline fractions, and the
-three single-shape gates (decode M=16, prefill 4096^3, square 8192^3 plain)
-are extra fields of the same line.
+Per-shape rows, the geometric mean of per-shape roofline fractions, the
+three single-shape gates (decode M=16, prefill 4096^3, square 8192^3 plain),
+the general form (alpha, beta, bias, row strides) and SwiGLU (the decoder
+layer's gate/up projections with the SiLU-multiply fused) on decoder-layer
+shapes are extra fields of the same line.
 """
 from __future__ import annotations
 
@@ -206,6 +208,62 @@ class GeneralCase(Case):
         ka.gemm_bf16_ex(x, W, c, b, self.w.alpha, self.w.beta, out=y)
 
 
+class GluCase(Case):
+    """A SwiGLU workload: H = silu(X Wg^T) * (X Wu^T)."""
+
+    def __init__(self, w, ka, torch, rotate=True, plan=None):
+        from paper_2608_17071_amd import workloads as wl
+        t = wl.make_glu_inputs(w)
+        self.w = w
+        self.host = t
+        x, g, u = t["X"].cuda(), t["Wg"].cuda(), t["Wu"].cuda()
+        n = 1
+        if rotate:
+            n = max(2, min(MAX_COPIES, -(-ROTATE_BYTES // w.algorithmic_bytes)))
+        self.sets = []
+        for i in range(n):
+            self.sets.append((x if i == 0 else x.clone(), g if i == 0 else g.clone(), u if i == 0 else u.clone(),
+                              torch.empty(w.M, w.N, dtype=torch.bfloat16, device="cuda")))
+        self.forced = plan
+        self.plan = ka.select_plan_swiglu(w.M, w.N, w.K) if plan is None else plan
+        self.plan_name = ka.plan_name(self.plan)
+        self.times = []
+        self.graph = None
+
+    def call(self, ka, i):
+        x, g, u, h = self.sets[i]
+        ka.swiglu_bf16(x, g, u, out=h, plan=self.forced)
+
+
+def cpu_baseline_glu(cases, seconds):
+    """The oracle's SwiGLU on rows 0, 1, ... of each case until its time share is used."""
+    import numpy as np
+    import oracle
+    from paper_2608_17071_amd import workloads as wl
+
+    orc = oracle.default()
+    per_shape = seconds / len(cases)
+    rates, rows_done = [], []
+    for c in cases:
+        w, h = c.w, c.host
+        xb, gb, ub = wl.bits(h["X"]), wl.bits(h["Wg"]), wl.bits(h["Wu"])
+        cols = np.arange(w.N, dtype=np.int64)
+        flops, rows, t0 = 0, 0, time.perf_counter()
+        while rows < w.M:
+            orc.swiglu_at(xb, gb, ub, np.full(w.N, rows, dtype=np.int64), cols)
+            rows += 1
+            flops += 4 * w.N * w.K
+            if time.perf_counter() - t0 >= per_shape:
+                break
+        rates.append(flops / (time.perf_counter() - t0) / 1e12)
+        rows_done.append(rows)
+    return {
+        "value": geomean(rates), "unit": "TFLOP/s (fp64 oracle, SwiGLU, geomean over its shapes)",
+        "cores": orc.threads(), "kind": "oracle",
+        "sample": f"whole output rows 0..r-1 of each SwiGLU shape, r = {rows_done} (about {per_shape:.2f} s each)",
+    }
+
+
 def cpu_baseline_general(cases, seconds):
     """The oracle's general form on rows 0, 1, ... of each case until its time share is used."""
     import numpy as np
@@ -337,8 +395,11 @@ def main():
     ap.add_argument("--no-gates", action="store_true", help="skip the decode/prefill/square extras")
     ap.add_argument("--no-general", action="store_true",
                     help="skip the general-form shapes (alpha, beta, bias, row strides)")
+    ap.add_argument("--no-swiglu", action="store_true",
+                    help="skip the SwiGLU gate/up shapes")
     ap.add_argument("--only", default="",
-                    help="comma-separated workload names: time just these (for profiling one kernel)")
+                    help="comma-separated workload names (sweep, gate, general-form or SwiGLU): "
+                         "time just these (for profiling one kernel)")
     ap.add_argument("--summarize-traffic", nargs=2, metavar=("PMC_DIR", "SHAPES"),
                     help="write profiles/traffic.json for the dominant plan from counter runs")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -378,8 +439,13 @@ def main():
         return
 
     if args.only:
-        only = [wl.BY_NAME[n] for n in args.only.split(",")]
-        cases = [Case(w, ka, torch, rotate=not args.hot) for w in only]
+        def case_of(n):
+            if n in wl.GLU_BY_NAME:
+                return GluCase(wl.GLU_BY_NAME[n], ka, torch, rotate=not args.hot)
+            if n in wl.GENERAL_BY_NAME:
+                return GeneralCase(wl.GENERAL_BY_NAME[n], ka, torch, rotate=not args.hot)
+            return Case(wl.BY_NAME[n], ka, torch, rotate=not args.hot)
+        cases = [case_of(n) for n in args.only.split(",")]
         time_cases(cases, args.steps, args.warmup, ka, torch, use_graph=not args.no_graph)
         print(json.dumps({"only": [shape_row(c) for c in cases]}), flush=True)
         return
@@ -460,6 +526,31 @@ def main():
             c.free()
         del gcases
 
+    # SwiGLU (NEXT row: the decoder layer's gate/up projections with the
+    # SiLU-multiply fused into the epilogue); reported beside the metric.
+    swiglu = None
+    if not args.no_swiglu:
+        for c in sweep:
+            c.free()
+        scases = [GluCase(w, ka, torch, rotate=not args.hot) for w in wl.GLU]
+        time_cases(scases, args.steps, args.warmup, ka, torch, use_graph=not args.no_graph)
+        srows = []
+        for c in scases:
+            r = shape_row(c)
+            srows.append(r)
+            log(f"  {r['shape']:40s} {r['plan']:28s} {r['us']:9.2f} us {r['tflops']:8.1f} TF "
+                f"{r['gbps']:7.0f} GB/s  {r['bound']} frac {r['roofline_frac']:.3f}")
+        swiglu = {"op": "H = silu(X Wg^T) * (X Wu^T), FLOPs counted as 4MNK",
+                  "shapes": srows,
+                  "geomean_tflops": round(geomean([r["tflops"] for r in srows]), 3),
+                  "geomean_roofline_frac": round(geomean([r["roofline_frac"] for r in srows]), 4)}
+        if not args.no_cpu_baseline:
+            log("timing the CPU oracle on SwiGLU (~4 s) ...")
+            swiglu["cpu_baseline"] = cpu_baseline_glu(scases, 4.0)
+        for c in scases:
+            c.free()
+        del scases
+
     cpu = None
     if not args.no_cpu_baseline:
         log(f"timing the CPU oracle (~{args.cpu_seconds:.0f} s) ...")
@@ -486,6 +577,7 @@ def main():
         "shapes": rows,
         "gates": gates,
         "general": general,
+        "swiglu": swiglu,
     }
     print(json.dumps(out), flush=True)
 

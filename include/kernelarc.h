@@ -163,6 +163,47 @@ int kernelarc_gemm_bf16_ex_with_plan(int plan, int64_t M, int64_t N, int64_t K, 
 int kernelarc_select_plan_ex(int64_t M, int64_t N, int64_t K, int has_c, int64_t ldx, int64_t ldw,
                              int64_t ldc, int64_t ldy, float alpha, float beta, int has_bias);
 
+/*
+ * Gated MLP input projection with the SiLU-multiply (SwiGLU): the decoder
+ * layer's gate and up projections and the activation that joins them
+ * (decoder-layer case study, Alg. 7: BF16 gate/up projections followed by a
+ * SiLU-multiply, and the fused gate/up GEMM with a SwiGLU epilogue), in one
+ * kernel:
+ *
+ *     H[i,j] = bf16( silu(G[i,j]) * U[i,j] ),   silu(z) = z / (1 + e^-z),
+ *     G = X Wg^T,  U = X Wu^T
+ *
+ * X is [M,K] (the normalised hidden states), Wg and Wu are [N,K] (gate and
+ * up weights, nn.Linear orientation, N = intermediate size), H is [M,N];
+ * all dense row-major bf16 device buffers owned by the caller.  G and U are
+ * accumulated in fp32 and never rounded to bf16; SiLU and the product are
+ * evaluated in fp32 (SiLU within a few fp32 ulps) and rounded once to bf16,
+ * nearest-even.  A merged [2N,K] gate_up weight is passed as Wg = W and
+ * Wu = W + N*K.  Wg and Wu may overlap each other (they are only read); H
+ * overlapping X, Wg or Wu is rejected with KERNELARC_ERR_INVALID_ARG.
+ * M, K >= 0 and below 2^31, 0 <= N < 2^30.  M == 0 or N == 0: no launch.
+ * K == 0: H = 0.  16-byte aligned pointers with K a multiple of 8 take the
+ * MFMA tile kernels; anything else takes a generic kernel with the same
+ * contract.  Non-finite sums propagate as the formula does in IEEE
+ * arithmetic (silu(-inf) is NaN).
+ */
+int kernelarc_swiglu_bf16(int64_t M, int64_t N, int64_t K, const void *X,
+                          const void *Wg, const void *Wu, void *H, hipStream_t stream);
+
+/* SwiGLU with a forced plan (KERNELARC_ERR_UNSUPPORTED if the plan cannot
+ * compute it: only tile plans whose waves hold gate/up block pairs, and the
+ * generic plan). */
+int kernelarc_swiglu_bf16_with_plan(int plan, int64_t M, int64_t N, int64_t K, const void *X,
+                                    const void *Wg, const void *Wu, void *H, hipStream_t stream);
+
+/* The plan kernelarc_swiglu_bf16 runs for these sizes with aligned
+ * pointers; -1 for negative sizes. */
+int kernelarc_select_plan_swiglu(int64_t M, int64_t N, int64_t K);
+
+/* 1 if `plan` can compute SwiGLU at these sizes, 0 if not, -1 for an unknown
+ * plan or negative sizes. */
+int kernelarc_plan_supports_swiglu(int plan, int64_t M, int64_t N, int64_t K);
+
 /* Static description of a status code. */
 const char *kernelarc_status_string(int status);
 

@@ -111,6 +111,10 @@ const PlanInfo PLANS[] = {
     {"stream_mfma16_k128", KIND_STREAM, 128, 1},
     {"stream_mfma16_k128_splitk", KIND_STREAM, 128, 0},
     {"stream_mfma16_k64_splitk", KIND_STREAM, 64, 0},
+    {"tile_32x256_k64s4_w4", KIND_TILE, TC_32x256_K64_S4_W4, 1},
+    {"tile_32x256_k64s4_w4_splitk", KIND_TILE, TC_32x256_K64_S4_W4, 0},
+    {"tile_256x256_k64_w4_tailsplit", KIND_TILE, TC_256x256_K64_S2_W4, -1},
+    {"tile_128x256_k64_w8_tailsplit", KIND_TILE, TC_128x256_K64_S2_W8, -1},
 };
 constexpr int NUM_PLANS = static_cast<int>(sizeof(PLANS) / sizeof(PLANS[0]));
 
@@ -318,6 +322,63 @@ int select(int64_t M, int64_t N, int64_t K, bool residual, const Layout &lay) {
     return plan >= 0 ? plan : PLAN_GENERIC;
 }
 
+// SwiGLU (gate and up projections with the SiLU-multiply): the tile plans
+// whose configuration pairs gate and up blocks, and the generic kernel.  A
+// tile computes BM x BN/2 outputs from a BM x BN block of products, so tile
+// counts and split-K rules are those of the doubled width 2N.
+bool supports_glu(int plan, int64_t M, int64_t N, int64_t K) {
+    if (M < 0 || N < 0 || K < 0 || M > LIMIT_DIM || N > LIMIT_DIM / 2 || K > LIMIT_DIM) return false;
+    if (plan < 0 || plan >= NUM_PLANS) return false;
+    const PlanInfo &pi = PLANS[plan];
+    if (pi.kind == KIND_GENERIC) return cdiv(M, 64) * cdiv(N, 64) * 256 <= LIMIT_ITEMS;
+    if (pi.kind != KIND_TILE || !tile_glu_ok(pi.tile_cfg) || K % 8 != 0) return false;
+    const TileShape ts = tile_shape(pi.tile_cfg);
+    if (ts.bm * K * 2 >= PANEL_LIMIT || (ts.bn / 2) * K * 2 >= PANEL_LIMIT || ts.bm * N * 2 >= PANEL_LIMIT)
+        return false;
+    const int64_t tiles = tile_count(ts, M, 2 * N);
+    const TileSplit sp = tile_split_plan(plan, M, 2 * N, K);
+    const int64_t split_tiles = tiles - sp.full_tiles;
+    if ((sp.full_tiles + split_tiles * sp.split) * 1024 > LIMIT_ITEMS) return false;
+    if (sp.split > 1 && (split_tiles * sp.split * ts.bm * ts.bn > WS_PARTIAL_FLOATS || split_tiles > WS_COUNTERS))
+        return false;
+    return true;
+}
+
+// SwiGLU plan rule (from measurements on MI355X over M = 1 .. 4096 at
+// Llama-class hidden/intermediate sizes; tile counts at width 2N): up to 64
+// rows the 64x128 4-stage tile, with split-K when its tiles fill at most
+// half the CUs and K is deep enough; up to 128 rows, or while 256x128 tiles
+// would fill less than half the CUs, 128x128 tiles (3 stages and split-K
+// when they fill at most half the CUs, else 4 stages with the lagged
+// refill); then the 256x256 8-wave tile once its tiles cover at least 80%
+// of the CUs (tail split past whole rounds), else the 256x128 8-wave tile
+// with 3 stages and the lagged refill.
+int select_glu(int64_t M, int64_t N, int64_t K) {
+    if (M < 0 || N < 0 || K < 0) return -1;
+    if (K % 8 != 0) return PLAN_GENERIC;
+    auto pick = [&](const char *name) {
+        const int plan = plan_index(name);
+        return (plan >= 0 && supports_glu(plan, M, N, K)) ? plan : -1;
+    };
+    const int64_t N2 = 2 * N;
+    const int64_t t64 = tile_count(tile_shape(TC_64x128_K64_S4_W4), M, N2);
+    const int64_t t128 = tile_count(tile_shape(TC_128x128_K64_S4_W4_L), M, N2);
+    const int64_t t256x128 = tile_count(tile_shape(TC_256x128_K64_S3_W8_L), M, N2);
+    const int64_t t256 = tile_count(tile_shape(TC_256x256_K64_S2_W8), M, N2);
+    int plan = -1;
+    if (M <= 64) {
+        plan = (2 * t64 <= CUS && K >= 2048) ? pick("tile_64x128_k64s4_w4_splitk") : pick("tile_64x128_k64s4_w4");
+    } else if (M <= 128 || 2 * t256x128 < CUS) {
+        plan = 2 * t128 <= CUS ? pick("tile_128x128_k64s3_w4_splitk") : pick("tile_128x128_k64s4_w4_lag");
+    } else if (5 * t256 >= 4 * CUS) {
+        plan = pick("tile_256x256_k64_w8_tailsplit");
+    } else {
+        plan = pick("tile_256x128_k64s3_w8_lag");
+    }
+    if (plan < 0) plan = pick("tile_128x128_k64_w4");
+    return plan >= 0 ? plan : PLAN_GENERIC;
+}
+
 // ------------------------------------------------------------ devices ----
 constexpr int MAX_DEVICES = 64;
 
@@ -509,6 +570,59 @@ int run(int plan, Request q, hipStream_t stream) {
     return KERNELARC_OK;
 }
 
+// SwiGLU call: H = bf16(silu(X Wg^T) * (X Wu^T)); plan < 0: choose.
+int run_glu(int plan, int64_t M, int64_t N, int64_t K, const void *X, const void *Wg, const void *Wu, void *H,
+            hipStream_t stream) {
+    g_last_error[0] = '\0';
+    if (M < 0 || N < 0 || K < 0)
+        return fail(KERNELARC_ERR_INVALID_ARG, "negative size M=%lld N=%lld K=%lld", (long long)M,
+                    (long long)N, (long long)K);
+    if (M > LIMIT_DIM || N > LIMIT_DIM / 2 || K > LIMIT_DIM)
+        return fail(KERNELARC_ERR_INVALID_ARG, "a size is too large (M, K < 2^31, N < 2^30)");
+    if (plan >= NUM_PLANS) return fail(KERNELARC_ERR_UNSUPPORTED, "unknown plan %d", plan);
+    if (M == 0 || N == 0) return KERNELARC_OK;
+    if (!H) return fail(KERNELARC_ERR_INVALID_ARG, "H is NULL");
+    if (K > 0 && (!X || !Wg || !Wu)) return fail(KERNELARC_ERR_INVALID_ARG, "X, Wg or Wu is NULL");
+    const int64_t hbytes = M * N * 2;
+    if (overlaps(H, hbytes, X, M * K * 2) || overlaps(H, hbytes, Wg, N * K * 2) || overlaps(H, hbytes, Wu, N * K * 2))
+        return fail(KERNELARC_ERR_INVALID_ARG, "H overlaps X, Wg or Wu");
+
+    int dev = 0, num_cus = 0;
+    const int st = current_device(&dev, &num_cus);
+    if (st != KERNELARC_OK) return st;
+
+    const bool vec_ok = aligned16(X) && aligned16(Wg) && aligned16(Wu) && aligned16(H) && K % 8 == 0;
+    if (plan < 0) {
+        plan = select_glu(M, N, K);
+        if (plan != PLAN_GENERIC && !vec_ok) plan = PLAN_GENERIC;
+    } else {
+        if (!supports_glu(plan, M, N, K))
+            return fail(KERNELARC_ERR_UNSUPPORTED, "plan %s cannot compute SwiGLU at M=%lld N=%lld K=%lld",
+                        PLANS[plan].name, (long long)M, (long long)N, (long long)K);
+        if (plan != PLAN_GENERIC && !vec_ok)
+            return fail(KERNELARC_ERR_UNSUPPORTED, "plan %s needs 16-byte aligned pointers and K a multiple of 8",
+                        PLANS[plan].name);
+    }
+    const GluProblem p{M, N, K, static_cast<const uint16_t *>(X), static_cast<const uint16_t *>(Wg),
+                       static_cast<const uint16_t *>(Wu), static_cast<uint16_t *>(H)};
+    (void)hipGetLastError();
+    hipError_t e = hipSuccess;
+    if (PLANS[plan].kind == KIND_GENERIC) {
+        e = launch_generic_glu(p, stream);
+    } else {
+        const TileSplit sp = tile_split_plan(plan, M, 2 * N, K);
+        Workspace ws{};
+        if (sp.split > 1) {
+            const int wst = workspace(dev, stream, &ws);
+            if (wst != KERNELARC_OK) return wst;
+        }
+        e = launch_tile_glu(PLANS[plan].tile_cfg, p, sp.split, sp.full_tiles, sp.split > 1 ? &ws : nullptr, stream);
+    }
+    if (e != hipSuccess)
+        return fail(KERNELARC_ERR_LAUNCH, "launch of %s failed: %s", PLANS[plan].name, hipGetErrorString(e));
+    return KERNELARC_OK;
+}
+
 }  // namespace
 }  // namespace kernelarc
 
@@ -567,6 +681,27 @@ int kernelarc_select_plan_ex(int64_t M, int64_t N, int64_t K, int has_c, int64_t
                      ldx != K || ldw != K || (residual && ldc != N) || ldy != N || alpha != 1.0f || beta != 1.0f ||
                          has_bias != 0};
     return select(M, N, K, residual, lay);
+}
+
+int kernelarc_swiglu_bf16(int64_t M, int64_t N, int64_t K, const void *X, const void *Wg, const void *Wu, void *H,
+                          hipStream_t stream) {
+    return run_glu(-1, M, N, K, X, Wg, Wu, H, stream);
+}
+
+int kernelarc_swiglu_bf16_with_plan(int plan, int64_t M, int64_t N, int64_t K, const void *X, const void *Wg,
+                                    const void *Wu, void *H, hipStream_t stream) {
+    if (plan < 0) {
+        g_last_error[0] = '\0';
+        return fail(KERNELARC_ERR_UNSUPPORTED, "unknown plan %d", plan);
+    }
+    return run_glu(plan, M, N, K, X, Wg, Wu, H, stream);
+}
+
+int kernelarc_select_plan_swiglu(int64_t M, int64_t N, int64_t K) { return select_glu(M, N, K); }
+
+int kernelarc_plan_supports_swiglu(int plan, int64_t M, int64_t N, int64_t K) {
+    if (plan < 0 || plan >= NUM_PLANS || M < 0 || N < 0 || K < 0) return -1;
+    return supports_glu(plan, M, N, K) ? 1 : 0;
 }
 
 int kernelarc_plan_count(void) { return NUM_PLANS; }

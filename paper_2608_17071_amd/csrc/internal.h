@@ -49,7 +49,8 @@ enum TileCfg : int {
     TC_64x64_K64_S2_G4 = 23,      // four K groups (16 waves)
     TC_256x128_K64_S3_W8_L = 24,   // lagged refill
     TC_128x128_K64_S4_W4_L = 25,
-    TC_COUNT = 26,
+    TC_32x256_K64_S4_W4 = 26,      // one 32-row wave band (skinny M)
+    TC_COUNT = 27,
 };
 
 struct TileShape {
@@ -78,7 +79,16 @@ struct DenseProblem {
     uint16_t *Y;
 };
 
-// Uniform access to either form inside the kernels.
+// Gated MLP input projection (SwiGLU): Y = bf16(silu(X W^T) * (X W2^T)),
+// W the gate and W2 the up weights, all dense.  The tile kernels stage the
+// two weight panels side by side as one B tile of twice the output width.
+struct GluProblem {
+    int64_t M, N, K;
+    const uint16_t *X, *W, *W2;  // X [M,K]; W (gate), W2 (up) [N,K]
+    uint16_t *Y;                 // [M,N]
+};
+
+// Uniform access to every form inside the kernels.
 __host__ __device__ inline int64_t ldx_of(const Problem &p) { return p.ldx; }
 __host__ __device__ inline int64_t ldw_of(const Problem &p) { return p.ldw; }
 __host__ __device__ inline int64_t ldr_of(const Problem &p) { return p.ldr; }
@@ -93,6 +103,17 @@ __host__ __device__ inline int64_t ldy_of(const DenseProblem &p) { return p.N; }
 __host__ __device__ inline float alpha_of(const DenseProblem &) { return 1.0f; }
 __host__ __device__ inline float beta_of(const DenseProblem &) { return 1.0f; }
 __host__ __device__ inline const uint16_t *bias_of(const DenseProblem &) { return nullptr; }
+
+__host__ __device__ inline int64_t ldx_of(const GluProblem &p) { return p.K; }
+__host__ __device__ inline int64_t ldw_of(const GluProblem &p) { return p.K; }
+__host__ __device__ inline int64_t ldr_of(const GluProblem &p) { return p.N; }
+__host__ __device__ inline int64_t ldy_of(const GluProblem &p) { return p.N; }
+__host__ __device__ inline float alpha_of(const GluProblem &) { return 1.0f; }
+__host__ __device__ inline float beta_of(const GluProblem &) { return 1.0f; }
+__host__ __device__ inline const uint16_t *bias_of(const GluProblem &) { return nullptr; }
+__host__ __device__ inline const uint16_t *resid_of(const Problem &p) { return p.R; }
+__host__ __device__ inline const uint16_t *resid_of(const DenseProblem &p) { return p.R; }
+__host__ __device__ inline const uint16_t *resid_of(const GluProblem &) { return nullptr; }
 
 // True unless the call is the plain operator (then the dense kernels run).
 inline bool is_general(const Problem &p) {
@@ -124,6 +145,12 @@ hipError_t launch_skinny(const Problem &p, int split_k, const Workspace *ws, hip
 // order) are split in K, the others run whole (see kernel_tile.hip).
 hipError_t launch_tile(int cfg, const Problem &p, int split, int64_t full_tiles, const Workspace *ws, hipStream_t s);
 hipError_t launch_stream(const Problem &p, int bk, int split, const Workspace *ws, hipStream_t s);
+// SwiGLU: the generic kernel, and the tile kernels of the configurations
+// that can pair gate and up blocks (tile_glu_ok).
+hipError_t launch_generic_glu(const GluProblem &p, hipStream_t s);
+hipError_t launch_tile_glu(int cfg, const GluProblem &p, int split, int64_t full_tiles, const Workspace *ws,
+                           hipStream_t s);
+bool tile_glu_ok(int cfg);
 
 // Shape rules of the kernels, used by the plan table (host only).
 int skinny_split_for(int64_t M, int64_t N, int64_t K);
@@ -156,6 +183,16 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
 __device__ __forceinline__ float combine(float acc, float r, bool has_r, float alpha, float beta) {
     const float a = alpha * acc;
     return has_r ? __builtin_fmaf(beta, r, a) : a;
+}
+
+// silu(z) = z * sigmoid(z) = z / (1 + e^-z) in fp32: e^-z as 2^(-z log2 e)
+// (v_exp_f32) and the reciprocal by v_rcp_f32, each within about 1 ulp, so
+// the result is within a few fp32 ulps (plus |z| 2^-24 relative from the
+// scaled exponent), far below one bf16 rounding.  For z <= -88.7 the power
+// overflows to infinity and the result is -0; for large z it is z.
+__device__ __forceinline__ float silu_f32(float z) {
+    const float t = __builtin_amdgcn_exp2f(-z * 1.44269504088896341f);
+    return z * __builtin_amdgcn_rcpf(1.0f + t);
 }
 
 // Two values at once (one v_cvt_pk_bf16_f32): lo in bits 0-15, hi in 16-31.

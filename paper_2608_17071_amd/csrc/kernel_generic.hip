@@ -1,5 +1,6 @@
-// Generic kernel: Y = alpha X W^T (+ beta R) (+ bias) for any shape, any
-// row strides and any pointer alignment.
+// Generic kernels: Y = alpha X W^T (+ beta R) (+ bias) for any shape, any
+// row strides and any pointer alignment, and SwiGLU for any shape and
+// alignment.
 //
 // This is the correctness fallback (K not a multiple of 8, pointers not
 // 16-byte aligned).  Each 256-thread workgroup computes a 64x64 output tile;
@@ -76,7 +77,82 @@ __global__ __launch_bounds__(256) void generic_kernel(Problem p, int64_t tiles_n
     }
 }
 
+// SwiGLU fallback: the same tiling with both weight operands staged, the
+// gate and up sums kept side by side, and silu(g) * u rounded once.
+__global__ __launch_bounds__(256) void generic_glu_kernel(GluProblem p, int64_t tiles_n) {
+    __shared__ float xs[GK][GT + 1];
+    __shared__ float gs[GK][GT + 1];
+    __shared__ float us[GK][GT + 1];
+
+    const int tx = threadIdx.x & 15;
+    const int ty = threadIdx.x >> 4;
+    const int64_t tile = blockIdx.x;
+    const int64_t m0 = (tile / tiles_n) * GT;
+    const int64_t n0 = (tile % tiles_n) * GT;
+
+    float g[4][4], u[4][4];
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int b = 0; b < 4; ++b) g[a][b] = u[a][b] = 0.0f;
+
+    for (int64_t k0 = 0; k0 < p.K; k0 += GK) {
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            const int idx = threadIdx.x + 256 * t;
+            const int r = idx / GK;
+            const int kk = idx % GK;
+            const int64_t k = k0 + kk;
+            const int64_t xm = m0 + r;
+            const int64_t wn = n0 + r;
+            const bool kin = k < p.K;
+            xs[kk][r] = (xm < p.M && kin) ? bf16_to_f32(p.X[xm * p.K + k]) : 0.0f;
+            gs[kk][r] = (wn < p.N && kin) ? bf16_to_f32(p.W[wn * p.K + k]) : 0.0f;
+            us[kk][r] = (wn < p.N && kin) ? bf16_to_f32(p.W2[wn * p.K + k]) : 0.0f;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int kk = 0; kk < GK; ++kk) {
+            float xv[4], gv[4], uv[4];
+#pragma unroll
+            for (int a = 0; a < 4; ++a) xv[a] = xs[kk][ty + 16 * a];
+#pragma unroll
+            for (int b = 0; b < 4; ++b) {
+                gv[b] = gs[kk][tx + 16 * b];
+                uv[b] = us[kk][tx + 16 * b];
+            }
+#pragma unroll
+            for (int a = 0; a < 4; ++a)
+#pragma unroll
+                for (int b = 0; b < 4; ++b) {
+                    g[a][b] = fmaf(xv[a], gv[b], g[a][b]);
+                    u[a][b] = fmaf(xv[a], uv[b], u[a][b]);
+                }
+        }
+        __syncthreads();
+    }
+
+#pragma unroll
+    for (int a = 0; a < 4; ++a) {
+        const int64_t i = m0 + ty + 16 * a;
+        if (i >= p.M) continue;
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+            const int64_t j = n0 + tx + 16 * b;
+            if (j >= p.N) continue;
+            p.Y[i * p.N + j] = f32_to_bf16_rne(silu_f32(g[a][b]) * u[a][b]);
+        }
+    }
+}
+
 }  // namespace
+
+hipError_t launch_generic_glu(const GluProblem &p, hipStream_t s) {
+    const int64_t tiles_n = (p.N + GT - 1) / GT;
+    const int64_t tiles = ((p.M + GT - 1) / GT) * tiles_n;
+    hipLaunchKernelGGL(generic_glu_kernel, dim3(static_cast<unsigned>(tiles)), dim3(256), 0, s, p, tiles_n);
+    return hipGetLastError();
+}
 
 hipError_t launch_generic(const Problem &p, hipStream_t s) {
     const int64_t tiles_m = (p.M + GT - 1) / GT;

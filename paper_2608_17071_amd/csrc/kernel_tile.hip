@@ -124,23 +124,42 @@ struct Cfg {
     static_assert(!LAG || STAGES >= 3, "lagged refill needs three stages");
 };
 
+// Load block (RPI rows of the stage's B tile) that B load qb of a wave
+// fills.  SwiGLU: the B tile alternates 32-row blocks of gate and up rows
+// (block 2b holds gate rows 32b.., block 2b+1 the up rows of the same
+// outputs); a wave's first B_LOADS/2 loads fill gate blocks and the rest up
+// blocks, so which weight a load reads is fixed at compile time.
+template <class C, bool GLU>
+__device__ __forceinline__ int b_block(int wave, int qb) {
+    if constexpr (!GLU) {
+        return wave * C::B_LOADS + qb;
+    } else {
+        constexpr int HALF = C::B_LOADS / 2, PER = 32 / C::RPI;   // load blocks per 32-row block
+        const bool up = qb >= HALF;
+        const int idx = wave * HALF + (up ? qb - HALF : qb);     // among the gate (or up) load blocks
+        return (idx / PER) * 2 * PER + (up ? PER : 0) + idx % PER;
+    }
+}
+
 // Enqueue LDS-direct load q (A loads first, then B) of the K step at
 // element kbase (byte kbytes within a row) into one stage buffer.  Chunks
-// at or past K are pointed out of range and arrive as zeros.
-template <class C, int q>
+// at or past K are pointed out of range and arrive as zeros.  rb2 is the
+// up-weight panel of SwiGLU (unused otherwise).
+template <class C, int q, bool GLU>
 __device__ __forceinline__ void issue_load(char *stage, const __amdgpu_buffer_rsrc_t &ra,
-                                           const __amdgpu_buffer_rsrc_t &rb, const uint32_t *a_off,
-                                           const int *a_k, const uint32_t *b_off, const int *b_k, int wave,
-                                           int64_t kbase, uint32_t kbytes, int64_t K) {
+                                           const __amdgpu_buffer_rsrc_t &rb, const __amdgpu_buffer_rsrc_t &rb2,
+                                           const uint32_t *a_off, const int *a_k, const uint32_t *b_off,
+                                           const int *b_k, int wave, int64_t kbase, uint32_t kbytes, int64_t K) {
     if constexpr (q < C::A_LOADS) {
         const int blk = wave * C::A_LOADS + q;
         const uint32_t off = (kbase + a_k[q] < K) ? a_off[q] + kbytes : OOB_OFFSET;
         __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void *)(stage + blk * 1024), 16, off, 0, 0, 0);
     } else {
         constexpr int qb = q - C::A_LOADS;
-        const int blk = wave * C::B_LOADS + qb;
+        const int blk = b_block<C, GLU>(wave, qb);
         const uint32_t off = (kbase + b_k[qb] < K) ? b_off[qb] + kbytes : OOB_OFFSET;
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_void *)(stage + C::A_BYTES + blk * 1024), 16,
+        const __amdgpu_buffer_rsrc_t &r = (GLU && qb >= C::B_LOADS / 2) ? rb2 : rb;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void *)(stage + C::A_BYTES + blk * 1024), 16,
                                                  off, 0, 0, 0);
     }
 }
@@ -155,15 +174,16 @@ __device__ __forceinline__ void static_for(F &&f) {
     if constexpr (E > B) static_for_impl<B>(f, std::make_integer_sequence<int, E - B>{});
 }
 
-template <class C>
+template <class C, bool GLU>
 __device__ __forceinline__ void issue_stage(char *stage, const __amdgpu_buffer_rsrc_t &ra,
-                                            const __amdgpu_buffer_rsrc_t &rb, const uint32_t *a_off,
-                                            const int *a_k, const uint32_t *b_off, const int *b_k,
-                                            int wave, int kt, int64_t K) {
+                                            const __amdgpu_buffer_rsrc_t &rb, const __amdgpu_buffer_rsrc_t &rb2,
+                                            const uint32_t *a_off, const int *a_k, const uint32_t *b_off,
+                                            const int *b_k, int wave, int kt, int64_t K) {
     const int64_t kbase = static_cast<int64_t>(kt) * C::BK;
     const uint32_t kbytes = static_cast<uint32_t>(kt) * C::ROW_BYTES;
     static_for<0, C::LOADS>([&](auto q) {
-        issue_load<C, decltype(q)::value>(stage, ra, rb, a_off, a_k, b_off, b_k, wave, kbase, kbytes, K);
+        issue_load<C, decltype(q)::value, GLU>(stage, ra, rb, rb2, a_off, a_k, b_off, b_k, wave, kbase, kbytes,
+                                               K);
     });
 }
 
@@ -206,12 +226,17 @@ struct SplitK {
 
 // P = Problem: the general form (row strides, alpha, beta, bias);
 // P = DenseProblem: dense operands, and the epilogue adds R as is (the plain
-// operator).
+// operator); P = GluProblem: SwiGLU, the B tile holds BN/2 gate and BN/2 up
+// rows (alternate 32-row blocks) and the output tile is BM x BN/2.
 template <class C, class P>
 __global__ __attribute__((amdgpu_flat_work_group_size(C::THREADS, C::THREADS),
                           amdgpu_waves_per_eu(C::WAVES_PER_EU, C::WAVES_PER_EU)))
 void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) {
     constexpr bool GEN = std::is_same<P, Problem>::value;
+    constexpr bool GLU = std::is_same<P, GluProblem>::value;
+    // Output columns of the tile and of one wave's block.
+    constexpr int BNO = GLU ? C::BN / 2 : C::BN, WNO = GLU ? C::WN / 2 : C::WN;
+    static_assert(!GLU || (C::TN % 2 == 0 && C::B_LOADS % 2 == 0 && 32 % C::RPI == 0), "gate/up pairing");
     const int64_t ldx = ldx_of(p), ldw = ldw_of(p), ldr = ldr_of(p), ldy = ldy_of(p);
     __shared__ __attribute__((aligned(1024))) char lds[C::LDS_BYTES];
 
@@ -260,7 +285,7 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
         tn = in_band / rows;
     }
     const int64_t m0 = tm * C::BM;
-    const int64_t n0 = tn * C::BN;
+    const int64_t n0 = tn * BNO;
     const int64_t K = p.K;
     // This workgroup's K range [kbeg, kend); loads at or past kend read zero.
     const int64_t kbeg = piece ? slice * sk.kslice : 0;
@@ -268,11 +293,15 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
 
     // Operand panels bounded by buffer resources: rows past M (N) read 0.
     const int64_t rows_a = (p.M - m0) < C::BM ? (p.M - m0) : C::BM;
-    const int64_t rows_b = (p.N - n0) < C::BN ? (p.N - n0) : C::BN;
+    const int64_t rows_b = (p.N - n0) < BNO ? (p.N - n0) : BNO;
     const __amdgpu_buffer_rsrc_t ra =
         make_rsrc(p.X + m0 * ldx, static_cast<uint32_t>(GEN ? strided_bytes(rows_a, K, ldx) : rows_a * K * 2));
     const __amdgpu_buffer_rsrc_t rb =
         make_rsrc(p.W + n0 * ldw, static_cast<uint32_t>(GEN ? strided_bytes(rows_b, K, ldw) : rows_b * K * 2));
+    const __amdgpu_buffer_rsrc_t rb2 = [&] {
+        if constexpr (GLU) return make_rsrc(p.W2 + n0 * ldw, static_cast<uint32_t>(rows_b * K * 2));
+        else return rb;
+    }();
 
     // Staging map: lane l of load block blk fills slot l % CHUNKS of row
     // RPI*blk + l / CHUNKS, which holds global chunk (l % CHUNKS) ^ swz(row).
@@ -288,9 +317,10 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
     }
 #pragma unroll
     for (int q = 0; q < C::B_LOADS; ++q) {
-        const int r = (wave * C::B_LOADS + q) * C::RPI + lane / C::CHUNKS;
+        const int r = b_block<C, GLU>(wave, q) * C::RPI + lane / C::CHUNKS;   // row of the B tile
         const int c = slot ^ swz<C::CHUNKS>(r);
-        b_off[q] = static_cast<uint32_t>(r * ldw * 2 + c * 16);
+        const int wr = GLU ? (r >> 6) * 32 + (r & 31) : r;                    // row of its weight panel
+        b_off[q] = static_cast<uint32_t>(wr * ldw * 2 + c * 16);
         b_k[q] = c * 8;
     }
 
@@ -331,15 +361,19 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
     const uint32_t rbytes = static_cast<uint32_t>(GEN ? strided_bytes(rows_y, N, ldr) : rows_y * N * 2);
     const __amdgpu_buffer_rsrc_t ry = make_rsrc(p.Y + m0 * ldy, ybytes);
     // Without a residual the R resource is empty (its loads read zero).
-    const __amdgpu_buffer_rsrc_t rr = make_rsrc(p.R ? p.R + m0 * ldr : p.Y, p.R ? rbytes : 0u);
-    const bool has_r = p.R != nullptr;
+    const uint16_t *const R = resid_of(p);
+    const __amdgpu_buffer_rsrc_t rr = make_rsrc(R ? R + m0 * ldr : p.Y, R ? rbytes : 0u);
+    const bool has_r = R != nullptr;
     // 16-byte R/Y accesses need every row to start 16-byte aligned.
     const bool vec = (N & 7) == 0 && (ldy & 7) == 0 && (!has_r || (ldr & 7) == 0);
-    const int pr = lane / C::LANES_PER_ROW;             // row within a pass
-    const int pc = (lane % C::LANES_PER_ROW) * 8;       // first of 8 columns
-    const int64_t col0 = n0 + wn0 + pc;
-    constexpr int PASSES = 32 / C::ROWS_PER_PASS;
-    auto row_of = [&](int i, int v) { return static_cast<int64_t>(wm0 + i * 32 + v * C::ROWS_PER_PASS + pr); };
+    // Epilogue staging geometry for the wave's WNO output columns.
+    constexpr int EPS = WNO + 4, LPR = WNO / 8, RPP = 64 / LPR;
+    static_assert(GLU || (EPS == C::EPI_STRIDE && LPR == C::LANES_PER_ROW && RPP == C::ROWS_PER_PASS), "staging");
+    const int pr = lane / LPR;                          // row within a pass
+    const int pc = (lane % LPR) * 8;                    // first of 8 columns
+    const int64_t col0 = n0 + wn0 / (C::WN / WNO) + pc;
+    constexpr int PASSES = 32 / RPP;
+    auto row_of = [&](int i, int v) { return static_cast<int64_t>(wm0 + i * 32 + v * RPP + pr); };
     auto base_of = [&](int i, int v) { return static_cast<uint32_t>(row_of(i, v) * ldy * 2 + col0 * 2); };
     auto rbase_of = [&](int i, int v) {
         return GEN ? static_cast<uint32_t>(row_of(i, v) * ldr * 2 + col0 * 2) : base_of(i, v);
@@ -397,7 +431,7 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
     // only write zeros into buffers whose contents are never used.
 #pragma unroll
     for (int s = 0; s < C::STAGES - 1; ++s)
-        issue_stage<C>(glds + s * C::STAGE_BYTES, ra, rb, a_off, a_k, b_off, b_k, wave, g0 + s, gend);
+        issue_stage<C, GLU>(glds + s * C::STAGE_BYTES, ra, rb, rb2, a_off, a_k, b_off, b_k, wave, g0 + s, gend);
     stage_barrier<VM_KEEP0>();
     static_for<0, PD>([&](auto ksc) {
         constexpr int ks = decltype(ksc)::value;
@@ -407,8 +441,8 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
         });
     });
     if constexpr (!C::LAG)
-        issue_stage<C>(glds + (C::STAGES - 1) * C::STAGE_BYTES, ra, rb, a_off, a_k, b_off, b_k, wave,
-                       g0 + C::STAGES - 1, gend);
+        issue_stage<C, GLU>(glds + (C::STAGES - 1) * C::STAGE_BYTES, ra, rb, rb2, a_off, a_k, b_off, b_k, wave,
+                            g0 + C::STAGES - 1, gend);
 
     int cur_stage = 0;
     for (int it = 0; it < iters; ++it) {
@@ -440,14 +474,14 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
                 if constexpr (C::LAG) {
                     constexpr int u = ks * MF + t;
                     static_for<u * C::LOADS / SLOTS, (u + 1) * C::LOADS / SLOTS>([&](auto q) {
-                        issue_load<C, decltype(q)::value>(dst, ra, rb, a_off, a_k, b_off, b_k, wave, kbase,
-                                                          kbytes, gend);
+                        issue_load<C, decltype(q)::value, GLU>(dst, ra, rb, rb2, a_off, a_k, b_off, b_k, wave,
+                                                               kbase, kbytes, gend);
                     });
                 } else if constexpr (ks >= KS - PD) {
                     constexpr int u = (ks - (KS - PD)) * MF + t;
                     static_for<u * C::LOADS / POST, (u + 1) * C::LOADS / POST>([&](auto q) {
-                        issue_load<C, decltype(q)::value>(dst, ra, rb, a_off, a_k, b_off, b_k, wave, kbase,
-                                                          kbytes, gend);
+                        issue_load<C, decltype(q)::value, GLU>(dst, ra, rb, rb2, a_off, a_k, b_off, b_k, wave,
+                                                               kbase, kbytes, gend);
                     });
                 }
                 __builtin_amdgcn_sched_barrier(0);
@@ -622,17 +656,28 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
     for (int i = 0; i < C::TM; ++i) {
         if (owner && vec && has_r && i + 1 < C::TM) load_r(i + 1, rv[(i + 1) & 1]);
         if (owner) {
+            if constexpr (GLU) {
+                // Block 2j holds the gate sums and block 2j+1 the up sums of
+                // the same 32 outputs, element for element.
 #pragma unroll
-            for (int j = 0; j < C::TN; ++j)
+                for (int j = 0; j < C::TN / 2; ++j)
 #pragma unroll
-                for (int e = 0; e < 16; ++e)
-                    ep[(8 * (e >> 2) + 4 * hi + (e & 3)) * C::EPI_STRIDE + j * 32 + frag_row] = acc[i][j][e];
+                    for (int e = 0; e < 16; ++e)
+                        ep[(8 * (e >> 2) + 4 * hi + (e & 3)) * EPS + j * 32 + frag_row] =
+                            silu_f32(acc[i][2 * j][e]) * acc[i][2 * j + 1][e];
+            } else {
+#pragma unroll
+                for (int j = 0; j < C::TN; ++j)
+#pragma unroll
+                    for (int e = 0; e < 16; ++e)
+                        ep[(8 * (e >> 2) + 4 * hi + (e & 3)) * EPS + j * 32 + frag_row] = acc[i][j][e];
+            }
         }
         __syncthreads();
         if (owner) {
 #pragma unroll
             for (int v = 0; v < PASSES; ++v) {
-                const float *src = ep + (v * C::ROWS_PER_PASS + pr) * C::EPI_STRIDE + pc;
+                const float *src = ep + (v * RPP + pr) * EPS + pc;
                 float y[8];
 #pragma unroll
                 for (int t = 0; t < 8; ++t) y[t] = src[t];
@@ -680,24 +725,32 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
     }
 }
 
+// Split-K arguments of one launch; false when a tail split cannot hand
+// the XCDs equal shares of both kinds of work.
+template <class C>
+bool split_args(int64_t K, int64_t tiles, int split, int64_t full_tiles, const Workspace *ws, SplitK &sk) {
+    sk = SplitK{1, ((K + C::BK - 1) / C::BK) * C::BK, nullptr, nullptr, 0};
+    if (split > 1) {
+        sk.split = split;
+        sk.kslice = (((K + split - 1) / split + C::BK - 1) / C::BK) * C::BK;
+        sk.partials = ws->partials;
+        sk.counters = ws->counters;
+        sk.full_tiles = full_tiles;
+        if (full_tiles > 0 && (full_tiles >= tiles || full_tiles % XCDS != 0 ||
+                               ((tiles - full_tiles) * split) % XCDS != 0))
+            return false;
+    }
+    return true;
+}
+
 template <class C>
 hipError_t launch_cfg(const Problem &p, int group_m, int split, int64_t full_tiles, const Workspace *ws,
                       hipStream_t s) {
     const int64_t tiles_m = (p.M + C::BM - 1) / C::BM;
     const int64_t tiles_n = (p.N + C::BN - 1) / C::BN;
     const int64_t tiles = tiles_m * tiles_n;
-    SplitK sk{1, ((p.K + C::BK - 1) / C::BK) * C::BK, nullptr, nullptr, 0};
-    if (split > 1) {
-        sk.split = split;
-        sk.kslice = (((p.K + split - 1) / split + C::BK - 1) / C::BK) * C::BK;
-        sk.partials = ws->partials;
-        sk.counters = ws->counters;
-        sk.full_tiles = full_tiles;
-        // the tail mapping hands the XCDs equal shares of both kinds of work
-        if (full_tiles > 0 && (full_tiles >= tiles || full_tiles % XCDS != 0 ||
-                               ((tiles - full_tiles) * split) % XCDS != 0))
-            return hipErrorInvalidValue;
-    }
+    SplitK sk;
+    if (!split_args<C>(p.K, tiles, split, full_tiles, ws, sk)) return hipErrorInvalidValue;
     const int64_t wgs = sk.full_tiles + (tiles - sk.full_tiles) * sk.split;
     if (is_general(p))
         hipLaunchKernelGGL((tile_kernel<C, Problem>), dim3(static_cast<unsigned>(wgs)), dim3(C::THREADS), 0, s, p,
@@ -706,6 +759,29 @@ hipError_t launch_cfg(const Problem &p, int group_m, int split, int64_t full_til
         hipLaunchKernelGGL((tile_kernel<C, DenseProblem>), dim3(static_cast<unsigned>(wgs)), dim3(C::THREADS), 0, s,
                            dense_of(p), tiles_m, tiles_n, group_m, sk);
     return hipGetLastError();
+}
+
+// SwiGLU needs an even number of 32-column blocks per wave (gate/up pairs)
+// and an even number of B loads per wave (half gate, half up).
+template <class C>
+constexpr bool glu_ok() { return C::TN % 2 == 0 && C::B_LOADS % 2 == 0 && 32 % C::RPI == 0; }
+
+template <class C>
+hipError_t launch_cfg_glu(const GluProblem &p, int group_m, int split, int64_t full_tiles, const Workspace *ws,
+                          hipStream_t s) {
+    if constexpr (!glu_ok<C>()) {
+        return hipErrorInvalidValue;
+    } else {
+        const int64_t tiles_m = (p.M + C::BM - 1) / C::BM;
+        const int64_t tiles_n = (p.N + C::BN / 2 - 1) / (C::BN / 2);
+        const int64_t tiles = tiles_m * tiles_n;
+        SplitK sk;
+        if (!split_args<C>(p.K, tiles, split, full_tiles, ws, sk)) return hipErrorInvalidValue;
+        const int64_t wgs = sk.full_tiles + (tiles - sk.full_tiles) * sk.split;
+        hipLaunchKernelGGL((tile_kernel<C, GluProblem>), dim3(static_cast<unsigned>(wgs)), dim3(C::THREADS), 0, s,
+                           p, tiles_m, tiles_n, group_m, sk);
+        return hipGetLastError();
+    }
 }
 
 }  // namespace
@@ -738,73 +814,76 @@ using C128x128k64g2 = Cfg<128, 128, 64, 2, 2, 2, 2, 2>;
 using C64x64k64g4 = Cfg<64, 64, 64, 2, 2, 2, 4, 4>;
 using C256x128s3w8L = Cfg<256, 128, 64, 4, 2, 3, 2, 1, 1, true>;
 using C128x128s4L = Cfg<128, 128, 64, 2, 2, 4, 1, 1, 1, true>;
+using C32x256k64s4 = Cfg<32, 256, 64, 1, 4, 4, 1>;
 
-template <class C>
-constexpr TileShape shape_of(int per_cu) { return TileShape{C::BM, C::BN, C::BK, per_cu}; }
+// Workgroups per CU that each configuration's LDS and registers allow, and
+// the dispatch from a TileCfg value to its type: f(C{}, per_cu).
+template <class F>
+auto with_cfg(int cfg, F &&f) -> decltype(f(C256x256w8{}, 1)) {
+    switch (cfg) {
+        case TC_256x256_K64_S2_W8: return f(C256x256w8{}, 1);
+        case TC_256x256_K64_S2_W4: return f(C256x256w4{}, 1);
+        case TC_256x128_K64_S2_W8: return f(C256x128w8{}, 1);
+        case TC_128x256_K64_S2_W8: return f(C128x256w8{}, 1);
+        case TC_256x128_K64_S2_W4: return f(C256x128w4{}, 1);
+        case TC_128x128_K64_S2_W4: return f(C128x128w4{}, 2);
+        case TC_64x256_K64_S2_W4: return f(C64x256w4{}, 2);
+        case TC_128x128_K64_S4_W4: return f(C128x128s4{}, 1);
+        case TC_128x128_K64_S3_W4: return f(C128x128s3{}, 1);
+        case TC_64x256_K64_S3_W4: return f(C64x256s3{}, 1);
+        case TC_256x128_K64_S3_W8: return f(C256x128s3w8{}, 1);
+        case TC_64x64_K64_S2_W4: return f(C64x64w4{}, 4);
+        case TC_64x128_K64_S2_W4: return f(C64x128w4{}, 3);
+        case TC_64x64_K128_S2_W4: return f(C64x64k128{}, 2);
+        case TC_128x128_K128_S2_W4: return f(C128x128k128{}, 1);
+        case TC_64x128_K128_S2_W4: return f(C64x128k128{}, 1);
+        case TC_64x64_K128_S3_W4: return f(C64x64k128s3{}, 1);
+        case TC_64x64_K64_S4_W4: return f(C64x64k64s4{}, 2);
+        case TC_128x128_K32_S4_W4: return f(C128x128k32s4{}, 2);
+        case TC_64x64_K64_S8_W4: return f(C64x64k64s8{}, 1);
+        case TC_64x128_K64_S4_W4: return f(C64x128k64s4{}, 1);
+        case TC_64x64_K128_S2_G2: return f(C64x64k128g2{}, 1);
+        case TC_128x128_K64_S2_G2: return f(C128x128k64g2{}, 1);
+        case TC_64x64_K64_S2_G4: return f(C64x64k64g4{}, 1);
+        case TC_256x128_K64_S3_W8_L: return f(C256x128s3w8L{}, 1);
+        case TC_128x128_K64_S4_W4_L: return f(C128x128s4L{}, 1);
+        case TC_32x256_K64_S4_W4: return f(C32x256k64s4{}, 1);
+        default: return f(nullptr, 0);
+    }
+}
 
 TileShape tile_shape(int cfg) {
-    switch (cfg) {
-        case TC_256x256_K64_S2_W8: return shape_of<C256x256w8>(1);
-        case TC_256x256_K64_S2_W4: return shape_of<C256x256w4>(1);
-        case TC_256x128_K64_S2_W8: return shape_of<C256x128w8>(1);
-        case TC_128x256_K64_S2_W8: return shape_of<C128x256w8>(1);
-        case TC_256x128_K64_S2_W4: return shape_of<C256x128w4>(1);
-        case TC_128x128_K64_S2_W4: return shape_of<C128x128w4>(2);
-        case TC_64x256_K64_S2_W4: return shape_of<C64x256w4>(2);
-        case TC_128x128_K64_S4_W4: return shape_of<C128x128s4>(1);
-        case TC_128x128_K64_S3_W4: return shape_of<C128x128s3>(1);
-        case TC_64x256_K64_S3_W4: return shape_of<C64x256s3>(1);
-        case TC_256x128_K64_S3_W8: return shape_of<C256x128s3w8>(1);
-        case TC_64x64_K64_S2_W4: return shape_of<C64x64w4>(4);
-        case TC_64x128_K64_S2_W4: return shape_of<C64x128w4>(3);
-        case TC_64x64_K128_S2_W4: return shape_of<C64x64k128>(2);
-        case TC_128x128_K128_S2_W4: return shape_of<C128x128k128>(1);
-        case TC_64x128_K128_S2_W4: return shape_of<C64x128k128>(1);
-        case TC_64x64_K128_S3_W4: return shape_of<C64x64k128s3>(1);
-        case TC_64x64_K64_S4_W4: return shape_of<C64x64k64s4>(2);
-        case TC_128x128_K32_S4_W4: return shape_of<C128x128k32s4>(2);
-        case TC_64x64_K64_S8_W4: return shape_of<C64x64k64s8>(1);
-        case TC_64x128_K64_S4_W4: return shape_of<C64x128k64s4>(1);
-        case TC_64x64_K128_S2_G2: return shape_of<C64x64k128g2>(1);
-        case TC_128x128_K64_S2_G2: return shape_of<C128x128k64g2>(1);
-        case TC_64x64_K64_S2_G4: return shape_of<C64x64k64g4>(1);
-        case TC_256x128_K64_S3_W8_L: return shape_of<C256x128s3w8L>(1);
-        case TC_128x128_K64_S4_W4_L: return shape_of<C128x128s4L>(1);
-        default: return TileShape{0, 0, 0, 0};
-    }
+    return with_cfg(cfg, [](auto c, int per_cu) {
+        using C = decltype(c);
+        if constexpr (std::is_same<C, std::nullptr_t>::value) return TileShape{0, 0, 0, 0};
+        else return TileShape{C::BM, C::BN, C::BK, per_cu};
+    });
+}
+
+bool tile_glu_ok(int cfg) {
+    return with_cfg(cfg, [](auto c, int) {
+        using C = decltype(c);
+        if constexpr (std::is_same<C, std::nullptr_t>::value) return false;
+        else return glu_ok<C>();
+    });
 }
 
 hipError_t launch_tile(int cfg, const Problem &p, int split, int64_t full_tiles, const Workspace *ws,
                        hipStream_t s) {
-    switch (cfg) {
-        case TC_256x256_K64_S2_W8: return launch_cfg<C256x256w8>(p, 8, split, full_tiles, ws, s);
-        case TC_256x256_K64_S2_W4: return launch_cfg<C256x256w4>(p, 8, split, full_tiles, ws, s);
-        case TC_256x128_K64_S2_W8: return launch_cfg<C256x128w8>(p, 8, split, full_tiles, ws, s);
-        case TC_128x256_K64_S2_W8: return launch_cfg<C128x256w8>(p, 8, split, full_tiles, ws, s);
-        case TC_256x128_K64_S2_W4: return launch_cfg<C256x128w4>(p, 8, split, full_tiles, ws, s);
-        case TC_128x128_K64_S2_W4: return launch_cfg<C128x128w4>(p, 8, split, full_tiles, ws, s);
-        case TC_64x256_K64_S2_W4: return launch_cfg<C64x256w4>(p, 8, split, full_tiles, ws, s);
-        case TC_128x128_K64_S4_W4: return launch_cfg<C128x128s4>(p, 8, split, full_tiles, ws, s);
-        case TC_128x128_K64_S3_W4: return launch_cfg<C128x128s3>(p, 8, split, full_tiles, ws, s);
-        case TC_64x256_K64_S3_W4: return launch_cfg<C64x256s3>(p, 8, split, full_tiles, ws, s);
-        case TC_256x128_K64_S3_W8: return launch_cfg<C256x128s3w8>(p, 8, split, full_tiles, ws, s);
-        case TC_64x64_K64_S2_W4: return launch_cfg<C64x64w4>(p, 8, split, full_tiles, ws, s);
-        case TC_64x128_K64_S2_W4: return launch_cfg<C64x128w4>(p, 8, split, full_tiles, ws, s);
-        case TC_64x64_K128_S2_W4: return launch_cfg<C64x64k128>(p, 8, split, full_tiles, ws, s);
-        case TC_128x128_K128_S2_W4: return launch_cfg<C128x128k128>(p, 8, split, full_tiles, ws, s);
-        case TC_64x128_K128_S2_W4: return launch_cfg<C64x128k128>(p, 8, split, full_tiles, ws, s);
-        case TC_64x64_K128_S3_W4: return launch_cfg<C64x64k128s3>(p, 8, split, full_tiles, ws, s);
-        case TC_64x64_K64_S4_W4: return launch_cfg<C64x64k64s4>(p, 8, split, full_tiles, ws, s);
-        case TC_128x128_K32_S4_W4: return launch_cfg<C128x128k32s4>(p, 8, split, full_tiles, ws, s);
-        case TC_64x64_K64_S8_W4: return launch_cfg<C64x64k64s8>(p, 8, split, full_tiles, ws, s);
-        case TC_64x128_K64_S4_W4: return launch_cfg<C64x128k64s4>(p, 8, split, full_tiles, ws, s);
-        case TC_64x64_K128_S2_G2: return launch_cfg<C64x64k128g2>(p, 8, split, full_tiles, ws, s);
-        case TC_128x128_K64_S2_G2: return launch_cfg<C128x128k64g2>(p, 8, split, full_tiles, ws, s);
-        case TC_64x64_K64_S2_G4: return launch_cfg<C64x64k64g4>(p, 8, split, full_tiles, ws, s);
-        case TC_256x128_K64_S3_W8_L: return launch_cfg<C256x128s3w8L>(p, 8, split, full_tiles, ws, s);
-        case TC_128x128_K64_S4_W4_L: return launch_cfg<C128x128s4L>(p, 8, split, full_tiles, ws, s);
-        default: return hipErrorInvalidValue;
-    }
+    return with_cfg(cfg, [&](auto c, int) {
+        using C = decltype(c);
+        if constexpr (std::is_same<C, std::nullptr_t>::value) return hipErrorInvalidValue;
+        else return launch_cfg<C>(p, 8, split, full_tiles, ws, s);
+    });
+}
+
+hipError_t launch_tile_glu(int cfg, const GluProblem &p, int split, int64_t full_tiles, const Workspace *ws,
+                           hipStream_t s) {
+    return with_cfg(cfg, [&](auto c, int) {
+        using C = decltype(c);
+        if constexpr (std::is_same<C, std::nullptr_t>::value) return hipErrorInvalidValue;
+        else return launch_cfg_glu<C>(p, 8, split, full_tiles, ws, s);
+    });
 }
 
 }  // namespace kernelarc

@@ -46,6 +46,10 @@ _SIGS = {
                                                         _P, _I64, ctypes.c_float, _P, _I64, _P, _P, _I64, _P]),
     "kernelarc_select_plan_ex": (ctypes.c_int, [_I64, _I64, _I64, ctypes.c_int, _I64, _I64, _I64, _I64,
                                                 ctypes.c_float, ctypes.c_float, ctypes.c_int]),
+    "kernelarc_swiglu_bf16": (ctypes.c_int, [_I64, _I64, _I64, _P, _P, _P, _P, _P]),
+    "kernelarc_swiglu_bf16_with_plan": (ctypes.c_int, [ctypes.c_int, _I64, _I64, _I64, _P, _P, _P, _P, _P]),
+    "kernelarc_select_plan_swiglu": (ctypes.c_int, [_I64, _I64, _I64]),
+    "kernelarc_plan_supports_swiglu": (ctypes.c_int, [ctypes.c_int, _I64, _I64, _I64]),
     "kernelarc_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "kernelarc_last_error": (ctypes.c_char_p, []),
 }
@@ -211,3 +215,33 @@ def select_plan_ex(M, N, K, has_c, ldx, ldw, ldc, ldy, alpha, beta, has_bias) ->
     """The plan the general form would run for these strides and scalars."""
     return _lib.kernelarc_select_plan_ex(M, N, K, int(has_c), ldx, ldw, ldc, ldy, float(alpha), float(beta),
                                          int(has_bias))
+
+
+def swiglu_bf16(x, wg, wu, out=None, stream=None, plan=None):
+    """H = silu(X Wg^T) * (X Wu^T) (the gated MLP input projection).
+
+    x is [..., K] (leading dimensions flattened into M), wg and wu are
+    [N, K]; the result is [..., N].  All contiguous bfloat16 GPU tensors.
+    """
+    if wu.dim() != 2 or tuple(wu.shape) != tuple(wg.shape):
+        raise ValueError("wg and wu must both be [N, K]")
+    M, N, K, out = _operands(x, wg, None, out)
+    for name, t in (("wu", wu),):
+        if t.dtype != torch.bfloat16 or not t.is_cuda or not t.is_contiguous() or t.device != x.device:
+            raise ValueError(f"{name} must be a contiguous bfloat16 tensor on {x.device}")
+    args = (M, N, K, x.data_ptr(), wg.data_ptr(), wu.data_ptr(), out.data_ptr(), _stream_handle(stream))
+    with torch.cuda.device(x.device):
+        if plan is None:
+            st = _lib.kernelarc_swiglu_bf16(*args)
+        else:
+            st = _lib.kernelarc_swiglu_bf16_with_plan(plan, *args)
+    _check(st, "kernelarc_swiglu_bf16" if plan is None else f"kernelarc_swiglu_bf16_with_plan({plan_name(plan)})")
+    return out
+
+
+def select_plan_swiglu(M: int, N: int, K: int) -> int:
+    return _lib.kernelarc_select_plan_swiglu(M, N, K)
+
+
+def plan_supports_swiglu(plan: int, M: int, N: int, K: int) -> bool:
+    return _lib.kernelarc_plan_supports_swiglu(plan, M, N, K) == 1

@@ -138,6 +138,53 @@ def make_general_inputs(w: GeneralWorkload) -> dict:
     return {"X": X, "W": W, "C": C if w.has_c else None, "bias": b if w.has_bias else None}
 
 
+# ---- SwiGLU: H = silu(X Wg^T) * (X Wu^T) -----------------------------------
+
+@dataclass(frozen=True)
+class GluWorkload:
+    """A SwiGLU call: X [M,K] (K = hidden size), Wg and Wu [N,K] (N =
+    intermediate size), H [M,N]."""
+    name: str
+    M: int
+    N: int
+    K: int
+    seed: int
+
+    @property
+    def flops(self) -> int:
+        """Both projections; the SiLU-multiply adds a few operations per output."""
+        return 4 * self.M * self.N * self.K
+
+    @property
+    def algorithmic_bytes(self) -> int:
+        """X, Wg and Wu read once, H written once, 2 bytes per element."""
+        return 2 * (self.M * self.K + 2 * self.N * self.K + self.M * self.N)
+
+
+# The decoder layer's gate/up projections at Llama-class sizes (hidden 4096,
+# intermediate 14336; hidden 5120, intermediate 13824): a decode step, a
+# prefill chunk below the paper's INT8 threshold of M = 1000 tokens (the
+# BF16 path), and a full prefill.
+GLU = (
+    GluWorkload("swiglu_decode_m16_h4096_i14336", 16, 14336, 4096, 201),
+    GluWorkload("swiglu_m512_h5120_i13824", 512, 13824, 5120, 202),
+    GluWorkload("swiglu_prefill_m4096_h4096_i14336", 4096, 14336, 4096, 203),
+)
+GLU_BY_NAME = {w.name: w for w in GLU}
+
+
+def make_glu_inputs(w: GluWorkload) -> dict:
+    """Draw X ~ N(0,1) (normalised hidden states), then Wg and Wu ~ N(0,1)/sqrt(K),
+    as bf16 CPU tensors from one seed, so that the gate and up sums are about
+    N(0,1) and the gate spans SiLU's curved range."""
+    g = torch.Generator().manual_seed(w.seed)
+    scale = 1.0 / math.sqrt(w.K) if w.K > 0 else 1.0
+    X = torch.randn((w.M, w.K), generator=g).to(torch.bfloat16)
+    Wg = (torch.randn((w.N, w.K), generator=g) * scale).to(torch.bfloat16)
+    Wu = (torch.randn((w.N, w.K), generator=g) * scale).to(torch.bfloat16)
+    return {"X": X, "Wg": Wg, "Wu": Wu}
+
+
 def custom(M: int, N: int, K: int, residual: bool = True, dist: str = "normal",
            seed: int = 0, name: str | None = None) -> Workload:
     return Workload(name or f"custom_m{M}_n{N}_k{K}", M, N, K, residual, dist, seed)

@@ -162,3 +162,41 @@ def test_general_form_plan_selection(ka):
     assert dense.startswith("stream") and general.startswith("tile")
     assert names[ka.select_plan_ex(2, 4096, 4096, 1, 4104, 4096, 4096, 4096, 1.0, 1.0, 1)] == "gemv_valu_w4"
     assert names[ka.select_plan_ex(4096, 4096, 14336, 1, 14336, 14336, 4096, 4096, 1.0, 1.0, 1)].startswith("tile")
+
+
+def test_swiglu_validation(ka):
+    f = ka.kernelarc_swiglu_bf16
+    buf = (ctypes.c_uint16 * 8192)()
+    base = ctypes.addressof(buf)
+    X, G, U, H = base, base + 2048, base + 4096, base + 8192
+    # (M, N, K, X, Wg, Wu, H, stream)
+    assert f(-1, 4, 8, X, G, U, H, None) == ka.ERR_INVALID_ARG
+    assert f(0, 4, 8, None, None, None, None, None) == ka.OK
+    assert f(4, 4, 8, X, G, U, None, None) == ka.ERR_INVALID_ARG            # H NULL
+    assert f(4, 4, 8, X, G, None, H, None) == ka.ERR_INVALID_ARG            # Wu NULL
+    assert f(4, 4, 8, X, G, U, U + 16, None) == ka.ERR_INVALID_ARG          # H overlaps Wu
+    assert ka.kernelarc_last_error().startswith(b"H overlaps")
+    assert f(4, 4, 8, X, G, U, X, None) == ka.ERR_INVALID_ARG               # H overlaps X
+    assert f(4, 1 << 30, 8, X, G, U, H, None) == ka.ERR_INVALID_ARG         # N too large
+    assert f(4, 4, 8, X, G, G, H, None) != ka.ERR_INVALID_ARG               # Wg == Wu is allowed
+    assert ka.kernelarc_swiglu_bf16_with_plan(-1, 4, 4, 8, X, G, U, H, None) == ka.ERR_UNSUPPORTED
+
+
+def test_swiglu_plans(ka):
+    names = ka.plan_names()
+    gen = names.index("generic_64x64_scalar")
+    assert ka.select_plan_swiglu(64, 100, 250) == gen                        # K % 8
+    assert ka.select_plan_swiglu(-1, 4, 8) == -1
+    for (M, N, K) in [(1, 14336, 4096), (16, 14336, 4096), (64, 4096, 4096), (512, 13824, 5120),
+                      (4096, 14336, 4096), (300, 77, 1000), (7, 9, 24), (0, 5, 8)]:
+        p = ka.select_plan_swiglu(M, N, K)
+        assert ka.plan_supports_swiglu(p, M, N, K), (M, N, K, names[p])
+        assert names[p].startswith("tile") or p == gen
+    # plans whose waves cannot hold gate/up block pairs, or that are not tiles
+    for n in ("tile_64x64_k64_w4", "tile_64x64_k128s3_w4_splitk", "stream_mfma16_k64_splitk", "gemv_valu_w4",
+              "skinny_mfma16_w8"):
+        assert not ka.plan_supports_swiglu(names.index(n), 64, 1024, 1024), n
+    for n in ("tile_256x256_k64_w8", "tile_128x128_k64_w4", "tile_32x256_k64s4_w4_splitk", "generic_64x64_scalar"):
+        assert ka.plan_supports_swiglu(names.index(n), 64, 1024, 1024), n
+    assert not ka.plan_supports_swiglu(names.index("tile_256x256_k64_w8"), 64, 1024, 1020)   # K % 8
+    assert ka.kernelarc_plan_supports_swiglu(999, 1, 1, 1) == -1
