@@ -1,6 +1,7 @@
 """CPU oracle for Y = X.W^T + R, its general form
-D = alpha.X.W^T + beta.C + bias, and the gated MLP input projection
-H = silu(X.Wg^T) * (X.Wu^T) (TEST INFRASTRUCTURE ONLY).
+D = alpha.X.W^T + beta.C + bias, the gated MLP input projection
+H = silu(X.Wg^T) * (X.Wu^T), and their INT8 forms with per-row and
+per-column dequantisation scales (TEST INFRASTRUCTURE ONLY).
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
 ``bench.py`` may import this package.  The GPU library never imports, links
@@ -64,6 +65,16 @@ class Oracle:
         lib.ka_oracle_swiglu.restype = ctypes.c_int
         lib.ka_oracle_swiglu_at.argtypes = [_I64, _I64, _I64, _P, _P, _P, _I64, _P, _P, _P]
         lib.ka_oracle_swiglu_at.restype = ctypes.c_int
+        lib.ka_oracle_i8_dot.argtypes = [_I64, _I64, _I64, _P, _P, _P]
+        lib.ka_oracle_i8_dot.restype = ctypes.c_int
+        lib.ka_oracle_i8_linear.argtypes = [_I64, _I64, _I64, _P, _P, _P, _P, _P, _P]
+        lib.ka_oracle_i8_linear.restype = ctypes.c_int
+        lib.ka_oracle_i8_linear_at.argtypes = [_I64, _I64, _I64, _P, _P, _P, _P, _P, _I64, _P, _P, _P]
+        lib.ka_oracle_i8_linear_at.restype = ctypes.c_int
+        lib.ka_oracle_i8_swiglu.argtypes = [_I64, _I64, _I64, _P, _P, _P, _P, _P, _P, _P]
+        lib.ka_oracle_i8_swiglu.restype = ctypes.c_int
+        lib.ka_oracle_i8_swiglu_at.argtypes = [_I64, _I64, _I64, _P, _P, _P, _P, _P, _P, _I64, _P, _P, _P]
+        lib.ka_oracle_i8_swiglu_at.restype = ctypes.c_int
         lib.ka_oracle_round_bf16.argtypes = [_I64, _P, _P]
         lib.ka_oracle_round_bf16.restype = None
         lib.ka_oracle_threads.argtypes = []
@@ -210,6 +221,100 @@ class Oracle:
                                           out.ctypes.data)
         if rc != 0:
             raise ValueError("oracle rejected its arguments")
+        return out
+
+    # ---- INT8 with dequantisation scales ------------------------------------
+    @staticmethod
+    def _i8(a, shape, what):
+        a = np.ascontiguousarray(a)
+        if a.dtype != np.int8:
+            raise TypeError(f"{what}: expected int8")
+        if a.shape != shape:
+            raise ValueError(f"{what}: expected shape {shape}, got {a.shape}")
+        return a
+
+    @staticmethod
+    def _f32(a, n, what):
+        a = np.ascontiguousarray(a)
+        if a.dtype != np.float32 or a.shape != (n,):
+            raise ValueError(f"{what}: expected float32 of shape ({n},)")
+        return a
+
+    @staticmethod
+    def _positions(rows, cols):
+        rows = np.ascontiguousarray(rows, dtype=np.int64)
+        cols = np.ascontiguousarray(cols, dtype=np.int64)
+        if rows.shape != cols.shape or rows.ndim != 1:
+            raise ValueError("rows and cols must be 1-D and of equal length")
+        return rows, cols
+
+    def i8_dot(self, qX, qW) -> np.ndarray:
+        """A = qX qW^T as exact int64 sums."""
+        M, K = qX.shape
+        N = qW.shape[0]
+        qX, qW = self._i8(qX, (M, K), "qX"), self._i8(qW, (N, K), "qW")
+        A = np.empty((M, N), dtype=np.int64)
+        if self.lib.ka_oracle_i8_dot(M, N, K, qX.ctypes.data, qW.ctypes.data, A.ctypes.data) != 0:
+            raise ValueError("oracle rejected its arguments")
+        return A
+
+    def _i8_args(self, qX, sx, qW, sw, R):
+        M, K = qX.shape
+        N = qW.shape[0]
+        qX, qW = self._i8(qX, (M, K), "qX"), self._i8(qW, (N, K), "qW")
+        sx, sw = self._f32(sx, M, "sx"), self._f32(sw, N, "sw")
+        Rp = None
+        if R is not None:
+            R = self._bits(R, (M, N))
+            Rp = R.ctypes.data
+        return (M, N, K, qX.ctypes.data, sx.ctypes.data, qW.ctypes.data, sw.ctypes.data, Rp), (qX, sx, qW, sw, R)
+
+    def i8_linear(self, qX, sx, qW, sw, R=None) -> np.ndarray:
+        """Y = sx[i] sw[j] (qX qW^T)[i,j] (+ R) in float64."""
+        args, keep = self._i8_args(qX, sx, qW, sw, R)
+        Y = np.empty((args[0], args[1]), dtype=np.float64)
+        if self.lib.ka_oracle_i8_linear(*args, Y.ctypes.data) != 0:
+            raise ValueError("oracle rejected its arguments")
+        del keep
+        return Y
+
+    def i8_linear_at(self, qX, sx, qW, sw, R, rows, cols) -> np.ndarray:
+        args, keep = self._i8_args(qX, sx, qW, sw, R)
+        rows, cols = self._positions(rows, cols)
+        out = np.empty(rows.shape[0], dtype=np.float64)
+        if self.lib.ka_oracle_i8_linear_at(*args, rows.shape[0], rows.ctypes.data, cols.ctypes.data,
+                                           out.ctypes.data) != 0:
+            raise ValueError("oracle rejected its arguments")
+        del keep
+        return out
+
+    def _i8_glu_args(self, qX, sx, qWg, swg, qWu, swu):
+        M, K = qX.shape
+        N = qWg.shape[0]
+        qX = self._i8(qX, (M, K), "qX")
+        qWg, qWu = self._i8(qWg, (N, K), "qWg"), self._i8(qWu, (N, K), "qWu")
+        sx = self._f32(sx, M, "sx")
+        swg, swu = self._f32(swg, N, "swg"), self._f32(swu, N, "swu")
+        keep = (qX, sx, qWg, swg, qWu, swu)
+        return (M, N, K) + tuple(a.ctypes.data for a in keep), keep
+
+    def i8_swiglu(self, qX, sx, qWg, swg, qWu, swu) -> np.ndarray:
+        """H = silu(sx swg (qX qWg^T)) * (sx swu (qX qWu^T)) in float64."""
+        args, keep = self._i8_glu_args(qX, sx, qWg, swg, qWu, swu)
+        H = np.empty((args[0], args[1]), dtype=np.float64)
+        if self.lib.ka_oracle_i8_swiglu(*args, H.ctypes.data) != 0:
+            raise ValueError("oracle rejected its arguments")
+        del keep
+        return H
+
+    def i8_swiglu_at(self, qX, sx, qWg, swg, qWu, swu, rows, cols) -> np.ndarray:
+        args, keep = self._i8_glu_args(qX, sx, qWg, swg, qWu, swu)
+        rows, cols = self._positions(rows, cols)
+        out = np.empty(rows.shape[0], dtype=np.float64)
+        if self.lib.ka_oracle_i8_swiglu_at(*args, rows.shape[0], rows.ctypes.data, cols.ctypes.data,
+                                           out.ctypes.data) != 0:
+            raise ValueError("oracle rejected its arguments")
+        del keep
         return out
 
     def threads(self) -> int:

@@ -3,8 +3,10 @@
  *
  *     Y[i,j] = sum_k X[i,k] * W[j,k]  +  R[i,j]          (R optional)
  *
- * its general form (alpha, beta, bias, leading dimensions) and the gated
- * MLP input projection H = silu(X Wg^T) * (X Wu^T) (SwiGLU).
+ * its general form (alpha, beta, bias, leading dimensions), the gated
+ * MLP input projection H = silu(X Wg^T) * (X Wu^T) (SwiGLU), and INT8
+ * versions of the linear layer and of SwiGLU with per-row and per-column
+ * dequantisation scales.
  *
  * TEST INFRASTRUCTURE ONLY.  This file is the slow, obviously correct
  * reference that the GPU library is checked against.  Only the test suite,
@@ -268,6 +270,124 @@ int ka_oracle_swiglu_at(int64_t M, int64_t N, int64_t K, const uint16_t *X,
 #pragma omp parallel for schedule(dynamic, 16)
     for (int64_t t = 0; t < n; ++t)
         out[t] = element_swiglu(rows[t], cols[t], K, X, Wg, Wu);
+    return 0;
+}
+
+/*
+ * INT8 linear layer with a dequantisation epilogue, and the INT8 SwiGLU
+ * gate/up projection (decoder-layer case study, Alg. 7: its INT8 path
+ * quantises the normalised activations and the gate/up weights and computes
+ * the gate/up GEMM with a fused dequantisation and SwiGLU epilogue, or an
+ * integer GEMM followed by a separate dequantisation/SwiGLU step).  The
+ * paper does not give the quantisation granularity; the reading here is the
+ * symmetric W8A8 scheme: one scale per activation row (token) and one per
+ * weight row (output channel), no zero points:
+ *
+ *     A[i,j] = sum_k qX[i,k] qW[j,k]                   (exact integer)
+ *     Y[i,j] = sx[i] sw[j] A[i,j]  (+ R[i,j])
+ *     H[i,j] = silu(sx[i] swg[j] Ag[i,j]) * (sx[i] swu[j] Au[i,j])
+ *
+ * qX is [M,K], qW, qWg, qWu are [N,K] int8; sx [M] and sw, swg, swu [N] are
+ * binary32 scales; R is an optional bf16 [M,N] residual.  The integer sums
+ * are exact (int64); the dequantised value is formed in double as
+ * (sx * sw) * A (the scale product is exact in double), then + R; silu as
+ * above.  Results are doubles, not rounded.
+ */
+static int64_t dot_i8(const int8_t *x, const int8_t *w, int64_t K)
+{
+    int64_t acc = 0;
+    for (int64_t k = 0; k < K; ++k)
+        acc += (int64_t)x[k] * (int64_t)w[k];
+    return acc;
+}
+
+static double element_i8(int64_t i, int64_t j, int64_t N, int64_t K, const int8_t *qX,
+                         const float *sx, const int8_t *qW, const float *sw, const uint16_t *R)
+{
+    double y = (double)sx[i] * (double)sw[j] * (double)dot_i8(qX + i * K, qW + j * K, K);
+    if (R)
+        y += bf16_bits_to_double(R[i * N + j]);
+    return y;
+}
+
+static double element_i8_swiglu(int64_t i, int64_t j, int64_t K, const int8_t *qX, const float *sx,
+                                const int8_t *qWg, const float *swg, const int8_t *qWu, const float *swu)
+{
+    double g = (double)sx[i] * (double)swg[j] * (double)dot_i8(qX + i * K, qWg + j * K, K);
+    double u = (double)sx[i] * (double)swu[j] * (double)dot_i8(qX + i * K, qWu + j * K, K);
+    return silu(g) * u;
+}
+
+static int check_i8(int64_t M, int64_t N, int64_t K, const void *qX, const float *sx,
+                    const void *qW, const float *sw)
+{
+    if (M < 0 || N < 0 || K < 0) return -1;
+    if (M > 0 && (!sx || (K > 0 && !qX))) return -1;
+    if (N > 0 && (!sw || (K > 0 && !qW))) return -1;
+    return 0;
+}
+
+/* The exact integer sums A = qX qW^T (int64), for the integer checks. */
+int ka_oracle_i8_dot(int64_t M, int64_t N, int64_t K, const int8_t *qX, const int8_t *qW, int64_t *A)
+{
+    if (M < 0 || N < 0 || K < 0) return -1;
+    if (M * N > 0 && (!A || (K > 0 && (!qX || !qW)))) return -1;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t i = 0; i < M; ++i)
+        for (int64_t j = 0; j < N; ++j)
+            A[i * N + j] = dot_i8(qX + i * K, qW + j * K, K);
+    return 0;
+}
+
+int ka_oracle_i8_linear(int64_t M, int64_t N, int64_t K, const int8_t *qX, const float *sx,
+                        const int8_t *qW, const float *sw, const uint16_t *R, double *Y)
+{
+    if (check_i8(M, N, K, qX, sx, qW, sw) != 0) return -1;
+    if (M * N > 0 && !Y) return -1;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t i = 0; i < M; ++i)
+        for (int64_t j = 0; j < N; ++j)
+            Y[i * N + j] = element_i8(i, j, N, K, qX, sx, qW, sw, R);
+    return 0;
+}
+
+int ka_oracle_i8_linear_at(int64_t M, int64_t N, int64_t K, const int8_t *qX, const float *sx,
+                           const int8_t *qW, const float *sw, const uint16_t *R, int64_t n,
+                           const int64_t *rows, const int64_t *cols, double *out)
+{
+    if (check_i8(M, N, K, qX, sx, qW, sw) != 0 || n < 0) return -1;
+    for (int64_t t = 0; t < n; ++t)
+        if (rows[t] < 0 || rows[t] >= M || cols[t] < 0 || cols[t] >= N) return -1;
+#pragma omp parallel for schedule(dynamic, 16)
+    for (int64_t t = 0; t < n; ++t)
+        out[t] = element_i8(rows[t], cols[t], N, K, qX, sx, qW, sw, R);
+    return 0;
+}
+
+int ka_oracle_i8_swiglu(int64_t M, int64_t N, int64_t K, const int8_t *qX, const float *sx,
+                        const int8_t *qWg, const float *swg, const int8_t *qWu, const float *swu,
+                        double *H)
+{
+    if (check_i8(M, N, K, qX, sx, qWg, swg) != 0 || check_i8(M, N, K, qX, sx, qWu, swu) != 0) return -1;
+    if (M * N > 0 && !H) return -1;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t i = 0; i < M; ++i)
+        for (int64_t j = 0; j < N; ++j)
+            H[i * N + j] = element_i8_swiglu(i, j, K, qX, sx, qWg, swg, qWu, swu);
+    return 0;
+}
+
+int ka_oracle_i8_swiglu_at(int64_t M, int64_t N, int64_t K, const int8_t *qX, const float *sx,
+                           const int8_t *qWg, const float *swg, const int8_t *qWu, const float *swu,
+                           int64_t n, const int64_t *rows, const int64_t *cols, double *out)
+{
+    if (check_i8(M, N, K, qX, sx, qWg, swg) != 0 || check_i8(M, N, K, qX, sx, qWu, swu) != 0 || n < 0)
+        return -1;
+    for (int64_t t = 0; t < n; ++t)
+        if (rows[t] < 0 || rows[t] >= M || cols[t] < 0 || cols[t] >= N) return -1;
+#pragma omp parallel for schedule(dynamic, 16)
+    for (int64_t t = 0; t < n; ++t)
+        out[t] = element_i8_swiglu(rows[t], cols[t], K, qX, sx, qWg, swg, qWu, swu);
     return 0;
 }
 

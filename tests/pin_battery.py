@@ -31,6 +31,13 @@ part silu(z) - silu(-z) = z and the even part silu(z) + silu(-z) =
 z tanh(z/2), by the saturated tails (z >= 40: silu(z) = z in double;
 z <= -800: 0), by zero operands, and by row and column permutations.
 
+The INT8 forms (``I8_PINS``: Y = sx[i] sw[j] sum_k qX qW (+ R) and
+H = silu(sx swg Ag) (sx swu Au)) are pinned by exact Python-integer sums
+(including the -128 x -128 extremes), exact rational dequantisation with
+random binary32 scales, reduction to the bf16 oracles (already pinned) when
+power-of-two scales make every dequantised operand an exact bf16 value, a
+zero weight, and the 60-digit decimal SiLU.
+
 ``ALL_PINS`` is run against the real oracle (all must pass) and against
 copies of the oracle with a planted mistake (at least one must fail).
 """
@@ -529,6 +536,147 @@ GLU_PINS = [
     pin_glu_at_matches_full,
 ]
 
+# ------------------------------------------------------------------- INT8 ----
+def _rand_i8(rng, shape, sigma=40.0):
+    """int8 values from a rounded normal, clipped to [-128, 127]."""
+    return np.clip(np.rint(rng.standard_normal(shape) * sigma), -128, 127).astype(np.int8)
+
+
+def _rand_scales(rng, n, lo=-12, hi=-4):
+    """Positive binary32 scales with random mantissas over a range of binades."""
+    return (2.0 ** rng.uniform(lo, hi, size=n)).astype(np.float32)
+
+
+def _pow2_scales(rng, n, lo=-10, hi=-3):
+    return (2.0 ** rng.integers(lo, hi, size=n)).astype(np.float32)
+
+
+def _bf16_from_f64(values):
+    """bf16 bit patterns of float64 values that are exactly representable."""
+    t = torch.from_numpy(np.asarray(values, dtype=np.float64))
+    out = wl.bits(t.to(torch.float32).to(torch.bfloat16)).copy()
+    assert (bf16_bits_to_f64(out) == np.asarray(values)).all(), "value is not an exact bf16"
+    return out
+
+
+def pin_i8_exact_integer_sums(orc, trials=20, seed=31):
+    """The integer sums equal Python's exact integer arithmetic, extremes included."""
+    rng = np.random.default_rng(seed)
+    for t in range(trials):
+        M, N, K = (int(v) for v in rng.integers(1, 11, size=3))
+        qX = _rand_i8(rng, (M, K), 90.0)
+        qW = _rand_i8(rng, (N, K), 90.0)
+        A = orc.i8_dot(qX, qW)
+        for i in range(M):
+            for j in range(N):
+                assert A[i, j] == sum(int(qX[i, k]) * int(qW[j, k]) for k in range(K))
+    K = 4099
+    lo = np.full((2, K), -128, np.int8)
+    assert (orc.i8_dot(lo, lo) == K * 16384).all()
+    hi = np.full((1, K), 127, np.int8)
+    assert (orc.i8_dot(hi, lo[:1]) == -K * 127 * 128).all()
+
+
+def pin_i8_dequant_exact(orc, trials=20, seed=32):
+    """Random binary32 scales: Y within 2^-52 |Y| of the exact rational
+    sx sw A (+ R)."""
+    rng = np.random.default_rng(seed)
+    for _ in range(trials):
+        M, N, K = (int(v) for v in rng.integers(1, 9, size=3))
+        qX, qW = _rand_i8(rng, (M, K)), _rand_i8(rng, (N, K))
+        sx, sw = _rand_scales(rng, M), _rand_scales(rng, N)
+        R = _rand_bits(rng, (M, N)) if rng.random() < 0.5 else None
+        Y = orc.i8_linear(qX, sx, qW, sw, R)
+        rf = bf16_bits_to_f64(R) if R is not None else None
+        for i in range(M):
+            for j in range(N):
+                a = sum(int(qX[i, k]) * int(qW[j, k]) for k in range(K))
+                exact = Fraction(float(sx[i])) * Fraction(float(sw[j])) * a
+                mag = abs(exact)
+                if rf is not None:
+                    exact += Fraction(rf[i, j])
+                    mag += abs(Fraction(rf[i, j]))
+                assert abs(Fraction(Y[i, j]) - exact) <= mag / 2**51 + Fraction(1, 2**1074), (i, j)
+
+
+def pin_i8_matches_bf16_oracle(orc, seed=33):
+    """Power-of-two scales: sx*qX and sw*qW are exact bf16 values, and the INT8
+    oracle equals the (pinned) bf16 oracle on those operands, bit for bit."""
+    rng = np.random.default_rng(seed)
+    M, N, K = 13, 17, 96
+    qX, qW = _rand_i8(rng, (M, K), 60.0), _rand_i8(rng, (N, K), 60.0)
+    sx, sw = _pow2_scales(rng, M), _pow2_scales(rng, N)
+    R = _rand_bits(rng, (M, N))
+    Xb = _bf16_from_f64(qX.astype(np.float64) * sx[:, None])
+    Wb = _bf16_from_f64(qW.astype(np.float64) * sw[:, None])
+    np.testing.assert_array_equal(orc.i8_linear(qX, sx, qW, sw, R), orc.linear(Xb, Wb, R))
+    np.testing.assert_array_equal(orc.i8_linear(qX, sx, qW, sw), orc.linear(Xb, Wb))
+    qWu = _rand_i8(rng, (N, K), 60.0)
+    swu = _pow2_scales(rng, N)
+    Wub = _bf16_from_f64(qWu.astype(np.float64) * swu[:, None])
+    np.testing.assert_array_equal(orc.i8_swiglu(qX, sx, qW, sw, qWu, swu), orc.swiglu(Xb, Wb, Wub))
+
+
+def pin_i8_zero_weight(orc, seed=34):
+    rng = np.random.default_rng(seed)
+    M, N, K = 5, 6, 40
+    qX = _rand_i8(rng, (M, K))
+    sx, sw = _rand_scales(rng, M), _rand_scales(rng, N)
+    R = _rand_bits(rng, (M, N))
+    z = np.zeros((N, K), np.int8)
+    np.testing.assert_array_equal(orc.i8_linear(qX, sx, z, sw, R), bf16_bits_to_f64(R))
+    assert (orc.i8_swiglu(qX, sx, z, sw, _rand_i8(rng, (N, K)), sw) == 0).all()
+    assert (orc.i8_swiglu(qX, sx, _rand_i8(rng, (N, K)), sw, z, sw) == 0).all()
+
+
+def pin_i8_swiglu_decimal(orc, trials=12, seed=35):
+    """INT8 SwiGLU within 2^-46 of silu(g) u from exact rational g and u and a
+    60-digit decimal exponential (gate sums up to about +-50)."""
+    rng = np.random.default_rng(seed)
+    for _ in range(trials):
+        M, N, K = (int(v) for v in rng.integers(1, 7, size=3))
+        qX, qWg, qWu = _rand_i8(rng, (M, K)), _rand_i8(rng, (N, K)), _rand_i8(rng, (N, K))
+        sx = _rand_scales(rng, M, -6, -3)
+        swg, swu = _rand_scales(rng, N, -8, -4), _rand_scales(rng, N, -8, -4)
+        H = orc.i8_swiglu(qX, sx, qWg, swg, qWu, swu)
+        with localcontext() as ctx:
+            ctx.prec = 60
+            for i in range(M):
+                for j in range(N):
+                    ag = sum(int(qX[i, k]) * int(qWg[j, k]) for k in range(K))
+                    au = sum(int(qX[i, k]) * int(qWu[j, k]) for k in range(K))
+                    g = Fraction(float(sx[i])) * Fraction(float(swg[j])) * ag
+                    u = Fraction(float(sx[i])) * Fraction(float(swu[j])) * au
+                    gd = Decimal(g.numerator) / Decimal(g.denominator)
+                    ud = Decimal(u.numerator) / Decimal(u.denominator)
+                    sd = gd / (1 + (-gd).exp())
+                    ref = sd * ud
+                    bound = (abs(sd * ud) + Decimal(1.1) * abs(gd * ud)) * Decimal(2) ** -46 + Decimal(2) ** -1000
+                    assert abs(Decimal(float(H[i, j])) - ref) <= bound, (i, j)
+
+
+def pin_i8_at_matches_full(orc, seed=36):
+    rng = np.random.default_rng(seed)
+    M, N, K = 7, 9, 24
+    qX, qW, qWu = _rand_i8(rng, (M, K)), _rand_i8(rng, (N, K)), _rand_i8(rng, (N, K))
+    sx, sw, swu = _rand_scales(rng, M), _rand_scales(rng, N), _rand_scales(rng, N)
+    R = _rand_bits(rng, (M, N))
+    rows, cols = rng.integers(0, M, 40), rng.integers(0, N, 40)
+    np.testing.assert_array_equal(orc.i8_linear_at(qX, sx, qW, sw, R, rows, cols),
+                                  orc.i8_linear(qX, sx, qW, sw, R)[rows, cols])
+    np.testing.assert_array_equal(orc.i8_swiglu_at(qX, sx, qW, sw, qWu, swu, rows, cols),
+                                  orc.i8_swiglu(qX, sx, qW, sw, qWu, swu)[rows, cols])
+
+
+I8_PINS = [
+    pin_i8_exact_integer_sums,
+    pin_i8_dequant_exact,
+    pin_i8_matches_bf16_oracle,
+    pin_i8_zero_weight,
+    pin_i8_swiglu_decimal,
+    pin_i8_at_matches_full,
+]
+
 ALL_PINS = [
     pin_exact_bruteforce,
     pin_golden_hand_worked,
@@ -542,4 +690,4 @@ ALL_PINS = [
     pin_round_midpoints,
     pin_round_specials,
     pin_round_like_torch,
-] + EX_PINS + GLU_PINS
+] + EX_PINS + GLU_PINS + I8_PINS

@@ -43,6 +43,14 @@ MUTANTS = {
                          "u += x * bf16_bits_to_double(Wu[j * K + (k + 1) % K]);"),
     "glu_float_gate": ("    double g = 0.0;\n", "    float g = 0.0f;\n"),
     "glu_exp_base_2": ("return z / (1.0 + exp(-z));", "return z / (1.0 + exp2(-z));"),
+    "i8_int16_accumulator": ("    int64_t acc = 0;\n    for (int64_t k = 0; k < K; ++k)\n        acc += (int64_t)x[k]",
+                             "    int16_t acc = 0;\n    for (int64_t k = 0; k < K; ++k)\n        acc += (int64_t)x[k]"),
+    "i8_unsigned_weights": ("acc += (int64_t)x[k] * (int64_t)w[k];", "acc += (int64_t)x[k] * (int64_t)(uint8_t)w[k];"),
+    "i8_row_scale_by_col": ("double y = (double)sx[i] * (double)sw[j]", "double y = (double)sx[j % (i + 1)] * (double)sw[j]"),
+    "i8_col_scale_dropped": ("double y = (double)sx[i] * (double)sw[j]", "double y = (double)sx[i]"),
+    "i8_residual_dropped": ("    if (R)\n        y += bf16_bits_to_double(R[i * N + j]);", "    (void)R;"),
+    "i8_glu_up_scale_from_gate": ("double u = (double)sx[i] * (double)swu[j]", "double u = (double)sx[i] * (double)swg[j]"),
+    "i8_glu_float_gate": ("    double g = (double)sx[i] * (double)swg[j]", "    float g = (double)sx[i] * (double)swg[j]"),
 }
 
 
