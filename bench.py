@@ -24,9 +24,10 @@ Printed JSON line (stdout, last line):
             of the same 16 shapes, same aggregation
 Per-shape rows, the geometric mean of per-shape roofline fractions, the
 three single-shape gates (decode M=16, prefill 4096^3, square 8192^3 plain),
-the general form (alpha, beta, bias, row strides) and SwiGLU (the decoder
-layer's gate/up projections with the SiLU-multiply fused) on decoder-layer
-shapes are extra fields of the same line.
+the general form (alpha, beta, bias, row strides), SwiGLU (the decoder
+layer's gate/up projections with the SiLU-multiply fused) and the INT8 forms
+(W8A8 with dequantisation, INT8 SwiGLU; against the int8 MFMA peak) on
+decoder-layer shapes are extra fields of the same line.
 """
 from __future__ import annotations
 
@@ -42,6 +43,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2516.6          # 256 CU x 4096 FLOP/clk x 2.4 GHz, dense
+PEAK_I8_TOPS = 5033.2              # 256 CU x 8192 OP/clk x 2.4 GHz, dense
 PEAK_HBM_GBPS = 8000.0
 ROTATE_BYTES = 1 << 30
 MAX_COPIES = 256
@@ -52,12 +54,17 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
+def mfma_peak(w):
+    """Dense MFMA peak (T op/s) of the workload's operand type."""
+    return PEAK_I8_TOPS if hasattr(w, "swiglu") else PEAK_BF16_TFLOPS
+
+
 def roofline_time(w):
-    return max(w.flops / (PEAK_BF16_TFLOPS * 1e12), w.algorithmic_bytes / (PEAK_HBM_GBPS * 1e9))
+    return max(w.flops / (mfma_peak(w) * 1e12), w.algorithmic_bytes / (PEAK_HBM_GBPS * 1e9))
 
 
 def bound_of(w):
-    return "mfma" if w.flops / (PEAK_BF16_TFLOPS * 1e12) >= w.algorithmic_bytes / (PEAK_HBM_GBPS * 1e9) else "hbm"
+    return "mfma" if w.flops / (mfma_peak(w) * 1e12) >= w.algorithmic_bytes / (PEAK_HBM_GBPS * 1e9) else "hbm"
 
 
 def geomean(xs):
@@ -235,6 +242,71 @@ class GluCase(Case):
         ka.swiglu_bf16(x, g, u, out=h, plan=self.forced)
 
 
+class I8Case(Case):
+    """An INT8 workload (W8A8 linear with dequantisation, or INT8 SwiGLU)."""
+
+    def __init__(self, w, ka, torch, rotate=True, plan=None):
+        from paper_2608_17071_amd import workloads as wl
+        t = wl.make_i8_inputs(w)
+        self.w = w
+        self.host = t
+        dev = {k: (v.cuda() if v is not None else None) for k, v in t.items()}
+        n = 1
+        if rotate:
+            n = max(2, min(MAX_COPIES, -(-ROTATE_BYTES // w.algorithmic_bytes)))
+        self.sets = []
+        for i in range(n):
+            d = {k: (v if (i == 0 or v is None) else v.clone()) for k, v in dev.items()}
+            d["Y"] = torch.empty(w.M, w.N, dtype=torch.bfloat16, device="cuda")
+            self.sets.append(d)
+        self.forced = plan
+        self.plan = ka.select_plan_i8(w.M, w.N, w.K, w.swiglu) if plan is None else plan
+        self.plan_name = ka.plan_name(self.plan)
+        self.times = []
+        self.graph = None
+
+    def call(self, ka, i):
+        d = self.sets[i]
+        if self.w.swiglu:
+            ka.swiglu_i8(d["qX"], d["sx"], d["qW"], d["sw"], d["qWu"], d["swu"], out=d["Y"], plan=self.forced)
+        else:
+            ka.gemm_i8(d["qX"], d["sx"], d["qW"], d["sw"], d["R"], out=d["Y"], plan=self.forced)
+
+
+def cpu_baseline_i8(cases, seconds):
+    """The oracle's INT8 forms on rows 0, 1, ... of each case until its time share is used."""
+    import numpy as np
+    import oracle
+    from paper_2608_17071_amd import workloads as wl
+
+    orc = oracle.default()
+    per_shape = seconds / len(cases)
+    rates, rows_done = [], []
+    for c in cases:
+        w, h = c.w, c.host
+        qx, sx, qw, sw = h["qX"].numpy(), h["sx"].numpy(), h["qW"].numpy(), h["sw"].numpy()
+        rb = wl.bits(h["R"]) if h["R"] is not None else None
+        cols = np.arange(w.N, dtype=np.int64)
+        ops, rows, t0 = 0, 0, time.perf_counter()
+        while rows < w.M:
+            r = np.full(w.N, rows, dtype=np.int64)
+            if w.swiglu:
+                orc.i8_swiglu_at(qx, sx, qw, sw, h["qWu"].numpy(), h["swu"].numpy(), r, cols)
+            else:
+                orc.i8_linear_at(qx, sx, qw, sw, rb, r, cols)
+            rows += 1
+            ops += (4 if w.swiglu else 2) * w.N * w.K
+            if time.perf_counter() - t0 >= per_shape:
+                break
+        rates.append(ops / (time.perf_counter() - t0) / 1e12)
+        rows_done.append(rows)
+    return {
+        "value": geomean(rates), "unit": "T op/s (oracle: exact int64 sums, fp64 dequantisation; geomean)",
+        "cores": orc.threads(), "kind": "oracle",
+        "sample": f"whole output rows 0..r-1 of each INT8 shape, r = {rows_done} (about {per_shape:.2f} s each)",
+    }
+
+
 def cpu_baseline_glu(cases, seconds):
     """The oracle's SwiGLU on rows 0, 1, ... of each case until its time share is used."""
     import numpy as np
@@ -397,6 +469,8 @@ def main():
                     help="skip the general-form shapes (alpha, beta, bias, row strides)")
     ap.add_argument("--no-swiglu", action="store_true",
                     help="skip the SwiGLU gate/up shapes")
+    ap.add_argument("--no-int8", action="store_true",
+                    help="skip the INT8 (W8A8 with dequantisation) shapes")
     ap.add_argument("--only", default="",
                     help="comma-separated workload names (sweep, gate, general-form or SwiGLU): "
                          "time just these (for profiling one kernel)")
@@ -444,6 +518,8 @@ def main():
                 return GluCase(wl.GLU_BY_NAME[n], ka, torch, rotate=not args.hot)
             if n in wl.GENERAL_BY_NAME:
                 return GeneralCase(wl.GENERAL_BY_NAME[n], ka, torch, rotate=not args.hot)
+            if n in wl.I8_BY_NAME:
+                return I8Case(wl.I8_BY_NAME[n], ka, torch, rotate=not args.hot)
             return Case(wl.BY_NAME[n], ka, torch, rotate=not args.hot)
         cases = [case_of(n) for n in args.only.split(",")]
         time_cases(cases, args.steps, args.warmup, ka, torch, use_graph=not args.no_graph)
@@ -551,6 +627,33 @@ def main():
             c.free()
         del scases
 
+    # INT8 (NEXT row: the precision axis, W8A8 with the dequantisation fused
+    # into the epilogue, and the decoder layer's INT8 gate/up path with the
+    # SwiGLU epilogue); roofline against the dense int8 MFMA peak.
+    int8 = None
+    if not args.no_int8:
+        for c in sweep:
+            c.free()
+        icases = [I8Case(w, ka, torch, rotate=not args.hot) for w in wl.I8]
+        time_cases(icases, args.steps, args.warmup, ka, torch, use_graph=not args.no_graph)
+        irows = []
+        for c in icases:
+            r = shape_row(c)
+            irows.append(r)
+            log(f"  {r['shape']:40s} {r['plan']:28s} {r['us']:9.2f} us {r['tflops']:8.1f} TOP {r['gbps']:7.0f} GB/s  "
+                f"{r['bound']} frac {r['roofline_frac']:.3f}")
+        int8 = {"op": "Y = bf16(sx[i] sw[j] sum_k qX qW (+ R)); SwiGLU: silu(sx swg Ag) * (sx swu Au); "
+                      "ops = 2MNK (4MNK for SwiGLU), peak = dense int8 MFMA",
+                "peak_tops": PEAK_I8_TOPS, "shapes": irows,
+                "geomean_tops": round(geomean([r["tflops"] for r in irows]), 3),
+                "geomean_roofline_frac": round(geomean([r["roofline_frac"] for r in irows]), 4)}
+        if not args.no_cpu_baseline:
+            log("timing the CPU oracle on INT8 (~4 s) ...")
+            int8["cpu_baseline"] = cpu_baseline_i8(icases, 4.0)
+        for c in icases:
+            c.free()
+        del icases
+
     cpu = None
     if not args.no_cpu_baseline:
         log(f"timing the CPU oracle (~{args.cpu_seconds:.0f} s) ...")
@@ -578,6 +681,7 @@ def main():
         "gates": gates,
         "general": general,
         "swiglu": swiglu,
+        "int8": int8,
     }
     print(json.dumps(out), flush=True)
 

@@ -204,6 +204,58 @@ int kernelarc_select_plan_swiglu(int64_t M, int64_t N, int64_t K);
  * plan or negative sizes. */
 int kernelarc_plan_supports_swiglu(int plan, int64_t M, int64_t N, int64_t K);
 
+/*
+ * INT8 linear layer with a dequantisation epilogue (W8A8), and the INT8
+ * SwiGLU gate/up projection of the decoder-layer case study (Alg. 7: its
+ * INT8 path computes the gate/up GEMM with a fused dequantisation and SwiGLU
+ * epilogue).  Symmetric quantisation with one binary32 scale per row of the
+ * activations (token) and one per output channel, no zero points:
+ *
+ *     A[i,j] = sum_k qX[i,k] qW[j,k]               (exact, int32)
+ *     Y[i,j] = bf16( sx[i] * sw[j] * A[i,j]  (+ R[i,j]) )
+ *     H[i,j] = bf16( silu(sx[i] swg[j] Ag[i,j]) * (sx[i] swu[j] Au[i,j]) )
+ *
+ * qX is [M,K], qW, qWg, qWu are [N,K] int8 (nn.Linear orientation), sx is
+ * [M] and sw, swg, swu are [N] floats; R (optional, NULL for none) and Y, H
+ * are [M,N] bf16; all dense row-major device buffers owned by the caller.
+ * The integer sums are exact (K <= 65536 keeps them in int32; a larger K is
+ * rejected with KERNELARC_ERR_INVALID_ARG); A is converted to fp32 and
+ * multiplied by sx[i] * sw[j] (formed in fp32); the residual is added in
+ * fp32; one round-to-nearest-even to bf16.  Y may equal R (in place); any
+ * other overlap of the output with an operand or a scale vector is
+ * rejected.  Scale vectors must be 4-byte aligned.  M == 0 or N == 0: no
+ * launch.  16-byte aligned int8 operands with K a multiple of 16 take the
+ * MFMA tile kernels (v_mfma_i32_32x32x32_i8); anything else a generic kernel
+ * with the same contract.
+ */
+int kernelarc_gemm_i8(int64_t M, int64_t N, int64_t K, const void *qX, const float *sx,
+                      const void *qW, const float *sw, const void *R, void *Y, hipStream_t stream);
+
+/* The INT8 GEMM with a forced plan (KERNELARC_ERR_UNSUPPORTED if the plan
+ * cannot compute it: only tile plans and the generic plan can). */
+int kernelarc_gemm_i8_with_plan(int plan, int64_t M, int64_t N, int64_t K, const void *qX,
+                                const float *sx, const void *qW, const float *sw, const void *R,
+                                void *Y, hipStream_t stream);
+
+/* INT8 SwiGLU (see above): 0 <= N < 2^30. */
+int kernelarc_swiglu_i8(int64_t M, int64_t N, int64_t K, const void *qX, const float *sx,
+                        const void *qWg, const float *swg, const void *qWu, const float *swu,
+                        void *H, hipStream_t stream);
+
+/* INT8 SwiGLU with a forced plan (tile plans that pair gate and up blocks,
+ * and the generic plan). */
+int kernelarc_swiglu_i8_with_plan(int plan, int64_t M, int64_t N, int64_t K, const void *qX,
+                                  const float *sx, const void *qWg, const float *swg,
+                                  const void *qWu, const float *swu, void *H, hipStream_t stream);
+
+/* The plan the INT8 GEMM (swiglu == 0) or INT8 SwiGLU (swiglu != 0) runs for
+ * these sizes with aligned operands; -1 for negative sizes. */
+int kernelarc_select_plan_i8(int64_t M, int64_t N, int64_t K, int swiglu);
+
+/* 1 if `plan` can compute the INT8 GEMM / SwiGLU at these sizes, 0 if not,
+ * -1 for an unknown plan or negative sizes. */
+int kernelarc_plan_supports_i8(int plan, int64_t M, int64_t N, int64_t K, int swiglu);
+
 /* Static description of a status code. */
 const char *kernelarc_status_string(int status);
 

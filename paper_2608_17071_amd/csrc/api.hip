@@ -379,6 +379,52 @@ int select_glu(int64_t M, int64_t N, int64_t K) {
     return plan >= 0 ? plan : PLAN_GENERIC;
 }
 
+// INT8 operands (W8A8 with dequantisation scales): the tile plans when K is
+// a multiple of 16 (16-byte chunks of int8), and the generic plan.  A stage
+// of an INT8 tile holds twice the K elements of a bf16 one, so panel sizes,
+// tile counts and split-K rules are those of the bf16 problem at K/2.
+// |A| <= K * 2^14 keeps the exact int32 sums in range for K <= 2^16.
+constexpr int64_t I8_MAX_K = int64_t{1} << 16;
+
+bool supports_i8(int plan, int64_t M, int64_t N, int64_t K, bool glu) {
+    if (M < 0 || N < 0 || K < 0 || M > LIMIT_DIM || N > (glu ? LIMIT_DIM / 2 : LIMIT_DIM) || K > I8_MAX_K) return false;
+    if (plan < 0 || plan >= NUM_PLANS) return false;
+    const PlanInfo &pi = PLANS[plan];
+    if (pi.kind == KIND_GENERIC) return cdiv(M, 64) * cdiv(N, 64) * 256 <= LIMIT_ITEMS;
+    if (pi.kind != KIND_TILE || K % 16 != 0) return false;
+    return glu ? supports_glu(plan, M, N, K / 2) : supports(plan, M, N, K / 2, true, dense_layout(N, K / 2));
+}
+
+// INT8 plan rule (measured on MI355X): the bf16 rules at K/2 (the same
+// bytes per stage), with three changes.  Plain GEMMs up to 64 rows take
+// 64x64 tiles, 3 stages of depth 256 with split-K while the tiles fill at
+// most half the CUs, else 4 stages of depth 128 (the bf16 choices there are
+// non-tile kernels).  The 256x256 tile runs without the tail split: an
+// INT8 tile covers its K range in half the steps, so the split's partial
+// round trip costs more than the idle CUs it saves (6% at M = 2048 SwiGLU).
+int select_i8(int64_t M, int64_t N, int64_t K, bool glu) {
+    if (M < 0 || N < 0 || K < 0) return -1;
+    if (K % 16 != 0 || K > I8_MAX_K) return PLAN_GENERIC;
+    auto pick = [&](const char *name) {
+        const int p = plan_index(name);
+        return (p >= 0 && supports_i8(p, M, N, K, glu)) ? p : -1;
+    };
+    int plan = -1;
+    if (!glu && M <= 64) {
+        const int64_t t64 = tile_count(tile_shape(TC_64x64_K64_S4_W4), M, N);
+        plan = 2 * t64 <= CUS ? pick("tile_64x64_k128s3_w4_splitk") : pick("tile_64x64_k64s4_w4");
+        if (plan >= 0) return plan;
+    }
+    plan = glu ? select_glu(M, N, K / 2) : select(M, N, K / 2, true, dense_layout(N, K / 2));
+    if (plan == plan_index("tile_256x256_k64_w8_tailsplit")) plan = plan_index("tile_256x256_k64_w8");
+    if (plan >= 0 && plan != PLAN_GENERIC && supports_i8(plan, M, N, K, glu)) return plan;
+    for (const char *name : {"tile_64x64_k128s3_w4_splitk", "tile_64x128_k64s4_w4", "tile_128x128_k64_w4"}) {
+        const int p = plan_index(name);
+        if (p >= 0 && supports_i8(p, M, N, K, glu)) return p;
+    }
+    return PLAN_GENERIC;
+}
+
 // ------------------------------------------------------------ devices ----
 constexpr int MAX_DEVICES = 64;
 
@@ -623,6 +669,89 @@ int run_glu(int plan, int64_t M, int64_t N, int64_t K, const void *X, const void
     return KERNELARC_OK;
 }
 
+bool aligned4(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
+
+// INT8 call.  glu: H = bf16(silu(sx swg Ag) (sx swu Au)) (W2, sw2 the up
+// operands); else Y = bf16(sx sw A (+ R)).  plan < 0: choose.
+int run_i8(int plan, bool glu, int64_t M, int64_t N, int64_t K, const void *X, const float *sx, const void *W,
+           const float *sw, const void *W2, const float *sw2, const void *R, void *Y, hipStream_t stream) {
+    g_last_error[0] = '\0';
+    if (M < 0 || N < 0 || K < 0)
+        return fail(KERNELARC_ERR_INVALID_ARG, "negative size M=%lld N=%lld K=%lld", (long long)M,
+                    (long long)N, (long long)K);
+    if (M > LIMIT_DIM || N > (glu ? LIMIT_DIM / 2 : LIMIT_DIM))
+        return fail(KERNELARC_ERR_INVALID_ARG, "a size is too large");
+    if (K > I8_MAX_K)
+        return fail(KERNELARC_ERR_INVALID_ARG, "K=%lld above %lld could overflow the int32 sums", (long long)K,
+                    (long long)I8_MAX_K);
+    if (plan >= NUM_PLANS) return fail(KERNELARC_ERR_UNSUPPORTED, "unknown plan %d", plan);
+    if (M == 0 || N == 0) return KERNELARC_OK;
+    if (!Y) return fail(KERNELARC_ERR_INVALID_ARG, "the output is NULL");
+    if (K > 0 && (!X || !W || (glu && !W2))) return fail(KERNELARC_ERR_INVALID_ARG, "an int8 operand is NULL");
+    if (!sx || !sw || (glu && !sw2)) return fail(KERNELARC_ERR_INVALID_ARG, "a scale vector is NULL");
+    if (!aligned4(sx) || !aligned4(sw) || (glu && !aligned4(sw2)))
+        return fail(KERNELARC_ERR_INVALID_ARG, "scale vectors must be 4-byte aligned");
+    const int64_t ybytes = M * N * 2;
+    if (overlaps(Y, ybytes, X, M * K) || overlaps(Y, ybytes, W, N * K) || (glu && overlaps(Y, ybytes, W2, N * K)) ||
+        overlaps(Y, ybytes, sx, M * 4) || overlaps(Y, ybytes, sw, N * 4) || (glu && overlaps(Y, ybytes, sw2, N * 4)))
+        return fail(KERNELARC_ERR_INVALID_ARG, "the output overlaps an operand or a scale vector");
+    if (R && R != Y && overlaps(Y, ybytes, R, ybytes))
+        return fail(KERNELARC_ERR_INVALID_ARG, "Y partially overlaps R (only Y == R is allowed)");
+
+    int dev = 0, num_cus = 0;
+    const int st = current_device(&dev, &num_cus);
+    if (st != KERNELARC_OK) return st;
+
+    const bool vec_ok = aligned16(X) && aligned16(W) && (!glu || aligned16(W2)) && aligned16(Y) &&
+                        (!R || aligned16(R)) && K % 16 == 0;
+    if (plan < 0) {
+        plan = select_i8(M, N, K, glu);
+        if (plan != PLAN_GENERIC && !vec_ok) plan = PLAN_GENERIC;
+    } else {
+        if (!supports_i8(plan, M, N, K, glu))
+            return fail(KERNELARC_ERR_UNSUPPORTED, "plan %s cannot compute the INT8 %s at M=%lld N=%lld K=%lld",
+                        PLANS[plan].name, glu ? "SwiGLU" : "GEMM", (long long)M, (long long)N, (long long)K);
+        if (plan != PLAN_GENERIC && !vec_ok)
+            return fail(KERNELARC_ERR_UNSUPPORTED, "plan %s needs 16-byte aligned operands and K a multiple of 16",
+                        PLANS[plan].name);
+    }
+    (void)hipGetLastError();
+    hipError_t e = hipSuccess;
+    const auto *x8 = static_cast<const int8_t *>(X);
+    const auto *w8 = static_cast<const int8_t *>(W);
+    if (PLANS[plan].kind == KIND_GENERIC) {
+        if (glu)
+            e = launch_generic_i8_glu(I8GluProblem{M, N, K, x8, w8, static_cast<const int8_t *>(W2),
+                                                   static_cast<uint16_t *>(Y), sx, sw, sw2},
+                                      stream);
+        else
+            e = launch_generic_i8(I8Problem{M, N, K, x8, w8, static_cast<const uint16_t *>(R),
+                                            static_cast<uint16_t *>(Y), sx, sw},
+                                  stream);
+    } else {
+        const TileSplit sp = tile_split_plan(plan, M, glu ? 2 * N : N, K / 2);
+        Workspace ws{};
+        if (sp.split > 1) {
+            const int wst = workspace(dev, stream, &ws);
+            if (wst != KERNELARC_OK) return wst;
+        }
+        const Workspace *wsp = sp.split > 1 ? &ws : nullptr;
+        if (glu)
+            e = launch_tile_i8_glu(PLANS[plan].tile_cfg,
+                                   I8GluProblem{M, N, K, x8, w8, static_cast<const int8_t *>(W2),
+                                                static_cast<uint16_t *>(Y), sx, sw, sw2},
+                                   sp.split, sp.full_tiles, wsp, stream);
+        else
+            e = launch_tile_i8(PLANS[plan].tile_cfg,
+                               I8Problem{M, N, K, x8, w8, static_cast<const uint16_t *>(R), static_cast<uint16_t *>(Y),
+                                         sx, sw},
+                               sp.split, sp.full_tiles, wsp, stream);
+    }
+    if (e != hipSuccess)
+        return fail(KERNELARC_ERR_LAUNCH, "launch of %s failed: %s", PLANS[plan].name, hipGetErrorString(e));
+    return KERNELARC_OK;
+}
+
 }  // namespace
 }  // namespace kernelarc
 
@@ -702,6 +831,42 @@ int kernelarc_select_plan_swiglu(int64_t M, int64_t N, int64_t K) { return selec
 int kernelarc_plan_supports_swiglu(int plan, int64_t M, int64_t N, int64_t K) {
     if (plan < 0 || plan >= NUM_PLANS || M < 0 || N < 0 || K < 0) return -1;
     return supports_glu(plan, M, N, K) ? 1 : 0;
+}
+
+int kernelarc_gemm_i8(int64_t M, int64_t N, int64_t K, const void *qX, const float *sx, const void *qW,
+                      const float *sw, const void *R, void *Y, hipStream_t stream) {
+    return run_i8(-1, false, M, N, K, qX, sx, qW, sw, nullptr, nullptr, R, Y, stream);
+}
+
+int kernelarc_gemm_i8_with_plan(int plan, int64_t M, int64_t N, int64_t K, const void *qX, const float *sx,
+                                const void *qW, const float *sw, const void *R, void *Y, hipStream_t stream) {
+    if (plan < 0) {
+        g_last_error[0] = '\0';
+        return fail(KERNELARC_ERR_UNSUPPORTED, "unknown plan %d", plan);
+    }
+    return run_i8(plan, false, M, N, K, qX, sx, qW, sw, nullptr, nullptr, R, Y, stream);
+}
+
+int kernelarc_swiglu_i8(int64_t M, int64_t N, int64_t K, const void *qX, const float *sx, const void *qWg,
+                        const float *swg, const void *qWu, const float *swu, void *H, hipStream_t stream) {
+    return run_i8(-1, true, M, N, K, qX, sx, qWg, swg, qWu, swu, nullptr, H, stream);
+}
+
+int kernelarc_swiglu_i8_with_plan(int plan, int64_t M, int64_t N, int64_t K, const void *qX, const float *sx,
+                                  const void *qWg, const float *swg, const void *qWu, const float *swu, void *H,
+                                  hipStream_t stream) {
+    if (plan < 0) {
+        g_last_error[0] = '\0';
+        return fail(KERNELARC_ERR_UNSUPPORTED, "unknown plan %d", plan);
+    }
+    return run_i8(plan, true, M, N, K, qX, sx, qWg, swg, qWu, swu, nullptr, H, stream);
+}
+
+int kernelarc_select_plan_i8(int64_t M, int64_t N, int64_t K, int swiglu) { return select_i8(M, N, K, swiglu != 0); }
+
+int kernelarc_plan_supports_i8(int plan, int64_t M, int64_t N, int64_t K, int swiglu) {
+    if (plan < 0 || plan >= NUM_PLANS || M < 0 || N < 0 || K < 0) return -1;
+    return supports_i8(plan, M, N, K, swiglu != 0) ? 1 : 0;
 }
 
 int kernelarc_plan_count(void) { return NUM_PLANS; }

@@ -88,6 +88,26 @@ struct GluProblem {
     uint16_t *Y;                 // [M,N]
 };
 
+// INT8 operands with dequantisation scales (symmetric W8A8: one scale per
+// row of X, one per row of W):
+//   Y = bf16(sx[i] sw[j] A[i,j] (+ R[i,j])),  A = qX qW^T summed exactly in int32.
+struct I8Problem {
+    int64_t M, N, K;
+    const int8_t *X, *W;         // [M,K], [N,K]
+    const uint16_t *R;           // [M,N] bf16 or null
+    uint16_t *Y;                 // [M,N] bf16
+    const float *sx, *sw;        // [M], [N]
+};
+
+// INT8 SwiGLU: Y = bf16(silu(sx swg Ag) * (sx swu Au)) with Ag = qX qW^T
+// (gate) and Au = qX qW2^T (up).
+struct I8GluProblem {
+    int64_t M, N, K;
+    const int8_t *X, *W, *W2;
+    uint16_t *Y;
+    const float *sx, *sw, *sw2;  // [M], gate [N], up [N]
+};
+
 // Uniform access to every form inside the kernels.
 __host__ __device__ inline int64_t ldx_of(const Problem &p) { return p.ldx; }
 __host__ __device__ inline int64_t ldw_of(const Problem &p) { return p.ldw; }
@@ -111,6 +131,22 @@ __host__ __device__ inline int64_t ldy_of(const GluProblem &p) { return p.N; }
 __host__ __device__ inline float alpha_of(const GluProblem &) { return 1.0f; }
 __host__ __device__ inline float beta_of(const GluProblem &) { return 1.0f; }
 __host__ __device__ inline const uint16_t *bias_of(const GluProblem &) { return nullptr; }
+__host__ __device__ inline int64_t ldx_of(const I8Problem &p) { return p.K; }
+__host__ __device__ inline int64_t ldw_of(const I8Problem &p) { return p.K; }
+__host__ __device__ inline int64_t ldr_of(const I8Problem &p) { return p.N; }
+__host__ __device__ inline int64_t ldy_of(const I8Problem &p) { return p.N; }
+__host__ __device__ inline float alpha_of(const I8Problem &) { return 1.0f; }
+__host__ __device__ inline float beta_of(const I8Problem &) { return 1.0f; }
+__host__ __device__ inline const uint16_t *bias_of(const I8Problem &) { return nullptr; }
+__host__ __device__ inline int64_t ldx_of(const I8GluProblem &p) { return p.K; }
+__host__ __device__ inline int64_t ldw_of(const I8GluProblem &p) { return p.K; }
+__host__ __device__ inline int64_t ldr_of(const I8GluProblem &p) { return p.N; }
+__host__ __device__ inline int64_t ldy_of(const I8GluProblem &p) { return p.N; }
+__host__ __device__ inline float alpha_of(const I8GluProblem &) { return 1.0f; }
+__host__ __device__ inline float beta_of(const I8GluProblem &) { return 1.0f; }
+__host__ __device__ inline const uint16_t *bias_of(const I8GluProblem &) { return nullptr; }
+__host__ __device__ inline const uint16_t *resid_of(const I8Problem &p) { return p.R; }
+__host__ __device__ inline const uint16_t *resid_of(const I8GluProblem &) { return nullptr; }
 __host__ __device__ inline const uint16_t *resid_of(const Problem &p) { return p.R; }
 __host__ __device__ inline const uint16_t *resid_of(const DenseProblem &p) { return p.R; }
 __host__ __device__ inline const uint16_t *resid_of(const GluProblem &) { return nullptr; }
@@ -151,6 +187,14 @@ hipError_t launch_generic_glu(const GluProblem &p, hipStream_t s);
 hipError_t launch_tile_glu(int cfg, const GluProblem &p, int split, int64_t full_tiles, const Workspace *ws,
                            hipStream_t s);
 bool tile_glu_ok(int cfg);
+// INT8: generic kernels (any K, any alignment) and the tile kernels (K a
+// multiple of 16; SwiGLU on the configurations of tile_glu_ok).
+hipError_t launch_generic_i8(const I8Problem &p, hipStream_t s);
+hipError_t launch_generic_i8_glu(const I8GluProblem &p, hipStream_t s);
+hipError_t launch_tile_i8(int cfg, const I8Problem &p, int split, int64_t full_tiles, const Workspace *ws,
+                          hipStream_t s);
+hipError_t launch_tile_i8_glu(int cfg, const I8GluProblem &p, int split, int64_t full_tiles, const Workspace *ws,
+                              hipStream_t s);
 
 // Shape rules of the kernels, used by the plan table (host only).
 int skinny_split_for(int64_t M, int64_t N, int64_t K);

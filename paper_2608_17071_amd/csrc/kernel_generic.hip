@@ -1,6 +1,6 @@
 // Generic kernels: Y = alpha X W^T (+ beta R) (+ bias) for any shape, any
-// row strides and any pointer alignment, and SwiGLU for any shape and
-// alignment.
+// row strides and any pointer alignment, and SwiGLU and the INT8 forms for
+// any shape and alignment.
 //
 // This is the correctness fallback (K not a multiple of 8, pointers not
 // 16-byte aligned).  Each 256-thread workgroup computes a 64x64 output tile;
@@ -145,7 +145,109 @@ __global__ __launch_bounds__(256) void generic_glu_kernel(GluProblem p, int64_t 
     }
 }
 
+// INT8 fallbacks: the same 64x64 tiling with int8 operands staged as int32
+// and exact int32 sums; dequantisation (and the residual, or SwiGLU) in fp32
+// as the tile kernels do it.
+template <bool GLU_, class P>
+__device__ __forceinline__ void generic_i8_body(const P &p, int64_t tiles_n) {
+    __shared__ int xs[GK][GT + 1];
+    __shared__ int gs[GK][GT + 1];
+    __shared__ int us[GLU_ ? GK : 1][GT + 1];
+
+    const int tx = threadIdx.x & 15;
+    const int ty = threadIdx.x >> 4;
+    const int64_t tile = blockIdx.x;
+    const int64_t m0 = (tile / tiles_n) * GT;
+    const int64_t n0 = (tile % tiles_n) * GT;
+
+    int g[4][4], u[4][4];
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int b = 0; b < 4; ++b) g[a][b] = u[a][b] = 0;
+
+    for (int64_t k0 = 0; k0 < p.K; k0 += GK) {
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            const int idx = threadIdx.x + 256 * t;
+            const int r = idx / GK;
+            const int kk = idx % GK;
+            const int64_t k = k0 + kk;
+            const int64_t xm = m0 + r;
+            const int64_t wn = n0 + r;
+            const bool kin = k < p.K;
+            xs[kk][r] = (xm < p.M && kin) ? p.X[xm * p.K + k] : 0;
+            gs[kk][r] = (wn < p.N && kin) ? p.W[wn * p.K + k] : 0;
+            if constexpr (GLU_) us[kk][r] = (wn < p.N && kin) ? p.W2[wn * p.K + k] : 0;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int kk = 0; kk < GK; ++kk) {
+            int xv[4], gv[4], uv[4];
+#pragma unroll
+            for (int a = 0; a < 4; ++a) xv[a] = xs[kk][ty + 16 * a];
+#pragma unroll
+            for (int b = 0; b < 4; ++b) {
+                gv[b] = gs[kk][tx + 16 * b];
+                if constexpr (GLU_) uv[b] = us[kk][tx + 16 * b];
+            }
+#pragma unroll
+            for (int a = 0; a < 4; ++a)
+#pragma unroll
+                for (int b = 0; b < 4; ++b) {
+                    g[a][b] += xv[a] * gv[b];
+                    if constexpr (GLU_) u[a][b] += xv[a] * uv[b];
+                }
+        }
+        __syncthreads();
+    }
+
+#pragma unroll
+    for (int a = 0; a < 4; ++a) {
+        const int64_t i = m0 + ty + 16 * a;
+        if (i >= p.M) continue;
+        const float sr = p.sx[i];
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+            const int64_t j = n0 + tx + 16 * b;
+            if (j >= p.N) continue;
+            float y;
+            if constexpr (GLU_) {
+                const float gv = static_cast<float>(g[a][b]) * (sr * p.sw[j]);
+                const float uv = static_cast<float>(u[a][b]) * (sr * p.sw2[j]);
+                y = silu_f32(gv) * uv;
+            } else {
+                y = static_cast<float>(g[a][b]) * (sr * p.sw[j]);
+                if (p.R) y += bf16_to_f32(p.R[i * p.N + j]);
+            }
+            p.Y[i * p.N + j] = f32_to_bf16_rne(y);
+        }
+    }
+}
+
+__global__ __launch_bounds__(256) void generic_i8_kernel(I8Problem p, int64_t tiles_n) {
+    generic_i8_body<false>(p, tiles_n);
+}
+
+__global__ __launch_bounds__(256) void generic_i8_glu_kernel(I8GluProblem p, int64_t tiles_n) {
+    generic_i8_body<true>(p, tiles_n);
+}
+
 }  // namespace
+
+hipError_t launch_generic_i8(const I8Problem &p, hipStream_t s) {
+    const int64_t tiles_n = (p.N + GT - 1) / GT;
+    const int64_t tiles = ((p.M + GT - 1) / GT) * tiles_n;
+    hipLaunchKernelGGL(generic_i8_kernel, dim3(static_cast<unsigned>(tiles)), dim3(256), 0, s, p, tiles_n);
+    return hipGetLastError();
+}
+
+hipError_t launch_generic_i8_glu(const I8GluProblem &p, hipStream_t s) {
+    const int64_t tiles_n = (p.N + GT - 1) / GT;
+    const int64_t tiles = ((p.M + GT - 1) / GT) * tiles_n;
+    hipLaunchKernelGGL(generic_i8_glu_kernel, dim3(static_cast<unsigned>(tiles)), dim3(256), 0, s, p, tiles_n);
+    return hipGetLastError();
+}
 
 hipError_t launch_generic_glu(const GluProblem &p, hipStream_t s) {
     const int64_t tiles_n = (p.N + GT - 1) / GT;

@@ -42,6 +42,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef int i32x16 __attribute__((ext_vector_type(16)));
 typedef __attribute__((address_space(3))) void lds_void;
 
 // Word 3 of a raw (unswizzled, stride 0) gfx9 buffer resource.
@@ -174,12 +175,14 @@ __device__ __forceinline__ void static_for(F &&f) {
     if constexpr (E > B) static_for_impl<B>(f, std::make_integer_sequence<int, E - B>{});
 }
 
-template <class C, bool GLU>
+// BKE: K elements per stage (BK for bf16 operands, 2*BK for int8 ones: a
+// stage always holds ROW_BYTES bytes of each row).
+template <class C, bool GLU, int BKE>
 __device__ __forceinline__ void issue_stage(char *stage, const __amdgpu_buffer_rsrc_t &ra,
                                             const __amdgpu_buffer_rsrc_t &rb, const __amdgpu_buffer_rsrc_t &rb2,
                                             const uint32_t *a_off, const int *a_k, const uint32_t *b_off,
                                             const int *b_k, int wave, int kt, int64_t K) {
-    const int64_t kbase = static_cast<int64_t>(kt) * C::BK;
+    const int64_t kbase = static_cast<int64_t>(kt) * BKE;
     const uint32_t kbytes = static_cast<uint32_t>(kt) * C::ROW_BYTES;
     static_for<0, C::LOADS>([&](auto q) {
         issue_load<C, decltype(q)::value, GLU>(stage, ra, rb, rb2, a_off, a_k, b_off, b_k, wave, kbase, kbytes,
@@ -212,6 +215,29 @@ __device__ __forceinline__ void stage_barrier() {
     asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
 }
 
+// Accumulator quads as 16 raw bytes (fp32 or int32 bits) for the K-group
+// and split-K hand-offs, and their sums (exact for int32).
+// (q is a constant once the callers' loops are unrolled.)
+__device__ __forceinline__ f32x4 quad_bits(const f32x16 &a, int q) {
+    return f32x4{a[4 * q], a[4 * q + 1], a[4 * q + 2], a[4 * q + 3]};
+}
+__device__ __forceinline__ f32x4 quad_bits(const i32x16 &a, int q) {
+    return __builtin_bit_cast(f32x4, i32x4{a[4 * q], a[4 * q + 1], a[4 * q + 2], a[4 * q + 3]});
+}
+__device__ __forceinline__ void add_quad(f32x16 &a, int q, const f32x4 &v) {
+    a[4 * q] += v[0];
+    a[4 * q + 1] += v[1];
+    a[4 * q + 2] += v[2];
+    a[4 * q + 3] += v[3];
+}
+__device__ __forceinline__ void add_quad(i32x16 &a, int q, const f32x4 &bits) {
+    const i32x4 v = __builtin_bit_cast(i32x4, bits);
+    a[4 * q] += v[0];
+    a[4 * q + 1] += v[1];
+    a[4 * q + 2] += v[2];
+    a[4 * q + 3] += v[3];
+}
+
 // Split-K bookkeeping of one launch (split == 1: none).
 struct SplitK {
     int split;          // K slices per split tile (1: none)
@@ -227,13 +253,21 @@ struct SplitK {
 // P = Problem: the general form (row strides, alpha, beta, bias);
 // P = DenseProblem: dense operands, and the epilogue adds R as is (the plain
 // operator); P = GluProblem: SwiGLU, the B tile holds BN/2 gate and BN/2 up
-// rows (alternate 32-row blocks) and the output tile is BM x BN/2.
+// rows (alternate 32-row blocks) and the output tile is BM x BN/2;
+// P = I8Problem, I8GluProblem: the same with int8 operands (a stage holds
+// twice the K elements, v_mfma_i32_32x32x32_i8 accumulates exactly in
+// int32) and dequantisation by the row and column scales in the epilogue.
 template <class C, class P>
 __global__ __attribute__((amdgpu_flat_work_group_size(C::THREADS, C::THREADS),
                           amdgpu_waves_per_eu(C::WAVES_PER_EU, C::WAVES_PER_EU)))
 void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) {
     constexpr bool GEN = std::is_same<P, Problem>::value;
-    constexpr bool GLU = std::is_same<P, GluProblem>::value;
+    constexpr bool I8 = std::is_same<P, I8Problem>::value || std::is_same<P, I8GluProblem>::value;
+    constexpr bool GLU = std::is_same<P, GluProblem>::value || std::is_same<P, I8GluProblem>::value;
+    constexpr int EB = I8 ? 1 : 2;                 // bytes per operand element
+    constexpr int BKE = C::ROW_BYTES / EB;         // K elements per stage
+    constexpr int CKE = 16 / EB;                   // K elements per 16-byte chunk
+    using AccV = typename std::conditional<I8, i32x16, f32x16>::type;
     // Output columns of the tile and of one wave's block.
     constexpr int BNO = GLU ? C::BN / 2 : C::BN, WNO = GLU ? C::WN / 2 : C::WN;
     static_assert(!GLU || (C::TN % 2 == 0 && C::B_LOADS % 2 == 0 && 32 % C::RPI == 0), "gate/up pairing");
@@ -295,11 +329,11 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
     const int64_t rows_a = (p.M - m0) < C::BM ? (p.M - m0) : C::BM;
     const int64_t rows_b = (p.N - n0) < BNO ? (p.N - n0) : BNO;
     const __amdgpu_buffer_rsrc_t ra =
-        make_rsrc(p.X + m0 * ldx, static_cast<uint32_t>(GEN ? strided_bytes(rows_a, K, ldx) : rows_a * K * 2));
+        make_rsrc(p.X + m0 * ldx, static_cast<uint32_t>(GEN ? strided_bytes(rows_a, K, ldx) : rows_a * K * EB));
     const __amdgpu_buffer_rsrc_t rb =
-        make_rsrc(p.W + n0 * ldw, static_cast<uint32_t>(GEN ? strided_bytes(rows_b, K, ldw) : rows_b * K * 2));
+        make_rsrc(p.W + n0 * ldw, static_cast<uint32_t>(GEN ? strided_bytes(rows_b, K, ldw) : rows_b * K * EB));
     const __amdgpu_buffer_rsrc_t rb2 = [&] {
-        if constexpr (GLU) return make_rsrc(p.W2 + n0 * ldw, static_cast<uint32_t>(rows_b * K * 2));
+        if constexpr (GLU) return make_rsrc(p.W2 + n0 * ldw, static_cast<uint32_t>(rows_b * K * EB));
         else return rb;
     }();
 
@@ -312,25 +346,25 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
     for (int q = 0; q < C::A_LOADS; ++q) {
         const int r = (wave * C::A_LOADS + q) * C::RPI + lane / C::CHUNKS;
         const int c = slot ^ swz<C::CHUNKS>(r);
-        a_off[q] = static_cast<uint32_t>(r * ldx * 2 + c * 16);
-        a_k[q] = c * 8;
+        a_off[q] = static_cast<uint32_t>(r * ldx * EB + c * 16);
+        a_k[q] = c * CKE;
     }
 #pragma unroll
     for (int q = 0; q < C::B_LOADS; ++q) {
         const int r = b_block<C, GLU>(wave, q) * C::RPI + lane / C::CHUNKS;   // row of the B tile
         const int c = slot ^ swz<C::CHUNKS>(r);
         const int wr = GLU ? (r >> 6) * 32 + (r & 31) : r;                    // row of its weight panel
-        b_off[q] = static_cast<uint32_t>(wr * ldw * 2 + c * 16);
-        b_k[q] = c * 8;
+        b_off[q] = static_cast<uint32_t>(wr * ldw * EB + c * 16);
+        b_k[q] = c * CKE;
     }
 
-    f32x16 acc[C::TM][C::TN];
+    AccV acc[C::TM][C::TN];
 #pragma unroll
     for (int i = 0; i < C::TM; ++i)
 #pragma unroll
         for (int j = 0; j < C::TN; ++j)
 #pragma unroll
-            for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+            for (int e = 0; e < 16; ++e) acc[i][j][e] = 0;
 
     // Fragment reads: row (lane % 32) of each 32-row block, chunk 2*ks + hi.
     const int frag_row = lane & 31;
@@ -344,13 +378,13 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
     // The workgroup's BK steps [kt0, kt1); K group g takes the contiguous
     // part [g0, g1).  Every group runs the same number of iterations (the
     // barrier is shared); steps past its part load out-of-range zeros.
-    const int kt0 = static_cast<int>(kbeg / C::BK);
-    const int kt1 = kend > kbeg ? static_cast<int>((kend + C::BK - 1) / C::BK) : kt0;
+    const int kt0 = static_cast<int>(kbeg / BKE);
+    const int kt1 = kend > kbeg ? static_cast<int>((kend + BKE - 1) / BKE) : kt0;
     const int nsteps = kt1 - kt0;
     const int g0 = kt0 + nsteps * group / C::KGROUPS;
     const int g1 = kt0 + nsteps * (group + 1) / C::KGROUPS;
     const int iters = (nsteps + C::KGROUPS - 1) / C::KGROUPS;
-    const int64_t gend = (static_cast<int64_t>(g1) * C::BK) < kend ? static_cast<int64_t>(g1) * C::BK : kend;
+    const int64_t gend = (static_cast<int64_t>(g1) * BKE) < kend ? static_cast<int64_t>(g1) * BKE : kend;
 
     const bool owner = group == 0;   // the waves that hold the tile's result
 
@@ -397,6 +431,49 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
         if constexpr (GEN) return combine(acc, r, has_r, alpha, beta);
         else return has_r ? acc + r : acc;
     };
+    // INT8 dequantisation scales.  The column scales and the first slab's
+    // row scales are requested before the K loop so that their latency
+    // hides behind it; each later slab's row scales are requested one slab
+    // ahead.  Plain: the scales of the lane's 8 columns and of its row in
+    // each pass; SwiGLU: the gate and up scales of the lane's column in each
+    // block pair and the scales of the slab's 16 accumulator rows.
+    constexpr int NSX = !I8 ? 1 : GLU ? 16 : PASSES;
+    constexpr int NSW = !I8 ? 1 : GLU ? C::TN : 8;
+    float sxr[2][NSX], swc[NSW];
+    [[maybe_unused]] __amdgpu_buffer_rsrc_t rsx;
+    auto ld = [](const __amdgpu_buffer_rsrc_t &r, uint32_t off) {
+        return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
+    };
+    // Row scales of slab i into sxr[i & 1].
+    auto load_sx = [&](int i) {
+        if constexpr (GLU) {
+#pragma unroll
+            for (int e = 0; e < 16; ++e)
+                sxr[i & 1][e] = ld(rsx, static_cast<uint32_t>((wm0 + i * 32 + 8 * (e >> 2) + 4 * hi + (e & 3)) * 4));
+        } else {
+#pragma unroll
+            for (int v = 0; v < PASSES; ++v) sxr[i & 1][v] = ld(rsx, static_cast<uint32_t>(row_of(i, v) * 4));
+        }
+    };
+    if constexpr (I8) {
+        rsx = make_rsrc(p.sx + m0, static_cast<uint32_t>(rows_y * 4));
+        const __amdgpu_buffer_rsrc_t rsw = make_rsrc(p.sw, static_cast<uint32_t>(N * 4));
+        if constexpr (GLU) {
+            const __amdgpu_buffer_rsrc_t rsw2 = make_rsrc(p.sw2, static_cast<uint32_t>(N * 4));
+#pragma unroll
+            for (int j = 0; j < C::TN / 2; ++j) {
+                const int64_t c = n0 + wn0 / 2 + j * 32 + frag_row;
+                swc[j] = ld(rsw, c < N ? static_cast<uint32_t>(c * 4) : OOB_OFFSET);
+                swc[C::TN / 2 + j] = ld(rsw2, c < N ? static_cast<uint32_t>(c * 4) : OOB_OFFSET);
+            }
+        } else {
+#pragma unroll
+            for (int t = 0; t < 8; ++t)
+                swc[t] = ld(rsw, col0 + t < N ? static_cast<uint32_t>((col0 + t) * 4) : OOB_OFFSET);
+        }
+        load_sx(0);
+    }
+
     // Small tiles request the first slab of R before the K loop (a few
     // registers); it is then in flight with the first loads instead of after
     // the loop, or after the split-K hand-off.
@@ -431,7 +508,8 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
     // only write zeros into buffers whose contents are never used.
 #pragma unroll
     for (int s = 0; s < C::STAGES - 1; ++s)
-        issue_stage<C, GLU>(glds + s * C::STAGE_BYTES, ra, rb, rb2, a_off, a_k, b_off, b_k, wave, g0 + s, gend);
+        issue_stage<C, GLU, BKE>(glds + s * C::STAGE_BYTES, ra, rb, rb2, a_off, a_k, b_off, b_k, wave, g0 + s,
+                                 gend);
     stage_barrier<VM_KEEP0>();
     static_for<0, PD>([&](auto ksc) {
         constexpr int ks = decltype(ksc)::value;
@@ -441,8 +519,8 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
         });
     });
     if constexpr (!C::LAG)
-        issue_stage<C, GLU>(glds + (C::STAGES - 1) * C::STAGE_BYTES, ra, rb, rb2, a_off, a_k, b_off, b_k, wave,
-                            g0 + C::STAGES - 1, gend);
+        issue_stage<C, GLU, BKE>(glds + (C::STAGES - 1) * C::STAGE_BYTES, ra, rb, rb2, a_off, a_k, b_off, b_k,
+                                 wave, g0 + C::STAGES - 1, gend);
 
     int cur_stage = 0;
     for (int it = 0; it < iters; ++it) {
@@ -453,7 +531,7 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
         const int prev_stage = cur_stage == 0 ? C::STAGES - 1 : cur_stage - 1;
         char *const dst = C::LAG ? glds + prev_stage * C::STAGE_BYTES : cur;
         const int refill = g0 + it + (C::LAG ? C::STAGES - 1 : C::STAGES);
-        const int64_t kbase = static_cast<int64_t>(refill) * C::BK;
+        const int64_t kbase = static_cast<int64_t>(refill) * BKE;
         const uint32_t kbytes = static_cast<uint32_t>(refill) * C::ROW_BYTES;
         static_for<0, KS>([&](auto ksc) {
             constexpr int ks = decltype(ksc)::value;
@@ -466,7 +544,12 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
             static_for<0, MF>([&](auto tc) {
                 constexpr int t = decltype(tc)::value;
                 constexpr int i = t / C::TN, j = t % C::TN;
-                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[set][i], fb[set][j], acc[i][j], 0, 0, 0);
+                if constexpr (I8)
+                    acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(__builtin_bit_cast(i32x4, fa[set][i]),
+                                                                      __builtin_bit_cast(i32x4, fb[set][j]),
+                                                                      acc[i][j], 0, 0, 0);
+                else
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[set][i], fb[set][j], acc[i][j], 0, 0, 0);
                 static_for<t * FR / MF, (t + 1) * FR / MF>([&](auto rc) {
                     read_frag<C, decltype(rc)::value>(src + a_row_byte, src + C::A_BYTES + b_row_byte, tcol,
                                                       fa[tset], fb[tset]);
@@ -513,7 +596,7 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
 #pragma unroll
                     for (int q = 0; q < 4; ++q)
                         red[(((group - 1) * C::TILE_WAVES + wave) * NB + (i * C::TN + j) * 4 + q) * 64 + lane] =
-                            f32x4{acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+                            quad_bits(acc[i][j], q);
         }
         __syncthreads();
         if (group == 0) {
@@ -524,11 +607,8 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
                     for (int j = 0; j < C::TN; ++j)
 #pragma unroll
                         for (int q = 0; q < 4; ++q) {
-                            const f32x4 v = red[(((g - 1) * C::TILE_WAVES + wave) * NB + (i * C::TN + j) * 4 + q) * 64 + lane];
-                            acc[i][j][4 * q] += v[0];
-                            acc[i][j][4 * q + 1] += v[1];
-                            acc[i][j][4 * q + 2] += v[2];
-                            acc[i][j][4 * q + 3] += v[3];
+                            add_quad(acc[i][j], q,
+                                     red[(((g - 1) * C::TILE_WAVES + wave) * NB + (i * C::TN + j) * 4 + q) * 64 + lane]);
                         }
         }
         __syncthreads();   // the partials are read before LDS is reused
@@ -557,8 +637,7 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
                 for (int j = 0; j < C::TN; ++j)
 #pragma unroll
                     for (int q = 0; q < 4; ++q) {
-                        const f32x4 v = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
-                                         acc[i][j][4 * q + 3]};
+                        const f32x4 v = quad_bits(acc[i][j], q);
                         const uint32_t off = mine + (((wblk + i * C::TN + j) * 4 + q) * 64 + lane) * 16;
                         __builtin_amdgcn_raw_buffer_store_b128(v, rp, off, 0, AUX_SC1);
                     }
@@ -581,7 +660,7 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
 #pragma unroll
                 for (int j = 0; j < C::TN; ++j)
 #pragma unroll
-                    for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+                    for (int e = 0; e < 16; ++e) acc[i][j][e] = 0;
             // Small tiles: D slices per round trip (as many as 128 registers
             // hold); a slice past the last reads out of range and is not added,
             // so the sum still runs over the slices in order.  Large tiles
@@ -598,12 +677,9 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
 #pragma unroll
                             for (int q = 0; q < 4; ++q) {
                                 const uint32_t off = base + (((wblk + i * C::TN + j) * 4 + q) * 64 + lane) * 16;
-                                const f32x4 v = __builtin_bit_cast(
-                                    f32x4, __builtin_amdgcn_raw_buffer_load_b128(rp, off, 0, AUX_SC1));
-                                acc[i][j][4 * q] += v[0];
-                                acc[i][j][4 * q + 1] += v[1];
-                                acc[i][j][4 * q + 2] += v[2];
-                                acc[i][j][4 * q + 3] += v[3];
+                                add_quad(acc[i][j], q,
+                                         __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rp, off, 0,
+                                                                                                         AUX_SC1)));
                             }
                 }
             } else {
@@ -627,11 +703,7 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
                             for (int j = 0; j < C::TN; ++j)
 #pragma unroll
                                 for (int q = 0; q < 4; ++q) {
-                                    const f32x4 &w = v[d][(i * C::TN + j) * 4 + q];
-                                    acc[i][j][4 * q] += w[0];
-                                    acc[i][j][4 * q + 1] += w[1];
-                                    acc[i][j][4 * q + 2] += w[2];
-                                    acc[i][j][4 * q + 3] += w[3];
+                                    add_quad(acc[i][j], q, v[d][(i * C::TN + j) * 4 + q]);
                                 }
                     }
                 }
@@ -655,6 +727,8 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
 #pragma unroll
     for (int i = 0; i < C::TM; ++i) {
         if (owner && vec && has_r && i + 1 < C::TM) load_r(i + 1, rv[(i + 1) & 1]);
+        if constexpr (I8)
+            if (owner && i + 1 < C::TM) load_sx(i + 1);
         if (owner) {
             if constexpr (GLU) {
                 // Block 2j holds the gate sums and block 2j+1 the up sums of
@@ -662,15 +736,25 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
 #pragma unroll
                 for (int j = 0; j < C::TN / 2; ++j)
 #pragma unroll
-                    for (int e = 0; e < 16; ++e)
-                        ep[(8 * (e >> 2) + 4 * hi + (e & 3)) * EPS + j * 32 + frag_row] =
-                            silu_f32(acc[i][2 * j][e]) * acc[i][2 * j + 1][e];
+                    for (int e = 0; e < 16; ++e) {
+                        float g, u;
+                        if constexpr (I8) {
+                            const float sr = sxr[i & 1][e];
+                            g = static_cast<float>(acc[i][2 * j][e]) * (sr * swc[j]);
+                            u = static_cast<float>(acc[i][2 * j + 1][e]) * (sr * swc[C::TN / 2 + j]);
+                        } else {
+                            g = acc[i][2 * j][e];
+                            u = acc[i][2 * j + 1][e];
+                        }
+                        ep[(8 * (e >> 2) + 4 * hi + (e & 3)) * EPS + j * 32 + frag_row] = silu_f32(g) * u;
+                    }
             } else {
 #pragma unroll
                 for (int j = 0; j < C::TN; ++j)
 #pragma unroll
                     for (int e = 0; e < 16; ++e)
-                        ep[(8 * (e >> 2) + 4 * hi + (e & 3)) * EPS + j * 32 + frag_row] = acc[i][j][e];
+                        ep[(8 * (e >> 2) + 4 * hi + (e & 3)) * EPS + j * 32 + frag_row] =
+                            static_cast<float>(acc[i][j][e]);
             }
         }
         __syncthreads();
@@ -681,6 +765,11 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
                 float y[8];
 #pragma unroll
                 for (int t = 0; t < 8; ++t) y[t] = src[t];
+                if constexpr (I8 && !GLU) {
+                    const float sr = sxr[i & 1][v];
+#pragma unroll
+                    for (int t = 0; t < 8; ++t) y[t] *= sr * swc[t];
+                }
                 const uint32_t base = base_of(i, v);
                 if (vec) {
                     if constexpr (GEN) {
@@ -727,12 +816,13 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
 
 // Split-K arguments of one launch; false when a tail split cannot hand
 // the XCDs equal shares of both kinds of work.
-template <class C>
+// BKE: K elements per stage (C::BK for bf16 operands, 2 * C::BK for int8).
+template <class C, int BKE = C::BK>
 bool split_args(int64_t K, int64_t tiles, int split, int64_t full_tiles, const Workspace *ws, SplitK &sk) {
-    sk = SplitK{1, ((K + C::BK - 1) / C::BK) * C::BK, nullptr, nullptr, 0};
+    sk = SplitK{1, ((K + BKE - 1) / BKE) * BKE, nullptr, nullptr, 0};
     if (split > 1) {
         sk.split = split;
-        sk.kslice = (((K + split - 1) / split + C::BK - 1) / C::BK) * C::BK;
+        sk.kslice = (((K + split - 1) / split + BKE - 1) / BKE) * BKE;
         sk.partials = ws->partials;
         sk.counters = ws->counters;
         sk.full_tiles = full_tiles;
@@ -761,6 +851,20 @@ hipError_t launch_cfg(const Problem &p, int group_m, int split, int64_t full_til
     return hipGetLastError();
 }
 
+template <class C>
+hipError_t launch_cfg_i8(const I8Problem &p, int group_m, int split, int64_t full_tiles, const Workspace *ws,
+                         hipStream_t s) {
+    const int64_t tiles_m = (p.M + C::BM - 1) / C::BM;
+    const int64_t tiles_n = (p.N + C::BN - 1) / C::BN;
+    const int64_t tiles = tiles_m * tiles_n;
+    SplitK sk;
+    if (!split_args<C, 2 * C::BK>(p.K, tiles, split, full_tiles, ws, sk)) return hipErrorInvalidValue;
+    const int64_t wgs = sk.full_tiles + (tiles - sk.full_tiles) * sk.split;
+    hipLaunchKernelGGL((tile_kernel<C, I8Problem>), dim3(static_cast<unsigned>(wgs)), dim3(C::THREADS), 0, s, p,
+                       tiles_m, tiles_n, group_m, sk);
+    return hipGetLastError();
+}
+
 // SwiGLU needs an even number of 32-column blocks per wave (gate/up pairs)
 // and an even number of B loads per wave (half gate, half up).
 template <class C>
@@ -779,6 +883,24 @@ hipError_t launch_cfg_glu(const GluProblem &p, int group_m, int split, int64_t f
         if (!split_args<C>(p.K, tiles, split, full_tiles, ws, sk)) return hipErrorInvalidValue;
         const int64_t wgs = sk.full_tiles + (tiles - sk.full_tiles) * sk.split;
         hipLaunchKernelGGL((tile_kernel<C, GluProblem>), dim3(static_cast<unsigned>(wgs)), dim3(C::THREADS), 0, s,
+                           p, tiles_m, tiles_n, group_m, sk);
+        return hipGetLastError();
+    }
+}
+
+template <class C>
+hipError_t launch_cfg_i8_glu(const I8GluProblem &p, int group_m, int split, int64_t full_tiles, const Workspace *ws,
+                             hipStream_t s) {
+    if constexpr (!glu_ok<C>()) {
+        return hipErrorInvalidValue;
+    } else {
+        const int64_t tiles_m = (p.M + C::BM - 1) / C::BM;
+        const int64_t tiles_n = (p.N + C::BN / 2 - 1) / (C::BN / 2);
+        const int64_t tiles = tiles_m * tiles_n;
+        SplitK sk;
+        if (!split_args<C, 2 * C::BK>(p.K, tiles, split, full_tiles, ws, sk)) return hipErrorInvalidValue;
+        const int64_t wgs = sk.full_tiles + (tiles - sk.full_tiles) * sk.split;
+        hipLaunchKernelGGL((tile_kernel<C, I8GluProblem>), dim3(static_cast<unsigned>(wgs)), dim3(C::THREADS), 0, s,
                            p, tiles_m, tiles_n, group_m, sk);
         return hipGetLastError();
     }
@@ -883,6 +1005,24 @@ hipError_t launch_tile_glu(int cfg, const GluProblem &p, int split, int64_t full
         using C = decltype(c);
         if constexpr (std::is_same<C, std::nullptr_t>::value) return hipErrorInvalidValue;
         else return launch_cfg_glu<C>(p, 8, split, full_tiles, ws, s);
+    });
+}
+
+hipError_t launch_tile_i8(int cfg, const I8Problem &p, int split, int64_t full_tiles, const Workspace *ws,
+                          hipStream_t s) {
+    return with_cfg(cfg, [&](auto c, int) {
+        using C = decltype(c);
+        if constexpr (std::is_same<C, std::nullptr_t>::value) return hipErrorInvalidValue;
+        else return launch_cfg_i8<C>(p, 8, split, full_tiles, ws, s);
+    });
+}
+
+hipError_t launch_tile_i8_glu(int cfg, const I8GluProblem &p, int split, int64_t full_tiles, const Workspace *ws,
+                              hipStream_t s) {
+    return with_cfg(cfg, [&](auto c, int) {
+        using C = decltype(c);
+        if constexpr (std::is_same<C, std::nullptr_t>::value) return hipErrorInvalidValue;
+        else return launch_cfg_i8_glu<C>(p, 8, split, full_tiles, ws, s);
     });
 }
 

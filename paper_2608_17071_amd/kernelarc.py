@@ -50,6 +50,13 @@ _SIGS = {
     "kernelarc_swiglu_bf16_with_plan": (ctypes.c_int, [ctypes.c_int, _I64, _I64, _I64, _P, _P, _P, _P, _P]),
     "kernelarc_select_plan_swiglu": (ctypes.c_int, [_I64, _I64, _I64]),
     "kernelarc_plan_supports_swiglu": (ctypes.c_int, [ctypes.c_int, _I64, _I64, _I64]),
+    "kernelarc_gemm_i8": (ctypes.c_int, [_I64, _I64, _I64, _P, _P, _P, _P, _P, _P, _P]),
+    "kernelarc_gemm_i8_with_plan": (ctypes.c_int, [ctypes.c_int, _I64, _I64, _I64, _P, _P, _P, _P, _P, _P, _P]),
+    "kernelarc_swiglu_i8": (ctypes.c_int, [_I64, _I64, _I64, _P, _P, _P, _P, _P, _P, _P, _P]),
+    "kernelarc_swiglu_i8_with_plan": (ctypes.c_int, [ctypes.c_int, _I64, _I64, _I64, _P, _P, _P, _P, _P, _P, _P,
+                                                     _P]),
+    "kernelarc_select_plan_i8": (ctypes.c_int, [_I64, _I64, _I64, ctypes.c_int]),
+    "kernelarc_plan_supports_i8": (ctypes.c_int, [ctypes.c_int, _I64, _I64, _I64, ctypes.c_int]),
     "kernelarc_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "kernelarc_last_error": (ctypes.c_char_p, []),
 }
@@ -245,3 +252,78 @@ def select_plan_swiglu(M: int, N: int, K: int) -> int:
 
 def plan_supports_swiglu(plan: int, M: int, N: int, K: int) -> bool:
     return _lib.kernelarc_plan_supports_swiglu(plan, M, N, K) == 1
+
+
+def _i8_operand(t, name, shape, device):
+    if t.dtype != torch.int8 or not t.is_cuda or not t.is_contiguous() or tuple(t.shape) != shape:
+        raise ValueError(f"{name} must be a contiguous int8 GPU tensor of shape {shape}")
+    if t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+
+
+def _scales(t, name, n, device):
+    if t.dtype != torch.float32 or not t.is_cuda or not t.is_contiguous() or tuple(t.shape) != (n,):
+        raise ValueError(f"{name} must be a contiguous float32 GPU tensor of shape ({n},)")
+    if t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+
+
+def gemm_i8(qx, sx, qw, sw, r=None, out=None, stream=None, plan=None):
+    """Y = bf16(sx[i] sw[j] (qX qW^T)[i,j] (+ R)): int8 qx [M, K] and qw [N, K],
+    float32 per-row scales sx [M] and per-output-channel scales sw [N],
+    optional bf16 residual r [M, N]; out may be r (in place)."""
+    if qx.dim() != 2 or qw.dim() != 2 or qx.shape[1] != qw.shape[1]:
+        raise ValueError("qx must be [M, K] and qw [N, K]")
+    M, K = qx.shape
+    N = qw.shape[0]
+    dev = qx.device
+    _i8_operand(qx, "qx", (M, K), dev)
+    _i8_operand(qw, "qw", (N, K), dev)
+    _scales(sx, "sx", M, dev)
+    _scales(sw, "sw", N, dev)
+    for name, t in (("r", r), ("out", out)):
+        if t is not None and (t.dtype != torch.bfloat16 or not t.is_cuda or not t.is_contiguous()
+                              or tuple(t.shape) != (M, N) or t.device != dev):
+            raise ValueError(f"{name} must be a contiguous bfloat16 GPU tensor of shape {(M, N)}")
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+    args = (M, N, K, qx.data_ptr(), sx.data_ptr(), qw.data_ptr(), sw.data_ptr(),
+            r.data_ptr() if r is not None else None, out.data_ptr(), _stream_handle(stream))
+    with torch.cuda.device(dev):
+        st = _lib.kernelarc_gemm_i8(*args) if plan is None else _lib.kernelarc_gemm_i8_with_plan(plan, *args)
+    _check(st, "kernelarc_gemm_i8" if plan is None else f"kernelarc_gemm_i8_with_plan({plan_name(plan)})")
+    return out
+
+
+def swiglu_i8(qx, sx, qwg, swg, qwu, swu, out=None, stream=None, plan=None):
+    """H = bf16(silu(sx swg (qX qWg^T)) * (sx swu (qX qWu^T))) with int8 operands
+    and float32 scales (per row of qx, per output channel of each weight)."""
+    if qx.dim() != 2 or qwg.dim() != 2 or qx.shape[1] != qwg.shape[1]:
+        raise ValueError("qx must be [M, K] and qwg, qwu [N, K]")
+    M, K = qx.shape
+    N = qwg.shape[0]
+    dev = qx.device
+    _i8_operand(qx, "qx", (M, K), dev)
+    _i8_operand(qwg, "qwg", (N, K), dev)
+    _i8_operand(qwu, "qwu", (N, K), dev)
+    _scales(sx, "sx", M, dev)
+    _scales(swg, "swg", N, dev)
+    _scales(swu, "swu", N, dev)
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+    elif out.dtype != torch.bfloat16 or not out.is_contiguous() or tuple(out.shape) != (M, N) or out.device != dev:
+        raise ValueError(f"out must be a contiguous bfloat16 GPU tensor of shape {(M, N)}")
+    args = (M, N, K, qx.data_ptr(), sx.data_ptr(), qwg.data_ptr(), swg.data_ptr(), qwu.data_ptr(), swu.data_ptr(),
+            out.data_ptr(), _stream_handle(stream))
+    with torch.cuda.device(dev):
+        st = _lib.kernelarc_swiglu_i8(*args) if plan is None else _lib.kernelarc_swiglu_i8_with_plan(plan, *args)
+    _check(st, "kernelarc_swiglu_i8" if plan is None else f"kernelarc_swiglu_i8_with_plan({plan_name(plan)})")
+    return out
+
+
+def select_plan_i8(M: int, N: int, K: int, swiglu: bool = False) -> int:
+    return _lib.kernelarc_select_plan_i8(M, N, K, int(swiglu))
+
+
+def plan_supports_i8(plan: int, M: int, N: int, K: int, swiglu: bool = False) -> bool:
+    return _lib.kernelarc_plan_supports_i8(plan, M, N, K, int(swiglu)) == 1

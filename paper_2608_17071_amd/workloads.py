@@ -185,6 +185,73 @@ def make_glu_inputs(w: GluWorkload) -> dict:
     return {"X": X, "Wg": Wg, "Wu": Wu}
 
 
+# ---- INT8 with dequantisation scales ----------------------------------------
+
+@dataclass(frozen=True)
+class I8Workload:
+    """An INT8 call: qX [M,K], qW (or qWg, qWu) [N,K] int8 with float32 scales
+    per row of qX and per output channel; a bf16 residual when `residual`;
+    SwiGLU when `swiglu`."""
+    name: str
+    M: int
+    N: int
+    K: int
+    swiglu: bool
+    residual: bool
+    seed: int
+
+    @property
+    def flops(self) -> int:
+        """Integer multiply-adds counted as 2 operations (4MNK for SwiGLU)."""
+        return (4 if self.swiglu else 2) * self.M * self.N * self.K
+
+    @property
+    def algorithmic_bytes(self) -> int:
+        """int8 operands and float32 scales read once, bf16 output written once."""
+        w = 2 if self.swiglu else 1
+        b = self.M * self.K + w * self.N * self.K + 4 * self.M + 4 * w * self.N + 2 * self.M * self.N
+        if self.residual:
+            b += 2 * self.M * self.N
+        return b
+
+
+# The precision axis of the same layers: the o-proj / down-proj site with a
+# residual (prefill and decode), the large square GEMM, and the decoder
+# layer's INT8 gate/up path, which the paper takes from M = 1000 tokens up.
+I8 = (
+    I8Workload("i8_decode_m16_h4096", 16, 4096, 4096, False, True, 301),
+    I8Workload("i8_prefill_m4096_h4096", 4096, 4096, 4096, False, True, 302),
+    I8Workload("i8_square_8192", 8192, 8192, 8192, False, False, 303),
+    I8Workload("swiglu_i8_m1024_h5120_i13824", 1024, 13824, 5120, True, False, 304),
+    I8Workload("swiglu_i8_prefill_m4096_h4096_i14336", 4096, 14336, 4096, True, False, 305),
+)
+I8_BY_NAME = {w.name: w for w in I8}
+
+
+def make_i8_inputs(w: I8Workload) -> dict:
+    """Draw, from one seed and in this order: qX = round(N(0,1) * 40) clipped
+    to [-128, 127] (int8); the weight(s) the same way; sx ~ U(0.5, 1.5)/40 per
+    row; per-channel scales ~ U(0.5, 1.5)/(40 sqrt(K)) per weight; R ~ N(0,1)
+    in bf16 when the workload has a residual.  The dequantised sums are then
+    about N(0,1) (the gate spans SiLU's curved range)."""
+    g = torch.Generator().manual_seed(w.seed)
+
+    def q(shape):
+        return torch.clamp(torch.round(torch.randn(shape, generator=g) * 40.0), -128, 127).to(torch.int8)
+
+    qx = q((w.M, w.K))
+    ws = [q((w.N, w.K)) for _ in range(2 if w.swiglu else 1)]
+    sx = ((torch.rand(w.M, generator=g) + 0.5) / 40.0).to(torch.float32)
+    kscale = 40.0 * math.sqrt(w.K) if w.K > 0 else 40.0
+    ss = [((torch.rand(w.N, generator=g) + 0.5) / kscale).to(torch.float32) for _ in ws]
+    out = {"qX": qx, "sx": sx, "qW": ws[0], "sw": ss[0], "R": None}
+    if w.swiglu:
+        out["qWu"], out["swu"] = ws[1], ss[1]
+    if w.residual:
+        out["R"] = torch.randn((w.M, w.N), generator=g).to(torch.bfloat16)
+    return out
+
+
 def custom(M: int, N: int, K: int, residual: bool = True, dist: str = "normal",
            seed: int = 0, name: str | None = None) -> Workload:
     return Workload(name or f"custom_m{M}_n{N}_k{K}", M, N, K, residual, dist, seed)

@@ -200,3 +200,35 @@ def test_swiglu_plans(ka):
         assert ka.plan_supports_swiglu(names.index(n), 64, 1024, 1024), n
     assert not ka.plan_supports_swiglu(names.index("tile_256x256_k64_w8"), 64, 1024, 1020)   # K % 8
     assert ka.kernelarc_plan_supports_swiglu(999, 1, 1, 1) == -1
+
+
+def test_i8_validation_and_plans(ka):
+    f = ka.kernelarc_gemm_i8
+    buf = (ctypes.c_uint8 * 16384)()
+    base = ctypes.addressof(buf)
+    X, W, SX, SW, Y = base, base + 2048, base + 4096, base + 4608, base + 8192
+    # (M, N, K, qX, sx, qW, sw, R, Y, stream)
+    assert f(-1, 4, 16, X, SX, W, SW, None, Y, None) == ka.ERR_INVALID_ARG
+    assert f(4, 4, 65536 + 16, X, SX, W, SW, None, Y, None) == ka.ERR_INVALID_ARG      # int32 range
+    assert ka.kernelarc_last_error().startswith(b"K=")
+    assert f(4, 4, 16, X, None, W, SW, None, Y, None) == ka.ERR_INVALID_ARG            # NULL scale
+    assert f(4, 4, 16, X, SX + 2, W, SW, None, Y, None) == ka.ERR_INVALID_ARG          # misaligned scale
+    assert f(4, 4, 16, X, SX, W, SW, None, X + 8, None) == ka.ERR_INVALID_ARG          # Y overlaps qX
+    assert f(4, 4, 16, X, SX, W, SW, None, SW, None) == ka.ERR_INVALID_ARG             # Y overlaps sw
+    assert f(4, 4, 16, X, SX, W, SW, Y + 2, Y, None) == ka.ERR_INVALID_ARG             # partial Y/R overlap
+    assert f(0, 4, 16, None, None, None, None, None, None, None) == ka.OK
+    g = ka.kernelarc_swiglu_i8
+    assert g(4, 4, 16, X, SX, W, SW, W, None, Y, None) == ka.ERR_INVALID_ARG           # NULL up scales
+    names = ka.plan_names()
+    gen = names.index("generic_64x64_scalar")
+    assert ka.select_plan_i8(64, 128, 40) == gen                                        # K % 16
+    for (M, N, K, glu) in [(16, 4096, 4096, 0), (4096, 4096, 4096, 0), (8192, 8192, 8192, 0),
+                           (1024, 13824, 5120, 1), (4096, 14336, 4096, 1), (1, 64, 16, 0), (300, 77, 1024, 1)]:
+        p = ka.select_plan_i8(M, N, K, glu)
+        assert ka.plan_supports_i8(p, M, N, K, glu), (M, N, K, glu, names[p])
+        assert names[p].startswith("tile"), (M, N, K, glu, names[p])
+    for n in ("stream_mfma16_k64_splitk", "gemv_valu_w4", "skinny_mfma16_w8"):
+        assert not ka.plan_supports_i8(names.index(n), 16, 1024, 1024)
+    assert not ka.plan_supports_i8(names.index("tile_64x64_k64_w4"), 64, 1024, 1024, True)
+    assert ka.plan_supports_i8(names.index("tile_64x64_k64_w4"), 64, 1024, 1024, False)
+    assert not ka.plan_supports_i8(names.index("tile_256x256_k64_w8"), 64, 1024, 1032)  # K % 16
