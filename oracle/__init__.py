@@ -1,7 +1,8 @@
 """CPU oracle for Y = X.W^T + R, its general form
 D = alpha.X.W^T + beta.C + bias, the gated MLP input projection
-H = silu(X.Wg^T) * (X.Wu^T), and their INT8 forms with per-row and
-per-column dequantisation scales (TEST INFRASTRUCTURE ONLY).
+H = silu(X.Wg^T) * (X.Wu^T), their INT8 forms with per-row and per-column
+dequantisation scales, and grouped (per-expert) forms over an expert-major
+padded layout (TEST INFRASTRUCTURE ONLY).
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
 ``bench.py`` may import this package.  The GPU library never imports, links
@@ -75,6 +76,13 @@ class Oracle:
         lib.ka_oracle_i8_swiglu.restype = ctypes.c_int
         lib.ka_oracle_i8_swiglu_at.argtypes = [_I64, _I64, _I64, _P, _P, _P, _P, _P, _P, _I64, _P, _P, _P]
         lib.ka_oracle_i8_swiglu_at.restype = ctypes.c_int
+        lib.ka_oracle_grouped_linear.argtypes = [_I64, _I64, _I64, _I64, _P, _P, _P, _P]
+        lib.ka_oracle_grouped_linear.restype = ctypes.c_int
+        lib.ka_oracle_grouped_swiglu.argtypes = [_I64, _I64, _I64, _I64, _P, _P, _P, _P, _P]
+        lib.ka_oracle_grouped_swiglu.restype = ctypes.c_int
+        lib.ka_oracle_grouped_at.argtypes = [_I64, _I64, _I64, _I64, _P, _P, _P, _P, ctypes.c_int, _I64, _P, _P,
+                                             _P, _P]
+        lib.ka_oracle_grouped_at.restype = ctypes.c_int
         lib.ka_oracle_round_bf16.argtypes = [_I64, _P, _P]
         lib.ka_oracle_round_bf16.restype = None
         lib.ka_oracle_threads.argtypes = []
@@ -315,6 +323,60 @@ class Oracle:
                                            out.ctypes.data) != 0:
             raise ValueError("oracle rejected its arguments")
         del keep
+        return out
+
+    # ---- grouped (per-expert) forms ------------------------------------------
+    def _grouped_args(self, X, W, W2, counts):
+        E, Mpad, K = X.shape
+        N = W.shape[1]
+        X = self._bits(X, (E, Mpad, K))
+        W = self._bits(W, (E, N, K))
+        if W2 is not None:
+            W2 = self._bits(W2, (E, N, K))
+        cp = None
+        if counts is not None:
+            counts = np.ascontiguousarray(counts)
+            if counts.dtype != np.int32 or counts.shape != (E,):
+                raise ValueError("counts: expected int32 of shape (E,)")
+            cp = counts.ctypes.data
+        return (E, Mpad, N, K), (X, W, W2, counts), cp
+
+    def grouped_linear(self, X, W, counts=None, out=None) -> np.ndarray:
+        """Y[e,i,:] = X[e,i,:] W[e]^T for the valid rows i < counts[e] of each
+        expert (float64); the other rows of `out` (default: NaN) are untouched."""
+        (E, Mpad, N, K), keep, cp = self._grouped_args(X, W, None, counts)
+        Y = np.full((E, Mpad, N), np.nan) if out is None else out
+        if Y.dtype != np.float64 or Y.shape != (E, Mpad, N) or not Y.flags.c_contiguous:
+            raise ValueError("out: expected a contiguous float64 array of shape (E, M_pad, N)")
+        if self.lib.ka_oracle_grouped_linear(E, Mpad, N, K, keep[0].ctypes.data, keep[1].ctypes.data, cp,
+                                             Y.ctypes.data) != 0:
+            raise ValueError("oracle rejected its arguments")
+        return Y
+
+    def grouped_swiglu(self, X, Wg, Wu, counts=None, out=None) -> np.ndarray:
+        """H[e,i,:] = silu(X[e,i,:] Wg[e]^T) * (X[e,i,:] Wu[e]^T) for the valid rows."""
+        (E, Mpad, N, K), keep, cp = self._grouped_args(X, Wg, Wu, counts)
+        H = np.full((E, Mpad, N), np.nan) if out is None else out
+        if H.dtype != np.float64 or H.shape != (E, Mpad, N) or not H.flags.c_contiguous:
+            raise ValueError("out: expected a contiguous float64 array of shape (E, M_pad, N)")
+        if self.lib.ka_oracle_grouped_swiglu(E, Mpad, N, K, keep[0].ctypes.data, keep[1].ctypes.data,
+                                             keep[2].ctypes.data, cp, H.ctypes.data) != 0:
+            raise ValueError("oracle rejected its arguments")
+        return H
+
+    def grouped_at(self, X, W, W2, counts, groups, rows, cols) -> np.ndarray:
+        """Either grouped form (SwiGLU when W2 is given) at (groups[t], rows[t], cols[t])."""
+        (E, Mpad, N, K), keep, cp = self._grouped_args(X, W, W2, counts)
+        groups = np.ascontiguousarray(groups, dtype=np.int64)
+        rows, cols = self._positions(rows, cols)
+        if groups.shape != rows.shape:
+            raise ValueError("groups, rows and cols must have equal length")
+        out = np.empty(rows.shape[0], dtype=np.float64)
+        w2 = keep[2].ctypes.data if keep[2] is not None else None
+        if self.lib.ka_oracle_grouped_at(E, Mpad, N, K, keep[0].ctypes.data, keep[1].ctypes.data, w2, cp,
+                                         int(W2 is not None), rows.shape[0], groups.ctypes.data, rows.ctypes.data,
+                                         cols.ctypes.data, out.ctypes.data) != 0:
+            raise ValueError("oracle rejected its arguments")
         return out
 
     def threads(self) -> int:

@@ -6,7 +6,8 @@
  * its general form (alpha, beta, bias, leading dimensions), the gated
  * MLP input projection H = silu(X Wg^T) * (X Wu^T) (SwiGLU), and INT8
  * versions of the linear layer and of SwiGLU with per-row and per-column
- * dequantisation scales.
+ * dequantisation scales, and grouped (per-expert) forms of the linear layer
+ * and of SwiGLU over an expert-major padded layout.
  *
  * TEST INFRASTRUCTURE ONLY.  This file is the slow, obviously correct
  * reference that the GPU library is checked against.  Only the test suite,
@@ -388,6 +389,93 @@ int ka_oracle_i8_swiglu_at(int64_t M, int64_t N, int64_t K, const int8_t *qX, co
 #pragma omp parallel for schedule(dynamic, 16)
     for (int64_t t = 0; t < n; ++t)
         out[t] = element_i8_swiglu(rows[t], cols[t], K, qX, sx, qWg, swg, qWu, swu);
+    return 0;
+}
+
+/*
+ * Grouped (batched) linear layer over an expert-major padded layout
+ * (mixture-of-experts case study, Alg. 4: token-expert pairs are placed in
+ * expert-contiguous rows of a [E x M_pad] buffer, gap rows zero-filled, and
+ * every projection runs as one strided-batched GEMM).  Expert e owns rows
+ * [e*M_pad, (e+1)*M_pad) of X and Y and its own weight W[e]:
+ *
+ *     Y[e,i,j] = sum_k X[e,i,k] W[e,j,k]            for i < rows(e)
+ *     H[e,i,j] = silu(X[e,i,:].Wg[e,j,:]) * (X[e,i,:].Wu[e,j,:])   (SwiGLU form)
+ *
+ * X is [E,M_pad,K], W (Wg, Wu) [E,N,K], Y (H) [E,M_pad,N], bf16 patterns;
+ * counts[e] is the number of valid rows of expert e, clamped to [0, M_pad]
+ * (NULL: every row is valid).  Rows at or past rows(e) are not computed and
+ * their outputs are left as they were (the gap rows).  Each valid element is
+ * the plain (or SwiGLU) definition above, in double, not rounded.
+ */
+static int64_t group_rows(const int32_t *counts, int64_t e, int64_t Mpad)
+{
+    if (!counts) return Mpad;
+    int64_t c = counts[e];
+    return c < 0 ? 0 : (c > Mpad ? Mpad : c);
+}
+
+static int check_grouped(int64_t E, int64_t Mpad, int64_t N, int64_t K, const void *X, const void *W)
+{
+    if (E < 0 || Mpad < 0 || N < 0 || K < 0) return -1;
+    if (E * Mpad * K > 0 && !X) return -1;
+    if (E * N * K > 0 && !W) return -1;
+    return 0;
+}
+
+int ka_oracle_grouped_linear(int64_t E, int64_t Mpad, int64_t N, int64_t K, const uint16_t *X,
+                             const uint16_t *W, const int32_t *counts, double *Y)
+{
+    if (check_grouped(E, Mpad, N, K, X, W) != 0) return -1;
+    if (E * Mpad * N > 0 && !Y) return -1;
+#pragma omp parallel for collapse(2) schedule(dynamic, 1)
+    for (int64_t e = 0; e < E; ++e)
+        for (int64_t i = 0; i < Mpad; ++i) {
+            if (i >= group_rows(counts, e, Mpad)) continue;
+            for (int64_t j = 0; j < N; ++j)
+                Y[(e * Mpad + i) * N + j] = element(i, j, N, K, X + e * Mpad * K, W + e * N * K, NULL);
+        }
+    return 0;
+}
+
+int ka_oracle_grouped_swiglu(int64_t E, int64_t Mpad, int64_t N, int64_t K, const uint16_t *X,
+                             const uint16_t *Wg, const uint16_t *Wu, const int32_t *counts, double *H)
+{
+    if (check_grouped(E, Mpad, N, K, X, Wg) != 0 || check_grouped(E, Mpad, N, K, X, Wu) != 0) return -1;
+    if (E * Mpad * N > 0 && !H) return -1;
+#pragma omp parallel for collapse(2) schedule(dynamic, 1)
+    for (int64_t e = 0; e < E; ++e)
+        for (int64_t i = 0; i < Mpad; ++i) {
+            if (i >= group_rows(counts, e, Mpad)) continue;
+            for (int64_t j = 0; j < N; ++j)
+                H[(e * Mpad + i) * N + j] =
+                    element_swiglu(i, j, K, X + e * Mpad * K, Wg + e * N * K, Wu + e * N * K);
+        }
+    return 0;
+}
+
+/*
+ * Either grouped form at the n positions (groups[t], rows[t], cols[t]); a
+ * position in a gap row is an error (-1).  swiglu != 0 selects the SwiGLU
+ * form (W2 the up weights), else the plain form (W2 unused).
+ */
+int ka_oracle_grouped_at(int64_t E, int64_t Mpad, int64_t N, int64_t K, const uint16_t *X,
+                         const uint16_t *W, const uint16_t *W2, const int32_t *counts, int swiglu,
+                         int64_t n, const int64_t *groups, const int64_t *rows, const int64_t *cols,
+                         double *out)
+{
+    if (check_grouped(E, Mpad, N, K, X, W) != 0 || n < 0) return -1;
+    if (swiglu && check_grouped(E, Mpad, N, K, X, W2) != 0) return -1;
+    for (int64_t t = 0; t < n; ++t)
+        if (groups[t] < 0 || groups[t] >= E || rows[t] < 0 || rows[t] >= group_rows(counts, groups[t], Mpad) ||
+            cols[t] < 0 || cols[t] >= N)
+            return -1;
+#pragma omp parallel for schedule(dynamic, 16)
+    for (int64_t t = 0; t < n; ++t) {
+        const int64_t e = groups[t];
+        out[t] = swiglu ? element_swiglu(rows[t], cols[t], K, X + e * Mpad * K, W + e * N * K, W2 + e * N * K)
+                        : element(rows[t], cols[t], N, K, X + e * Mpad * K, W + e * N * K, NULL);
+    }
     return 0;
 }
 

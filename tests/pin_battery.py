@@ -38,6 +38,13 @@ random binary32 scales, reduction to the bf16 oracles (already pinned) when
 power-of-two scales make every dequantised operand an exact bf16 value, a
 zero weight, and the 60-digit decimal SiLU.
 
+The grouped forms over an expert-major padded layout (``GRP_PINS``: per
+expert e, Y[e,i] = X[e,i] W[e]^T for the rows i below counts[e] clamped to
+[0, M_pad]) are pinned by exact rational brute force with empty, partial,
+full, negative and oversized counts, by reduction expert by expert to the
+(pinned) plain and SwiGLU oracles, by gap rows left exactly as they were,
+and by expert permutations.
+
 ``ALL_PINS`` is run against the real oracle (all must pass) and against
 copies of the oracle with a planted mistake (at least one must fail).
 """
@@ -677,6 +684,102 @@ I8_PINS = [
     pin_i8_at_matches_full,
 ]
 
+# ---------------------------------------------------------------- grouped ----
+def _rows_of(counts, e, Mpad):
+    return Mpad if counts is None else int(min(max(int(counts[e]), 0), Mpad))
+
+
+def pin_grouped_exact_bruteforce(orc, trials=12, seed=51):
+    rng = np.random.default_rng(seed)
+    for t in range(trials):
+        E, Mpad, N, K = (int(v) for v in rng.integers(1, 6, size=4))
+        X = _rand_bits(rng, (E, Mpad, K))
+        W = _rand_bits(rng, (E, N, K))
+        counts = None if t % 4 == 0 else rng.integers(-2, Mpad + 3, size=E).astype(np.int32)
+        Y = orc.grouped_linear(X, W, counts)
+        xf, wf = bf16_bits_to_f64(X), bf16_bits_to_f64(W)
+        for e in range(E):
+            r = _rows_of(counts, e, Mpad)
+            assert np.isnan(Y[e, r:]).all()
+            for i in range(r):
+                for j in range(N):
+                    exact = sum((Fraction(xf[e, i, k]) * Fraction(wf[e, j, k]) for k in range(K)), Fraction(0))
+                    mag = sum(abs(Fraction(xf[e, i, k]) * Fraction(wf[e, j, k])) for k in range(K))
+                    assert abs(Fraction(Y[e, i, j]) - exact) <= mag / 2**50, (e, i, j)
+
+
+def pin_grouped_reduces_per_expert(orc, seed=52):
+    """Expert by expert, the valid rows equal the plain and SwiGLU oracles bit for bit."""
+    rng = np.random.default_rng(seed)
+    E, Mpad, N, K = 5, 9, 7, 33
+    X = _rand_bits(rng, (E, Mpad, K), 2.0)
+    W = _rand_bits(rng, (E, N, K), 1.0 / np.sqrt(K))
+    Wu = _rand_bits(rng, (E, N, K), 1.0 / np.sqrt(K))
+    counts = np.array([0, 3, 9, 12, -1], np.int32)
+    Y = orc.grouped_linear(X, W, counts)
+    H = orc.grouped_swiglu(X, W, Wu, counts)
+    for e in range(E):
+        r = _rows_of(counts, e, Mpad)
+        if r:
+            np.testing.assert_array_equal(Y[e, :r], orc.linear(X[e, :r], W[e]))
+            np.testing.assert_array_equal(H[e, :r], orc.swiglu(X[e, :r], W[e], Wu[e]))
+    np.testing.assert_array_equal(orc.grouped_linear(X, W)[2], orc.linear(X[2], W[2]))
+
+
+def pin_grouped_gap_rows_untouched(orc, seed=53):
+    rng = np.random.default_rng(seed)
+    E, Mpad, N, K = 4, 6, 5, 8
+    X = _rand_bits(rng, (E, Mpad, K))
+    W = _rand_bits(rng, (E, N, K))
+    counts = np.array([2, 0, 6, 4], np.int32)
+    out = np.full((E, Mpad, N), 12345.5)
+    orc.grouped_linear(X, W, counts, out=out)
+    for e in range(E):
+        r = int(counts[e])
+        assert (out[e, r:] == 12345.5).all()
+        assert not (out[e, :r] == 12345.5).any()
+
+
+def pin_grouped_expert_permutation(orc, seed=54):
+    rng = np.random.default_rng(seed)
+    E, Mpad, N, K = 6, 5, 4, 12
+    X = _rand_bits(rng, (E, Mpad, K))
+    W = _rand_bits(rng, (E, N, K))
+    counts = rng.integers(0, Mpad + 1, size=E).astype(np.int32)
+    pe = rng.permutation(E)
+    np.testing.assert_array_equal(orc.grouped_linear(X[pe], W[pe], counts[pe]),
+                                  orc.grouped_linear(X, W, counts)[pe])
+
+
+def pin_grouped_at_matches_full(orc, seed=55):
+    rng = np.random.default_rng(seed)
+    E, Mpad, N, K = 4, 7, 6, 10
+    X = _rand_bits(rng, (E, Mpad, K))
+    W = _rand_bits(rng, (E, N, K))
+    Wu = _rand_bits(rng, (E, N, K))
+    counts = np.array([7, 2, 5, 1], np.int32)
+    full, fullh = orc.grouped_linear(X, W, counts), orc.grouped_swiglu(X, W, Wu, counts)
+    g = rng.integers(0, E, 60)
+    r = np.array([rng.integers(0, counts[e]) for e in g])
+    c = rng.integers(0, N, 60)
+    np.testing.assert_array_equal(orc.grouped_at(X, W, None, counts, g, r, c), full[g, r, c])
+    np.testing.assert_array_equal(orc.grouped_at(X, W, Wu, counts, g, r, c), fullh[g, r, c])
+    try:
+        orc.grouped_at(X, W, None, counts, [1], [2], [0])      # row 2 of expert 1 is a gap row
+    except ValueError:
+        pass
+    else:
+        raise AssertionError("a gap-row position was accepted")
+
+
+GRP_PINS = [
+    pin_grouped_exact_bruteforce,
+    pin_grouped_reduces_per_expert,
+    pin_grouped_gap_rows_untouched,
+    pin_grouped_expert_permutation,
+    pin_grouped_at_matches_full,
+]
+
 ALL_PINS = [
     pin_exact_bruteforce,
     pin_golden_hand_worked,
@@ -690,4 +793,4 @@ ALL_PINS = [
     pin_round_midpoints,
     pin_round_specials,
     pin_round_like_torch,
-] + EX_PINS + GLU_PINS + I8_PINS
+] + EX_PINS + GLU_PINS + I8_PINS + GRP_PINS

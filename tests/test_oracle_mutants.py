@@ -51,6 +51,15 @@ MUTANTS = {
     "i8_residual_dropped": ("    if (R)\n        y += bf16_bits_to_double(R[i * N + j]);", "    (void)R;"),
     "i8_glu_up_scale_from_gate": ("double u = (double)sx[i] * (double)swu[j]", "double u = (double)sx[i] * (double)swg[j]"),
     "i8_glu_float_gate": ("    double g = (double)sx[i] * (double)swg[j]", "    float g = (double)sx[i] * (double)swg[j]"),
+    "grp_counts_ignored": ("            if (i >= group_rows(counts, e, Mpad)) continue;\n", "            (void)0;\n"),
+    "grp_weight_stride": ("element(i, j, N, K, X + e * Mpad * K, W + e * N * K, NULL);",
+                          "element(i, j, N, K, X + e * Mpad * K, W + (e / 2) * N * K, NULL);"),
+    "grp_x_stride": ("element(i, j, N, K, X + e * Mpad * K, W + e * N * K, NULL);",
+                     "element(i, j, N, K, X + e * K, W + e * N * K, NULL);"),
+    "grp_swiglu_up_from_gate": ("element_swiglu(i, j, K, X + e * Mpad * K, Wg + e * N * K, Wu + e * N * K);",
+                                "element_swiglu(i, j, K, X + e * Mpad * K, Wg + e * N * K, Wg + e * N * K);"),
+    "grp_negative_counts_unclamped": ("return c < 0 ? 0 : (c > Mpad ? Mpad : c);",
+                                      "return c < 0 ? Mpad : (c > Mpad ? Mpad : c);"),
 }
 
 
