@@ -27,7 +27,8 @@ three single-shape gates (decode M=16, prefill 4096^3, square 8192^3 plain),
 the general form (alpha, beta, bias, row strides), SwiGLU (the decoder
 layer's gate/up projections with the SiLU-multiply fused) and the INT8 forms
 (W8A8 with dequantisation, INT8 SwiGLU; against the int8 MFMA peak) on
-decoder-layer shapes are extra fields of the same line.
+decoder-layer shapes, and the grouped mixture-of-experts projections are
+extra fields of the same line.
 """
 from __future__ import annotations
 
@@ -56,7 +57,7 @@ def log(msg):
 
 def mfma_peak(w):
     """Dense MFMA peak (T op/s) of the workload's operand type."""
-    return PEAK_I8_TOPS if hasattr(w, "swiglu") else PEAK_BF16_TFLOPS
+    return PEAK_I8_TOPS if getattr(w, "int8", False) else PEAK_BF16_TFLOPS
 
 
 def roofline_time(w):
@@ -273,6 +274,75 @@ class I8Case(Case):
             ka.gemm_i8(d["qX"], d["sx"], d["qW"], d["sw"], d["R"], out=d["Y"], plan=self.forced)
 
 
+class GroupedCase(Case):
+    """A grouped (per-expert) workload over an expert-major padded layout."""
+
+    def __init__(self, w, ka, torch, rotate=True, plan=None):
+        from paper_2608_17071_amd import workloads as wl
+        t = wl.make_grouped_inputs(w, device="cuda")
+        self.w = w
+        self.host = t          # device tensors; the CPU baseline copies the experts it samples
+        self.Mpad = t["Mpad"]
+        dev = {k: t[k] for k in ("X", "W", "Wu", "counts") if k in t}
+        n = 1
+        if rotate:
+            n = max(2, min(MAX_COPIES, -(-ROTATE_BYTES // w.algorithmic_bytes)))
+        self.sets = []
+        for i in range(n):
+            d = {k: (v if i == 0 else v.clone()) for k, v in dev.items()}
+            d["Y"] = torch.empty((w.G, self.Mpad, w.N), dtype=torch.bfloat16, device="cuda")
+            self.sets.append(d)
+        self.forced = plan
+        self.plan = ka.select_plan_grouped(w.G, self.Mpad, w.N, w.K, w.swiglu) if plan is None else plan
+        self.plan_name = ka.plan_name(self.plan)
+        self.times = []
+        self.graph = None
+
+    def call(self, ka, i):
+        d = self.sets[i]
+        if self.w.swiglu:
+            ka.swiglu_bf16_grouped(d["X"], d["W"], d["Wu"], d["counts"], out=d["Y"], plan=self.forced)
+        else:
+            ka.gemm_bf16_grouped(d["X"], d["W"], d["counts"], out=d["Y"], plan=self.forced)
+
+
+def cpu_baseline_grouped(cases, seconds):
+    """The oracle's grouped forms on whole experts 0, 1, ... of each case until
+    its time share is used."""
+    import numpy as np
+    import oracle
+    from paper_2608_17071_amd import workloads as wl
+
+    orc = oracle.default()
+    per_shape = seconds / len(cases)
+    rates, done = [], []
+    for c in cases:
+        w, h = c.w, c.host
+        E = min(w.G, 16)              # the sample never reaches further; only these are copied
+        xb, wb = wl.bits(h["X"][:E].cpu()), wl.bits(h["W"][:E].cpu())
+        ub = wl.bits(h["Wu"][:E].cpu()) if w.swiglu else None
+        cnt = h["counts"][:E].cpu().numpy()
+        ops, e, t0 = 0, 0, time.perf_counter()
+        while e < E:
+            r = int(cnt[e])
+            if r:
+                gi = np.full(r * w.N, e, dtype=np.int64)
+                ri = np.repeat(np.arange(r, dtype=np.int64), w.N)
+                ci = np.tile(np.arange(w.N, dtype=np.int64), r)
+                orc.grouped_at(xb, wb, ub, cnt, gi, ri, ci)
+                ops += (4 if w.swiglu else 2) * r * w.N * w.K
+            e += 1
+            if time.perf_counter() - t0 >= per_shape:
+                break
+        rates.append(ops / (time.perf_counter() - t0) / 1e12)
+        done.append(e)
+    return {
+        "value": geomean(rates), "unit": "TFLOP/s (fp64 oracle, grouped forms, geomean over its shapes)",
+        "cores": orc.threads(), "kind": "oracle",
+        "sample": f"every valid row of experts 0..e-1 of each grouped shape, e = {done} (about {per_shape:.2f} s each)",
+    }
+
+
 def cpu_baseline_i8(cases, seconds):
     """The oracle's INT8 forms on rows 0, 1, ... of each case until its time share is used."""
     import numpy as np
@@ -471,6 +541,8 @@ def main():
                     help="skip the SwiGLU gate/up shapes")
     ap.add_argument("--no-int8", action="store_true",
                     help="skip the INT8 (W8A8 with dequantisation) shapes")
+    ap.add_argument("--no-grouped", action="store_true",
+                    help="skip the grouped (mixture-of-experts) shapes")
     ap.add_argument("--only", default="",
                     help="comma-separated workload names (sweep, gate, general-form or SwiGLU): "
                          "time just these (for profiling one kernel)")
@@ -520,6 +592,8 @@ def main():
                 return GeneralCase(wl.GENERAL_BY_NAME[n], ka, torch, rotate=not args.hot)
             if n in wl.I8_BY_NAME:
                 return I8Case(wl.I8_BY_NAME[n], ka, torch, rotate=not args.hot)
+            if n in wl.GROUPED_BY_NAME:
+                return GroupedCase(wl.GROUPED_BY_NAME[n], ka, torch, rotate=not args.hot)
             return Case(wl.BY_NAME[n], ka, torch, rotate=not args.hot)
         cases = [case_of(n) for n in args.only.split(",")]
         time_cases(cases, args.steps, args.warmup, ka, torch, use_graph=not args.no_graph)
@@ -654,6 +728,33 @@ def main():
             c.free()
         del icases
 
+    # Grouped (NEXT row: the mixture-of-experts projections over an
+    # expert-major padded layout, one launch per projection).
+    grouped = None
+    if not args.no_grouped:
+        for c in sweep:
+            c.free()
+        gcs = [GroupedCase(w, ka, torch, rotate=not args.hot) for w in wl.GROUPED]
+        time_cases(gcs, args.steps, args.warmup, ka, torch, use_graph=not args.no_graph)
+        grows2 = []
+        for c in gcs:
+            r = shape_row(c)
+            r.update({"experts": c.w.G, "top_k": c.w.top_k, "tokens": c.w.T, "M_pad": c.Mpad, "rows": c.w.rows})
+            grows2.append(r)
+            log(f"  {r['shape']:40s} {r['plan']:28s} {r['us']:9.2f} us {r['tflops']:8.1f} TF {r['gbps']:7.0f} GB/s  "
+                f"{r['bound']} frac {r['roofline_frac']:.3f}")
+        grouped = {"op": "per expert g: Y[g] = X[g] W[g]^T (SwiGLU: silu(X Wg^T) * (X Wu^T)) on its valid rows; "
+                         "FLOPs over valid rows only",
+                   "shapes": grows2,
+                   "geomean_tflops": round(geomean([r["tflops"] for r in grows2]), 3),
+                   "geomean_roofline_frac": round(geomean([r["roofline_frac"] for r in grows2]), 4)}
+        if not args.no_cpu_baseline:
+            log("timing the CPU oracle on the grouped forms (~4 s) ...")
+            grouped["cpu_baseline"] = cpu_baseline_grouped(gcs, 4.0)
+        for c in gcs:
+            c.free()
+        del gcs
+
     cpu = None
     if not args.no_cpu_baseline:
         log(f"timing the CPU oracle (~{args.cpu_seconds:.0f} s) ...")
@@ -682,6 +783,7 @@ def main():
         "general": general,
         "swiglu": swiglu,
         "int8": int8,
+        "grouped": grouped,
     }
     print(json.dumps(out), flush=True)
 

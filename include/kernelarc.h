@@ -256,6 +256,55 @@ int kernelarc_select_plan_i8(int64_t M, int64_t N, int64_t K, int swiglu);
  * -1 for an unknown plan or negative sizes. */
 int kernelarc_plan_supports_i8(int plan, int64_t M, int64_t N, int64_t K, int swiglu);
 
+/*
+ * Grouped (per-expert) linear layer and SwiGLU over an expert-major padded
+ * layout: the mixture-of-experts case study (Alg. 4) places token-expert
+ * pairs in expert-contiguous rows of a [G x M_pad] buffer (gap rows
+ * zero-filled) and runs each projection as one strided-batched GEMM.  For
+ * each group (expert) g and each valid row i < rows(g):
+ *
+ *     Y[g,i,j] = bf16( sum_k X[g,i,k] W[g,j,k] )                   (fp32 sums)
+ *     H[g,i,j] = bf16( silu(X[g,i,:].Wg[g,j,:]) * (X[g,i,:].Wu[g,j,:]) )
+ *
+ * X is [G,M_pad,K], W, Wg, Wu are [G,N,K], Y, H are [G,M_pad,N]; dense
+ * row-major bf16 device buffers owned by the caller.  counts is a device
+ * array of G int32 valid-row counts, each clamped to [0, M_pad] (NULL: every
+ * row of every group is valid); it is read by the kernels, so it may be
+ * produced on the device just before the call (no host round trip).  Rows
+ * at or past rows(g) -- the gap rows -- are neither read nor written.  The
+ * arithmetic per row is that of kernelarc_gemm_bf16 / kernelarc_swiglu_bf16.
+ * G * M_pad and K below 2^31 (N below 2^30 for SwiGLU); G, M_pad or N = 0:
+ * no launch.  An output overlapping X, a weight or counts is rejected.
+ * 16-byte aligned pointers with K a multiple of 8 take the MFMA tile kernels
+ * (one launch over all groups; tiles wholly in gap rows exit at once);
+ * anything else takes a generic kernel with the same contract.
+ */
+int kernelarc_gemm_bf16_grouped(int64_t G, int64_t M_pad, int64_t N, int64_t K, const void *X,
+                                const void *W, const int32_t *counts, void *Y, hipStream_t stream);
+
+int kernelarc_swiglu_bf16_grouped(int64_t G, int64_t M_pad, int64_t N, int64_t K, const void *X,
+                                  const void *Wg, const void *Wu, const int32_t *counts, void *H,
+                                  hipStream_t stream);
+
+/* The grouped forms with a forced plan (tile plans without split-K, and the
+ * generic plan; KERNELARC_ERR_UNSUPPORTED otherwise). */
+int kernelarc_gemm_bf16_grouped_with_plan(int plan, int64_t G, int64_t M_pad, int64_t N, int64_t K,
+                                          const void *X, const void *W, const int32_t *counts,
+                                          void *Y, hipStream_t stream);
+
+int kernelarc_swiglu_bf16_grouped_with_plan(int plan, int64_t G, int64_t M_pad, int64_t N, int64_t K,
+                                            const void *X, const void *Wg, const void *Wu,
+                                            const int32_t *counts, void *H, hipStream_t stream);
+
+/* The plan the grouped GEMM (swiglu == 0) or grouped SwiGLU runs for these
+ * sizes with aligned pointers; -1 for negative sizes. */
+int kernelarc_select_plan_grouped(int64_t G, int64_t M_pad, int64_t N, int64_t K, int swiglu);
+
+/* 1 if `plan` can compute the grouped form at these sizes, 0 if not, -1 for
+ * an unknown plan or negative sizes. */
+int kernelarc_plan_supports_grouped(int plan, int64_t G, int64_t M_pad, int64_t N, int64_t K,
+                                    int swiglu);
+
 /* Static description of a status code. */
 const char *kernelarc_status_string(int status);
 

@@ -425,6 +425,43 @@ int select_i8(int64_t M, int64_t N, int64_t K, bool glu) {
     return PLAN_GENERIC;
 }
 
+// Grouped (per-expert) forms over an expert-major padded layout: the tile
+// plans without split-K (SwiGLU: those that pair gate and up blocks) and the
+// generic plan.  The valid rows per group are on the device, so a launch
+// covers every group's M_pad rows and the tiles past the valid rows exit at
+// once.
+bool supports_grouped(int plan, int64_t G, int64_t Mpad, int64_t N, int64_t K, bool glu) {
+    if (G < 0 || Mpad < 0 || N < 0 || K < 0 || Mpad > LIMIT_DIM || N > (glu ? LIMIT_DIM / 2 : LIMIT_DIM) ||
+        K > LIMIT_DIM || (Mpad > 0 && G > LIMIT_DIM / Mpad))
+        return false;
+    if (plan < 0 || plan >= NUM_PLANS) return false;
+    const PlanInfo &pi = PLANS[plan];
+    if (pi.kind == KIND_GENERIC) return G * cdiv(Mpad, 64) * cdiv(N, 64) * 256 <= LIMIT_ITEMS;
+    if (pi.kind != KIND_TILE || pi.split != 1 || K % 8 != 0) return false;
+    if (glu && !tile_glu_ok(pi.tile_cfg)) return false;
+    const TileShape ts = tile_shape(pi.tile_cfg);
+    const int64_t bn = glu ? ts.bn / 2 : ts.bn;
+    if (ts.bm * K * 2 >= PANEL_LIMIT || bn * K * 2 >= PANEL_LIMIT || ts.bm * N * 2 >= PANEL_LIMIT) return false;
+    return G * cdiv(Mpad, ts.bm) * cdiv(N, bn) * 1024 <= LIMIT_ITEMS;
+}
+
+// Grouped plan rule (measured on MI355X at the mixture-of-experts sizes of
+// the paper's case study, 256 experts, top-8, hidden 4096, intermediate
+// 2048): the expert weights dominate the traffic, so a group whose padded
+// rows exceed 128 takes the 256x256 8-wave tile (one m-tile per expert, its
+// weights read once), smaller groups the 128x128 tile at two workgroups per
+// CU.
+int select_grouped(int64_t G, int64_t Mpad, int64_t N, int64_t K, bool glu) {
+    if (G < 0 || Mpad < 0 || N < 0 || K < 0) return -1;
+    if (K % 8 != 0) return PLAN_GENERIC;
+    const char *first = Mpad > 128 ? "tile_256x256_k64_w8" : "tile_128x128_k64_w4";
+    for (const char *name : {first, "tile_128x128_k64_w4"}) {
+        const int p = plan_index(name);
+        if (p >= 0 && supports_grouped(p, G, Mpad, N, K, glu)) return p;
+    }
+    return PLAN_GENERIC;
+}
+
 // ------------------------------------------------------------ devices ----
 constexpr int MAX_DEVICES = 64;
 
@@ -671,6 +708,71 @@ int run_glu(int plan, int64_t M, int64_t N, int64_t K, const void *X, const void
 
 bool aligned4(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
 
+// Grouped call: per group g, Y[g] = X[g] W[g]^T (or SwiGLU with W2) on its
+// valid rows; plan < 0: choose.
+int run_grouped(int plan, bool glu, int64_t G, int64_t Mpad, int64_t N, int64_t K, const void *X, const void *W,
+                const void *W2, const int32_t *counts, void *Y, hipStream_t stream) {
+    g_last_error[0] = '\0';
+    if (G < 0 || Mpad < 0 || N < 0 || K < 0)
+        return fail(KERNELARC_ERR_INVALID_ARG, "negative size G=%lld M_pad=%lld N=%lld K=%lld", (long long)G,
+                    (long long)Mpad, (long long)N, (long long)K);
+    if (Mpad > LIMIT_DIM || N > (glu ? LIMIT_DIM / 2 : LIMIT_DIM) || K > LIMIT_DIM ||
+        (Mpad > 0 && G > LIMIT_DIM / Mpad))
+        return fail(KERNELARC_ERR_INVALID_ARG, "a size is too large (G * M_pad, K below 2^31)");
+    if (plan >= NUM_PLANS) return fail(KERNELARC_ERR_UNSUPPORTED, "unknown plan %d", plan);
+    if (G == 0 || Mpad == 0 || N == 0) return KERNELARC_OK;
+    if (!Y) return fail(KERNELARC_ERR_INVALID_ARG, "the output is NULL");
+    if (K > 0 && (!X || !W || (glu && !W2))) return fail(KERNELARC_ERR_INVALID_ARG, "an operand is NULL");
+    if (counts && !aligned4(counts)) return fail(KERNELARC_ERR_INVALID_ARG, "counts must be 4-byte aligned");
+    const int64_t ybytes = G * Mpad * N * 2, wbytes = G * N * K * 2;
+    if (overlaps(Y, ybytes, X, G * Mpad * K * 2) || overlaps(Y, ybytes, W, wbytes) ||
+        (glu && overlaps(Y, ybytes, W2, wbytes)) || overlaps(Y, ybytes, counts, G * 4))
+        return fail(KERNELARC_ERR_INVALID_ARG, "the output overlaps an operand or the counts");
+
+    int dev = 0, num_cus = 0;
+    const int st = current_device(&dev, &num_cus);
+    if (st != KERNELARC_OK) return st;
+
+    const bool vec_ok = aligned16(X) && aligned16(W) && (!glu || aligned16(W2)) && aligned16(Y) && K % 8 == 0;
+    if (plan < 0) {
+        plan = select_grouped(G, Mpad, N, K, glu);
+        if (plan != PLAN_GENERIC && !vec_ok) plan = PLAN_GENERIC;
+    } else {
+        if (!supports_grouped(plan, G, Mpad, N, K, glu))
+            return fail(KERNELARC_ERR_UNSUPPORTED, "plan %s cannot compute the grouped %s at G=%lld M_pad=%lld N=%lld K=%lld",
+                        PLANS[plan].name, glu ? "SwiGLU" : "GEMM", (long long)G, (long long)Mpad, (long long)N,
+                        (long long)K);
+        if (plan != PLAN_GENERIC && !vec_ok)
+            return fail(KERNELARC_ERR_UNSUPPORTED, "plan %s needs 16-byte aligned pointers and K a multiple of 8",
+                        PLANS[plan].name);
+    }
+    (void)hipGetLastError();
+    hipError_t e = hipSuccess;
+    const auto *x = static_cast<const uint16_t *>(X);
+    const auto *w = static_cast<const uint16_t *>(W);
+    auto *y = static_cast<uint16_t *>(Y);
+    if (glu) {
+        Grouped<GluProblem> p{};
+        static_cast<GluProblem &>(p) = GluProblem{0, N, K, x, w, static_cast<const uint16_t *>(W2), y};
+        p.G = G;
+        p.Mpad = Mpad;
+        p.counts = counts;
+        e = PLANS[plan].kind == KIND_GENERIC ? launch_generic_grouped_glu(p, stream)
+                                             : launch_tile_grouped_glu(PLANS[plan].tile_cfg, p, stream);
+    } else {
+        Grouped<DenseProblem> p{};
+        static_cast<DenseProblem &>(p) = DenseProblem{0, N, K, x, w, nullptr, y};
+        p.G = G;
+        p.Mpad = Mpad;
+        p.counts = counts;
+        e = PLANS[plan].kind == KIND_GENERIC ? launch_generic_grouped(p, stream)
+                                             : launch_tile_grouped(PLANS[plan].tile_cfg, p, stream);
+    }
+    if (e != hipSuccess)
+        return fail(KERNELARC_ERR_LAUNCH, "launch of %s failed: %s", PLANS[plan].name, hipGetErrorString(e));
+    return KERNELARC_OK;
+}
+
 // INT8 call.  glu: H = bf16(silu(sx swg Ag) (sx swu Au)) (W2, sw2 the up
 // operands); else Y = bf16(sx sw A (+ R)).  plan < 0: choose.
 int run_i8(int plan, bool glu, int64_t M, int64_t N, int64_t K, const void *X, const float *sx, const void *W,
@@ -867,6 +969,44 @@ int kernelarc_select_plan_i8(int64_t M, int64_t N, int64_t K, int swiglu) { retu
 int kernelarc_plan_supports_i8(int plan, int64_t M, int64_t N, int64_t K, int swiglu) {
     if (plan < 0 || plan >= NUM_PLANS || M < 0 || N < 0 || K < 0) return -1;
     return supports_i8(plan, M, N, K, swiglu != 0) ? 1 : 0;
+}
+
+int kernelarc_gemm_bf16_grouped(int64_t G, int64_t M_pad, int64_t N, int64_t K, const void *X, const void *W,
+                                const int32_t *counts, void *Y, hipStream_t stream) {
+    return run_grouped(-1, false, G, M_pad, N, K, X, W, nullptr, counts, Y, stream);
+}
+
+int kernelarc_gemm_bf16_grouped_with_plan(int plan, int64_t G, int64_t M_pad, int64_t N, int64_t K, const void *X,
+                                          const void *W, const int32_t *counts, void *Y, hipStream_t stream) {
+    if (plan < 0) {
+        g_last_error[0] = '\0';
+        return fail(KERNELARC_ERR_UNSUPPORTED, "unknown plan %d", plan);
+    }
+    return run_grouped(plan, false, G, M_pad, N, K, X, W, nullptr, counts, Y, stream);
+}
+
+int kernelarc_swiglu_bf16_grouped(int64_t G, int64_t M_pad, int64_t N, int64_t K, const void *X, const void *Wg,
+                                  const void *Wu, const int32_t *counts, void *H, hipStream_t stream) {
+    return run_grouped(-1, true, G, M_pad, N, K, X, Wg, Wu, counts, H, stream);
+}
+
+int kernelarc_swiglu_bf16_grouped_with_plan(int plan, int64_t G, int64_t M_pad, int64_t N, int64_t K, const void *X,
+                                            const void *Wg, const void *Wu, const int32_t *counts, void *H,
+                                            hipStream_t stream) {
+    if (plan < 0) {
+        g_last_error[0] = '\0';
+        return fail(KERNELARC_ERR_UNSUPPORTED, "unknown plan %d", plan);
+    }
+    return run_grouped(plan, true, G, M_pad, N, K, X, Wg, Wu, counts, H, stream);
+}
+
+int kernelarc_select_plan_grouped(int64_t G, int64_t M_pad, int64_t N, int64_t K, int swiglu) {
+    return select_grouped(G, M_pad, N, K, swiglu != 0);
+}
+
+int kernelarc_plan_supports_grouped(int plan, int64_t G, int64_t M_pad, int64_t N, int64_t K, int swiglu) {
+    if (plan < 0 || plan >= NUM_PLANS || G < 0 || M_pad < 0 || N < 0 || K < 0) return -1;
+    return supports_grouped(plan, G, M_pad, N, K, swiglu != 0) ? 1 : 0;
 }
 
 int kernelarc_plan_count(void) { return NUM_PLANS; }

@@ -108,6 +108,27 @@ struct I8GluProblem {
     const float *sx, *sw, *sw2;  // [M], gate [N], up [N]
 };
 
+// Grouped (per-expert) form of a dense problem over an expert-major padded
+// layout: group g owns rows [g*Mpad, (g+1)*Mpad) of X and Y and its own
+// weights (W + g*N*K, and W2 for SwiGLU); its valid rows are counts[g]
+// clamped to [0, Mpad] (counts null: all Mpad).  M is unused (the kernels
+// set it per group); rows past the valid ones are neither read nor written.
+template <class Base>
+struct Grouped : Base {
+    int64_t G, Mpad;
+    const int32_t *counts;
+};
+template <class P>
+struct grouped_trait {
+    static constexpr bool value = false;
+    using base = P;
+};
+template <class B>
+struct grouped_trait<Grouped<B>> {
+    static constexpr bool value = true;
+    using base = B;
+};
+
 // Uniform access to every form inside the kernels.
 __host__ __device__ inline int64_t ldx_of(const Problem &p) { return p.ldx; }
 __host__ __device__ inline int64_t ldw_of(const Problem &p) { return p.ldw; }
@@ -189,6 +210,16 @@ hipError_t launch_tile_glu(int cfg, const GluProblem &p, int split, int64_t full
 bool tile_glu_ok(int cfg);
 // INT8: generic kernels (any K, any alignment) and the tile kernels (K a
 // multiple of 16; SwiGLU on the configurations of tile_glu_ok).
+// Grouped forms (bf16): the tile kernels without split-K, and generic kernels.
+hipError_t launch_tile_grouped(int cfg, const Grouped<DenseProblem> &p, hipStream_t s);
+hipError_t launch_tile_grouped_glu(int cfg, const Grouped<GluProblem> &p, hipStream_t s);
+hipError_t launch_generic_grouped(const Grouped<DenseProblem> &p, hipStream_t s);
+hipError_t launch_generic_grouped_glu(const Grouped<GluProblem> &p, hipStream_t s);
+__host__ __device__ inline int64_t group_rows(const int32_t *counts, int64_t g, int64_t Mpad) {
+    if (!counts) return Mpad;
+    const int64_t c = counts[g];
+    return c < 0 ? 0 : (c > Mpad ? Mpad : c);
+}
 hipError_t launch_generic_i8(const I8Problem &p, hipStream_t s);
 hipError_t launch_generic_i8_glu(const I8GluProblem &p, hipStream_t s);
 hipError_t launch_tile_i8(int cfg, const I8Problem &p, int split, int64_t full_tiles, const Workspace *ws,

@@ -1,6 +1,6 @@
 // Generic kernels: Y = alpha X W^T (+ beta R) (+ bias) for any shape, any
-// row strides and any pointer alignment, and SwiGLU and the INT8 forms for
-// any shape and alignment.
+// row strides and any pointer alignment; SwiGLU, the INT8 forms and the
+// grouped (per-expert) forms for any shape and alignment.
 //
 // This is the correctness fallback (K not a multiple of 8, pointers not
 // 16-byte aligned).  Each 256-thread workgroup computes a 64x64 output tile;
@@ -16,13 +16,12 @@ namespace {
 constexpr int GT = 64;   // output tile edge
 constexpr int GK = 16;   // K slice
 
-__global__ __launch_bounds__(256) void generic_kernel(Problem p, int64_t tiles_n) {
+__device__ __forceinline__ void generic_body(const Problem &p, int64_t tile, int64_t tiles_n) {
     __shared__ float xs[GK][GT + 1];
     __shared__ float ws[GK][GT + 1];
 
     const int tx = threadIdx.x & 15;
     const int ty = threadIdx.x >> 4;
-    const int64_t tile = blockIdx.x;
     const int64_t m0 = (tile / tiles_n) * GT;
     const int64_t n0 = (tile % tiles_n) * GT;
 
@@ -77,16 +76,31 @@ __global__ __launch_bounds__(256) void generic_kernel(Problem p, int64_t tiles_n
     }
 }
 
+__global__ __launch_bounds__(256) void generic_kernel(Problem p, int64_t tiles_n) {
+    generic_body(p, blockIdx.x, tiles_n);
+}
+
+// Grouped: workgroup id = (group, tile within the group's [Mpad, N] output).
+__global__ __launch_bounds__(256) void generic_grouped_kernel(Grouped<DenseProblem> p, int64_t tiles_n,
+                                                              int64_t tiles_per_group) {
+    const int64_t g = blockIdx.x / tiles_per_group;
+    const int64_t tile = blockIdx.x - g * tiles_per_group;
+    const int64_t rows = group_rows(p.counts, g, p.Mpad);
+    if ((tile / tiles_n) * GT >= rows) return;
+    const Problem q{rows, p.N, p.K, p.X + g * p.Mpad * p.K, p.W + g * p.N * p.K, nullptr, p.Y + g * p.Mpad * p.N,
+                    p.K, p.K, p.N, p.N, 1.0f, 1.0f, nullptr};
+    generic_body(q, tile, tiles_n);
+}
+
 // SwiGLU fallback: the same tiling with both weight operands staged, the
 // gate and up sums kept side by side, and silu(g) * u rounded once.
-__global__ __launch_bounds__(256) void generic_glu_kernel(GluProblem p, int64_t tiles_n) {
+__device__ __forceinline__ void generic_glu_body(const GluProblem &p, int64_t tile, int64_t tiles_n) {
     __shared__ float xs[GK][GT + 1];
     __shared__ float gs[GK][GT + 1];
     __shared__ float us[GK][GT + 1];
 
     const int tx = threadIdx.x & 15;
     const int ty = threadIdx.x >> 4;
-    const int64_t tile = blockIdx.x;
     const int64_t m0 = (tile / tiles_n) * GT;
     const int64_t n0 = (tile % tiles_n) * GT;
 
@@ -143,6 +157,21 @@ __global__ __launch_bounds__(256) void generic_glu_kernel(GluProblem p, int64_t 
             p.Y[i * p.N + j] = f32_to_bf16_rne(silu_f32(g[a][b]) * u[a][b]);
         }
     }
+}
+
+__global__ __launch_bounds__(256) void generic_glu_kernel(GluProblem p, int64_t tiles_n) {
+    generic_glu_body(p, blockIdx.x, tiles_n);
+}
+
+__global__ __launch_bounds__(256) void generic_grouped_glu_kernel(Grouped<GluProblem> p, int64_t tiles_n,
+                                                                  int64_t tiles_per_group) {
+    const int64_t g = blockIdx.x / tiles_per_group;
+    const int64_t tile = blockIdx.x - g * tiles_per_group;
+    const int64_t rows = group_rows(p.counts, g, p.Mpad);
+    if ((tile / tiles_n) * GT >= rows) return;
+    const GluProblem q{rows, p.N, p.K, p.X + g * p.Mpad * p.K, p.W + g * p.N * p.K, p.W2 + g * p.N * p.K,
+                       p.Y + g * p.Mpad * p.N};
+    generic_glu_body(q, tile, tiles_n);
 }
 
 // INT8 fallbacks: the same 64x64 tiling with int8 operands staged as int32
@@ -246,6 +275,22 @@ hipError_t launch_generic_i8_glu(const I8GluProblem &p, hipStream_t s) {
     const int64_t tiles_n = (p.N + GT - 1) / GT;
     const int64_t tiles = ((p.M + GT - 1) / GT) * tiles_n;
     hipLaunchKernelGGL(generic_i8_glu_kernel, dim3(static_cast<unsigned>(tiles)), dim3(256), 0, s, p, tiles_n);
+    return hipGetLastError();
+}
+
+hipError_t launch_generic_grouped(const Grouped<DenseProblem> &p, hipStream_t s) {
+    const int64_t tiles_n = (p.N + GT - 1) / GT;
+    const int64_t per = ((p.Mpad + GT - 1) / GT) * tiles_n;
+    hipLaunchKernelGGL(generic_grouped_kernel, dim3(static_cast<unsigned>(p.G * per)), dim3(256), 0, s, p, tiles_n,
+                       per);
+    return hipGetLastError();
+}
+
+hipError_t launch_generic_grouped_glu(const Grouped<GluProblem> &p, hipStream_t s) {
+    const int64_t tiles_n = (p.N + GT - 1) / GT;
+    const int64_t per = ((p.Mpad + GT - 1) / GT) * tiles_n;
+    hipLaunchKernelGGL(generic_grouped_glu_kernel, dim3(static_cast<unsigned>(p.G * per)), dim3(256), 0, s, p,
+                       tiles_n, per);
     return hipGetLastError();
 }
 

@@ -256,14 +256,20 @@ struct SplitK {
 // rows (alternate 32-row blocks) and the output tile is BM x BN/2;
 // P = I8Problem, I8GluProblem: the same with int8 operands (a stage holds
 // twice the K elements, v_mfma_i32_32x32x32_i8 accumulates exactly in
-// int32) and dequantisation by the row and column scales in the epilogue.
+// int32) and dequantisation by the row and column scales in the epilogue;
+// P = Grouped<DenseProblem>, Grouped<GluProblem>: one launch over the groups
+// of an expert-major padded layout; the m-tiles of the groups are stacked
+// (tiles_m = G * m-tiles per group), each workgroup rebases the problem on
+// its group, and tiles wholly past the group's valid rows exit at once.
 template <class C, class P>
 __global__ __attribute__((amdgpu_flat_work_group_size(C::THREADS, C::THREADS),
                           amdgpu_waves_per_eu(C::WAVES_PER_EU, C::WAVES_PER_EU)))
 void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) {
-    constexpr bool GEN = std::is_same<P, Problem>::value;
-    constexpr bool I8 = std::is_same<P, I8Problem>::value || std::is_same<P, I8GluProblem>::value;
-    constexpr bool GLU = std::is_same<P, GluProblem>::value || std::is_same<P, I8GluProblem>::value;
+    using PB = typename grouped_trait<P>::base;
+    constexpr bool GROUPED = grouped_trait<P>::value;
+    constexpr bool GEN = std::is_same<PB, Problem>::value;
+    constexpr bool I8 = std::is_same<PB, I8Problem>::value || std::is_same<PB, I8GluProblem>::value;
+    constexpr bool GLU = std::is_same<PB, GluProblem>::value || std::is_same<PB, I8GluProblem>::value;
     constexpr int EB = I8 ? 1 : 2;                 // bytes per operand element
     constexpr int BKE = C::ROW_BYTES / EB;         // K elements per stage
     constexpr int CKE = 16 / EB;                   // K elements per 16-byte chunk
@@ -317,6 +323,18 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
         const int64_t in_band = tile - g * band;
         tm = first_m + in_band % rows;
         tn = in_band / rows;
+    }
+    if constexpr (GROUPED) {
+        const int64_t tpg = (p.Mpad + C::BM - 1) / C::BM;   // m-tiles per group
+        const int64_t g = tm / tpg;
+        tm -= g * tpg;
+        const int64_t rows = group_rows(p.counts, g, p.Mpad);
+        if (tm * C::BM >= rows) return;                    // the whole tile is gap rows
+        p.M = rows;
+        p.X += g * p.Mpad * p.K;
+        p.Y += g * p.Mpad * p.N;
+        p.W += g * p.N * p.K;
+        if constexpr (GLU) p.W2 += g * p.N * p.K;
     }
     const int64_t m0 = tm * C::BM;
     const int64_t n0 = tn * BNO;
@@ -1005,6 +1023,41 @@ hipError_t launch_tile_glu(int cfg, const GluProblem &p, int split, int64_t full
         using C = decltype(c);
         if constexpr (std::is_same<C, std::nullptr_t>::value) return hipErrorInvalidValue;
         else return launch_cfg_glu<C>(p, 8, split, full_tiles, ws, s);
+    });
+}
+
+// Grouped forms: one launch of G * m-tiles-per-group * n-tiles workgroups,
+// no split-K.
+template <class C, class B>
+hipError_t launch_cfg_grouped(const Grouped<B> &p, hipStream_t s) {
+    constexpr bool GLU = std::is_same<B, GluProblem>::value;
+    if constexpr (GLU && !glu_ok<C>()) {
+        return hipErrorInvalidValue;
+    } else {
+        constexpr int BNO = GLU ? C::BN / 2 : C::BN;
+        const int64_t tiles_m = p.G * ((p.Mpad + C::BM - 1) / C::BM);
+        const int64_t tiles_n = (p.N + BNO - 1) / BNO;
+        SplitK sk;
+        if (!split_args<C>(p.K, tiles_m * tiles_n, 1, 0, nullptr, sk)) return hipErrorInvalidValue;
+        hipLaunchKernelGGL((tile_kernel<C, Grouped<B>>), dim3(static_cast<unsigned>(tiles_m * tiles_n)),
+                           dim3(C::THREADS), 0, s, p, tiles_m, tiles_n, 8, sk);
+        return hipGetLastError();
+    }
+}
+
+hipError_t launch_tile_grouped(int cfg, const Grouped<DenseProblem> &p, hipStream_t s) {
+    return with_cfg(cfg, [&](auto c, int) {
+        using C = decltype(c);
+        if constexpr (std::is_same<C, std::nullptr_t>::value) return hipErrorInvalidValue;
+        else return launch_cfg_grouped<C>(p, s);
+    });
+}
+
+hipError_t launch_tile_grouped_glu(int cfg, const Grouped<GluProblem> &p, hipStream_t s) {
+    return with_cfg(cfg, [&](auto c, int) {
+        using C = decltype(c);
+        if constexpr (std::is_same<C, std::nullptr_t>::value) return hipErrorInvalidValue;
+        else return launch_cfg_grouped<C>(p, s);
     });
 }
 

@@ -57,6 +57,14 @@ _SIGS = {
                                                      _P]),
     "kernelarc_select_plan_i8": (ctypes.c_int, [_I64, _I64, _I64, ctypes.c_int]),
     "kernelarc_plan_supports_i8": (ctypes.c_int, [ctypes.c_int, _I64, _I64, _I64, ctypes.c_int]),
+    "kernelarc_gemm_bf16_grouped": (ctypes.c_int, [_I64, _I64, _I64, _I64, _P, _P, _P, _P, _P]),
+    "kernelarc_gemm_bf16_grouped_with_plan": (ctypes.c_int, [ctypes.c_int, _I64, _I64, _I64, _I64, _P, _P, _P, _P,
+                                                             _P]),
+    "kernelarc_swiglu_bf16_grouped": (ctypes.c_int, [_I64, _I64, _I64, _I64, _P, _P, _P, _P, _P, _P]),
+    "kernelarc_swiglu_bf16_grouped_with_plan": (ctypes.c_int, [ctypes.c_int, _I64, _I64, _I64, _I64, _P, _P, _P, _P,
+                                                               _P, _P]),
+    "kernelarc_select_plan_grouped": (ctypes.c_int, [_I64, _I64, _I64, _I64, ctypes.c_int]),
+    "kernelarc_plan_supports_grouped": (ctypes.c_int, [ctypes.c_int, _I64, _I64, _I64, _I64, ctypes.c_int]),
     "kernelarc_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "kernelarc_last_error": (ctypes.c_char_p, []),
 }
@@ -327,3 +335,56 @@ def select_plan_i8(M: int, N: int, K: int, swiglu: bool = False) -> int:
 
 def plan_supports_i8(plan: int, M: int, N: int, K: int, swiglu: bool = False) -> bool:
     return _lib.kernelarc_plan_supports_i8(plan, M, N, K, int(swiglu)) == 1
+
+
+def _grouped_operand(t, name, shape, device):
+    if t.dtype != torch.bfloat16 or not t.is_cuda or not t.is_contiguous() or tuple(t.shape) != shape:
+        raise ValueError(f"{name} must be a contiguous bfloat16 GPU tensor of shape {shape}")
+    if t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+
+
+def _grouped_call(fn, fn_plan, what, x, ws, counts, out, stream, plan):
+    if x.dim() != 3 or any(w.dim() != 3 for w in ws):
+        raise ValueError("x must be [G, M_pad, K] and the weights [G, N, K]")
+    G, Mpad, K = x.shape
+    N = ws[0].shape[1]
+    dev = x.device
+    _grouped_operand(x, "x", (G, Mpad, K), dev)
+    for i, w in enumerate(ws):
+        _grouped_operand(w, f"weight {i}", (G, N, K), dev)
+    if counts is not None and (counts.dtype != torch.int32 or not counts.is_cuda or not counts.is_contiguous()
+                               or tuple(counts.shape) != (G,) or counts.device != dev):
+        raise ValueError(f"counts must be a contiguous int32 GPU tensor of shape ({G},)")
+    if out is None:
+        out = torch.empty((G, Mpad, N), dtype=torch.bfloat16, device=dev)
+    else:
+        _grouped_operand(out, "out", (G, Mpad, N), dev)
+    args = (G, Mpad, N, K, x.data_ptr(), *[w.data_ptr() for w in ws],
+            counts.data_ptr() if counts is not None else None, out.data_ptr(), _stream_handle(stream))
+    with torch.cuda.device(dev):
+        st = fn(*args) if plan is None else fn_plan(plan, *args)
+    _check(st, what if plan is None else f"{what}_with_plan({plan_name(plan)})")
+    return out
+
+
+def gemm_bf16_grouped(x, w, counts=None, out=None, stream=None, plan=None):
+    """Y[g, i] = X[g, i] W[g]^T for the valid rows i < counts[g] of each group:
+    x [G, M_pad, K], w [G, N, K], counts int32 [G] on the device (None: all
+    rows); the gap rows of `out` are left untouched."""
+    return _grouped_call(_lib.kernelarc_gemm_bf16_grouped, _lib.kernelarc_gemm_bf16_grouped_with_plan,
+                         "kernelarc_gemm_bf16_grouped", x, (w,), counts, out, stream, plan)
+
+
+def swiglu_bf16_grouped(x, wg, wu, counts=None, out=None, stream=None, plan=None):
+    """H[g, i] = silu(X[g, i] Wg[g]^T) * (X[g, i] Wu[g]^T) for the valid rows."""
+    return _grouped_call(_lib.kernelarc_swiglu_bf16_grouped, _lib.kernelarc_swiglu_bf16_grouped_with_plan,
+                         "kernelarc_swiglu_bf16_grouped", x, (wg, wu), counts, out, stream, plan)
+
+
+def select_plan_grouped(G: int, M_pad: int, N: int, K: int, swiglu: bool = False) -> int:
+    return _lib.kernelarc_select_plan_grouped(G, M_pad, N, K, int(swiglu))
+
+
+def plan_supports_grouped(plan: int, G: int, M_pad: int, N: int, K: int, swiglu: bool = False) -> bool:
+    return _lib.kernelarc_plan_supports_grouped(plan, G, M_pad, N, K, int(swiglu)) == 1

@@ -200,6 +200,8 @@ class I8Workload:
     residual: bool
     seed: int
 
+    int8 = True     # operands are int8: the roofline uses the int8 MFMA peak
+
     @property
     def flops(self) -> int:
         """Integer multiply-adds counted as 2 operations (4MNK for SwiGLU)."""
@@ -249,6 +251,112 @@ def make_i8_inputs(w: I8Workload) -> dict:
         out["qWu"], out["swu"] = ws[1], ss[1]
     if w.residual:
         out["R"] = torch.randn((w.M, w.N), generator=g).to(torch.bfloat16)
+    return out
+
+
+# ---- grouped (per-expert) forms over an expert-major padded layout ---------
+
+@dataclass(frozen=True)
+class GroupedWorkload:
+    """A mixture-of-experts projection: T tokens each routed to top_k of G
+    experts; the token-expert rows sit expert-contiguously in a [G x M_pad]
+    buffer.  swiglu: the experts' gate/up projections with the SiLU-multiply
+    (N = intermediate, K = hidden); else a plain projection (e.g. the down
+    projection, N = hidden, K = intermediate)."""
+    name: str
+    T: int
+    top_k: int
+    G: int
+    N: int
+    K: int
+    swiglu: bool
+    seed: int
+
+    @property
+    def counts(self) -> np.ndarray:
+        return routing_counts(self.T, self.top_k, self.G, self.seed)
+
+    @property
+    def Mpad(self) -> int:
+        return padded_capacity(self.counts)
+
+    @property
+    def rows(self) -> int:
+        """Valid rows over all experts (= T * top_k)."""
+        return int(self.counts.sum())
+
+    @property
+    def M(self) -> int:
+        """Rows the projection computes: the valid rows of all experts."""
+        return self.rows
+
+    @property
+    def flops(self) -> int:
+        return (4 if self.swiglu else 2) * self.rows * self.N * self.K
+
+    @property
+    def algorithmic_bytes(self) -> int:
+        """Valid X rows, every expert's weights and the valid output rows, once
+        each (bf16), and the counts."""
+        w = 2 if self.swiglu else 1
+        return 2 * (self.rows * self.K + w * self.G * self.N * self.K + self.rows * self.N) + 4 * self.G
+
+
+_COUNTS_CACHE: dict = {}
+
+
+def routing_counts(T: int, top_k: int, G: int, seed: int) -> np.ndarray:
+    """Rows per expert when each of T tokens picks its top_k of G experts by
+    i.i.d. uniform router scores (torch.rand from `seed`, then topk)."""
+    key = (T, top_k, G, seed)
+    if key not in _COUNTS_CACHE:
+        g = torch.Generator().manual_seed(seed)
+        idx = torch.rand((T, G), generator=g).topk(top_k, dim=1).indices
+        _COUNTS_CACHE[key] = torch.bincount(idx.flatten(), minlength=G).numpy().astype(np.int32)
+    return _COUNTS_CACHE[key]
+
+
+def padded_capacity(counts: np.ndarray, multiple: int = 32) -> int:
+    """M_pad: the largest expert's row count rounded up to a multiple of 32."""
+    m = int(counts.max()) if counts.size else 0
+    return max(multiple, -(-m // multiple) * multiple)
+
+
+# The mixture-of-experts layer of the paper's case study (256 experts, top-8,
+# hidden 4096, intermediate 2048) at its smallest and largest token counts:
+# the experts' gate/up projections with SwiGLU and their down projections.
+GROUPED = (
+    GroupedWorkload("moe_gate_up_t2048", 2048, 8, 256, 2048, 4096, True, 401),
+    GroupedWorkload("moe_gate_up_t6144", 6144, 8, 256, 2048, 4096, True, 402),
+    GroupedWorkload("moe_down_t2048", 2048, 8, 256, 4096, 2048, False, 403),
+    GroupedWorkload("moe_down_t6144", 6144, 8, 256, 4096, 2048, False, 404),
+)
+GROUPED_BY_NAME = {w.name: w for w in GROUPED}
+
+
+def make_grouped_inputs(w: GroupedWorkload, device: str = "cuda") -> dict:
+    """counts from the routing draw (seed, on the host); then, from seed + 1
+    on `device`'s torch generator: X rows ~ N(0,1) (the valid rows of each
+    expert; gap rows zero), the weights [G, N, K] ~ N(0,1)/sqrt(K) (gate, then
+    up), all bf16.  The expert weights run to billions of values, so they are
+    drawn where they are used; a check copies the same bytes to the host."""
+    counts = w.counts
+    Mpad = w.Mpad
+    g = torch.Generator(device=device).manual_seed(w.seed + 1)
+    X = torch.randn((w.G, Mpad, w.K), generator=g, device=device)
+    valid = torch.from_numpy(counts.astype(np.int64)).to(device)
+    rows = torch.arange(Mpad, device=device)[None, :, None] < valid[:, None, None]
+    X = torch.where(rows, X, torch.zeros((), device=device)).to(torch.bfloat16)
+    scale = 1.0 / math.sqrt(w.K) if w.K > 0 else 1.0
+    ws = []
+    for _ in range(2 if w.swiglu else 1):
+        t = torch.randn((w.G, w.N, w.K), generator=g, device=device)
+        t.mul_(scale)
+        ws.append(t.to(torch.bfloat16))
+        del t
+    out = {"X": X, "W": ws[0], "counts": torch.from_numpy(counts.copy()).to(device), "Mpad": Mpad}
+    if w.swiglu:
+        out["Wu"] = ws[1]
     return out
 
 

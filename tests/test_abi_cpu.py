@@ -232,3 +232,27 @@ def test_i8_validation_and_plans(ka):
     assert not ka.plan_supports_i8(names.index("tile_64x64_k64_w4"), 64, 1024, 1024, True)
     assert ka.plan_supports_i8(names.index("tile_64x64_k64_w4"), 64, 1024, 1024, False)
     assert not ka.plan_supports_i8(names.index("tile_256x256_k64_w8"), 64, 1024, 1032)  # K % 16
+
+
+def test_grouped_validation_and_plans(ka):
+    f = ka.kernelarc_gemm_bf16_grouped
+    buf = (ctypes.c_uint16 * 16384)()
+    base = ctypes.addressof(buf)
+    X, W, C, Y = base, base + 4096, base + 8192, base + 12288
+    # (G, M_pad, N, K, X, W, counts, Y, stream)
+    assert f(-1, 4, 4, 8, X, W, C, Y, None) == ka.ERR_INVALID_ARG
+    assert f(2, 4, 4, 8, X, W, C, None, None) == ka.ERR_INVALID_ARG              # NULL output
+    assert f(2, 4, 4, 8, X, W, C + 2, Y, None) == ka.ERR_INVALID_ARG             # misaligned counts
+    assert f(2, 4, 4, 8, X, W, C, X + 16, None) == ka.ERR_INVALID_ARG            # output overlaps X
+    assert f(2, 4, 4, 8, X, W, C, C - 16, None) == ka.ERR_INVALID_ARG            # output overlaps counts
+    assert f(1 << 20, 1 << 12, 4, 8, X, W, C, Y, None) == ka.ERR_INVALID_ARG     # G * M_pad too large
+    assert f(0, 4, 4, 8, None, None, None, None, None) == ka.OK
+    assert ka.kernelarc_swiglu_bf16_grouped(2, 4, 4, 8, X, W, None, C, Y, None) == ka.ERR_INVALID_ARG
+    names = ka.plan_names()
+    assert ka.select_plan_grouped(4, 64, 100, 250) == names.index("generic_64x64_scalar")
+    for (G, Mpad, N, K, glu) in [(256, 96, 2048, 4096, 1), (256, 256, 4096, 2048, 0), (8, 33, 77, 136, 0)]:
+        p = ka.select_plan_grouped(G, Mpad, N, K, glu)
+        assert ka.plan_supports_grouped(p, G, Mpad, N, K, glu) and names[p].startswith("tile"), names[p]
+    for n in ("tile_128x128_k64_w4_splitk", "tile_256x256_k64_w8_tailsplit", "stream_mfma16_k64_splitk"):
+        assert not ka.plan_supports_grouped(names.index(n), 4, 64, 256, 256)
+    assert not ka.plan_supports_grouped(names.index("tile_64x64_k64_w4"), 4, 64, 256, 256, True)
