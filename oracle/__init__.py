@@ -1,8 +1,8 @@
 """CPU oracle for Y = X.W^T + R, its general form
 D = alpha.X.W^T + beta.C + bias, the gated MLP input projection
-H = silu(X.Wg^T) * (X.Wu^T), their INT8 forms with per-row and per-column
-dequantisation scales, and grouped (per-expert) forms over an expert-major
-padded layout (TEST INFRASTRUCTURE ONLY).
+H = silu(X.Wg^T) * (X.Wu^T), their INT8 and FP8 (E4M3) forms with per-row
+and per-column dequantisation scales, and grouped (per-expert) forms over an
+expert-major padded layout (TEST INFRASTRUCTURE ONLY).
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
 ``bench.py`` may import this package.  The GPU library never imports, links
@@ -83,6 +83,16 @@ class Oracle:
         lib.ka_oracle_grouped_at.argtypes = [_I64, _I64, _I64, _I64, _P, _P, _P, _P, ctypes.c_int, _I64, _P, _P,
                                              _P, _P]
         lib.ka_oracle_grouped_at.restype = ctypes.c_int
+        lib.ka_oracle_fp8_decode.argtypes = [_I64, _P, _P]
+        lib.ka_oracle_fp8_decode.restype = None
+        lib.ka_oracle_f8_linear.argtypes = [_I64, _I64, _I64, _P, _P, _P, _P, _P, _P]
+        lib.ka_oracle_f8_linear.restype = ctypes.c_int
+        lib.ka_oracle_f8_linear_at.argtypes = [_I64, _I64, _I64, _P, _P, _P, _P, _P, _I64, _P, _P, _P]
+        lib.ka_oracle_f8_linear_at.restype = ctypes.c_int
+        lib.ka_oracle_f8_swiglu.argtypes = [_I64, _I64, _I64, _P, _P, _P, _P, _P, _P, _P]
+        lib.ka_oracle_f8_swiglu.restype = ctypes.c_int
+        lib.ka_oracle_f8_swiglu_at.argtypes = [_I64, _I64, _I64, _P, _P, _P, _P, _P, _P, _I64, _P, _P, _P]
+        lib.ka_oracle_f8_swiglu_at.restype = ctypes.c_int
         lib.ka_oracle_round_bf16.argtypes = [_I64, _P, _P]
         lib.ka_oracle_round_bf16.restype = None
         lib.ka_oracle_threads.argtypes = []
@@ -320,6 +330,81 @@ class Oracle:
         rows, cols = self._positions(rows, cols)
         out = np.empty(rows.shape[0], dtype=np.float64)
         if self.lib.ka_oracle_i8_swiglu_at(*args, rows.shape[0], rows.ctypes.data, cols.ctypes.data,
+                                           out.ctypes.data) != 0:
+            raise ValueError("oracle rejected its arguments")
+        del keep
+        return out
+
+    # ---- FP8 (E4M3 bit patterns in numpy.uint8) with dequantisation scales ----
+    @staticmethod
+    def _u8(a, shape, what):
+        a = np.ascontiguousarray(a)
+        if a.dtype != np.uint8:
+            raise TypeError(f"{what}: expected E4M3 bit patterns (numpy.uint8)")
+        if a.shape != shape:
+            raise ValueError(f"{what}: expected shape {shape}, got {a.shape}")
+        return a
+
+    def fp8_decode(self, bits) -> np.ndarray:
+        """E4M3 bit patterns to float64 (exact)."""
+        b = np.ascontiguousarray(bits, dtype=np.uint8)
+        out = np.empty(b.shape, dtype=np.float64)
+        self.lib.ka_oracle_fp8_decode(b.size, b.ctypes.data, out.ctypes.data)
+        return out
+
+    def _f8_args(self, qX, sx, qW, sw, R):
+        M, K = qX.shape
+        N = qW.shape[0]
+        qX, qW = self._u8(qX, (M, K), "qX"), self._u8(qW, (N, K), "qW")
+        sx, sw = self._f32(sx, M, "sx"), self._f32(sw, N, "sw")
+        Rp = None
+        if R is not None:
+            R = self._bits(R, (M, N))
+            Rp = R.ctypes.data
+        return (M, N, K, qX.ctypes.data, sx.ctypes.data, qW.ctypes.data, sw.ctypes.data, Rp), (qX, sx, qW, sw, R)
+
+    def f8_linear(self, qX, sx, qW, sw, R=None) -> np.ndarray:
+        """Y = sx[i] sw[j] sum_k x8(qX) x8(qW) (+ R) in float64."""
+        args, keep = self._f8_args(qX, sx, qW, sw, R)
+        Y = np.empty((args[0], args[1]), dtype=np.float64)
+        if self.lib.ka_oracle_f8_linear(*args, Y.ctypes.data) != 0:
+            raise ValueError("oracle rejected its arguments")
+        del keep
+        return Y
+
+    def f8_linear_at(self, qX, sx, qW, sw, R, rows, cols) -> np.ndarray:
+        args, keep = self._f8_args(qX, sx, qW, sw, R)
+        rows, cols = self._positions(rows, cols)
+        out = np.empty(rows.shape[0], dtype=np.float64)
+        if self.lib.ka_oracle_f8_linear_at(*args, rows.shape[0], rows.ctypes.data, cols.ctypes.data,
+                                           out.ctypes.data) != 0:
+            raise ValueError("oracle rejected its arguments")
+        del keep
+        return out
+
+    def _f8_glu_args(self, qX, sx, qWg, swg, qWu, swu):
+        M, K = qX.shape
+        N = qWg.shape[0]
+        qX = self._u8(qX, (M, K), "qX")
+        qWg, qWu = self._u8(qWg, (N, K), "qWg"), self._u8(qWu, (N, K), "qWu")
+        sx = self._f32(sx, M, "sx")
+        swg, swu = self._f32(swg, N, "swg"), self._f32(swu, N, "swu")
+        keep = (qX, sx, qWg, swg, qWu, swu)
+        return (M, N, K) + tuple(a.ctypes.data for a in keep), keep
+
+    def f8_swiglu(self, qX, sx, qWg, swg, qWu, swu) -> np.ndarray:
+        args, keep = self._f8_glu_args(qX, sx, qWg, swg, qWu, swu)
+        H = np.empty((args[0], args[1]), dtype=np.float64)
+        if self.lib.ka_oracle_f8_swiglu(*args, H.ctypes.data) != 0:
+            raise ValueError("oracle rejected its arguments")
+        del keep
+        return H
+
+    def f8_swiglu_at(self, qX, sx, qWg, swg, qWu, swu, rows, cols) -> np.ndarray:
+        args, keep = self._f8_glu_args(qX, sx, qWg, swg, qWu, swu)
+        rows, cols = self._positions(rows, cols)
+        out = np.empty(rows.shape[0], dtype=np.float64)
+        if self.lib.ka_oracle_f8_swiglu_at(*args, rows.shape[0], rows.ctypes.data, cols.ctypes.data,
                                            out.ctypes.data) != 0:
             raise ValueError("oracle rejected its arguments")
         del keep

@@ -6,8 +6,9 @@
  * its general form (alpha, beta, bias, leading dimensions), the gated
  * MLP input projection H = silu(X Wg^T) * (X Wu^T) (SwiGLU), and INT8
  * versions of the linear layer and of SwiGLU with per-row and per-column
- * dequantisation scales, and grouped (per-expert) forms of the linear layer
- * and of SwiGLU over an expert-major padded layout.
+ * dequantisation scales, FP8 (E4M3) versions with the same scales, and
+ * grouped (per-expert) forms of the linear layer and of SwiGLU over an
+ * expert-major padded layout.
  *
  * TEST INFRASTRUCTURE ONLY.  This file is the slow, obviously correct
  * reference that the GPU library is checked against.  Only the test suite,
@@ -476,6 +477,122 @@ int ka_oracle_grouped_at(int64_t E, int64_t Mpad, int64_t N, int64_t K, const ui
         out[t] = swiglu ? element_swiglu(rows[t], cols[t], K, X + e * Mpad * K, W + e * N * K, W2 + e * N * K)
                         : element(rows[t], cols[t], N, K, X + e * Mpad * K, W + e * N * K, NULL);
     }
+    return 0;
+}
+
+/*
+ * FP8 (E4M3) linear layer and SwiGLU with dequantisation scales: the
+ * precision axis the paper's strategy skills name (FP8 / BF16 choices), in
+ * the same scaled form as the INT8 path above, with FP8 E4M3 operands in
+ * place of int8 (one binary32 scale per activation row and per output
+ * channel):
+ *
+ *     Y[i,j] = sx[i] sw[j] sum_k x8(qX[i,k]) x8(qW[j,k])  (+ R[i,j])
+ *     H[i,j] = silu(sx[i] swg[j] Sg[i,j]) * (sx[i] swu[j] Su[i,j])
+ *
+ * x8() decodes the OCP 8-bit E4M3 format (the "FN" variant): sign bit,
+ * 4 exponent bits with bias 7, 3 mantissa bits; exponent field 0 gives
+ * subnormals m/8 * 2^-6; exponent field 15 with mantissa 7 is NaN (there are
+ * no infinities), so the largest finite magnitude is 1.75 * 2^8 = 448.
+ * Every decoded value and every product of two is exact in double; the
+ * k-sum runs ascending in double; then (sx * sw) * S (+ R); silu as above.
+ */
+static double fp8_e4m3_to_double(uint8_t b)
+{
+    int sign = b >> 7;
+    int e = (b >> 3) & 15;
+    int m = b & 7;
+    double v;
+    if (e == 15 && m == 7)
+        v = NAN;
+    else if (e == 0)
+        v = ldexp((double)m, -9);            /* m/8 * 2^-6 */
+    else
+        v = ldexp((double)(8 + m), e - 10);  /* (1 + m/8) * 2^(e-7) */
+    return sign ? -v : v;
+}
+
+static double dot_f8(const uint8_t *x, const uint8_t *w, int64_t K)
+{
+    double acc = 0.0;
+    for (int64_t k = 0; k < K; ++k)
+        acc += fp8_e4m3_to_double(x[k]) * fp8_e4m3_to_double(w[k]);
+    return acc;
+}
+
+static double element_f8(int64_t i, int64_t j, int64_t N, int64_t K, const uint8_t *qX,
+                         const float *sx, const uint8_t *qW, const float *sw, const uint16_t *R)
+{
+    double y = (double)sx[i] * (double)sw[j] * dot_f8(qX + i * K, qW + j * K, K);
+    if (R)
+        y += bf16_bits_to_double(R[i * N + j]);
+    return y;
+}
+
+static double element_f8_swiglu(int64_t i, int64_t j, int64_t K, const uint8_t *qX, const float *sx,
+                                const uint8_t *qWg, const float *swg, const uint8_t *qWu, const float *swu)
+{
+    double g = (double)sx[i] * (double)swg[j] * dot_f8(qX + i * K, qWg + j * K, K);
+    double u = (double)sx[i] * (double)swu[j] * dot_f8(qX + i * K, qWu + j * K, K);
+    return silu(g) * u;
+}
+
+/* Decode n E4M3 bytes (the format definition above) into doubles. */
+void ka_oracle_fp8_decode(int64_t n, const uint8_t *in, double *out)
+{
+    for (int64_t t = 0; t < n; ++t)
+        out[t] = fp8_e4m3_to_double(in[t]);
+}
+
+int ka_oracle_f8_linear(int64_t M, int64_t N, int64_t K, const uint8_t *qX, const float *sx,
+                        const uint8_t *qW, const float *sw, const uint16_t *R, double *Y)
+{
+    if (check_i8(M, N, K, qX, sx, qW, sw) != 0) return -1;
+    if (M * N > 0 && !Y) return -1;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t i = 0; i < M; ++i)
+        for (int64_t j = 0; j < N; ++j)
+            Y[i * N + j] = element_f8(i, j, N, K, qX, sx, qW, sw, R);
+    return 0;
+}
+
+int ka_oracle_f8_linear_at(int64_t M, int64_t N, int64_t K, const uint8_t *qX, const float *sx,
+                           const uint8_t *qW, const float *sw, const uint16_t *R, int64_t n,
+                           const int64_t *rows, const int64_t *cols, double *out)
+{
+    if (check_i8(M, N, K, qX, sx, qW, sw) != 0 || n < 0) return -1;
+    for (int64_t t = 0; t < n; ++t)
+        if (rows[t] < 0 || rows[t] >= M || cols[t] < 0 || cols[t] >= N) return -1;
+#pragma omp parallel for schedule(dynamic, 16)
+    for (int64_t t = 0; t < n; ++t)
+        out[t] = element_f8(rows[t], cols[t], N, K, qX, sx, qW, sw, R);
+    return 0;
+}
+
+int ka_oracle_f8_swiglu(int64_t M, int64_t N, int64_t K, const uint8_t *qX, const float *sx,
+                        const uint8_t *qWg, const float *swg, const uint8_t *qWu, const float *swu,
+                        double *H)
+{
+    if (check_i8(M, N, K, qX, sx, qWg, swg) != 0 || check_i8(M, N, K, qX, sx, qWu, swu) != 0) return -1;
+    if (M * N > 0 && !H) return -1;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t i = 0; i < M; ++i)
+        for (int64_t j = 0; j < N; ++j)
+            H[i * N + j] = element_f8_swiglu(i, j, K, qX, sx, qWg, swg, qWu, swu);
+    return 0;
+}
+
+int ka_oracle_f8_swiglu_at(int64_t M, int64_t N, int64_t K, const uint8_t *qX, const float *sx,
+                           const uint8_t *qWg, const float *swg, const uint8_t *qWu, const float *swu,
+                           int64_t n, const int64_t *rows, const int64_t *cols, double *out)
+{
+    if (check_i8(M, N, K, qX, sx, qWg, swg) != 0 || check_i8(M, N, K, qX, sx, qWu, swu) != 0 || n < 0)
+        return -1;
+    for (int64_t t = 0; t < n; ++t)
+        if (rows[t] < 0 || rows[t] >= M || cols[t] < 0 || cols[t] >= N) return -1;
+#pragma omp parallel for schedule(dynamic, 16)
+    for (int64_t t = 0; t < n; ++t)
+        out[t] = element_f8_swiglu(rows[t], cols[t], K, qX, sx, qWg, swg, qWu, swu);
     return 0;
 }
 

@@ -38,6 +38,13 @@ random binary32 scales, reduction to the bf16 oracles (already pinned) when
 power-of-two scales make every dequantised operand an exact bf16 value, a
 zero weight, and the 60-digit decimal SiLU.
 
+The FP8 forms (``F8_PINS``: E4M3 operands with the same scales) are pinned
+by the decoding of all 256 bit patterns against torch's float8_e4m3fn, the
+format's landmarks (1, 448, the smallest normal and subnormal, NaN), exact
+rational dequantisation with random scales, and bit-identity with the bf16
+oracles when power-of-two scales make every dequantised operand an exact bf16
+value.
+
 The grouped forms over an expert-major padded layout (``GRP_PINS``: per
 expert e, Y[e,i] = X[e,i] W[e]^T for the rows i below counts[e] clamped to
 [0, M_pad]) are pinned by exact rational brute force with empty, partial,
@@ -684,6 +691,88 @@ I8_PINS = [
     pin_i8_at_matches_full,
 ]
 
+# -------------------------------------------------------------------- FP8 ----
+def _rand_f8(rng, shape, sigma=8.0):
+    """E4M3 bit patterns of N(0,1)*sigma draws (torch rounds to the format)."""
+    t = torch.from_numpy((rng.standard_normal(shape) * sigma).astype(np.float32))
+    return t.to(torch.float8_e4m3fn).view(torch.uint8).numpy().copy()
+
+
+def pin_f8_decode(orc):
+    """All 256 E4M3 patterns decode as torch's float8_e4m3fn does; landmarks."""
+    bits = np.arange(256, dtype=np.uint8)
+    ours = orc.fp8_decode(bits)
+    ref = torch.from_numpy(bits.copy()).view(torch.float8_e4m3fn).to(torch.float32).numpy().astype(np.float64)
+    assert (np.isnan(ours) == np.isnan(ref)).all()
+    ok = ~np.isnan(ref)
+    np.testing.assert_array_equal(ours[ok], ref[ok])
+    assert np.array_equal(np.signbit(ours[ok]), np.signbit(ref[ok]))
+    land = {0x38: 1.0, 0x7E: 448.0, 0xFE: -448.0, 0x08: 2.0 ** -6, 0x01: 2.0 ** -9, 0x07: 7 * 2.0 ** -9,
+            0x40: 2.0, 0x3C: 1.5}
+    for b, v in land.items():
+        assert ours[b] == v, (hex(b), ours[b], v)
+    assert np.isnan(ours[0x7F]) and np.isnan(ours[0xFF]) and np.isfinite(ours[0x78])
+
+
+def pin_f8_dequant_exact(orc, trials=15, seed=71):
+    rng = np.random.default_rng(seed)
+    for _ in range(trials):
+        M, N, K = (int(v) for v in rng.integers(1, 8, size=3))
+        qX, qW = _rand_f8(rng, (M, K)), _rand_f8(rng, (N, K))
+        sx, sw = _rand_scales(rng, M), _rand_scales(rng, N)
+        R = _rand_bits(rng, (M, N)) if rng.random() < 0.5 else None
+        Y = orc.f8_linear(qX, sx, qW, sw, R)
+        xd, wd = orc.fp8_decode(qX), orc.fp8_decode(qW)
+        rf = bf16_bits_to_f64(R) if R is not None else None
+        for i in range(M):
+            for j in range(N):
+                s_ = sum((Fraction(xd[i, k]) * Fraction(wd[j, k]) for k in range(K)), Fraction(0))
+                mag = sum(abs(Fraction(xd[i, k]) * Fraction(wd[j, k])) for k in range(K))
+                sc = Fraction(float(sx[i])) * Fraction(float(sw[j]))
+                exact = sc * s_
+                bound = sc * mag / 2**50
+                if rf is not None:
+                    exact += Fraction(rf[i, j])
+                    bound += abs(Fraction(rf[i, j])) / 2**52
+                assert abs(Fraction(Y[i, j]) - exact) <= bound + Fraction(1, 2**1074), (i, j)
+
+
+def pin_f8_matches_bf16_oracle(orc, seed=72):
+    """Power-of-two scales: the dequantised FP8 operands are exact bf16 values
+    and the FP8 oracle equals the (pinned) bf16 oracles bit for bit."""
+    rng = np.random.default_rng(seed)
+    M, N, K = 11, 13, 80
+    qX, qW, qWu = _rand_f8(rng, (M, K)), _rand_f8(rng, (N, K)), _rand_f8(rng, (N, K))
+    sx, sw, swu = _pow2_scales(rng, M, -4, 3), _pow2_scales(rng, N, -9, -4), _pow2_scales(rng, N, -9, -4)
+    R = _rand_bits(rng, (M, N))
+    Xb = _bf16_from_f64(orc.fp8_decode(qX) * sx[:, None].astype(np.float64))
+    Wb = _bf16_from_f64(orc.fp8_decode(qW) * sw[:, None].astype(np.float64))
+    Wub = _bf16_from_f64(orc.fp8_decode(qWu) * swu[:, None].astype(np.float64))
+    np.testing.assert_array_equal(orc.f8_linear(qX, sx, qW, sw, R), orc.linear(Xb, Wb, R))
+    np.testing.assert_array_equal(orc.f8_swiglu(qX, sx, qW, sw, qWu, swu), orc.swiglu(Xb, Wb, Wub))
+
+
+def pin_f8_at_matches_full(orc, seed=73):
+    rng = np.random.default_rng(seed)
+    M, N, K = 7, 9, 24
+    qX, qW, qWu = _rand_f8(rng, (M, K)), _rand_f8(rng, (N, K)), _rand_f8(rng, (N, K))
+    sx, sw, swu = _rand_scales(rng, M), _rand_scales(rng, N), _rand_scales(rng, N)
+    R = _rand_bits(rng, (M, N))
+    rows, cols = rng.integers(0, M, 40), rng.integers(0, N, 40)
+    np.testing.assert_array_equal(orc.f8_linear_at(qX, sx, qW, sw, R, rows, cols),
+                                  orc.f8_linear(qX, sx, qW, sw, R)[rows, cols])
+    np.testing.assert_array_equal(orc.f8_swiglu_at(qX, sx, qW, sw, qWu, swu, rows, cols),
+                                  orc.f8_swiglu(qX, sx, qW, sw, qWu, swu)[rows, cols])
+
+
+F8_PINS = [
+    pin_f8_decode,
+    pin_f8_dequant_exact,
+    pin_f8_matches_bf16_oracle,
+    pin_f8_at_matches_full,
+]
+
+
 # ---------------------------------------------------------------- grouped ----
 def _rows_of(counts, e, Mpad):
     return Mpad if counts is None else int(min(max(int(counts[e]), 0), Mpad))
@@ -793,4 +882,4 @@ ALL_PINS = [
     pin_round_midpoints,
     pin_round_specials,
     pin_round_like_torch,
-] + EX_PINS + GLU_PINS + I8_PINS + GRP_PINS
+] + EX_PINS + GLU_PINS + I8_PINS + F8_PINS + GRP_PINS

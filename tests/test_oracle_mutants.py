@@ -51,6 +51,11 @@ MUTANTS = {
     "i8_residual_dropped": ("    if (R)\n        y += bf16_bits_to_double(R[i * N + j]);", "    (void)R;"),
     "i8_glu_up_scale_from_gate": ("double u = (double)sx[i] * (double)swu[j]", "double u = (double)sx[i] * (double)swg[j]"),
     "i8_glu_float_gate": ("    double g = (double)sx[i] * (double)swg[j]", "    float g = (double)sx[i] * (double)swg[j]"),
+    "f8_exponent_bias_8": ("v = ldexp((double)(8 + m), e - 10);", "v = ldexp((double)(8 + m), e - 11);"),
+    "f8_subnormals_as_normals": ("v = ldexp((double)m, -9);", "v = ldexp((double)(8 + m), -10);"),
+    "f8_sign_ignored": ("    return sign ? -v : v;\n}\n\nstatic double dot_f8", "    (void)sign;\n    return v;\n}\n\nstatic double dot_f8"),
+    "f8_no_nan": ("    if (e == 15 && m == 7)\n        v = NAN;", "    if (0)\n        v = NAN;"),
+    "f8_mantissa_dropped_bit": ("int m = b & 7;", "int m = b & 6;"),
     "grp_counts_ignored": ("            if (i >= group_rows(counts, e, Mpad)) continue;\n", "            (void)0;\n"),
     "grp_weight_stride": ("element(i, j, N, K, X + e * Mpad * K, W + e * N * K, NULL);",
                           "element(i, j, N, K, X + e * Mpad * K, W + (e / 2) * N * K, NULL);"),
