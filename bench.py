@@ -44,7 +44,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2516.6          # 256 CU x 4096 FLOP/clk x 2.4 GHz, dense
-PEAK_I8_TOPS = 5033.2              # 256 CU x 8192 OP/clk x 2.4 GHz, dense
+PEAK_I8_TOPS = 5033.2              # 256 CU x 8192 OP/clk x 2.4 GHz, dense (int8 and fp8)
 PEAK_HBM_GBPS = 8000.0
 ROTATE_BYTES = 1 << 30
 MAX_COPIES = 256
@@ -57,7 +57,7 @@ def log(msg):
 
 def mfma_peak(w):
     """Dense MFMA peak (T op/s) of the workload's operand type."""
-    return PEAK_I8_TOPS if getattr(w, "int8", False) else PEAK_BF16_TFLOPS
+    return PEAK_I8_TOPS if getattr(w, "eight_bit", False) else PEAK_BF16_TFLOPS
 
 
 def roofline_time(w):
@@ -261,17 +261,21 @@ class I8Case(Case):
             d["Y"] = torch.empty(w.M, w.N, dtype=torch.bfloat16, device="cuda")
             self.sets.append(d)
         self.forced = plan
-        self.plan = ka.select_plan_i8(w.M, w.N, w.K, w.swiglu) if plan is None else plan
+        select = ka.select_plan_i8 if w.fmt == "i8" else ka.select_plan_f8
+        self.plan = select(w.M, w.N, w.K, w.swiglu) if plan is None else plan
         self.plan_name = ka.plan_name(self.plan)
         self.times = []
         self.graph = None
 
     def call(self, ka, i):
         d = self.sets[i]
+        f8 = self.w.fmt == "f8"
         if self.w.swiglu:
-            ka.swiglu_i8(d["qX"], d["sx"], d["qW"], d["sw"], d["qWu"], d["swu"], out=d["Y"], plan=self.forced)
+            (ka.swiglu_f8 if f8 else ka.swiglu_i8)(d["qX"], d["sx"], d["qW"], d["sw"], d["qWu"], d["swu"], out=d["Y"],
+                                                   plan=self.forced)
         else:
-            ka.gemm_i8(d["qX"], d["sx"], d["qW"], d["sw"], d["R"], out=d["Y"], plan=self.forced)
+            (ka.gemm_f8 if f8 else ka.gemm_i8)(d["qX"], d["sx"], d["qW"], d["sw"], d["R"], out=d["Y"],
+                                               plan=self.forced)
 
 
 class GroupedCase(Case):
@@ -344,8 +348,9 @@ def cpu_baseline_grouped(cases, seconds):
 
 
 def cpu_baseline_i8(cases, seconds):
-    """The oracle's INT8 forms on rows 0, 1, ... of each case until its time share is used."""
+    """The oracle's INT8 / FP8 forms on rows 0, 1, ... of each case until its time share is used."""
     import numpy as np
+    import torch
     import oracle
     from paper_2608_17071_amd import workloads as wl
 
@@ -354,16 +359,22 @@ def cpu_baseline_i8(cases, seconds):
     rates, rows_done = [], []
     for c in cases:
         w, h = c.w, c.host
-        qx, sx, qw, sw = h["qX"].numpy(), h["sx"].numpy(), h["qW"].numpy(), h["sw"].numpy()
+        f8 = w.fmt == "f8"
+
+        def raw(t):
+            return t.view(torch.uint8).numpy() if f8 else t.numpy()
+
+        qx, sx, qw, sw = raw(h["qX"]), h["sx"].numpy(), raw(h["qW"]), h["sw"].numpy()
         rb = wl.bits(h["R"]) if h["R"] is not None else None
         cols = np.arange(w.N, dtype=np.int64)
         ops, rows, t0 = 0, 0, time.perf_counter()
         while rows < w.M:
             r = np.full(w.N, rows, dtype=np.int64)
             if w.swiglu:
-                orc.i8_swiglu_at(qx, sx, qw, sw, h["qWu"].numpy(), h["swu"].numpy(), r, cols)
+                (orc.f8_swiglu_at if f8 else orc.i8_swiglu_at)(qx, sx, qw, sw, raw(h["qWu"]), h["swu"].numpy(), r,
+                                                                cols)
             else:
-                orc.i8_linear_at(qx, sx, qw, sw, rb, r, cols)
+                (orc.f8_linear_at if f8 else orc.i8_linear_at)(qx, sx, qw, sw, rb, r, cols)
             rows += 1
             ops += (4 if w.swiglu else 2) * w.N * w.K
             if time.perf_counter() - t0 >= per_shape:
@@ -592,6 +603,8 @@ def main():
                 return GeneralCase(wl.GENERAL_BY_NAME[n], ka, torch, rotate=not args.hot)
             if n in wl.I8_BY_NAME:
                 return I8Case(wl.I8_BY_NAME[n], ka, torch, rotate=not args.hot)
+            if n in wl.F8_BY_NAME:
+                return I8Case(wl.F8_BY_NAME[n], ka, torch, rotate=not args.hot)
             if n in wl.GROUPED_BY_NAME:
                 return GroupedCase(wl.GROUPED_BY_NAME[n], ka, torch, rotate=not args.hot)
             return Case(wl.BY_NAME[n], ka, torch, rotate=not args.hot)
@@ -701,14 +714,15 @@ def main():
             c.free()
         del scases
 
-    # INT8 (NEXT row: the precision axis, W8A8 with the dequantisation fused
-    # into the epilogue, and the decoder layer's INT8 gate/up path with the
-    # SwiGLU epilogue); roofline against the dense int8 MFMA peak.
+    # INT8 and FP8 (NEXT row: the precision axis, W8A8 with the
+    # dequantisation fused into the epilogue, and the decoder layer's INT8
+    # gate/up path with the SwiGLU epilogue); roofline against the dense 8-bit
+    # MFMA peak.
     int8 = None
     if not args.no_int8:
         for c in sweep:
             c.free()
-        icases = [I8Case(w, ka, torch, rotate=not args.hot) for w in wl.I8]
+        icases = [I8Case(w, ka, torch, rotate=not args.hot) for w in wl.I8 + wl.F8]
         time_cases(icases, args.steps, args.warmup, ka, torch, use_graph=not args.no_graph)
         irows = []
         for c in icases:
@@ -717,7 +731,8 @@ def main():
             log(f"  {r['shape']:40s} {r['plan']:28s} {r['us']:9.2f} us {r['tflops']:8.1f} TOP {r['gbps']:7.0f} GB/s  "
                 f"{r['bound']} frac {r['roofline_frac']:.3f}")
         int8 = {"op": "Y = bf16(sx[i] sw[j] sum_k qX qW (+ R)); SwiGLU: silu(sx swg Ag) * (sx swu Au); "
-                      "ops = 2MNK (4MNK for SwiGLU), peak = dense int8 MFMA",
+                      "int8 (i8_*) or FP8 E4M3 (f8_*) operands; ops = 2MNK (4MNK for SwiGLU), "
+                      "peak = dense 8-bit MFMA",
                 "peak_tops": PEAK_I8_TOPS, "shapes": irows,
                 "geomean_tops": round(geomean([r["tflops"] for r in irows]), 3),
                 "geomean_roofline_frac": round(geomean([r["roofline_frac"] for r in irows]), 4)}

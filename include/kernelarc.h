@@ -257,6 +257,42 @@ int kernelarc_select_plan_i8(int64_t M, int64_t N, int64_t K, int swiglu);
 int kernelarc_plan_supports_i8(int plan, int64_t M, int64_t N, int64_t K, int swiglu);
 
 /*
+ * FP8 forms: the INT8 entry points above with OCP FP8 E4M3 operands (the
+ * "FN" variant: bias 7, no infinities, S.1111.111 is NaN, largest finite
+ * 448) in place of int8, the same per-row and per-column float scales,
+ * layout, residual, aliasing and error rules:
+ *
+ *     Y[i,j] = bf16( sx[i] * sw[j] * S[i,j]  (+ R[i,j]) ),  S = sum_k x8(qX[i,k]) x8(qW[j,k])
+ *     H[i,j] = bf16( silu(sx[i] swg[j] Sg[i,j]) * (sx[i] swu[j] Su[i,j]) )
+ *
+ * The products of decoded values are exact in fp32 and S is accumulated in
+ * fp32 (the summation order is not part of the contract); K has no limit
+ * beyond 2^31.  qX, qW, qWg, qWu hold E4M3 bit patterns (one byte each).
+ * 16-byte aligned operands with K a multiple of 16 take the MFMA tile
+ * kernels (v_mfma_scale_f32_32x32x64_f8f6f4 with unit scales, twice the
+ * bf16 rate); anything else a generic kernel with the same contract.
+ */
+int kernelarc_gemm_f8(int64_t M, int64_t N, int64_t K, const void *qX, const float *sx,
+                      const void *qW, const float *sw, const void *R, void *Y, hipStream_t stream);
+
+int kernelarc_gemm_f8_with_plan(int plan, int64_t M, int64_t N, int64_t K, const void *qX,
+                                const float *sx, const void *qW, const float *sw, const void *R,
+                                void *Y, hipStream_t stream);
+
+int kernelarc_swiglu_f8(int64_t M, int64_t N, int64_t K, const void *qX, const float *sx,
+                        const void *qWg, const float *swg, const void *qWu, const float *swu,
+                        void *H, hipStream_t stream);
+
+int kernelarc_swiglu_f8_with_plan(int plan, int64_t M, int64_t N, int64_t K, const void *qX,
+                                  const float *sx, const void *qWg, const float *swg,
+                                  const void *qWu, const float *swu, void *H, hipStream_t stream);
+
+/* Plan choice and plan capability of the FP8 forms (as for INT8). */
+int kernelarc_select_plan_f8(int64_t M, int64_t N, int64_t K, int swiglu);
+
+int kernelarc_plan_supports_f8(int plan, int64_t M, int64_t N, int64_t K, int swiglu);
+
+/*
  * Grouped (per-expert) linear layer and SwiGLU over an expert-major padded
  * layout: the mixture-of-experts case study (Alg. 4) places token-expert
  * pairs in expert-contiguous rows of a [G x M_pad] buffer (gap rows

@@ -386,12 +386,17 @@ int select_glu(int64_t M, int64_t N, int64_t K) {
 // |A| <= K * 2^14 keeps the exact int32 sums in range for K <= 2^16.
 constexpr int64_t I8_MAX_K = int64_t{1} << 16;
 
-bool supports_i8(int plan, int64_t M, int64_t N, int64_t K, bool glu) {
-    if (M < 0 || N < 0 || K < 0 || M > LIMIT_DIM || N > (glu ? LIMIT_DIM / 2 : LIMIT_DIM) || K > I8_MAX_K) return false;
+// FP8 (E4M3) operands share the INT8 path's layout, scales, plans and rules;
+// their tile configurations also need sub-steps of 64 K bytes
+// (tile_f8_ok), and K has no integer-range limit.
+bool supports_i8(int plan, int64_t M, int64_t N, int64_t K, bool glu, bool f8 = false) {
+    if (M < 0 || N < 0 || K < 0 || M > LIMIT_DIM || N > (glu ? LIMIT_DIM / 2 : LIMIT_DIM) ||
+        K > (f8 ? LIMIT_DIM : I8_MAX_K))
+        return false;
     if (plan < 0 || plan >= NUM_PLANS) return false;
     const PlanInfo &pi = PLANS[plan];
     if (pi.kind == KIND_GENERIC) return cdiv(M, 64) * cdiv(N, 64) * 256 <= LIMIT_ITEMS;
-    if (pi.kind != KIND_TILE || K % 16 != 0) return false;
+    if (pi.kind != KIND_TILE || K % 16 != 0 || (f8 && !tile_f8_ok(pi.tile_cfg))) return false;
     return glu ? supports_glu(plan, M, N, K / 2) : supports(plan, M, N, K / 2, true, dense_layout(N, K / 2));
 }
 
@@ -402,12 +407,12 @@ bool supports_i8(int plan, int64_t M, int64_t N, int64_t K, bool glu) {
 // non-tile kernels).  The 256x256 tile runs without the tail split: an
 // INT8 tile covers its K range in half the steps, so the split's partial
 // round trip costs more than the idle CUs it saves (6% at M = 2048 SwiGLU).
-int select_i8(int64_t M, int64_t N, int64_t K, bool glu) {
+int select_i8(int64_t M, int64_t N, int64_t K, bool glu, bool f8 = false) {
     if (M < 0 || N < 0 || K < 0) return -1;
-    if (K % 16 != 0 || K > I8_MAX_K) return PLAN_GENERIC;
+    if (K % 16 != 0 || K > (f8 ? LIMIT_DIM : I8_MAX_K)) return PLAN_GENERIC;
     auto pick = [&](const char *name) {
         const int p = plan_index(name);
-        return (p >= 0 && supports_i8(p, M, N, K, glu)) ? p : -1;
+        return (p >= 0 && supports_i8(p, M, N, K, glu, f8)) ? p : -1;
     };
     int plan = -1;
     if (!glu && M <= 64) {
@@ -417,10 +422,10 @@ int select_i8(int64_t M, int64_t N, int64_t K, bool glu) {
     }
     plan = glu ? select_glu(M, N, K / 2) : select(M, N, K / 2, true, dense_layout(N, K / 2));
     if (plan == plan_index("tile_256x256_k64_w8_tailsplit")) plan = plan_index("tile_256x256_k64_w8");
-    if (plan >= 0 && plan != PLAN_GENERIC && supports_i8(plan, M, N, K, glu)) return plan;
+    if (plan >= 0 && plan != PLAN_GENERIC && supports_i8(plan, M, N, K, glu, f8)) return plan;
     for (const char *name : {"tile_64x64_k128s3_w4_splitk", "tile_64x128_k64s4_w4", "tile_128x128_k64_w4"}) {
-        const int p = plan_index(name);
-        if (p >= 0 && supports_i8(p, M, N, K, glu)) return p;
+        const int p = pick(name);
+        if (p >= 0) return p;
     }
     return PLAN_GENERIC;
 }
@@ -776,16 +781,18 @@ int run_grouped(int plan, bool glu, int64_t G, int64_t Mpad, int64_t N, int64_t 
 // INT8 call.  glu: H = bf16(silu(sx swg Ag) (sx swu Au)) (W2, sw2 the up
 // operands); else Y = bf16(sx sw A (+ R)).  plan < 0: choose.
 int run_i8(int plan, bool glu, int64_t M, int64_t N, int64_t K, const void *X, const float *sx, const void *W,
-           const float *sw, const void *W2, const float *sw2, const void *R, void *Y, hipStream_t stream) {
+           const float *sw, const void *W2, const float *sw2, const void *R, void *Y, hipStream_t stream,
+           bool f8 = false) {
     g_last_error[0] = '\0';
     if (M < 0 || N < 0 || K < 0)
         return fail(KERNELARC_ERR_INVALID_ARG, "negative size M=%lld N=%lld K=%lld", (long long)M,
                     (long long)N, (long long)K);
     if (M > LIMIT_DIM || N > (glu ? LIMIT_DIM / 2 : LIMIT_DIM))
         return fail(KERNELARC_ERR_INVALID_ARG, "a size is too large");
-    if (K > I8_MAX_K)
+    if (!f8 && K > I8_MAX_K)
         return fail(KERNELARC_ERR_INVALID_ARG, "K=%lld above %lld could overflow the int32 sums", (long long)K,
                     (long long)I8_MAX_K);
+    if (K > LIMIT_DIM) return fail(KERNELARC_ERR_INVALID_ARG, "K is 2^31 or more");
     if (plan >= NUM_PLANS) return fail(KERNELARC_ERR_UNSUPPORTED, "unknown plan %d", plan);
     if (M == 0 || N == 0) return KERNELARC_OK;
     if (!Y) return fail(KERNELARC_ERR_INVALID_ARG, "the output is NULL");
@@ -807,12 +814,13 @@ int run_i8(int plan, bool glu, int64_t M, int64_t N, int64_t K, const void *X, c
     const bool vec_ok = aligned16(X) && aligned16(W) && (!glu || aligned16(W2)) && aligned16(Y) &&
                         (!R || aligned16(R)) && K % 16 == 0;
     if (plan < 0) {
-        plan = select_i8(M, N, K, glu);
+        plan = select_i8(M, N, K, glu, f8);
         if (plan != PLAN_GENERIC && !vec_ok) plan = PLAN_GENERIC;
     } else {
-        if (!supports_i8(plan, M, N, K, glu))
-            return fail(KERNELARC_ERR_UNSUPPORTED, "plan %s cannot compute the INT8 %s at M=%lld N=%lld K=%lld",
-                        PLANS[plan].name, glu ? "SwiGLU" : "GEMM", (long long)M, (long long)N, (long long)K);
+        if (!supports_i8(plan, M, N, K, glu, f8))
+            return fail(KERNELARC_ERR_UNSUPPORTED, "plan %s cannot compute the %s %s at M=%lld N=%lld K=%lld",
+                        PLANS[plan].name, f8 ? "FP8" : "INT8", glu ? "SwiGLU" : "GEMM", (long long)M, (long long)N,
+                        (long long)K);
         if (plan != PLAN_GENERIC && !vec_ok)
             return fail(KERNELARC_ERR_UNSUPPORTED, "plan %s needs 16-byte aligned operands and K a multiple of 16",
                         PLANS[plan].name);
@@ -821,7 +829,41 @@ int run_i8(int plan, bool glu, int64_t M, int64_t N, int64_t K, const void *X, c
     hipError_t e = hipSuccess;
     const auto *x8 = static_cast<const int8_t *>(X);
     const auto *w8 = static_cast<const int8_t *>(W);
-    if (PLANS[plan].kind == KIND_GENERIC) {
+    if (f8) {
+        const auto *xf = static_cast<const uint8_t *>(X);
+        const auto *wf = static_cast<const uint8_t *>(W);
+        const bool generic = PLANS[plan].kind == KIND_GENERIC;
+        if (glu) {
+            const F8GluProblem p{M, N, K, xf, wf, static_cast<const uint8_t *>(W2), static_cast<uint16_t *>(Y),
+                                 sx, sw, sw2};
+            if (generic) {
+                e = launch_generic_f8_glu(p, stream);
+            } else {
+                const TileSplit sp = tile_split_plan(plan, M, 2 * N, K / 2);
+                Workspace ws{};
+                if (sp.split > 1) {
+                    const int wst = workspace(dev, stream, &ws);
+                    if (wst != KERNELARC_OK) return wst;
+                }
+                e = launch_tile_f8_glu(PLANS[plan].tile_cfg, p, sp.split, sp.full_tiles, sp.split > 1 ? &ws : nullptr,
+                                       stream);
+            }
+        } else {
+            const F8Problem p{M, N, K, xf, wf, static_cast<const uint16_t *>(R), static_cast<uint16_t *>(Y), sx, sw};
+            if (generic) {
+                e = launch_generic_f8(p, stream);
+            } else {
+                const TileSplit sp = tile_split_plan(plan, M, N, K / 2);
+                Workspace ws{};
+                if (sp.split > 1) {
+                    const int wst = workspace(dev, stream, &ws);
+                    if (wst != KERNELARC_OK) return wst;
+                }
+                e = launch_tile_f8(PLANS[plan].tile_cfg, p, sp.split, sp.full_tiles, sp.split > 1 ? &ws : nullptr,
+                                   stream);
+            }
+        }
+    } else if (PLANS[plan].kind == KIND_GENERIC) {
         if (glu)
             e = launch_generic_i8_glu(I8GluProblem{M, N, K, x8, w8, static_cast<const int8_t *>(W2),
                                                    static_cast<uint16_t *>(Y), sx, sw, sw2},
@@ -965,6 +1007,44 @@ int kernelarc_swiglu_i8_with_plan(int plan, int64_t M, int64_t N, int64_t K, con
 }
 
 int kernelarc_select_plan_i8(int64_t M, int64_t N, int64_t K, int swiglu) { return select_i8(M, N, K, swiglu != 0); }
+
+int kernelarc_gemm_f8(int64_t M, int64_t N, int64_t K, const void *qX, const float *sx, const void *qW,
+                      const float *sw, const void *R, void *Y, hipStream_t stream) {
+    return run_i8(-1, false, M, N, K, qX, sx, qW, sw, nullptr, nullptr, R, Y, stream, true);
+}
+
+int kernelarc_gemm_f8_with_plan(int plan, int64_t M, int64_t N, int64_t K, const void *qX, const float *sx,
+                                const void *qW, const float *sw, const void *R, void *Y, hipStream_t stream) {
+    if (plan < 0) {
+        g_last_error[0] = '\0';
+        return fail(KERNELARC_ERR_UNSUPPORTED, "unknown plan %d", plan);
+    }
+    return run_i8(plan, false, M, N, K, qX, sx, qW, sw, nullptr, nullptr, R, Y, stream, true);
+}
+
+int kernelarc_swiglu_f8(int64_t M, int64_t N, int64_t K, const void *qX, const float *sx, const void *qWg,
+                        const float *swg, const void *qWu, const float *swu, void *H, hipStream_t stream) {
+    return run_i8(-1, true, M, N, K, qX, sx, qWg, swg, qWu, swu, nullptr, H, stream, true);
+}
+
+int kernelarc_swiglu_f8_with_plan(int plan, int64_t M, int64_t N, int64_t K, const void *qX, const float *sx,
+                                  const void *qWg, const float *swg, const void *qWu, const float *swu, void *H,
+                                  hipStream_t stream) {
+    if (plan < 0) {
+        g_last_error[0] = '\0';
+        return fail(KERNELARC_ERR_UNSUPPORTED, "unknown plan %d", plan);
+    }
+    return run_i8(plan, true, M, N, K, qX, sx, qWg, swg, qWu, swu, nullptr, H, stream, true);
+}
+
+int kernelarc_select_plan_f8(int64_t M, int64_t N, int64_t K, int swiglu) {
+    return select_i8(M, N, K, swiglu != 0, true);
+}
+
+int kernelarc_plan_supports_f8(int plan, int64_t M, int64_t N, int64_t K, int swiglu) {
+    if (plan < 0 || plan >= NUM_PLANS || M < 0 || N < 0 || K < 0) return -1;
+    return supports_i8(plan, M, N, K, swiglu != 0, true) ? 1 : 0;
+}
 
 int kernelarc_plan_supports_i8(int plan, int64_t M, int64_t N, int64_t K, int swiglu) {
     if (plan < 0 || plan >= NUM_PLANS || M < 0 || N < 0 || K < 0) return -1;

@@ -108,6 +108,23 @@ struct I8GluProblem {
     const float *sx, *sw, *sw2;  // [M], gate [N], up [N]
 };
 
+// FP8 (OCP E4M3) operands with the same dequantisation scales as the INT8
+// forms: Y = bf16(sx[i] sw[j] S[i,j] (+ R)), S the fp32 sum of the products
+// of the decoded values.  Bit patterns are held as uint8.
+struct F8Problem {
+    int64_t M, N, K;
+    const uint8_t *X, *W;
+    const uint16_t *R;
+    uint16_t *Y;
+    const float *sx, *sw;
+};
+struct F8GluProblem {
+    int64_t M, N, K;
+    const uint8_t *X, *W, *W2;
+    uint16_t *Y;
+    const float *sx, *sw, *sw2;
+};
+
 // Grouped (per-expert) form of a dense problem over an expert-major padded
 // layout: group g owns rows [g*Mpad, (g+1)*Mpad) of X and Y and its own
 // weights (W + g*N*K, and W2 for SwiGLU); its valid rows are counts[g]
@@ -166,6 +183,22 @@ __host__ __device__ inline int64_t ldy_of(const I8GluProblem &p) { return p.N; }
 __host__ __device__ inline float alpha_of(const I8GluProblem &) { return 1.0f; }
 __host__ __device__ inline float beta_of(const I8GluProblem &) { return 1.0f; }
 __host__ __device__ inline const uint16_t *bias_of(const I8GluProblem &) { return nullptr; }
+__host__ __device__ inline int64_t ldx_of(const F8Problem &p) { return p.K; }
+__host__ __device__ inline int64_t ldw_of(const F8Problem &p) { return p.K; }
+__host__ __device__ inline int64_t ldr_of(const F8Problem &p) { return p.N; }
+__host__ __device__ inline int64_t ldy_of(const F8Problem &p) { return p.N; }
+__host__ __device__ inline float alpha_of(const F8Problem &) { return 1.0f; }
+__host__ __device__ inline float beta_of(const F8Problem &) { return 1.0f; }
+__host__ __device__ inline const uint16_t *bias_of(const F8Problem &) { return nullptr; }
+__host__ __device__ inline int64_t ldx_of(const F8GluProblem &p) { return p.K; }
+__host__ __device__ inline int64_t ldw_of(const F8GluProblem &p) { return p.K; }
+__host__ __device__ inline int64_t ldr_of(const F8GluProblem &p) { return p.N; }
+__host__ __device__ inline int64_t ldy_of(const F8GluProblem &p) { return p.N; }
+__host__ __device__ inline float alpha_of(const F8GluProblem &) { return 1.0f; }
+__host__ __device__ inline float beta_of(const F8GluProblem &) { return 1.0f; }
+__host__ __device__ inline const uint16_t *bias_of(const F8GluProblem &) { return nullptr; }
+__host__ __device__ inline const uint16_t *resid_of(const F8Problem &p) { return p.R; }
+__host__ __device__ inline const uint16_t *resid_of(const F8GluProblem &) { return nullptr; }
 __host__ __device__ inline const uint16_t *resid_of(const I8Problem &p) { return p.R; }
 __host__ __device__ inline const uint16_t *resid_of(const I8GluProblem &) { return nullptr; }
 __host__ __device__ inline const uint16_t *resid_of(const Problem &p) { return p.R; }
@@ -219,6 +252,25 @@ __host__ __device__ inline int64_t group_rows(const int32_t *counts, int64_t g, 
     if (!counts) return Mpad;
     const int64_t c = counts[g];
     return c < 0 ? 0 : (c > Mpad ? Mpad : c);
+}
+// FP8: tile kernels (configurations of tile_f8_ok; SwiGLU also tile_glu_ok)
+// and generic kernels.
+bool tile_f8_ok(int cfg);
+hipError_t launch_tile_f8(int cfg, const F8Problem &p, int split, int64_t full_tiles, const Workspace *ws,
+                          hipStream_t s);
+hipError_t launch_tile_f8_glu(int cfg, const F8GluProblem &p, int split, int64_t full_tiles, const Workspace *ws,
+                              hipStream_t s);
+hipError_t launch_generic_f8(const F8Problem &p, hipStream_t s);
+hipError_t launch_generic_f8_glu(const F8GluProblem &p, hipStream_t s);
+// OCP E4M3 (bias 7, no infinities, S.1111.111 = NaN) to fp32, exact.
+__device__ __forceinline__ float fp8_e4m3_to_f32(uint8_t b) {
+    const uint32_t sign = static_cast<uint32_t>(b & 0x80) << 24;
+    const uint32_t e = (b >> 3) & 15, m = b & 7;
+    float v;
+    if (e == 15 && m == 7) v = __builtin_nanf("");
+    else if (e == 0) v = static_cast<float>(m) * 0.001953125f;              // m * 2^-9
+    else v = __uint_as_float(((e + 120) << 23) | (m << 20));                  // (1 + m/8) 2^(e-7)
+    return __uint_as_float(__float_as_uint(v) | sign);
 }
 hipError_t launch_generic_i8(const I8Problem &p, hipStream_t s);
 hipError_t launch_generic_i8_glu(const I8GluProblem &p, hipStream_t s);

@@ -1,6 +1,6 @@
 // Generic kernels: Y = alpha X W^T (+ beta R) (+ bias) for any shape, any
-// row strides and any pointer alignment; SwiGLU, the INT8 forms and the
-// grouped (per-expert) forms for any shape and alignment.
+// row strides and any pointer alignment; SwiGLU, the INT8 and FP8 forms
+// and the grouped (per-expert) forms for any shape and alignment.
 //
 // This is the correctness fallback (K not a multiple of 8, pointers not
 // 16-byte aligned).  Each 256-thread workgroup computes a 64x64 output tile;
@@ -9,6 +9,8 @@
 // checked scalar loads; products of bf16 values are exact in fp32 and the
 // k-terms are accumulated in ascending order.
 #include "internal.h"
+
+#include <type_traits>
 
 namespace kernelarc {
 namespace {
@@ -174,14 +176,21 @@ __global__ __launch_bounds__(256) void generic_grouped_glu_kernel(Grouped<GluPro
     generic_glu_body(q, tile, tiles_n);
 }
 
-// INT8 fallbacks: the same 64x64 tiling with int8 operands staged as int32
-// and exact int32 sums; dequantisation (and the residual, or SwiGLU) in fp32
-// as the tile kernels do it.
+// INT8 and FP8 fallbacks: the same 64x64 tiling with the operands staged
+// as int32 (exact int32 sums) or as decoded fp32 (E4M3 values and their
+// products are exact in fp32); dequantisation (and the residual, or SwiGLU)
+// in fp32 as the tile kernels do it.
+template <class T>
+__device__ __forceinline__ T widen(int8_t v) { return v; }
+template <class T>
+__device__ __forceinline__ T widen(uint8_t v) { return fp8_e4m3_to_f32(v); }
+
 template <bool GLU_, class P>
 __device__ __forceinline__ void generic_i8_body(const P &p, int64_t tiles_n) {
-    __shared__ int xs[GK][GT + 1];
-    __shared__ int gs[GK][GT + 1];
-    __shared__ int us[GLU_ ? GK : 1][GT + 1];
+    using T = typename std::conditional<std::is_same<decltype(p.X), const int8_t *>::value, int, float>::type;
+    __shared__ T xs[GK][GT + 1];
+    __shared__ T gs[GK][GT + 1];
+    __shared__ T us[GLU_ ? GK : 1][GT + 1];
 
     const int tx = threadIdx.x & 15;
     const int ty = threadIdx.x >> 4;
@@ -189,7 +198,7 @@ __device__ __forceinline__ void generic_i8_body(const P &p, int64_t tiles_n) {
     const int64_t m0 = (tile / tiles_n) * GT;
     const int64_t n0 = (tile % tiles_n) * GT;
 
-    int g[4][4], u[4][4];
+    T g[4][4], u[4][4];
 #pragma unroll
     for (int a = 0; a < 4; ++a)
 #pragma unroll
@@ -205,14 +214,14 @@ __device__ __forceinline__ void generic_i8_body(const P &p, int64_t tiles_n) {
             const int64_t xm = m0 + r;
             const int64_t wn = n0 + r;
             const bool kin = k < p.K;
-            xs[kk][r] = (xm < p.M && kin) ? p.X[xm * p.K + k] : 0;
-            gs[kk][r] = (wn < p.N && kin) ? p.W[wn * p.K + k] : 0;
-            if constexpr (GLU_) us[kk][r] = (wn < p.N && kin) ? p.W2[wn * p.K + k] : 0;
+            xs[kk][r] = (xm < p.M && kin) ? widen<T>(p.X[xm * p.K + k]) : T(0);
+            gs[kk][r] = (wn < p.N && kin) ? widen<T>(p.W[wn * p.K + k]) : T(0);
+            if constexpr (GLU_) us[kk][r] = (wn < p.N && kin) ? widen<T>(p.W2[wn * p.K + k]) : T(0);
         }
         __syncthreads();
 #pragma unroll
         for (int kk = 0; kk < GK; ++kk) {
-            int xv[4], gv[4], uv[4];
+            T xv[4], gv[4], uv[4];
 #pragma unroll
             for (int a = 0; a < 4; ++a) xv[a] = xs[kk][ty + 16 * a];
 #pragma unroll
@@ -262,12 +271,34 @@ __global__ __launch_bounds__(256) void generic_i8_glu_kernel(I8GluProblem p, int
     generic_i8_body<true>(p, tiles_n);
 }
 
+__global__ __launch_bounds__(256) void generic_f8_kernel(F8Problem p, int64_t tiles_n) {
+    generic_i8_body<false>(p, tiles_n);
+}
+
+__global__ __launch_bounds__(256) void generic_f8_glu_kernel(F8GluProblem p, int64_t tiles_n) {
+    generic_i8_body<true>(p, tiles_n);
+}
+
 }  // namespace
 
 hipError_t launch_generic_i8(const I8Problem &p, hipStream_t s) {
     const int64_t tiles_n = (p.N + GT - 1) / GT;
     const int64_t tiles = ((p.M + GT - 1) / GT) * tiles_n;
     hipLaunchKernelGGL(generic_i8_kernel, dim3(static_cast<unsigned>(tiles)), dim3(256), 0, s, p, tiles_n);
+    return hipGetLastError();
+}
+
+hipError_t launch_generic_f8(const F8Problem &p, hipStream_t s) {
+    const int64_t tiles_n = (p.N + GT - 1) / GT;
+    const int64_t tiles = ((p.M + GT - 1) / GT) * tiles_n;
+    hipLaunchKernelGGL(generic_f8_kernel, dim3(static_cast<unsigned>(tiles)), dim3(256), 0, s, p, tiles_n);
+    return hipGetLastError();
+}
+
+hipError_t launch_generic_f8_glu(const F8GluProblem &p, hipStream_t s) {
+    const int64_t tiles_n = (p.N + GT - 1) / GT;
+    const int64_t tiles = ((p.M + GT - 1) / GT) * tiles_n;
+    hipLaunchKernelGGL(generic_f8_glu_kernel, dim3(static_cast<unsigned>(tiles)), dim3(256), 0, s, p, tiles_n);
     return hipGetLastError();
 }
 

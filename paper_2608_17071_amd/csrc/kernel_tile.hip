@@ -43,6 +43,7 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 typedef int i32x16 __attribute__((ext_vector_type(16)));
+typedef int i32x8 __attribute__((ext_vector_type(8)));
 typedef __attribute__((address_space(3))) void lds_void;
 
 // Word 3 of a raw (unswizzled, stride 0) gfx9 buffer resource.
@@ -204,6 +205,25 @@ __device__ __forceinline__ void read_frag(const char *a_base, const char *b_base
         fa[r - C::TN] = *reinterpret_cast<const bf16x8 *>(a_base + (r - C::TN) * 32 * C::ROW_BYTES + col);
 }
 
+// FP8 fragment read r (same order as read_frag): 32 bytes per lane, the two
+// 16-byte chunks at byte columns col and col2 of the lane's row (the 64 K
+// bytes of one v_mfma_scale_f32_32x32x64_f8f6f4 split between the lane
+// halves; A and B use the same byte-to-K assignment, so the sum over K is
+// the full one whatever order the instruction takes its bytes in).
+template <class C, int r>
+__device__ __forceinline__ void read_frag8(const char *a_base, const char *b_base, int col, int col2, i32x8 *fa,
+                                           i32x8 *fb) {
+    const char *base = r == 0 ? a_base
+                       : r <= C::TN ? b_base + (r - 1) * 32 * C::ROW_BYTES
+                                    : a_base + (r - C::TN) * 32 * C::ROW_BYTES;
+    const i32x4 lo = *reinterpret_cast<const i32x4 *>(base + col);
+    const i32x4 hi = *reinterpret_cast<const i32x4 *>(base + col2);
+    const i32x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    if constexpr (r == 0) fa[0] = v;
+    else if constexpr (r <= C::TN) fb[r - 1] = v;
+    else fa[r - C::TN] = v;
+}
+
 // Workgroup barrier that keeps the newest N LDS-direct loads of each wave
 // in flight.  A __syncthreads() here would drain every outstanding load
 // (its fence waits for vmcnt(0)) and so empty the staging ring at every K
@@ -257,6 +277,9 @@ struct SplitK {
 // P = I8Problem, I8GluProblem: the same with int8 operands (a stage holds
 // twice the K elements, v_mfma_i32_32x32x32_i8 accumulates exactly in
 // int32) and dequantisation by the row and column scales in the epilogue;
+// P = F8Problem, F8GluProblem: the same with FP8 E4M3 operands
+// (v_mfma_scale_f32_32x32x64_f8f6f4 with unit scales, fp32 accumulation,
+// sub-steps of 64 K bytes);
 // P = Grouped<DenseProblem>, Grouped<GluProblem>: one launch over the groups
 // of an expert-major padded layout; the m-tiles of the groups are stacked
 // (tiles_m = G * m-tiles per group), each workgroup rebases the problem on
@@ -269,8 +292,11 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
     constexpr bool GROUPED = grouped_trait<P>::value;
     constexpr bool GEN = std::is_same<PB, Problem>::value;
     constexpr bool I8 = std::is_same<PB, I8Problem>::value || std::is_same<PB, I8GluProblem>::value;
-    constexpr bool GLU = std::is_same<PB, GluProblem>::value || std::is_same<PB, I8GluProblem>::value;
-    constexpr int EB = I8 ? 1 : 2;                 // bytes per operand element
+    constexpr bool F8 = std::is_same<PB, F8Problem>::value || std::is_same<PB, F8GluProblem>::value;
+    constexpr bool Q8 = I8 || F8;                  // 1-byte operands with dequantisation scales
+    constexpr bool GLU = std::is_same<PB, GluProblem>::value || std::is_same<PB, I8GluProblem>::value ||
+                         std::is_same<PB, F8GluProblem>::value;
+    constexpr int EB = Q8 ? 1 : 2;                 // bytes per operand element
     constexpr int BKE = C::ROW_BYTES / EB;         // K elements per stage
     constexpr int CKE = 16 / EB;                   // K elements per 16-byte chunk
     using AccV = typename std::conditional<I8, i32x16, f32x16>::type;
@@ -455,8 +481,8 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
     // ahead.  Plain: the scales of the lane's 8 columns and of its row in
     // each pass; SwiGLU: the gate and up scales of the lane's column in each
     // block pair and the scales of the slab's 16 accumulator rows.
-    constexpr int NSX = !I8 ? 1 : GLU ? 16 : PASSES;
-    constexpr int NSW = !I8 ? 1 : GLU ? C::TN : 8;
+    constexpr int NSX = !Q8 ? 1 : GLU ? 16 : PASSES;
+    constexpr int NSW = !Q8 ? 1 : GLU ? C::TN : 8;
     float sxr[2][NSX], swc[NSW];
     [[maybe_unused]] __amdgpu_buffer_rsrc_t rsx;
     auto ld = [](const __amdgpu_buffer_rsrc_t &r, uint32_t off) {
@@ -473,7 +499,7 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
             for (int v = 0; v < PASSES; ++v) sxr[i & 1][v] = ld(rsx, static_cast<uint32_t>(row_of(i, v) * 4));
         }
     };
-    if constexpr (I8) {
+    if constexpr (Q8) {
         rsx = make_rsrc(p.sx + m0, static_cast<uint32_t>(rows_y * 4));
         const __amdgpu_buffer_rsrc_t rsw = make_rsrc(p.sw, static_cast<uint32_t>(N * 4));
         if constexpr (GLU) {
@@ -507,7 +533,10 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
     // the refill (step kt + STAGES into this buffer) go among those last
     // MFMAs, whose operands are already in registers.  The instruction order
     // is pinned slot by slot (one MFMA and its share of reads and loads).
-    constexpr int KS = C::KSTEPS, PD = C::PD, NSETS = PD + 1;
+    // One MFMA sub-step covers 32 bytes of K per row (bf16 32x32x16, int8
+    // 32x32x32) or 64 (FP8 32x32x64).
+    constexpr int KS = F8 ? C::KSTEPS / 2 : C::KSTEPS, PD = C::PD, NSETS = PD + 1;
+    static_assert(KS > PD && KS % NSETS == 0, "fragment prefetch distance");
     constexpr int MF = C::TM * C::TN, FR = C::TM + C::TN, POST = PD * MF, SLOTS = KS * MF;
     // Loads a wave may leave in flight at a step's barrier (step kt+1 must
     // have landed): the steps requested after it, and with the lagged
@@ -515,10 +544,25 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
     constexpr int LPRE = C::LAG ? ((KS - PD) * MF * C::LOADS) / SLOTS : 0;
     constexpr int VM_KEEP = C::LAG ? C::LOADS * (C::STAGES - 3) + LPRE : C::LOADS * (C::STAGES - 2);
     constexpr int VM_KEEP0 = C::LOADS * (C::STAGES - 2);   // prologue: step g0 landed
-    int colk[KS];
+    int colk[KS], colk2[KS];
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) colk[ks] = ((2 * ks + hi) ^ frag_swz) * 16;
-    bf16x8 fa[NSETS][C::TM], fb[NSETS][C::TN];
+    for (int ks = 0; ks < KS; ++ks) {
+        if constexpr (F8) {
+            colk[ks] = ((4 * ks + 2 * hi) ^ frag_swz) * 16;
+            colk2[ks] = ((4 * ks + 2 * hi + 1) ^ frag_swz) * 16;
+        } else {
+            colk[ks] = ((2 * ks + hi) ^ frag_swz) * 16;
+            colk2[ks] = 0;
+        }
+    }
+    using Frag = typename std::conditional<F8, i32x8, bf16x8>::type;
+    Frag fa[NSETS][C::TM], fb[NSETS][C::TN];
+    auto read_any = [&](auto rc, const char *src, int col, int col2, Frag *ta, Frag *tb) {
+        if constexpr (F8)
+            read_frag8<C, decltype(rc)::value>(src + a_row_byte, src + C::A_BYTES + b_row_byte, col, col2, ta, tb);
+        else
+            read_frag<C, decltype(rc)::value>(src + a_row_byte, src + C::A_BYTES + b_row_byte, col, ta, tb);
+    };
 
     // Prologue: steps g0 .. g0+STAGES-2 requested, step g0 landed in every
     // wave, the fragments of its first PD sub-steps requested, then step
@@ -531,10 +575,7 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
     stage_barrier<VM_KEEP0>();
     static_for<0, PD>([&](auto ksc) {
         constexpr int ks = decltype(ksc)::value;
-        static_for<0, FR>([&](auto rc) {
-            read_frag<C, decltype(rc)::value>(glds + a_row_byte, glds + C::A_BYTES + b_row_byte, colk[ks],
-                                              fa[ks], fb[ks]);
-        });
+        static_for<0, FR>([&](auto rc) { read_any(rc, glds, colk[ks], colk2[ks], fa[ks], fb[ks]); });
     });
     if constexpr (!C::LAG)
         issue_stage<C, GLU, BKE>(glds + (C::STAGES - 1) * C::STAGE_BYTES, ra, rb, rb2, a_off, a_k, b_off, b_k,
@@ -558,7 +599,7 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
             constexpr int tgt = ks + PD;              // sub-step whose fragments are read
             constexpr int tset = tgt % NSETS;
             const char *const src = tgt < KS ? cur : nxt;
-            const int tcol = colk[tgt % KS];
+            const int tcol = colk[tgt % KS], tcol2 = colk2[tgt % KS];
             static_for<0, MF>([&](auto tc) {
                 constexpr int t = decltype(tc)::value;
                 constexpr int i = t / C::TN, j = t % C::TN;
@@ -566,12 +607,14 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
                     acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(__builtin_bit_cast(i32x4, fa[set][i]),
                                                                       __builtin_bit_cast(i32x4, fb[set][j]),
                                                                       acc[i][j], 0, 0, 0);
+                else if constexpr (F8)
+                    // A and B as E4M3 (format codes 0), unit E8M0 scales (127).
+                    acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fa[set][i], fb[set][j], acc[i][j], 0,
+                                                                                0, 0, 127, 0, 127);
                 else
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[set][i], fb[set][j], acc[i][j], 0, 0, 0);
-                static_for<t * FR / MF, (t + 1) * FR / MF>([&](auto rc) {
-                    read_frag<C, decltype(rc)::value>(src + a_row_byte, src + C::A_BYTES + b_row_byte, tcol,
-                                                      fa[tset], fb[tset]);
-                });
+                static_for<t * FR / MF, (t + 1) * FR / MF>(
+                    [&](auto rc) { read_any(rc, src, tcol, tcol2, fa[tset], fb[tset]); });
                 if constexpr (C::LAG) {
                     constexpr int u = ks * MF + t;
                     static_for<u * C::LOADS / SLOTS, (u + 1) * C::LOADS / SLOTS>([&](auto q) {
@@ -745,7 +788,7 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
 #pragma unroll
     for (int i = 0; i < C::TM; ++i) {
         if (owner && vec && has_r && i + 1 < C::TM) load_r(i + 1, rv[(i + 1) & 1]);
-        if constexpr (I8)
+        if constexpr (Q8)
             if (owner && i + 1 < C::TM) load_sx(i + 1);
         if (owner) {
             if constexpr (GLU) {
@@ -756,7 +799,7 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
 #pragma unroll
                     for (int e = 0; e < 16; ++e) {
                         float g, u;
-                        if constexpr (I8) {
+                        if constexpr (Q8) {
                             const float sr = sxr[i & 1][e];
                             g = static_cast<float>(acc[i][2 * j][e]) * (sr * swc[j]);
                             u = static_cast<float>(acc[i][2 * j + 1][e]) * (sr * swc[C::TN / 2 + j]);
@@ -783,7 +826,7 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
                 float y[8];
 #pragma unroll
                 for (int t = 0; t < 8; ++t) y[t] = src[t];
-                if constexpr (I8 && !GLU) {
+                if constexpr (Q8 && !GLU) {
                     const float sr = sxr[i & 1][v];
 #pragma unroll
                     for (int t = 0; t < 8; ++t) y[t] *= sr * swc[t];
@@ -1058,6 +1101,56 @@ hipError_t launch_tile_grouped_glu(int cfg, const Grouped<GluProblem> &p, hipStr
         using C = decltype(c);
         if constexpr (std::is_same<C, std::nullptr_t>::value) return hipErrorInvalidValue;
         else return launch_cfg_grouped<C>(p, s);
+    });
+}
+
+// FP8 needs sub-steps of 64 K bytes that split into fragment-prefetch sets.
+template <class C>
+constexpr bool f8_ok() { return C::KSTEPS / 2 > C::PD && (C::KSTEPS / 2) % (C::PD + 1) == 0; }
+
+template <class C, class P>
+hipError_t launch_cfg_q8(const P &p, int group_m, int split, int64_t full_tiles, const Workspace *ws,
+                         hipStream_t s) {
+    constexpr bool GLU = std::is_same<P, F8GluProblem>::value;
+    if constexpr (!f8_ok<C>() || (GLU && !glu_ok<C>())) {
+        return hipErrorInvalidValue;
+    } else {
+        constexpr int BNO = GLU ? C::BN / 2 : C::BN;
+        const int64_t tiles_m = (p.M + C::BM - 1) / C::BM;
+        const int64_t tiles_n = (p.N + BNO - 1) / BNO;
+        const int64_t tiles = tiles_m * tiles_n;
+        SplitK sk;
+        if (!split_args<C, 2 * C::BK>(p.K, tiles, split, full_tiles, ws, sk)) return hipErrorInvalidValue;
+        const int64_t wgs = sk.full_tiles + (tiles - sk.full_tiles) * sk.split;
+        hipLaunchKernelGGL((tile_kernel<C, P>), dim3(static_cast<unsigned>(wgs)), dim3(C::THREADS), 0, s, p, tiles_m,
+                           tiles_n, group_m, sk);
+        return hipGetLastError();
+    }
+}
+
+bool tile_f8_ok(int cfg) {
+    return with_cfg(cfg, [](auto c, int) {
+        using C = decltype(c);
+        if constexpr (std::is_same<C, std::nullptr_t>::value) return false;
+        else return f8_ok<C>();
+    });
+}
+
+hipError_t launch_tile_f8(int cfg, const F8Problem &p, int split, int64_t full_tiles, const Workspace *ws,
+                          hipStream_t s) {
+    return with_cfg(cfg, [&](auto c, int) {
+        using C = decltype(c);
+        if constexpr (std::is_same<C, std::nullptr_t>::value) return hipErrorInvalidValue;
+        else return launch_cfg_q8<C>(p, 8, split, full_tiles, ws, s);
+    });
+}
+
+hipError_t launch_tile_f8_glu(int cfg, const F8GluProblem &p, int split, int64_t full_tiles, const Workspace *ws,
+                              hipStream_t s) {
+    return with_cfg(cfg, [&](auto c, int) {
+        using C = decltype(c);
+        if constexpr (std::is_same<C, std::nullptr_t>::value) return hipErrorInvalidValue;
+        else return launch_cfg_q8<C>(p, 8, split, full_tiles, ws, s);
     });
 }
 

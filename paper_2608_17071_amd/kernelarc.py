@@ -65,6 +65,13 @@ _SIGS = {
                                                                _P, _P]),
     "kernelarc_select_plan_grouped": (ctypes.c_int, [_I64, _I64, _I64, _I64, ctypes.c_int]),
     "kernelarc_plan_supports_grouped": (ctypes.c_int, [ctypes.c_int, _I64, _I64, _I64, _I64, ctypes.c_int]),
+    "kernelarc_gemm_f8": (ctypes.c_int, [_I64, _I64, _I64, _P, _P, _P, _P, _P, _P, _P]),
+    "kernelarc_gemm_f8_with_plan": (ctypes.c_int, [ctypes.c_int, _I64, _I64, _I64, _P, _P, _P, _P, _P, _P, _P]),
+    "kernelarc_swiglu_f8": (ctypes.c_int, [_I64, _I64, _I64, _P, _P, _P, _P, _P, _P, _P, _P]),
+    "kernelarc_swiglu_f8_with_plan": (ctypes.c_int, [ctypes.c_int, _I64, _I64, _I64, _P, _P, _P, _P, _P, _P, _P,
+                                                     _P]),
+    "kernelarc_select_plan_f8": (ctypes.c_int, [_I64, _I64, _I64, ctypes.c_int]),
+    "kernelarc_plan_supports_f8": (ctypes.c_int, [ctypes.c_int, _I64, _I64, _I64, ctypes.c_int]),
     "kernelarc_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "kernelarc_last_error": (ctypes.c_char_p, []),
 }
@@ -262,9 +269,9 @@ def plan_supports_swiglu(plan: int, M: int, N: int, K: int) -> bool:
     return _lib.kernelarc_plan_supports_swiglu(plan, M, N, K) == 1
 
 
-def _i8_operand(t, name, shape, device):
-    if t.dtype != torch.int8 or not t.is_cuda or not t.is_contiguous() or tuple(t.shape) != shape:
-        raise ValueError(f"{name} must be a contiguous int8 GPU tensor of shape {shape}")
+def _i8_operand(t, name, shape, device, dtype=torch.int8):
+    if t.dtype != dtype or not t.is_cuda or not t.is_contiguous() or tuple(t.shape) != shape:
+        raise ValueError(f"{name} must be a contiguous {dtype} GPU tensor of shape {shape}")
     if t.device != device:
         raise ValueError(f"{name} is on {t.device}, expected {device}")
 
@@ -274,6 +281,60 @@ def _scales(t, name, n, device):
         raise ValueError(f"{name} must be a contiguous float32 GPU tensor of shape ({n},)")
     if t.device != device:
         raise ValueError(f"{name} is on {t.device}, expected {device}")
+
+
+def _q8_call(fmt, swiglu, qx, sx, ws, r, out, stream, plan):
+    """INT8 (fmt "i8", torch.int8 operands) or FP8 (fmt "f8", torch.float8_e4m3fn
+    operands) call; ws = ((qw, sw),) or ((qwg, swg), (qwu, swu))."""
+    dtype = torch.int8 if fmt == "i8" else torch.float8_e4m3fn
+    if qx.dim() != 2 or any(w.dim() != 2 or w.shape[1] != qx.shape[1] for w, _ in ws):
+        raise ValueError("qx must be [M, K] and the weights [N, K]")
+    M, K = qx.shape
+    N = ws[0][0].shape[0]
+    dev = qx.device
+    _i8_operand(qx, "qx", (M, K), dev, dtype)
+    _scales(sx, "sx", M, dev)
+    for i, (w, s) in enumerate(ws):
+        _i8_operand(w, f"weight {i}", (N, K), dev, dtype)
+        _scales(s, f"scale {i}", N, dev)
+    for name, t in (("r", r), ("out", out)):
+        if t is not None and (t.dtype != torch.bfloat16 or not t.is_cuda or not t.is_contiguous()
+                              or tuple(t.shape) != (M, N) or t.device != dev):
+            raise ValueError(f"{name} must be a contiguous bfloat16 GPU tensor of shape {(M, N)}")
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+    wargs = []
+    for w, s in ws:
+        wargs += [w.data_ptr(), s.data_ptr()]
+    if swiglu:
+        args = (M, N, K, qx.data_ptr(), sx.data_ptr(), *wargs, out.data_ptr(), _stream_handle(stream))
+    else:
+        args = (M, N, K, qx.data_ptr(), sx.data_ptr(), *wargs, r.data_ptr() if r is not None else None,
+                out.data_ptr(), _stream_handle(stream))
+    name = f"kernelarc_{'swiglu' if swiglu else 'gemm'}_{fmt}"
+    with torch.cuda.device(dev):
+        st = getattr(_lib, name)(*args) if plan is None else getattr(_lib, name + "_with_plan")(plan, *args)
+    _check(st, name if plan is None else f"{name}_with_plan({plan_name(plan)})")
+    return out
+
+
+def gemm_f8(qx, sx, qw, sw, r=None, out=None, stream=None, plan=None):
+    """Y = bf16(sx[i] sw[j] sum_k qX qW (+ R)) with torch.float8_e4m3fn qx [M, K],
+    qw [N, K] and float32 scales sx [M], sw [N]; out may be r (in place)."""
+    return _q8_call("f8", False, qx, sx, ((qw, sw),), r, out, stream, plan)
+
+
+def swiglu_f8(qx, sx, qwg, swg, qwu, swu, out=None, stream=None, plan=None):
+    """H = bf16(silu(sx swg (qX qWg^T)) * (sx swu (qX qWu^T))) with E4M3 operands."""
+    return _q8_call("f8", True, qx, sx, ((qwg, swg), (qwu, swu)), None, out, stream, plan)
+
+
+def select_plan_f8(M: int, N: int, K: int, swiglu: bool = False) -> int:
+    return _lib.kernelarc_select_plan_f8(M, N, K, int(swiglu))
+
+
+def plan_supports_f8(plan: int, M: int, N: int, K: int, swiglu: bool = False) -> bool:
+    return _lib.kernelarc_plan_supports_f8(plan, M, N, K, int(swiglu)) == 1
 
 
 def gemm_i8(qx, sx, qw, sw, r=None, out=None, stream=None, plan=None):

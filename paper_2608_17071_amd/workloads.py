@@ -189,9 +189,9 @@ def make_glu_inputs(w: GluWorkload) -> dict:
 
 @dataclass(frozen=True)
 class I8Workload:
-    """An INT8 call: qX [M,K], qW (or qWg, qWu) [N,K] int8 with float32 scales
-    per row of qX and per output channel; a bf16 residual when `residual`;
-    SwiGLU when `swiglu`."""
+    """An 8-bit call: qX [M,K], qW (or qWg, qWu) [N,K] int8 (fmt "i8") or FP8
+    E4M3 (fmt "f8") with float32 scales per row of qX and per output channel;
+    a bf16 residual when `residual`; SwiGLU when `swiglu`."""
     name: str
     M: int
     N: int
@@ -199,8 +199,9 @@ class I8Workload:
     swiglu: bool
     residual: bool
     seed: int
+    fmt: str = "i8"
 
-    int8 = True     # operands are int8: the roofline uses the int8 MFMA peak
+    eight_bit = True     # 8-bit operands: the roofline uses the 8-bit MFMA peak
 
     @property
     def flops(self) -> int:
@@ -229,22 +230,34 @@ I8 = (
 )
 I8_BY_NAME = {w.name: w for w in I8}
 
+# The same layers with FP8 E4M3 operands.
+F8 = (
+    I8Workload("f8_prefill_m4096_h4096", 4096, 4096, 4096, False, True, 311, "f8"),
+    I8Workload("f8_square_8192", 8192, 8192, 8192, False, False, 312, "f8"),
+    I8Workload("swiglu_f8_prefill_m4096_h4096_i14336", 4096, 14336, 4096, True, False, 313, "f8"),
+)
+F8_BY_NAME = {w.name: w for w in F8}
+
 
 def make_i8_inputs(w: I8Workload) -> dict:
     """Draw, from one seed and in this order: qX = round(N(0,1) * 40) clipped
-    to [-128, 127] (int8); the weight(s) the same way; sx ~ U(0.5, 1.5)/40 per
-    row; per-channel scales ~ U(0.5, 1.5)/(40 sqrt(K)) per weight; R ~ N(0,1)
-    in bf16 when the workload has a residual.  The dequantised sums are then
-    about N(0,1) (the gate spans SiLU's curved range)."""
+    to [-128, 127] (int8), or N(0,1) * 8 rounded to E4M3 (FP8); the weight(s)
+    the same way; sx ~ U(0.5, 1.5)/a per row; per-channel scales
+    ~ U(0.5, 1.5)/(a sqrt(K)) per weight (a = 40 for int8, 8 for FP8); R
+    ~ N(0,1) in bf16 when the workload has a residual.  The dequantised sums
+    are then about N(0,1) (the gate spans SiLU's curved range)."""
     g = torch.Generator().manual_seed(w.seed)
+    amp = 40.0 if w.fmt == "i8" else 8.0
 
     def q(shape):
-        return torch.clamp(torch.round(torch.randn(shape, generator=g) * 40.0), -128, 127).to(torch.int8)
+        if w.fmt == "f8":      # N(0,1) * 8 rounded to E4M3 by torch (|values| stay far below 448)
+            return (torch.randn(shape, generator=g) * amp).to(torch.float8_e4m3fn)
+        return torch.clamp(torch.round(torch.randn(shape, generator=g) * amp), -128, 127).to(torch.int8)
 
     qx = q((w.M, w.K))
     ws = [q((w.N, w.K)) for _ in range(2 if w.swiglu else 1)]
-    sx = ((torch.rand(w.M, generator=g) + 0.5) / 40.0).to(torch.float32)
-    kscale = 40.0 * math.sqrt(w.K) if w.K > 0 else 40.0
+    sx = ((torch.rand(w.M, generator=g) + 0.5) / amp).to(torch.float32)
+    kscale = amp * math.sqrt(w.K) if w.K > 0 else amp
     ss = [((torch.rand(w.N, generator=g) + 0.5) / kscale).to(torch.float32) for _ in ws]
     out = {"qX": qx, "sx": sx, "qW": ws[0], "sw": ss[0], "R": None}
     if w.swiglu:

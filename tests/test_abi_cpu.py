@@ -256,3 +256,14 @@ def test_grouped_validation_and_plans(ka):
     for n in ("tile_128x128_k64_w4_splitk", "tile_256x256_k64_w8_tailsplit", "stream_mfma16_k64_splitk"):
         assert not ka.plan_supports_grouped(names.index(n), 4, 64, 256, 256)
     assert not ka.plan_supports_grouped(names.index("tile_64x64_k64_w4"), 4, 64, 256, 256, True)
+
+
+def test_f8_plans(ka):
+    names = ka.plan_names()
+    for (M, N, K, glu) in [(16, 4096, 4096, 0), (4096, 4096, 4096, 0), (8192, 8192, 8192, 0),
+                           (4096, 14336, 4096, 1), (300, 77, 1024, 1)]:
+        p = ka.select_plan_f8(M, N, K, glu)
+        assert ka.plan_supports_f8(p, M, N, K, glu) and names[p].startswith("tile"), (M, N, K, glu, names[p])
+    assert not ka.plan_supports_f8(names.index("tile_128x128_k32s4_w4"), 64, 1024, 1024)   # 32-byte stages
+    assert ka.plan_supports_f8(names.index("tile_256x256_k64_w8"), 64, 1024, 1 << 17)      # no int32 limit
+    assert ka.select_plan_f8(64, 128, 40) == names.index("generic_64x64_scalar")
