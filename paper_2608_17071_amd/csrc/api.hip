@@ -49,6 +49,7 @@ struct PlanInfo {
     int tile_cfg;   // TileCfg for tile plans, K depth (BK) for stream plans, -1 otherwise
     int split;      // tile and stream plans: 1 = no split-K, 0 = split-K by rule,
                     // -1 (tile) = split only the tiles of a partial last round
+    int stages = 2; // stream plans: per-wave W buffers
 };
 
 const PlanInfo PLANS[] = {
@@ -649,7 +650,7 @@ int run(int plan, Request q, hipStream_t stream) {
                 const int wst = workspace(dev, stream, &ws);
                 if (wst != KERNELARC_OK) return wst;
             }
-            e = launch_stream(p, PLANS[plan].tile_cfg, split, split > 1 ? &ws : nullptr, stream);
+            e = launch_stream(p, PLANS[plan].tile_cfg, PLANS[plan].stages, split, split > 1 ? &ws : nullptr, stream);
             break;
         }
     }

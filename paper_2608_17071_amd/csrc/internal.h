@@ -234,7 +234,7 @@ hipError_t launch_skinny(const Problem &p, int split_k, const Workspace *ws, hip
 // full_tiles > 0 with split > 1: tiles past the first full_tiles (band
 // order) are split in K, the others run whole (see kernel_tile.hip).
 hipError_t launch_tile(int cfg, const Problem &p, int split, int64_t full_tiles, const Workspace *ws, hipStream_t s);
-hipError_t launch_stream(const Problem &p, int bk, int split, const Workspace *ws, hipStream_t s);
+hipError_t launch_stream(const Problem &p, int bk, int stages, int split, const Workspace *ws, hipStream_t s);
 // SwiGLU: the generic kernel, and the tile kernels of the configurations
 // that can pair gate and up blocks (tile_glu_ok).
 hipError_t launch_generic_glu(const GluProblem &p, hipStream_t s);

@@ -9,11 +9,11 @@
 //   * a workgroup of 4 waves owns one 64-row block of W and one K slice;
 //     each wave takes a contiguous quarter of the slice's BK steps and runs
 //     its own pipeline;
-//   * W goes through LDS-direct loads into the wave's private two-buffer
-//     ring (64 rows x BK, 16-byte chunk c of row r at slot c ^ swz(r)); one
-//     load instruction reads 64/(BK/8) whole row segments of BK*2
-//     contiguous bytes, and the wave's own vmcnt says when a buffer has
-//     landed;
+//   * W goes through LDS-direct loads into the wave's private ring of
+//     STAGES buffers (64 rows x BK, 16-byte chunk c of row r at slot
+//     c ^ swz(r)), requested STAGES-1 steps ahead; one load instruction
+//     reads 64/(BK/8) whole row segments of BK*2 contiguous bytes, and the
+//     wave's own vmcnt says when a buffer has landed;
 //   * X (at most 64 rows, L2-resident after first use) is read straight
 //     into MFMA A fragments, one step ahead;
 //   * v_mfma_f32_16x16x32_bf16 with A = 16 rows of X x 32 k and B = 16 rows
@@ -40,7 +40,6 @@ constexpr int AUX_SC1 = 16;   // device-scope (cross-XCD coherent) access
 constexpr int WAVES = 4;
 constexpr int THREADS = 64 * WAVES;
 constexpr int ROWS = 64;      // W rows per workgroup
-constexpr int STAGES = 2;     // per-wave W buffers
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, uint32_t bytes) {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), static_cast<short>(0),
@@ -64,8 +63,10 @@ struct StreamSplit {
     unsigned *counters; // one arrival counter per row block, zero between calls
 };
 
-template <int MB, int BK>
+template <int MB, int BK, int STAGES_>
 struct StreamCfg {
+    static constexpr int STAGES = STAGES_;                // per-wave W buffers
+    static constexpr int PF = STAGES - 1;                 // W steps requested ahead
     static constexpr int CHUNKS = BK / 8, ROW_BYTES = BK * 2, RPI = 64 / CHUNKS;
     static constexpr int STAGE_BYTES = ROWS * ROW_BYTES;
     static constexpr int W_LOADS = STAGE_BYTES / 1024;   // load instructions per stage
@@ -77,12 +78,13 @@ struct StreamCfg {
     static_assert(BK == 64 || BK == 128, "BK");
     static_assert(MB >= 1 && MB <= 4, "token blocks");
     static_assert(RED_BYTES <= LDS_BYTES, "reduction fits in the stage buffers");
-    static_assert(W_LOADS + X_LOADS < 64, "vmcnt range");
+    static_assert(LDS_BYTES <= 160 * 1024, "LDS capacity");
+    static_assert(STAGES >= 2 && PF * (W_LOADS + X_LOADS) < 64, "vmcnt range");
 };
 
-template <int MB, int BK>
+template <int MB, int BK, int STAGES>
 __global__ __launch_bounds__(THREADS) void stream_kernel(DenseProblem p, int64_t nblocks, StreamSplit sk) {
-    using C = StreamCfg<MB, BK>;
+    using C = StreamCfg<MB, BK, STAGES>;
     __shared__ __attribute__((aligned(1024))) char lds[C::LDS_BYTES];
 
     const int lane = threadIdx.x & 63;
@@ -184,24 +186,37 @@ __global__ __launch_bounds__(THREADS) void stream_kernel(DenseProblem p, int64_t
     const int frag_row = lane & 15;
     const int frag_hi = lane >> 4;
 
-    // Pipeline: step t's W is in buffer t % 2, issued one step ahead; X
-    // sub-step s of step t+1 is loaded into the registers of sub-step s of
-    // step t as soon as those have been multiplied (one step of lookahead).
+    // Pipeline: step t's W is in buffer t % STAGES, requested PF = STAGES-1
+    // steps ahead (iteration t requests step t+PF into the buffer that step
+    // t-1 used); X sub-step s of step t+1 is loaded into the registers of
+    // sub-step s of step t as soon as those have been multiplied (one step
+    // of lookahead).  Steps past the wave's range load nothing (out of
+    // range) and only keep the vmcnt bookkeeping uniform.  The waits count
+    // loads in issue order, so every W issue is fenced with scheduling
+    // barriers: no X load may be moved ahead of the W loads it is counted
+    // after.
     bf16x8 xf[C::KS][MB];
     if (nsteps > 0) {
+#pragma unroll
+        for (int u = 0; u < C::PF; ++u) issue_w(u, step0 + u, rem_of(step0 + u, u < nsteps));
+        __builtin_amdgcn_sched_barrier(0);
         const int rem0 = rem_of(step0, true);
-        issue_w(0, step0, rem0);
 #pragma unroll
         for (int s = 0; s < C::KS; ++s) issue_x(xf[s], step0, s, rem0);
     }
+    int buf = 0;
     for (int t = 0; t < nsteps; ++t) {
         const int64_t step = step0 + t;
-        const int buf = t & 1;
+        const int pbuf = buf == 0 ? C::STAGES - 1 : buf - 1;   // the buffer step t-1 used
+        __builtin_amdgcn_sched_barrier(0);
+        issue_w(pbuf, step + C::PF, rem_of(step + C::PF, t + C::PF < nsteps));
+        __builtin_amdgcn_sched_barrier(0);
         const int rem1 = rem_of(step + 1, t + 1 < nsteps);
-        issue_w(buf ^ 1, step + 1, rem1);
-        // Step t's W has landed once only step t+1's W and step t's X (in
-        // issue order after it) may be outstanding.
-        __builtin_amdgcn_s_waitcnt(waitcnt_vm(C::W_LOADS + C::X_LOADS));
+        // Step t's W has landed once only what was issued after it may be
+        // outstanding: the W of steps t+1 .. t+PF and the X of steps
+        // t-PF+1 .. t (one X set per iteration, after that iteration's W).
+        __builtin_amdgcn_s_waitcnt(waitcnt_vm(C::PF * (C::W_LOADS + C::X_LOADS)));
+        __builtin_amdgcn_sched_barrier(0);
         const char *base = ring + buf * C::STAGE_BYTES + frag_row * C::ROW_BYTES;
 #pragma unroll
         for (int s = 0; s < C::KS; ++s) {
@@ -218,6 +233,7 @@ __global__ __launch_bounds__(THREADS) void stream_kernel(DenseProblem p, int64_t
                     acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xf[s][i], wf[j], acc[i][j], 0, 0, 0);
             issue_x(xf[s], step + 1, s, rem1);
         }
+        buf = buf + 1 == C::STAGES ? 0 : buf + 1;
     }
 
     // Add the four wave partials in LDS (wave order).  Wave w then owns row
@@ -298,7 +314,7 @@ __global__ __launch_bounds__(THREADS) void stream_kernel(DenseProblem p, int64_t
         }
 }
 
-template <int MB, int BK>
+template <int MB, int BK, int STAGES>
 hipError_t launch_mb(const Problem &p, int split, const Workspace *ws, hipStream_t s) {
     const int64_t nblocks = (p.N + ROWS - 1) / ROWS;
     StreamSplit sk{1, ((p.K + BK - 1) / BK) * BK, nullptr, nullptr};
@@ -308,18 +324,18 @@ hipError_t launch_mb(const Problem &p, int split, const Workspace *ws, hipStream
         sk.partials = ws->partials;
         sk.counters = ws->counters;
     }
-    hipLaunchKernelGGL((stream_kernel<MB, BK>), dim3(static_cast<unsigned>(nblocks * sk.split)), dim3(THREADS), 0,
-                       s, dense_of(p), nblocks, sk);
+    hipLaunchKernelGGL((stream_kernel<MB, BK, STAGES>), dim3(static_cast<unsigned>(nblocks * sk.split)),
+                       dim3(THREADS), 0, s, dense_of(p), nblocks, sk);
     return hipGetLastError();
 }
 
-template <int BK>
+template <int BK, int STAGES>
 hipError_t launch_bk(const Problem &p, int split, const Workspace *ws, hipStream_t s) {
     switch ((p.M + 15) / 16) {
-        case 1: return launch_mb<1, BK>(p, split, ws, s);
-        case 2: return launch_mb<2, BK>(p, split, ws, s);
-        case 3: return launch_mb<3, BK>(p, split, ws, s);
-        case 4: return launch_mb<4, BK>(p, split, ws, s);
+        case 1: return launch_mb<1, BK, STAGES>(p, split, ws, s);
+        case 2: return launch_mb<2, BK, STAGES>(p, split, ws, s);
+        case 3: return launch_mb<3, BK, STAGES>(p, split, ws, s);
+        case 4: return launch_mb<4, BK, STAGES>(p, split, ws, s);
         default: return hipErrorInvalidValue;
     }
 }
@@ -345,10 +361,10 @@ int64_t stream_workspace_floats(int64_t M, int64_t N, int split) {
 
 int64_t stream_counter_count(int64_t N) { return (N + ROWS - 1) / ROWS; }
 
-hipError_t launch_stream(const Problem &p, int bk, int split, const Workspace *ws, hipStream_t s) {
+hipError_t launch_stream(const Problem &p, int bk, int stages, int split, const Workspace *ws, hipStream_t s) {
     if (p.M < 1 || p.M > 64) return hipErrorInvalidValue;
-    if (bk == 128) return launch_bk<128>(p, split, ws, s);
-    if (bk == 64) return launch_bk<64>(p, split, ws, s);
+    if (bk == 128 && stages == 2) return launch_bk<128, 2>(p, split, ws, s);
+    if (bk == 64 && stages == 2) return launch_bk<64, 2>(p, split, ws, s);
     return hipErrorInvalidValue;
 }
 
