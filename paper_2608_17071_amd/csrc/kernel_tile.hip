@@ -568,18 +568,24 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
     // wave, the fragments of its first PD sub-steps requested, then step
     // g0+STAGES-1 into the last buffer.  Past the end of the range the loads
     // only write zeros into buffers whose contents are never used.
+    // The counted waits assume the steps' loads are issued in step order:
+    // scheduling barriers keep the compiler from interleaving them.
 #pragma unroll
-    for (int s = 0; s < C::STAGES - 1; ++s)
+    for (int s = 0; s < C::STAGES - 1; ++s) {
         issue_stage<C, GLU, BKE>(glds + s * C::STAGE_BYTES, ra, rb, rb2, a_off, a_k, b_off, b_k, wave, g0 + s,
                                  gend);
+        __builtin_amdgcn_sched_barrier(0);
+    }
     stage_barrier<VM_KEEP0>();
     static_for<0, PD>([&](auto ksc) {
         constexpr int ks = decltype(ksc)::value;
         static_for<0, FR>([&](auto rc) { read_any(rc, glds, colk[ks], colk2[ks], fa[ks], fb[ks]); });
     });
+    __builtin_amdgcn_sched_barrier(0);
     if constexpr (!C::LAG)
         issue_stage<C, GLU, BKE>(glds + (C::STAGES - 1) * C::STAGE_BYTES, ra, rb, rb2, a_off, a_k, b_off, b_k,
                                  wave, g0 + C::STAGES - 1, gend);
+    __builtin_amdgcn_sched_barrier(0);
 
     int cur_stage = 0;
     for (int it = 0; it < iters; ++it) {
