@@ -48,8 +48,10 @@ struct PlanInfo {
     PlanKind kind;
     int tile_cfg;   // TileCfg for tile plans, K depth (BK) for stream plans, -1 otherwise
     int split;      // tile and stream plans: 1 = no split-K, 0 = split-K by rule,
-                    // -1 (tile) = split only the tiles of a partial last round
-    int stages = 2; // stream plans: per-wave W buffers
+                    // -1 (tile) = split only the tiles of a partial last round,
+                    // -1 (stream) = split-K by rule, none when the rule says 1
+    int stages = 2; // stream plans: per-wave stage buffers
+    int rows = 64;  // stream plans: W rows per workgroup
 };
 
 const PlanInfo PLANS[] = {
@@ -116,6 +118,11 @@ const PlanInfo PLANS[] = {
     {"tile_32x256_k64s4_w4_splitk", KIND_TILE, TC_32x256_K64_S4_W4, 0},
     {"tile_256x256_k64_w4_tailsplit", KIND_TILE, TC_256x256_K64_S2_W4, -1},
     {"tile_128x256_k64_w8_tailsplit", KIND_TILE, TC_128x256_K64_S2_W8, -1},
+    {"stream_mfma16_r16_k64s4", KIND_STREAM, 64, -1, 4, 16},
+    {"stream_mfma16_r16_k64s8", KIND_STREAM, 64, -1, 8, 16},
+    {"stream_mfma16_r16_k128s2", KIND_STREAM, 128, -1, 2, 16},
+    {"stream_mfma16_r16_k128s4", KIND_STREAM, 128, -1, 4, 16},
+    {"stream_mfma16_r32_k64s4", KIND_STREAM, 64, -1, 4, 32},
 };
 constexpr int NUM_PLANS = static_cast<int>(sizeof(PLANS) / sizeof(PLANS[0]));
 
@@ -171,7 +178,8 @@ int tile_split_of(int plan, int64_t M, int64_t N, int64_t K) { return tile_split
 int stream_split_of(int plan, int64_t M, int64_t N, int64_t K) {
     const PlanInfo &pi = PLANS[plan];
     if (pi.split >= 1) return pi.split;
-    const int rule = stream_split_for(M, N, K, pi.tile_cfg);
+    const int rule = stream_split_for(M, N, K, pi.tile_cfg, pi.rows);
+    if (pi.split < 0) return rule;
     return rule < 2 ? 2 : rule;
 }
 
@@ -208,11 +216,12 @@ bool supports(int plan, int64_t M, int64_t N, int64_t K, bool residual, const La
                    strided_bytes(M, N, lay.ldy) < PANEL_LIMIT && strided_bytes(M, N, lay.ldr) < PANEL_LIMIT;
         case KIND_STREAM: {
             if (lay.general || M < 1 || M > 64 || K % 8 != 0) return false;
-            if (64 * K * 2 >= PANEL_LIMIT || M * N * 2 >= PANEL_LIMIT) return false;
+            if (!stream_config_exists(pi.tile_cfg, pi.stages, pi.rows)) return false;
+            if (pi.rows * K * 2 >= PANEL_LIMIT || M * K * 2 >= PANEL_LIMIT || M * N * 2 >= PANEL_LIMIT) return false;
             const int split = stream_split_of(plan, M, N, K);
-            if (cdiv(N, 64) * split * 256 > LIMIT_ITEMS) return false;
-            if (split > 1 && (stream_workspace_floats(M, N, split) > WS_PARTIAL_FLOATS ||
-                              stream_counter_count(N) > WS_COUNTERS))
+            if (cdiv(N, pi.rows) * split * 256 > LIMIT_ITEMS) return false;
+            if (split > 1 && (stream_workspace_floats(M, N, split, pi.rows) > WS_PARTIAL_FLOATS ||
+                              stream_counter_count(N, pi.rows) > WS_COUNTERS))
                 return false;
             return true;
         }
@@ -256,8 +265,8 @@ const TableEntry TABLE[] = {
     {1, 4096, 4096, 1, "gemv_valu_w4"},
     {1, 5120, 5120, 1, "gemv_valu_w4"},
     {1, 8192, 8192, 1, "gemv_valu_w4"},
-    {16, 4096, 4096, 1, "stream_mfma16_k64_splitk"},
-    {64, 2048, 2048, 1, "tile_64x64_k64s4_w4_splitk"},
+    {16, 4096, 4096, 1, "stream_mfma16_r16_k128s2"},
+    {64, 2048, 2048, 1, "stream_mfma16_r16_k128s2"},
     {64, 4096, 4096, 1, "tile_64x64_k128s3_w4_splitk"},
     {64, 5120, 5120, 1, "tile_64x64_k128s3_w4_splitk"},
     {64, 8192, 8192, 1, "tile_64x64_k128s3_w4_splitk"},
@@ -275,8 +284,11 @@ const TableEntry TABLE[] = {
 };
 
 // Rule-based choice when no table entry matches (from the same
-// measurements): the VALU GEMV up to 4 rows; the streaming kernel with
-// split-K up to 32 rows; up to 1024 rows: 64x64 tiles (3 stages of K depth
+// measurements): the VALU GEMV up to 4 rows; the streaming kernel up to 32
+// rows, with 16-row blocks of W when they fit one round on the CUs (N up to
+// 4096; no cross-workgroup split there) and 64-row blocks with split-K
+// beyond; up to 64 rows, the 16-row streaming kernel while N <= 2048 and
+// K <= 4096; up to 1024 rows: 64x64 tiles (3 stages of K depth
 // 128, split-K) while they fill at most half the CUs, 64x64 tiles (4 stages
 // of depth 64, two per CU) while they fit one round, else 128x128 tiles
 // with 3 stages and split-K when they would keep at most half the CUs busy,
@@ -300,6 +312,9 @@ int select(int64_t M, int64_t N, int64_t K, bool residual, const Layout &lay) {
     };
     int plan = -1;
     if (M >= 1 && M <= 4) plan = pick("gemv_valu_w4");
+    if (plan >= 0) return plan;
+    if (M >= 1 && M <= 64 && cdiv(N, 16) <= CUS && (M <= 32 || (N <= 2048 && K <= 4096)))
+        plan = pick("stream_mfma16_r16_k128s2");
     if (plan >= 0) return plan;
     if (M >= 1 && M <= 32) {
         plan = pick("stream_mfma16_k64_splitk");
@@ -650,7 +665,8 @@ int run(int plan, Request q, hipStream_t stream) {
                 const int wst = workspace(dev, stream, &ws);
                 if (wst != KERNELARC_OK) return wst;
             }
-            e = launch_stream(p, PLANS[plan].tile_cfg, PLANS[plan].stages, split, split > 1 ? &ws : nullptr, stream);
+            e = launch_stream(p, PLANS[plan].tile_cfg, PLANS[plan].stages, PLANS[plan].rows, split,
+                              split > 1 ? &ws : nullptr, stream);
             break;
         }
     }

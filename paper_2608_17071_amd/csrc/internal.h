@@ -234,7 +234,9 @@ hipError_t launch_skinny(const Problem &p, int split_k, const Workspace *ws, hip
 // full_tiles > 0 with split > 1: tiles past the first full_tiles (band
 // order) are split in K, the others run whole (see kernel_tile.hip).
 hipError_t launch_tile(int cfg, const Problem &p, int split, int64_t full_tiles, const Workspace *ws, hipStream_t s);
-hipError_t launch_stream(const Problem &p, int bk, int stages, int split, const Workspace *ws, hipStream_t s);
+hipError_t launch_stream(const Problem &p, int bk, int stages, int rows, int split, const Workspace *ws,
+                         hipStream_t s);
+bool stream_config_exists(int bk, int stages, int rows);
 // SwiGLU: the generic kernel, and the tile kernels of the configurations
 // that can pair gate and up blocks (tile_glu_ok).
 hipError_t launch_generic_glu(const GluProblem &p, hipStream_t s);
@@ -284,9 +286,9 @@ int skinny_split_for(int64_t M, int64_t N, int64_t K);
 int64_t skinny_workspace_floats(int64_t M, int64_t N, int split_k);
 int64_t skinny_counter_count(int64_t N);
 bool gemv_fits(int64_t M, int64_t N, int64_t K, int64_t ldw);
-int stream_split_for(int64_t M, int64_t N, int64_t K, int bk);
-int64_t stream_workspace_floats(int64_t M, int64_t N, int split);
-int64_t stream_counter_count(int64_t N);
+int stream_split_for(int64_t M, int64_t N, int64_t K, int bk, int rows);
+int64_t stream_workspace_floats(int64_t M, int64_t N, int split, int rows);
+int64_t stream_counter_count(int64_t N, int rows);
 
 // ------------------------------------------------------- device helpers ----
 // bf16 <-> fp32.  Widening is exact (bf16 is the top half of a binary32).

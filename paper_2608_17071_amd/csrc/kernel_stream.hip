@@ -6,19 +6,23 @@
 // decides the rate unless each CU keeps several tens of kilobytes in flight.
 // The tile kernels synchronise their waves at every K step; here no wave
 // ever waits for another inside the K loop:
-//   * a workgroup of 4 waves owns one 64-row block of W and one K slice;
-//     each wave takes a contiguous quarter of the slice's BK steps and runs
-//     its own pipeline;
+//   * a workgroup of 4 waves owns one block of ROWS = 16, 32 or 64 rows of
+//     W and one K slice; each wave takes a contiguous quarter of the
+//     slice's BK steps and runs its own pipeline;
 //   * W goes through LDS-direct loads into the wave's private ring of
-//     STAGES buffers (64 rows x BK, 16-byte chunk c of row r at slot
+//     STAGES buffers (ROWS rows x BK, 16-byte chunk c of row r at slot
 //     c ^ swz(r)), requested STAGES-1 steps ahead; one load instruction
 //     reads 64/(BK/8) whole row segments of BK*2 contiguous bytes, and the
 //     wave's own vmcnt says when a buffer has landed;
 //   * X (at most 64 rows, L2-resident after first use) is read straight
 //     into MFMA A fragments, one step ahead;
 //   * v_mfma_f32_16x16x32_bf16 with A = 16 rows of X x 32 k and B = 16 rows
-//     of W x 32 k: MB = ceil(M/16) x 4 blocks per 32-k step, fp32
+//     of W x 32 k: MB = ceil(M/16) x ROWS/16 blocks per 32-k step, fp32
 //     accumulation in K order.
+// Fewer rows per workgroup give more workgroups without a K split (16-row
+// blocks: one workgroup per CU at N = 4096 and no cross-workgroup hand-off)
+// at the price of reading X once per 16 rows of W instead of once per 64;
+// X is small and stays in L2.
 // After the loop the four wave partials are added in LDS in wave order; a
 // split of K across workgroups goes through the fp32 workspace, where the
 // last workgroup of a row block adds the slices in slice order.  The
@@ -39,7 +43,6 @@ constexpr uint32_t OOB_OFFSET = 0x80000000u;
 constexpr int AUX_SC1 = 16;   // device-scope (cross-XCD coherent) access
 constexpr int WAVES = 4;
 constexpr int THREADS = 64 * WAVES;
-constexpr int ROWS = 64;      // W rows per workgroup
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, uint32_t bytes) {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), static_cast<short>(0),
@@ -63,18 +66,39 @@ struct StreamSplit {
     unsigned *counters; // one arrival counter per row block, zero between calls
 };
 
-template <int MB, int BK, int STAGES_>
+// RB 16-row blocks of W per workgroup.
+// X path: with RB = 4 the X fragments go straight from L2 into registers one
+// step ahead.  Loads complete in issue order, so waiting for step t+1's X
+// (issued after step t+PF-1's W) also waits for that W: a deeper W ring
+// would buy nothing, and these configurations keep PF = 1.  With RB < 4
+// each stage holds the step's 16*MB rows of X after its W rows, both moved
+// by LDS-direct loads; every load of a wave is then counted in stage order
+// and the ring is as deep as asked, capped by the vmcnt range and by LDS.
+template <int MB, int BK, int STAGES_, int RB_>
 struct StreamCfg {
-    static constexpr int STAGES = STAGES_;                // per-wave W buffers
-    static constexpr int PF = STAGES - 1;                 // W steps requested ahead
+    static constexpr int RB = RB_, ROWS = 16 * RB;
+    static constexpr bool XL = RB < 4;                    // X staged through LDS
     static constexpr int CHUNKS = BK / 8, ROW_BYTES = BK * 2, RPI = 64 / CHUNKS;
-    static constexpr int STAGE_BYTES = ROWS * ROW_BYTES;
-    static constexpr int W_LOADS = STAGE_BYTES / 1024;   // load instructions per stage
+    static constexpr int W_BYTES = ROWS * ROW_BYTES;
+    static constexpr int X_BYTES = XL ? 16 * MB * ROW_BYTES : 0;
+    static constexpr int STAGE_BYTES = W_BYTES + X_BYTES;
+    static constexpr int W_LOADS = W_BYTES / 1024;       // load instructions per stage
     static constexpr int KS = BK / 32;                    // MFMA k steps per stage
-    static constexpr int X_LOADS = MB * KS;
+    static constexpr int X_LOADS = XL ? X_BYTES / 1024 : MB * KS;
+    static constexpr int PF_VM = 63 / (W_LOADS + X_LOADS);
+    static constexpr int ST_LDS = 160 * 1024 / (WAVES * STAGE_BYTES);
+    static constexpr int ST_CAP = PF_VM + 1 < ST_LDS ? PF_VM + 1 : ST_LDS;
+    static constexpr int STAGES = STAGES_ < ST_CAP ? STAGES_ : ST_CAP;   // per-wave buffers
+    static constexpr int PF = STAGES - 1;                 // steps requested ahead
     static constexpr int WAVE_BYTES = STAGES * STAGE_BYTES;
     static constexpr int LDS_BYTES = WAVES * WAVE_BYTES;
-    static constexpr int RED_BYTES = WAVES * MB * 4 * 64 * 16;   // wave partials, f32x4 per lane
+    static constexpr int RED_BYTES = WAVES * MB * RB * 64 * 16;   // wave partials, f32x4 per lane
+    // After the wave partials are added, wave w writes row block OWN_J(w)
+    // and the EPW accumulator values [e0, e0 + EPW) of each lane's f32x4.
+    static constexpr int EPW = RB;
+    static_assert(RB == 1 || RB == 2 || RB == 4, "row blocks");
+    static_assert(W_BYTES % 1024 == 0 && X_BYTES % 1024 == 0, "whole load instructions per stage");
+    static_assert(XL || STAGES == 2, "register X path: one step ahead");
     static_assert(BK == 64 || BK == 128, "BK");
     static_assert(MB >= 1 && MB <= 4, "token blocks");
     static_assert(RED_BYTES <= LDS_BYTES, "reduction fits in the stage buffers");
@@ -82,16 +106,20 @@ struct StreamCfg {
     static_assert(STAGES >= 2 && PF * (W_LOADS + X_LOADS) < 64, "vmcnt range");
 };
 
-template <int MB, int BK, int STAGES>
+template <int MB, int BK, int STAGES, int RB>
 __global__ __launch_bounds__(THREADS) void stream_kernel(DenseProblem p, int64_t nblocks, StreamSplit sk) {
-    using C = StreamCfg<MB, BK, STAGES>;
+    using C = StreamCfg<MB, BK, STAGES, RB>;
     __shared__ __attribute__((aligned(1024))) char lds[C::LDS_BYTES];
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int64_t nb = blockIdx.x % nblocks;
     const int64_t slice = blockIdx.x / nblocks;
-    const int64_t n0 = nb * ROWS;
+    const int64_t n0 = nb * C::ROWS;
+    // Outputs this wave writes after the reduction: row block j_own, values
+    // [e0, e0 + EPW) of each f32x4.
+    const int j_own = wave * RB / WAVES;
+    const int e0 = (wave % (WAVES / RB)) * RB;
     const int64_t K = p.K;
 
     // K range of the workgroup, then of this wave (a quarter of its steps).
@@ -101,16 +129,16 @@ __global__ __launch_bounds__(THREADS) void stream_kernel(DenseProblem p, int64_t
     const int64_t step0 = kbeg / BK + steps * wave / WAVES;
     const int nsteps = static_cast<int>(steps * (wave + 1) / WAVES - steps * wave / WAVES);
 
-    // Residual of the outputs this lane writes in the epilogue (wave w owns
-    // row block w after the reduction): fetched now, so its latency hides
-    // under the K loop.  Every element is read here before any lane writes
+    // Residual of the outputs of this lane's row block in the epilogue
+    // (all four values; the wave writes EPW of them): fetched now, so its
+    // latency hides under the K loop.  Every element is read here before any lane writes
     // Y, so Y may alias R.
     const int64_t N = p.N;
     const uint32_t ybytes = static_cast<uint32_t>(p.M * N * 2);
     const __amdgpu_buffer_rsrc_t ry = make_rsrc(p.Y, ybytes);
     // Without a residual the R resource is empty: its loads read zero.
     const __amdgpu_buffer_rsrc_t rr = make_rsrc(p.R ? p.R : p.Y, p.R ? ybytes : 0u);
-    const int64_t n_out = n0 + 16 * wave + (lane & 15);
+    const int64_t n_out = n0 + 16 * j_own + (lane & 15);
     // Offset of output (16i + 4*(l/16) + e, n_out): rows past M fall outside
     // the resource; a column past N is pointed out of range.  Computed
     // without branches so the loads below issue back to back.
@@ -127,7 +155,7 @@ __global__ __launch_bounds__(THREADS) void stream_kernel(DenseProblem p, int64_t
 #pragma unroll
         for (int e = 0; e < 4; ++e) rres[i][e] = __builtin_amdgcn_raw_buffer_load_b16(rr, y_off(i, e), 0, 0);
 
-    const int64_t rows_w = (p.N - n0) < ROWS ? (p.N - n0) : ROWS;
+    const int64_t rows_w = (p.N - n0) < C::ROWS ? (p.N - n0) : C::ROWS;
     const __amdgpu_buffer_rsrc_t rw = make_rsrc(p.W + n0 * K, static_cast<uint32_t>(rows_w * K * 2));
     const __amdgpu_buffer_rsrc_t rx = make_rsrc(p.X, static_cast<uint32_t>(p.M * K * 2));
 
@@ -142,8 +170,21 @@ __global__ __launch_bounds__(THREADS) void stream_kernel(DenseProblem p, int64_t
         w_off[q] = static_cast<uint32_t>(r * K * 2 + c * 16);
         w_k[q] = c * 8;
     }
-    // A fragment of token block i at k step s: token 16i + l % 16, k chunk
-    // 4s + l / 16 of the stage.
+    // X staging map (RB < 4), the same map over the 16*MB rows of X (rows
+    // past M fall outside the resource and read zero).
+    uint32_t x_off[C::XL ? C::X_LOADS : 1];
+    int x_kc[C::XL ? C::X_LOADS : 1];
+    if constexpr (C::XL) {
+#pragma unroll
+        for (int q = 0; q < C::X_LOADS; ++q) {
+            const int r = q * C::RPI + lane / C::CHUNKS;
+            const int c = (lane % C::CHUNKS) ^ swz<C::CHUNKS>(r);
+            x_off[q] = static_cast<uint32_t>(r * K * 2 + c * 16);
+            x_kc[q] = c * 8;
+        }
+    }
+    // A fragment of token block i at k step s (register path): token
+    // 16i + l % 16, k chunk 4s + l / 16 of the stage.
     const uint32_t x_row = static_cast<uint32_t>((lane & 15) * K * 2);
     const int x_k = 8 * (lane >> 4);
     char *ring = lds + wave * C::WAVE_BYTES;
@@ -163,6 +204,14 @@ __global__ __launch_bounds__(THREADS) void stream_kernel(DenseProblem p, int64_t
             __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_void *)(ring + buf * C::STAGE_BYTES + q * 1024), 16,
                                                      off, 0, 0, 0);
         }
+        if constexpr (C::XL) {
+#pragma unroll
+            for (int q = 0; q < C::X_LOADS; ++q) {
+                const uint32_t off = x_kc[q] < rem ? x_off[q] + kb2 : OOB_OFFSET;
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    rx, (lds_void *)(ring + buf * C::STAGE_BYTES + C::W_BYTES + q * 1024), 16, off, 0, 0, 0);
+            }
+        }
     };
     // X fragments of sub-step s of a step, token blocks 0..MB-1.
     auto issue_x = [&](bf16x8 (&xs)[MB], int64_t step, int s, int rem) {
@@ -175,11 +224,11 @@ __global__ __launch_bounds__(THREADS) void stream_kernel(DenseProblem p, int64_t
         }
     };
 
-    f32x4 acc[MB][4];
+    f32x4 acc[MB][RB];
 #pragma unroll
     for (int i = 0; i < MB; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+        for (int j = 0; j < RB; ++j) acc[i][j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 
     // B fragment of row block j at k step s: row 16j + l % 16, chunk
     // 4s + l / 16.
@@ -195,14 +244,19 @@ __global__ __launch_bounds__(THREADS) void stream_kernel(DenseProblem p, int64_t
     // loads in issue order, so every W issue is fenced with scheduling
     // barriers: no X load may be moved ahead of the W loads it is counted
     // after.
+    // With X through LDS (RB < 4) the stage loads are the wave's only
+    // loads in the loop: after step t's come exactly those of steps
+    // t+1 .. t+PF, in the prologue as in the steady state.
     bf16x8 xf[C::KS][MB];
     if (nsteps > 0) {
 #pragma unroll
         for (int u = 0; u < C::PF; ++u) issue_w(u, step0 + u, rem_of(step0 + u, u < nsteps));
         __builtin_amdgcn_sched_barrier(0);
-        const int rem0 = rem_of(step0, true);
+        if constexpr (!C::XL) {
+            const int rem0 = rem_of(step0, true);
 #pragma unroll
-        for (int s = 0; s < C::KS; ++s) issue_x(xf[s], step0, s, rem0);
+            for (int s = 0; s < C::KS; ++s) issue_x(xf[s], step0, s, rem0);
+        }
     }
     int buf = 0;
     for (int t = 0; t < nsteps; ++t) {
@@ -212,52 +266,63 @@ __global__ __launch_bounds__(THREADS) void stream_kernel(DenseProblem p, int64_t
         issue_w(pbuf, step + C::PF, rem_of(step + C::PF, t + C::PF < nsteps));
         __builtin_amdgcn_sched_barrier(0);
         const int rem1 = rem_of(step + 1, t + 1 < nsteps);
-        // Step t's W has landed once only what was issued after it may be
-        // outstanding: the W of steps t+1 .. t+PF and the X of steps
-        // t-PF+1 .. t (one X set per iteration, after that iteration's W).
+        // Step t's loads have landed once only what was issued after them
+        // may be outstanding: the stages of steps t+1 .. t+PF (X through
+        // LDS), or the W of step t+1 and the X of step t (register X path,
+        // PF = 1: one X set per iteration, after that iteration's W).
         __builtin_amdgcn_s_waitcnt(waitcnt_vm(C::PF * (C::W_LOADS + C::X_LOADS)));
         __builtin_amdgcn_sched_barrier(0);
         const char *base = ring + buf * C::STAGE_BYTES + frag_row * C::ROW_BYTES;
 #pragma unroll
         for (int s = 0; s < C::KS; ++s) {
-            bf16x8 wf[4];
+            bf16x8 wf[RB];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
+            for (int j = 0; j < RB; ++j) {
                 const int slot = (4 * s + frag_hi) ^ swz<C::CHUNKS>(16 * j + frag_row);
                 wf[j] = *reinterpret_cast<const bf16x8 *>(base + 16 * j * C::ROW_BYTES + slot * 16);
+            }
+            if constexpr (C::XL) {
+#pragma unroll
+                for (int i = 0; i < MB; ++i) {
+                    const int slot = (4 * s + frag_hi) ^ swz<C::CHUNKS>(16 * i + frag_row);
+                    xf[s][i] = *reinterpret_cast<const bf16x8 *>(base + C::W_BYTES + 16 * i * C::ROW_BYTES +
+                                                                 slot * 16);
+                }
             }
 #pragma unroll
             for (int i = 0; i < MB; ++i)
 #pragma unroll
-                for (int j = 0; j < 4; ++j)
+                for (int j = 0; j < RB; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xf[s][i], wf[j], acc[i][j], 0, 0, 0);
-            issue_x(xf[s], step + 1, s, rem1);
+            if constexpr (!C::XL) issue_x(xf[s], step + 1, s, rem1);
         }
         buf = buf + 1 == C::STAGES ? 0 : buf + 1;
     }
 
-    // Add the four wave partials in LDS (wave order).  Wave w then owns row
-    // block j = w of every token block.
+    // Add the four wave partials in LDS (wave order).  Wave w then holds
+    // row block j_own of every token block.
     __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
     __syncthreads();
     f32x4 *red = reinterpret_cast<f32x4 *>(lds);
 #pragma unroll
     for (int i = 0; i < MB; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) red[((wave * MB + i) * 4 + j) * 64 + lane] = acc[i][j];
+        for (int j = 0; j < RB; ++j) red[((wave * MB + i) * RB + j) * 64 + lane] = acc[i][j];
     __syncthreads();
     f32x4 sum[MB];
 #pragma unroll
     for (int i = 0; i < MB; ++i) {
-        sum[i] = red[((0 * MB + i) * 4 + wave) * 64 + lane];
+        sum[i] = red[((0 * MB + i) * RB + j_own) * 64 + lane];
 #pragma unroll
-        for (int w = 1; w < WAVES; ++w) sum[i] += red[((w * MB + i) * 4 + wave) * 64 + lane];
+        for (int w = 1; w < WAVES; ++w) sum[i] += red[((w * MB + i) * RB + j_own) * 64 + lane];
     }
 
     if (sk.split > 1) {
         // Publish this slice with device-scope stores; once every wave's
         // stores have completed the arrival is counted, and the last slice
         // to arrive adds all slices (device-scope loads) in slice order.
+        // (With RB < 4 several waves hold the same row block; each stores
+        // and later reads its own copy.)
         constexpr int BLOCK_FLOATS = WAVES * MB * 64 * 4;
         const float *first = sk.partials + nb * sk.split * BLOCK_FLOATS;
         const __amdgpu_buffer_rsrc_t rp = make_rsrc(first, static_cast<uint32_t>(sk.split) * BLOCK_FLOATS * 4u);
@@ -303,20 +368,21 @@ __global__ __launch_bounds__(THREADS) void stream_kernel(DenseProblem p, int64_t
             __hip_atomic_store(sk.counters + nb, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
 
-    // Epilogue: sum[i][e] is Y[16i + 4*(l/16) + e][n0 + 16*wave + l%16].
+    // Epilogue: sum[i][e] is Y[16i + 4*(l/16) + e][n0 + 16*j_own + l%16].
 #pragma unroll
     for (int i = 0; i < MB; ++i)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
+            if (RB < WAVES && (e < e0 || e >= e0 + C::EPW)) continue;   // another wave's value
             float y = sum[i][e];
             if (p.R) y += bf16_to_f32(rres[i][e]);
             __builtin_amdgcn_raw_buffer_store_b16(f32_to_bf16_rne(y), ry, y_off(i, e), 0, 0);
         }
 }
 
-template <int MB, int BK, int STAGES>
+template <int MB, int BK, int STAGES, int RB>
 hipError_t launch_mb(const Problem &p, int split, const Workspace *ws, hipStream_t s) {
-    const int64_t nblocks = (p.N + ROWS - 1) / ROWS;
+    const int64_t nblocks = (p.N + 16 * RB - 1) / (16 * RB);
     StreamSplit sk{1, ((p.K + BK - 1) / BK) * BK, nullptr, nullptr};
     if (split > 1) {
         sk.split = split;
@@ -324,29 +390,29 @@ hipError_t launch_mb(const Problem &p, int split, const Workspace *ws, hipStream
         sk.partials = ws->partials;
         sk.counters = ws->counters;
     }
-    hipLaunchKernelGGL((stream_kernel<MB, BK, STAGES>), dim3(static_cast<unsigned>(nblocks * sk.split)),
+    hipLaunchKernelGGL((stream_kernel<MB, BK, STAGES, RB>), dim3(static_cast<unsigned>(nblocks * sk.split)),
                        dim3(THREADS), 0, s, dense_of(p), nblocks, sk);
     return hipGetLastError();
 }
 
-template <int BK, int STAGES>
+template <int BK, int STAGES, int RB>
 hipError_t launch_bk(const Problem &p, int split, const Workspace *ws, hipStream_t s) {
     switch ((p.M + 15) / 16) {
-        case 1: return launch_mb<1, BK, STAGES>(p, split, ws, s);
-        case 2: return launch_mb<2, BK, STAGES>(p, split, ws, s);
-        case 3: return launch_mb<3, BK, STAGES>(p, split, ws, s);
-        case 4: return launch_mb<4, BK, STAGES>(p, split, ws, s);
+        case 1: return launch_mb<1, BK, STAGES, RB>(p, split, ws, s);
+        case 2: return launch_mb<2, BK, STAGES, RB>(p, split, ws, s);
+        case 3: return launch_mb<3, BK, STAGES, RB>(p, split, ws, s);
+        case 4: return launch_mb<4, BK, STAGES, RB>(p, split, ws, s);
         default: return hipErrorInvalidValue;
     }
 }
 
 }  // namespace
 
-// K slices per 64-row block: enough workgroups for one per CU, each wave
-// at least one BK step of its slice.
-int stream_split_for(int64_t M, int64_t N, int64_t K, int bk) {
+// K slices per row block: enough workgroups for one per CU, each wave at
+// least one BK step of its slice.
+int stream_split_for(int64_t M, int64_t N, int64_t K, int bk, int rows) {
     (void)M;
-    const int64_t nblocks = (N + ROWS - 1) / ROWS;
+    const int64_t nblocks = (N + rows - 1) / rows;
     int64_t split = nblocks > 0 ? 256 / nblocks : 1;
     const int64_t by_depth = K / (WAVES * bk);
     if (split > by_depth) split = by_depth;
@@ -354,17 +420,29 @@ int stream_split_for(int64_t M, int64_t N, int64_t K, int bk) {
     return split < 1 ? 1 : static_cast<int>(split);
 }
 
-int64_t stream_workspace_floats(int64_t M, int64_t N, int split) {
-    const int64_t nblocks = (N + ROWS - 1) / ROWS;
+int64_t stream_workspace_floats(int64_t M, int64_t N, int split, int rows) {
+    const int64_t nblocks = (N + rows - 1) / rows;
     return nblocks * split * WAVES * ((M + 15) / 16) * 64 * 4;
 }
 
-int64_t stream_counter_count(int64_t N) { return (N + ROWS - 1) / ROWS; }
+int64_t stream_counter_count(int64_t N, int rows) { return (N + rows - 1) / rows; }
 
-hipError_t launch_stream(const Problem &p, int bk, int stages, int split, const Workspace *ws, hipStream_t s) {
+bool stream_config_exists(int bk, int stages, int rows) {
+    return (rows == 64 && stages == 2 && (bk == 64 || bk == 128)) ||
+           (rows == 16 && ((bk == 64 && (stages == 4 || stages == 8)) || (bk == 128 && (stages == 2 || stages == 4)))) ||
+           (rows == 32 && bk == 64 && stages == 4);
+}
+
+hipError_t launch_stream(const Problem &p, int bk, int stages, int rows, int split, const Workspace *ws,
+                         hipStream_t s) {
     if (p.M < 1 || p.M > 64) return hipErrorInvalidValue;
-    if (bk == 128 && stages == 2) return launch_bk<128, 2>(p, split, ws, s);
-    if (bk == 64 && stages == 2) return launch_bk<64, 2>(p, split, ws, s);
+    if (rows == 64 && bk == 128 && stages == 2) return launch_bk<128, 2, 4>(p, split, ws, s);
+    if (rows == 64 && bk == 64 && stages == 2) return launch_bk<64, 2, 4>(p, split, ws, s);
+    if (rows == 16 && bk == 64 && stages == 4) return launch_bk<64, 4, 1>(p, split, ws, s);
+    if (rows == 16 && bk == 64 && stages == 8) return launch_bk<64, 8, 1>(p, split, ws, s);
+    if (rows == 16 && bk == 128 && stages == 2) return launch_bk<128, 2, 1>(p, split, ws, s);
+    if (rows == 16 && bk == 128 && stages == 4) return launch_bk<128, 4, 1>(p, split, ws, s);
+    if (rows == 32 && bk == 64 && stages == 4) return launch_bk<64, 4, 2>(p, split, ws, s);
     return hipErrorInvalidValue;
 }
 

@@ -86,6 +86,33 @@ def test_plan_limits(ka):
     assert ka.kernelarc_plan_uses_workspace(stream, 16, 4096, 4096) == 0
 
 
+def test_row_block_stream_plans(ka):
+    """16-row streaming blocks: no K split once the blocks fill the CUs
+    (N = 4096 gives 256 workgroups), the rule's split below that; chosen for
+    few rows up to N = 4096, and for up to 64 rows while N <= 2048 and
+    K <= 4096."""
+    names = ka.plan_names()
+    r16 = names.index("stream_mfma16_r16_k128s2")
+    r32 = names.index("stream_mfma16_r32_k64s4")
+    assert ka.plan_supports(r16, 1, 8, 8) and ka.plan_supports(r16, 64, 4096, 14336)
+    assert not ka.plan_supports(r16, 65, 512, 512)
+    assert not ka.plan_supports(r16, 16, 512, 516)              # K % 8
+    assert ka.kernelarc_plan_uses_workspace(r16, 16, 4096, 4096) == 0
+    assert ka.kernelarc_plan_uses_workspace(r16, 16, 1024, 4096) == 1
+    assert ka.kernelarc_plan_uses_workspace(r32, 16, 4096, 4096) == 1
+    assert ka.kernelarc_plan_uses_workspace(r16, 16, 4096, 256) == 0   # too shallow to split
+    sel = lambda m, n, k: names[ka.select_plan(m, n, k, True)]
+    assert sel(16, 4096, 4096) == "stream_mfma16_r16_k128s2"
+    assert sel(8, 2048, 2048) == "stream_mfma16_r16_k128s2"
+    assert sel(32, 4096, 14336) == "stream_mfma16_r16_k128s2"
+    assert sel(16, 8192, 8192) == "stream_mfma16_k64_splitk"
+    assert sel(64, 2048, 2048) == "stream_mfma16_r16_k128s2"
+    assert sel(48, 1024, 4096) == "stream_mfma16_r16_k128s2"
+    assert sel(64, 2048, 8192).startswith("tile_")
+    assert sel(64, 4096, 4096).startswith("tile_")
+    assert sel(3, 4096, 4096) == "gemv_valu_w4"
+
+
 def test_validation_before_any_device_work(ka):
     f = ka.kernelarc_gemm_bf16_residual
     buf = (ctypes.c_uint16 * 4096)()

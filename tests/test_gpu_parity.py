@@ -70,6 +70,11 @@ PLAN_SHAPES = {
     "stream_mfma16_k128": [(1, 8, 8), (17, 520, 1000), (64, 96, 4104), (33, 100, 264), (49, 130, 136)],
     "stream_mfma16_k128_splitk": [(1, 24, 8), (5, 520, 1000), (64, 96, 4104), (48, 100, 2064), (16, 70, 1032)],
     "stream_mfma16_k64_splitk": [(2, 24, 8), (31, 520, 1000), (64, 96, 4104), (60, 200, 2056)],
+    # 16- and 32-row blocks with X staged through LDS: the rule's split
+    # ranges from none (K too shallow) to 16 slices; ragged M, N and K.
+    **{n: [(1, 8, 8), (16, 520, 1000), (17, 100, 4104), (64, 96, 2056), (33, 130, 136), (5, 24, 264)]
+       for n in ("stream_mfma16_r16_k64s4", "stream_mfma16_r16_k64s8", "stream_mfma16_r16_k128s2",
+                 "stream_mfma16_r16_k128s4", "stream_mfma16_r32_k64s4")},
 }
 PLAN_SHAPES.update({n: TILE_SHAPES for n in _all_plan_names() if n.startswith("tile_")})
 assert set(PLAN_SHAPES) == set(_all_plan_names()), "every plan has test shapes"
