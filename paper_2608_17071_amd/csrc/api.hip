@@ -412,15 +412,20 @@ bool supports_i8(int plan, int64_t M, int64_t N, int64_t K, bool glu, bool f8 = 
     if (plan < 0 || plan >= NUM_PLANS) return false;
     const PlanInfo &pi = PLANS[plan];
     if (pi.kind == KIND_GENERIC) return cdiv(M, 64) * cdiv(N, 64) * 256 <= LIMIT_ITEMS;
+    // INT8 GEMMs also stream through the 16- and 32-row configurations
+    // (the same bytes per stage as bf16 at K/2).
+    if (pi.kind == KIND_STREAM)
+        return !glu && !f8 && pi.rows < 64 && K % 16 == 0 && supports(plan, M, N, K / 2, true, dense_layout(N, K / 2));
     if (pi.kind != KIND_TILE || K % 16 != 0 || (f8 && !tile_f8_ok(pi.tile_cfg))) return false;
     return glu ? supports_glu(plan, M, N, K / 2) : supports(plan, M, N, K / 2, true, dense_layout(N, K / 2));
 }
 
 // INT8 plan rule (measured on MI355X): the bf16 rules at K/2 (the same
-// bytes per stage), with three changes.  Plain GEMMs up to 64 rows take
-// 64x64 tiles, 3 stages of depth 256 with split-K while the tiles fill at
-// most half the CUs, else 4 stages of depth 128 (the bf16 choices there are
-// non-tile kernels).  The 256x256 tile runs without the tail split: an
+// bytes per stage), with these changes.  Plain INT8 GEMMs up to 64 rows
+// stream: 16-row blocks while they fit one round on the CUs (N <= 4096),
+// else 32-row blocks while those do (N <= 8192); past that (and for FP8
+// operands) 64x64 tiles, 3 stages of depth 256 with split-K while the tiles
+// fill at most half the CUs, else 4 stages of depth 128.  The 256x256 tile runs without the tail split: an
 // INT8 tile covers its K range in half the steps, so the split's partial
 // round trip costs more than the idle CUs it saves (6% at M = 2048 SwiGLU).
 int select_i8(int64_t M, int64_t N, int64_t K, bool glu, bool f8 = false) {
@@ -431,6 +436,11 @@ int select_i8(int64_t M, int64_t N, int64_t K, bool glu, bool f8 = false) {
         return (p >= 0 && supports_i8(p, M, N, K, glu, f8)) ? p : -1;
     };
     int plan = -1;
+    if (!glu && !f8 && M >= 1 && M <= 64) {
+        if (cdiv(N, 16) <= CUS) plan = pick("stream_mfma16_r16_k128s2");
+        else if (cdiv(N, 32) <= CUS) plan = pick("stream_mfma16_r32_k64s4");
+        if (plan >= 0) return plan;
+    }
     if (!glu && M <= 64) {
         const int64_t t64 = tile_count(tile_shape(TC_64x64_K64_S4_W4), M, N);
         plan = 2 * t64 <= CUS ? pick("tile_64x64_k128s3_w4_splitk") : pick("tile_64x64_k64s4_w4");
@@ -880,6 +890,17 @@ int run_i8(int plan, bool glu, int64_t M, int64_t N, int64_t K, const void *X, c
                                    stream);
             }
         }
+    } else if (PLANS[plan].kind == KIND_STREAM) {
+        const int split = stream_split_of(plan, M, N, K / 2);
+        Workspace ws{};
+        if (split > 1) {
+            const int wst = workspace(dev, stream, &ws);
+            if (wst != KERNELARC_OK) return wst;
+        }
+        e = launch_stream_i8(I8Problem{M, N, K, x8, w8, static_cast<const uint16_t *>(R), static_cast<uint16_t *>(Y),
+                                       sx, sw},
+                             PLANS[plan].tile_cfg, PLANS[plan].stages, PLANS[plan].rows, split,
+                             split > 1 ? &ws : nullptr, stream);
     } else if (PLANS[plan].kind == KIND_GENERIC) {
         if (glu)
             e = launch_generic_i8_glu(I8GluProblem{M, N, K, x8, w8, static_cast<const int8_t *>(W2),

@@ -237,6 +237,9 @@ hipError_t launch_tile(int cfg, const Problem &p, int split, int64_t full_tiles,
 hipError_t launch_stream(const Problem &p, int bk, int stages, int rows, int split, const Workspace *ws,
                          hipStream_t s);
 bool stream_config_exists(int bk, int stages, int rows);
+// INT8 operands through the 16- and 32-row streaming configurations.
+hipError_t launch_stream_i8(const I8Problem &p, int bk, int stages, int rows, int split, const Workspace *ws,
+                            hipStream_t s);
 // SwiGLU: the generic kernel, and the tile kernels of the configurations
 // that can pair gate and up blocks (tile_glu_ok).
 hipError_t launch_generic_glu(const GluProblem &p, hipStream_t s);

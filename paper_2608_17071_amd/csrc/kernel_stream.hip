@@ -23,6 +23,11 @@
 // blocks: one workgroup per CU at N = 4096 and no cross-workgroup hand-off)
 // at the price of reading X once per 16 rows of W instead of once per 64;
 // X is small and stays in L2.
+// INT8 operands (16- and 32-row blocks only): a stage holds the same bytes,
+// i.e. twice the K elements, v_mfma_i32_16x16x64_i8 takes the same 16 bytes
+// per lane as the bf16 16x16x32 form and accumulates exactly in int32 (the
+// wave and split-K partials are added as integers), and the epilogue
+// multiplies by the row and column scales before adding R.
 // After the loop the four wave partials are added in LDS in wave order; a
 // split of K across workgroups goes through the fp32 workspace, where the
 // last workgroup of a row block adds the slices in slice order.  The
@@ -106,9 +111,16 @@ struct StreamCfg {
     static_assert(STAGES >= 2 && PF * (W_LOADS + X_LOADS) < 64, "vmcnt range");
 };
 
-template <int MB, int BK, int STAGES, int RB>
-__global__ __launch_bounds__(THREADS) void stream_kernel(DenseProblem p, int64_t nblocks, StreamSplit sk) {
+// P = DenseProblem (bf16) or I8Problem (int8 with scales).
+template <int MB, int BK, int STAGES, int RB, class P>
+__global__ __launch_bounds__(THREADS) void stream_kernel(P p, int64_t nblocks, StreamSplit sk) {
     using C = StreamCfg<MB, BK, STAGES, RB>;
+    constexpr bool I8 = std::is_same<P, I8Problem>::value;
+    static_assert(!I8 || C::XL, "INT8 operands take the LDS-staged X path");
+    constexpr int EB = I8 ? 1 : 2;                 // bytes per operand element
+    constexpr int BKE = C::ROW_BYTES / EB;         // K elements per stage
+    constexpr int CKE = 16 / EB;                   // K elements per 16-byte chunk
+    using AccV = typename std::conditional<I8, i32x4, f32x4>::type;
     __shared__ __attribute__((aligned(1024))) char lds[C::LDS_BYTES];
 
     const int lane = threadIdx.x & 63;
@@ -125,8 +137,8 @@ __global__ __launch_bounds__(THREADS) void stream_kernel(DenseProblem p, int64_t
     // K range of the workgroup, then of this wave (a quarter of its steps).
     const int64_t kbeg = slice * sk.kslice;
     const int64_t kend = (kbeg + sk.kslice) < K ? (kbeg + sk.kslice) : K;
-    const int64_t steps = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
-    const int64_t step0 = kbeg / BK + steps * wave / WAVES;
+    const int64_t steps = kend > kbeg ? (kend - kbeg + BKE - 1) / BKE : 0;
+    const int64_t step0 = kbeg / BKE + steps * wave / WAVES;
     const int nsteps = static_cast<int>(steps * (wave + 1) / WAVES - steps * wave / WAVES);
 
     // Residual of the outputs of this lane's row block in the epilogue
@@ -154,10 +166,26 @@ __global__ __launch_bounds__(THREADS) void stream_kernel(DenseProblem p, int64_t
     for (int i = 0; i < MB; ++i)
 #pragma unroll
         for (int e = 0; e < 4; ++e) rres[i][e] = __builtin_amdgcn_raw_buffer_load_b16(rr, y_off(i, e), 0, 0);
+    // INT8: the column scale of the lane's output column and the row
+    // scales of its rows, requested with R.
+    [[maybe_unused]] float scw = 0.0f, scx[MB][4];
+    if constexpr (I8) {
+        const __amdgpu_buffer_rsrc_t rsw = make_rsrc(p.sw, static_cast<uint32_t>(N * 4));
+        const __amdgpu_buffer_rsrc_t rsx = make_rsrc(p.sx, static_cast<uint32_t>(p.M * 4));
+        scw = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                            rsw, col_ok ? static_cast<uint32_t>(n_out * 4) : OOB_OFFSET, 0, 0));
+#pragma unroll
+        for (int i = 0; i < MB; ++i)
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                scx[i][e] = __builtin_bit_cast(
+                    float, __builtin_amdgcn_raw_buffer_load_b32(
+                               rsx, static_cast<uint32_t>((16 * i + 4 * (lane >> 4) + e) * 4), 0, 0));
+    }
 
     const int64_t rows_w = (p.N - n0) < C::ROWS ? (p.N - n0) : C::ROWS;
-    const __amdgpu_buffer_rsrc_t rw = make_rsrc(p.W + n0 * K, static_cast<uint32_t>(rows_w * K * 2));
-    const __amdgpu_buffer_rsrc_t rx = make_rsrc(p.X, static_cast<uint32_t>(p.M * K * 2));
+    const __amdgpu_buffer_rsrc_t rw = make_rsrc(p.W + n0 * K, static_cast<uint32_t>(rows_w * K * EB));
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc(p.X, static_cast<uint32_t>(p.M * K * EB));
 
     // W staging map: lane l of load q fills slot l % CHUNKS of row
     // RPI*q + l / CHUNKS with global chunk slot ^ swz(row).
@@ -167,8 +195,8 @@ __global__ __launch_bounds__(THREADS) void stream_kernel(DenseProblem p, int64_t
     for (int q = 0; q < C::W_LOADS; ++q) {
         const int r = q * C::RPI + lane / C::CHUNKS;
         const int c = (lane % C::CHUNKS) ^ swz<C::CHUNKS>(r);
-        w_off[q] = static_cast<uint32_t>(r * K * 2 + c * 16);
-        w_k[q] = c * 8;
+        w_off[q] = static_cast<uint32_t>(r * K * EB + c * 16);
+        w_k[q] = c * CKE;
     }
     // X staging map (RB < 4), the same map over the 16*MB rows of X (rows
     // past M fall outside the resource and read zero).
@@ -179,8 +207,8 @@ __global__ __launch_bounds__(THREADS) void stream_kernel(DenseProblem p, int64_t
         for (int q = 0; q < C::X_LOADS; ++q) {
             const int r = q * C::RPI + lane / C::CHUNKS;
             const int c = (lane % C::CHUNKS) ^ swz<C::CHUNKS>(r);
-            x_off[q] = static_cast<uint32_t>(r * K * 2 + c * 16);
-            x_kc[q] = c * 8;
+            x_off[q] = static_cast<uint32_t>(r * K * EB + c * 16);
+            x_kc[q] = c * CKE;
         }
     }
     // A fragment of token block i at k step s (register path): token
@@ -193,11 +221,11 @@ __global__ __launch_bounds__(THREADS) void stream_kernel(DenseProblem p, int64_t
     // (rem = k values left in the step, 0 for a step past the range) are
     // pointed out of range; they move no data and only complete in order.
     auto rem_of = [&](int64_t step, bool valid) {
-        const int64_t left = kend - step * BK;
-        return valid ? static_cast<int>(left < BK ? left : BK) : 0;
+        const int64_t left = kend - step * BKE;
+        return valid ? static_cast<int>(left < BKE ? left : BKE) : 0;
     };
     auto issue_w = [&](int buf, int64_t step, int rem) {
-        const uint32_t kb2 = static_cast<uint32_t>(step * BK * 2);
+        const uint32_t kb2 = static_cast<uint32_t>(step * C::ROW_BYTES);
 #pragma unroll
         for (int q = 0; q < C::W_LOADS; ++q) {
             const uint32_t off = w_k[q] < rem ? w_off[q] + kb2 : OOB_OFFSET;
@@ -224,11 +252,11 @@ __global__ __launch_bounds__(THREADS) void stream_kernel(DenseProblem p, int64_t
         }
     };
 
-    f32x4 acc[MB][RB];
+    AccV acc[MB][RB];
 #pragma unroll
     for (int i = 0; i < MB; ++i)
 #pragma unroll
-        for (int j = 0; j < RB; ++j) acc[i][j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+        for (int j = 0; j < RB; ++j) acc[i][j] = AccV{0, 0, 0, 0};
 
     // B fragment of row block j at k step s: row 16j + l % 16, chunk
     // 4s + l / 16.
@@ -292,8 +320,14 @@ __global__ __launch_bounds__(THREADS) void stream_kernel(DenseProblem p, int64_t
 #pragma unroll
             for (int i = 0; i < MB; ++i)
 #pragma unroll
-                for (int j = 0; j < RB; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xf[s][i], wf[j], acc[i][j], 0, 0, 0);
+                for (int j = 0; j < RB; ++j) {
+                    if constexpr (I8)
+                        acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4, xf[s][i]),
+                                                                          __builtin_bit_cast(i32x4, wf[j]),
+                                                                          acc[i][j], 0, 0, 0);
+                    else
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xf[s][i], wf[j], acc[i][j], 0, 0, 0);
+                }
             if constexpr (!C::XL) issue_x(xf[s], step + 1, s, rem1);
         }
         buf = buf + 1 == C::STAGES ? 0 : buf + 1;
@@ -303,13 +337,13 @@ __global__ __launch_bounds__(THREADS) void stream_kernel(DenseProblem p, int64_t
     // row block j_own of every token block.
     __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
     __syncthreads();
-    f32x4 *red = reinterpret_cast<f32x4 *>(lds);
+    AccV *red = reinterpret_cast<AccV *>(lds);
 #pragma unroll
     for (int i = 0; i < MB; ++i)
 #pragma unroll
         for (int j = 0; j < RB; ++j) red[((wave * MB + i) * RB + j) * 64 + lane] = acc[i][j];
     __syncthreads();
-    f32x4 sum[MB];
+    AccV sum[MB];
 #pragma unroll
     for (int i = 0; i < MB; ++i) {
         sum[i] = red[((0 * MB + i) * RB + j_own) * 64 + lane];
@@ -343,18 +377,18 @@ __global__ __launch_bounds__(THREADS) void stream_kernel(DenseProblem p, int64_t
         const bool last = *flag != 0;
         if (!last) return;
 #pragma unroll
-        for (int i = 0; i < MB; ++i) sum[i] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+        for (int i = 0; i < MB; ++i) sum[i] = AccV{0, 0, 0, 0};
         // Eight slices per round trip; a slice past the last reads out of
         // range and is not added, so the sum runs over the slices in order.
         constexpr int D = 8;
         for (int t0 = 0; t0 < sk.split; t0 += D) {
-            f32x4 v[D][MB];
+            AccV v[D][MB];
 #pragma unroll
             for (int d = 0; d < D; ++d)
 #pragma unroll
                 for (int i = 0; i < MB; ++i)
                     v[d][i] = __builtin_bit_cast(
-                        f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                        AccV, __builtin_amdgcn_raw_buffer_load_b128(
                                    rp, static_cast<uint32_t>(t0 + d) * BLOCK_FLOATS * 4u + ((wave * MB + i) * 64 + lane) * 16,
                                    0, AUX_SC1));
 #pragma unroll
@@ -374,29 +408,34 @@ __global__ __launch_bounds__(THREADS) void stream_kernel(DenseProblem p, int64_t
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             if (RB < WAVES && (e < e0 || e >= e0 + C::EPW)) continue;   // another wave's value
-            float y = sum[i][e];
+            float y;
+            if constexpr (I8) y = static_cast<float>(sum[i][e]) * (scx[i][e] * scw);
+            else y = sum[i][e];
             if (p.R) y += bf16_to_f32(rres[i][e]);
             __builtin_amdgcn_raw_buffer_store_b16(f32_to_bf16_rne(y), ry, y_off(i, e), 0, 0);
         }
 }
 
-template <int MB, int BK, int STAGES, int RB>
-hipError_t launch_mb(const Problem &p, int split, const Workspace *ws, hipStream_t s) {
+// P: DenseProblem or I8Problem; a K slice is a whole number of stages
+// (BK bf16 or 2*BK int8 elements).
+template <int MB, int BK, int STAGES, int RB, class P>
+hipError_t launch_mb(const P &p, int split, const Workspace *ws, hipStream_t s) {
+    constexpr int BKE = std::is_same<P, I8Problem>::value ? 2 * BK : BK;
     const int64_t nblocks = (p.N + 16 * RB - 1) / (16 * RB);
-    StreamSplit sk{1, ((p.K + BK - 1) / BK) * BK, nullptr, nullptr};
+    StreamSplit sk{1, ((p.K + BKE - 1) / BKE) * BKE, nullptr, nullptr};
     if (split > 1) {
         sk.split = split;
-        sk.kslice = (((p.K + split - 1) / split + BK - 1) / BK) * BK;
+        sk.kslice = (((p.K + split - 1) / split + BKE - 1) / BKE) * BKE;
         sk.partials = ws->partials;
         sk.counters = ws->counters;
     }
-    hipLaunchKernelGGL((stream_kernel<MB, BK, STAGES, RB>), dim3(static_cast<unsigned>(nblocks * sk.split)),
-                       dim3(THREADS), 0, s, dense_of(p), nblocks, sk);
+    hipLaunchKernelGGL((stream_kernel<MB, BK, STAGES, RB, P>), dim3(static_cast<unsigned>(nblocks * sk.split)),
+                       dim3(THREADS), 0, s, p, nblocks, sk);
     return hipGetLastError();
 }
 
-template <int BK, int STAGES, int RB>
-hipError_t launch_bk(const Problem &p, int split, const Workspace *ws, hipStream_t s) {
+template <int BK, int STAGES, int RB, class P>
+hipError_t launch_bk(const P &p, int split, const Workspace *ws, hipStream_t s) {
     switch ((p.M + 15) / 16) {
         case 1: return launch_mb<1, BK, STAGES, RB>(p, split, ws, s);
         case 2: return launch_mb<2, BK, STAGES, RB>(p, split, ws, s);
@@ -404,6 +443,17 @@ hipError_t launch_bk(const Problem &p, int split, const Workspace *ws, hipStream
         case 4: return launch_mb<4, BK, STAGES, RB>(p, split, ws, s);
         default: return hipErrorInvalidValue;
     }
+}
+
+// The configurations with 16- and 32-row blocks, for either operand type.
+template <class P>
+hipError_t launch_rows(const P &p, int bk, int stages, int rows, int split, const Workspace *ws, hipStream_t s) {
+    if (rows == 16 && bk == 64 && stages == 4) return launch_bk<64, 4, 1>(p, split, ws, s);
+    if (rows == 16 && bk == 64 && stages == 8) return launch_bk<64, 8, 1>(p, split, ws, s);
+    if (rows == 16 && bk == 128 && stages == 2) return launch_bk<128, 2, 1>(p, split, ws, s);
+    if (rows == 16 && bk == 128 && stages == 4) return launch_bk<128, 4, 1>(p, split, ws, s);
+    if (rows == 32 && bk == 64 && stages == 4) return launch_bk<64, 4, 2>(p, split, ws, s);
+    return hipErrorInvalidValue;
 }
 
 }  // namespace
@@ -436,14 +486,16 @@ bool stream_config_exists(int bk, int stages, int rows) {
 hipError_t launch_stream(const Problem &p, int bk, int stages, int rows, int split, const Workspace *ws,
                          hipStream_t s) {
     if (p.M < 1 || p.M > 64) return hipErrorInvalidValue;
-    if (rows == 64 && bk == 128 && stages == 2) return launch_bk<128, 2, 4>(p, split, ws, s);
-    if (rows == 64 && bk == 64 && stages == 2) return launch_bk<64, 2, 4>(p, split, ws, s);
-    if (rows == 16 && bk == 64 && stages == 4) return launch_bk<64, 4, 1>(p, split, ws, s);
-    if (rows == 16 && bk == 64 && stages == 8) return launch_bk<64, 8, 1>(p, split, ws, s);
-    if (rows == 16 && bk == 128 && stages == 2) return launch_bk<128, 2, 1>(p, split, ws, s);
-    if (rows == 16 && bk == 128 && stages == 4) return launch_bk<128, 4, 1>(p, split, ws, s);
-    if (rows == 32 && bk == 64 && stages == 4) return launch_bk<64, 4, 2>(p, split, ws, s);
-    return hipErrorInvalidValue;
+    const DenseProblem d = dense_of(p);
+    if (rows == 64 && bk == 128 && stages == 2) return launch_bk<128, 2, 4>(d, split, ws, s);
+    if (rows == 64 && bk == 64 && stages == 2) return launch_bk<64, 2, 4>(d, split, ws, s);
+    return launch_rows(d, bk, stages, rows, split, ws, s);
+}
+
+hipError_t launch_stream_i8(const I8Problem &p, int bk, int stages, int rows, int split, const Workspace *ws,
+                            hipStream_t s) {
+    if (p.M < 1 || p.M > 64 || rows == 64) return hipErrorInvalidValue;
+    return launch_rows(p, bk, stages, rows, split, ws, s);
 }
 
 }  // namespace kernelarc

@@ -249,13 +249,22 @@ def test_i8_validation_and_plans(ka):
     names = ka.plan_names()
     gen = names.index("generic_64x64_scalar")
     assert ka.select_plan_i8(64, 128, 40) == gen                                        # K % 16
-    for (M, N, K, glu) in [(16, 4096, 4096, 0), (4096, 4096, 4096, 0), (8192, 8192, 8192, 0),
-                           (1024, 13824, 5120, 1), (4096, 14336, 4096, 1), (1, 64, 16, 0), (300, 77, 1024, 1)]:
+    for (M, N, K, glu) in [(4096, 4096, 4096, 0), (8192, 8192, 8192, 0), (1024, 13824, 5120, 1),
+                           (4096, 14336, 4096, 1), (300, 77, 1024, 1), (16, 4096, 4096, 1), (64, 16384, 1024, 0)]:
         p = ka.select_plan_i8(M, N, K, glu)
         assert ka.plan_supports_i8(p, M, N, K, glu), (M, N, K, glu, names[p])
         assert names[p].startswith("tile"), (M, N, K, glu, names[p])
+    # plain INT8 GEMMs up to 64 rows stream: 16-row blocks up to N = 4096,
+    # 32-row blocks up to N = 8192
+    for (M, N, K, plan) in [(16, 4096, 4096, "stream_mfma16_r16_k128s2"), (1, 64, 16, "stream_mfma16_r16_k128s2"),
+                            (64, 2048, 2048, "stream_mfma16_r16_k128s2"), (16, 8192, 8192, "stream_mfma16_r32_k64s4")]:
+        assert names[ka.select_plan_i8(M, N, K, False)] == plan, (M, N, K)
     for n in ("stream_mfma16_k64_splitk", "gemv_valu_w4", "skinny_mfma16_w8"):
         assert not ka.plan_supports_i8(names.index(n), 16, 1024, 1024)
+    r16 = names.index("stream_mfma16_r16_k128s2")
+    assert ka.plan_supports_i8(r16, 16, 1024, 1024) and not ka.plan_supports_i8(r16, 16, 1024, 1024, True)
+    assert not ka.plan_supports_i8(r16, 65, 1024, 1024) and not ka.plan_supports_i8(r16, 16, 1024, 1032)
+    assert not ka.plan_supports_f8(r16, 16, 1024, 1024)
     assert not ka.plan_supports_i8(names.index("tile_64x64_k64_w4"), 64, 1024, 1024, True)
     assert ka.plan_supports_i8(names.index("tile_64x64_k64_w4"), 64, 1024, 1024, False)
     assert not ka.plan_supports_i8(names.index("tile_256x256_k64_w8"), 64, 1024, 1032)  # K % 16

@@ -84,6 +84,22 @@ def test_i8_gemm_every_plan(ka, name):
     _check(ka, M, N, K, 41, False, plan=ka.plan_names().index(name), what="every-plan")
 
 
+def _stream_plans():
+    from paper_2608_17071_amd import kernelarc
+    names = kernelarc.plan_names()
+    return [n for i, n in enumerate(names) if n.startswith("stream") and kernelarc.plan_supports_i8(i, 33, 264, 1040, False)]
+
+
+@pytest.mark.parametrize("name", _stream_plans())
+@pytest.mark.parametrize("M,N,K", [(1, 8, 16), (16, 520, 1040), (17, 100, 4112), (64, 96, 2064), (33, 130, 144),
+                                   (5, 24, 272)])
+def test_i8_stream_plans(ka, name, M, N, K):
+    """The streaming plans (16- and 32-row blocks) on INT8 operands: one to
+    four token blocks, ragged N, K tails inside a stage and K splits from
+    none to four slices."""
+    _check(ka, M, N, K, 43, False, plan=ka.plan_names().index(name), what="stream")
+
+
 @pytest.mark.parametrize("name", _plans(True))
 def test_i8_swiglu_every_plan(ka, name):
     M, N, K = _shape_for(name)
@@ -105,11 +121,12 @@ def _unit_case(M, N, K, seed, swiglu):
 
 @pytest.mark.parametrize("name", ["tile_256x256_k64_w8", "tile_64x64_k128s3_w4_splitk", "tile_128x128_k64_g2",
                                   "tile_64x64_k64_g4_splitk", "tile_256x128_k64s3_w8_lag_splitk",
-                                  "tile_32x256_k64s4_w4_splitk", "generic_64x64_scalar"])
+                                  "tile_32x256_k64s4_w4_splitk", "generic_64x64_scalar",
+                                  "stream_mfma16_r16_k128s2", "stream_mfma16_r32_k64s4"])
 def test_i8_integer_sums_bit_exact(ka, name):
     """Unit scales and |A| <= 256: the outputs are the exact integer sums."""
     plan = ka.plan_names().index(name)
-    M, N, K = 150, 200, 256
+    M, N, K = (64 if name.startswith("stream") else 150), 200, 256
     t = _unit_case(M, N, K, 7, False)
     gu.note(f"i8 exact integer sums plan={name}")
     got = _run(ka, t, False, plan)
