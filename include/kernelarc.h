@@ -143,9 +143,7 @@ int kernelarc_gemm_bf16_with_plan(int plan, int64_t M, int64_t N, int64_t K,
  * bias is rejected with KERNELARC_ERR_INVALID_ARG.  Pointers 16-byte aligned
  * with K, ldx and ldw multiples of 8 take the MFMA and GEMV kernels (16-byte
  * R/Y accesses also need ldc and ldy multiples of 8, otherwise 2-byte ones);
- * anything else takes the generic kernel.  The streaming kernels of the
- * dense form (4 < M <= 32, up to 64 rows when N <= 2048) are not used for
- * the general form.
+ * anything else takes the generic kernel.
  */
 int kernelarc_gemm_bf16_ex(int64_t M, int64_t N, int64_t K, float alpha,
                            const void *X, int64_t ldx, const void *W, int64_t ldw,

@@ -184,9 +184,9 @@ int stream_split_of(int plan, int64_t M, int64_t N, int64_t K) {
 }
 
 // Row strides of a call and whether it is the general form (strides other
-// than dense, alpha or beta other than 1, or a bias).  The streaming and
-// skinny kernels compute only the dense plain form; the GEMV, tile and
-// generic kernels compute every form.
+// than dense, alpha or beta other than 1, or a bias).  The skinny kernel
+// computes only the dense plain form; the GEMV, streaming, tile and generic
+// kernels compute every form.
 struct Layout {
     int64_t ldx, ldw, ldr, ldy;
     bool general;
@@ -215,9 +215,11 @@ bool supports(int plan, int64_t M, int64_t N, int64_t K, bool residual, const La
             return gemv_fits(M, N, K, lay.ldw) && cdiv(N, 4) * 256 <= LIMIT_ITEMS &&
                    strided_bytes(M, N, lay.ldy) < PANEL_LIMIT && strided_bytes(M, N, lay.ldr) < PANEL_LIMIT;
         case KIND_STREAM: {
-            if (lay.general || M < 1 || M > 64 || K % 8 != 0) return false;
+            if (M < 1 || M > 64 || K % 8 != 0) return false;
             if (!stream_config_exists(pi.tile_cfg, pi.stages, pi.rows)) return false;
-            if (pi.rows * K * 2 >= PANEL_LIMIT || M * K * 2 >= PANEL_LIMIT || M * N * 2 >= PANEL_LIMIT) return false;
+            if (strided_bytes(pi.rows, K, lay.ldw) >= PANEL_LIMIT || strided_bytes(M, K, lay.ldx) >= PANEL_LIMIT ||
+                strided_bytes(M, N, lay.ldy) >= PANEL_LIMIT || strided_bytes(M, N, lay.ldr) >= PANEL_LIMIT)
+                return false;
             const int split = stream_split_of(plan, M, N, K);
             if (cdiv(N, pi.rows) * split * 256 > LIMIT_ITEMS) return false;
             if (split > 1 && (stream_workspace_floats(M, N, split, pi.rows) > WS_PARTIAL_FLOATS ||
@@ -319,7 +321,7 @@ int select(int64_t M, int64_t N, int64_t K, bool residual, const Layout &lay) {
     if (M >= 1 && M <= 32) {
         plan = pick("stream_mfma16_k64_splitk");
         if (plan < 0) plan = pick("skinny_mfma16_w8");
-        if (plan < 0) plan = pick("tile_64x64_k128s3_w4_splitk");   // general form
+        if (plan < 0) plan = pick("tile_64x64_k128s3_w4_splitk");
     } else if (M <= 1024) {
         const int64_t tiles64 = tile_count(tile_shape(TC_64x64_K64_S4_W4), M, N);
         const int64_t tiles128 = tile_count(tile_shape(TC_128x128_K64_S4_W4_L), M, N);

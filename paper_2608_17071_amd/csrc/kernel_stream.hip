@@ -111,11 +111,14 @@ struct StreamCfg {
     static_assert(STAGES >= 2 && PF * (W_LOADS + X_LOADS) < 64, "vmcnt range");
 };
 
-// P = DenseProblem (bf16) or I8Problem (int8 with scales).
+// P = DenseProblem (bf16, the plain operator), Problem (bf16, the general
+// form: row strides, alpha, beta, bias) or I8Problem (int8 with scales).
 template <int MB, int BK, int STAGES, int RB, class P>
 __global__ __launch_bounds__(THREADS) void stream_kernel(P p, int64_t nblocks, StreamSplit sk) {
     using C = StreamCfg<MB, BK, STAGES, RB>;
     constexpr bool I8 = std::is_same<P, I8Problem>::value;
+    constexpr bool GEN = std::is_same<P, Problem>::value;
+    const int64_t ldx = ldx_of(p), ldw = ldw_of(p), ldr = ldr_of(p), ldy = ldy_of(p);
     static_assert(!I8 || C::XL, "INT8 operands take the LDS-staged X path");
     constexpr int EB = I8 ? 1 : 2;                 // bytes per operand element
     constexpr int BKE = C::ROW_BYTES / EB;         // K elements per stage
@@ -146,26 +149,32 @@ __global__ __launch_bounds__(THREADS) void stream_kernel(P p, int64_t nblocks, S
     // latency hides under the K loop.  Every element is read here before any lane writes
     // Y, so Y may alias R.
     const int64_t N = p.N;
-    const uint32_t ybytes = static_cast<uint32_t>(p.M * N * 2);
-    const __amdgpu_buffer_rsrc_t ry = make_rsrc(p.Y, ybytes);
+    const __amdgpu_buffer_rsrc_t ry = make_rsrc(p.Y, static_cast<uint32_t>(strided_bytes(p.M, N, ldy)));
     // Without a residual the R resource is empty: its loads read zero.
-    const __amdgpu_buffer_rsrc_t rr = make_rsrc(p.R ? p.R : p.Y, p.R ? ybytes : 0u);
+    const __amdgpu_buffer_rsrc_t rr =
+        make_rsrc(p.R ? p.R : p.Y, p.R ? static_cast<uint32_t>(strided_bytes(p.M, N, ldr)) : 0u);
     const int64_t n_out = n0 + 16 * j_own + (lane & 15);
-    // Offset of output (16i + 4*(l/16) + e, n_out): rows past M fall outside
-    // the resource; a column past N is pointed out of range.  Computed
-    // without branches so the loads below issue back to back.
-    const uint32_t y_base = static_cast<uint32_t>((4 * (lane >> 4) * N + n_out) * 2);
-    const uint32_t row_bytes = static_cast<uint32_t>(N * 2);
+    // Offsets of output (16i + 4*(l/16) + e, n_out) in Y and R: rows past M
+    // fall outside the resources; a column past N is pointed out of range.
+    // Computed without branches so the loads below issue back to back.
     const bool col_ok = n_out < N;
-    auto y_off = [&](int i, int e) {
-        const uint32_t off = y_base + static_cast<uint32_t>(16 * i + e) * row_bytes;
+    auto out_off = [&](int64_t ld, int i, int e) {
+        const uint32_t off = static_cast<uint32_t>(((16 * i + 4 * (lane >> 4) + e) * ld + n_out) * 2);
         return col_ok ? off : OOB_OFFSET;
     };
     uint16_t rres[MB][4];
 #pragma unroll
     for (int i = 0; i < MB; ++i)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) rres[i][e] = __builtin_amdgcn_raw_buffer_load_b16(rr, y_off(i, e), 0, 0);
+        for (int e = 0; e < 4; ++e) rres[i][e] = __builtin_amdgcn_raw_buffer_load_b16(rr, out_off(ldr, i, e), 0, 0);
+    // General form: the bias of the lane's output column.
+    [[maybe_unused]] float bias_v = 0.0f;
+    if constexpr (GEN) {
+        if (p.bias)
+            bias_v = bf16_to_f32(__builtin_amdgcn_raw_buffer_load_b16(
+                make_rsrc(p.bias, static_cast<uint32_t>(N * 2)), col_ok ? static_cast<uint32_t>(n_out * 2) : OOB_OFFSET,
+                0, 0));
+    }
     // INT8: the column scale of the lane's output column and the row
     // scales of its rows, requested with R.
     [[maybe_unused]] float scw = 0.0f, scx[MB][4];
@@ -184,8 +193,10 @@ __global__ __launch_bounds__(THREADS) void stream_kernel(P p, int64_t nblocks, S
     }
 
     const int64_t rows_w = (p.N - n0) < C::ROWS ? (p.N - n0) : C::ROWS;
-    const __amdgpu_buffer_rsrc_t rw = make_rsrc(p.W + n0 * K, static_cast<uint32_t>(rows_w * K * EB));
-    const __amdgpu_buffer_rsrc_t rx = make_rsrc(p.X, static_cast<uint32_t>(p.M * K * EB));
+    const __amdgpu_buffer_rsrc_t rw =
+        make_rsrc(p.W + n0 * ldw, static_cast<uint32_t>(GEN ? strided_bytes(rows_w, K, ldw) : rows_w * K * EB));
+    const __amdgpu_buffer_rsrc_t rx =
+        make_rsrc(p.X, static_cast<uint32_t>(GEN ? strided_bytes(p.M, K, ldx) : p.M * K * EB));
 
     // W staging map: lane l of load q fills slot l % CHUNKS of row
     // RPI*q + l / CHUNKS with global chunk slot ^ swz(row).
@@ -195,7 +206,7 @@ __global__ __launch_bounds__(THREADS) void stream_kernel(P p, int64_t nblocks, S
     for (int q = 0; q < C::W_LOADS; ++q) {
         const int r = q * C::RPI + lane / C::CHUNKS;
         const int c = (lane % C::CHUNKS) ^ swz<C::CHUNKS>(r);
-        w_off[q] = static_cast<uint32_t>(r * K * EB + c * 16);
+        w_off[q] = static_cast<uint32_t>(r * ldw * EB + c * 16);
         w_k[q] = c * CKE;
     }
     // X staging map (RB < 4), the same map over the 16*MB rows of X (rows
@@ -207,13 +218,13 @@ __global__ __launch_bounds__(THREADS) void stream_kernel(P p, int64_t nblocks, S
         for (int q = 0; q < C::X_LOADS; ++q) {
             const int r = q * C::RPI + lane / C::CHUNKS;
             const int c = (lane % C::CHUNKS) ^ swz<C::CHUNKS>(r);
-            x_off[q] = static_cast<uint32_t>(r * K * EB + c * 16);
+            x_off[q] = static_cast<uint32_t>(r * ldx * EB + c * 16);
             x_kc[q] = c * CKE;
         }
     }
     // A fragment of token block i at k step s (register path): token
     // 16i + l % 16, k chunk 4s + l / 16 of the stage.
-    const uint32_t x_row = static_cast<uint32_t>((lane & 15) * K * 2);
+    const uint32_t x_row = static_cast<uint32_t>((lane & 15) * ldx * 2);
     const int x_k = 8 * (lane >> 4);
     char *ring = lds + wave * C::WAVE_BYTES;
 
@@ -247,7 +258,7 @@ __global__ __launch_bounds__(THREADS) void stream_kernel(P p, int64_t nblocks, S
         const uint32_t base = x_row + static_cast<uint32_t>((step * BK + kr) * 2);
 #pragma unroll
         for (int i = 0; i < MB; ++i) {
-            const uint32_t off = kr < rem ? base + static_cast<uint32_t>(16 * i * K * 2) : OOB_OFFSET;
+            const uint32_t off = kr < rem ? base + static_cast<uint32_t>(16 * i * ldx * 2) : OOB_OFFSET;
             xs[i] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rx, off, 0, 0));
         }
     };
@@ -411,8 +422,13 @@ __global__ __launch_bounds__(THREADS) void stream_kernel(P p, int64_t nblocks, S
             float y;
             if constexpr (I8) y = static_cast<float>(sum[i][e]) * (scx[i][e] * scw);
             else y = sum[i][e];
-            if (p.R) y += bf16_to_f32(rres[i][e]);
-            __builtin_amdgcn_raw_buffer_store_b16(f32_to_bf16_rne(y), ry, y_off(i, e), 0, 0);
+            if constexpr (GEN) {
+                y = combine(y, bf16_to_f32(rres[i][e]), p.R != nullptr, p.alpha, p.beta);
+                if (p.bias) y += bias_v;
+            } else if (p.R) {
+                y += bf16_to_f32(rres[i][e]);
+            }
+            __builtin_amdgcn_raw_buffer_store_b16(f32_to_bf16_rne(y), ry, out_off(ldy, i, e), 0, 0);
         }
 }
 
@@ -486,6 +502,11 @@ bool stream_config_exists(int bk, int stages, int rows) {
 hipError_t launch_stream(const Problem &p, int bk, int stages, int rows, int split, const Workspace *ws,
                          hipStream_t s) {
     if (p.M < 1 || p.M > 64) return hipErrorInvalidValue;
+    if (is_general(p)) {
+        if (rows == 64 && bk == 128 && stages == 2) return launch_bk<128, 2, 4>(p, split, ws, s);
+        if (rows == 64 && bk == 64 && stages == 2) return launch_bk<64, 2, 4>(p, split, ws, s);
+        return launch_rows(p, bk, stages, rows, split, ws, s);
+    }
     const DenseProblem d = dense_of(p);
     if (rows == 64 && bk == 128 && stages == 2) return launch_bk<128, 2, 4>(d, split, ws, s);
     if (rows == 64 && bk == 64 && stages == 2) return launch_bk<64, 2, 4>(d, split, ws, s);

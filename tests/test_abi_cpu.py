@@ -182,11 +182,14 @@ def test_general_form_validation(ka):
 
 def test_general_form_plan_selection(ka):
     names = ka.plan_names()
-    # the dense form of a decode shape streams; the general form of it cannot
+    # decode shapes stream in both forms, strided ones too
     dense = names[ka.select_plan_ex(16, 4096, 4096, 1, 4096, 4096, 4096, 4096, 1.0, 1.0, 0)]
     general = names[ka.select_plan_ex(16, 4096, 4096, 1, 4096, 4096, 4096, 4096, 2.0, 1.0, 0)]
+    strided = names[ka.select_plan_ex(16, 4096, 4096, 1, 4104, 4112, 4100, 4096, 1.0, 0.5, 1)]
     assert dense == names[ka.select_plan(16, 4096, 4096, True)]
-    assert dense.startswith("stream") and general.startswith("tile")
+    assert dense == general == strided == "stream_mfma16_r16_k128s2"
+    assert names[ka.select_plan_ex(16, 8192, 8192, 1, 8192, 8192, 8192, 8192, 2.0, 1.0, 1)] == \
+        "stream_mfma16_k64_splitk"
     assert names[ka.select_plan_ex(2, 4096, 4096, 1, 4104, 4096, 4096, 4096, 1.0, 1.0, 1)] == "gemv_valu_w4"
     assert names[ka.select_plan_ex(4096, 4096, 14336, 1, 14336, 14336, 4096, 4096, 1.0, 1.0, 1)].startswith("tile")
 

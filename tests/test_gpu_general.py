@@ -77,6 +77,8 @@ def _general_case(ka, M, N, K, seed, alpha, beta, with_c, with_bias, pads=(8, 16
 def _shape_for(name):
     if name == "gemv_valu_w4":
         return (3, 520, 264)
+    if name.startswith("stream"):
+        return (33, 264, 1032)
     if name.endswith("splitk") or name.endswith("tailsplit"):
         return (200, 264, 1032)
     return (77, 136, 520)
@@ -84,7 +86,8 @@ def _shape_for(name):
 
 def _general_plan_names():
     from paper_2608_17071_amd import kernelarc
-    return [n for n in kernelarc.plan_names() if n.startswith("tile_") or n in ("gemv_valu_w4", "generic_64x64_scalar")]
+    return [n for n in kernelarc.plan_names()
+            if n.startswith(("tile_", "stream_")) or n in ("gemv_valu_w4", "generic_64x64_scalar")]
 
 
 @pytest.mark.parametrize("name", _general_plan_names())
@@ -108,6 +111,8 @@ def test_general_strides(ka, pads):
     # odd X/W strides cannot take the 16-byte loads (generic kernel); odd
     # C/Y strides take the 2-byte epilogue of the MFMA kernels
     _general_case(ka, 96, 200, 136, 5, 1.5, 0.5, True, True, pads=pads)
+    # the same strides on a streaming shape (16-row blocks, 16-bit R and Y)
+    _general_case(ka, 24, 200, 1032, 6, 1.5, 0.5, True, True, pads=pads)
 
 
 def test_general_large_k_ne_n(ka):
@@ -151,8 +156,9 @@ def test_general_beta_zero_does_not_read_c(ka):
     assert torch.equal(y.view(torch.int16), y0.view(torch.int16))
 
 
-def test_general_in_place(ka):
-    M, N, K = 200, 264, 520
+@pytest.mark.parametrize("M", [200, 16])
+def test_general_in_place(ka, M):
+    N, K = 264, 520
     g = torch.Generator().manual_seed(6)
     X = _bf16(g, (M, K), K ** -0.5)
     W = _bf16(g, (N, K), K ** -0.5)
@@ -171,10 +177,10 @@ def test_general_rejects(ka):
     x = _bf16(g, (64, 128), 1.0).cuda()
     w = _bf16(g, (96, 128), 1.0).cuda()
     c = _bf16(g, (64, 96), 1.0).cuda()
-    stream = ka.plan_names().index("stream_mfma16_k64_splitk")
+    skinny = ka.plan_names().index("skinny_mfma16_w8")
     gu.note("general rejects")
     with pytest.raises(ka.KernelArcError) as e:
-        ka.gemm_bf16_ex(x[:16], w, c[:16], None, 2.0, 1.0, plan=stream)   # the streaming kernel is dense-only
+        ka.gemm_bf16_ex(x[:16], w, c[:16], None, 2.0, 1.0, plan=skinny)   # the skinny kernel is dense-only
     assert e.value.status == ka.ERR_UNSUPPORTED
     big = torch.zeros(64, 200, dtype=torch.bfloat16, device="cuda")
     with pytest.raises(ka.KernelArcError) as e:                            # Y partially overlaps C
