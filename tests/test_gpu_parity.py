@@ -221,7 +221,7 @@ def test_edge_sizes(ka):
     gu.note("N=0")
     assert ka.gemm_bf16(torch.zeros(5, 64, dtype=torch.bfloat16, device="cuda"),
                         torch.zeros(0, 64, dtype=torch.bfloat16, device="cuda")).shape == (5, 0)
-    for M in (3, 100):
+    for M in (3, 16, 48, 100):      # GEMV, 16-row streaming (twice), tiles
         r = torch.randn(M, 40, device="cuda").to(torch.bfloat16)
         xe = torch.zeros(M, 0, dtype=torch.bfloat16, device="cuda")
         we = torch.zeros(40, 0, dtype=torch.bfloat16, device="cuda")
@@ -290,3 +290,16 @@ def test_graph_replay_matches_eager(ka):
             ka.gemm_bf16_with_plan(p, x, w, r, out=y2)   # eager work between replays
             torch.cuda.synchronize()
             np.testing.assert_array_equal(gu.to_bits(y2), eager)
+
+
+@pytest.mark.parametrize("plan", ["stream_mfma16_r16_k128s2", "stream_mfma16_r32_k64s4"])
+def test_stream_many_row_blocks(ka, plan):
+    """A wide, shallow decode-like shape forced onto the 16- and 32-row
+    streaming plans: thousands of row blocks (several rounds of workgroups,
+    no K split), the last block ragged; whole output against the oracle."""
+    M, N, K = 16, 65544, 64
+    p = plan_id(ka, plan)
+    t = wl.make_inputs(wl.custom(M, N, K, seed=14))
+    gu.note(f"{plan} many row blocks M={M} N={N} K={K}")
+    y = gu.run_library(t["X"], t["W"], t["R"], plan=p)
+    gu.check_tolerance(y, gu.oracle_reference(t["X"], t["W"], t["R"]), plan)
