@@ -81,10 +81,13 @@ def source_digest(paths):
 
 
 # Kernel symbol fragment of each tile plan (rocprofv3 reports symbols).
-# Cfg<BM, BN, BK, WAVES_M, WAVES_N, STAGES, WAVES_PER_EU, KGROUPS, PD, LAG>.
+# Cfg<BM, BN, BK, WAVES_M, WAVES_N, STAGES, WAVES_PER_EU, KGROUPS, PD, LAG, M16>.
 PLAN_SYMBOL = {
-    "tile_256x256_k64_w8": "Cfg<256, 256, 64, 2, 4, 2, 2, 1, 1, false>",
+    "tile_256x256_k64_w8": "Cfg<256, 256, 64, 2, 4, 2, 2, 1, 1, false, false>",
+    "tile_256x256_k64_w8_m16": "Cfg<256, 256, 64, 2, 4, 2, 2, 1, 1, false, true>",
 }
+# The plan whose HBM traffic the counter runs summarise (the big sweep shapes' plan).
+TRAFFIC_PLAN = "tile_256x256_k64_w8_m16"
 KERNEL_SOURCES = ["paper_2608_17071_amd/csrc/kernel_tile.hip", "paper_2608_17071_amd/csrc/internal.h"]
 
 
@@ -182,6 +185,23 @@ class Case:
     def free(self):
         self.sets = []
         self.graph = None
+
+
+class BlasCase(Case):
+    """The same workload through torch's GEMM (hipBLASLt on ROCm), for
+    comparison only: identical inputs, operand copies and timing protocol."""
+
+    def __init__(self, w, ka, torch, rotate=True):
+        super().__init__(w, ka, torch, rotate)
+        self.plan, self.plan_name = -1, "torch(hipBLASLt)"
+        self.torch = torch
+
+    def call(self, ka, i):
+        x, W, r, y = self.sets[i]
+        if r is not None:
+            self.torch.addmm(r, x, W.t(), out=y)
+        else:
+            self.torch.mm(x, W.t(), out=y)
 
 
 class GeneralCase(Case):
@@ -557,6 +577,8 @@ def main():
     ap.add_argument("--only", default="",
                     help="comma-separated workload names (sweep, gate, general-form or SwiGLU): "
                          "time just these (for profiling one kernel)")
+    ap.add_argument("--blas", action="store_true",
+                    help="with --only: also time torch's GEMM (hipBLASLt) on the plain shapes, same protocol")
     ap.add_argument("--summarize-traffic", nargs=2, metavar=("PMC_DIR", "SHAPES"),
                     help="write profiles/traffic.json for the dominant plan from counter runs")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -569,7 +591,7 @@ def main():
         cmd = ("rocprofv3 --pmc FETCH_SIZE (then WRITE_SIZE) -d <dir>/fetch (write) -o p --output-format csv "
                f"-- python bench.py --only {','.join(shapes)} --steps 2 --warmup 1; the same two counters of "
                "python bench.py --copy-calibration into <dir>/copy_fetch, <dir>/copy_write")
-        summarize_traffic(pmc_dir, "tile_256x256_k64_w8", shapes, cmd)
+        summarize_traffic(pmc_dir, TRAFFIC_PLAN, shapes, cmd)
         return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -609,6 +631,8 @@ def main():
                 return GroupedCase(wl.GROUPED_BY_NAME[n], ka, torch, rotate=not args.hot)
             return Case(wl.BY_NAME[n], ka, torch, rotate=not args.hot)
         cases = [case_of(n) for n in args.only.split(",")]
+        if args.blas:
+            cases += [BlasCase(c.w, ka, torch, rotate=not args.hot) for c in list(cases) if type(c) is Case]
         time_cases(cases, args.steps, args.warmup, ka, torch, use_graph=not args.no_graph)
         print(json.dumps({"only": [shape_row(c) for c in cases]}), flush=True)
         return

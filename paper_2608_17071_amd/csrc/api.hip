@@ -123,6 +123,8 @@ const PlanInfo PLANS[] = {
     {"stream_mfma16_r16_k128s2", KIND_STREAM, 128, -1, 2, 16},
     {"stream_mfma16_r16_k128s4", KIND_STREAM, 128, -1, 4, 16},
     {"stream_mfma16_r32_k64s4", KIND_STREAM, 64, -1, 4, 32},
+    {"tile_256x256_k64_w8_m16", KIND_TILE, TC_256x256_K64_S2_W8_M16, 1},
+    {"tile_256x256_k64_w8_m16_tailsplit", KIND_TILE, TC_256x256_K64_S2_W8_M16, -1},
 };
 constexpr int NUM_PLANS = static_cast<int>(sizeof(PLANS) / sizeof(PLANS[0]));
 
@@ -277,11 +279,11 @@ const TableEntry TABLE[] = {
     {512, 5120, 5120, 1, "tile_256x128_k64s3_w8_splitk"},
     {512, 8192, 8192, 1, "tile_128x128_k64s4_w4_lag"},
     {4096, 2048, 2048, 1, "tile_256x128_k64s3_w8_lag"},
-    {4096, 4096, 4096, 1, "tile_256x256_k64_w8"},
+    {4096, 4096, 4096, 1, "tile_256x256_k64_w8_m16"},
     {4096, 5120, 5120, 1, "tile_256x256_k64_w8_tailsplit"},
-    {4096, 8192, 8192, 1, "tile_256x256_k64_w8"},
+    {4096, 8192, 8192, 1, "tile_256x256_k64_w8_m16"},
     // plain BF16 GEMM
-    {8192, 8192, 8192, 0, "tile_256x256_k64_w8"},
+    {8192, 8192, 8192, 0, "tile_256x256_k64_w8_m16"},
     {-1, 0, 0, 0, ""},   // sentinel
 };
 
@@ -297,8 +299,8 @@ const TableEntry TABLE[] = {
 // 256x128 8-wave tiles (3 stages, lagged refill) with split-K when 128x128
 // tiles would leave some CUs idle, else 128x128 tiles with 4 stages and the
 // lagged refill; above that the 256x256 8-wave tile when it
-// fills the 256 CUs (tail split: the tiles of a partial last round are split
-// in K), the 256x128 8-wave tile (3 stages, lagged refill) when that fills
+// fills the 256 CUs (16x16x32 MFMA; tail split: the tiles of a partial last
+// round are split in K), the 256x128 8-wave tile (3 stages, lagged refill) when that fills
 // them, else the 128x128 tile.
 int select(int64_t M, int64_t N, int64_t K, bool residual, const Layout &lay) {
     if (M < 0 || N < 0 || K < 0) return -1;
@@ -332,7 +334,7 @@ int select(int64_t M, int64_t N, int64_t K, bool residual, const Layout &lay) {
         else plan = pick("tile_128x128_k64s4_w4_lag");
         if (plan < 0) plan = pick("tile_128x128_k64_w4_splitk");
     } else {
-        if (tile_count(tile_shape(TC_256x256_K64_S2_W8), M, N) >= CUS) plan = pick("tile_256x256_k64_w8_tailsplit");
+        if (tile_count(tile_shape(TC_256x256_K64_S2_W8), M, N) >= CUS) plan = pick("tile_256x256_k64_w8_m16_tailsplit");
         else if (tile_count(tile_shape(TC_256x128_K64_S3_W8_L), M, N) >= CUS) plan = pick("tile_256x128_k64s3_w8_lag");
         if (plan < 0) plan = pick("tile_128x128_k64_w4");
     }
@@ -418,7 +420,8 @@ bool supports_i8(int plan, int64_t M, int64_t N, int64_t K, bool glu, bool f8 = 
     // (the same bytes per stage as bf16 at K/2).
     if (pi.kind == KIND_STREAM)
         return !glu && !f8 && pi.rows < 64 && K % 16 == 0 && supports(plan, M, N, K / 2, true, dense_layout(N, K / 2));
-    if (pi.kind != KIND_TILE || K % 16 != 0 || (f8 && !tile_f8_ok(pi.tile_cfg))) return false;
+    if (pi.kind != KIND_TILE || K % 16 != 0 || tile_is_m16(pi.tile_cfg) || (f8 && !tile_f8_ok(pi.tile_cfg)))
+        return false;
     return glu ? supports_glu(plan, M, N, K / 2) : supports(plan, M, N, K / 2, true, dense_layout(N, K / 2));
 }
 
@@ -449,7 +452,10 @@ int select_i8(int64_t M, int64_t N, int64_t K, bool glu, bool f8 = false) {
         if (plan >= 0) return plan;
     }
     plan = glu ? select_glu(M, N, K / 2) : select(M, N, K / 2, true, dense_layout(N, K / 2));
-    if (plan == plan_index("tile_256x256_k64_w8_tailsplit")) plan = plan_index("tile_256x256_k64_w8");
+    // (the 16x16 MFMA form of the 256x256 tile is bf16 only: its 32x32 form)
+    if (plan == plan_index("tile_256x256_k64_w8_tailsplit") || plan == plan_index("tile_256x256_k64_w8_m16") ||
+        plan == plan_index("tile_256x256_k64_w8_m16_tailsplit"))
+        plan = plan_index("tile_256x256_k64_w8");
     if (plan >= 0 && plan != PLAN_GENERIC && supports_i8(plan, M, N, K, glu, f8)) return plan;
     for (const char *name : {"tile_64x64_k128s3_w4_splitk", "tile_64x128_k64s4_w4", "tile_128x128_k64_w4"}) {
         const int p = pick(name);

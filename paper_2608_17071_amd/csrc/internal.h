@@ -50,7 +50,8 @@ enum TileCfg : int {
     TC_256x128_K64_S3_W8_L = 24,   // lagged refill
     TC_128x128_K64_S4_W4_L = 25,
     TC_32x256_K64_S4_W4 = 26,      // one 32-row wave band (skinny M)
-    TC_COUNT = 27,
+    TC_256x256_K64_S2_W8_M16 = 27, // 16x16x32 MFMA (bf16 plain and general forms)
+    TC_COUNT = 28,
 };
 
 struct TileShape {
@@ -261,6 +262,8 @@ __host__ __device__ inline int64_t group_rows(const int32_t *counts, int64_t g, 
 // FP8: tile kernels (configurations of tile_f8_ok; SwiGLU also tile_glu_ok)
 // and generic kernels.
 bool tile_f8_ok(int cfg);
+// 16x16x32 MFMA tile configurations (bf16 plain and general forms only).
+bool tile_is_m16(int cfg);
 hipError_t launch_tile_f8(int cfg, const F8Problem &p, int split, int64_t full_tiles, const Workspace *ws,
                           hipStream_t s);
 hipError_t launch_tile_f8_glu(int cfg, const F8GluProblem &p, int split, int64_t full_tiles, const Workspace *ws,

@@ -73,7 +73,7 @@ __device__ __forceinline__ int swz(int r) {
 }
 
 template <int BM_, int BN_, int BK_, int WAVES_M_, int WAVES_N_, int STAGES_, int WAVES_PER_EU_, int KGROUPS_ = 1,
-          int PD_ = 1, bool LAG_ = false>
+          int PD_ = 1, bool LAG_ = false, bool M16_ = false>
 struct Cfg {
     static constexpr int BM = BM_, BN = BN_, BK = BK_, STAGES = STAGES_;
     static constexpr int WAVES_M = WAVES_M_, WAVES_N = WAVES_N_;
@@ -84,7 +84,13 @@ struct Cfg {
     static constexpr int WAVES = TILE_WAVES * KGROUPS, THREADS = 64 * WAVES;
     static constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;   // per-wave block
     static constexpr int TM = WM / 32, TN = WN / 32;             // 32x32 blocks per wave
-    static constexpr int KSTEPS = BK / 16;                        // MFMA sub-steps per stage
+    // MFMA shape: 32x32x16 (default) or, with M16, 16x16x32 (bf16 plain and
+    // general forms only): each 32x32 accumulator block is then four 16x16
+    // blocks, quad q = 2*(row half) + (column half) in its elements 4q..4q+3.
+    // Same operand bytes and MFMA cycles per K; half the accumulator
+    // register traffic per product.
+    static constexpr bool M16 = M16_;
+    static constexpr int KSTEPS = BK / (M16 ? 32 : 16);           // MFMA sub-steps per stage
     // Fragment prefetch distance: the LDS reads of sub-step s + PD are
     // issued among the MFMAs of sub-step s (PD + 1 register sets).
     static constexpr int PD = PD_;
@@ -123,6 +129,7 @@ struct Cfg {
     static_assert(RED_BYTES <= LDS_BYTES, "K-group reduction fits");
     static_assert(LOADS * (STAGES - 2) < 64, "vmcnt range");
     static_assert(PD >= 1 && PD < KSTEPS && KSTEPS % (PD + 1) == 0, "fragment prefetch distance");
+    static_assert(!M16 || KGROUPS == 1, "16x16 MFMA tiles run one K group");
     static_assert(!LAG || STAGES >= 3, "lagged refill needs three stages");
 };
 
@@ -203,6 +210,21 @@ __device__ __forceinline__ void read_frag(const char *a_base, const char *b_base
         fb[r - 1] = *reinterpret_cast<const bf16x8 *>(b_base + (r - 1) * 32 * C::ROW_BYTES + col);
     else
         fa[r - C::TN] = *reinterpret_cast<const bf16x8 *>(a_base + (r - C::TN) * 32 * C::ROW_BYTES + col);
+}
+
+// Fragment read r of a 16x16x32 sub-step (M16), in the order the MFMAs
+// first use them (a0, b0 .. b[2TN-1], a1 .. a[2TM-1]): lane l reads row
+// l % 16 of a 16-row block at byte column col.
+template <class C, int r>
+__device__ __forceinline__ void read_frag16(const char *a_base, const char *b_base, int col, bf16x8 *fa,
+                                            bf16x8 *fb) {
+    constexpr int FTN = 2 * C::TN;
+    if constexpr (r == 0)
+        fa[0] = *reinterpret_cast<const bf16x8 *>(a_base + col);
+    else if constexpr (r <= FTN)
+        fb[r - 1] = *reinterpret_cast<const bf16x8 *>(b_base + (r - 1) * 16 * C::ROW_BYTES + col);
+    else
+        fa[r - FTN] = *reinterpret_cast<const bf16x8 *>(a_base + (r - FTN) * 16 * C::ROW_BYTES + col);
 }
 
 // FP8 fragment read r (same order as read_frag): 32 bytes per lane, the two
@@ -296,6 +318,7 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
     constexpr bool Q8 = I8 || F8;                  // 1-byte operands with dequantisation scales
     constexpr bool GLU = std::is_same<PB, GluProblem>::value || std::is_same<PB, I8GluProblem>::value ||
                          std::is_same<PB, F8GluProblem>::value;
+    static_assert(!C::M16 || (!Q8 && !GLU), "16x16 MFMA tiles take bf16 plain or general problems");
     constexpr int EB = Q8 ? 1 : 2;                 // bytes per operand element
     constexpr int BKE = C::ROW_BYTES / EB;         // K elements per stage
     constexpr int CKE = 16 / EB;                   // K elements per 16-byte chunk
@@ -410,9 +433,11 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[i][j][e] = 0;
 
-    // Fragment reads: row (lane % 32) of each 32-row block, chunk 2*ks + hi.
-    const int frag_row = lane & 31;
-    const int hi = lane >> 5;
+    // Fragment reads: row (lane % 32) of each 32-row block, chunk 2*ks + hi
+    // (32x32x16); with M16, row (lane % 16) of each 16-row block, chunk
+    // 4*ks + hi (hi = lane / 16).  Rows 16 apart share their swizzle.
+    const int frag_row = C::M16 ? (lane & 15) : (lane & 31);
+    const int hi = C::M16 ? (lane >> 4) : (lane >> 5);
     const int wm0 = (wave / C::WAVES_N) * C::WM;
     const int wn0 = (wave % C::WAVES_N) * C::WN;
     const int a_row_byte = (wm0 + frag_row) * C::ROW_BYTES;
@@ -537,7 +562,11 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
     // 32x32x32) or 64 (FP8 32x32x64).
     constexpr int KS = F8 ? C::KSTEPS / 2 : C::KSTEPS, PD = C::PD, NSETS = PD + 1;
     static_assert(KS > PD && KS % NSETS == 0, "fragment prefetch distance");
-    constexpr int MF = C::TM * C::TN, FR = C::TM + C::TN, POST = PD * MF, SLOTS = KS * MF;
+    // Per sub-step: MF MFMAs and FR fragment reads (A blocks then B blocks
+    // of 32 rows, or of 16 rows with M16: twice as many of each block kind,
+    // four 16x16 products per 32x32 accumulator block).
+    constexpr int FTM = C::M16 ? 2 * C::TM : C::TM, FTN = C::M16 ? 2 * C::TN : C::TN;
+    constexpr int MF = FTM * FTN, FR = FTM + FTN, POST = PD * MF, SLOTS = KS * MF;
     // Loads a wave may leave in flight at a step's barrier (step kt+1 must
     // have landed): the steps requested after it, and with the lagged
     // refill also the loads of this step's refill issued before the barrier.
@@ -550,16 +579,21 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
         if constexpr (F8) {
             colk[ks] = ((4 * ks + 2 * hi) ^ frag_swz) * 16;
             colk2[ks] = ((4 * ks + 2 * hi + 1) ^ frag_swz) * 16;
+        } else if constexpr (C::M16) {
+            colk[ks] = ((4 * ks + hi) ^ frag_swz) * 16;
+            colk2[ks] = 0;
         } else {
             colk[ks] = ((2 * ks + hi) ^ frag_swz) * 16;
             colk2[ks] = 0;
         }
     }
     using Frag = typename std::conditional<F8, i32x8, bf16x8>::type;
-    Frag fa[NSETS][C::TM], fb[NSETS][C::TN];
+    Frag fa[NSETS][FTM], fb[NSETS][FTN];
     auto read_any = [&](auto rc, const char *src, int col, int col2, Frag *ta, Frag *tb) {
         if constexpr (F8)
             read_frag8<C, decltype(rc)::value>(src + a_row_byte, src + C::A_BYTES + b_row_byte, col, col2, ta, tb);
+        else if constexpr (C::M16)
+            read_frag16<C, decltype(rc)::value>(src + a_row_byte, src + C::A_BYTES + b_row_byte, col, ta, tb);
         else
             read_frag<C, decltype(rc)::value>(src + a_row_byte, src + C::A_BYTES + b_row_byte, col, ta, tb);
     };
@@ -608,8 +642,19 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
             const int tcol = colk[tgt % KS], tcol2 = colk2[tgt % KS];
             static_for<0, MF>([&](auto tc) {
                 constexpr int t = decltype(tc)::value;
-                constexpr int i = t / C::TN, j = t % C::TN;
-                if constexpr (I8)
+                constexpr int i = t / FTN, j = t % FTN;
+                if constexpr (C::M16) {
+                    // 16x16 block (i, j) lives in quad 2*(i%2) + j%2 of
+                    // 32x32 accumulator block (i/2, j/2).
+                    constexpr int q = 2 * (i % 2) + (j % 2);
+                    f32x16 &a = acc[i / 2][j / 2];
+                    f32x4 c = {a[4 * q], a[4 * q + 1], a[4 * q + 2], a[4 * q + 3]};
+                    c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[set][i], fb[set][j], c, 0, 0, 0);
+                    a[4 * q] = c[0];
+                    a[4 * q + 1] = c[1];
+                    a[4 * q + 2] = c[2];
+                    a[4 * q + 3] = c[3];
+                } else if constexpr (I8)
                     acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(__builtin_bit_cast(i32x4, fa[set][i]),
                                                                       __builtin_bit_cast(i32x4, fb[set][j]),
                                                                       acc[i][j], 0, 0, 0);
@@ -819,9 +864,14 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
 #pragma unroll
                 for (int j = 0; j < C::TN; ++j)
 #pragma unroll
-                    for (int e = 0; e < 16; ++e)
-                        ep[(8 * (e >> 2) + 4 * hi + (e & 3)) * EPS + j * 32 + frag_row] =
-                            static_cast<float>(acc[i][j][e]);
+                    for (int e = 0; e < 16; ++e) {
+                        if constexpr (C::M16)   // quad q = e/4: rows 16*(q/2) + 4*hi + e%4, columns 16*(q%2) + lane%16
+                            ep[(16 * (e >> 3) + 4 * hi + (e & 3)) * EPS + j * 32 + 16 * ((e >> 2) & 1) + frag_row] =
+                                static_cast<float>(acc[i][j][e]);
+                        else
+                            ep[(8 * (e >> 2) + 4 * hi + (e & 3)) * EPS + j * 32 + frag_row] =
+                                static_cast<float>(acc[i][j][e]);
+                    }
             }
         }
         __syncthreads();
@@ -921,21 +971,26 @@ hipError_t launch_cfg(const Problem &p, int group_m, int split, int64_t full_til
 template <class C>
 hipError_t launch_cfg_i8(const I8Problem &p, int group_m, int split, int64_t full_tiles, const Workspace *ws,
                          hipStream_t s) {
-    const int64_t tiles_m = (p.M + C::BM - 1) / C::BM;
-    const int64_t tiles_n = (p.N + C::BN - 1) / C::BN;
-    const int64_t tiles = tiles_m * tiles_n;
-    SplitK sk;
-    if (!split_args<C, 2 * C::BK>(p.K, tiles, split, full_tiles, ws, sk)) return hipErrorInvalidValue;
-    const int64_t wgs = sk.full_tiles + (tiles - sk.full_tiles) * sk.split;
-    hipLaunchKernelGGL((tile_kernel<C, I8Problem>), dim3(static_cast<unsigned>(wgs)), dim3(C::THREADS), 0, s, p,
-                       tiles_m, tiles_n, group_m, sk);
-    return hipGetLastError();
+    if constexpr (C::M16) {
+        return hipErrorInvalidValue;   // 16x16 MFMA tiles are bf16 only
+    } else {
+        const int64_t tiles_m = (p.M + C::BM - 1) / C::BM;
+        const int64_t tiles_n = (p.N + C::BN - 1) / C::BN;
+        const int64_t tiles = tiles_m * tiles_n;
+        SplitK sk;
+        if (!split_args<C, 2 * C::BK>(p.K, tiles, split, full_tiles, ws, sk)) return hipErrorInvalidValue;
+        const int64_t wgs = sk.full_tiles + (tiles - sk.full_tiles) * sk.split;
+        hipLaunchKernelGGL((tile_kernel<C, I8Problem>), dim3(static_cast<unsigned>(wgs)), dim3(C::THREADS), 0, s, p,
+                           tiles_m, tiles_n, group_m, sk);
+        return hipGetLastError();
+    }
 }
 
 // SwiGLU needs an even number of 32-column blocks per wave (gate/up pairs)
-// and an even number of B loads per wave (half gate, half up).
+// and an even number of B loads per wave (half gate, half up), and the
+// 32x32 MFMA layout its register pairing assumes.
 template <class C>
-constexpr bool glu_ok() { return C::TN % 2 == 0 && C::B_LOADS % 2 == 0 && 32 % C::RPI == 0; }
+constexpr bool glu_ok() { return !C::M16 && C::TN % 2 == 0 && C::B_LOADS % 2 == 0 && 32 % C::RPI == 0; }
 
 template <class C>
 hipError_t launch_cfg_glu(const GluProblem &p, int group_m, int split, int64_t full_tiles, const Workspace *ws,
@@ -1004,6 +1059,8 @@ using C64x64k64g4 = Cfg<64, 64, 64, 2, 2, 2, 4, 4>;
 using C256x128s3w8L = Cfg<256, 128, 64, 4, 2, 3, 2, 1, 1, true>;
 using C128x128s4L = Cfg<128, 128, 64, 2, 2, 4, 1, 1, 1, true>;
 using C32x256k64s4 = Cfg<32, 256, 64, 1, 4, 4, 1>;
+// 16x16x32 MFMA form of the 256x256 8-wave tile (bf16 plain and general only).
+using C256x256w8m16 = Cfg<256, 256, 64, 2, 4, 2, 2, 1, 1, false, true>;
 
 // Workgroups per CU that each configuration's LDS and registers allow, and
 // the dispatch from a TileCfg value to its type: f(C{}, per_cu).
@@ -1037,6 +1094,7 @@ auto with_cfg(int cfg, F &&f) -> decltype(f(C256x256w8{}, 1)) {
         case TC_256x128_K64_S3_W8_L: return f(C256x128s3w8L{}, 1);
         case TC_128x128_K64_S4_W4_L: return f(C128x128s4L{}, 1);
         case TC_32x256_K64_S4_W4: return f(C32x256k64s4{}, 1);
+        case TC_256x256_K64_S2_W8_M16: return f(C256x256w8m16{}, 1);
         default: return f(nullptr, 0);
     }
 }
@@ -1112,7 +1170,7 @@ hipError_t launch_tile_grouped_glu(int cfg, const Grouped<GluProblem> &p, hipStr
 
 // FP8 needs sub-steps of 64 K bytes that split into fragment-prefetch sets.
 template <class C>
-constexpr bool f8_ok() { return C::KSTEPS / 2 > C::PD && (C::KSTEPS / 2) % (C::PD + 1) == 0; }
+constexpr bool f8_ok() { return !C::M16 && C::KSTEPS / 2 > C::PD && (C::KSTEPS / 2) % (C::PD + 1) == 0; }
 
 template <class C, class P>
 hipError_t launch_cfg_q8(const P &p, int group_m, int split, int64_t full_tiles, const Workspace *ws,
@@ -1132,6 +1190,14 @@ hipError_t launch_cfg_q8(const P &p, int group_m, int split, int64_t full_tiles,
                            tiles_n, group_m, sk);
         return hipGetLastError();
     }
+}
+
+bool tile_is_m16(int cfg) {
+    return with_cfg(cfg, [](auto c, int) {
+        using C = decltype(c);
+        if constexpr (std::is_same<C, std::nullptr_t>::value) return false;
+        else return C::M16;
+    });
 }
 
 bool tile_f8_ok(int cfg) {
