@@ -299,8 +299,9 @@ const TableEntry TABLE[] = {
 // 256x128 8-wave tiles (3 stages, lagged refill) with split-K when 128x128
 // tiles would leave some CUs idle, else 128x128 tiles with 4 stages and the
 // lagged refill; above that the 256x256 8-wave tile when it
-// fills the 256 CUs (16x16x32 MFMA; tail split: the tiles of a partial last
-// round are split in K), the 256x128 8-wave tile (3 stages, lagged refill) when that fills
+// fills the 256 CUs (16x16x32 MFMA when the tiles fill whole rounds; else
+// 32x32 with the tail split: the tiles of a partial last round are split in
+// K), the 256x128 8-wave tile (3 stages, lagged refill) when that fills
 // them, else the 128x128 tile.
 int select(int64_t M, int64_t N, int64_t K, bool residual, const Layout &lay) {
     if (M < 0 || N < 0 || K < 0) return -1;
@@ -334,7 +335,9 @@ int select(int64_t M, int64_t N, int64_t K, bool residual, const Layout &lay) {
         else plan = pick("tile_128x128_k64s4_w4_lag");
         if (plan < 0) plan = pick("tile_128x128_k64_w4_splitk");
     } else {
-        if (tile_count(tile_shape(TC_256x256_K64_S2_W8), M, N) >= CUS) plan = pick("tile_256x256_k64_w8_m16_tailsplit");
+        const int64_t t256 = tile_count(tile_shape(TC_256x256_K64_S2_W8), M, N);
+        if (t256 >= CUS)   // whole rounds: 16x16 MFMAs; a partial last round: 32x32 with the tail split
+            plan = pick(t256 % CUS == 0 ? "tile_256x256_k64_w8_m16" : "tile_256x256_k64_w8_tailsplit");
         else if (tile_count(tile_shape(TC_256x128_K64_S3_W8_L), M, N) >= CUS) plan = pick("tile_256x128_k64s3_w8_lag");
         if (plan < 0) plan = pick("tile_128x128_k64_w4");
     }

@@ -434,8 +434,9 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
             for (int e = 0; e < 16; ++e) acc[i][j][e] = 0;
 
     // Fragment reads: row (lane % 32) of each 32-row block, chunk 2*ks + hi
-    // (32x32x16); with M16, row (lane % 16) of each 16-row block, chunk
-    // 4*ks + hi (hi = lane / 16).  Rows 16 apart share their swizzle.
+    // (32x32x16); with M16, row (lane % 16) of each 16-row block, one of
+    // the sub-step's four chunks per lane quarter hi = lane / 16.  Rows 16
+    // apart share their swizzle.
     const int frag_row = C::M16 ? (lane & 15) : (lane & 31);
     const int hi = C::M16 ? (lane >> 4) : (lane >> 5);
     const int wm0 = (wave / C::WAVES_N) * C::WM;
@@ -580,7 +581,12 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
             colk[ks] = ((4 * ks + 2 * hi) ^ frag_swz) * 16;
             colk2[ks] = ((4 * ks + 2 * hi + 1) ^ frag_swz) * 16;
         } else if constexpr (C::M16) {
-            colk[ks] = ((4 * ks + hi) ^ frag_swz) * 16;
+            // Lane quarter h takes chunk (h & 1) * 2 + (h >> 1) of the
+            // sub-step (A and B alike, so the sum over k is unchanged): a
+            // ds_read_b128 serves lanes l and l + 32 together, and their
+            // chunks must differ in the low bit, as in the 32x32 layout,
+            // for the XOR-swizzled rows to fall in distinct banks.
+            colk[ks] = ((4 * ks + ((hi & 1) << 1) + (hi >> 1)) ^ frag_swz) * 16;
             colk2[ks] = 0;
         } else {
             colk[ks] = ((2 * ks + hi) ^ frag_swz) * 16;
