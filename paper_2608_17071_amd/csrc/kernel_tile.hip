@@ -432,6 +432,15 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
         for (int j = 0; j < C::TN; ++j)
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[i][j][e] = 0;
+    // M16: the K loop accumulates 16x16 blocks in their own registers; they
+    // are moved into the quads of the 32x32 blocks once, after the loop.
+    f32x4 acc16[C::M16 ? 2 * C::TM : 1][C::M16 ? 2 * C::TN : 1];
+    if constexpr (C::M16) {
+#pragma unroll
+        for (int i = 0; i < 2 * C::TM; ++i)
+#pragma unroll
+            for (int j = 0; j < 2 * C::TN; ++j) acc16[i][j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    }
 
     // Fragment reads: row (lane % 32) of each 32-row block, chunk 2*ks + hi
     // (32x32x16); with M16, row (lane % 16) of each 16-row block, one of
@@ -649,18 +658,9 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
             static_for<0, MF>([&](auto tc) {
                 constexpr int t = decltype(tc)::value;
                 constexpr int i = t / FTN, j = t % FTN;
-                if constexpr (C::M16) {
-                    // 16x16 block (i, j) lives in quad 2*(i%2) + j%2 of
-                    // 32x32 accumulator block (i/2, j/2).
-                    constexpr int q = 2 * (i % 2) + (j % 2);
-                    f32x16 &a = acc[i / 2][j / 2];
-                    f32x4 c = {a[4 * q], a[4 * q + 1], a[4 * q + 2], a[4 * q + 3]};
-                    c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[set][i], fb[set][j], c, 0, 0, 0);
-                    a[4 * q] = c[0];
-                    a[4 * q + 1] = c[1];
-                    a[4 * q + 2] = c[2];
-                    a[4 * q + 3] = c[3];
-                } else if constexpr (I8)
+                if constexpr (C::M16)
+                    acc16[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[set][i], fb[set][j], acc16[i][j], 0, 0, 0);
+                else if constexpr (I8)
                     acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(__builtin_bit_cast(i32x4, fa[set][i]),
                                                                       __builtin_bit_cast(i32x4, fb[set][j]),
                                                                       acc[i][j], 0, 0, 0);
@@ -689,6 +689,15 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
             });
         });
         cur_stage = next_stage;
+    }
+    if constexpr (C::M16) {
+        // 16x16 block (i, j) becomes quad 2*(i%2) + j%2 of 32x32 block (i/2, j/2).
+#pragma unroll
+        for (int i = 0; i < 2 * C::TM; ++i)
+#pragma unroll
+            for (int j = 0; j < 2 * C::TN; ++j)
+#pragma unroll
+                for (int k = 0; k < 4; ++k) acc[i / 2][j / 2][4 * (2 * (i % 2) + (j % 2)) + k] = acc16[i][j][k];
     }
 
     // Epilogue.  Accumulator element e of a 32x32 block sits at row
