@@ -394,7 +394,8 @@ int select_glu(int64_t M, int64_t N, int64_t K) {
     } else if (M <= 128 || 2 * t256x128 < CUS) {
         plan = 2 * t128 <= CUS ? pick("tile_128x128_k64s3_w4_splitk") : pick("tile_128x128_k64s4_w4_lag");
     } else if (5 * t256 >= 4 * CUS) {
-        plan = pick("tile_256x256_k64_w8_tailsplit");
+        // whole rounds: 16x16 MFMAs; else 32x32 with the tail split
+        plan = pick(t256 % CUS == 0 ? "tile_256x256_k64_w8_m16" : "tile_256x256_k64_w8_tailsplit");
     } else {
         plan = pick("tile_256x128_k64s3_w8_lag");
     }

@@ -318,7 +318,7 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
     constexpr bool Q8 = I8 || F8;                  // 1-byte operands with dequantisation scales
     constexpr bool GLU = std::is_same<PB, GluProblem>::value || std::is_same<PB, I8GluProblem>::value ||
                          std::is_same<PB, F8GluProblem>::value;
-    static_assert(!C::M16 || (!Q8 && !GLU), "16x16 MFMA tiles take bf16 plain or general problems");
+    static_assert(!C::M16 || !Q8, "16x16 MFMA tiles take bf16 problems");
     constexpr int EB = Q8 ? 1 : 2;                 // bytes per operand element
     constexpr int BKE = C::ROW_BYTES / EB;         // K elements per stage
     constexpr int CKE = 16 / EB;                   // K elements per 16-byte chunk
@@ -873,7 +873,11 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
                             g = acc[i][2 * j][e];
                             u = acc[i][2 * j + 1][e];
                         }
-                        ep[(8 * (e >> 2) + 4 * hi + (e & 3)) * EPS + j * 32 + frag_row] = silu_f32(g) * u;
+                        if constexpr (C::M16)
+                            ep[(16 * (e >> 3) + 4 * hi + (e & 3)) * EPS + j * 32 + 16 * ((e >> 2) & 1) + frag_row] =
+                                silu_f32(g) * u;
+                        else
+                            ep[(8 * (e >> 2) + 4 * hi + (e & 3)) * EPS + j * 32 + frag_row] = silu_f32(g) * u;
                     }
             } else {
 #pragma unroll
@@ -1002,10 +1006,11 @@ hipError_t launch_cfg_i8(const I8Problem &p, int group_m, int split, int64_t ful
 }
 
 // SwiGLU needs an even number of 32-column blocks per wave (gate/up pairs)
-// and an even number of B loads per wave (half gate, half up), and the
-// 32x32 MFMA layout its register pairing assumes.
+// and an even number of B loads per wave (half gate, half up).  (With 16x16
+// MFMAs the gate and up blocks of a pair still hold their values in the same
+// element order, so the pairing is the same.)
 template <class C>
-constexpr bool glu_ok() { return !C::M16 && C::TN % 2 == 0 && C::B_LOADS % 2 == 0 && 32 % C::RPI == 0; }
+constexpr bool glu_ok() { return C::TN % 2 == 0 && C::B_LOADS % 2 == 0 && 32 % C::RPI == 0; }
 
 template <class C>
 hipError_t launch_cfg_glu(const GluProblem &p, int group_m, int split, int64_t full_tiles, const Workspace *ws,
@@ -1028,7 +1033,7 @@ hipError_t launch_cfg_glu(const GluProblem &p, int group_m, int split, int64_t f
 template <class C>
 hipError_t launch_cfg_i8_glu(const I8GluProblem &p, int group_m, int split, int64_t full_tiles, const Workspace *ws,
                              hipStream_t s) {
-    if constexpr (!glu_ok<C>()) {
+    if constexpr (!glu_ok<C>() || C::M16) {   // 16x16 MFMA tiles are bf16 only
         return hipErrorInvalidValue;
     } else {
         const int64_t tiles_m = (p.M + C::BM - 1) / C::BM;
