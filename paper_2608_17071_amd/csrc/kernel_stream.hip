@@ -1,5 +1,5 @@
 // Streaming MFMA kernel for few rows (M <= 64): Y = X W^T (+ R) as one pass
-// over the weight.
+// over the weight (also the general form: row strides, alpha, beta, bias).
 //
 // With at most 64 rows of X the work is bound by reading W (N*K*2 bytes)
 // from HBM, and the time a load takes to come back (microseconds under load)
@@ -14,8 +14,9 @@
 //     c ^ swz(r)), requested STAGES-1 steps ahead; one load instruction
 //     reads 64/(BK/8) whole row segments of BK*2 contiguous bytes, and the
 //     wave's own vmcnt says when a buffer has landed;
-//   * X (at most 64 rows, L2-resident after first use) is read straight
-//     into MFMA A fragments, one step ahead;
+//   * X (at most 64 rows, L2-resident after first use) is staged in the
+//     same ring beside W (16- and 32-row blocks) or read straight into
+//     MFMA A fragments one step ahead (64-row blocks);
 //   * v_mfma_f32_16x16x32_bf16 with A = 16 rows of X x 32 k and B = 16 rows
 //     of W x 32 k: MB = ceil(M/16) x ROWS/16 blocks per 32-k step, fp32
 //     accumulation in K order.
@@ -31,8 +32,9 @@
 // After the loop the four wave partials are added in LDS in wave order; a
 // split of K across workgroups goes through the fp32 workspace, where the
 // last workgroup of a row block adds the slices in slice order.  The
-// epilogue adds fp32(R) and rounds once to bf16; each output element is
-// read (R) and written (Y) by one lane, so Y may alias R.
+// epilogue adds fp32(R) (the general form: alpha*acc + beta*R + bias) and
+// rounds once to bf16; each output element is read (R) and written (Y) by
+// one lane, so Y may alias R.
 #include "internal.h"
 
 namespace kernelarc {
