@@ -219,8 +219,12 @@ bool supports(int plan, int64_t M, int64_t N, int64_t K, bool residual, const La
         case KIND_STREAM: {
             if (M < 1 || M > 64 || K % 8 != 0) return false;
             if (!stream_config_exists(pi.tile_cfg, pi.stages, pi.rows)) return false;
-            if (strided_bytes(pi.rows, K, lay.ldw) >= PANEL_LIMIT || strided_bytes(M, K, lay.ldx) >= PANEL_LIMIT ||
-                strided_bytes(M, N, lay.ldy) >= PANEL_LIMIT || strided_bytes(M, N, lay.ldr) >= PANEL_LIMIT)
+            // The kernel addresses whole 16-row token blocks of X, R and Y
+            // (rows past M fall outside the buffer resources): their 32-bit
+            // offsets must stay below the panel limit.
+            const int64_t mb = 16 * cdiv(M, 16);
+            if (strided_bytes(pi.rows, K, lay.ldw) >= PANEL_LIMIT || strided_bytes(mb, K, lay.ldx) >= PANEL_LIMIT ||
+                strided_bytes(mb, N, lay.ldy) >= PANEL_LIMIT || strided_bytes(mb, N, lay.ldr) >= PANEL_LIMIT)
                 return false;
             const int split = stream_split_of(plan, M, N, K);
             if (cdiv(N, pi.rows) * split * 256 > LIMIT_ITEMS) return false;

@@ -101,6 +101,9 @@ def test_row_block_stream_plans(ka):
     assert ka.kernelarc_plan_uses_workspace(r16, 16, 1024, 4096) == 1
     assert ka.kernelarc_plan_uses_workspace(r32, 16, 4096, 4096) == 1
     assert ka.kernelarc_plan_uses_workspace(r16, 16, 4096, 256) == 0   # too shallow to split
+    # the kernel addresses whole 16-row token blocks: a wide output whose
+    # 16-row block passes 2^31 bytes is refused even for one row
+    assert ka.plan_supports(r16, 1, 1 << 25, 8) and not ka.plan_supports(r16, 1, 1 << 26, 8)
     sel = lambda m, n, k: names[ka.select_plan(m, n, k, True)]
     assert sel(16, 4096, 4096) == "stream_mfma16_r16_k128s2"
     assert sel(8, 2048, 2048) == "stream_mfma16_r16_k128s2"
