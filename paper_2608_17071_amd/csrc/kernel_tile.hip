@@ -318,7 +318,7 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
     constexpr bool Q8 = I8 || F8;                  // 1-byte operands with dequantisation scales
     constexpr bool GLU = std::is_same<PB, GluProblem>::value || std::is_same<PB, I8GluProblem>::value ||
                          std::is_same<PB, F8GluProblem>::value;
-    static_assert(!C::M16 || !Q8, "16x16 MFMA tiles take bf16 problems");
+    static_assert(!C::M16 || (!F8 && !(I8 && GLU)), "16x16 MFMA tiles take bf16 and plain INT8 problems");
     constexpr int EB = Q8 ? 1 : 2;                 // bytes per operand element
     constexpr int BKE = C::ROW_BYTES / EB;         // K elements per stage
     constexpr int CKE = 16 / EB;                   // K elements per 16-byte chunk
@@ -434,12 +434,13 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
             for (int e = 0; e < 16; ++e) acc[i][j][e] = 0;
     // M16: the K loop accumulates 16x16 blocks in their own registers; they
     // are moved into the quads of the 32x32 blocks once, after the loop.
-    f32x4 acc16[C::M16 ? 2 * C::TM : 1][C::M16 ? 2 * C::TN : 1];
+    using AccQ = typename std::conditional<I8, i32x4, f32x4>::type;
+    AccQ acc16[C::M16 ? 2 * C::TM : 1][C::M16 ? 2 * C::TN : 1];
     if constexpr (C::M16) {
 #pragma unroll
         for (int i = 0; i < 2 * C::TM; ++i)
 #pragma unroll
-            for (int j = 0; j < 2 * C::TN; ++j) acc16[i][j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+            for (int j = 0; j < 2 * C::TN; ++j) acc16[i][j] = AccQ{0, 0, 0, 0};
     }
 
     // Fragment reads: row (lane % 32) of each 32-row block, chunk 2*ks + hi
@@ -659,7 +660,15 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
                 constexpr int t = decltype(tc)::value;
                 constexpr int i = t / FTN, j = t % FTN;
                 if constexpr (C::M16)
-                    acc16[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[set][i], fb[set][j], acc16[i][j], 0, 0, 0);
+                {
+                    if constexpr (I8)   // 16x16x64 int8: the same 16 bytes per lane
+                        acc16[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4, fa[set][i]),
+                                                                            __builtin_bit_cast(i32x4, fb[set][j]),
+                                                                            acc16[i][j], 0, 0, 0);
+                    else
+                        acc16[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[set][i], fb[set][j], acc16[i][j], 0,
+                                                                              0, 0);
+                }
                 else if constexpr (I8)
                     acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(__builtin_bit_cast(i32x4, fa[set][i]),
                                                                       __builtin_bit_cast(i32x4, fb[set][j]),
@@ -990,19 +999,15 @@ hipError_t launch_cfg(const Problem &p, int group_m, int split, int64_t full_til
 template <class C>
 hipError_t launch_cfg_i8(const I8Problem &p, int group_m, int split, int64_t full_tiles, const Workspace *ws,
                          hipStream_t s) {
-    if constexpr (C::M16) {
-        return hipErrorInvalidValue;   // 16x16 MFMA tiles are bf16 only
-    } else {
-        const int64_t tiles_m = (p.M + C::BM - 1) / C::BM;
-        const int64_t tiles_n = (p.N + C::BN - 1) / C::BN;
-        const int64_t tiles = tiles_m * tiles_n;
-        SplitK sk;
-        if (!split_args<C, 2 * C::BK>(p.K, tiles, split, full_tiles, ws, sk)) return hipErrorInvalidValue;
-        const int64_t wgs = sk.full_tiles + (tiles - sk.full_tiles) * sk.split;
-        hipLaunchKernelGGL((tile_kernel<C, I8Problem>), dim3(static_cast<unsigned>(wgs)), dim3(C::THREADS), 0, s, p,
-                           tiles_m, tiles_n, group_m, sk);
-        return hipGetLastError();
-    }
+    const int64_t tiles_m = (p.M + C::BM - 1) / C::BM;
+    const int64_t tiles_n = (p.N + C::BN - 1) / C::BN;
+    const int64_t tiles = tiles_m * tiles_n;
+    SplitK sk;
+    if (!split_args<C, 2 * C::BK>(p.K, tiles, split, full_tiles, ws, sk)) return hipErrorInvalidValue;
+    const int64_t wgs = sk.full_tiles + (tiles - sk.full_tiles) * sk.split;
+    hipLaunchKernelGGL((tile_kernel<C, I8Problem>), dim3(static_cast<unsigned>(wgs)), dim3(C::THREADS), 0, s, p,
+                       tiles_m, tiles_n, group_m, sk);
+    return hipGetLastError();
 }
 
 // SwiGLU needs an even number of 32-column blocks per wave (gate/up pairs)

@@ -122,7 +122,7 @@ def _unit_case(M, N, K, seed, swiglu):
 @pytest.mark.parametrize("name", ["tile_256x256_k64_w8", "tile_64x64_k128s3_w4_splitk", "tile_128x128_k64_g2",
                                   "tile_64x64_k64_g4_splitk", "tile_256x128_k64s3_w8_lag_splitk",
                                   "tile_32x256_k64s4_w4_splitk", "generic_64x64_scalar",
-                                  "stream_mfma16_r16_k128s2", "stream_mfma16_r32_k64s4"])
+                                  "stream_mfma16_r16_k128s2", "stream_mfma16_r32_k64s4", "tile_256x256_k64_w8_m16"])
 def test_i8_integer_sums_bit_exact(ka, name):
     """Unit scales and |A| <= 256: the outputs are the exact integer sums."""
     plan = ka.plan_names().index(name)
