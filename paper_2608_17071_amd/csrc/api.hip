@@ -296,7 +296,9 @@ const TableEntry TABLE[] = {
 // rows, with 16-row blocks of W when they fit one round on the CUs (N up to
 // 4096; no cross-workgroup split there) and 64-row blocks with split-K
 // beyond; up to 64 rows, the 16-row streaming kernel while N <= 2048 and
-// K <= 4096; up to 1024 rows: 64x64 tiles (3 stages of K depth
+// K <= 4096; up to 1024 rows: the 256x256 tile when its tiles reach 2/3
+// of the CUs, the 256x128 3-stage lagged tile above 512 rows when its tiles
+// fill them, else 64x64 tiles (3 stages of K depth
 // 128, split-K) while they fill at most half the CUs, 64x64 tiles (4 stages
 // of depth 64, two per CU) while they fit one round, else 128x128 tiles
 // with 3 stages and split-K when they would keep at most half the CUs busy,
@@ -332,7 +334,13 @@ int select(int64_t M, int64_t N, int64_t K, bool residual, const Layout &lay) {
     } else if (M <= 1024) {
         const int64_t tiles64 = tile_count(tile_shape(TC_64x64_K64_S4_W4), M, N);
         const int64_t tiles128 = tile_count(tile_shape(TC_128x128_K64_S4_W4_L), M, N);
-        if (2 * tiles64 <= CUS) plan = pick("tile_64x64_k128s3_w4_splitk");
+        const int64_t t256 = tile_count(tile_shape(TC_256x256_K64_S2_W8), M, N);
+        const int64_t t256x128 = tile_count(tile_shape(TC_256x128_K64_S3_W8_L), M, N);
+        if (3 * t256 >= 2 * CUS)   // wide outputs: the 256x256 tiles reach 2/3 of the CUs
+            plan = pick(t256 % CUS == 0 ? "tile_256x256_k64_w8_m16" : "tile_256x256_k64_w8_tailsplit");
+        else if (t256x128 >= CUS && M > 512)
+            plan = pick("tile_256x128_k64s3_w8_lag");
+        else if (2 * tiles64 <= CUS) plan = pick("tile_64x64_k128s3_w4_splitk");
         else if (tiles64 <= 2 * CUS) plan = pick("tile_64x64_k64s4_w4");
         else if (2 * tiles128 <= CUS) plan = pick("tile_128x128_k64s3_w4_splitk");
         else if (tiles128 < CUS) plan = pick("tile_256x128_k64s3_w8_lag_splitk");

@@ -114,6 +114,10 @@ def test_row_block_stream_plans(ka):
     assert sel(64, 2048, 8192).startswith("tile_")
     assert sel(64, 4096, 4096).startswith("tile_")
     assert sel(3, 4096, 4096) == "gemv_valu_w4"
+    # wide outputs between 512 and 1024 rows take the big tiles
+    assert sel(1024, 13824, 5120).startswith("tile_256x256_k64_w8")
+    assert sel(1024, 8192, 8192) == "tile_256x128_k64s3_w8_lag"
+    assert sel(512, 8192, 8192) == "tile_128x128_k64s4_w4_lag"        # the measured table entry
 
 
 def test_validation_before_any_device_work(ka):
