@@ -81,14 +81,15 @@ def source_digest(paths):
 
 
 # Kernel symbol fragment of each tile plan (rocprofv3 reports symbols).
-# Cfg<BM, BN, BK, WAVES_M, WAVES_N, STAGES, WAVES_PER_EU, KGROUPS, PD, LAG, M16>.
+# Cfg<BM, BN, BK, WAVES_M, WAVES_N, STAGES, WAVES_PER_EU, LAG, M16>.
 PLAN_SYMBOL = {
-    "tile_256x256_k64_w8": "Cfg<256, 256, 64, 2, 4, 2, 2, 1, 1, false, false>",
-    "tile_256x256_k64_w8_m16": "Cfg<256, 256, 64, 2, 4, 2, 2, 1, 1, false, true>",
+    "tile_256x256_k64_w8": "Cfg<256, 256, 64, 2, 4, 2, 2, false, false>",
+    "tile_256x256_k64_w8_m16": "Cfg<256, 256, 64, 2, 4, 2, 2, false, true>",
 }
 # The plan whose HBM traffic the counter runs summarise (the big sweep shapes' plan).
 TRAFFIC_PLAN = "tile_256x256_k64_w8_m16"
-KERNEL_SOURCES = ["paper_2608_17071_amd/csrc/kernel_tile.hip", "paper_2608_17071_amd/csrc/internal.h"]
+KERNEL_SOURCES = ["paper_2608_17071_amd/csrc/tile_kernel.h", "paper_2608_17071_amd/csrc/kernel_tile.hip",
+                  "paper_2608_17071_amd/csrc/internal.h"]
 
 
 def summarize_traffic(pmc_dir, plan, shapes, command):

@@ -22,15 +22,21 @@
  *   - X is [M,K], W is [N,K], R and Y are [M,N]; all dense row-major with no
  *     padding (leading dimensions K, K, N, N);
  *   - the caller owns every buffer; the library never allocates, frees or
- *     retains them.  Internal state is limited to a per-device property cache
- *     and per-device split-K workspaces that the library allocates once and
- *     keeps until the process ends.
+ *     retains them.  Internal state is limited to a per-device property
+ *     cache, a per-thread cache of plan choices, and a per-device split-K
+ *     workspace (64 MiB of fp32 partials and 64 Ki arrival counters) that
+ *     the first call needing it allocates and keeps until the process ends.
  *
- * Execution: calls enqueue work on `stream` and return without synchronising;
- * a fault in a kernel surfaces at the caller's next synchronisation.  Calls
- * on one stream are ordered; the split-K workspace of a device is shared, so
- * calls that may run concurrently on different streams of the same device
- * must not both pick a split-K plan (kernelarc_plan_uses_workspace).
+ * Execution: calls enqueue work on `stream` and return without synchronising
+ * the stream or the device; a fault in a kernel surfaces at the caller's next
+ * synchronisation.  The call that allocates the split-K workspace (the first
+ * one on a device whose plan splits K) clears its counters with a kernel on
+ * `stream`; under stream capture that call cannot allocate and returns
+ * KERNELARC_ERR_UNSUPPORTED instead, so make one such call before capturing.
+ * Calls on one stream are ordered; the split-K workspace of a device is
+ * shared, so calls that may run concurrently on different streams of the
+ * same device must not both pick a split-K plan
+ * (kernelarc_plan_uses_workspace).
  *
  * Errors: every entry point returns a status (KERNELARC_OK on success) and
  * never throws, aborts or prints.  kernelarc_last_error() gives a detail
@@ -91,8 +97,18 @@ int kernelarc_gemm_bf16(int64_t M, int64_t N, int64_t K,
  */
 int kernelarc_plan_count(void);
 
-/* Static, NUL-terminated name of a plan, or NULL for an unknown id. */
-const char *kernelarc_plan_name(int plan);
+/*
+ * Name of the plan the library runs for this shape (Alg. 3's per-M plan
+ * choice) when the pointers are 16-byte aligned: written NUL-terminated into
+ * buf, which holds len bytes.  Returns KERNELARC_OK; KERNELARC_ERR_INVALID_ARG
+ * for negative sizes, buf == NULL, or len too small for the name (then
+ * nothing is written).  Plan names are shorter than 64 bytes.  Does not touch
+ * the GPU.
+ */
+int kernelarc_plan_name(int64_t M, int64_t N, int64_t K, int residual, char *buf, size_t len);
+
+/* Static, NUL-terminated name of plan id `plan`, or NULL for an unknown id. */
+const char *kernelarc_plan_label(int plan);
 
 /*
  * 1 if `plan` can compute this shape (size limits and the K % 8 rule of the

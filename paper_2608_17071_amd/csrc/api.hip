@@ -41,7 +41,7 @@ constexpr int64_t WS_COUNTERS = int64_t{1} << 16;
 constexpr int64_t CUS = 256;        // MI355X compute units
 constexpr int MAX_SPLIT = 16;
 
-enum PlanKind { KIND_GENERIC, KIND_SKINNY, KIND_GEMV, KIND_TILE, KIND_STREAM };
+enum PlanKind { KIND_GENERIC, KIND_GEMV, KIND_TILE, KIND_STREAM };
 
 struct PlanInfo {
     const char *name;
@@ -54,87 +54,32 @@ struct PlanInfo {
     int rows = 64;  // stream plans: W rows per workgroup
 };
 
+// The plans the table and the rules select (plus the generic fallback).
+// Order fixes the plan ids; PLAN_GENERIC and PLAN_GEMV are the first two.
 const PlanInfo PLANS[] = {
     {"generic_64x64_scalar", KIND_GENERIC, -1, 1},
-    {"skinny_mfma16_w8", KIND_SKINNY, -1, 1},
-    {"skinny_mfma16_w8_splitk", KIND_SKINNY, -1, 0},
     {"gemv_valu_w4", KIND_GEMV, -1, 1},
-    {"tile_256x256_k64_w8", KIND_TILE, TC_256x256_K64_S2_W8, 1},
-    {"tile_256x256_k64_w4", KIND_TILE, TC_256x256_K64_S2_W4, 1},
-    {"tile_256x128_k64_w8", KIND_TILE, TC_256x128_K64_S2_W8, 1},
-    {"tile_128x256_k64_w8", KIND_TILE, TC_128x256_K64_S2_W8, 1},
-    {"tile_256x128_k64_w4", KIND_TILE, TC_256x128_K64_S2_W4, 1},
-    {"tile_128x128_k64_w4", KIND_TILE, TC_128x128_K64_S2_W4, 1},
-    {"tile_64x256_k64_w4", KIND_TILE, TC_64x256_K64_S2_W4, 1},
-    {"tile_256x256_k64_w8_splitk", KIND_TILE, TC_256x256_K64_S2_W8, 0},
-    {"tile_256x128_k64_w8_splitk", KIND_TILE, TC_256x128_K64_S2_W8, 0},
-    {"tile_128x256_k64_w8_splitk", KIND_TILE, TC_128x256_K64_S2_W8, 0},
-    {"tile_128x128_k64_w4_splitk", KIND_TILE, TC_128x128_K64_S2_W4, 0},
-    {"tile_64x256_k64_w4_splitk", KIND_TILE, TC_64x256_K64_S2_W4, 0},
-    {"tile_128x128_k64s4_w4", KIND_TILE, TC_128x128_K64_S4_W4, 1},
-    {"tile_128x128_k64s4_w4_splitk", KIND_TILE, TC_128x128_K64_S4_W4, 0},
-    {"tile_128x128_k64s3_w4", KIND_TILE, TC_128x128_K64_S3_W4, 1},
-    {"tile_128x128_k64s3_w4_splitk", KIND_TILE, TC_128x128_K64_S3_W4, 0},
-    {"tile_64x256_k64s3_w4_splitk", KIND_TILE, TC_64x256_K64_S3_W4, 0},
-    {"tile_256x128_k64s3_w8", KIND_TILE, TC_256x128_K64_S3_W8, 1},
-    {"tile_256x128_k64s3_w8_splitk", KIND_TILE, TC_256x128_K64_S3_W8, 0},
-    {"tile_64x64_k64_w4", KIND_TILE, TC_64x64_K64_S2_W4, 1},
-    {"tile_64x64_k64_w4_splitk", KIND_TILE, TC_64x64_K64_S2_W4, 0},
-    {"tile_64x128_k64_w4", KIND_TILE, TC_64x128_K64_S2_W4, 1},
-    {"tile_64x128_k64_w4_splitk", KIND_TILE, TC_64x128_K64_S2_W4, 0},
-    {"tile_64x64_k128_w4", KIND_TILE, TC_64x64_K128_S2_W4, 1},
-    {"tile_64x64_k128_w4_splitk", KIND_TILE, TC_64x64_K128_S2_W4, 0},
-    {"tile_128x128_k128_w4", KIND_TILE, TC_128x128_K128_S2_W4, 1},
-    {"tile_128x128_k128_w4_splitk", KIND_TILE, TC_128x128_K128_S2_W4, 0},
-    {"tile_64x128_k128_w4", KIND_TILE, TC_64x128_K128_S2_W4, 1},
-    {"tile_64x128_k128_w4_splitk", KIND_TILE, TC_64x128_K128_S2_W4, 0},
-    {"tile_64x64_k128s3_w4", KIND_TILE, TC_64x64_K128_S3_W4, 1},
-    {"tile_64x64_k128s3_w4_splitk", KIND_TILE, TC_64x64_K128_S3_W4, 0},
+    {"stream_mfma16_r16_k128s2", KIND_STREAM, 128, -1, 2, 16},
+    {"stream_mfma16_r32_k64s4", KIND_STREAM, 64, -1, 4, 32},
+    {"stream_mfma16_k64_splitk", KIND_STREAM, 64, 0},
     {"tile_64x64_k64s4_w4", KIND_TILE, TC_64x64_K64_S4_W4, 1},
-    {"tile_64x64_k64s4_w4_splitk", KIND_TILE, TC_64x64_K64_S4_W4, 0},
-    {"tile_128x128_k32s4_w4", KIND_TILE, TC_128x128_K32_S4_W4, 1},
-    {"tile_128x128_k32s4_w4_splitk", KIND_TILE, TC_128x128_K32_S4_W4, 0},
-    {"tile_64x64_k64s8_w4", KIND_TILE, TC_64x64_K64_S8_W4, 1},
-    {"tile_64x64_k64s8_w4_splitk", KIND_TILE, TC_64x64_K64_S8_W4, 0},
+    {"tile_64x64_k128s3_w4_splitk", KIND_TILE, TC_64x64_K128_S3_W4, 0},
     {"tile_64x128_k64s4_w4", KIND_TILE, TC_64x128_K64_S4_W4, 1},
     {"tile_64x128_k64s4_w4_splitk", KIND_TILE, TC_64x128_K64_S4_W4, 0},
-    {"tile_64x64_k128_g2", KIND_TILE, TC_64x64_K128_S2_G2, 1},
-    {"tile_64x64_k128_g2_splitk", KIND_TILE, TC_64x64_K128_S2_G2, 0},
-    {"tile_128x128_k64_g2", KIND_TILE, TC_128x128_K64_S2_G2, 1},
-    {"tile_128x128_k64_g2_splitk", KIND_TILE, TC_128x128_K64_S2_G2, 0},
-    {"tile_64x64_k64_g4", KIND_TILE, TC_64x64_K64_S2_G4, 1},
-    {"tile_64x64_k64_g4_splitk", KIND_TILE, TC_64x64_K64_S2_G4, 0},
-    {"tile_128x128_k64_w4_tailsplit", KIND_TILE, TC_128x128_K64_S2_W4, -1},
-    {"tile_256x256_k64_w8_tailsplit", KIND_TILE, TC_256x256_K64_S2_W8, -1},
-    {"tile_256x128_k64_w8_tailsplit", KIND_TILE, TC_256x128_K64_S2_W8, -1},
+    {"tile_128x128_k64_w4", KIND_TILE, TC_128x128_K64_S2_W4, 1},
+    {"tile_128x128_k64_w4_splitk", KIND_TILE, TC_128x128_K64_S2_W4, 0},
+    {"tile_128x128_k64s3_w4_splitk", KIND_TILE, TC_128x128_K64_S3_W4, 0},
+    {"tile_128x128_k64s4_w4_lag", KIND_TILE, TC_128x128_K64_S4_W4_L, 1},
+    {"tile_256x128_k64s3_w8_splitk", KIND_TILE, TC_256x128_K64_S3_W8, 0},
     {"tile_256x128_k64s3_w8_lag", KIND_TILE, TC_256x128_K64_S3_W8_L, 1},
     {"tile_256x128_k64s3_w8_lag_splitk", KIND_TILE, TC_256x128_K64_S3_W8_L, 0},
-    {"tile_128x128_k64s4_w4_lag", KIND_TILE, TC_128x128_K64_S4_W4_L, 1},
-    {"tile_128x128_k64s4_w4_lag_splitk", KIND_TILE, TC_128x128_K64_S4_W4_L, 0},
-    {"stream_mfma16_k128", KIND_STREAM, 128, 1},
-    {"stream_mfma16_k128_splitk", KIND_STREAM, 128, 0},
-    {"stream_mfma16_k64_splitk", KIND_STREAM, 64, 0},
-    {"tile_32x256_k64s4_w4", KIND_TILE, TC_32x256_K64_S4_W4, 1},
-    {"tile_32x256_k64s4_w4_splitk", KIND_TILE, TC_32x256_K64_S4_W4, 0},
-    {"tile_256x256_k64_w4_tailsplit", KIND_TILE, TC_256x256_K64_S2_W4, -1},
-    {"tile_128x256_k64_w8_tailsplit", KIND_TILE, TC_128x256_K64_S2_W8, -1},
-    {"stream_mfma16_r16_k64s4", KIND_STREAM, 64, -1, 4, 16},
-    {"stream_mfma16_r16_k64s8", KIND_STREAM, 64, -1, 8, 16},
-    {"stream_mfma16_r16_k128s2", KIND_STREAM, 128, -1, 2, 16},
-    {"stream_mfma16_r16_k128s4", KIND_STREAM, 128, -1, 4, 16},
-    {"stream_mfma16_r32_k64s4", KIND_STREAM, 64, -1, 4, 32},
+    {"tile_256x256_k64_w8", KIND_TILE, TC_256x256_K64_S2_W8, 1},
+    {"tile_256x256_k64_w8_tailsplit", KIND_TILE, TC_256x256_K64_S2_W8, -1},
     {"tile_256x256_k64_w8_m16", KIND_TILE, TC_256x256_K64_S2_W8_M16, 1},
-    {"tile_256x256_k64_w8_m16_tailsplit", KIND_TILE, TC_256x256_K64_S2_W8_M16, -1},
 };
 constexpr int NUM_PLANS = static_cast<int>(sizeof(PLANS) / sizeof(PLANS[0]));
 
 int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
-
-int skinny_split_of(int plan, int64_t M, int64_t N, int64_t K) {
-    if (plan == PLAN_SKINNY) return 1;
-    const int rule = skinny_split_for(M, N, K);
-    return rule < 2 ? 2 : rule;
-}
 
 int64_t tile_count(const TileShape &ts, int64_t M, int64_t N) { return cdiv(M, ts.bm) * cdiv(N, ts.bn); }
 
@@ -186,9 +131,8 @@ int stream_split_of(int plan, int64_t M, int64_t N, int64_t K) {
 }
 
 // Row strides of a call and whether it is the general form (strides other
-// than dense, alpha or beta other than 1, or a bias).  The skinny kernel
-// computes only the dense plain form; the GEMV, streaming, tile and generic
-// kernels compute every form.
+// than dense, alpha or beta other than 1, or a bias).  Every kernel computes
+// every form.
 struct Layout {
     int64_t ldx, ldw, ldr, ldy;
     bool general;
@@ -203,16 +147,6 @@ bool supports(int plan, int64_t M, int64_t N, int64_t K, bool residual, const La
     switch (pi.kind) {
         case KIND_GENERIC:
             return cdiv(M, 64) * cdiv(N, 64) * 256 <= LIMIT_ITEMS;
-        case KIND_SKINNY: {
-            if (lay.general || M < 1 || M > 64 || K % 8 != 0) return false;
-            if (N * K * 2 >= PANEL_LIMIT || 64 * K * 2 >= PANEL_LIMIT) return false;
-            const int split = skinny_split_of(plan, M, N, K);
-            if (cdiv(N, 16) * split * 512 > LIMIT_ITEMS) return false;
-            if (split > 1 && (skinny_workspace_floats(M, N, split) > WS_PARTIAL_FLOATS ||
-                              skinny_counter_count(N) > WS_COUNTERS))
-                return false;
-            return true;
-        }
         case KIND_GEMV:
             return gemv_fits(M, N, K, lay.ldw) && cdiv(N, 4) * 256 <= LIMIT_ITEMS &&
                    strided_bytes(M, N, lay.ldy) < PANEL_LIMIT && strided_bytes(M, N, lay.ldr) < PANEL_LIMIT;
@@ -329,7 +263,6 @@ int select(int64_t M, int64_t N, int64_t K, bool residual, const Layout &lay) {
     if (plan >= 0) return plan;
     if (M >= 1 && M <= 32) {
         plan = pick("stream_mfma16_k64_splitk");
-        if (plan < 0) plan = pick("skinny_mfma16_w8");
         if (plan < 0) plan = pick("tile_64x64_k128s3_w4_splitk");
     } else if (M <= 1024) {
         const int64_t tiles64 = tile_count(tile_shape(TC_64x64_K64_S4_W4), M, N);
@@ -476,7 +409,6 @@ int select_i8(int64_t M, int64_t N, int64_t K, bool glu, bool f8 = false) {
     // the CUs (an INT8 tile covers its K range in half the steps: at
     // M = 1024, N = 13824, K = 5120, 90 us against 128 us for 128x128).
     if (plan == plan_index("tile_256x256_k64_w8_tailsplit") || plan == plan_index("tile_256x256_k64_w8_m16") ||
-        plan == plan_index("tile_256x256_k64_w8_m16_tailsplit") ||
         (!glu && 5 * tile_count(tile_shape(TC_256x256_K64_S2_W8), M, N) >= 4 * CUS))
         plan = plan_index("tile_256x256_k64_w8");
     if (plan >= 0 && plan != PLAN_GENERIC && supports_i8(plan, M, N, K, glu, f8)) return plan;
@@ -524,6 +456,43 @@ int select_grouped(int64_t G, int64_t Mpad, int64_t N, int64_t K, bool glu) {
     return PLAN_GENERIC;
 }
 
+// ---------------------------------------------------------- plan cache ----
+// Alg. 3 keeps the chosen plan per shape so that the table and the rules are
+// consulted once.  The key is everything a choice depends on (the operation,
+// the sizes, the row strides and whether the call is the general form),
+// never data.  Each thread holds its own direct-mapped table, so a lookup
+// takes no lock; a colliding shape replaces the entry.
+enum PlanOp { OP_LINEAR = 0, OP_GLU, OP_I8, OP_I8_GLU, OP_F8, OP_F8_GLU, OP_GROUPED, OP_GROUPED_GLU };
+
+struct PlanKey {
+    int op;
+    int flags;   // OP_LINEAR: bit 0 residual, bit 1 general form
+    int64_t M, N, K, a, b, c, d;   // OP_LINEAR: row strides; OP_GROUPED*: a = G
+    bool operator==(const PlanKey &o) const {
+        return op == o.op && flags == o.flags && M == o.M && N == o.N && K == o.K && a == o.a && b == o.b &&
+               c == o.c && d == o.d;
+    }
+};
+
+constexpr int PLAN_CACHE_SLOTS = 64;
+struct PlanCacheEntry {
+    PlanKey key;
+    int plan;
+    bool valid;
+};
+thread_local PlanCacheEntry g_plan_cache[PLAN_CACHE_SLOTS];
+
+template <class F>
+int cached_plan(const PlanKey &k, F &&choose) {
+    uint64_t h = static_cast<uint64_t>(k.op) * 0x9E3779B97F4A7C15ull ^ static_cast<uint64_t>(k.flags);
+    for (int64_t v : {k.M, k.N, k.K, k.a, k.b, k.c, k.d}) h = (h ^ static_cast<uint64_t>(v)) * 0x100000001B3ull;
+    PlanCacheEntry &e = g_plan_cache[(h ^ (h >> 29)) % PLAN_CACHE_SLOTS];
+    if (e.valid && e.key == k) return e.plan;
+    const int plan = choose();
+    e = PlanCacheEntry{k, plan, true};
+    return plan;
+}
+
 // ------------------------------------------------------------ devices ----
 constexpr int MAX_DEVICES = 64;
 
@@ -565,21 +534,47 @@ int current_device(int *dev, int *num_cus) {
     return KERNELARC_OK;
 }
 
-// The split-K workspace of device `dev`, allocated and zeroed on first use.
+// Sets n counters to zero on the caller's stream: a kernel rather than
+// hipMemsetAsync, so the clearing is an ordinary kernel node if a caller
+// captures the stream.
+__global__ void zero_counters_kernel(unsigned *c, int64_t n) {
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i < n) c[i] = 0u;
+}
+
+hipError_t zero_counters(unsigned *c, int64_t n, hipStream_t stream) {
+    hipLaunchKernelGGL(zero_counters_kernel, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0, stream, c,
+                       n);
+    return hipGetLastError();
+}
+
+// The split-K workspace of device `dev`, allocated on first use.  Its
+// counters are cleared by a kernel on `stream`, ahead of the call's own
+// kernel on the same stream; nothing waits for the stream.  The kernels
+// leave every counter at zero, so later calls need no clearing.  A first
+// use under stream capture cannot allocate (and the clearing would only run
+// when the graph is replayed), so it is refused.
 int workspace(int dev, hipStream_t stream, Workspace *out) {
     std::lock_guard<std::mutex> lock(g_mutex);
     DeviceState &st = g_devices[dev];
     if (!st.ws_partials) {
+        hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+        hipError_t e = hipStreamIsCapturing(stream, &cap);
+        if (e != hipSuccess)
+            return fail(KERNELARC_ERR_LAUNCH, "hipStreamIsCapturing: %s", hipGetErrorString(e));
+        if (cap != hipStreamCaptureStatusNone)
+            return fail(KERNELARC_ERR_UNSUPPORTED,
+                        "the split-K workspace of device %d is allocated by the first call that needs it, which "
+                        "cannot run under stream capture: make one call of this plan before capturing", dev);
         void *parts = nullptr;
         void *counters = nullptr;
-        hipError_t e = hipMalloc(&parts, WS_PARTIAL_FLOATS * sizeof(float));
+        e = hipMalloc(&parts, WS_PARTIAL_FLOATS * sizeof(float));
         if (e == hipSuccess) e = hipMalloc(&counters, WS_COUNTERS * sizeof(unsigned));
-        if (e == hipSuccess) e = hipMemsetAsync(counters, 0, WS_COUNTERS * sizeof(unsigned), stream);
-        if (e == hipSuccess) e = hipStreamSynchronize(stream);
+        if (e == hipSuccess) e = zero_counters(static_cast<unsigned *>(counters), WS_COUNTERS, stream);
         if (e != hipSuccess) {
             if (parts) (void)hipFree(parts);
             if (counters) (void)hipFree(counters);
-            return fail(KERNELARC_ERR_LAUNCH, "split-K workspace allocation: %s", hipGetErrorString(e));
+            return fail(KERNELARC_ERR_LAUNCH, "split-K workspace set-up: %s", hipGetErrorString(e));
         }
         st.ws_partials = static_cast<float *>(parts);
         st.ws_counters = static_cast<unsigned *>(counters);
@@ -655,7 +650,9 @@ int run(int plan, Request q, hipStream_t stream) {
     const bool vec_ok = aligned16(q.X) && aligned16(q.W) && aligned16(q.Y) && (!residual || aligned16(q.R)) &&
                         K % 8 == 0 && q.ldx % 8 == 0 && q.ldw % 8 == 0;
     if (plan < 0) {
-        plan = select(M, N, K, residual, lay);
+        const PlanKey key{OP_LINEAR, (residual ? 1 : 0) | (lay.general ? 2 : 0), M, N, K, lay.ldx, lay.ldw, lay.ldr,
+                          lay.ldy};
+        plan = cached_plan(key, [&] { return select(M, N, K, residual, lay); });
         if (plan != PLAN_GENERIC && !vec_ok) plan = PLAN_GENERIC;
     } else {
         if (!supports(plan, M, N, K, residual, lay))
@@ -676,16 +673,6 @@ int run(int plan, Request q, hipStream_t stream) {
         case KIND_GENERIC:
             e = launch_generic(p, stream);
             break;
-        case KIND_SKINNY: {
-            const int split = skinny_split_of(plan, M, N, K);
-            Workspace ws{};
-            if (split > 1) {
-                const int wst = workspace(dev, stream, &ws);
-                if (wst != KERNELARC_OK) return wst;
-            }
-            e = launch_skinny(p, split, split > 1 ? &ws : nullptr, stream);
-            break;
-        }
         case KIND_GEMV:
             e = launch_gemv(p, stream);
             break;
@@ -739,7 +726,7 @@ int run_glu(int plan, int64_t M, int64_t N, int64_t K, const void *X, const void
 
     const bool vec_ok = aligned16(X) && aligned16(Wg) && aligned16(Wu) && aligned16(H) && K % 8 == 0;
     if (plan < 0) {
-        plan = select_glu(M, N, K);
+        plan = cached_plan(PlanKey{OP_GLU, 0, M, N, K, 0, 0, 0, 0}, [&] { return select_glu(M, N, K); });
         if (plan != PLAN_GENERIC && !vec_ok) plan = PLAN_GENERIC;
     } else {
         if (!supports_glu(plan, M, N, K))
@@ -798,7 +785,8 @@ int run_grouped(int plan, bool glu, int64_t G, int64_t Mpad, int64_t N, int64_t 
 
     const bool vec_ok = aligned16(X) && aligned16(W) && (!glu || aligned16(W2)) && aligned16(Y) && K % 8 == 0;
     if (plan < 0) {
-        plan = select_grouped(G, Mpad, N, K, glu);
+        plan = cached_plan(PlanKey{glu ? OP_GROUPED_GLU : OP_GROUPED, 0, Mpad, N, K, G, 0, 0, 0},
+                           [&] { return select_grouped(G, Mpad, N, K, glu); });
         if (plan != PLAN_GENERIC && !vec_ok) plan = PLAN_GENERIC;
     } else {
         if (!supports_grouped(plan, G, Mpad, N, K, glu))
@@ -872,7 +860,8 @@ int run_i8(int plan, bool glu, int64_t M, int64_t N, int64_t K, const void *X, c
     const bool vec_ok = aligned16(X) && aligned16(W) && (!glu || aligned16(W2)) && aligned16(Y) &&
                         (!R || aligned16(R)) && K % 16 == 0;
     if (plan < 0) {
-        plan = select_i8(M, N, K, glu, f8);
+        const int op = f8 ? (glu ? OP_F8_GLU : OP_F8) : (glu ? OP_I8_GLU : OP_I8);
+        plan = cached_plan(PlanKey{op, 0, M, N, K, 0, 0, 0, 0}, [&] { return select_i8(M, N, K, glu, f8); });
         if (plan != PLAN_GENERIC && !vec_ok) plan = PLAN_GENERIC;
     } else {
         if (!supports_i8(plan, M, N, K, glu, f8))
@@ -1160,8 +1149,21 @@ int kernelarc_plan_supports_grouped(int plan, int64_t G, int64_t M_pad, int64_t 
 
 int kernelarc_plan_count(void) { return NUM_PLANS; }
 
-const char *kernelarc_plan_name(int plan) {
+const char *kernelarc_plan_label(int plan) {
     return (plan >= 0 && plan < NUM_PLANS) ? PLANS[plan].name : nullptr;
+}
+
+int kernelarc_plan_name(int64_t M, int64_t N, int64_t K, int residual, char *buf, size_t len) {
+    g_last_error[0] = '\0';
+    if (M < 0 || N < 0 || K < 0)
+        return fail(KERNELARC_ERR_INVALID_ARG, "negative size M=%lld N=%lld K=%lld", (long long)M, (long long)N,
+                    (long long)K);
+    if (!buf) return fail(KERNELARC_ERR_INVALID_ARG, "buf is NULL");
+    const int plan = select(M, N, K, residual != 0, dense_layout(N, K));
+    const size_t need = std::strlen(PLANS[plan].name) + 1;
+    if (len < need) return fail(KERNELARC_ERR_INVALID_ARG, "buf holds %zu bytes; the name needs %zu", len, need);
+    std::memcpy(buf, PLANS[plan].name, need);
+    return KERNELARC_OK;
 }
 
 int kernelarc_plan_supports(int plan, int64_t M, int64_t N, int64_t K, int residual) {
@@ -1175,7 +1177,6 @@ int kernelarc_select_plan(int64_t M, int64_t N, int64_t K, int residual) {
 
 int kernelarc_plan_uses_workspace(int plan, int64_t M, int64_t N, int64_t K) {
     if (!supports(plan, M, N, K, true, dense_layout(N, K))) return 0;
-    if (PLANS[plan].kind == KIND_SKINNY) return skinny_split_of(plan, M, N, K) > 1 ? 1 : 0;
     if (PLANS[plan].kind == KIND_TILE) return tile_split_of(plan, M, N, K) > 1 ? 1 : 0;
     if (PLANS[plan].kind == KIND_STREAM) return stream_split_of(plan, M, N, K) > 1 ? 1 : 0;
     return 0;

@@ -14,44 +14,23 @@ namespace kernelarc {
 // kernels.
 enum PlanId : int {
     PLAN_GENERIC = 0,          // scalar LDS-tiled kernel: any K, any alignment
-    PLAN_SKINNY = 1,           // M <= 64: stream W once, MFMA 16x16x32, in-WG split-K
-    PLAN_SKINNY_SPLITK = 2,    // as PLAN_SKINNY plus a cross-workgroup split-K
-    PLAN_GEMV = 3,             // M <= 4: contiguous W stream, VALU dot products
-    PLAN_FIRST_TILE = 4,       // MFMA macro-tile plans follow (api.hip)
+    PLAN_GEMV = 1,             // M <= 4: contiguous W stream, VALU dot products
 };
 
-// MFMA macro-tile kernel configurations (kernel_tile.hip):
+// MFMA macro-tile kernel configurations (tile_kernel.h):
 // BM x BN output tile, BK deep stages, STAGES-deep LDS ring, waves.
 enum TileCfg : int {
     TC_256x256_K64_S2_W8 = 0,
-    TC_256x256_K64_S2_W4 = 1,
-    TC_256x128_K64_S2_W8 = 2,
-    TC_128x256_K64_S2_W8 = 3,
-    TC_256x128_K64_S2_W4 = 4,
-    TC_128x128_K64_S2_W4 = 5,
-    TC_64x256_K64_S2_W4 = 6,
-    TC_128x128_K64_S4_W4 = 7,
-    TC_128x128_K64_S3_W4 = 8,
-    TC_64x256_K64_S3_W4 = 9,
-    TC_256x128_K64_S3_W8 = 10,
-    TC_64x64_K64_S2_W4 = 11,
-    TC_64x128_K64_S2_W4 = 12,
-    TC_64x64_K128_S2_W4 = 13,
-    TC_128x128_K128_S2_W4 = 14,
-    TC_64x128_K128_S2_W4 = 15,
-    TC_64x64_K128_S3_W4 = 16,
-    TC_64x64_K64_S4_W4 = 17,
-    TC_128x128_K32_S4_W4 = 18,
-    TC_64x64_K64_S8_W4 = 19,
-    TC_64x128_K64_S4_W4 = 20,
-    TC_64x64_K128_S2_G2 = 21,     // two K groups of 4 waves (8 waves)
-    TC_128x128_K64_S2_G2 = 22,
-    TC_64x64_K64_S2_G4 = 23,      // four K groups (16 waves)
-    TC_256x128_K64_S3_W8_L = 24,   // lagged refill
-    TC_128x128_K64_S4_W4_L = 25,
-    TC_32x256_K64_S4_W4 = 26,      // one 32-row wave band (skinny M)
-    TC_256x256_K64_S2_W8_M16 = 27, // 16x16x32 MFMA (bf16 plain and general forms)
-    TC_COUNT = 28,
+    TC_256x256_K64_S2_W8_M16 = 1,  // 16x16x32 MFMA (bf16 plain and general forms)
+    TC_256x128_K64_S3_W8 = 2,
+    TC_256x128_K64_S3_W8_L = 3,    // lagged refill
+    TC_128x128_K64_S2_W4 = 4,
+    TC_128x128_K64_S3_W4 = 5,
+    TC_128x128_K64_S4_W4_L = 6,
+    TC_64x64_K128_S3_W4 = 7,
+    TC_64x64_K64_S4_W4 = 8,
+    TC_64x128_K64_S4_W4 = 9,
+    TC_COUNT = 10,
 };
 
 struct TileShape {
@@ -231,9 +210,8 @@ struct Workspace {
 // hipError_t of the launch.
 hipError_t launch_generic(const Problem &p, hipStream_t s);
 hipError_t launch_gemv(const Problem &p, hipStream_t s);
-hipError_t launch_skinny(const Problem &p, int split_k, const Workspace *ws, hipStream_t s);
 // full_tiles > 0 with split > 1: tiles past the first full_tiles (band
-// order) are split in K, the others run whole (see kernel_tile.hip).
+// order) are split in K, the others run whole (see tile_kernel.h).
 hipError_t launch_tile(int cfg, const Problem &p, int split, int64_t full_tiles, const Workspace *ws, hipStream_t s);
 hipError_t launch_stream(const Problem &p, int bk, int stages, int rows, int split, const Workspace *ws,
                          hipStream_t s);
@@ -288,9 +266,6 @@ hipError_t launch_tile_i8_glu(int cfg, const I8GluProblem &p, int split, int64_t
                               hipStream_t s);
 
 // Shape rules of the kernels, used by the plan table (host only).
-int skinny_split_for(int64_t M, int64_t N, int64_t K);
-int64_t skinny_workspace_floats(int64_t M, int64_t N, int split_k);
-int64_t skinny_counter_count(int64_t N);
 bool gemv_fits(int64_t M, int64_t N, int64_t K, int64_t ldw);
 int stream_split_for(int64_t M, int64_t N, int64_t K, int bk, int rows);
 int64_t stream_workspace_floats(int64_t M, int64_t N, int split, int rows);

@@ -466,10 +466,7 @@ hipError_t launch_bk(const P &p, int split, const Workspace *ws, hipStream_t s) 
 // The configurations with 16- and 32-row blocks, for either operand type.
 template <class P>
 hipError_t launch_rows(const P &p, int bk, int stages, int rows, int split, const Workspace *ws, hipStream_t s) {
-    if (rows == 16 && bk == 64 && stages == 4) return launch_bk<64, 4, 1>(p, split, ws, s);
-    if (rows == 16 && bk == 64 && stages == 8) return launch_bk<64, 8, 1>(p, split, ws, s);
     if (rows == 16 && bk == 128 && stages == 2) return launch_bk<128, 2, 1>(p, split, ws, s);
-    if (rows == 16 && bk == 128 && stages == 4) return launch_bk<128, 4, 1>(p, split, ws, s);
     if (rows == 32 && bk == 64 && stages == 4) return launch_bk<64, 4, 2>(p, split, ws, s);
     return hipErrorInvalidValue;
 }
@@ -496,8 +493,7 @@ int64_t stream_workspace_floats(int64_t M, int64_t N, int split, int rows) {
 int64_t stream_counter_count(int64_t N, int rows) { return (N + rows - 1) / rows; }
 
 bool stream_config_exists(int bk, int stages, int rows) {
-    return (rows == 64 && stages == 2 && (bk == 64 || bk == 128)) ||
-           (rows == 16 && ((bk == 64 && (stages == 4 || stages == 8)) || (bk == 128 && (stages == 2 || stages == 4)))) ||
+    return (rows == 64 && stages == 2 && bk == 64) || (rows == 16 && bk == 128 && stages == 2) ||
            (rows == 32 && bk == 64 && stages == 4);
 }
 
@@ -505,12 +501,10 @@ hipError_t launch_stream(const Problem &p, int bk, int stages, int rows, int spl
                          hipStream_t s) {
     if (p.M < 1 || p.M > 64) return hipErrorInvalidValue;
     if (is_general(p)) {
-        if (rows == 64 && bk == 128 && stages == 2) return launch_bk<128, 2, 4>(p, split, ws, s);
         if (rows == 64 && bk == 64 && stages == 2) return launch_bk<64, 2, 4>(p, split, ws, s);
         return launch_rows(p, bk, stages, rows, split, ws, s);
     }
     const DenseProblem d = dense_of(p);
-    if (rows == 64 && bk == 128 && stages == 2) return launch_bk<128, 2, 4>(d, split, ws, s);
     if (rows == 64 && bk == 64 && stages == 2) return launch_bk<64, 2, 4>(d, split, ws, s);
     return launch_rows(d, bk, stages, rows, split, ws, s);
 }

@@ -1,0 +1,24 @@
+// Tile-kernel launchers of the FP8 (E4M3) forms.
+#include "tile_kernel.h"
+
+namespace kernelarc {
+
+hipError_t launch_tile_f8(int cfg, const F8Problem &p, int split, int64_t full_tiles, const Workspace *ws,
+                          hipStream_t s) {
+    return with_cfg(cfg, [&](auto c, int) {
+        using C = decltype(c);
+        if constexpr (std::is_same<C, std::nullptr_t>::value) return hipErrorInvalidValue;
+        else return launch_cfg_q8<C>(p, 8, split, full_tiles, ws, s);
+    });
+}
+
+hipError_t launch_tile_f8_glu(int cfg, const F8GluProblem &p, int split, int64_t full_tiles, const Workspace *ws,
+                              hipStream_t s) {
+    return with_cfg(cfg, [&](auto c, int) {
+        using C = decltype(c);
+        if constexpr (std::is_same<C, std::nullptr_t>::value) return hipErrorInvalidValue;
+        else return launch_cfg_q8<C>(p, 8, split, full_tiles, ws, s);
+    });
+}
+
+}  // namespace kernelarc

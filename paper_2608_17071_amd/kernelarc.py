@@ -36,7 +36,8 @@ _SIGS = {
     "kernelarc_gemm_bf16": (ctypes.c_int, [_I64, _I64, _I64, _P, _P, _P, _P]),
     "kernelarc_gemm_bf16_with_plan": (ctypes.c_int, [ctypes.c_int, _I64, _I64, _I64, _P, _P, _P, _P, _P]),
     "kernelarc_plan_count": (ctypes.c_int, []),
-    "kernelarc_plan_name": (ctypes.c_char_p, [ctypes.c_int]),
+    "kernelarc_plan_name": (ctypes.c_int, [_I64, _I64, _I64, ctypes.c_int, ctypes.c_char_p, ctypes.c_size_t]),
+    "kernelarc_plan_label": (ctypes.c_char_p, [ctypes.c_int]),
     "kernelarc_plan_supports": (ctypes.c_int, [ctypes.c_int, _I64, _I64, _I64, ctypes.c_int]),
     "kernelarc_select_plan": (ctypes.c_int, [_I64, _I64, _I64, ctypes.c_int]),
     "kernelarc_plan_uses_workspace": (ctypes.c_int, [ctypes.c_int, _I64, _I64, _I64]),
@@ -103,8 +104,16 @@ def plan_count() -> int:
 
 
 def plan_name(plan: int) -> str | None:
-    n = _lib.kernelarc_plan_name(plan)
+    """Name of plan id `plan` (None for an unknown id)."""
+    n = _lib.kernelarc_plan_label(plan)
     return n.decode() if n is not None else None
+
+
+def plan_name_for(M: int, N: int, K: int, residual: bool = True) -> str:
+    """Name of the plan the library runs for this shape (kernelarc_plan_name)."""
+    buf = ctypes.create_string_buffer(64)
+    _check(_lib.kernelarc_plan_name(M, N, K, int(residual), buf, len(buf)), "kernelarc_plan_name")
+    return buf.value.decode()
 
 
 def plan_names() -> list[str]:

@@ -48,7 +48,7 @@ def test_plan_table(ka):
     assert len(set(names)) == len(names)
     assert ka.plan_name(-1) is None and ka.plan_name(ka.plan_count()) is None
     gen = names.index("generic_64x64_scalar")
-    # K not a multiple of 8 -> generic; skinny M -> a skinny plan; big -> a tile plan
+    # K not a multiple of 8 -> generic; few rows -> GEMV or streaming; more -> a tile plan
     assert ka.select_plan(128, 256, 250) == gen
     for M in (1, 4):
         assert names[ka.select_plan(M, 4096, 4096)].startswith("gemv")
@@ -68,22 +68,36 @@ def test_plan_table(ka):
 def test_plan_limits(ka):
     names = ka.plan_names()
     tile = names.index("tile_256x256_k64_w8")
-    skinny = names.index("skinny_mfma16_w8")
     assert not ka.plan_supports(tile, 512, 512, 12)            # K % 8
-    assert not ka.plan_supports(skinny, 65, 512, 512)          # M > 64
-    assert not ka.plan_supports(skinny, 0, 512, 512)
     assert ka.kernelarc_plan_supports(99, 1, 1, 1, 1) == -1
     assert ka.kernelarc_plan_supports(tile, -1, 1, 1, 1) == -1
-    split = names.index("skinny_mfma16_w8_splitk")
-    assert ka.kernelarc_plan_uses_workspace(split, 16, 1024, 4096) == 1
-    assert ka.kernelarc_plan_uses_workspace(skinny, 16, 1024, 4096) == 0
-    stream = names.index("stream_mfma16_k128")
+    assert ka.kernelarc_plan_uses_workspace(tile, 4096, 4096, 4096) == 0
+    assert ka.kernelarc_plan_uses_workspace(names.index("tile_128x128_k64_w4_splitk"), 512, 1024, 2048) == 1
     stream_split = names.index("stream_mfma16_k64_splitk")
-    assert ka.plan_supports(stream, 64, 8192, 8192) and ka.plan_supports(stream, 1, 8, 8)
-    assert not ka.plan_supports(stream, 65, 512, 512)          # M > 64
-    assert not ka.plan_supports(stream_split, 16, 512, 516)     # K % 8
+    assert ka.plan_supports(stream_split, 64, 8192, 8192) and ka.plan_supports(stream_split, 1, 8, 8)
+    assert not ka.plan_supports(stream_split, 65, 512, 512)    # M > 64
+    assert not ka.plan_supports(stream_split, 0, 512, 512)
+    assert not ka.plan_supports(stream_split, 16, 512, 516)    # K % 8
     assert ka.kernelarc_plan_uses_workspace(stream_split, 16, 4096, 4096) == 1
-    assert ka.kernelarc_plan_uses_workspace(stream, 16, 4096, 4096) == 0
+
+
+def test_plan_name_for_a_shape(ka):
+    """kernelarc_plan_name(M, N, K, residual, buf, len): the chosen plan's
+    name, the same as the id query, with its buffer and size checks."""
+    for (M, N, K, r) in [(16, 4096, 4096, 1), (4096, 4096, 4096, 1), (8192, 8192, 8192, 0), (1, 2048, 2048, 1),
+                         (128, 256, 250, 1), (0, 5, 8, 0)]:
+        assert ka.plan_name_for(M, N, K, bool(r)) == ka.plan_name(ka.select_plan(M, N, K, bool(r)))
+    buf = ctypes.create_string_buffer(64)
+    f = ka.kernelarc_plan_name
+    assert f(16, 4096, 4096, 1, buf, 64) == ka.OK and buf.value == b"stream_mfma16_r16_k128s2"
+    need = len(buf.value) + 1
+    small = ctypes.create_string_buffer(b"x" * 8, need - 1)
+    assert f(16, 4096, 4096, 1, small, need - 1) == ka.ERR_INVALID_ARG    # too small: nothing written
+    assert small.raw[:8] == b"x" * 8
+    assert ka.kernelarc_last_error().startswith(b"buf holds")
+    assert f(16, 4096, 4096, 1, buf, need) == ka.OK
+    assert f(-1, 4, 4, 1, buf, 64) == ka.ERR_INVALID_ARG
+    assert f(4, 4, 4, 1, None, 64) == ka.ERR_INVALID_ARG
 
 
 def test_row_block_stream_plans(ka):
@@ -230,10 +244,10 @@ def test_swiglu_plans(ka):
         assert ka.plan_supports_swiglu(p, M, N, K), (M, N, K, names[p])
         assert names[p].startswith("tile") or p == gen
     # plans whose waves cannot hold gate/up block pairs, or that are not tiles
-    for n in ("tile_64x64_k64_w4", "tile_64x64_k128s3_w4_splitk", "stream_mfma16_k64_splitk", "gemv_valu_w4",
-              "skinny_mfma16_w8"):
+    for n in ("tile_64x64_k64s4_w4", "tile_64x64_k128s3_w4_splitk", "stream_mfma16_k64_splitk", "gemv_valu_w4",
+              "stream_mfma16_r16_k128s2"):
         assert not ka.plan_supports_swiglu(names.index(n), 64, 1024, 1024), n
-    for n in ("tile_256x256_k64_w8", "tile_128x128_k64_w4", "tile_32x256_k64s4_w4_splitk", "generic_64x64_scalar"):
+    for n in ("tile_256x256_k64_w8", "tile_128x128_k64_w4", "tile_64x128_k64s4_w4_splitk", "generic_64x64_scalar"):
         assert ka.plan_supports_swiglu(names.index(n), 64, 1024, 1024), n
     assert not ka.plan_supports_swiglu(names.index("tile_256x256_k64_w8"), 64, 1024, 1020)   # K % 8
     assert ka.kernelarc_plan_supports_swiglu(999, 1, 1, 1) == -1
@@ -269,14 +283,14 @@ def test_i8_validation_and_plans(ka):
     for (M, N, K, plan) in [(16, 4096, 4096, "stream_mfma16_r16_k128s2"), (1, 64, 16, "stream_mfma16_r16_k128s2"),
                             (64, 2048, 2048, "stream_mfma16_r16_k128s2"), (16, 8192, 8192, "stream_mfma16_r32_k64s4")]:
         assert names[ka.select_plan_i8(M, N, K, False)] == plan, (M, N, K)
-    for n in ("stream_mfma16_k64_splitk", "gemv_valu_w4", "skinny_mfma16_w8"):
+    for n in ("stream_mfma16_k64_splitk", "gemv_valu_w4"):
         assert not ka.plan_supports_i8(names.index(n), 16, 1024, 1024)
     r16 = names.index("stream_mfma16_r16_k128s2")
     assert ka.plan_supports_i8(r16, 16, 1024, 1024) and not ka.plan_supports_i8(r16, 16, 1024, 1024, True)
     assert not ka.plan_supports_i8(r16, 65, 1024, 1024) and not ka.plan_supports_i8(r16, 16, 1024, 1032)
     assert not ka.plan_supports_f8(r16, 16, 1024, 1024)
-    assert not ka.plan_supports_i8(names.index("tile_64x64_k64_w4"), 64, 1024, 1024, True)
-    assert ka.plan_supports_i8(names.index("tile_64x64_k64_w4"), 64, 1024, 1024, False)
+    assert not ka.plan_supports_i8(names.index("tile_64x64_k64s4_w4"), 64, 1024, 1024, True)
+    assert ka.plan_supports_i8(names.index("tile_64x64_k64s4_w4"), 64, 1024, 1024, False)
     assert not ka.plan_supports_i8(names.index("tile_256x256_k64_w8"), 64, 1024, 1032)  # K % 16
 
 
@@ -301,7 +315,7 @@ def test_grouped_validation_and_plans(ka):
         assert ka.plan_supports_grouped(p, G, Mpad, N, K, glu) and names[p].startswith("tile"), names[p]
     for n in ("tile_128x128_k64_w4_splitk", "tile_256x256_k64_w8_tailsplit", "stream_mfma16_k64_splitk"):
         assert not ka.plan_supports_grouped(names.index(n), 4, 64, 256, 256)
-    assert not ka.plan_supports_grouped(names.index("tile_64x64_k64_w4"), 4, 64, 256, 256, True)
+    assert not ka.plan_supports_grouped(names.index("tile_64x64_k64s4_w4"), 4, 64, 256, 256, True)
 
 
 def test_f8_plans(ka):
@@ -310,6 +324,6 @@ def test_f8_plans(ka):
                            (4096, 14336, 4096, 1), (300, 77, 1024, 1)]:
         p = ka.select_plan_f8(M, N, K, glu)
         assert ka.plan_supports_f8(p, M, N, K, glu) and names[p].startswith("tile"), (M, N, K, glu, names[p])
-    assert not ka.plan_supports_f8(names.index("tile_128x128_k32s4_w4"), 64, 1024, 1024)   # 32-byte stages
+    assert not ka.plan_supports_f8(names.index("tile_256x256_k64_w8_m16"), 64, 1024, 1024)  # 16x16 MFMA tile
     assert ka.plan_supports_f8(names.index("tile_256x256_k64_w8"), 64, 1024, 1 << 17)      # no int32 limit
     assert ka.select_plan_f8(64, 128, 40) == names.index("generic_64x64_scalar")

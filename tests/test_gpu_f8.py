@@ -89,9 +89,9 @@ def test_f8_swiglu_every_plan(ka, name):
     _check(ka, M, N, K, 82, True, plan=ka.plan_names().index(name), what="every-plan")
 
 
-@pytest.mark.parametrize("name", ["tile_256x256_k64_w8", "tile_64x64_k128s3_w4_splitk", "tile_128x128_k64_g2",
-                                  "tile_64x64_k64_g4_splitk", "tile_256x128_k64s3_w8_lag_splitk",
-                                  "tile_32x256_k64s4_w4_splitk", "generic_64x64_scalar"])
+@pytest.mark.parametrize("name", ["tile_256x256_k64_w8", "tile_64x64_k128s3_w4_splitk", "tile_128x128_k64s4_w4_lag",
+                                  "tile_64x64_k64s4_w4", "tile_256x128_k64s3_w8_lag_splitk",
+                                  "tile_64x128_k64s4_w4_splitk", "generic_64x64_scalar"])
 def test_f8_small_integer_sums_bit_exact(ka, name):
     plan = ka.plan_names().index(name)
     M, N, K = 150, 200, 256
@@ -142,7 +142,7 @@ def test_f8_rejects(ka):
     qw = torch.zeros(96, 128, dtype=torch.float8_e4m3fn, device="cuda")
     sx = torch.ones(64, dtype=torch.float32, device="cuda")
     sw = torch.ones(96, dtype=torch.float32, device="cuda")
-    for n in ("stream_mfma16_k64_splitk", "gemv_valu_w4", "tile_128x128_k32s4_w4"):
+    for n in ("stream_mfma16_k64_splitk", "gemv_valu_w4", "tile_256x256_k64_w8_m16"):
         with pytest.raises(ka.KernelArcError) as e:
             ka.gemm_f8(qx, sx, qw, sw, plan=names.index(n))
         assert e.value.status == ka.ERR_UNSUPPORTED

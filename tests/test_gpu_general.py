@@ -122,7 +122,7 @@ def test_general_large_k_ne_n(ka):
     _general_case(ka, M, N, K, 9, 1.0, 1.0, True, True, pads=(0, 0, 0, 0), positions=pos)
 
 
-@pytest.mark.parametrize("name", ["tile_256x256_k64_w8", "tile_64x64_k64s4_w4_splitk",
+@pytest.mark.parametrize("name", ["tile_256x256_k64_w8", "tile_64x64_k128s3_w4_splitk",
                                   "tile_256x128_k64s3_w8_lag", "gemv_valu_w4", "generic_64x64_scalar"])
 def test_general_default_is_plain_bitwise(ka, name):
     plan = ka.plan_names().index(name)
@@ -177,10 +177,10 @@ def test_general_rejects(ka):
     x = _bf16(g, (64, 128), 1.0).cuda()
     w = _bf16(g, (96, 128), 1.0).cuda()
     c = _bf16(g, (64, 96), 1.0).cuda()
-    skinny = ka.plan_names().index("skinny_mfma16_w8")
+    gemv = ka.plan_names().index("gemv_valu_w4")
     gu.note("general rejects")
     with pytest.raises(ka.KernelArcError) as e:
-        ka.gemm_bf16_ex(x[:16], w, c[:16], None, 2.0, 1.0, plan=skinny)   # the skinny kernel is dense-only
+        ka.gemm_bf16_ex(x[:16], w, c[:16], None, 2.0, 1.0, plan=gemv)     # the GEMV takes at most 4 rows
     assert e.value.status == ka.ERR_UNSUPPORTED
     big = torch.zeros(64, 200, dtype=torch.bfloat16, device="cuda")
     with pytest.raises(ka.KernelArcError) as e:                            # Y partially overlaps C

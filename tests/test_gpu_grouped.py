@@ -128,7 +128,7 @@ def test_grouped_rejects(ka):
             ka.gemm_bf16_grouped(x, w, plan=names.index(n))
         assert e.value.status == ka.ERR_UNSUPPORTED
     with pytest.raises(ka.KernelArcError) as e:
-        ka.swiglu_bf16_grouped(x, w, w, plan=names.index("tile_64x64_k64_w4"))
+        ka.swiglu_bf16_grouped(x, w, w, plan=names.index("tile_64x64_k64s4_w4"))
     assert e.value.status == ka.ERR_UNSUPPORTED
     with pytest.raises(ValueError):
         ka.gemm_bf16_grouped(x, w, torch.zeros(3, dtype=torch.int32, device="cuda"))

@@ -64,17 +64,12 @@ TILE_SHAPES = [(65, 8, 8), (300, 264, 200), (130, 100, 72), (513, 520, 136)]
 PLAN_SHAPES = {
     # plan name: ragged shapes (M, N, K) it supports, K % 8 == 0 for MFMA plans
     "generic_64x64_scalar": [(1, 1, 1), (70, 33, 13), (130, 100, 72)],
-    "skinny_mfma16_w8": [(1, 8, 8), (17, 520, 1000), (64, 96, 4104), (33, 100, 264)],
-    "skinny_mfma16_w8_splitk": [(1, 24, 8), (5, 520, 1000), (64, 96, 4104), (48, 100, 2064)],
     "gemv_valu_w4": [(1, 8, 8), (1, 520, 1000), (3, 100, 4104), (4, 2048, 2048), (2, 77, 136), (1, 9000, 520)],
-    "stream_mfma16_k128": [(1, 8, 8), (17, 520, 1000), (64, 96, 4104), (33, 100, 264), (49, 130, 136)],
-    "stream_mfma16_k128_splitk": [(1, 24, 8), (5, 520, 1000), (64, 96, 4104), (48, 100, 2064), (16, 70, 1032)],
     "stream_mfma16_k64_splitk": [(2, 24, 8), (31, 520, 1000), (64, 96, 4104), (60, 200, 2056)],
     # 16- and 32-row blocks with X staged through LDS: the rule's split
     # ranges from none (K too shallow) to 16 slices; ragged M, N and K.
     **{n: [(1, 8, 8), (16, 520, 1000), (17, 100, 4104), (64, 96, 2056), (33, 130, 136), (5, 24, 264)]
-       for n in ("stream_mfma16_r16_k64s4", "stream_mfma16_r16_k64s8", "stream_mfma16_r16_k128s2",
-                 "stream_mfma16_r16_k128s4", "stream_mfma16_r32_k64s4")},
+       for n in ("stream_mfma16_r16_k128s2", "stream_mfma16_r32_k64s4")},
 }
 PLAN_SHAPES.update({n: TILE_SHAPES for n in _all_plan_names() if n.startswith("tile_")})
 assert set(PLAN_SHAPES) == set(_all_plan_names()), "every plan has test shapes"
@@ -102,7 +97,7 @@ def _unsigned_zero(bits):
 def _closed_form_shapes(plan):
     if plan.startswith("gemv"):
         return (4, 200, 200), (3, 136, 1000)
-    if plan.startswith("skinny") or plan.startswith("stream"):
+    if plan.startswith("stream"):
         return (23, 200, 200), (40, 136, 1000)
     return (300, 264, 264), (130, 100, 520)
 
@@ -147,12 +142,12 @@ def test_closed_forms_bitwise_every_plan(ka, plan):
 
 # Shapes where the tail-split plans split only the tiles of a partial last
 # round: (plan, M, N, K).  Each is checked to really take that path.
-TAIL_SPLIT_CASES = [("tile_128x128_k64_w4_tailsplit", 2048, 4224, 1024),    # 528 tiles, 512 slots
-                    ("tile_256x256_k64_w8_tailsplit", 2048, 8448, 1024),    # 264 tiles, 256 slots
-                    ("tile_256x128_k64_w8_tailsplit", 2048, 8448, 1040)]    # 528 tiles, K tail
+TAIL_SPLIT_CASES = [("tile_256x256_k64_w8_tailsplit", 2048, 8448, 1024),    # 264 tiles, 256 slots
+                    ("tile_256x256_k64_w8_tailsplit", 4096, 5120, 5120),    # 320 tiles: the benchmark shape
+                    ("tile_256x256_k64_w8_tailsplit", 2048, 8448, 1040)]    # 264 tiles, K tail
 
 
-@pytest.mark.parametrize("case", TAIL_SPLIT_CASES, ids=[c[0] for c in TAIL_SPLIT_CASES])
+@pytest.mark.parametrize("case", TAIL_SPLIT_CASES, ids=[f"{c[0]}_{c[1]}x{c[2]}x{c[3]}" for c in TAIL_SPLIT_CASES])
 def test_tail_split_whole_output(ka, case):
     plan, M, N, K = case
     p = plan_id(ka, plan)
@@ -263,12 +258,12 @@ def test_leading_dims_flatten(ka):
 def test_graph_replay_matches_eager(ka):
     """Calls captured in a HIP graph give the eager result on every replay
     (the split-K plans' arrival counters must reset themselves)."""
-    cases = [("skinny_mfma16_w8_splitk", (16, 1024, 4096)), ("skinny_mfma16_w8", (3, 520, 1000)),
+    cases = [("stream_mfma16_r16_k128s2", (16, 1024, 4096)), ("stream_mfma16_r32_k64s4", (16, 4096, 4096)),
              ("gemv_valu_w4", (1, 4096, 4096)),
              ("tile_128x128_k64_w4_splitk", (512, 1024, 2048)), ("tile_256x256_k64_w8", (300, 520, 264)),
-             ("tile_64x256_k64_w4_splitk", (64, 768, 4096)), ("stream_mfma16_k128_splitk", (64, 1024, 4096)),
-             ("stream_mfma16_k64_splitk", (16, 2048, 2048)),
-             ("tile_128x128_k64_w4_tailsplit", (2048, 4224, 1024))]
+             ("tile_64x64_k128s3_w4_splitk", (64, 768, 4096)), ("stream_mfma16_k64_splitk", (64, 1024, 4096)),
+             ("tile_256x128_k64s3_w8_lag_splitk", (512, 1024, 4096)),
+             ("tile_256x256_k64_w8_tailsplit", (2048, 8448, 1024))]
     for name, (M, N, K) in cases:
         p = plan_id(ka, name)
         t = wl.make_inputs(wl.custom(M, N, K, seed=21))

@@ -137,7 +137,7 @@ def test_swiglu_rejects(ka):
     w = torch.zeros(96, 128, dtype=torch.bfloat16, device="cuda")
     gu.note("swiglu rejects")
     names = ka.plan_names()
-    for n in ("stream_mfma16_k64_splitk", "tile_64x64_k64_w4", "gemv_valu_w4"):
+    for n in ("stream_mfma16_k64_splitk", "tile_64x64_k64s4_w4", "gemv_valu_w4"):
         with pytest.raises(ka.KernelArcError) as e:
             ka.swiglu_bf16(x, w, w, plan=names.index(n))
         assert e.value.status == ka.ERR_UNSUPPORTED
