@@ -557,6 +557,68 @@ def cpu_baseline(cases, seconds):
     }
 
 
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def gpu_clocks() -> dict:
+    """Current shader (sclk) and memory (mclk) clocks of GPU 0 in MHz, read by
+    the SMI tool in a child process (a snapshot between timed regions, not an
+    average over them); {} when no tool answers."""
+    import re
+    import subprocess
+    for cmd in (["amd-smi", "metric", "-g", "0", "--clock"], ["rocm-smi", "-d", "0", "--showclocks"]):
+        try:
+            r = subprocess.run(cmd, capture_output=True, text=True, timeout=30)
+        except (OSError, subprocess.SubprocessError):
+            continue
+        text = r.stdout
+        out = {}
+        for key, pats in (("sclk_mhz", (r"sclk[^\n(]*\((\d+)\s*Mhz", r"GFX_0:\s*\n\s*CLK:\s*(\d+)\s*MHz")),
+                          ("mclk_mhz", (r"mclk[^\n(]*\((\d+)\s*Mhz", r"MEM_0:\s*\n\s*CLK:\s*(\d+)\s*MHz"))):
+            for pat in pats:
+                m = re.search(pat, text, flags=re.I)
+                if m:
+                    out[key] = int(m.group(1))
+                    break
+        if out:
+            out["tool"] = cmd[0]
+            return out
+    return {}
+
+
+def oracle_config_seconds():
+    """Whole-output oracle seconds for the tiny, decode and prefill configs
+    with every host thread, and on one thread for tiny and decode (the CPU
+    baseline plan: the oracle's own speed, not a target)."""
+    import oracle
+    from paper_2608_17071_amd import workloads as wl
+
+    orc = oracle.default()
+    threads = orc.threads()
+    res = {"threads": threads, "whole_config_seconds": {}, "single_thread_seconds": {}}
+    for w in (wl.TINY, wl.DECODE, wl.PREFILL):
+        t = wl.make_inputs(w)
+        xb, wb, rb = wl.bits(t["X"]), wl.bits(t["W"]), wl.bits(t["R"])
+        t0 = time.perf_counter()
+        orc.linear(xb, wb, rb)
+        res["whole_config_seconds"][w.name] = round(time.perf_counter() - t0, 4)
+        if w is not wl.PREFILL:
+            orc.set_threads(1)
+            t0 = time.perf_counter()
+            orc.linear(xb, wb, rb)
+            res["single_thread_seconds"][w.name] = round(time.perf_counter() - t0, 4)
+            orc.set_threads(threads)
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -640,8 +702,10 @@ def main():
     log("generating inputs ...")
     sweep = [Case(w, ka, torch, rotate=not args.hot) for w in wl.SWEEP]
     torch.cuda.synchronize()
+    clocks = {"before_sweep": gpu_clocks()}
     log(f"timing {len(sweep)} shapes x {args.steps} steps (warmup {args.warmup}) ...")
     wall = time_cases(sweep, args.steps, args.warmup, ka, torch, use_graph=not args.no_graph)
+    clocks["after_sweep"] = gpu_clocks()
     rows = [shape_row(c) for c in sweep]
     for r in rows:
         log(f"  {r['shape']:24s} {r['plan']:28s} {r['us']:9.2f} us {r['tflops']:8.1f} TF "
@@ -682,7 +746,9 @@ def main():
         for c in sweep:
             c.free()
         extra = [Case(w, ka, torch, rotate=not args.hot) for w in (wl.DECODE, wl.PREFILL, wl.SQUARE)]
+        clocks["before_gates"] = gpu_clocks()
         time_cases(extra, args.steps, args.warmup, ka, torch, use_graph=not args.no_graph)
+        clocks["after_gates"] = gpu_clocks()
         for c in extra:
             r = shape_row(c)
             gates[c.w.name] = r
@@ -799,6 +865,9 @@ def main():
     if not args.no_cpu_baseline:
         log(f"timing the CPU oracle (~{args.cpu_seconds:.0f} s) ...")
         cpu = cpu_baseline(sweep, args.cpu_seconds)
+        cpu["cpu_model"] = cpu_model()
+        log("timing the CPU oracle on whole configs (tiny, decode, prefill; ~5 s) ...")
+        cpu.update(oracle_config_seconds())
 
     out = {
         "metric": "BF16 TFLOP/s and % of MFMA peak (or % HBM BW) per shape; geomean over sweep",
@@ -816,6 +885,7 @@ def main():
             "accumulate": "fp32",
         },
         "sweep_geomean_roofline_frac": round(frac_geo, 4),
+        "gpu_clocks_mhz": clocks,
         "roofline": roof,
         "cpu_baseline": cpu,
         "shapes": rows,

@@ -54,6 +54,8 @@ class Oracle:
         lib = ctypes.CDLL(path)
         lib.ka_oracle_linear.argtypes = [_I64, _I64, _I64, _P, _P, _P, _P]
         lib.ka_oracle_linear.restype = ctypes.c_int
+        lib.ka_oracle_linear_pair.argtypes = [_I64, _I64, _I64, _P, _P, _P, _P, _P]
+        lib.ka_oracle_linear_pair.restype = ctypes.c_int
         lib.ka_oracle_linear_at.argtypes = [_I64, _I64, _I64, _P, _P, _P, _I64, _P, _P, _P]
         lib.ka_oracle_linear_at.restype = ctypes.c_int
         lib.ka_oracle_linear_ex.argtypes = [_I64, _I64, _I64, ctypes.c_float, _P, _I64, _P, _I64,
@@ -97,6 +99,8 @@ class Oracle:
         lib.ka_oracle_round_bf16.restype = None
         lib.ka_oracle_threads.argtypes = []
         lib.ka_oracle_threads.restype = ctypes.c_int
+        lib.ka_oracle_set_threads.argtypes = [ctypes.c_int]
+        lib.ka_oracle_set_threads.restype = None
         self.lib = lib
         self.path = path
 
@@ -125,6 +129,22 @@ class Oracle:
         if rc != 0:
             raise ValueError("oracle rejected its arguments")
         return Y
+
+    def linear_pair(self, X, W, R):
+        """(X W^T, X W^T + R) in float64 from one evaluation of each k-sum:
+        the values of linear(X, W) and linear(X, W, R)."""
+        M, K = X.shape
+        N = W.shape[0]
+        X = self._bits(X, (M, K))
+        W = self._bits(W, (N, K))
+        R = self._bits(R, (M, N))
+        Yp = np.empty((M, N), dtype=np.float64)
+        Yr = np.empty((M, N), dtype=np.float64)
+        rc = self.lib.ka_oracle_linear_pair(M, N, K, X.ctypes.data, W.ctypes.data, R.ctypes.data,
+                                            Yp.ctypes.data, Yr.ctypes.data)
+        if rc != 0:
+            raise ValueError("oracle rejected its arguments")
+        return Yp, Yr
 
     def linear_at(self, X, W, R, rows, cols) -> np.ndarray:
         """The same definition evaluated at the positions (rows[t], cols[t])."""
@@ -467,6 +487,10 @@ class Oracle:
     def threads(self) -> int:
         """OpenMP threads the oracle's loops use."""
         return int(self.lib.ka_oracle_threads())
+
+    def set_threads(self, n: int) -> None:
+        """Threads the oracle's loops use from now on (n >= 1)."""
+        self.lib.ka_oracle_set_threads(int(n))
 
     def round_bf16(self, values) -> np.ndarray:
         """Round float64 values to bf16 bit patterns (nearest, ties to even)."""

@@ -85,6 +85,32 @@ int ka_oracle_linear(int64_t M, int64_t N, int64_t K,
 }
 
 /*
+ * Both operators over the whole output from one evaluation of each k-sum:
+ * Yp = the product alone (R absent) and Yr = the product plus R, element for
+ * element the values ka_oracle_linear gives without and with R (the same
+ * sum in the same order, then the same single addition of R).  Used where
+ * the whole output of both forms is checked at sizes where two passes would
+ * double the CPU time.  R is required.
+ */
+int ka_oracle_linear_pair(int64_t M, int64_t N, int64_t K,
+                          const uint16_t *X, const uint16_t *W, const uint16_t *R,
+                          double *Yp, double *Yr)
+{
+    if (M < 0 || N < 0 || K < 0) return -1;
+    if (M * N > 0 && (!Yp || !Yr || !R)) return -1;
+    if (M * K > 0 && !X) return -1;
+    if (N * K > 0 && !W) return -1;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t i = 0; i < M; ++i)
+        for (int64_t j = 0; j < N; ++j) {
+            const double acc = element(i, j, N, K, X, W, NULL);
+            Yp[i * N + j] = acc;
+            Yr[i * N + j] = acc + bf16_bits_to_double(R[i * N + j]);
+        }
+    return 0;
+}
+
+/*
  * The same definition evaluated only at the n listed positions
  * (rows[t], cols[t]); used for sampled checks at sizes where the full
  * product is too slow on the CPU.  Indices must lie in [0,M) x [0,N).
@@ -603,5 +629,16 @@ int ka_oracle_threads(void)
     return omp_get_max_threads();
 #else
     return 1;
+#endif
+}
+
+/* Sets the number of threads the OpenMP loops use from now on (n >= 1; no
+ * effect without OpenMP).  Used to time the oracle on one core. */
+void ka_oracle_set_threads(int n)
+{
+#ifdef _OPENMP
+    if (n >= 1) omp_set_num_threads(n);
+#else
+    (void)n;
 #endif
 }
