@@ -87,6 +87,32 @@ int kernelarc_gemm_bf16(int64_t M, int64_t N, int64_t K,
                         const void *X, const void *W, void *Y, hipStream_t stream);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops that must not call hipMalloc, harnesses that forbid
+ * it): kernelarc_gemm_bf16_residual with the same plans, kernels and result
+ * (bit for bit), except that R == NULL computes the plain product Y = X W^T
+ * and that the split-K partials go to a static scratch area compiled into
+ * the library instead of the allocated per-device workspace.  The call
+ * allocates nothing (no hipMalloc, no allocating library routine) and never
+ * synchronises.
+ *
+ * The scratch holds at most 16 Mi fp32 partials (64 MiB) and 64 Ki arrival
+ * counters per device; each device the library runs on keeps its copy until
+ * the process ends.  A plan needing more is rejected with
+ * KERNELARC_ERR_UNSUPPORTED (the plan choice never picks such a split, so
+ * this does not happen for shapes the library accepts).  The first call on a
+ * device clears the counters with a kernel on `stream`; the kernels leave
+ * them at zero.  Every call on one device shares that device's scratch and
+ * its contents persist between calls: calls that may overlap in time on one
+ * device (different streams, concurrently replayed graphs) race on it and
+ * must be serialised by the caller.  Arguments and other errors as
+ * kernelarc_gemm_bf16_residual.
+ */
+int kernelarc_gemm_bf16_residual_noalloc(int64_t M, int64_t N, int64_t K,
+                                         const void *X, const void *W, const void *R,
+                                         void *Y, hipStream_t stream);
+
+/*
  * Plan introspection and forced-plan execution (for tests, the benchmark
  * and offline tuning; Alg. 3's per-M plan cache, static validated table and
  * heuristic fallback correspond to kernelarc_select_plan).

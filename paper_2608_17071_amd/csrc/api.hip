@@ -503,6 +503,8 @@ struct DeviceState {
     char arch[64] = "";
     float *ws_partials = nullptr;
     unsigned *ws_counters = nullptr;
+    float *scratch = nullptr;        // this device's copy of `scratch` (hipGetSymbolAddress)
+    bool scratch_cleared = false;    // its counters were cleared by an uncaptured kernel
 };
 
 std::mutex g_mutex;
@@ -586,6 +588,49 @@ int workspace(int dev, hipStream_t stream, Workspace *out) {
     return KERNELARC_OK;
 }
 
+// Split-K scratch of kernelarc_gemm_bf16_residual_noalloc, for callers that
+// cannot allocate: the same capacity as the workspace above (fp32 partials,
+// then the arrival counters as 32-bit words), reserved in the code object,
+// so each device holds its own copy from the moment the library's code is
+// loaded onto it until the process ends.  Host code must not pass the
+// array's name to a kernel (in host code it is only a stand-in for the
+// symbol); it uses the device address that hipGetSymbolAddress returns.
+constexpr int64_t SCRATCH_FLOATS = WS_PARTIAL_FLOATS + WS_COUNTERS;
+static __device__ __align__(256) float scratch[SCRATCH_FLOATS];
+
+// The scratch of device `dev` (the current device) as a workspace.  The first
+// call on a device looks up its address and clears the counters with a
+// kernel on `stream` (no allocation, no memset node, no wait); the kernels
+// leave every counter at zero, so later calls need no clearing.  If that
+// first clearing is captured into a graph, it runs only when the graph is
+// replayed (before the captured GEMM, which is all that graph needs), so the
+// next uncaptured call clears again.
+int scratch_workspace(int dev, hipStream_t stream, Workspace *out) {
+    std::lock_guard<std::mutex> lock(g_mutex);
+    DeviceState &st = g_devices[dev];
+    if (!st.scratch) {
+        void *ptr = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !ptr)
+            return fail(KERNELARC_ERR_LAUNCH, "hipGetSymbolAddress(scratch) on device %d: %s", dev,
+                        hipGetErrorString(e));
+        st.scratch = static_cast<float *>(ptr);
+    }
+    unsigned *const counters = reinterpret_cast<unsigned *>(st.scratch + WS_PARTIAL_FLOATS);
+    if (!st.scratch_cleared) {
+        hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+        hipError_t e = hipStreamIsCapturing(stream, &cap);
+        if (e == hipSuccess) e = zero_counters(counters, WS_COUNTERS, stream);
+        if (e != hipSuccess) return fail(KERNELARC_ERR_LAUNCH, "clearing the scratch counters: %s", hipGetErrorString(e));
+        if (cap == hipStreamCaptureStatusNone) st.scratch_cleared = true;
+    }
+    out->partials = st.scratch;
+    out->partial_floats = WS_PARTIAL_FLOATS;
+    out->counters = counters;
+    out->counter_count = WS_COUNTERS;
+    return KERNELARC_OK;
+}
+
 bool overlaps(const void *a, int64_t abytes, const void *b, int64_t bbytes) {
     if (!a || !b || abytes == 0 || bbytes == 0) return false;
     const auto pa = reinterpret_cast<uintptr_t>(a);
@@ -611,8 +656,10 @@ struct Request {
     int64_t ldy;
 };
 
-// plan < 0: choose; otherwise run exactly that plan.
-int run(int plan, Request q, hipStream_t stream) {
+// plan < 0: choose; otherwise run exactly that plan.  static_scratch: the
+// split-K partials go to the static scratch instead of the allocated
+// workspace (nothing is allocated).
+int run(int plan, Request q, hipStream_t stream, bool static_scratch = false) {
     g_last_error[0] = '\0';
     const int64_t M = q.M, N = q.N, K = q.K;
     if (M < 0 || N < 0 || K < 0)
@@ -679,8 +726,18 @@ int run(int plan, Request q, hipStream_t stream) {
         case KIND_TILE: {
             const TileSplit sp = tile_split_plan(plan, M, N, K);
             Workspace ws{};
+            if (static_scratch && sp.split > 1) {
+                const TileShape ts = tile_shape(PLANS[plan].tile_cfg);
+                const int64_t split_tiles = tile_count(ts, M, N) - sp.full_tiles;
+                const int64_t need = split_tiles * sp.split * ts.bm * ts.bn;
+                if (need > WS_PARTIAL_FLOATS || split_tiles > WS_COUNTERS)
+                    return fail(KERNELARC_ERR_UNSUPPORTED,
+                                "plan %s needs %lld fp32 partials and %lld counters; the static scratch holds %lld "
+                                "and %lld", PLANS[plan].name, (long long)need, (long long)split_tiles,
+                                (long long)WS_PARTIAL_FLOATS, (long long)WS_COUNTERS);
+            }
             if (sp.split > 1) {
-                const int wst = workspace(dev, stream, &ws);
+                const int wst = static_scratch ? scratch_workspace(dev, stream, &ws) : workspace(dev, stream, &ws);
                 if (wst != KERNELARC_OK) return wst;
             }
             e = launch_tile(PLANS[plan].tile_cfg, p, sp.split, sp.full_tiles, sp.split > 1 ? &ws : nullptr, stream);
@@ -689,8 +746,17 @@ int run(int plan, Request q, hipStream_t stream) {
         case KIND_STREAM: {
             const int split = stream_split_of(plan, M, N, K);
             Workspace ws{};
+            if (static_scratch && split > 1) {
+                const int64_t need = stream_workspace_floats(M, N, split, PLANS[plan].rows);
+                const int64_t counters = stream_counter_count(N, PLANS[plan].rows);
+                if (need > WS_PARTIAL_FLOATS || counters > WS_COUNTERS)
+                    return fail(KERNELARC_ERR_UNSUPPORTED,
+                                "plan %s needs %lld fp32 partials and %lld counters; the static scratch holds %lld "
+                                "and %lld", PLANS[plan].name, (long long)need, (long long)counters,
+                                (long long)WS_PARTIAL_FLOATS, (long long)WS_COUNTERS);
+            }
             if (split > 1) {
-                const int wst = workspace(dev, stream, &ws);
+                const int wst = static_scratch ? scratch_workspace(dev, stream, &ws) : workspace(dev, stream, &ws);
                 if (wst != KERNELARC_OK) return wst;
             }
             e = launch_stream(p, PLANS[plan].tile_cfg, PLANS[plan].stages, PLANS[plan].rows, split,
@@ -977,6 +1043,11 @@ int kernelarc_gemm_bf16_residual(int64_t M, int64_t N, int64_t K, const void *X,
 int kernelarc_gemm_bf16(int64_t M, int64_t N, int64_t K, const void *X, const void *W, void *Y,
                         hipStream_t stream) {
     return run(-1, dense_request(M, N, K, X, W, nullptr, Y), stream);
+}
+
+int kernelarc_gemm_bf16_residual_noalloc(int64_t M, int64_t N, int64_t K, const void *X, const void *W,
+                                         const void *R, void *Y, hipStream_t stream) {
+    return run(-1, dense_request(M, N, K, X, W, R, Y), stream, true);
 }
 
 int kernelarc_gemm_bf16_with_plan(int plan, int64_t M, int64_t N, int64_t K, const void *X,

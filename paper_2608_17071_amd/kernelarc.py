@@ -34,6 +34,7 @@ _P = ctypes.c_void_p
 _SIGS = {
     "kernelarc_gemm_bf16_residual": (ctypes.c_int, [_I64, _I64, _I64, _P, _P, _P, _P, _P]),
     "kernelarc_gemm_bf16": (ctypes.c_int, [_I64, _I64, _I64, _P, _P, _P, _P]),
+    "kernelarc_gemm_bf16_residual_noalloc": (ctypes.c_int, [_I64, _I64, _I64, _P, _P, _P, _P, _P]),
     "kernelarc_gemm_bf16_with_plan": (ctypes.c_int, [ctypes.c_int, _I64, _I64, _I64, _P, _P, _P, _P, _P]),
     "kernelarc_plan_count": (ctypes.c_int, []),
     "kernelarc_plan_name": (ctypes.c_int, [_I64, _I64, _I64, ctypes.c_int, ctypes.c_char_p, ctypes.c_size_t]),
@@ -180,6 +181,19 @@ def gemm_bf16(x, w, out=None, stream=None):
         st = _lib.kernelarc_gemm_bf16(M, N, K, x.data_ptr(), w.data_ptr(), out.data_ptr(),
                                       _stream_handle(stream))
     _check(st, "kernelarc_gemm_bf16")
+    return out
+
+
+def gemm_bf16_residual_noalloc(x, w, r=None, out=None, stream=None):
+    """Y = X W^T (+ R) with the split-K partials in the library's static
+    scratch: the call allocates no device memory (``out`` must then be given
+    by callers that cannot allocate)."""
+    M, N, K, out = _operands(x, w, r, out)
+    with torch.cuda.device(x.device):
+        st = _lib.kernelarc_gemm_bf16_residual_noalloc(M, N, K, x.data_ptr(), w.data_ptr(),
+                                                       r.data_ptr() if r is not None else None,
+                                                       out.data_ptr(), _stream_handle(stream))
+    _check(st, "kernelarc_gemm_bf16_residual_noalloc")
     return out
 
 
