@@ -80,14 +80,15 @@ def source_digest(paths):
     return h.hexdigest()
 
 
-# Kernel symbol fragment of each tile plan (rocprofv3 reports symbols).
-# Cfg<BM, BN, BK, WAVES_M, WAVES_N, STAGES, WAVES_PER_EU, LAG, M16>.
+# Kernel symbol fragment and threads per workgroup of each 256x256 tile plan
+# (rocprofv3 reports symbols).
+# Cfg<BM, BN, BK, WAVES_M, WAVES_N, STAGES, WAVES_PER_EU, LAG, M16, AACC>.
 PLAN_SYMBOL = {
-    "tile_256x256_k64_w8": "Cfg<256, 256, 64, 2, 4, 2, 2, false, false>",
-    "tile_256x256_k64_w8_m16": "Cfg<256, 256, 64, 2, 4, 2, 2, false, true>",
+    "tile_256x256_k64_w8": ("Cfg<256, 256, 64, 2, 4, 2, 2, false, false, false>", 512),
+    "tile_256x256_k64_w4_m16a": ("Cfg<256, 256, 64, 2, 2, 2, 1, false, true, true>", 256),
 }
 # The plan whose HBM traffic the counter runs summarise (the big sweep shapes' plan).
-TRAFFIC_PLAN = "tile_256x256_k64_w8_m16"
+TRAFFIC_PLAN = "tile_256x256_k64_w4_m16a"
 KERNEL_SOURCES = ["paper_2608_17071_amd/csrc/tile_kernel.h", "paper_2608_17071_amd/csrc/kernel_tile.hip",
                   "paper_2608_17071_amd/csrc/internal.h"]
 
@@ -112,7 +113,7 @@ def summarize_traffic(pmc_dir, plan, shapes, command):
     cw = per_grid("copy_write", "WRITE_SIZE", "copyBuffer")
     fetch_scale = copy_bytes / (1024 * max(cf.values()))
     write_scale = copy_bytes / (1024 * max(cw.values()))
-    sym = PLAN_SYMBOL[plan]     # a 256x256 tile, 512 threads per workgroup
+    sym, threads = PLAN_SYMBOL[plan]     # a 256x256 tile
     fetch = per_grid("fetch", "FETCH_SIZE", sym)
     write = per_grid("write", "WRITE_SIZE", sym)
     rows, total = [], 0.0
@@ -120,7 +121,7 @@ def summarize_traffic(pmc_dir, plan, shapes, command):
         w = wl.BY_NAME[name]
         # the shapes of one run have distinct grids (work-items = output
         # tiles x threads per workgroup, no split-K for this plan)
-        g = -(-w.M // 256) * -(-w.N // 256) * 512
+        g = -(-w.M // 256) * -(-w.N // 256) * threads
         b = fetch[g] * 1024 * fetch_scale + write[g] * 1024 * write_scale
         total += b
         rows.append({"shape": name, "fetch_kib": fetch[g], "write_kib": write[g], "hbm_bytes": b,
@@ -151,7 +152,7 @@ def measured_traffic(plan_name):
 
 
 class Case:
-    def __init__(self, w, ka, torch, rotate=True):
+    def __init__(self, w, ka, torch, rotate=True, plan=None):
         from paper_2608_17071_amd import workloads as wl
         t = wl.make_inputs(w)
         self.w = w
@@ -167,14 +168,21 @@ class Case:
             self.sets.append((x if i == 0 else x.clone(), W if i == 0 else W.clone(),
                               None if r is None else (r if i == 0 else r.clone()),
                               torch.empty(w.M, w.N, dtype=torch.bfloat16, device="cuda")))
-        self.plan = ka.select_plan(w.M, w.N, w.K, w.residual)
+        self.force(ka, plan)
+
+    def force(self, ka, plan):
+        """Run `plan` (an id) from now on; None: the library's own choice."""
+        self.forced = plan
+        self.plan = ka.select_plan(self.w.M, self.w.N, self.w.K, self.w.residual) if plan is None else plan
         self.plan_name = ka.plan_name(self.plan)
         self.times = []
         self.graph = None
 
     def call(self, ka, i):
         x, W, r, y = self.sets[i]
-        if r is not None:
+        if self.forced is not None:
+            ka.gemm_bf16_with_plan(self.forced, x, W, r, out=y)
+        elif r is not None:
             ka.gemm_bf16_residual(x, W, r, out=y)
         else:
             ka.gemm_bf16(x, W, out=y)
@@ -194,7 +202,7 @@ class BlasCase(Case):
 
     def __init__(self, w, ka, torch, rotate=True):
         super().__init__(w, ka, torch, rotate)
-        self.plan, self.plan_name = -1, "torch(hipBLASLt)"
+        self.forced, self.plan, self.plan_name = None, -1, "torch(hipBLASLt)"
         self.torch = torch
 
     def call(self, ka, i):
@@ -208,7 +216,7 @@ class BlasCase(Case):
 class GeneralCase(Case):
     """A general-form workload: X read through its row stride, C, bias, alpha, beta."""
 
-    def __init__(self, w, ka, torch, rotate=True):
+    def __init__(self, w, ka, torch, rotate=True, plan=None):
         from paper_2608_17071_amd import workloads as wl
         t = wl.make_general_inputs(w)
         self.w = w
@@ -227,14 +235,16 @@ class GeneralCase(Case):
             self.sets.append((xb[:, :w.K], W if i == 0 else W.clone(),
                               None if c is None else (c if i == 0 else c.clone()),
                               torch.empty(w.M, w.N, dtype=torch.bfloat16, device="cuda"), b))
-        self.plan = ka.select_plan_ex(w.M, w.N, w.K, w.has_c, w.ldx, w.K, w.N, w.N, w.alpha, w.beta, w.has_bias)
+        self.forced = plan
+        self.plan = ka.select_plan_ex(w.M, w.N, w.K, w.has_c, w.ldx, w.K, w.N, w.N, w.alpha, w.beta,
+                                      w.has_bias) if plan is None else plan
         self.plan_name = ka.plan_name(self.plan)
         self.times = []
         self.graph = None
 
     def call(self, ka, i):
         x, W, c, y, b = self.sets[i]
-        ka.gemm_bf16_ex(x, W, c, b, self.w.alpha, self.w.beta, out=y)
+        ka.gemm_bf16_ex(x, W, c, b, self.w.alpha, self.w.beta, out=y, plan=self.forced)
 
 
 class GluCase(Case):
@@ -619,6 +629,84 @@ def oracle_config_seconds():
     return res
 
 
+def compare_plans(names, plans, steps, warmup, ka, torch, rotate=True):
+    """Time every plan that can run each workload (or the listed ones) under
+    the benchmark's protocol (cold operands, graph replay); one workload's
+    operand copies at a time.  Workloads: the sweep and gate configs, the
+    general-form and the SwiGLU ones.  Returns one row per workload."""
+    from paper_2608_17071_amd import workloads as wl
+    all_plans = ka.plan_names()
+    rows = []
+    for n in names:
+        if n in wl.GLU_BY_NAME:
+            w = wl.GLU_BY_NAME[n]
+            ok = lambda p: ka.plan_supports_swiglu(p, w.M, w.N, w.K)
+            make = lambda p: GluCase(w, ka, torch, rotate=rotate, plan=p)
+            selected = ka.plan_name(ka.select_plan_swiglu(w.M, w.N, w.K))
+            base = None
+        elif n in wl.GENERAL_BY_NAME:
+            w = wl.GENERAL_BY_NAME[n]
+            ok = lambda p: ka.plan_supports(p, w.M, w.N, w.K, w.has_c)
+            make = lambda p: GeneralCase(w, ka, torch, rotate=rotate, plan=p)
+            selected = ka.plan_name(ka.select_plan_ex(w.M, w.N, w.K, w.has_c, w.ldx, w.K, w.N, w.N, w.alpha,
+                                                      w.beta, w.has_bias))
+            base = None
+        else:
+            w = wl.BY_NAME[n]
+            ok = lambda p: ka.plan_supports(p, w.M, w.N, w.K, w.residual)
+            base = Case(w, ka, torch, rotate=rotate)
+
+            def make(p, base=base):
+                base.force(ka, p)
+                return base
+            selected = base.plan_name
+        cand = [p for p in (plans or all_plans) if not p.startswith("generic") and ok(all_plans.index(p))]
+        times = {}
+        for p in cand:
+            case = make(all_plans.index(p))
+            log(f"  {n} plan {p} ...")
+            try:
+                time_cases([case], steps, warmup, ka, torch)
+            except ka.KernelArcError as e:      # a form the plan cannot compute (strides, scalars)
+                log(f"    skipped: {e}")
+                continue
+            times[p] = round(median(case.times) * 1e6, 3)
+            if case is not base:
+                case.free()
+            del case
+            torch.cuda.synchronize()
+        if base is not None:
+            base.free()
+        best = min(times, key=times.get) if times else None
+        rows.append({"shape": n, "M": w.M, "N": w.N, "K": w.K, "selected": selected, "fastest": best,
+                     "us": times})
+        log(f"  {n}: selected {selected} {times.get(selected)} us, fastest {best} {times.get(best)} us")
+    return rows
+
+
+def write_plan_table(rows, path, command):
+    """Markdown summary of compare_plans: per workload the selected plan, the
+    fastest plan and every candidate's time."""
+    lines = ["# Plan comparison on MI355X (the benchmark's cold-operand protocol, HIP-graph replay)", "",
+             "Command (repository root on the GPU box):", "", "```", command, "```", "",
+             "Per workload: the plan the library selects, the fastest candidate, and the median per-call time of",
+             "every plan that can run the shape (generic kernel excluded), in microseconds.", "",
+             "| shape | selected | selected us | fastest | fastest us | selected / fastest |",
+             "|---|---|---|---|---|---|"]
+    for r in rows:
+        t = r["us"]
+        sel, best = r["selected"], r["fastest"]
+        ratio = t[sel] / t[best] if sel in t and best in t and t[best] else float("nan")
+        lines.append(f"| {r['shape']} | {sel} | {t.get(sel, float('nan')):.2f} | {best} | "
+                     f"{t.get(best, float('nan')):.2f} | {ratio:.3f} |")
+    lines += ["", "## Every candidate", ""]
+    for r in rows:
+        cells = ", ".join(f"{p} {v:.2f}" for p, v in sorted(r["us"].items(), key=lambda kv: kv[1]))
+        lines.append(f"- **{r['shape']}** (M={r['M']}, N={r['N']}, K={r['K']}): {cells}")
+    with open(path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -644,6 +732,11 @@ def main():
                     help="with --only: also time torch's GEMM (hipBLASLt) on the plain shapes, same protocol")
     ap.add_argument("--summarize-traffic", nargs=2, metavar=("PMC_DIR", "SHAPES"),
                     help="write profiles/traffic.json for the dominant plan from counter runs")
+    ap.add_argument("--compare-plans", action="store_true",
+                    help="time every plan that can run each workload of --only (default: the 20 benchmark "
+                         "workloads) under the benchmark's protocol; --plans limits the candidates")
+    ap.add_argument("--plans", default="", help="with --compare-plans: comma-separated plan names")
+    ap.add_argument("--write-table", default="", help="with --compare-plans: write a markdown summary here")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device copy 10 times (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -678,6 +771,19 @@ def main():
             b.copy_(a)
         torch.cuda.synchronize()
         print(json.dumps({"copy_calibration_bytes_read": a.numel(), "bytes_written": b.numel(), "launches": 10}))
+        return
+
+    if args.compare_plans:
+        names = args.only.split(",") if args.only else [w.name for w in wl.SWEEP] + \
+            [wl.DECODE.name, wl.PREFILL.name, wl.SQUARE.name]
+        plans = args.plans.split(",") if args.plans else None
+        rows = compare_plans(names, plans, args.steps, args.warmup, ka, torch, rotate=not args.hot)
+        if args.write_table:
+            cmd = "python bench.py --compare-plans" + (f" --only {args.only}" if args.only else "") + \
+                  (f" --plans {args.plans}" if args.plans else "") + f" --steps {args.steps} --warmup {args.warmup}" + \
+                  f" --write-table {args.write_table}"
+            write_plan_table(rows, args.write_table, cmd)
+        print(json.dumps({"plan_table": rows}), flush=True)
         return
 
     if args.only:

@@ -75,7 +75,7 @@ const PlanInfo PLANS[] = {
     {"tile_256x128_k64s3_w8_lag_splitk", KIND_TILE, TC_256x128_K64_S3_W8_L, 0},
     {"tile_256x256_k64_w8", KIND_TILE, TC_256x256_K64_S2_W8, 1},
     {"tile_256x256_k64_w8_tailsplit", KIND_TILE, TC_256x256_K64_S2_W8, -1},
-    {"tile_256x256_k64_w8_m16", KIND_TILE, TC_256x256_K64_S2_W8_M16, 1},
+    {"tile_256x256_k64_w4_m16a", KIND_TILE, TC_256x256_K64_S2_W4_M16A, 1},
 };
 constexpr int NUM_PLANS = static_cast<int>(sizeof(PLANS) / sizeof(PLANS[0]));
 
@@ -217,11 +217,11 @@ const TableEntry TABLE[] = {
     {512, 5120, 5120, 1, "tile_256x128_k64s3_w8_splitk"},
     {512, 8192, 8192, 1, "tile_128x128_k64s4_w4_lag"},
     {4096, 2048, 2048, 1, "tile_256x128_k64s3_w8_lag"},
-    {4096, 4096, 4096, 1, "tile_256x256_k64_w8_m16"},
+    {4096, 4096, 4096, 1, "tile_256x256_k64_w4_m16a"},
     {4096, 5120, 5120, 1, "tile_256x256_k64_w8_tailsplit"},
-    {4096, 8192, 8192, 1, "tile_256x256_k64_w8_m16"},
+    {4096, 8192, 8192, 1, "tile_256x256_k64_w4_m16a"},
     // plain BF16 GEMM
-    {8192, 8192, 8192, 0, "tile_256x256_k64_w8_m16"},
+    {8192, 8192, 8192, 0, "tile_256x256_k64_w4_m16a"},
     {-1, 0, 0, 0, ""},   // sentinel
 };
 
@@ -270,7 +270,7 @@ int select(int64_t M, int64_t N, int64_t K, bool residual, const Layout &lay) {
         const int64_t t256 = tile_count(tile_shape(TC_256x256_K64_S2_W8), M, N);
         const int64_t t256x128 = tile_count(tile_shape(TC_256x128_K64_S3_W8_L), M, N);
         if (3 * t256 >= 2 * CUS)   // wide outputs: the 256x256 tiles reach 2/3 of the CUs
-            plan = pick(t256 % CUS == 0 ? "tile_256x256_k64_w8_m16" : "tile_256x256_k64_w8_tailsplit");
+            plan = pick(t256 % CUS == 0 || t256 < CUS ? "tile_256x256_k64_w4_m16a" : "tile_256x256_k64_w8_tailsplit");
         else if (t256x128 >= CUS && M > 512)
             plan = pick("tile_256x128_k64s3_w8_lag");
         else if (2 * tiles64 <= CUS) plan = pick("tile_64x64_k128s3_w4_splitk");
@@ -281,8 +281,8 @@ int select(int64_t M, int64_t N, int64_t K, bool residual, const Layout &lay) {
         if (plan < 0) plan = pick("tile_128x128_k64_w4_splitk");
     } else {
         const int64_t t256 = tile_count(tile_shape(TC_256x256_K64_S2_W8), M, N);
-        if (t256 >= CUS)   // whole rounds: 16x16 MFMAs; a partial last round: 32x32 with the tail split
-            plan = pick(t256 % CUS == 0 ? "tile_256x256_k64_w8_m16" : "tile_256x256_k64_w8_tailsplit");
+        if (t256 >= CUS)   // whole rounds: 4 waves on AGPRs; a partial last round: 8 waves with the tail split
+            plan = pick(t256 % CUS == 0 ? "tile_256x256_k64_w4_m16a" : "tile_256x256_k64_w8_tailsplit");
         else if (tile_count(tile_shape(TC_256x128_K64_S3_W8_L), M, N) >= CUS) plan = pick("tile_256x128_k64s3_w8_lag");
         if (plan < 0) plan = pick("tile_128x128_k64_w4");
     }
@@ -339,8 +339,8 @@ int select_glu(int64_t M, int64_t N, int64_t K) {
     } else if (M <= 128 || 2 * t256x128 < CUS) {
         plan = 2 * t128 <= CUS ? pick("tile_128x128_k64s3_w4_splitk") : pick("tile_128x128_k64s4_w4_lag");
     } else if (5 * t256 >= 4 * CUS) {
-        // whole rounds: 16x16 MFMAs; else 32x32 with the tail split
-        plan = pick(t256 % CUS == 0 ? "tile_256x256_k64_w8_m16" : "tile_256x256_k64_w8_tailsplit");
+        // whole rounds or one partial round: 4 waves on AGPRs; else 8 waves with the tail split
+        plan = pick(t256 % CUS == 0 || t256 < CUS ? "tile_256x256_k64_w4_m16a" : "tile_256x256_k64_w8_tailsplit");
     } else {
         plan = pick("tile_256x128_k64s3_w8_lag");
     }
@@ -369,8 +369,8 @@ bool supports_i8(int plan, int64_t M, int64_t N, int64_t K, bool glu, bool f8 = 
     // (the same bytes per stage as bf16 at K/2).
     if (pi.kind == KIND_STREAM)
         return !glu && !f8 && pi.rows < 64 && K % 16 == 0 && supports(plan, M, N, K / 2, true, dense_layout(N, K / 2));
-    // (16x16 MFMA tiles take plain INT8 only: not FP8, not SwiGLU)
-    if (pi.kind != KIND_TILE || K % 16 != 0 || (tile_is_m16(pi.tile_cfg) && (f8 || glu)) ||
+    // (16x16 MFMA tiles take bf16 operands only)
+    if (pi.kind != KIND_TILE || K % 16 != 0 || tile_is_m16(pi.tile_cfg) ||
         (f8 && !tile_f8_ok(pi.tile_cfg)))
         return false;
     return glu ? supports_glu(plan, M, N, K / 2) : supports(plan, M, N, K / 2, true, dense_layout(N, K / 2));
@@ -403,12 +403,11 @@ int select_i8(int64_t M, int64_t N, int64_t K, bool glu, bool f8 = false) {
         if (plan >= 0) return plan;
     }
     plan = glu ? select_glu(M, N, K / 2) : select(M, N, K / 2, true, dense_layout(N, K / 2));
-    // The 256x256 tile without the tail split, on 32x32 MFMAs (its 16x16
-    // form, which plain INT8 can also run, measured 3.5 % faster at 4096^3
-    // and 2 % slower at 8192^3), and already when its tiles reach 4/5 of
-    // the CUs (an INT8 tile covers its K range in half the steps: at
-    // M = 1024, N = 13824, K = 5120, 90 us against 128 us for 128x128).
-    if (plan == plan_index("tile_256x256_k64_w8_tailsplit") || plan == plan_index("tile_256x256_k64_w8_m16") ||
+    // The 256x256 8-wave tile without the tail split (the 4-wave AGPR tile
+    // is bf16 only), and already when its tiles reach 4/5 of the CUs (an
+    // INT8 tile covers its K range in half the steps: at M = 1024,
+    // N = 13824, K = 5120, 90 us against 128 us for 128x128).
+    if (plan == plan_index("tile_256x256_k64_w8_tailsplit") || plan == plan_index("tile_256x256_k64_w4_m16a") ||
         (!glu && 5 * tile_count(tile_shape(TC_256x256_K64_S2_W8), M, N) >= 4 * CUS))
         plan = plan_index("tile_256x256_k64_w8");
     if (plan >= 0 && plan != PLAN_GENERIC && supports_i8(plan, M, N, K, glu, f8)) return plan;

@@ -21,7 +21,7 @@ enum PlanId : int {
 // BM x BN output tile, BK deep stages, STAGES-deep LDS ring, waves.
 enum TileCfg : int {
     TC_256x256_K64_S2_W8 = 0,
-    TC_256x256_K64_S2_W8_M16 = 1,  // 16x16x32 MFMA (bf16 plain and general forms)
+    TC_256x256_K64_S2_W4_M16A = 1,  // 4 waves of 128x128, 16x16x32 MFMA, AGPR accumulators (bf16)
     TC_256x128_K64_S3_W8 = 2,
     TC_256x128_K64_S3_W8_L = 3,    // lagged refill
     TC_128x128_K64_S2_W4 = 4,
@@ -240,7 +240,7 @@ __host__ __device__ inline int64_t group_rows(const int32_t *counts, int64_t g, 
 // FP8: tile kernels (configurations of tile_f8_ok; SwiGLU also tile_glu_ok)
 // and generic kernels.
 bool tile_f8_ok(int cfg);
-// 16x16x32 MFMA tile configurations (bf16 plain and general forms only).
+// 16x16x32 MFMA tile configurations (bf16 operands only).
 bool tile_is_m16(int cfg);
 hipError_t launch_tile_f8(int cfg, const F8Problem &p, int split, int64_t full_tiles, const Workspace *ws,
                           hipStream_t s);

@@ -65,17 +65,29 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, ui
 constexpr int waitcnt_vm(int n) { return (n & 0xF) | ((n >> 4) << 14) | (0x7 << 4) | (0xF << 8); }
 
 // Slot of 16-byte chunk c of row r: c ^ swz(r).  16 chunks per row
-// (BK=128), 8 (BK=64) or 4 (BK=32); each spreads rows 0..7 and rows 0..15
-// over distinct bank groups.
+// (BK=128), 8 (BK=64) or 4 (BK=32).  A fragment read touches one chunk of
+// 32 consecutive rows (32x32 MFMA) or two or four chunks of 16 (16x16 MFMA,
+// lane quarters reading chunks that differ in their low bit); each swizzle
+// puts the rows such a read serves together in distinct 16-byte bank groups.
+// The fragment readers compute swz from the row within a 16-row block, so
+// every swizzle repeats every 16 rows (checked below).
 template <int CHUNKS>
-__device__ __forceinline__ int swz(int r) {
+__host__ __device__ constexpr int swz(int r) {
     if constexpr (CHUNKS == 16) return r & 15;
     else if constexpr (CHUNKS == 8) return (r & 7) ^ ((r >> 3) & 1);
-    else return ((r >> 1) ^ (r >> 3)) & 3;
+    else return (((r >> 1) & 1) << 1) | ((r >> 2) & 1);   // 64-byte rows: pairs of rows share 128 bytes
 }
+template <int CHUNKS>
+constexpr bool swz_repeats_every_16_rows() {
+    for (int r = 0; r < 64; ++r)
+        if (swz<CHUNKS>(r) != swz<CHUNKS>(r & 15)) return false;
+    return true;
+}
+static_assert(swz_repeats_every_16_rows<4>() && swz_repeats_every_16_rows<8>() && swz_repeats_every_16_rows<16>(),
+              "fragment reads assume 16-row periodic swizzles");
 
 template <int BM_, int BN_, int BK_, int WAVES_M_, int WAVES_N_, int STAGES_, int WAVES_PER_EU_, bool LAG_ = false,
-          bool M16_ = false>
+          bool M16_ = false, bool AACC_ = false>
 struct Cfg {
     static constexpr int BM = BM_, BN = BN_, BK = BK_, STAGES = STAGES_;
     static constexpr int WAVES_M = WAVES_M_, WAVES_N = WAVES_N_;
@@ -89,6 +101,14 @@ struct Cfg {
     // Same operand bytes and MFMA cycles per K; half the accumulator
     // register traffic per product.
     static constexpr bool M16 = M16_;
+    // AACC (with M16, bf16 only): the MFMAs are issued as inline assembly
+    // whose accumulator operands are AGPRs, so the 16x16 accumulator blocks
+    // stay in the AGPR file for the whole K loop.  This is what lets one wave
+    // hold a 128x128 block (256 accumulator registers, the whole AGPR file)
+    // with its fragments and addresses in VGPRs; with the builtin the
+    // compiler moves accumulators between the two files every step.
+    static constexpr bool AACC = AACC_;
+
     static constexpr int KSTEPS = BK / (M16 ? 32 : 16);           // MFMA sub-steps per stage
     // Fragment prefetch distance: the LDS reads of sub-step s + PD are
     // issued among the MFMAs of sub-step s (PD + 1 register sets).
@@ -123,8 +143,9 @@ struct Cfg {
     static_assert(LDS_BYTES <= 160 * 1024, "LDS capacity");
     static_assert(TILE_WAVES * EPI_WAVE_FLOATS * 4 <= LDS_BYTES, "epilogue staging fits");
     static_assert(LOADS * (STAGES - 2) < 64, "vmcnt range");
-    static_assert(PD >= 1 && PD < KSTEPS && KSTEPS % (PD + 1) == 0, "fragment prefetch distance");
+    static_assert(PD >= 1 && PD <= KSTEPS, "fragment prefetch distance");
     static_assert(!LAG || STAGES >= 3, "lagged refill needs three stages");
+    static_assert(!AACC || M16, "AGPR accumulators are a 16x16 MFMA option");
 };
 
 // Load block (RPI rows of the stage's B tile) that B load qb of a wave
@@ -166,6 +187,8 @@ __device__ __forceinline__ void issue_load(char *stage, const __amdgpu_buffer_rs
                                                  off, 0, 0, 0);
     }
 }
+
+constexpr int gcd_int(int a, int b) { return b == 0 ? a : gcd_int(b, a % b); }
 
 // Compile-time loop: f(std::integral_constant<int, I>) for I = B .. E-1.
 template <int B, class F, int... I>
@@ -251,15 +274,8 @@ __device__ __forceinline__ void stage_barrier() {
     asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
 }
 
-// Accumulator quads as 16 raw bytes (fp32 or int32 bits) for the split-K
-// hand-off, and their sums (exact for int32).
-// (q is a constant once the callers' loops are unrolled.)
-__device__ __forceinline__ f32x4 quad_bits(const f32x16 &a, int q) {
-    return f32x4{a[4 * q], a[4 * q + 1], a[4 * q + 2], a[4 * q + 3]};
-}
-__device__ __forceinline__ f32x4 quad_bits(const i32x16 &a, int q) {
-    return __builtin_bit_cast(f32x4, i32x4{a[4 * q], a[4 * q + 1], a[4 * q + 2], a[4 * q + 3]});
-}
+// Adds 16 raw bytes (fp32 or int32 bits) to quad q of a 32x32 block (exact
+// for int32).
 __device__ __forceinline__ void add_quad(f32x16 &a, int q, const f32x4 &v) {
     a[4 * q] += v[0];
     a[4 * q + 1] += v[1];
@@ -272,6 +288,15 @@ __device__ __forceinline__ void add_quad(i32x16 &a, int q, const f32x4 &bits) {
     a[4 * q + 1] += v[1];
     a[4 * q + 2] += v[2];
     a[4 * q + 3] += v[3];
+}
+
+// 16 raw bytes added to an fp32 or int32 quad (exact for int32).
+__device__ __forceinline__ void add_bits(f32x4 &a, const f32x4 &bits) { a += bits; }
+__device__ __forceinline__ void add_bits(i32x4 &a, const f32x4 &bits) { a += __builtin_bit_cast(i32x4, bits); }
+
+// v_mfma_f32_16x16x32_bf16 with the accumulator in AGPRs (see Cfg::AACC).
+__device__ __forceinline__ void mfma16_agpr(f32x4 &acc, const bf16x8 &a, const bf16x8 &b) {
+    asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
 }
 
 // Split-K bookkeeping of one launch (split == 1: none).
@@ -312,7 +337,7 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
     constexpr bool Q8 = I8 || F8;                  // 1-byte operands with dequantisation scales
     constexpr bool GLU = std::is_same<PB, GluProblem>::value || std::is_same<PB, I8GluProblem>::value ||
                          std::is_same<PB, F8GluProblem>::value;
-    static_assert(!C::M16 || (!F8 && !(I8 && GLU)), "16x16 MFMA tiles take bf16 and plain INT8 problems");
+    static_assert(!C::M16 || !Q8, "16x16 MFMA tiles take bf16 problems");
     constexpr int EB = Q8 ? 1 : 2;                 // bytes per operand element
     constexpr int BKE = C::ROW_BYTES / EB;         // K elements per stage
     constexpr int CKE = 16 / EB;                   // K elements per 16-byte chunk
@@ -417,23 +442,37 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
         b_k[q] = c * CKE;
     }
 
-    AccV acc[C::TM][C::TN];
-#pragma unroll
-    for (int i = 0; i < C::TM; ++i)
-#pragma unroll
-        for (int j = 0; j < C::TN; ++j)
-#pragma unroll
-            for (int e = 0; e < 16; ++e) acc[i][j][e] = 0;
-    // M16: the K loop accumulates 16x16 blocks in their own registers; they
-    // are moved into the quads of the 32x32 blocks once, after the loop.
+    // Accumulators: 32x32 blocks (acc), or with M16 16x16 blocks (acc16),
+    // where quad q of 32x32 block (i, j) -- its elements 4q .. 4q+3 -- is
+    // 16x16 block (2i + q/2, 2j + q%2).  Everything after the K loop reads
+    // and writes them through quad_of / set_quad in 32x32-block terms.
     using AccQ = typename std::conditional<I8, i32x4, f32x4>::type;
+    AccV acc[C::M16 ? 1 : C::TM][C::M16 ? 1 : C::TN];
     AccQ acc16[C::M16 ? 2 * C::TM : 1][C::M16 ? 2 * C::TN : 1];
-    if constexpr (C::M16) {
+    auto quad_of = [&](int i, int j, int q) -> AccQ {
+        if constexpr (C::M16) return acc16[2 * i + (q >> 1)][2 * j + (q & 1)];
+        else return AccQ{acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+    };
+    auto quad_ref_add = [&](int i, int j, int q, const f32x4 &bits) {
+        if constexpr (C::M16) add_bits(acc16[2 * i + (q >> 1)][2 * j + (q & 1)], bits);
+        else add_quad(acc[i][j], q, bits);
+    };
+    auto zero_acc = [&] {
+        if constexpr (C::M16) {
 #pragma unroll
-        for (int i = 0; i < 2 * C::TM; ++i)
+            for (int i = 0; i < 2 * C::TM; ++i)
 #pragma unroll
-            for (int j = 0; j < 2 * C::TN; ++j) acc16[i][j] = AccQ{0, 0, 0, 0};
-    }
+                for (int j = 0; j < 2 * C::TN; ++j) acc16[i][j] = AccQ{0, 0, 0, 0};
+        } else {
+#pragma unroll
+            for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+                for (int j = 0; j < C::TN; ++j)
+#pragma unroll
+                    for (int e = 0; e < 16; ++e) acc[i][j][e] = 0;
+        }
+    };
+    zero_acc();
 
     // Fragment reads: row (lane % 32) of each 32-row block, chunk 2*ks + hi
     // (32x32x16); with M16, row (lane % 16) of each 16-row block, one of
@@ -556,7 +595,15 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
     // One MFMA sub-step covers 32 bytes of K per row (bf16 32x32x16, int8
     // 32x32x32) or 64 (FP8 32x32x64).
     constexpr int KS = F8 ? C::KSTEPS / 2 : C::KSTEPS, PD = C::PD, NSETS = PD + 1;
-    static_assert(KS > PD && KS % NSETS == 0, "fragment prefetch distance");
+    static_assert(KS >= PD, "fragment prefetch distance");
+    // Sub-step g of the workgroup's range (g = step * KS + ks) multiplies the
+    // fragments of register set g % NSETS.  When KS is not a multiple of
+    // NSETS the loop body covers UNROLL steps, each with its phase fixed at
+    // compile time, so every set index stays a constant; the step count is
+    // then rounded up to a multiple of UNROLL, and the extra step, past the
+    // end of the K range, multiplies stage buffers its loads filled with
+    // zeros (out-of-range chunks arrive as zeros), adding exact zeros.
+    constexpr int UNROLL = NSETS / gcd_int(KS, NSETS);
     // Per sub-step: MF MFMAs and FR fragment reads (A blocks then B blocks
     // of 32 rows, or of 16 rows with M16: twice as many of each block kind,
     // four 16x16 products per 32x32 accumulator block).
@@ -622,7 +669,8 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
     __builtin_amdgcn_sched_barrier(0);
 
     int cur_stage = 0;
-    for (int it = 0; it < iters; ++it) {
+    auto k_step = [&](int it, auto phc) {
+        constexpr int PH = decltype(phc)::value;   // it % UNROLL
         const int next_stage = cur_stage + 1 == C::STAGES ? 0 : cur_stage + 1;
         char *const cur = glds + cur_stage * C::STAGE_BYTES;
         const char *const nxt = glds + next_stage * C::STAGE_BYTES;
@@ -635,9 +683,9 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
         static_for<0, KS>([&](auto ksc) {
             constexpr int ks = decltype(ksc)::value;
             if constexpr (ks == KS - PD) stage_barrier<VM_KEEP>();
-            constexpr int set = ks % NSETS;
+            constexpr int set = (PH * KS + ks) % NSETS;
             constexpr int tgt = ks + PD;              // sub-step whose fragments are read
-            constexpr int tset = tgt % NSETS;
+            constexpr int tset = (PH * KS + tgt) % NSETS;
             const char *const src = tgt < KS ? cur : nxt;
             const int tcol = colk[tgt % KS], tcol2 = colk2[tgt % KS];
             static_for<0, MF>([&](auto tc) {
@@ -645,10 +693,8 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
                 constexpr int i = t / FTN, j = t % FTN;
                 if constexpr (C::M16)
                 {
-                    if constexpr (I8)   // 16x16x64 int8: the same 16 bytes per lane
-                        acc16[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4, fa[set][i]),
-                                                                            __builtin_bit_cast(i32x4, fb[set][j]),
-                                                                            acc16[i][j], 0, 0, 0);
+                    if constexpr (C::AACC)
+                        mfma16_agpr(acc16[i][j], fa[set][i], fb[set][j]);
                     else
                         acc16[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[set][i], fb[set][j], acc16[i][j], 0,
                                                                               0, 0);
@@ -682,16 +728,14 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
             });
         });
         cur_stage = next_stage;
-    }
-    if constexpr (C::M16) {
-        // 16x16 block (i, j) becomes quad 2*(i%2) + j%2 of 32x32 block (i/2, j/2).
-#pragma unroll
-        for (int i = 0; i < 2 * C::TM; ++i)
-#pragma unroll
-            for (int j = 0; j < 2 * C::TN; ++j)
-#pragma unroll
-                for (int k = 0; k < 4; ++k) acc[i / 2][j / 2][4 * (2 * (i % 2) + (j % 2)) + k] = acc16[i][j][k];
-    }
+    };
+    const int iters_run = (iters + UNROLL - 1) / UNROLL * UNROLL;
+    for (int it = 0; it < iters_run; it += UNROLL)
+        static_for<0, UNROLL>([&](auto ph) { k_step(it + decltype(ph)::value, ph); });
+    // The compiler does not see the inline-assembly MFMAs, so it cannot
+    // space their last AGPR writes from the first reads below: 32 idle
+    // cycles cover the longest required gap of a 16x16x32 MFMA.
+    if constexpr (C::AACC) asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
 
     // Epilogue.  Accumulator element e of a 32x32 block sits at row
     // 8*(e/4) + 4*hi + e%4 and column lane % 32.  Each 32-row slab of the
@@ -725,7 +769,7 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
                 for (int j = 0; j < C::TN; ++j)
 #pragma unroll
                     for (int q = 0; q < 4; ++q) {
-                        const f32x4 v = quad_bits(acc[i][j], q);
+                        const f32x4 v = __builtin_bit_cast(f32x4, quad_of(i, j, q));
                         const uint32_t off = mine + (((wblk + i * C::TN + j) * 4 + q) * 64 + lane) * 16;
                         __builtin_amdgcn_raw_buffer_store_b128(v, rp, off, 0, AUX_SC1);
                     }
@@ -743,12 +787,7 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
         __syncthreads();                      // the flag is read before LDS is reused
         if (!last) return;
         {
-#pragma unroll
-            for (int i = 0; i < C::TM; ++i)
-#pragma unroll
-                for (int j = 0; j < C::TN; ++j)
-#pragma unroll
-                    for (int e = 0; e < 16; ++e) acc[i][j][e] = 0;
+            zero_acc();
             // Small tiles: D slices per round trip (as many as 128 registers
             // hold); a slice past the last reads out of range and is not added,
             // so the sum still runs over the slices in order.  Large tiles
@@ -765,9 +804,9 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
 #pragma unroll
                             for (int q = 0; q < 4; ++q) {
                                 const uint32_t off = base + (((wblk + i * C::TN + j) * 4 + q) * 64 + lane) * 16;
-                                add_quad(acc[i][j], q,
-                                         __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rp, off, 0,
-                                                                                                         AUX_SC1)));
+                                quad_ref_add(i, j, q,
+                                             __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                                               rp, off, 0, AUX_SC1)));
                             }
                 }
             } else {
@@ -791,7 +830,7 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
                             for (int j = 0; j < C::TN; ++j)
 #pragma unroll
                                 for (int q = 0; q < 4; ++q) {
-                                    add_quad(acc[i][j], q, v[d][(i * C::TN + j) * 4 + q]);
+                                    quad_ref_add(i, j, q, v[d][(i * C::TN + j) * 4 + q]);
                                 }
                     }
                 }
@@ -828,11 +867,11 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
                         float g, u;
                         if constexpr (Q8) {
                             const float sr = sxr[i & 1][e];
-                            g = static_cast<float>(acc[i][2 * j][e]) * (sr * swc[j]);
-                            u = static_cast<float>(acc[i][2 * j + 1][e]) * (sr * swc[C::TN / 2 + j]);
+                            g = static_cast<float>(quad_of(i, 2 * j, e >> 2)[e & 3]) * (sr * swc[j]);
+                            u = static_cast<float>(quad_of(i, 2 * j + 1, e >> 2)[e & 3]) * (sr * swc[C::TN / 2 + j]);
                         } else {
-                            g = acc[i][2 * j][e];
-                            u = acc[i][2 * j + 1][e];
+                            g = quad_of(i, 2 * j, e >> 2)[e & 3];
+                            u = quad_of(i, 2 * j + 1, e >> 2)[e & 3];
                         }
                         if constexpr (C::M16)
                             ep[(16 * (e >> 3) + 4 * hi + (e & 3)) * EPS + j * 32 + 16 * ((e >> 2) & 1) + frag_row] =
@@ -847,10 +886,10 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
                     for (int e = 0; e < 16; ++e) {
                         if constexpr (C::M16)   // quad q = e/4: rows 16*(q/2) + 4*hi + e%4, columns 16*(q%2) + lane%16
                             ep[(16 * (e >> 3) + 4 * hi + (e & 3)) * EPS + j * 32 + 16 * ((e >> 2) & 1) + frag_row] =
-                                static_cast<float>(acc[i][j][e]);
+                                static_cast<float>(quad_of(i, j, e >> 2)[e & 3]);
                         else
                             ep[(8 * (e >> 2) + 4 * hi + (e & 3)) * EPS + j * 32 + frag_row] =
-                                static_cast<float>(acc[i][j][e]);
+                                static_cast<float>(quad_of(i, j, e >> 2)[e & 3]);
                     }
             }
         }
@@ -951,15 +990,19 @@ hipError_t launch_cfg(const Problem &p, int group_m, int split, int64_t full_til
 template <class C>
 hipError_t launch_cfg_i8(const I8Problem &p, int group_m, int split, int64_t full_tiles, const Workspace *ws,
                          hipStream_t s) {
-    const int64_t tiles_m = (p.M + C::BM - 1) / C::BM;
-    const int64_t tiles_n = (p.N + C::BN - 1) / C::BN;
-    const int64_t tiles = tiles_m * tiles_n;
-    SplitK sk;
-    if (!split_args<C, 2 * C::BK>(p.K, tiles, split, full_tiles, ws, sk)) return hipErrorInvalidValue;
-    const int64_t wgs = sk.full_tiles + (tiles - sk.full_tiles) * sk.split;
-    hipLaunchKernelGGL((tile_kernel<C, I8Problem>), dim3(static_cast<unsigned>(wgs)), dim3(C::THREADS), 0, s, p,
-                       tiles_m, tiles_n, group_m, sk);
-    return hipGetLastError();
+    if constexpr (C::M16) {   // 16x16 MFMA tiles: bf16 only
+        return hipErrorInvalidValue;
+    } else {
+        const int64_t tiles_m = (p.M + C::BM - 1) / C::BM;
+        const int64_t tiles_n = (p.N + C::BN - 1) / C::BN;
+        const int64_t tiles = tiles_m * tiles_n;
+        SplitK sk;
+        if (!split_args<C, 2 * C::BK>(p.K, tiles, split, full_tiles, ws, sk)) return hipErrorInvalidValue;
+        const int64_t wgs = sk.full_tiles + (tiles - sk.full_tiles) * sk.split;
+        hipLaunchKernelGGL((tile_kernel<C, I8Problem>), dim3(static_cast<unsigned>(wgs)), dim3(C::THREADS), 0, s, p,
+                           tiles_m, tiles_n, group_m, sk);
+        return hipGetLastError();
+    }
 }
 
 // SwiGLU needs an even number of 32-column blocks per wave (gate/up pairs)
@@ -1006,9 +1049,9 @@ hipError_t launch_cfg_i8_glu(const I8GluProblem &p, int group_m, int split, int6
 }
 
 // Tile shape, K depth, wave grid, pipeline depth and occupancy of each tile
-// configuration: Cfg<BM, BN, BK, WAVES_M, WAVES_N, STAGES, WAVES_PER_EU, LAG, M16>.
+// configuration: Cfg<BM, BN, BK, WAVES_M, WAVES_N, STAGES, WAVES_PER_EU, LAG, M16, AACC>.
 using C256x256w8 = Cfg<256, 256, 64, 2, 4, 2, 2>;
-using C256x256w8m16 = Cfg<256, 256, 64, 2, 4, 2, 2, false, true>;
+using C256x256w4m16a = Cfg<256, 256, 64, 2, 2, 2, 1, false, true, true>;
 using C256x128s3w8 = Cfg<256, 128, 64, 4, 2, 3, 2>;
 using C256x128s3w8L = Cfg<256, 128, 64, 4, 2, 3, 2, true>;
 using C128x128w4 = Cfg<128, 128, 64, 2, 2, 2, 2>;
@@ -1024,7 +1067,7 @@ template <class F>
 auto with_cfg(int cfg, F &&f) -> decltype(f(C256x256w8{}, 1)) {
     switch (cfg) {
         case TC_256x256_K64_S2_W8: return f(C256x256w8{}, 1);
-        case TC_256x256_K64_S2_W8_M16: return f(C256x256w8m16{}, 1);
+        case TC_256x256_K64_S2_W4_M16A: return f(C256x256w4m16a{}, 1);
         case TC_256x128_K64_S3_W8: return f(C256x128s3w8{}, 1);
         case TC_256x128_K64_S3_W8_L: return f(C256x128s3w8L{}, 1);
         case TC_128x128_K64_S2_W4: return f(C128x128w4{}, 2);

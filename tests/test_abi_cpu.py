@@ -129,7 +129,9 @@ def test_row_block_stream_plans(ka):
     assert sel(64, 4096, 4096).startswith("tile_")
     assert sel(3, 4096, 4096) == "gemv_valu_w4"
     # wide outputs between 512 and 1024 rows take the big tiles
-    assert sel(1024, 13824, 5120).startswith("tile_256x256_k64_w8")
+    assert sel(1024, 13824, 5120) == "tile_256x256_k64_w4_m16a"       # one partial round of 256x256 tiles
+    assert sel(4096, 5120, 5120) == "tile_256x256_k64_w8_tailsplit"   # whole rounds plus a partial one
+    assert sel(8192, 8192, 8192) == "tile_256x256_k64_w4_m16a"
     assert sel(1024, 8192, 8192) == "tile_256x128_k64s3_w8_lag"
     assert sel(512, 8192, 8192) == "tile_128x128_k64s4_w4_lag"        # the measured table entry
 
@@ -324,6 +326,7 @@ def test_f8_plans(ka):
                            (4096, 14336, 4096, 1), (300, 77, 1024, 1)]:
         p = ka.select_plan_f8(M, N, K, glu)
         assert ka.plan_supports_f8(p, M, N, K, glu) and names[p].startswith("tile"), (M, N, K, glu, names[p])
-    assert not ka.plan_supports_f8(names.index("tile_256x256_k64_w8_m16"), 64, 1024, 1024)  # 16x16 MFMA tile
+    assert not ka.plan_supports_f8(names.index("tile_256x256_k64_w4_m16a"), 64, 1024, 1024)  # 16x16 MFMA tile
+    assert not ka.plan_supports_i8(names.index("tile_256x256_k64_w4_m16a"), 64, 1024, 1024)  # bf16 only
     assert ka.plan_supports_f8(names.index("tile_256x256_k64_w8"), 64, 1024, 1 << 17)      # no int32 limit
     assert ka.select_plan_f8(64, 128, 40) == names.index("generic_64x64_scalar")

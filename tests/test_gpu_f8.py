@@ -142,7 +142,7 @@ def test_f8_rejects(ka):
     qw = torch.zeros(96, 128, dtype=torch.float8_e4m3fn, device="cuda")
     sx = torch.ones(64, dtype=torch.float32, device="cuda")
     sw = torch.ones(96, dtype=torch.float32, device="cuda")
-    for n in ("stream_mfma16_k64_splitk", "gemv_valu_w4", "tile_256x256_k64_w8_m16"):
+    for n in ("stream_mfma16_k64_splitk", "gemv_valu_w4", "tile_256x256_k64_w4_m16a"):
         with pytest.raises(ka.KernelArcError) as e:
             ka.gemm_f8(qx, sx, qw, sw, plan=names.index(n))
         assert e.value.status == ka.ERR_UNSUPPORTED

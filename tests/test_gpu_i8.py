@@ -122,7 +122,7 @@ def _unit_case(M, N, K, seed, swiglu):
 @pytest.mark.parametrize("name", ["tile_256x256_k64_w8", "tile_64x64_k128s3_w4_splitk", "tile_128x128_k64s4_w4_lag",
                                   "tile_64x64_k64s4_w4", "tile_256x128_k64s3_w8_lag_splitk",
                                   "tile_64x128_k64s4_w4_splitk", "generic_64x64_scalar",
-                                  "stream_mfma16_r16_k128s2", "stream_mfma16_r32_k64s4", "tile_256x256_k64_w8_m16"])
+                                  "stream_mfma16_r16_k128s2", "stream_mfma16_r32_k64s4"])
 def test_i8_integer_sums_bit_exact(ka, name):
     """Unit scales and |A| <= 256: the outputs are the exact integer sums."""
     plan = ka.plan_names().index(name)
@@ -176,7 +176,7 @@ def test_i8_rejects(ka):
     qw = torch.zeros(96, 128, dtype=torch.int8, device="cuda")
     sx = torch.ones(64, dtype=torch.float32, device="cuda")
     sw = torch.ones(96, dtype=torch.float32, device="cuda")
-    for n in ("stream_mfma16_k64_splitk", "gemv_valu_w4"):
+    for n in ("stream_mfma16_k64_splitk", "gemv_valu_w4", "tile_256x256_k64_w4_m16a"):
         with pytest.raises(ka.KernelArcError) as e:
             ka.gemm_i8(qx, sx, qw, sw, plan=names.index(n))
         assert e.value.status == ka.ERR_UNSUPPORTED
