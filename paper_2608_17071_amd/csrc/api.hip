@@ -231,18 +231,20 @@ const TableEntry TABLE[] = {
 // 4096; no cross-workgroup split there) and 64-row blocks with split-K
 // beyond; up to 64 rows, the 16-row streaming kernel while N <= 2048 and
 // K <= 4096; up to 1024 rows: the 256x256 tile when its tiles reach 2/3
-// of the CUs, the 256x128 3-stage lagged tile above 512 rows when its tiles
-// fill them, else 64x64 tiles (3 stages of K depth
-// 128, split-K) while they fill at most half the CUs, 64x64 tiles (4 stages
-// of depth 64, two per CU) while they fit one round, else 128x128 tiles
+// of the CUs (the 4-wave form when they fit one round or fill whole ones),
+// the 256x128 3-stage lagged tile above 512 rows when its tiles fill them,
+// else 64x64 tiles (3 stages of K depth 128, split-K) while they fill at
+// most half the CUs, 64x64 tiles (4 stages of depth 64, two per CU) while
+// they fit one round, else 128x128 tiles
 // with 3 stages and split-K when they would keep at most half the CUs busy,
 // 256x128 8-wave tiles (3 stages, lagged refill) with split-K when 128x128
 // tiles would leave some CUs idle, else 128x128 tiles with 4 stages and the
-// lagged refill; above that the 256x256 8-wave tile when it
-// fills the 256 CUs (16x16x32 MFMA when the tiles fill whole rounds; else
-// 32x32 with the tail split: the tiles of a partial last round are split in
-// K), the 256x128 8-wave tile (3 stages, lagged refill) when that fills
-// them, else the 128x128 tile.
+// lagged refill; above that the 256x256 tile when it fills the 256 CUs
+// (4 waves of 128x128 on 16x16x32 MFMAs with AGPR accumulators when the
+// tiles fill whole rounds; else 8 waves on 32x32 MFMAs with the tail split:
+// the tiles of a partial last round are split in K), the 256x128 8-wave
+// tile (3 stages, lagged refill) when that fills them, else the 128x128
+// tile.
 int select(int64_t M, int64_t N, int64_t K, bool residual, const Layout &lay) {
     if (M < 0 || N < 0 || K < 0) return -1;
     for (const TableEntry &e : TABLE) {
