@@ -43,11 +43,13 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef int i32x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) void lds_void;
 
 constexpr int RSRC_WORD3 = 0x00020000;
 constexpr uint32_t OOB_OFFSET = 0x80000000u;
 constexpr int AUX_SC1 = 16;   // device-scope (cross-XCD coherent) access
+constexpr int AUX_NT = 2;     // non-temporal: each weight byte is read once
 constexpr int WAVES = 4;
 constexpr int THREADS = 64 * WAVES;
 
@@ -243,7 +245,7 @@ __global__ __launch_bounds__(THREADS) void stream_kernel(P p, int64_t nblocks, S
         for (int q = 0; q < C::W_LOADS; ++q) {
             const uint32_t off = w_k[q] < rem ? w_off[q] + kb2 : OOB_OFFSET;
             __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_void *)(ring + buf * C::STAGE_BYTES + q * 1024), 16,
-                                                     off, 0, 0, 0);
+                                                     off, 0, 0, AUX_NT);
         }
         if constexpr (C::XL) {
 #pragma unroll
@@ -368,16 +370,35 @@ __global__ __launch_bounds__(THREADS) void stream_kernel(P p, int64_t nblocks, S
         // Publish this slice with device-scope stores; once every wave's
         // stores have completed the arrival is counted, and the last slice
         // to arrive adds all slices (device-scope loads) in slice order.
-        // (With RB < 4 several waves hold the same row block; each stores
-        // and later reads its own copy.)
-        constexpr int BLOCK_FLOATS = WAVES * MB * 64 * 4;
+        // A slice holds one copy of the workgroup's sums: wave w stores and
+        // later reads back only the EPW values of each f32x4 that it writes
+        // to Y (all four with 64-row blocks, one with 16-row blocks).
+        constexpr int EPW = C::EPW, CH = 4 / EPW;
+        constexpr int BLOCK_FLOATS = MB * RB * 64 * 4;
         const float *first = sk.partials + nb * sk.split * BLOCK_FLOATS;
         const __amdgpu_buffer_rsrc_t rp = make_rsrc(first, static_cast<uint32_t>(sk.split) * BLOCK_FLOATS * 4u);
         const uint32_t mine = static_cast<uint32_t>(slice) * BLOCK_FLOATS * 4u;
+        const int c_own = e0 / EPW;
+        auto part_off = [&](int i) {
+            return static_cast<uint32_t>((((i * RB + j_own) * CH + c_own) * 64 + lane) * EPW * 4);
+        };
+        using E = typename std::conditional<I8, int, float>::type;
+        using B64 = decltype(__builtin_amdgcn_raw_buffer_load_b64(rp, 0u, 0, 0));
+        static_assert(sizeof(B64) == 8, "64-bit buffer access");
 #pragma unroll
-        for (int i = 0; i < MB; ++i)
-            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(i32x4, sum[i]), rp,
-                                                   mine + ((wave * MB + i) * 64 + lane) * 16, 0, AUX_SC1);
+        for (int i = 0; i < MB; ++i) {
+            if constexpr (EPW == 4) {
+                __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(i32x4, sum[i]), rp, mine + part_off(i), 0,
+                                                       AUX_SC1);
+            } else if constexpr (EPW == 2) {
+                const i32x2 v = {__builtin_bit_cast(int, static_cast<E>(sum[i][e0])),
+                                 __builtin_bit_cast(int, static_cast<E>(sum[i][e0 + 1]))};
+                __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(B64, v), rp, mine + part_off(i), 0, AUX_SC1);
+            } else {
+                __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, static_cast<E>(sum[i][e0])), rp,
+                                                      mine + part_off(i), 0, AUX_SC1);
+            }
+        }
         __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
         __syncthreads();
         int *flag = reinterpret_cast<int *>(lds);   // every wave has read its sums (barrier above)
@@ -389,28 +410,49 @@ __global__ __launch_bounds__(THREADS) void stream_kernel(P p, int64_t nblocks, S
         __syncthreads();
         const bool last = *flag != 0;
         if (!last) return;
-#pragma unroll
-        for (int i = 0; i < MB; ++i) sum[i] = AccV{0, 0, 0, 0};
         // Eight slices per round trip; a slice past the last reads out of
         // range and is not added, so the sum runs over the slices in order.
+        E tot[MB][EPW];
+#pragma unroll
+        for (int i = 0; i < MB; ++i)
+#pragma unroll
+            for (int k = 0; k < EPW; ++k) tot[i][k] = 0;
         constexpr int D = 8;
         for (int t0 = 0; t0 < sk.split; t0 += D) {
-            AccV v[D][MB];
+            E v[D][MB][EPW];
 #pragma unroll
             for (int d = 0; d < D; ++d)
 #pragma unroll
-                for (int i = 0; i < MB; ++i)
-                    v[d][i] = __builtin_bit_cast(
-                        AccV, __builtin_amdgcn_raw_buffer_load_b128(
-                                   rp, static_cast<uint32_t>(t0 + d) * BLOCK_FLOATS * 4u + ((wave * MB + i) * 64 + lane) * 16,
-                                   0, AUX_SC1));
+                for (int i = 0; i < MB; ++i) {
+                    const uint32_t off = static_cast<uint32_t>(t0 + d) * BLOCK_FLOATS * 4u + part_off(i);
+                    if constexpr (EPW == 4) {
+                        const i32x4 w = __builtin_amdgcn_raw_buffer_load_b128(rp, off, 0, AUX_SC1);
+#pragma unroll
+                        for (int k = 0; k < 4; ++k) v[d][i][k] = __builtin_bit_cast(E, static_cast<int>(w[k]));
+                    } else if constexpr (EPW == 2) {
+                        // Vector elements go through a value (static_cast) before
+                        // __builtin_bit_cast: applied to an element of a vector
+                        // lvalue, it reads the vector's first element instead.
+                        const i32x2 w = __builtin_bit_cast(i32x2, __builtin_amdgcn_raw_buffer_load_b64(rp, off, 0, AUX_SC1));
+                        v[d][i][0] = __builtin_bit_cast(E, static_cast<int>(w[0]));
+                        v[d][i][1] = __builtin_bit_cast(E, static_cast<int>(w[1]));
+                    } else {
+                        v[d][i][0] = __builtin_bit_cast(E, __builtin_amdgcn_raw_buffer_load_b32(rp, off, 0, AUX_SC1));
+                    }
+                }
 #pragma unroll
             for (int d = 0; d < D; ++d) {
                 if (t0 + d >= sk.split) break;
 #pragma unroll
-                for (int i = 0; i < MB; ++i) sum[i] += v[d][i];
+                for (int i = 0; i < MB; ++i)
+#pragma unroll
+                    for (int k = 0; k < EPW; ++k) tot[i][k] += v[d][i][k];
             }
         }
+#pragma unroll
+        for (int i = 0; i < MB; ++i)
+#pragma unroll
+            for (int k = 0; k < EPW; ++k) sum[i][e0 + k] = tot[i][k];
         if (threadIdx.x == 0)
             __hip_atomic_store(sk.counters + nb, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
@@ -487,7 +529,7 @@ int stream_split_for(int64_t M, int64_t N, int64_t K, int bk, int rows) {
 
 int64_t stream_workspace_floats(int64_t M, int64_t N, int split, int rows) {
     const int64_t nblocks = (N + rows - 1) / rows;
-    return nblocks * split * WAVES * ((M + 15) / 16) * 64 * 4;
+    return nblocks * split * (rows / 16) * ((M + 15) / 16) * 64 * 4;
 }
 
 int64_t stream_counter_count(int64_t N, int rows) { return (N + rows - 1) / rows; }
