@@ -11,8 +11,9 @@
 //
 //   * X (M rows of K, each row padded to whole kilobytes in LDS, at most
 //     64 KB) is copied to LDS once per workgroup with LDS-direct loads (1 KB
-//     each, all in flight together); lane l reads the 8 values of X that
-//     face its 16 bytes of W.
+//     each, all in flight together, and in flight together with the first
+//     batch of weight loads); lane l reads the 8 values of X that face its
+//     16 bytes of W.
 //   * a wave owns RPW consecutive rows and walks them k-segment by
 //     k-segment (all rows of a segment share one read of X from LDS), two
 //     batches of BATCH loads in flight;
@@ -33,10 +34,10 @@ typedef __attribute__((address_space(3))) void lds_void;
 constexpr int RSRC_WORD3 = 0x00020000;
 constexpr uint32_t OOB_OFFSET = 0x80000000u;
 constexpr int AUX_NT = 2;
-constexpr int WAITCNT_VM0 = 0x0F70;      // s_waitcnt vmcnt(0); expcnt and lgkmcnt not waited
 constexpr int WAVES = 4;
 constexpr int THREADS = 64 * WAVES;
 constexpr int BATCH = 4;                 // loads per batch (one kilobyte each)
+constexpr int WAITCNT_VM_BATCH = 0x0F70 | BATCH;   // s_waitcnt vmcnt(BATCH)
 constexpr int MAX_ROWS_PER_WAVE = 4;     // a batch must hold whole segments
 constexpr int X_LDS_BYTES = 64 * 1024;   // X lives in LDS: M rows of x_pitch(K) bytes
 
@@ -124,8 +125,7 @@ __global__ __launch_bounds__(THREADS) void gemv_kernel(P p) {
             __builtin_amdgcn_raw_ptr_buffer_load_lds(rxs, (lds_void *)(xs + q * 1024), 16,
                                                      static_cast<uint32_t>(q * 1024 + lane * 16), 0, 0, 0);
     }
-    __builtin_amdgcn_s_waitcnt(WAITCNT_VM0);
-    __syncthreads();
+    __builtin_amdgcn_sched_barrier(0);
 
     const __amdgpu_buffer_rsrc_t rw = make_rsrc(p.W, static_cast<uint32_t>(GEN ? strided_bytes(N, K, ldw) : N * K * 2));
     float acc[RPW][MT];
@@ -148,22 +148,38 @@ __global__ __launch_bounds__(THREADS) void gemv_kernel(P p) {
         }
     };
     auto consume = [&](const i32x4 (&wv)[BATCH], int seg0) {
+        // Exactly one later batch has been issued: wait for this one as a
+        // whole.  The body has no branches (segments past K and tokens past
+        // M read a valid LDS address and multiply zeros), so the compiler's
+        // own waits cannot end up on a path some lanes skip, which made the
+        // loop head wait for every load, the next batch included.
+        __builtin_amdgcn_s_waitcnt(WAITCNT_VM_BATCH);
 #pragma unroll
         for (int sb = 0; sb < SPB; ++sb) {
             const int64_t k = static_cast<int64_t>(seg0 + sb) * 512 + lane * 8;
-            if (k >= K) continue;
+            const bool k_ok = k < K;
 #pragma unroll
             for (int t = 0; t < MT; ++t) {
-                if (t >= p.M) break;
-                const i32x4 xv = *reinterpret_cast<const i32x4 *>(xs + t * xp + k * 2);
+                const bool ok = k_ok && t < p.M;
+                const int tt = t < p.M ? t : 0;
+                const i32x4 xr = *reinterpret_cast<const i32x4 *>(xs + tt * xp + (k_ok ? k : 0) * 2);
+                const i32x4 xv = ok ? xr : i32x4{0, 0, 0, 0};
 #pragma unroll
                 for (int r = 0; r < RPW; ++r) acc[r][t] = dot8(wv[sb * RPW + r], xv, acc[r][t]);
             }
         }
     };
 
+    // The first weight batch goes out before X has landed, so the two
+    // round trips overlap.  Loads complete in issue order: once at most
+    // that batch is outstanding, this wave's X loads (and the residual) are
+    // in LDS; the barrier then covers every wave's.  (__syncthreads() would
+    // wait for the weight batch too.)
     i32x4 wa[BATCH], wb[BATCH];
     issue(wa, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(BATCH) : "memory");
+    __builtin_amdgcn_sched_barrier(0);
     for (int s0 = 0; s0 < segs; s0 += 2 * SPB) {
         issue(wb, s0 + SPB);
         __builtin_amdgcn_sched_barrier(0);
