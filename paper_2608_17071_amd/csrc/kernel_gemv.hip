@@ -149,10 +149,8 @@ __global__ __launch_bounds__(THREADS) void gemv_kernel(P p) {
     };
     auto consume = [&](const i32x4 (&wv)[BATCH], int seg0) {
         // Exactly one later batch has been issued: wait for this one as a
-        // whole.  The body has no branches (segments past K and tokens past
-        // M read a valid LDS address and multiply zeros), so the compiler's
-        // own waits cannot end up on a path some lanes skip, which made the
-        // loop head wait for every load, the next batch included.
+        // whole.  No branches (segments past K and tokens past M read a
+        // valid LDS address and multiply zeros).
         __builtin_amdgcn_s_waitcnt(WAITCNT_VM_BATCH);
 #pragma unroll
         for (int sb = 0; sb < SPB; ++sb) {
@@ -180,6 +178,9 @@ __global__ __launch_bounds__(THREADS) void gemv_kernel(P p) {
     __builtin_amdgcn_sched_barrier(0);
     asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(BATCH) : "memory");
     __builtin_amdgcn_sched_barrier(0);
+    // (With the exit below the compiler waits for every load at the head
+    // of the loop; a loop without it, consuming batches in pairs past K,
+    // keeps two batches in flight but measured slower on M = 1 shapes.)
     for (int s0 = 0; s0 < segs; s0 += 2 * SPB) {
         issue(wb, s0 + SPB);
         __builtin_amdgcn_sched_barrier(0);
