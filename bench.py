@@ -607,7 +607,7 @@ def gpu_clocks() -> dict:
 def oracle_config_seconds():
     """Whole-output oracle seconds for the tiny, decode and prefill configs
     with every host thread, and on one thread for tiny and decode (the CPU
-    baseline plan: the oracle's own speed, not a target)."""
+    baseline: the oracle's own speed, reported, not a target)."""
     import oracle
     from paper_2608_17071_amd import workloads as wl
 
@@ -688,7 +688,7 @@ def write_plan_table(rows, path, command):
     """Markdown summary of compare_plans: per workload the selected plan, the
     fastest plan and every candidate's time."""
     lines = ["# Plan comparison on MI355X (the benchmark's cold-operand protocol, HIP-graph replay)", "",
-             "Command (repository root on the GPU box):", "", "```", command, "```", "",
+             "Command (repository root, on the MI355X):", "", "```", command, "```", "",
              "Per workload: the plan the library selects, the fastest candidate, and the median per-call time of",
              "every plan that can run the shape (generic kernel excluded), in microseconds.", "",
              "| shape | selected | selected us | fastest | fastest us | selected / fastest |",
