@@ -644,6 +644,20 @@ def compare_plans(names, plans, steps, warmup, ka, torch, rotate=True):
             make = lambda p: GluCase(w, ka, torch, rotate=rotate, plan=p)
             selected = ka.plan_name(ka.select_plan_swiglu(w.M, w.N, w.K))
             base = None
+        elif n in wl.GROUPED_BY_NAME:
+            w = wl.GROUPED_BY_NAME[n]
+            base = GroupedCase(w, ka, torch, rotate=rotate)      # the selected plan; gives M_pad
+            mpad = base.Mpad
+            ok = lambda p: ka.plan_supports_grouped(p, w.G, mpad, w.N, w.K, w.swiglu)
+
+            def make(p, base=base):
+                base.forced = p
+                base.plan = p
+                base.plan_name = ka.plan_name(p)
+                base.times = []
+                base.graph = None
+                return base
+            selected = base.plan_name
         elif n in wl.GENERAL_BY_NAME:
             w = wl.GENERAL_BY_NAME[n]
             ok = lambda p: ka.plan_supports(p, w.M, w.N, w.K, w.has_c)
@@ -678,8 +692,8 @@ def compare_plans(names, plans, steps, warmup, ka, torch, rotate=True):
         if base is not None:
             base.free()
         best = min(times, key=times.get) if times else None
-        rows.append({"shape": n, "M": w.M, "N": w.N, "K": w.K, "selected": selected, "fastest": best,
-                     "us": times})
+        rows.append({"shape": n, "M": getattr(w, "M", None) or getattr(w, "G", 0) * (mpad if n in wl.GROUPED_BY_NAME else 1),
+                     "N": w.N, "K": w.K, "selected": selected, "fastest": best, "us": times})
         log(f"  {n}: selected {selected} {times.get(selected)} us, fastest {best} {times.get(best)} us")
     return rows
 
