@@ -346,7 +346,7 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
     constexpr int BNO = GLU ? C::BN / 2 : C::BN, WNO = GLU ? C::WN / 2 : C::WN;
     static_assert(!GLU || (C::TN % 2 == 0 && C::B_LOADS % 2 == 0 && 32 % C::RPI == 0), "gate/up pairing");
     const int64_t ldx = ldx_of(p), ldw = ldw_of(p), ldr = ldr_of(p), ldy = ldy_of(p);
-    __shared__ __attribute__((aligned(1024))) char lds[C::LDS_BYTES];
+    __shared__ __attribute__((aligned(1024))) char lds[C::LDS_BYTES + (C::AACC ? 256 : 0)];   // + prefetch sink
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -441,6 +441,36 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
         b_off[q] = static_cast<uint32_t>(wr * ldw * EB + c * 16);
         b_k[q] = c * CKE;
     }
+
+    // L2 prefetch of A (AGPR tile only).  The tiles of one tile row that run
+    // together on an XCD (consecutive tn within a band) stage the same A
+    // rows, and their loads of a new K step miss the XCD's L2 together.  Tile
+    // tn % 4 owns a quarter of the rows: at the end of each K step its waves
+    // touch the step PF_AHEAD ahead of the K loop in each owned row (16 rows
+    // a wave, one dword per 128-byte line, a second one when a row's slice
+    // straddles two lines), so that the line is in L2 when the staging loads
+    // of all four tiles ask for it.  The dwords land in an LDS sink that
+    // nothing reads; the prefetch is the newest load at every barrier, so
+    // the counted wait leaves it in flight.  A tile with no neighbour for an
+    // owned row (narrow problems, other bands) only fetches that line early.
+    constexpr int PFN = C::AACC ? 1 : 0;             // prefetch loads per wave per step
+    static_assert(!PFN || (C::STAGES == 2 && !C::LAG), "the counted waits place one prefetch per barrier");
+    constexpr int PF_AHEAD = C::STAGES + 1;          // one step past the refill
+    uint32_t pf_off = OOB_OFFSET;
+    if constexpr (C::AACC) {
+        const int64_t r = 64 * (tn & 3) + 16 * wave + (lane & 15);
+        const bool straddles =
+            (reinterpret_cast<uintptr_t>(p.X + (m0 + r) * ldx) & (C::ROW_BYTES - 1)) != 0;
+        if (lane < 16 || (lane < 32 && straddles))
+            pf_off = static_cast<uint32_t>(r * ldx * EB + (lane < 16 ? 0 : C::ROW_BYTES - 4));
+    }
+    auto prefetch_a = [&](int step) {
+        if constexpr (C::AACC) {
+            const bool in_range = static_cast<int64_t>(step) * BKE < kend && pf_off != OOB_OFFSET;
+            const uint32_t off = in_range ? pf_off + static_cast<uint32_t>(step) * C::ROW_BYTES : OOB_OFFSET;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void *)(lds + C::LDS_BYTES), 4, off, 0, 0, 0);
+        }
+    };
 
     // Accumulators: 32x32 blocks (acc), or with M16 16x16 blocks (acc16),
     // where quad q of 32x32 block (i, j) -- its elements 4q .. 4q+3 -- is
@@ -620,7 +650,8 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
     constexpr int MF = FTM * FTN, FR = FTM + FTN, POST = PD * MF, SLOTS = KS * MF;
     // Loads a wave may leave in flight at a step's barrier (step kt+1 must
     // have landed): the steps requested after it, and with the lagged
-    // refill also the loads of this step's refill issued before the barrier.
+    // refill also the loads of this step's refill issued before the barrier,
+    // and with the A prefetch the PFN loads issued at the end of step kt-1.
     constexpr int LPRE = C::LAG ? ((KS - PD) * MF * C::LOADS) / SLOTS : 0;
     constexpr int VM_KEEP = C::LAG ? C::LOADS * (C::STAGES - 3) + LPRE : C::LOADS * (C::STAGES - 2);
     constexpr int VM_KEEP0 = C::LOADS * (C::STAGES - 2);   // prologue: step g0 landed
@@ -656,8 +687,10 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
 
     // Prologue: steps g0 .. g0+STAGES-2 requested, step g0 landed in every
     // wave, the fragments of its first PD sub-steps requested, then step
-    // g0+STAGES-1 into the last buffer.  Past the end of the range the loads
-    // only write zeros into buffers whose contents are never used.
+    // g0+STAGES-1 into the last buffer and the first A prefetch (AGPR tile),
+    // so that a prefetch is the newest load at every barrier.  Past the end
+    // of the range the loads only write zeros into buffers whose contents
+    // are never used.
     // The counted waits assume the steps' loads are issued in step order:
     // scheduling barriers keep the compiler from interleaving them.
 #pragma unroll
@@ -676,6 +709,8 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
         issue_stage<C, GLU, BKE>(glds + (C::STAGES - 1) * C::STAGE_BYTES, ra, rb, rb2, a_off, a_k, b_off, b_k,
                                  wave, g0 + C::STAGES - 1, gend);
     __builtin_amdgcn_sched_barrier(0);
+    prefetch_a(g0 + PF_AHEAD - 1);
+    __builtin_amdgcn_sched_barrier(0);
 
     int cur_stage = 0;
     auto k_step = [&](int it, auto phc) {
@@ -691,7 +726,7 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
         const uint32_t kbytes = static_cast<uint32_t>(refill) * C::ROW_BYTES;
         static_for<0, KS>([&](auto ksc) {
             constexpr int ks = decltype(ksc)::value;
-            if constexpr (ks == KS - PD) stage_barrier<VM_KEEP>();
+            if constexpr (ks == KS - PD) stage_barrier<VM_KEEP + PFN>();
             constexpr int set = (PH * KS + ks) % NSETS;
             constexpr int tgt = ks + PD;              // sub-step whose fragments are read
             constexpr int tset = (PH * KS + tgt) % NSETS;
@@ -734,6 +769,10 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
                     });
                 }
                 __builtin_amdgcn_sched_barrier(0);
+                if constexpr (PFN > 0 && ks == KS - 1 && t == MF - 1) {
+                    prefetch_a(g0 + it + PF_AHEAD);
+                    __builtin_amdgcn_sched_barrier(0);
+                }
             });
         });
         cur_stage = next_stage;
