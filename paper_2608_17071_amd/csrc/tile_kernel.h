@@ -168,13 +168,26 @@ __device__ __forceinline__ int b_block(int wave, int qb) {
 // Enqueue LDS-direct load q (A loads first, then B) of the K step at
 // element kbase (byte kbytes within a row) into one stage buffer.  Chunks
 // at or past K are pointed out of range and arrive as zeros.  rb2 is the
-// up-weight panel of SwiGLU (unused otherwise).
-template <class C, int q, bool GLU>
+// up-weight panel of SwiGLU (unused otherwise).  FULL: the caller knows the
+// whole step lies below K, so the lane's offset stays fixed and the step's
+// byte offset goes in the scalar offset (no per-load vector arithmetic).
+template <class C, int q, bool GLU, bool FULL = false>
 __device__ __forceinline__ void issue_load(char *stage, const __amdgpu_buffer_rsrc_t &ra,
                                            const __amdgpu_buffer_rsrc_t &rb, const __amdgpu_buffer_rsrc_t &rb2,
                                            const uint32_t *a_off, const int *a_k, const uint32_t *b_off,
                                            const int *b_k, int wave, int64_t kbase, uint32_t kbytes, int64_t K) {
-    if constexpr (q < C::A_LOADS) {
+    if constexpr (FULL) {
+        if constexpr (q < C::A_LOADS) {
+            const int blk = wave * C::A_LOADS + q;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void *)(stage + blk * 1024), 16, a_off[q], kbytes, 0, 0);
+        } else {
+            constexpr int qb = q - C::A_LOADS;
+            const int blk = b_block<C, GLU>(wave, qb);
+            const __amdgpu_buffer_rsrc_t &r = (GLU && qb >= C::B_LOADS / 2) ? rb2 : rb;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void *)(stage + C::A_BYTES + blk * 1024), 16, b_off[qb],
+                                                     kbytes, 0, 0);
+        }
+    } else if constexpr (q < C::A_LOADS) {
         const int blk = wave * C::A_LOADS + q;
         const uint32_t off = (kbase + a_k[q] < K) ? a_off[q] + kbytes : OOB_OFFSET;
         __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void *)(stage + blk * 1024), 16, off, 0, 0, 0);
@@ -713,8 +726,9 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
     __builtin_amdgcn_sched_barrier(0);
 
     int cur_stage = 0;
-    auto k_step = [&](int it, auto phc) {
+    auto k_step = [&](int it, auto phc, auto fullc) {
         constexpr int PH = decltype(phc)::value;   // it % UNROLL
+        constexpr bool FULL = decltype(fullc)::value;   // the refill step lies wholly below kend
         const int next_stage = cur_stage + 1 == C::STAGES ? 0 : cur_stage + 1;
         char *const cur = glds + cur_stage * C::STAGE_BYTES;
         const char *const nxt = glds + next_stage * C::STAGE_BYTES;
@@ -758,13 +772,13 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
                 if constexpr (C::LAG) {
                     constexpr int u = ks * MF + t;
                     static_for<u * C::LOADS / SLOTS, (u + 1) * C::LOADS / SLOTS>([&](auto q) {
-                        issue_load<C, decltype(q)::value, GLU>(dst, ra, rb, rb2, a_off, a_k, b_off, b_k, wave,
+                        issue_load<C, decltype(q)::value, GLU, FULL>(dst, ra, rb, rb2, a_off, a_k, b_off, b_k, wave,
                                                                kbase, kbytes, gend);
                     });
                 } else if constexpr (ks >= KS - PD) {
                     constexpr int u = (ks - (KS - PD)) * MF + t;
                     static_for<u * C::LOADS / POST, (u + 1) * C::LOADS / POST>([&](auto q) {
-                        issue_load<C, decltype(q)::value, GLU>(dst, ra, rb, rb2, a_off, a_k, b_off, b_k, wave,
+                        issue_load<C, decltype(q)::value, GLU, FULL>(dst, ra, rb, rb2, a_off, a_k, b_off, b_k, wave,
                                                                kbase, kbytes, gend);
                     });
                 }
@@ -778,8 +792,16 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
         cur_stage = next_stage;
     };
     const int iters_run = (iters + UNROLL - 1) / UNROLL * UNROLL;
-    for (int it = 0; it < iters_run; it += UNROLL)
-        static_for<0, UNROLL>([&](auto ph) { k_step(it + decltype(ph)::value, ph); });
+    int it = 0;
+    if constexpr (UNROLL == 1) {
+        // Iterations whose refill step lies wholly below kend skip the
+        // per-chunk K check: a second copy of the loop body takes the rest
+        // (a partial last step, the steps past the range).
+        const int full_iters = static_cast<int>(kend / BKE) - g0 - (C::LAG ? C::STAGES - 1 : C::STAGES);
+        for (; it < full_iters; ++it) k_step(it, std::integral_constant<int, 0>{}, std::true_type{});
+    }
+    for (; it < iters_run; it += UNROLL)
+        static_for<0, UNROLL>([&](auto ph) { k_step(it + decltype(ph)::value, ph, std::false_type{}); });
     // The compiler does not see the inline-assembly MFMAs, so it cannot
     // space their last AGPR writes from the first reads below: 32 idle
     // cycles cover the longest required gap of a 16x16x32 MFMA.
