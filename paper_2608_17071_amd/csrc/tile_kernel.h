@@ -576,8 +576,13 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
             rv[v] = __builtin_amdgcn_raw_buffer_load_b128(rr, col0 < N ? rbase_of(i, v) : OOB_OFFSET, 0, 0);
     };
     // Two slabs of R in registers: slab i+1 is requested before slab i is
-    // staged and stored, so only slab 0's latency is exposed.
-    i32x4 rv[2][PASSES];
+    // staged and stored, so only slab 0's latency is exposed.  The AGPR tile
+    // (whose fragment registers are free after the K loop) requests every
+    // slab of its block at once, so the whole block waits for one latency.
+    constexpr bool R_ALL = C::AACC;
+    constexpr int RV = R_ALL ? C::TM : 2;
+    i32x4 rv[RV][PASSES];
+    auto rslot = [](int i) { return R_ALL ? i : (i & 1); };
     const bool has_bias = GEN && bias_of(p) != nullptr;
     const float alpha = alpha_of(p), beta = beta_of(p);
     // The value before rounding: the plain operator's acc + r, or the
@@ -767,8 +772,13 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
                                                                                 0, 0, 127, 0, 127);
                 else
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[set][i], fb[set][j], acc[i][j], 0, 0, 0);
-                static_for<t * FR / MF, (t + 1) * FR / MF>(
-                    [&](auto rc) { read_any(rc, src, tcol, tcol2, fa[tset], fb[tset]); });
+                // AGPR tile: the reads before the barrier go in the first
+                // three quarters of the sub-step's slots, so that they have
+                // landed when the barrier waits for them.
+                constexpr int RS = (C::AACC && ks < KS - PD) ? MF * 3 / 4 : MF;
+                if constexpr (t < RS)
+                    static_for<t * FR / RS, (t + 1) * FR / RS>(
+                        [&](auto rc) { read_any(rc, src, tcol, tcol2, fa[tset], fb[tset]); });
                 if constexpr (C::LAG) {
                     constexpr int u = ks * MF + t;
                     static_for<u * C::LOADS / SLOTS, (u + 1) * C::LOADS / SLOTS>([&](auto q) {
@@ -955,8 +965,13 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
         }
         if (threadIdx.x == 0) __hip_atomic_store(arrived, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
-    if constexpr (!EARLY_R)
+    if constexpr (R_ALL) {
+        if (vec && has_r)
+#pragma unroll
+            for (int i = 0; i < C::TM; ++i) load_r(i, rv[i]);
+    } else if constexpr (!EARLY_R) {
         if (vec && has_r) load_r(0, rv[0]);
+    }
     // The bias of the lane's 8 columns (fixed for the whole tile).
     float bv[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     if (has_bias) {
@@ -969,7 +984,7 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
     float *ep = reinterpret_cast<float *>(lds) + wave * C::EPI_WAVE_FLOATS;
 #pragma unroll
     for (int i = 0; i < C::TM; ++i) {
-        if (vec && has_r && i + 1 < C::TM) load_r(i + 1, rv[(i + 1) & 1]);
+        if (!R_ALL && vec && has_r && i + 1 < C::TM) load_r(i + 1, rv[rslot(i + 1)]);
         if constexpr (Q8)
             if (i + 1 < C::TM) load_sx(i + 1);
         {
@@ -1027,7 +1042,7 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
                     if constexpr (GEN) {
 #pragma unroll
                         for (int t = 0; t < 4; ++t) {
-                            const uint32_t w = static_cast<uint32_t>(rv[i & 1][v][t]);
+                            const uint32_t w = static_cast<uint32_t>(rv[rslot(i)][v][t]);
                             y[2 * t] = value(y[2 * t], bf16_to_f32(static_cast<uint16_t>(w & 0xffffu)));
                             y[2 * t + 1] = value(y[2 * t + 1], bf16_to_f32(static_cast<uint16_t>(w >> 16)));
                         }
@@ -1038,7 +1053,7 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
                     } else if (has_r) {
 #pragma unroll
                         for (int t = 0; t < 4; ++t) {
-                            const uint32_t w = static_cast<uint32_t>(rv[i & 1][v][t]);
+                            const uint32_t w = static_cast<uint32_t>(rv[rslot(i)][v][t]);
                             y[2 * t] += bf16_to_f32(static_cast<uint16_t>(w & 0xffffu));
                             y[2 * t + 1] += bf16_to_f32(static_cast<uint16_t>(w >> 16));
                         }
