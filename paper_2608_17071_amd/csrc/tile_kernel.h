@@ -287,6 +287,12 @@ __device__ __forceinline__ void stage_barrier() {
     asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
 }
 
+// Workgroup barrier for LDS only: the wave's LDS accesses are complete
+// before it arrives, its global stores may still be in flight.
+__device__ __forceinline__ void lds_barrier() {
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
 // Adds 16 raw bytes (fp32 or int32 bits) to quad q of a 32x32 block (exact
 // for int32).
 __device__ __forceinline__ void add_quad(f32x16 &a, int q, const f32x4 &v) {
@@ -1024,7 +1030,10 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
                     }
             }
         }
-        __syncthreads();
+        // The slab's staging area is the wave's own, so only LDS order
+        // matters here: the Y stores of the previous slab keep flowing
+        // (a __syncthreads() would wait for them to complete).
+        lds_barrier();
         {
 #pragma unroll
             for (int v = 0; v < PASSES; ++v) {
@@ -1077,7 +1086,7 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
                 }
             }
         }
-        __syncthreads();
+        lds_barrier();   // the staging area is read before the next slab overwrites it
     }
 }
 
