@@ -780,8 +780,11 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[set][i], fb[set][j], acc[i][j], 0, 0, 0);
                 // AGPR tile: the reads before the barrier go in the first
                 // three quarters of the sub-step's slots, so that they have
-                // landed when the barrier waits for them.
-                constexpr int RS = (C::AACC && ks < KS - PD) ? MF * 3 / 4 : MF;
+                // landed when the barrier waits for them; the reads after
+                // it go in the first quarter, one per slot, ahead of most of
+                // the refill loads (a wave's LDS reads complete after its
+                // earlier LDS-direct loads have written their data).
+                constexpr int RS = !C::AACC ? MF : ks < KS - PD ? MF * 3 / 4 : MF / 4;
                 if constexpr (t < RS)
                     static_for<t * FR / RS, (t + 1) * FR / RS>(
                         [&](auto rc) { read_any(rc, src, tcol, tcol2, fa[tset], fb[tset]); });
