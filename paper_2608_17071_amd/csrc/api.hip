@@ -41,7 +41,7 @@ constexpr int64_t WS_COUNTERS = int64_t{1} << 16;
 constexpr int64_t CUS = 256;        // MI355X compute units
 constexpr int MAX_SPLIT = 16;
 
-enum PlanKind { KIND_GENERIC, KIND_GEMV, KIND_TILE, KIND_STREAM };
+enum PlanKind { KIND_GENERIC, KIND_GEMV, KIND_TILE, KIND_STREAM, KIND_BANDS };
 
 struct PlanInfo {
     const char *name;
@@ -76,6 +76,10 @@ const PlanInfo PLANS[] = {
     {"tile_256x256_k64_w8", KIND_TILE, TC_256x256_K64_S2_W8, 1},
     {"tile_256x256_k64_w8_tailsplit", KIND_TILE, TC_256x256_K64_S2_W8, -1},
     {"tile_256x256_k64_w4_m16a", KIND_TILE, TC_256x256_K64_S2_W4_M16A, 1},
+    // Two column bands: the widest one whose 256x256 tiles fill whole rounds
+    // of the CUs on the 4-wave AGPR tile, the other columns on the 128x128
+    // 4-stage lagged tile (two launches on the stream).
+    {"tile_256x256_k64_w4_m16a_bands", KIND_BANDS, -1, 1},
 };
 constexpr int NUM_PLANS = static_cast<int>(sizeof(PLANS) / sizeof(PLANS[0]));
 
@@ -139,6 +143,23 @@ struct Layout {
 };
 Layout dense_layout(int64_t N, int64_t K) { return Layout{K, K, N, N, false}; }
 
+int plan_index(const char *name);
+
+// Column bands of the banded plan: columns [0, N1) on BAND_MAIN, whose
+// 256x256 tiles then fill whole rounds of the CUs (the tile rows times the
+// band's tile columns is a multiple of CUS), the rest on BAND_REST.  N1 is
+// a multiple of 256 (0 or N when no such split exists).
+const char *const BAND_MAIN = "tile_256x256_k64_w4_m16a";
+const char *const BAND_REST = "tile_128x128_k64s4_w4_lag";
+int64_t gcd64(int64_t a, int64_t b) { return b == 0 ? a : gcd64(b, a % b); }
+int64_t band_split(int64_t M, int64_t N) {
+    const int64_t tm = cdiv(M, 256), tn = cdiv(N, 256);
+    if (tm == 0 || tn == 0) return 0;
+    const int64_t q = CUS / gcd64(tm, CUS);        // band tile columns come in multiples of q
+    const int64_t tn1 = (tn / q) * q;
+    return tn1 >= tn ? N : tn1 * 256;
+}
+
 bool supports(int plan, int64_t M, int64_t N, int64_t K, bool residual, const Layout &lay) {
     (void)residual;
     if (M < 0 || N < 0 || K < 0 || M > LIMIT_DIM || N > LIMIT_DIM || K > LIMIT_DIM) return false;
@@ -167,6 +188,12 @@ bool supports(int plan, int64_t M, int64_t N, int64_t K, bool residual, const La
                 return false;
             return true;
         }
+        case KIND_BANDS: {
+            const int64_t N1 = band_split(M, N);
+            const Layout band{lay.ldx, lay.ldw, lay.ldr, lay.ldy, true};
+            return (N1 == 0 || supports(plan_index(BAND_MAIN), M, N1, K, residual, band)) &&
+                   (N1 == N || supports(plan_index(BAND_REST), M, N - N1, K, residual, band));
+        }
         case KIND_TILE: {
             const TileShape ts = tile_shape(pi.tile_cfg);
             if (K % 8 != 0) return false;
@@ -194,6 +221,7 @@ int plan_index(const char *name) {
     return -1;
 }
 
+
 // Exact-shape entries (M, N, K, residual) -> plan name; from measurements on
 // MI355X (the benchmark's cold-cache protocol).  The sentinel has M = -1.
 struct TableEntry {
@@ -218,7 +246,7 @@ const TableEntry TABLE[] = {
     {512, 8192, 8192, 1, "tile_128x128_k64s4_w4_lag"},
     {4096, 2048, 2048, 1, "tile_256x128_k64s3_w8_lag"},
     {4096, 4096, 4096, 1, "tile_256x256_k64_w4_m16a"},
-    {4096, 5120, 5120, 1, "tile_256x256_k64_w8_tailsplit"},
+    {4096, 5120, 5120, 1, "tile_256x256_k64_w4_m16a_bands"},
     {4096, 8192, 8192, 1, "tile_256x256_k64_w4_m16a"},
     // plain BF16 GEMM
     {8192, 8192, 8192, 0, "tile_256x256_k64_w4_m16a"},
@@ -283,8 +311,17 @@ int select(int64_t M, int64_t N, int64_t K, bool residual, const Layout &lay) {
         if (plan < 0) plan = pick("tile_128x128_k64_w4_splitk");
     } else {
         const int64_t t256 = tile_count(tile_shape(TC_256x256_K64_S2_W8), M, N);
-        if (t256 >= CUS)   // whole rounds: 4 waves on AGPRs; a partial last round: 8 waves with the tail split
-            plan = pick(t256 % CUS == 0 ? "tile_256x256_k64_w4_m16a" : "tile_256x256_k64_w8_tailsplit");
+        if (t256 >= CUS && t256 % CUS == 0) {   // whole rounds: 4 waves on AGPRs
+            plan = pick("tile_256x256_k64_w4_m16a");
+        } else if (t256 >= CUS) {
+            // A partial last round: two column bands when the columns past
+            // the widest whole-round band give the 128x128 tile a round of
+            // its own, else 8 waves with the tail split.
+            const int64_t N1 = band_split(M, N);
+            if (N1 > 0 && N1 < N && tile_count(tile_shape(TC_128x128_K64_S4_W4_L), M, N - N1) >= CUS)
+                plan = pick("tile_256x256_k64_w4_m16a_bands");
+            if (plan < 0) plan = pick("tile_256x256_k64_w8_tailsplit");
+        }
         else if (tile_count(tile_shape(TC_256x128_K64_S3_W8_L), M, N) >= CUS) plan = pick("tile_256x128_k64s3_w8_lag");
         if (plan < 0) plan = pick("tile_128x128_k64_w4");
     }
@@ -661,6 +698,29 @@ struct Request {
     int64_t ldy;
 };
 
+// Launch tile plan tp on p: its split-K workspace (the allocated one, or the
+// static scratch), then the kernel; e receives the launch status.
+int run_tile_plan(int tp, const Problem &p, int dev, bool static_scratch, hipStream_t stream, hipError_t &e) {
+    const TileSplit sp = tile_split_plan(tp, p.M, p.N, p.K);
+    Workspace ws{};
+    if (static_scratch && sp.split > 1) {
+        const TileShape ts = tile_shape(PLANS[tp].tile_cfg);
+        const int64_t split_tiles = tile_count(ts, p.M, p.N) - sp.full_tiles;
+        const int64_t need = split_tiles * sp.split * ts.bm * ts.bn;
+        if (need > WS_PARTIAL_FLOATS || split_tiles > WS_COUNTERS)
+            return fail(KERNELARC_ERR_UNSUPPORTED,
+                        "plan %s needs %lld fp32 partials and %lld counters; the static scratch holds %lld "
+                        "and %lld", PLANS[tp].name, (long long)need, (long long)split_tiles,
+                        (long long)WS_PARTIAL_FLOATS, (long long)WS_COUNTERS);
+    }
+    if (sp.split > 1) {
+        const int wst = static_scratch ? scratch_workspace(dev, stream, &ws) : workspace(dev, stream, &ws);
+        if (wst != KERNELARC_OK) return wst;
+    }
+    e = launch_tile(PLANS[tp].tile_cfg, p, sp.split, sp.full_tiles, sp.split > 1 ? &ws : nullptr, stream);
+    return KERNELARC_OK;
+}
+
 // plan < 0: choose; otherwise run exactly that plan.  static_scratch: the
 // split-K partials go to the static scratch instead of the allocated
 // workspace (nothing is allocated).
@@ -729,23 +789,30 @@ int run(int plan, Request q, hipStream_t stream, bool static_scratch = false) {
             e = launch_gemv(p, stream);
             break;
         case KIND_TILE: {
-            const TileSplit sp = tile_split_plan(plan, M, N, K);
-            Workspace ws{};
-            if (static_scratch && sp.split > 1) {
-                const TileShape ts = tile_shape(PLANS[plan].tile_cfg);
-                const int64_t split_tiles = tile_count(ts, M, N) - sp.full_tiles;
-                const int64_t need = split_tiles * sp.split * ts.bm * ts.bn;
-                if (need > WS_PARTIAL_FLOATS || split_tiles > WS_COUNTERS)
-                    return fail(KERNELARC_ERR_UNSUPPORTED,
-                                "plan %s needs %lld fp32 partials and %lld counters; the static scratch holds %lld "
-                                "and %lld", PLANS[plan].name, (long long)need, (long long)split_tiles,
-                                (long long)WS_PARTIAL_FLOATS, (long long)WS_COUNTERS);
+            const int st_tile = run_tile_plan(plan, p, dev, static_scratch, stream, e);
+            if (st_tile != KERNELARC_OK) return st_tile;
+            break;
+        }
+        case KIND_BANDS: {
+            // Two launches on the stream: the columns [0, N1) and [N1, N)
+            // are independent, each element computed by one of them.
+            const int64_t N1 = band_split(M, N);
+            if (N1 > 0) {
+                Problem p1 = p;
+                p1.N = N1;
+                const int st1 = run_tile_plan(plan_index(BAND_MAIN), p1, dev, static_scratch, stream, e);
+                if (st1 != KERNELARC_OK) return st1;
             }
-            if (sp.split > 1) {
-                const int wst = static_scratch ? scratch_workspace(dev, stream, &ws) : workspace(dev, stream, &ws);
-                if (wst != KERNELARC_OK) return wst;
+            if (N1 < N && e == hipSuccess) {
+                Problem p2 = p;
+                p2.N = N - N1;
+                p2.W += N1 * q.ldw;
+                if (p2.R) p2.R += N1;
+                p2.Y += N1;
+                if (p2.bias) p2.bias += N1;
+                const int st2 = run_tile_plan(plan_index(BAND_REST), p2, dev, static_scratch, stream, e);
+                if (st2 != KERNELARC_OK) return st2;
             }
-            e = launch_tile(PLANS[plan].tile_cfg, p, sp.split, sp.full_tiles, sp.split > 1 ? &ws : nullptr, stream);
             break;
         }
         case KIND_STREAM: {
@@ -1255,6 +1322,13 @@ int kernelarc_plan_uses_workspace(int plan, int64_t M, int64_t N, int64_t K) {
     if (!supports(plan, M, N, K, true, dense_layout(N, K))) return 0;
     if (PLANS[plan].kind == KIND_TILE) return tile_split_of(plan, M, N, K) > 1 ? 1 : 0;
     if (PLANS[plan].kind == KIND_STREAM) return stream_split_of(plan, M, N, K) > 1 ? 1 : 0;
+    if (PLANS[plan].kind == KIND_BANDS) {
+        const int64_t N1 = band_split(M, N);
+        return (N1 > 0 && tile_split_of(plan_index(BAND_MAIN), M, N1, K) > 1) ||
+                       (N1 < N && tile_split_of(plan_index(BAND_REST), M, N - N1, K) > 1)
+                   ? 1
+                   : 0;
+    }
     return 0;
 }
 

@@ -141,10 +141,19 @@ def test_row_block_stream_plans(ka):
     assert sel(3, 4096, 4096) == "gemv_valu_w4"
     # wide outputs between 512 and 1024 rows take the big tiles
     assert sel(1024, 13824, 5120) == "tile_256x256_k64_w4_m16a"       # one partial round of 256x256 tiles
-    assert sel(4096, 5120, 5120) == "tile_256x256_k64_w8_tailsplit"   # whole rounds plus a partial one
+    assert sel(2048, 8448, 1024) == "tile_256x256_k64_w8_tailsplit"   # whole rounds plus a partial one
     assert sel(8192, 8192, 8192) == "tile_256x256_k64_w4_m16a"
     assert sel(1024, 8192, 8192) == "tile_256x128_k64s3_w8_lag"
     assert sel(512, 8192, 8192) == "tile_128x128_k64s4_w4_lag"        # the measured table entry
+    # a partial last round of 256x256 tiles: two column bands when the rest
+    # gives the 128x128 tile a round of its own, else the tail split
+    assert sel(4096, 5120, 5120) == "tile_256x256_k64_w4_m16a_bands"  # the measured table entry
+    assert sel(8192, 5120, 5120) == "tile_256x256_k64_w4_m16a_bands"
+    assert sel(4096, 4352, 4096) == "tile_256x256_k64_w8_tailsplit"
+    bands = names.index("tile_256x256_k64_w4_m16a_bands")
+    for (M, N, K) in [(65, 8, 8), (4000, 4360, 200), (4096, 5120, 5120)]:
+        assert ka.plan_supports(bands, M, N, K)
+        assert ka.kernelarc_plan_uses_workspace(bands, M, N, K) == 0
 
 
 def test_validation_before_any_device_work(ka):

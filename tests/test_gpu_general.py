@@ -115,6 +115,14 @@ def test_general_strides(ka, pads):
     _general_case(ka, 24, 200, 1032, 6, 1.5, 0.5, True, True, pads=pads)
 
 
+def test_general_bands(ka):
+    # the banded plan with both column bands (4096 columns of 256x256 tiles,
+    # 264 on the 128x128 tile) in the general form: strides, alpha, beta, bias
+    plan = ka.plan_names().index("tile_256x256_k64_w4_m16a_bands")
+    _general_case(ka, 4000, 4360, 200, 31, 0.75, -1.25, True, True, plan=plan)
+    _general_case(ka, 4096, 4608, 136, 32, 1.0, 0.0, True, False, pads=(0, 8, 0, 16), plan=plan)
+
+
 def test_general_large_k_ne_n(ka):
     # a decoder layer's down projection: K = 3.5 * hidden
     M, N, K = 4096, 4096, 14336

@@ -166,6 +166,34 @@ def test_tail_split_whole_output(ka, case):
     np.testing.assert_array_equal(gu.run_library(t["X"], t["W"], t["R"], plan=p), y1)
 
 
+# Shapes where the banded plan runs both column bands: (M, N, K, N1), N1 the
+# first band's width (whole rounds of 256x256 tiles); ragged M, N and K.
+BAND_CASES = [(4000, 4360, 200, 4096), (4096, 4608, 136, 4096), (2048, 8448, 72, 8192)]
+
+
+@pytest.mark.parametrize("case", BAND_CASES, ids=[f"{c[0]}x{c[1]}x{c[2]}" for c in BAND_CASES])
+def test_bands_whole_output(ka, case):
+    M, N, K, N1 = case
+    p = plan_id(ka, "tile_256x256_k64_w4_m16a_bands")
+    assert ka.plan_supports(p, M, N, K)
+    orc = oracle.default()
+    # every element bitwise, through rank-1 integer inputs, into a NaN-prefilled output
+    X1, W1, R1, a, b, u, v = wl.rank1_integer(M, N, K, seed=8)
+    exact1 = (np.outer(a, b) * int(np.dot(u, v))).astype(np.float64) + 0.0
+    for R, want, form in ((R1, exact1 + bf16_bits_to_f64(wl.bits(R1)) + 0.0, "residual"), (None, exact1, "plain")):
+        gu.note(f"bands rank-1 M={M} N={N} K={K} N1={N1} {form}")
+        out = torch.full((M, N), float("nan"), dtype=torch.bfloat16, device="cuda")
+        y = gu.run_library(X1, W1, R, plan=p, out=out)
+        np.testing.assert_array_equal(_unsigned_zero(y), orc.round_bf16(want), err_msg=f"bands {form}")
+    # random inputs: the whole output against the oracle
+    t = wl.make_inputs(wl.custom(M, N, K, seed=14))
+    for R in (t["R"], None):
+        gu.note(f"bands random M={M} N={N} K={K} residual={R is not None}")
+        out = torch.full((M, N), float("nan"), dtype=torch.bfloat16, device="cuda")
+        y = gu.run_library(t["X"], t["W"], R, plan=p, out=out)
+        gu.check_tolerance(y, gu.oracle_reference(t["X"], t["W"], R), f"bands {M}x{N}x{K}")
+
+
 @pytest.mark.parametrize("plan", sorted(PLAN_SHAPES))
 def test_deterministic_and_row_permutation(ka, plan):
     p = plan_id(ka, plan)
