@@ -408,8 +408,8 @@ bool supports_i8(int plan, int64_t M, int64_t N, int64_t K, bool glu, bool f8 = 
     // (the same bytes per stage as bf16 at K/2).
     if (pi.kind == KIND_STREAM)
         return !glu && !f8 && pi.rows < 64 && K % 16 == 0 && supports(plan, M, N, K / 2, true, dense_layout(N, K / 2));
-    // (16x16 MFMA tiles take bf16 operands only)
-    if (pi.kind != KIND_TILE || K % 16 != 0 || tile_is_m16(pi.tile_cfg) ||
+    // (the 16x16 MFMA tiles take plain int8 operands: not FP8, not SwiGLU)
+    if (pi.kind != KIND_TILE || K % 16 != 0 || ((f8 || glu) && tile_is_m16(pi.tile_cfg)) ||
         (f8 && !tile_f8_ok(pi.tile_cfg)))
         return false;
     return glu ? supports_glu(plan, M, N, K / 2) : supports(plan, M, N, K / 2, true, dense_layout(N, K / 2));
@@ -442,12 +442,20 @@ int select_i8(int64_t M, int64_t N, int64_t K, bool glu, bool f8 = false) {
         if (plan >= 0) return plan;
     }
     plan = glu ? select_glu(M, N, K / 2) : select(M, N, K / 2, true, dense_layout(N, K / 2));
-    // The 256x256 8-wave tile without the tail split (the 4-wave AGPR tile
-    // is bf16 only), and already when its tiles reach 4/5 of the CUs (an
-    // INT8 tile covers its K range in half the steps: at M = 1024,
-    // N = 13824, K = 5120, 90 us against 128 us for 128x128).
-    if (plan == plan_index("tile_256x256_k64_w8_tailsplit") || plan == plan_index("tile_256x256_k64_w4_m16a") ||
-        (!glu && 5 * tile_count(tile_shape(TC_256x256_K64_S2_W8), M, N) >= 4 * CUS))
+    // The 4-wave AGPR tile keeps plain INT8 from K = 8192 up (its 16x16
+    // layout has no FP8 or SwiGLU form), also where the bf16 rule splits it
+    // into column bands: a long K loop pays for its costlier prologue (at
+    // 8192^3 415 us against 457 us for the 8-wave tile; at M = 4096,
+    // N = 14336, K = 4096 it is 2% behind). Otherwise the 256x256 8-wave
+    // tile without the tail split, and already
+    // when its tiles reach 4/5 of the CUs (an INT8 tile covers its K range
+    // in half the steps: at M = 1024, N = 13824, K = 5120, 90 us against
+    // 128 us for 128x128).
+    const int m16a = plan_index("tile_256x256_k64_w4_m16a");
+    if (plan == plan_index("tile_256x256_k64_w4_m16a_bands")) plan = m16a;
+    const bool keep_m16a = plan == m16a && !glu && !f8 && K >= 8192;
+    if (!keep_m16a && (plan == plan_index("tile_256x256_k64_w8_tailsplit") || plan == m16a ||
+                       (!glu && 5 * tile_count(tile_shape(TC_256x256_K64_S2_W8), M, N) >= 4 * CUS)))
         plan = plan_index("tile_256x256_k64_w8");
     if (plan >= 0 && plan != PLAN_GENERIC && supports_i8(plan, M, N, K, glu, f8)) return plan;
     for (const char *name : {"tile_64x64_k128s3_w4_splitk", "tile_64x128_k64s4_w4", "tile_128x128_k64_w4"}) {

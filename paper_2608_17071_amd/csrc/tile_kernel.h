@@ -317,6 +317,11 @@ __device__ __forceinline__ void add_bits(i32x4 &a, const f32x4 &bits) { a += __b
 __device__ __forceinline__ void mfma16_agpr(f32x4 &acc, const bf16x8 &a, const bf16x8 &b) {
     asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
 }
+// The INT8 form: 16 x 64 int8 operands (the same 16 bytes per lane), exact
+// int32 sums.
+__device__ __forceinline__ void mfma16_agpr(i32x4 &acc, const bf16x8 &a, const bf16x8 &b) {
+    asm volatile("v_mfma_i32_16x16x64_i8 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+}
 
 // Split-K bookkeeping of one launch (split == 1: none).
 struct SplitK {
@@ -356,7 +361,7 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
     constexpr bool Q8 = I8 || F8;                  // 1-byte operands with dequantisation scales
     constexpr bool GLU = std::is_same<PB, GluProblem>::value || std::is_same<PB, I8GluProblem>::value ||
                          std::is_same<PB, F8GluProblem>::value;
-    static_assert(!C::M16 || !Q8, "16x16 MFMA tiles take bf16 problems");
+    static_assert(!C::M16 || !F8, "16x16 MFMA tiles take bf16 or int8 problems");
     constexpr int EB = Q8 ? 1 : 2;                 // bytes per operand element
     constexpr int BKE = C::ROW_BYTES / EB;         // K elements per stage
     constexpr int CKE = 16 / EB;                   // K elements per 16-byte chunk
@@ -764,6 +769,10 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
                 {
                     if constexpr (C::AACC)
                         mfma16_agpr(acc16[i][j], fa[set][i], fb[set][j]);
+                    else if constexpr (I8)
+                        acc16[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4, fa[set][i]),
+                                                                            __builtin_bit_cast(i32x4, fb[set][j]),
+                                                                            acc16[i][j], 0, 0, 0);
                     else
                         acc16[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[set][i], fb[set][j], acc16[i][j], 0,
                                                                               0, 0);
@@ -1133,9 +1142,7 @@ hipError_t launch_cfg(const Problem &p, int group_m, int split, int64_t full_til
 template <class C>
 hipError_t launch_cfg_i8(const I8Problem &p, int group_m, int split, int64_t full_tiles, const Workspace *ws,
                          hipStream_t s) {
-    if constexpr (C::M16) {   // 16x16 MFMA tiles: bf16 only
-        return hipErrorInvalidValue;
-    } else {
+    {
         const int64_t tiles_m = (p.M + C::BM - 1) / C::BM;
         const int64_t tiles_n = (p.N + C::BN - 1) / C::BN;
         const int64_t tiles = tiles_m * tiles_n;
@@ -1176,7 +1183,7 @@ hipError_t launch_cfg_glu(const GluProblem &p, int group_m, int split, int64_t f
 template <class C>
 hipError_t launch_cfg_i8_glu(const I8GluProblem &p, int group_m, int split, int64_t full_tiles, const Workspace *ws,
                              hipStream_t s) {
-    if constexpr (!glu_ok<C>() || C::M16) {   // 16x16 MFMA tiles are bf16 only
+    if constexpr (!glu_ok<C>() || C::M16) {   // (the INT8 SwiGLU epilogue reads the 32x32 layout)
         return hipErrorInvalidValue;
     } else {
         const int64_t tiles_m = (p.M + C::BM - 1) / C::BM;

@@ -307,6 +307,14 @@ def test_i8_validation_and_plans(ka):
     for (M, N, K, plan) in [(16, 4096, 4096, "stream_mfma16_r16_k128s2"), (1, 64, 16, "stream_mfma16_r16_k128s2"),
                             (64, 2048, 2048, "stream_mfma16_r16_k128s2"), (16, 8192, 8192, "stream_mfma16_r32_k64s4")]:
         assert names[ka.select_plan_i8(M, N, K, False)] == plan, (M, N, K)
+    # the 4-wave AGPR tile takes plain INT8 with K from 8192 up
+    for (M, N, K, glu, plan) in [(8192, 8192, 8192, 0, "tile_256x256_k64_w4_m16a"),
+                                 (4096, 5120, 10240, 0, "tile_256x256_k64_w4_m16a"),
+                                 (4096, 4096, 4096, 0, "tile_256x256_k64_w8"),
+                                 (4096, 14336, 4096, 0, "tile_256x256_k64_w8"),
+                                 (8192, 8192, 8192, 1, "tile_256x256_k64_w8")]:
+        assert names[ka.select_plan_i8(M, N, K, glu)] == plan, (M, N, K, glu)
+    assert names[ka.select_plan_f8(8192, 8192, 8192, False)] == "tile_256x256_k64_w8"
     for n in ("stream_mfma16_k64_splitk", "gemv_valu_w4"):
         assert not ka.plan_supports_i8(names.index(n), 16, 1024, 1024)
     r16 = names.index("stream_mfma16_r16_k128s2")
@@ -353,6 +361,7 @@ def test_f8_plans(ka):
         p = ka.select_plan_f8(M, N, K, glu)
         assert ka.plan_supports_f8(p, M, N, K, glu) and names[p].startswith("tile"), (M, N, K, glu, names[p])
     assert not ka.plan_supports_f8(names.index("tile_256x256_k64_w4_m16a"), 64, 1024, 1024)  # 16x16 MFMA tile
-    assert not ka.plan_supports_i8(names.index("tile_256x256_k64_w4_m16a"), 64, 1024, 1024)  # bf16 only
+    assert ka.plan_supports_i8(names.index("tile_256x256_k64_w4_m16a"), 64, 1024, 1024)      # plain INT8
+    assert not ka.plan_supports_i8(names.index("tile_256x256_k64_w4_m16a"), 64, 1024, 1024, True)  # no SwiGLU
     assert ka.plan_supports_f8(names.index("tile_256x256_k64_w8"), 64, 1024, 1 << 17)      # no int32 limit
     assert ka.select_plan_f8(64, 128, 40) == names.index("generic_64x64_scalar")

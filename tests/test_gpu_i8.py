@@ -176,10 +176,13 @@ def test_i8_rejects(ka):
     qw = torch.zeros(96, 128, dtype=torch.int8, device="cuda")
     sx = torch.ones(64, dtype=torch.float32, device="cuda")
     sw = torch.ones(96, dtype=torch.float32, device="cuda")
-    for n in ("stream_mfma16_k64_splitk", "gemv_valu_w4", "tile_256x256_k64_w4_m16a"):
+    for n in ("stream_mfma16_k64_splitk", "gemv_valu_w4"):
         with pytest.raises(ka.KernelArcError) as e:
             ka.gemm_i8(qx, sx, qw, sw, plan=names.index(n))
         assert e.value.status == ka.ERR_UNSUPPORTED
+    with pytest.raises(ka.KernelArcError) as e:          # the 16x16 AGPR tile: plain INT8 only
+        ka.swiglu_i8(qx, sx, qw, sw, qw, sw, plan=names.index("tile_256x256_k64_w4_m16a"))
+    assert e.value.status == ka.ERR_UNSUPPORTED
     with pytest.raises(ka.KernelArcError) as e:          # 64x64 waves cannot pair gate/up blocks
         ka.swiglu_i8(qx, sx, qw, sw, qw, sw, plan=names.index("tile_64x64_k64s4_w4"))
     assert e.value.status == ka.ERR_UNSUPPORTED
