@@ -314,12 +314,21 @@ int select(int64_t M, int64_t N, int64_t K, bool residual, const Layout &lay) {
         if (t256 >= CUS && t256 % CUS == 0) {   // whole rounds: 4 waves on AGPRs
             plan = pick("tile_256x256_k64_w4_m16a");
         } else if (t256 >= CUS) {
-            // A partial last round: two column bands when the columns past
-            // the widest whole-round band give the 128x128 tile a round of
-            // its own, else 8 waves with the tail split.
+            // A partial last round, which takes most of a full round's time
+            // whatever its fill: two column bands when the columns past the
+            // widest whole-round band fit one round of 128x128 tiles (at
+            // most 0.4 of a 256x256 round); else the 4-wave tile over every
+            // tile, or the 8-wave tail split after a single full round when
+            // the last one holds at most a quarter of the CUs (with more full
+            // rounds the 8-wave tile's slower rounds cost more than the
+            // split saves).
             const int64_t N1 = band_split(M, N);
-            if (N1 > 0 && N1 < N && tile_count(tile_shape(TC_128x128_K64_S4_W4_L), M, N - N1) >= CUS)
+            if (N1 > 0 && N1 < N && tile_count(tile_shape(TC_128x128_K64_S4_W4_L), M, N - N1) <= CUS)
                 plan = pick("tile_256x256_k64_w4_m16a_bands");
+            else if (t256 < 2 * CUS && 4 * (t256 % CUS) <= CUS)
+                plan = pick("tile_256x256_k64_w8_tailsplit");
+            else
+                plan = pick("tile_256x256_k64_w4_m16a");
             if (plan < 0) plan = pick("tile_256x256_k64_w8_tailsplit");
         }
         else if (tile_count(tile_shape(TC_256x128_K64_S3_W8_L), M, N) >= CUS) plan = pick("tile_256x128_k64s3_w8_lag");

@@ -141,15 +141,20 @@ def test_row_block_stream_plans(ka):
     assert sel(3, 4096, 4096) == "gemv_valu_w4"
     # wide outputs between 512 and 1024 rows take the big tiles
     assert sel(1024, 13824, 5120) == "tile_256x256_k64_w4_m16a"       # one partial round of 256x256 tiles
-    assert sel(2048, 8448, 1024) == "tile_256x256_k64_w8_tailsplit"   # whole rounds plus a partial one
+    assert sel(2048, 8448, 1024) == "tile_256x256_k64_w4_m16a_bands"  # whole rounds plus a partial one
     assert sel(8192, 8192, 8192) == "tile_256x256_k64_w4_m16a"
     assert sel(1024, 8192, 8192) == "tile_256x128_k64s3_w8_lag"
     assert sel(512, 8192, 8192) == "tile_128x128_k64s4_w4_lag"        # the measured table entry
     # a partial last round of 256x256 tiles: two column bands when the rest
-    # gives the 128x128 tile a round of its own, else the tail split
+    # fits one round of 128x128 tiles, else the 4-wave tile over every tile,
+    # or the tail split after one full round when the last holds at most a
+    # quarter of the CUs
     assert sel(4096, 5120, 5120) == "tile_256x256_k64_w4_m16a_bands"  # the measured table entry
-    assert sel(8192, 5120, 5120) == "tile_256x256_k64_w4_m16a_bands"
-    assert sel(4096, 4352, 4096) == "tile_256x256_k64_w8_tailsplit"
+    assert sel(4096, 4352, 4096) == "tile_256x256_k64_w4_m16a_bands"
+    for (M, N, K) in [(8192, 5120, 5120), (4096, 14336, 4096), (2048, 14336, 4096), (4096, 11008, 4096)]:
+        assert sel(M, N, K) == "tile_256x256_k64_w4_m16a", (M, N, K)
+    assert sel(6144, 6144, 6144) == "tile_256x256_k64_w4_m16a"         # two full rounds and a quarter
+    assert sel(6144, 2816, 4096) == "tile_256x256_k64_w8_tailsplit"    # one full round and 8 tiles, no bands
     bands = names.index("tile_256x256_k64_w4_m16a_bands")
     for (M, N, K) in [(65, 8, 8), (4000, 4360, 200), (4096, 5120, 5120)]:
         assert ka.plan_supports(bands, M, N, K)
