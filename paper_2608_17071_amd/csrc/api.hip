@@ -253,6 +253,26 @@ const TableEntry TABLE[] = {
     {-1, 0, 0, 0, ""},   // sentinel
 };
 
+// The 256x256 plan for t256 tiles.  Whole rounds, or fewer tiles than CUs:
+// the 4-wave AGPR tile.  A partial last round takes most of a full round's
+// time whatever its fill (each tile still runs its whole K loop), while one
+// round of 128x128 tiles takes about 0.4 of it: two column bands when the
+// columns past the widest whole-round band fit one round of 128x128 tiles
+// (bands_ok: plain and general forms); else the 8-wave tail split after a
+// single full round when the last one holds at most a quarter of the CUs
+// (with more full rounds the 8-wave tile's slower rounds cost more than the
+// split saves); else the 4-wave tile over every tile.
+const char *wide_tile_plan(int64_t M, int64_t N, int64_t t256, bool bands_ok) {
+    if (t256 % CUS == 0 || t256 < CUS) return "tile_256x256_k64_w4_m16a";
+    if (bands_ok) {
+        const int64_t N1 = band_split(M, N);
+        if (N1 > 0 && N1 < N && tile_count(tile_shape(TC_128x128_K64_S4_W4_L), M, N - N1) <= CUS)
+            return "tile_256x256_k64_w4_m16a_bands";
+    }
+    if (t256 < 2 * CUS && 4 * (t256 % CUS) <= CUS) return "tile_256x256_k64_w8_tailsplit";
+    return "tile_256x256_k64_w4_m16a";
+}
+
 // Rule-based choice when no table entry matches (from the same
 // measurements): the VALU GEMV up to 4 rows; the streaming kernel up to 32
 // rows, with 16-row blocks of W when they fit one round on the CUs (N up to
@@ -299,9 +319,10 @@ int select(int64_t M, int64_t N, int64_t K, bool residual, const Layout &lay) {
         const int64_t tiles128 = tile_count(tile_shape(TC_128x128_K64_S4_W4_L), M, N);
         const int64_t t256 = tile_count(tile_shape(TC_256x256_K64_S2_W8), M, N);
         const int64_t t256x128 = tile_count(tile_shape(TC_256x128_K64_S3_W8_L), M, N);
-        if (3 * t256 >= 2 * CUS)   // wide outputs: the 256x256 tiles reach 2/3 of the CUs
-            plan = pick(t256 % CUS == 0 || t256 < CUS ? "tile_256x256_k64_w4_m16a" : "tile_256x256_k64_w8_tailsplit");
-        else if (t256x128 >= CUS && M > 512)
+        if (3 * t256 >= 2 * CUS) {   // wide outputs: the 256x256 tiles reach 2/3 of the CUs
+            plan = pick(wide_tile_plan(M, N, t256, true));
+            if (plan < 0) plan = pick("tile_256x256_k64_w8_tailsplit");
+        } else if (t256x128 >= CUS && M > 512)
             plan = pick("tile_256x128_k64s3_w8_lag");
         else if (2 * tiles64 <= CUS) plan = pick("tile_64x64_k128s3_w4_splitk");
         else if (tiles64 <= 2 * CUS) plan = pick("tile_64x64_k64s4_w4");
@@ -311,24 +332,8 @@ int select(int64_t M, int64_t N, int64_t K, bool residual, const Layout &lay) {
         if (plan < 0) plan = pick("tile_128x128_k64_w4_splitk");
     } else {
         const int64_t t256 = tile_count(tile_shape(TC_256x256_K64_S2_W8), M, N);
-        if (t256 >= CUS && t256 % CUS == 0) {   // whole rounds: 4 waves on AGPRs
-            plan = pick("tile_256x256_k64_w4_m16a");
-        } else if (t256 >= CUS) {
-            // A partial last round, which takes most of a full round's time
-            // whatever its fill: two column bands when the columns past the
-            // widest whole-round band fit one round of 128x128 tiles (at
-            // most 0.4 of a 256x256 round); else the 4-wave tile over every
-            // tile, or the 8-wave tail split after a single full round when
-            // the last one holds at most a quarter of the CUs (with more full
-            // rounds the 8-wave tile's slower rounds cost more than the
-            // split saves).
-            const int64_t N1 = band_split(M, N);
-            if (N1 > 0 && N1 < N && tile_count(tile_shape(TC_128x128_K64_S4_W4_L), M, N - N1) <= CUS)
-                plan = pick("tile_256x256_k64_w4_m16a_bands");
-            else if (t256 < 2 * CUS && 4 * (t256 % CUS) <= CUS)
-                plan = pick("tile_256x256_k64_w8_tailsplit");
-            else
-                plan = pick("tile_256x256_k64_w4_m16a");
+        if (t256 >= CUS) {
+            plan = pick(wide_tile_plan(M, N, t256, true));
             if (plan < 0) plan = pick("tile_256x256_k64_w8_tailsplit");
         }
         else if (tile_count(tile_shape(TC_256x128_K64_S3_W8_L), M, N) >= CUS) plan = pick("tile_256x128_k64s3_w8_lag");
@@ -387,8 +392,8 @@ int select_glu(int64_t M, int64_t N, int64_t K) {
     } else if (M <= 128 || 2 * t256x128 < CUS) {
         plan = 2 * t128 <= CUS ? pick("tile_128x128_k64s3_w4_splitk") : pick("tile_128x128_k64s4_w4_lag");
     } else if (5 * t256 >= 4 * CUS) {
-        // whole rounds or one partial round: 4 waves on AGPRs; else 8 waves with the tail split
-        plan = pick(t256 % CUS == 0 || t256 < CUS ? "tile_256x256_k64_w4_m16a" : "tile_256x256_k64_w8_tailsplit");
+        plan = pick(wide_tile_plan(M, N2, t256, false));
+        if (plan < 0) plan = pick("tile_256x256_k64_w8_tailsplit");
     } else {
         plan = pick("tile_256x128_k64s3_w8_lag");
     }

@@ -141,6 +141,9 @@ def test_row_block_stream_plans(ka):
     assert sel(3, 4096, 4096) == "gemv_valu_w4"
     # wide outputs between 512 and 1024 rows take the big tiles
     assert sel(1024, 13824, 5120) == "tile_256x256_k64_w4_m16a"       # one partial round of 256x256 tiles
+    assert sel(1024, 20480, 4096) == "tile_256x256_k64_w4_m16a_bands"  # the rest fits one 128x128 round
+    assert sel(1024, 28672, 4096) == "tile_256x256_k64_w4_m16a"
+    assert sel(768, 24576, 4096) == "tile_256x256_k64_w8_tailsplit"    # one round and an eighth, no bands
     assert sel(2048, 8448, 1024) == "tile_256x256_k64_w4_m16a_bands"  # whole rounds plus a partial one
     assert sel(8192, 8192, 8192) == "tile_256x256_k64_w4_m16a"
     assert sel(1024, 8192, 8192) == "tile_256x128_k64s3_w8_lag"
@@ -272,6 +275,9 @@ def test_swiglu_plans(ka):
         p = ka.select_plan_swiglu(M, N, K)
         assert ka.plan_supports_swiglu(p, M, N, K), (M, N, K, names[p])
         assert names[p].startswith("tile") or p == gen
+    # partial last rounds of 256x256 gate/up tiles run on the 4-wave AGPR tile
+    for (M, N, K) in [(2048, 14336, 4096), (1024, 14336, 4096), (4096, 11008, 4096)]:
+        assert names[ka.select_plan_swiglu(M, N, K)] == "tile_256x256_k64_w4_m16a", (M, N, K)
     # plans whose waves cannot hold gate/up block pairs, or that are not tiles
     for n in ("tile_64x64_k64s4_w4", "tile_64x64_k128s3_w4_splitk", "stream_mfma16_k64_splitk", "gemv_valu_w4",
               "stream_mfma16_r16_k128s2"):
