@@ -53,8 +53,11 @@ constexpr int RSRC_WORD3 = 0x00020000;
 // A byte offset that is out of range for every panel (panels are < 2^31 B).
 constexpr uint32_t OOB_OFFSET = 0x80000000u;
 constexpr int XCDS = 8;
-// Cache policy of buffer accesses: sc1 = device scope (coherent across XCDs).
+// Cache policy of buffer accesses: sc1 = device scope (coherent across XCDs);
+// nt = non-temporal, for the residual and the output, which a launch reads
+// or writes once (1-2.6 % faster on the MFMA-sized shapes).
 constexpr int AUX_SC1 = 16;
+constexpr int AUX_NT = 2;
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, uint32_t bytes) {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), static_cast<short>(0),
@@ -584,7 +587,7 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
     auto load_r = [&](int i, i32x4 (&rv)[PASSES]) {
 #pragma unroll
         for (int v = 0; v < PASSES; ++v)
-            rv[v] = __builtin_amdgcn_raw_buffer_load_b128(rr, col0 < N ? rbase_of(i, v) : OOB_OFFSET, 0, 0);
+            rv[v] = __builtin_amdgcn_raw_buffer_load_b128(rr, col0 < N ? rbase_of(i, v) : OOB_OFFSET, 0, AUX_NT);
     };
     // Two slabs of R in registers: slab i+1 is requested before slab i is
     // staged and stored, so only slab 0's latency is exposed.  The AGPR tile
@@ -1082,7 +1085,7 @@ void tile_kernel(P p, int64_t tiles_m, int64_t tiles_n, int group_m, SplitK sk) 
                     i32x4 out;
 #pragma unroll
                     for (int t = 0; t < 4; ++t) out[t] = static_cast<int>(f32x2_to_bf16x2_rne(y[2 * t], y[2 * t + 1]));
-                    __builtin_amdgcn_raw_buffer_store_b128(out, ry, col0 < N ? base : OOB_OFFSET, 0, 0);
+                    __builtin_amdgcn_raw_buffer_store_b128(out, ry, col0 < N ? base : OOB_OFFSET, 0, AUX_NT);
                 } else {
                     uint16_t rs[8];
                     const int cols = static_cast<int>(N - col0);   // columns of this lane's 8 that exist
