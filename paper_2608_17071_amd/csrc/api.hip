@@ -243,7 +243,7 @@ const TableEntry TABLE[] = {
     {512, 2048, 2048, 1, "tile_64x64_k64s4_w4"},
     {512, 4096, 4096, 1, "tile_128x128_k64s3_w4_splitk"},
     {512, 5120, 5120, 1, "tile_256x128_k64s3_w8_lag_splitk"},
-    {512, 8192, 8192, 1, "tile_128x128_k64s4_w4_lag"},
+    {512, 8192, 8192, 1, "tile_256x128_k64s3_w8_lag_splitk"},
     {4096, 2048, 2048, 1, "tile_256x128_k64s3_w8_lag"},
     {4096, 4096, 4096, 1, "tile_256x256_k64_w4_m16a"},
     {4096, 5120, 5120, 1, "tile_256x256_k64_w4_m16a_bands"},

@@ -147,7 +147,7 @@ def test_row_block_stream_plans(ka):
     assert sel(2048, 8448, 1024) == "tile_256x256_k64_w4_m16a_bands"  # whole rounds plus a partial one
     assert sel(8192, 8192, 8192) == "tile_256x256_k64_w4_m16a"
     assert sel(1024, 8192, 8192) == "tile_256x128_k64s3_w8_lag"
-    assert sel(512, 8192, 8192) == "tile_128x128_k64s4_w4_lag"        # the measured table entry
+    assert sel(512, 8192, 8192) == "tile_256x128_k64s3_w8_lag_splitk"  # the measured table entry
     # a partial last round of 256x256 tiles: two column bands when the rest
     # fits one round of 128x128 tiles, else the 4-wave tile over every tile,
     # or the tail split after one full round when the last holds at most a
